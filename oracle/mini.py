@@ -1,0 +1,116 @@
+"""Second oracle, pure Python, for tiny inputs.  TEST INFRASTRUCTURE ONLY.
+
+Same definitions as the C oracle, written independently: Python integers
+for the modular sums, exact rationals (``fractions.Fraction``) for rounding,
+byte strings for arenas.  Used to cross-check the C oracle by brute force
+on many random tiny tables.
+"""
+from __future__ import annotations
+
+from fractions import Fraction
+
+M64 = (1 << 64) - 1
+
+
+def frsum(b: bytes):
+    """(sum, wsum) of little-endian 32-bit words, zero-filled tail."""
+    s = ws = 0
+    for i in range(0, len(b), 4):
+        w = int.from_bytes(b[i:i + 4].ljust(4, b"\0"), "little")
+        s += w
+        ws += (i // 4 + 1) * w
+    return s & M64, ws & M64
+
+
+def _f32_value(u: int) -> Fraction:
+    """Exact value of a finite fp32 bit pattern's magnitude."""
+    e = (u >> 23) & 0xFF
+    m = u & 0x7FFFFF
+    if e == 0:
+        return Fraction(m, 1 << 149)
+    return Fraction((1 << 23) | m, 1 << 23) * (Fraction(2) ** (e - 127))
+
+
+def _bf16_value(h: int) -> Fraction:
+    h &= 0x7FFF
+    if h == 0x7F80:
+        return Fraction(2) ** 128  # one step past the largest finite value
+    return _f32_value(h << 16)
+
+
+def rne_bf16(u: int) -> int:
+    u &= 0xFFFFFFFF
+    mag, sign = u & 0x7FFFFFFF, (u >> 16) & 0x8000
+    if mag > 0x7F800000:
+        return (u >> 16) | 0x0040
+    if mag == 0x7F800000:
+        return sign | 0x7F80
+    x = _f32_value(mag)
+    cands = [mag >> 16, (mag >> 16) + 1]
+    best = min(cands, key=lambda h: (abs(_bf16_value(h) - x), h & 1))
+    return sign | best
+
+
+def _esize(dt):
+    return 4 if dt == 1 else 2
+
+
+def plan(table, C):
+    nch, base, pay = [], [0], []
+    p = 0
+    for e in table:
+        nb = int(e["numel"]) * _esize(int(e["dtype"]))
+        nch.append(-(-nb // C))
+        base.append(base[-1] + nch[-1])
+        if int(e["derive_from"]) >= 0:
+            pay.append(None)
+        else:
+            pay.append(p)
+            p += -(-nb // 16) * 16
+    return nch, base, pay, p
+
+
+def _chunks(table, C, arena: bytes, key):
+    """Yield (global id, bytes) of every chunk, reading entries at ``key``."""
+    c = 0
+    for e in table:
+        nb = int(e["numel"]) * _esize(int(e["dtype"]))
+        o = int(e[key])
+        for j in range(0, nb, C):
+            yield c, arena[o + j:o + min(j + C, nb)]
+            c += 1
+
+
+def pack(table, C, src: bytes):
+    _, base, pay, pb = plan(table, C)
+    payload = bytearray(pb)
+    for k, e in enumerate(table):
+        if pay[k] is not None:
+            nb = int(e["numel"]) * _esize(int(e["dtype"]))
+            o = int(e["src_offset"])
+            payload[pay[k]:pay[k] + nb] = src[o:o + nb]
+    sums = [frsum(b) for _, b in _chunks(table, C, src, "src_offset")]
+    return bytes(payload), sums
+
+
+def unpack(table, C, payload: bytes, sums, dst: bytearray):
+    _, base, pay, _ = plan(table, C)
+    for k, e in enumerate(table):
+        nb = int(e["numel"]) * _esize(int(e["dtype"]))
+        o = int(e["dst_offset"])
+        s = int(e["derive_from"])
+        if s < 0:
+            dst[o:o + nb] = payload[pay[k]:pay[k] + nb]
+        else:
+            for i in range(int(e["numel"])):
+                u = int.from_bytes(payload[pay[s] + 4 * i:pay[s] + 4 * i + 4], "little")
+                dst[o + 2 * i:o + 2 * i + 2] = rne_bf16(u).to_bytes(2, "little")
+    got = [frsum(b) for _, b in _chunks(table, C, bytes(dst), "dst_offset")]
+    bad = {c for c, (g, w) in enumerate(zip(got, sums)) if tuple(g) != tuple(w)}
+    return bad
+
+
+def verify(table, C, a: bytes, b: bytes):
+    ca = dict(_chunks(table, C, a, "src_offset"))
+    cb = dict(_chunks(table, C, b, "src_offset"))
+    return {c for c in ca if ca[c] != cb[c]}
