@@ -1,0 +1,213 @@
+/*
+ * flashrestore: data-parallel replica state restore on MI355X (gfx950).
+ *
+ * The checkpoint-free recovery of FlashRecovery (arXiv 2509.03047) rebuilds a
+ * recreated process's model state -- parameters, optimizer state and other
+ * training state -- from a healthy replica in its data-parallel group rather
+ * than from a checkpoint, by collective communication (Section III-B item 3;
+ * Section III-E, "Model states Restoration").  Data parallelism is what makes
+ * the replicas exist and keeps them identical (Section III-A).  This library
+ * is the per-GPU data path of that restore:
+ *
+ *   fr_pack_state      donor side: gather every tensor of the state into one
+ *                      contiguous transfer buffer and checksum every chunk;
+ *   fr_unpack_state    receiver side: scatter the buffer into the receiver's
+ *                      tensor layout, re-derive bf16 parameters from their
+ *                      fp32 master copies, and check every chunk;
+ *   fr_verify_replicas compare two replicas chunk by chunk;
+ *   fr_checksum_state  chunk checksums of one state.
+ *
+ * The transfer itself (the collective) is not part of this library: between
+ * pack and unpack the caller moves `payload` and `sums` by any means.  The
+ * paper fixes no buffer format, checksum or dtype handling; the definitions
+ * below are this library's and are stated in full so that any other
+ * implementation can reproduce every output byte.
+ *
+ * Definitions
+ *   Tensor table.  An array of fr_tensor_desc.  Entry k has
+ *     nbytes_k = numel_k * esize (4 for FR_F32, 2 for FR_BF16).
+ *   Chunks.  Entry k is cut into ceil(nbytes_k / C) chunks of C = chunk_bytes
+ *     bytes (only the last may be shorter).  Chunk j of entry k has global id
+ *     chunk_base_k + j, where chunk_base is the exclusive prefix sum of the
+ *     per-entry chunk counts in table order.  Derived entries are chunked the
+ *     same way.
+ *   FRSUM-128.  A chunk's bytes read as little-endian 32-bit words w_0, w_1,
+ *     ... (a short last word is zero-filled): sum = sum_i w_i mod 2^64 and
+ *     wsum = sum_i (i+1) w_i mod 2^64.  Any single-bit change alters sum; any
+ *     two-bit change within a chunk of < 2^32 words alters (sum, wsum).
+ *   Derived entries.  A FR_BF16 entry with derive_from = s >= 0 holds
+ *     RNE(master_s): it is not sent; its chunk sums are.  The receiver
+ *     recomputes it from the received master, so the check proves it equal to
+ *     the donor's bytes.
+ *   RNE.  fp32 bit pattern u -> bf16: if (u & 0x7FFFFFFF) > 0x7F800000 (NaN)
+ *     the result is (u >> 16) | 0x0040, otherwise the nearer bf16 neighbour
+ *     with ties to an even last bit, overflow to infinity, denormals rounded
+ *     exactly (no flush to zero).
+ *   Payload.  The bytes of every non-derived entry in table order; segment k
+ *     starts at the 16-byte-aligned end of the previous one (0 for the
+ *     first); every byte between segments and after the last is 0;
+ *     payload_bytes = the 16-aligned end of the last segment.
+ *   Bitmaps.  Bit c of a result set lives in 32-bit word c / 32 at bit c % 32.
+ *
+ * Conventions
+ *   All sizes and offsets are in bytes.  All device pointers are plain
+ *   addresses of device memory on the plan's device; the caller owns every
+ *   buffer.  The four operations validate synchronously, then enqueue on
+ *   `stream` (a hipStream_t; NULL is the null stream) and return without
+ *   waiting; their outputs are valid once the stream reaches that point.
+ *   On any error nothing is enqueued and no output is touched.  A checksum or
+ *   compare mismatch is data (a set bit and a count), not an error.  Calls on
+ *   one plan from several host threads at once are not supported.
+ */
+#ifndef FLASHRESTORE_H
+#define FLASHRESTORE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FR_ABI_VERSION 1
+
+enum fr_dtype { FR_F32 = 1, FR_BF16 = 2 };
+
+enum fr_status {
+  FR_OK = 0,
+  FR_E_INVAL = -1,           /* null required pointer, bad dtype, bad derive_from,
+                                bad chunk_bytes, bad argument value */
+  FR_E_ALIGN = -2,           /* an offset or a pointer not suitably aligned */
+  FR_E_RANGE = -3,           /* an entry past its arena, a buffer too small or
+                                past its allocation, too many chunks */
+  FR_E_OVERLAP = -4,         /* overlapping receiver ranges or buffers */
+  FR_E_NOMEM = -5,           /* host or device allocation failed */
+  FR_E_DEVICE = -6,          /* a HIP call failed (see fr_last_hip_error) */
+  FR_E_DEVICE_MISMATCH = -7  /* current device, stream or pointer not on the
+                                plan's device */
+};
+
+/* One tensor of the state.  32 bytes, no padding. */
+typedef struct fr_tensor_desc {
+  uint64_t src_offset; /* from the sender / replica arena base; multiple of 16 */
+  uint64_t dst_offset; /* from the receiver arena base; multiple of 16 */
+  uint64_t numel;      /* elements; 0 allowed (no chunks, no payload) */
+  uint32_t dtype;      /* FR_F32 or FR_BF16 */
+  int32_t derive_from; /* -1, or the index of a non-derived FR_F32 entry with
+                          the same numel; this entry must then be FR_BF16.  At
+                          most one entry may derive from a given master. */
+} fr_tensor_desc;
+
+/* FRSUM-128 of one chunk.  16 bytes. */
+typedef struct fr_chunk_sum {
+  uint64_t sum;
+  uint64_t wsum;
+} fr_chunk_sum;
+
+typedef struct fr_plan fr_plan; /* opaque, owned by the library */
+
+typedef struct fr_plan_info {
+  uint64_t n_entries;
+  uint64_t chunk_bytes;
+  uint64_t n_chunks;        /* total chunks; ids are < 2^32 */
+  uint64_t payload_bytes;
+  uint64_t bitmap_words;    /* ceil(n_chunks / 32) */
+  uint64_t src_arena_bytes;
+  uint64_t dst_arena_bytes;
+  uint64_t state_bytes;     /* sum of nbytes over all entries */
+  int64_t device;           /* HIP device the plan is bound to; -1 for a layout query */
+} fr_plan_info;
+
+/* ---------------------------------------------------------------- plans */
+
+/* Validate a tensor table and build a plan on the current HIP device.
+ *   table            n_entries descriptors (host memory; copied)
+ *   chunk_bytes      C: a power of two in [16, 2^30]
+ *   src_arena_bytes  size of every sender / replica arena the plan will see
+ *   dst_arena_bytes  size of every receiver arena
+ *   out              receives the plan (unchanged on error)
+ * Entries must lie inside their arenas (FR_E_RANGE), offsets must be
+ * multiples of 16 (FR_E_ALIGN), receiver ranges must not overlap
+ * (FR_E_OVERLAP; sender ranges may), the chunk count must be < 2^32
+ * (FR_E_RANGE).  Synchronous: the plan's device tables are uploaded before
+ * return.  The plan is immutable and bound to the device current at
+ * creation. */
+int fr_plan_create(const fr_tensor_desc* table, uint32_t n_entries, uint64_t chunk_bytes,
+                   uint64_t src_arena_bytes, uint64_t dst_arena_bytes, fr_plan** out);
+
+/* Sizes of a plan.  Host only. */
+int fr_plan_get_info(const fr_plan* plan, fr_plan_info* out);
+
+/* Global id of the chunk holding byte `byte_in_entry` of entry `entry`.
+ * FR_E_RANGE if the entry or byte does not exist.  Host only. */
+int fr_plan_chunk_of(const fr_plan* plan, uint32_t entry, uint64_t byte_in_entry, uint64_t* chunk);
+
+/* Payload offset of entry `entry` (UINT64_MAX for derived entries) and its
+ * first chunk id.  Host only. */
+int fr_plan_entry_layout(const fr_plan* plan, uint32_t entry, uint64_t* payload_offset,
+                         uint64_t* first_chunk, uint64_t* n_chunks);
+
+/* Free a plan and its device tables.  NULL is a no-op.  The caller must not
+ * destroy a plan while work that uses it is still pending on a stream. */
+int fr_plan_destroy(fr_plan* plan);
+
+/* The same validation and layout as fr_plan_create, on the host only, with no
+ * device and no plan: fills `info` (device = -1) and, when non-NULL,
+ * payload_offset[n_entries] (UINT64_MAX for derived entries) and
+ * chunk_base[n_entries + 1]. */
+int fr_layout_query(const fr_tensor_desc* table, uint32_t n_entries, uint64_t chunk_bytes,
+                    uint64_t src_arena_bytes, uint64_t dst_arena_bytes, fr_plan_info* info,
+                    uint64_t* payload_offset, uint64_t* chunk_base);
+
+/* ----------------------------------------------------------- operations */
+
+/* Donor side of a restore (Section III-E): payload <- the non-derived entries
+ * of the arena at src_base, laid out as defined above with zero padding;
+ * sums[c] <- FRSUM-128 of chunk c read from src_base, for every chunk,
+ * derived entries included.
+ *   src_base     device, 16-byte aligned, src_arena_bytes long
+ *   payload      device, 16-byte aligned, payload_cap >= payload_bytes
+ *   sums         device, 16-byte aligned, n_chunks entries
+ * src, payload and sums must not overlap (FR_E_OVERLAP). */
+int fr_pack_state(const fr_plan* plan, const void* src_base, void* payload, uint64_t payload_cap,
+                  fr_chunk_sum* sums, void* stream);
+
+/* Receiver side of a restore (Section III-E): for each non-derived entry copy
+ * its payload segment to dst_base + dst_offset; for each derived entry write
+ * RNE of the received master; then recompute FRSUM-128 of every chunk from
+ * the bytes written and set bit c of bad_bitmap iff it differs from sums[c];
+ * *n_bad = number of set bits.  Data is written even for bad chunks.  Bytes
+ * of the receiver arena outside the entries are never written.
+ *   payload      device, 16-byte aligned, payload_bytes long
+ *   sums         device, 16-byte aligned, n_chunks entries (as sent)
+ *   dst_base     device, 16-byte aligned, dst_arena_bytes long
+ *   bad_bitmap   device, 4-byte aligned, bitmap_words words (may be NULL
+ *                when n_chunks == 0); zeroed by the call
+ *   n_bad        device, 8-byte aligned, one uint64; zeroed by the call
+ * The receiver arena must not overlap any other argument. */
+int fr_unpack_state(const fr_plan* plan, const void* payload, const fr_chunk_sum* sums,
+                    void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad, void* stream);
+
+/* Replica-consistency compare (Section III-A: data-parallel replicas must
+ * hold the same state): bit c of diff_bitmap is set iff the bytes of chunk c
+ * differ between the arenas at base_a and base_b (exact comparison, both
+ * read at src offsets); *n_diff = number of set bits.  When sums_a / sums_b
+ * are non-NULL they receive the chunk sums of each arena.  base_a == base_b
+ * is allowed (empty result).  Outputs must not overlap inputs or each other. */
+int fr_verify_replicas(const fr_plan* plan, const void* base_a, const void* base_b,
+                       uint32_t* diff_bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
+                       fr_chunk_sum* sums_b, void* stream);
+
+/* sums[c] <- FRSUM-128 of chunk c of the arena at base (src offsets); equal
+ * to the sums fr_pack_state produces for the same bytes. */
+int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums, void* stream);
+
+/* ---------------------------------------------------------------- misc */
+
+const char* fr_strerror(int status);
+int fr_last_hip_error(void); /* HIP error code behind the last FR_E_DEVICE on this thread */
+int fr_abi_version(void);    /* FR_ABI_VERSION */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FLASHRESTORE_H */

@@ -1,0 +1,192 @@
+// C-ABI entry points of the four operations: synchronous argument checks,
+// then stream-ordered kernel launches.  Nothing is enqueued and no output is
+// touched unless every check passes.
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+
+#include "fr_internal.h"
+
+namespace fr {
+extern thread_local int g_last_hip_error;
+}
+
+using namespace fr;
+
+namespace {
+
+struct Region {
+  const void* p;
+  uint64_t bytes;
+};
+
+int device_error(hipError_t e) {
+  g_last_hip_error = int(e);
+  return FR_E_DEVICE;
+}
+
+int check_device_and_stream(const fr_plan* plan, void* stream) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return device_error(e);
+  if (dev != plan->device) return FR_E_DEVICE_MISMATCH;
+  if (stream) {
+    hipDevice_t sd = -1;
+    e = hipStreamGetDevice(hipStream_t(stream), &sd);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return FR_E_INVAL;
+    }
+    if (int(sd) != plan->device) return FR_E_DEVICE_MISMATCH;
+  }
+  return FR_OK;
+}
+
+// A buffer the kernels will touch: it must be device memory of the plan's
+// device, aligned, and lie inside one allocation.  An empty buffer is never
+// touched, so any pointer (NULL included) is accepted for it.
+int check_buffer(const fr_plan* plan, const void* p, uint64_t bytes, uint64_t align) {
+  if (bytes == 0) return FR_OK;
+  if (p == nullptr) return FR_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(p) % align) return FR_E_ALIGN;
+  hipPointerAttribute_t attr{};
+  hipError_t e = hipPointerGetAttributes(&attr, p);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return FR_E_INVAL;  // not memory HIP knows about
+  }
+  if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged) return FR_E_INVAL;
+  if (attr.device != plan->device) return FR_E_DEVICE_MISMATCH;
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  e = hipMemGetAddressRange(&base, &size, hipDeviceptr_t(const_cast<void*>(p)));
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return FR_E_INVAL;
+  }
+  const uintptr_t b = reinterpret_cast<uintptr_t>(base), q = reinterpret_cast<uintptr_t>(p);
+  if (q < b || bytes > size || q - b > size - bytes) return FR_E_RANGE;
+  return FR_OK;
+}
+
+bool overlap(const Region& x, const Region& y) {
+  if (!x.p || !y.p || x.bytes == 0 || y.bytes == 0) return false;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(x.p), b = reinterpret_cast<uintptr_t>(y.p);
+  return a < b + y.bytes && b < a + x.bytes;
+}
+
+// Outputs must not overlap each other or any input.
+int check_disjoint(const Region* outs, int n_out, const Region* ins, int n_in) {
+  for (int i = 0; i < n_out; i++) {
+    for (int j = i + 1; j < n_out; j++)
+      if (overlap(outs[i], outs[j])) return FR_E_OVERLAP;
+    for (int j = 0; j < n_in; j++)
+      if (overlap(outs[i], ins[j])) return FR_E_OVERLAP;
+  }
+  return FR_OK;
+}
+
+int launch_result(int hip_rc) {
+  if (hip_rc == 0) return FR_OK;
+  return device_error(hipError_t(hip_rc));
+}
+
+#define FR_TRY(expr)            \
+  do {                          \
+    const int rc_ = (expr);     \
+    if (rc_ != FR_OK) return rc_; \
+  } while (0)
+
+}  // namespace
+
+extern "C" int fr_pack_state(const fr_plan* plan, const void* src_base, void* payload,
+                             uint64_t payload_cap, fr_chunk_sum* sums, void* stream) {
+  if (!plan) return FR_E_INVAL;
+  const Layout& L = plan->layout;
+  if (payload_cap < L.payload_bytes) return FR_E_RANGE;
+  FR_TRY(check_device_and_stream(plan, stream));
+  FR_TRY(check_buffer(plan, src_base, plan->src_arena_bytes, 16));
+  FR_TRY(check_buffer(plan, payload, L.payload_bytes, 16));
+  FR_TRY(check_buffer(plan, sums, L.n_chunks * sizeof(fr_chunk_sum), 16));
+  const Region outs[] = {{payload, L.payload_bytes}, {sums, L.n_chunks * sizeof(fr_chunk_sum)}};
+  const Region ins[] = {{src_base, plan->src_arena_bytes}};
+  FR_TRY(check_disjoint(outs, 2, ins, 1));
+  return launch_result(launch_pack(plan->d_chunks, uint32_t(L.n_chunks), src_base, payload, sums,
+                                   plan->cfg, stream));
+}
+
+extern "C" int fr_unpack_state(const fr_plan* plan, const void* payload, const fr_chunk_sum* sums,
+                               void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad,
+                               void* stream) {
+  if (!plan || !n_bad) return FR_E_INVAL;
+  const Layout& L = plan->layout;
+  const uint64_t words = (L.n_chunks + 31) / 32;
+  FR_TRY(check_device_and_stream(plan, stream));
+  FR_TRY(check_buffer(plan, payload, L.payload_bytes, 16));
+  FR_TRY(check_buffer(plan, sums, L.n_chunks * sizeof(fr_chunk_sum), 16));
+  FR_TRY(check_buffer(plan, dst_base, plan->dst_arena_bytes, 16));
+  FR_TRY(check_buffer(plan, bad_bitmap, words * 4, 4));
+  FR_TRY(check_buffer(plan, n_bad, 8, 8));
+  const Region outs[] = {{dst_base, plan->dst_arena_bytes}, {bad_bitmap, words * 4}, {n_bad, 8}};
+  const Region ins[] = {{payload, L.payload_bytes}, {sums, L.n_chunks * sizeof(fr_chunk_sum)}};
+  FR_TRY(check_disjoint(outs, 3, ins, 2));
+  return launch_result(launch_unpack(plan->d_chunks, plan->d_units, plan->n_units, L.C, words,
+                                     payload, sums, dst_base, bad_bitmap, n_bad, plan->cfg,
+                                     stream));
+}
+
+extern "C" int fr_verify_replicas(const fr_plan* plan, const void* base_a, const void* base_b,
+                                  uint32_t* diff_bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
+                                  fr_chunk_sum* sums_b, void* stream) {
+  if (!plan || !n_diff) return FR_E_INVAL;
+  if ((sums_a == nullptr) != (sums_b == nullptr)) return FR_E_INVAL;
+  const Layout& L = plan->layout;
+  const uint64_t words = (L.n_chunks + 31) / 32;
+  const uint64_t sb = sums_a ? L.n_chunks * sizeof(fr_chunk_sum) : 0;
+  FR_TRY(check_device_and_stream(plan, stream));
+  FR_TRY(check_buffer(plan, base_a, plan->src_arena_bytes, 16));
+  FR_TRY(check_buffer(plan, base_b, plan->src_arena_bytes, 16));
+  FR_TRY(check_buffer(plan, diff_bitmap, words * 4, 4));
+  FR_TRY(check_buffer(plan, n_diff, 8, 8));
+  if (sums_a) {
+    FR_TRY(check_buffer(plan, sums_a, sb, 16));
+    FR_TRY(check_buffer(plan, sums_b, sb, 16));
+  }
+  const Region outs[] = {{diff_bitmap, words * 4}, {n_diff, 8}, {sums_a, sb}, {sums_b, sb}};
+  const Region ins[] = {{base_a, plan->src_arena_bytes}, {base_b, plan->src_arena_bytes}};
+  FR_TRY(check_disjoint(outs, 4, ins, 2));
+  return launch_result(launch_verify(plan->d_chunks, uint32_t(L.n_chunks), words, base_a, base_b,
+                                     diff_bitmap, n_diff, sums_a, sums_b, plan->cfg, stream));
+}
+
+extern "C" int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums,
+                                 void* stream) {
+  if (!plan) return FR_E_INVAL;
+  const Layout& L = plan->layout;
+  FR_TRY(check_device_and_stream(plan, stream));
+  FR_TRY(check_buffer(plan, base, plan->src_arena_bytes, 16));
+  FR_TRY(check_buffer(plan, sums, L.n_chunks * sizeof(fr_chunk_sum), 16));
+  const Region outs[] = {{sums, L.n_chunks * sizeof(fr_chunk_sum)}};
+  const Region ins[] = {{base, plan->src_arena_bytes}};
+  FR_TRY(check_disjoint(outs, 1, ins, 1));
+  return launch_result(
+      launch_checksum(plan->d_chunks, uint32_t(L.n_chunks), base, sums, plan->cfg, stream));
+}
+
+extern "C" const char* fr_strerror(int status) {
+  switch (status) {
+    case FR_OK: return "ok";
+    case FR_E_INVAL: return "invalid argument";
+    case FR_E_ALIGN: return "misaligned offset or pointer";
+    case FR_E_RANGE: return "out of range";
+    case FR_E_OVERLAP: return "overlapping ranges or buffers";
+    case FR_E_NOMEM: return "out of memory";
+    case FR_E_DEVICE: return "HIP error";
+    case FR_E_DEVICE_MISMATCH: return "device mismatch";
+    default: return "unknown status";
+  }
+}
+
+extern "C" int fr_last_hip_error(void) { return g_last_hip_error; }
+
+extern "C" int fr_abi_version(void) { return FR_ABI_VERSION; }

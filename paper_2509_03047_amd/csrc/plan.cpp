@@ -1,0 +1,265 @@
+// Plan: validation of a tensor table, the chunk / payload layout, and the
+// device tables the kernels walk (one ChunkRec per chunk, plus the unpack
+// work list).
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "fr_internal.h"
+
+namespace fr {
+
+thread_local int g_last_hip_error = 0;
+
+static uint64_t esize(uint32_t dtype) { return dtype == FR_F32 ? 4 : 2; }
+static uint64_t align16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
+
+int validate_and_layout(const fr_tensor_desc* t, uint32_t n, uint64_t C, uint64_t src_bytes,
+                        uint64_t dst_bytes, Layout* L) {
+  if (n > 0 && t == nullptr) return FR_E_INVAL;
+  if (n > 0x7FFFFFFFu) return FR_E_INVAL;
+  if (C < 16 || C > (uint64_t(1) << 30) || (C & (C - 1)) != 0) return FR_E_INVAL;
+  // Field checks, in an order that makes the reported error deterministic:
+  // dtype and derive_from first (INVAL), then alignment, then ranges.
+  std::vector<uint8_t> used_as_master(n, 0);
+  for (uint32_t k = 0; k < n; k++) {
+    const fr_tensor_desc& e = t[k];
+    if (e.dtype != FR_F32 && e.dtype != FR_BF16) return FR_E_INVAL;
+    if (e.numel > (uint64_t(1) << 61)) return FR_E_RANGE;
+    if (e.derive_from != -1) {
+      if (e.derive_from < 0 || uint32_t(e.derive_from) >= n || uint32_t(e.derive_from) == k)
+        return FR_E_INVAL;
+      const fr_tensor_desc& m = t[e.derive_from];
+      if (e.dtype != FR_BF16 || m.dtype != FR_F32 || m.derive_from != -1 || m.numel != e.numel)
+        return FR_E_INVAL;
+      if (used_as_master[e.derive_from]) return FR_E_INVAL;
+      used_as_master[e.derive_from] = 1;
+    }
+  }
+  for (uint32_t k = 0; k < n; k++)
+    if ((t[k].src_offset | t[k].dst_offset) & 15) return FR_E_ALIGN;
+  uint64_t state = 0;
+  for (uint32_t k = 0; k < n; k++) {
+    uint64_t nb = t[k].numel * esize(t[k].dtype);
+    if (t[k].src_offset > src_bytes || nb > src_bytes - t[k].src_offset) return FR_E_RANGE;
+    if (t[k].dst_offset > dst_bytes || nb > dst_bytes - t[k].dst_offset) return FR_E_RANGE;
+    state += nb;
+  }
+  // Receiver ranges must be disjoint: unpack writes every one of them.
+  std::vector<std::pair<uint64_t, uint64_t>> ranges;
+  ranges.reserve(n);
+  for (uint32_t k = 0; k < n; k++) {
+    uint64_t nb = t[k].numel * esize(t[k].dtype);
+    if (nb) ranges.emplace_back(t[k].dst_offset, t[k].dst_offset + nb);
+  }
+  std::sort(ranges.begin(), ranges.end());
+  for (size_t i = 1; i < ranges.size(); i++)
+    if (ranges[i].first < ranges[i - 1].second) return FR_E_OVERLAP;
+
+  L->C = C;
+  L->pay_off.assign(n, 0);
+  L->chunk_base.assign(size_t(n) + 1, 0);
+  uint64_t base = 0, pay = 0;
+  for (uint32_t k = 0; k < n; k++) {
+    uint64_t nb = t[k].numel * esize(t[k].dtype);
+    L->chunk_base[k] = base;
+    base += (nb + C - 1) / C;
+    if (t[k].derive_from >= 0) {
+      L->pay_off[k] = kNoPayload;
+    } else {
+      L->pay_off[k] = pay;
+      pay = align16(pay + nb);
+    }
+  }
+  L->chunk_base[n] = base;
+  if (base > 0xFFFFFFFFull) return FR_E_RANGE;  // chunk ids are 32-bit
+  L->n_chunks = base;
+  L->payload_bytes = pay;
+  L->state_bytes = state;
+  return FR_OK;
+}
+
+static void fill_info(const Layout& L, uint32_t n, uint64_t src, uint64_t dst, int64_t dev,
+                      fr_plan_info* info) {
+  info->n_entries = n;
+  info->chunk_bytes = L.C;
+  info->n_chunks = L.n_chunks;
+  info->payload_bytes = L.payload_bytes;
+  info->bitmap_words = (L.n_chunks + 31) / 32;
+  info->src_arena_bytes = src;
+  info->dst_arena_bytes = dst;
+  info->state_bytes = L.state_bytes;
+  info->device = dev;
+}
+
+static uint32_t env_u32(const char* name, uint32_t dflt) {
+  const char* v = std::getenv(name);
+  if (!v || !*v) return dflt;
+  char* end = nullptr;
+  unsigned long x = std::strtoul(v, &end, 10);
+  return (end && *end == 0) ? uint32_t(x) : dflt;
+}
+
+}  // namespace fr
+
+using namespace fr;
+
+extern "C" int fr_layout_query(const fr_tensor_desc* table, uint32_t n, uint64_t C,
+                               uint64_t src_bytes, uint64_t dst_bytes, fr_plan_info* info,
+                               uint64_t* payload_offset, uint64_t* chunk_base) {
+  if (!info) return FR_E_INVAL;
+  Layout L;
+  int rc;
+  try {
+    rc = validate_and_layout(table, n, C, src_bytes, dst_bytes, &L);
+  } catch (const std::bad_alloc&) {
+    return FR_E_NOMEM;
+  }
+  if (rc != FR_OK) return rc;
+  fill_info(L, n, src_bytes, dst_bytes, -1, info);
+  if (payload_offset) std::memcpy(payload_offset, L.pay_off.data(), sizeof(uint64_t) * n);
+  if (chunk_base) std::memcpy(chunk_base, L.chunk_base.data(), sizeof(uint64_t) * (size_t(n) + 1));
+  return FR_OK;
+}
+
+static int hip_fail(hipError_t e) {
+  g_last_hip_error = int(e);
+  return FR_E_DEVICE;
+}
+
+extern "C" int fr_plan_destroy(fr_plan* p) {
+  if (!p) return FR_OK;
+  int prev = -1;
+  bool switched = false;
+  if (p->device >= 0 && hipGetDevice(&prev) == hipSuccess && prev != p->device) {
+    switched = hipSetDevice(p->device) == hipSuccess;
+  }
+  if (p->d_chunks) (void)hipFree(p->d_chunks);
+  if (p->d_units) (void)hipFree(p->d_units);
+  if (switched) (void)hipSetDevice(prev);
+  delete p;
+  return FR_OK;
+}
+
+extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t C,
+                              uint64_t src_bytes, uint64_t dst_bytes, fr_plan** out) {
+  if (!out) return FR_E_INVAL;
+  fr_plan* p = nullptr;
+  try {
+    p = new fr_plan();
+    int rc = validate_and_layout(table, n, C, src_bytes, dst_bytes, &p->layout);
+    if (rc != FR_OK) {
+      delete p;
+      return rc;
+    }
+    p->table.assign(table, table + n);
+    p->src_arena_bytes = src_bytes;
+    p->dst_arena_bytes = dst_bytes;
+
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+      delete p;
+      return hip_fail(e);
+    }
+    p->device = dev;
+    // 0 = one workgroup per unit (capped by the hardware grid limit).
+    uint32_t mg = env_u32("FLASHRESTORE_MAX_GRID", 0);
+    p->cfg.max_grid = mg ? mg : (1u << 22);
+
+    const Layout& L = p->layout;
+    std::vector<ChunkRec> recs(L.n_chunks);
+    std::vector<uint32_t> units_derived, units_plain;
+    std::vector<uint8_t> is_master(n, 0);
+    for (uint32_t k = 0; k < n; k++)
+      if (table[k].derive_from >= 0) is_master[table[k].derive_from] = 1;
+    for (uint32_t k = 0; k < n; k++) {
+      const fr_tensor_desc& d = table[k];
+      uint64_t nb = d.numel * (d.dtype == FR_F32 ? 4 : 2);
+      uint64_t nc = L.chunk_base[k + 1] - L.chunk_base[k];
+      for (uint64_t j = 0; j < nc; j++) {
+        uint64_t c = L.chunk_base[k] + j;
+        ChunkRec& r = recs[c];
+        r.src_off = d.src_offset + j * C;
+        r.dst_off = d.dst_offset + j * C;
+        r.pay_off = L.pay_off[k] == kNoPayload ? kNoPayload : L.pay_off[k] + j * C;
+        r.len = uint32_t(std::min<uint64_t>(C, nb - j * C));
+        r.master = kNoMaster;
+        if (d.derive_from >= 0) {
+          // param chunk j covers master chunks 2j and 2j + 1
+          r.master = uint32_t(L.chunk_base[d.derive_from] + 2 * j);
+          units_derived.push_back(uint32_t(c));
+        } else if (!is_master[k]) {
+          units_plain.push_back(uint32_t(c));
+        }
+      }
+    }
+    // Unpack work list: the heavier derived groups first, then plain chunks.
+    std::vector<uint32_t> units;
+    units.reserve(units_derived.size() + units_plain.size());
+    units.insert(units.end(), units_derived.begin(), units_derived.end());
+    units.insert(units.end(), units_plain.begin(), units_plain.end());
+    p->n_units = uint32_t(units.size());
+
+    if (!recs.empty()) {
+      e = hipMalloc(&p->d_chunks, recs.size() * sizeof(ChunkRec));
+      if (e != hipSuccess) {
+        fr_plan_destroy(p);
+        return e == hipErrorOutOfMemory ? FR_E_NOMEM : hip_fail(e);
+      }
+      e = hipMemcpy(p->d_chunks, recs.data(), recs.size() * sizeof(ChunkRec), hipMemcpyHostToDevice);
+      if (e != hipSuccess) {
+        fr_plan_destroy(p);
+        return hip_fail(e);
+      }
+    }
+    if (!units.empty()) {
+      e = hipMalloc(&p->d_units, units.size() * sizeof(uint32_t));
+      if (e != hipSuccess) {
+        fr_plan_destroy(p);
+        return e == hipErrorOutOfMemory ? FR_E_NOMEM : hip_fail(e);
+      }
+      e = hipMemcpy(p->d_units, units.data(), units.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
+      if (e != hipSuccess) {
+        fr_plan_destroy(p);
+        return hip_fail(e);
+      }
+    }
+  } catch (const std::bad_alloc&) {
+    if (p) fr_plan_destroy(p);
+    return FR_E_NOMEM;
+  }
+  *out = p;
+  return FR_OK;
+}
+
+extern "C" int fr_plan_get_info(const fr_plan* p, fr_plan_info* info) {
+  if (!p || !info) return FR_E_INVAL;
+  fill_info(p->layout, uint32_t(p->table.size()), p->src_arena_bytes, p->dst_arena_bytes,
+            p->device, info);
+  return FR_OK;
+}
+
+extern "C" int fr_plan_chunk_of(const fr_plan* p, uint32_t entry, uint64_t byte, uint64_t* chunk) {
+  if (!p || !chunk) return FR_E_INVAL;
+  if (entry >= p->table.size()) return FR_E_RANGE;
+  const fr_tensor_desc& d = p->table[entry];
+  uint64_t nb = d.numel * (d.dtype == FR_F32 ? 4 : 2);
+  if (byte >= nb) return FR_E_RANGE;
+  *chunk = p->layout.chunk_base[entry] + byte / p->layout.C;
+  return FR_OK;
+}
+
+extern "C" int fr_plan_entry_layout(const fr_plan* p, uint32_t entry, uint64_t* payload_offset,
+                                    uint64_t* first_chunk, uint64_t* n_chunks) {
+  if (!p) return FR_E_INVAL;
+  if (entry >= p->table.size()) return FR_E_RANGE;
+  if (payload_offset) *payload_offset = p->layout.pay_off[entry];
+  if (first_chunk) *first_chunk = p->layout.chunk_base[entry];
+  if (n_chunks) *n_chunks = p->layout.chunk_base[entry + 1] - p->layout.chunk_base[entry];
+  return FR_OK;
+}

@@ -1,0 +1,302 @@
+"""Python binding of libflashrestore (ctypes; argument marshalling only).
+
+Every function here has the name of the C entry point it calls and does no
+computation of its own: all work happens in the gfx950 kernels behind the
+C ABI.  PyTorch is used only for device memory (``torch.empty(...,
+device="cuda")``) and for the current stream.  There is no fallback: if the
+shared library is missing or fails to load, importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libflashrestore.so")
+
+FR_F32 = 1
+FR_BF16 = 2
+FR_OK = 0
+STATUS = {
+    0: "FR_OK",
+    -1: "FR_E_INVAL",
+    -2: "FR_E_ALIGN",
+    -3: "FR_E_RANGE",
+    -4: "FR_E_OVERLAP",
+    -5: "FR_E_NOMEM",
+    -6: "FR_E_DEVICE",
+    -7: "FR_E_DEVICE_MISMATCH",
+}
+NO_PAYLOAD = (1 << 64) - 1
+
+# fr_tensor_desc: 32 bytes.
+DESC_DTYPE = np.dtype(
+    [("src_offset", "<u8"), ("dst_offset", "<u8"), ("numel", "<u8"), ("dtype", "<u4"), ("derive_from", "<i4")]
+)
+SUM_BYTES = 16  # fr_chunk_sum
+
+
+class fr_plan_info(C.Structure):
+    _fields_ = [
+        ("n_entries", C.c_uint64),
+        ("chunk_bytes", C.c_uint64),
+        ("n_chunks", C.c_uint64),
+        ("payload_bytes", C.c_uint64),
+        ("bitmap_words", C.c_uint64),
+        ("src_arena_bytes", C.c_uint64),
+        ("dst_arena_bytes", C.c_uint64),
+        ("state_bytes", C.c_uint64),
+        ("device", C.c_int64),
+    ]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+class FlashRestoreError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        name = STATUS.get(status, str(status))
+        msg = _lib.fr_strerror(status).decode()
+        if status == -6:
+            msg += f" (hipError {_lib.fr_last_hip_error()})"
+        super().__init__(f"{where}: {name}: {msg}")
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run `python -m paper_2509_03047_amd.build` "
+            "(or __graft_entry__.build()) first"
+        )
+    lib = C.CDLL(LIB_PATH)
+    P, u32, u64, i32 = C.c_void_p, C.c_uint32, C.c_uint64, C.c_int
+    sig = {
+        "fr_plan_create": [P, u32, u64, u64, u64, C.POINTER(P)],
+        "fr_plan_get_info": [P, C.POINTER(fr_plan_info)],
+        "fr_plan_chunk_of": [P, u32, u64, C.POINTER(u64)],
+        "fr_plan_entry_layout": [P, u32, C.POINTER(u64), C.POINTER(u64), C.POINTER(u64)],
+        "fr_plan_destroy": [P],
+        "fr_layout_query": [P, u32, u64, u64, u64, C.POINTER(fr_plan_info), P, P],
+        "fr_pack_state": [P, P, P, u64, P, P],
+        "fr_unpack_state": [P, P, P, P, P, P, P],
+        "fr_verify_replicas": [P, P, P, P, P, P, P, P],
+        "fr_checksum_state": [P, P, P, P],
+        "fr_strerror": [i32],
+        "fr_last_hip_error": [],
+        "fr_abi_version": [],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = C.c_int
+    lib.fr_strerror.restype = C.c_char_p
+    if lib.fr_abi_version() != 1:
+        raise ImportError("libflashrestore ABI version mismatch")
+    return lib
+
+
+_lib = _load()
+
+EXPORTED = (
+    "fr_plan_create", "fr_plan_get_info", "fr_plan_chunk_of", "fr_plan_entry_layout",
+    "fr_plan_destroy", "fr_layout_query", "fr_pack_state", "fr_unpack_state",
+    "fr_verify_replicas", "fr_checksum_state", "fr_strerror", "fr_last_hip_error",
+    "fr_abi_version",
+)
+
+
+def _check(rc: int, where: str):
+    if rc != FR_OK:
+        raise FlashRestoreError(rc, where)
+
+
+def as_table(table) -> np.ndarray:
+    """A contiguous fr_tensor_desc array (any structured array with the same
+    field names, or rows of (src_offset, dst_offset, numel, dtype, derive_from))."""
+    if isinstance(table, np.ndarray) and table.dtype.names:
+        out = np.zeros(len(table), dtype=DESC_DTYPE)
+        for f in DESC_DTYPE.names:
+            out[f] = table[f]
+        return out
+    return np.array([tuple(r) for r in table], dtype=DESC_DTYPE)
+
+
+def _ptr(x) -> int | None:
+    """Device address of a torch tensor, an int address, or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+
+        return torch.cuda.current_stream().cuda_stream or None
+    if isinstance(stream, int):
+        return stream or None
+    return stream.cuda_stream or None
+
+
+def fr_layout_query(table, chunk_bytes: int, src_arena_bytes: int, dst_arena_bytes: int):
+    """Host-only validation and layout: (info dict, payload offsets, chunk bases)."""
+    t = as_table(table)
+    info = fr_plan_info()
+    pay = np.zeros(max(len(t), 1), np.uint64)
+    base = np.zeros(len(t) + 1, np.uint64)
+    rc = _lib.fr_layout_query(t.ctypes.data if len(t) else None, len(t), chunk_bytes,
+                              src_arena_bytes, dst_arena_bytes, C.byref(info),
+                              pay.ctypes.data, base.ctypes.data)
+    _check(rc, "fr_layout_query")
+    return info.as_dict(), pay[: len(t)], base
+
+
+class Plan:
+    """A plan bound to the current HIP device (``fr_plan_create``)."""
+
+    def __init__(self, table, chunk_bytes: int, src_arena_bytes: int, dst_arena_bytes: int):
+        self._h = None
+        self.table = as_table(table)
+        h = C.c_void_p()
+        rc = _lib.fr_plan_create(self.table.ctypes.data if len(self.table) else None, len(self.table),
+                                 chunk_bytes, src_arena_bytes, dst_arena_bytes, C.byref(h))
+        _check(rc, "fr_plan_create")
+        self._h = h
+        info = fr_plan_info()
+        _check(_lib.fr_plan_get_info(self._h, C.byref(info)), "fr_plan_get_info")
+        self.info = info.as_dict()
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise ValueError("plan destroyed")
+        return self._h
+
+    def destroy(self):
+        if self._h is not None:
+            _lib.fr_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+    # -- sizes
+    @property
+    def n_chunks(self) -> int:
+        return self.info["n_chunks"]
+
+    @property
+    def payload_bytes(self) -> int:
+        return self.info["payload_bytes"]
+
+    @property
+    def bitmap_words(self) -> int:
+        return self.info["bitmap_words"]
+
+    def chunk_of(self, entry: int, byte_in_entry: int) -> int:
+        c = C.c_uint64()
+        _check(_lib.fr_plan_chunk_of(self.handle, entry, byte_in_entry, C.byref(c)), "fr_plan_chunk_of")
+        return c.value
+
+    def entry_layout(self, entry: int):
+        p, f, n = C.c_uint64(), C.c_uint64(), C.c_uint64()
+        _check(_lib.fr_plan_entry_layout(self.handle, entry, C.byref(p), C.byref(f), C.byref(n)),
+               "fr_plan_entry_layout")
+        return p.value, f.value, n.value
+
+    # -- device buffers (torch allocations, uint8 / int64 / int32)
+    def empty_payload(self, device="cuda"):
+        import torch
+
+        return torch.empty(max(self.payload_bytes, 1), dtype=torch.uint8, device=device)
+
+    def empty_sums(self, device="cuda"):
+        import torch
+
+        return torch.empty(max(self.n_chunks, 1), 2, dtype=torch.int64, device=device)
+
+    def empty_bitmap(self, device="cuda"):
+        import torch
+
+        return torch.empty(max(self.bitmap_words, 1), dtype=torch.int32, device=device)
+
+    def empty_counter(self, device="cuda"):
+        import torch
+
+        return torch.empty(1, dtype=torch.int64, device=device)
+
+    # -- operations
+    def pack(self, src, payload, sums, stream=None, payload_cap=None):
+        return fr_pack_state(self, src, payload, payload_cap, sums, stream)
+
+    def unpack(self, payload, sums, dst, bitmap, n_bad, stream=None):
+        return fr_unpack_state(self, payload, sums, dst, bitmap, n_bad, stream)
+
+    def verify_replicas(self, a, b, bitmap, n_diff, sums_a=None, sums_b=None, stream=None):
+        return fr_verify_replicas(self, a, b, bitmap, n_diff, sums_a, sums_b, stream)
+
+    def checksum_state(self, base, sums, stream=None):
+        return fr_checksum_state(self, base, sums, stream)
+
+
+def _nbytes(x):
+    if x is None or isinstance(x, int):
+        return None
+    return x.numel() * x.element_size()
+
+
+def fr_plan_create(table, chunk_bytes, src_arena_bytes, dst_arena_bytes) -> Plan:
+    return Plan(table, chunk_bytes, src_arena_bytes, dst_arena_bytes)
+
+
+def fr_plan_destroy(plan: Plan) -> None:
+    plan.destroy()
+
+
+def fr_pack_state(plan: Plan, src, payload, payload_cap, sums, stream=None) -> None:
+    if payload_cap is None:
+        payload_cap = _nbytes(payload)
+        if payload_cap is None:
+            payload_cap = plan.payload_bytes
+    _check(_lib.fr_pack_state(plan.handle, _ptr(src), _ptr(payload), payload_cap, _ptr(sums),
+                              _stream(stream)), "fr_pack_state")
+
+
+def fr_unpack_state(plan: Plan, payload, sums, dst, bad_bitmap, n_bad, stream=None) -> None:
+    _check(_lib.fr_unpack_state(plan.handle, _ptr(payload), _ptr(sums), _ptr(dst), _ptr(bad_bitmap),
+                                _ptr(n_bad), _stream(stream)), "fr_unpack_state")
+
+
+def fr_verify_replicas(plan: Plan, base_a, base_b, diff_bitmap, n_diff, sums_a=None, sums_b=None,
+                       stream=None) -> None:
+    _check(_lib.fr_verify_replicas(plan.handle, _ptr(base_a), _ptr(base_b), _ptr(diff_bitmap),
+                                   _ptr(n_diff), _ptr(sums_a), _ptr(sums_b), _stream(stream)),
+           "fr_verify_replicas")
+
+
+def fr_checksum_state(plan: Plan, base, sums, stream=None) -> None:
+    _check(_lib.fr_checksum_state(plan.handle, _ptr(base), _ptr(sums), _stream(stream)),
+           "fr_checksum_state")
+
+
+def fr_strerror(status: int) -> str:
+    return _lib.fr_strerror(status).decode()
+
+
+def fr_abi_version() -> int:
+    return _lib.fr_abi_version()
+
+
+def bitmap_indices(bitmap, n_chunks: int) -> np.ndarray:
+    """Sorted chunk ids of the set bits of a result bitmap (host copy)."""
+    b = bitmap.detach().cpu().numpy() if hasattr(bitmap, "detach") else np.asarray(bitmap)
+    bits = np.unpackbits(np.ascontiguousarray(b).view(np.uint8), bitorder="little")
+    return np.nonzero(bits[:n_chunks])[0]

@@ -1,0 +1,190 @@
+"""GPU parity on small inputs: the HIP path through the C ABI vs the CPU
+oracle, bit for bit (payload, sums, receiver arena with canaries, bitmaps,
+counts), plus fault injection, determinism and error behaviour."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+from oracle import cpu  # noqa: E402
+from paper_2509_03047_amd import workloads as W  # noqa: E402
+
+from tests.gpu_util import Restore, log, sums_host, to_dev, to_host  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2509_03047_amd import flashrestore  # noqa: F401  (fails loudly if unbuilt)
+
+
+def _check_against_oracle(t, C, src_np, src_bytes, dst_bytes, corrupt_rng=None, tag=""):
+    r = Restore(t, C, src_bytes, dst_bytes)
+    src = to_dev(src_np) if src_np.size else torch.empty(1, dtype=torch.uint8, device="cuda")
+    r.pack(src)
+    pay, sums = cpu.pack(t, C, src_np)
+    nc = r.n_chunks
+    g_pay = to_host(r.payload)[: pay.size]
+    g_sums = sums_host(r.sums, nc)
+    assert np.array_equal(g_pay, pay), f"payload {tag}"
+    assert np.array_equal(g_sums, sums), f"sums {tag}"
+    # optionally corrupt the wire
+    if corrupt_rng is not None and pay.size and corrupt_rng.random() < 0.5:
+        b = int(corrupt_rng.integers(0, pay.size * 8))
+        pay[b // 8] ^= np.uint8(1 << (b % 8))
+        r.payload[b // 8] ^= 1 << (b % 8)
+    if corrupt_rng is not None and nc and corrupt_rng.random() < 0.25:
+        c = int(corrupt_rng.integers(0, nc))
+        sums[2 * c] ^= np.uint64(1)
+        r.sums[c, 0] ^= 1
+    r.unpack()
+    dst = np.full(max(dst_bytes, 1), 0xA5, np.uint8)
+    bm, nbad = cpu.unpack(t, C, pay, sums, dst)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(r.dst), dst), f"dst {tag}"
+    assert r.bad_set() == set(cpu.bitmap_to_set(bm, nc)), f"bad set {tag}"
+    assert int(r.n_bad.item()) == nbad
+    # verify the restored replica against the sender (same layout only) and a flipped copy
+    b_np = src_np.copy()
+    if b_np.size:
+        for _ in range(int((corrupt_rng or np.random.default_rng(0)).integers(0, 3))):
+            b = int((corrupt_rng or np.random.default_rng(0)).integers(0, b_np.size * 8))
+            b_np[b // 8] ^= np.uint8(1 << (b % 8))
+    bd = to_dev(b_np) if b_np.size else torch.empty(1, dtype=torch.uint8, device="cuda")
+    sa, sb = r.plan.empty_sums(), r.plan.empty_sums()
+    r.verify(src, bd, sa, sb)
+    vbm, nd, osa, osb = cpu.verify(t, C, src_np, b_np, with_sums=True)
+    assert r.diff_set() == set(cpu.bitmap_to_set(vbm, nc)), f"diff {tag}"
+    assert int(r.n_diff.item()) == nd
+    assert np.array_equal(sums_host(sa, nc), osa) and np.array_equal(sums_host(sb, nc), osb)
+    r.verify(src, bd)  # without sums: same set
+    assert r.diff_set() == set(cpu.bitmap_to_set(vbm, nc))
+    r.checksum(src)
+    torch.cuda.synchronize()
+    assert np.array_equal(sums_host(r.csum, nc), cpu.checksum(t, C, src_np))
+
+
+def test_bruteforce_tiny_tables():
+    rng = np.random.default_rng(1234)
+    n = 1000
+    for it in range(n):
+        t, sb, db = W.random_tiny_table(rng)
+        C = int(rng.choice([16, 32, 64, 256]))
+        src = W.random_tiny_state(t, sb, rng)
+        _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"table {it} C={C}")
+        if it % 200 == 0:
+            log(f"tiny table {it}/{n}")
+
+
+def test_bruteforce_multi_tile_ragged():
+    """Tables whose chunks span several workgroup passes with ragged tails."""
+    rng = np.random.default_rng(99)
+    for it in range(40):
+        t, sb, db = W.random_tiny_table(rng, max_entries=8, max_numel=300_000)
+        C = int(rng.choice([4096, 16384, 65536, 1 << 20]))
+        src = W.random_tiny_state(t, sb, rng)
+        _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"multi {it} C={C}")
+
+
+def test_toy_decoder_full_parity():
+    w = W.make_workload(0)
+    src = W.fill_state(w)
+    log("toy decoder", w.n_params, "params")
+    _check_against_oracle(w.table, w.chunk_bytes, src, w.src_arena_bytes, w.dst_arena_bytes, tag="toy")
+    # exact round trip and nothing flagged
+    r = Restore(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
+    s = to_dev(src)
+    r.pack(s)
+    r.unpack()
+    torch.cuda.synchronize()
+    assert torch.equal(r.dst, s) and int(r.n_bad.item()) == 0
+
+
+def test_fault_injection_toy_exact_sets():
+    """Single flips in the payload, the sums, the sender's param or master:
+    the GPU flags exactly the oracle's chunks."""
+    w = W.make_workload(0)
+    src = W.fill_state(w)
+    t, C = w.table, w.chunk_bytes
+    rng = np.random.default_rng(7)
+    r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes)
+    s = to_dev(src)
+    r.pack(s)
+    pay, sums = cpu.pack(t, C, src)
+    nc = r.n_chunks
+    for _ in range(24):  # payload flips
+        b = int(rng.integers(0, pay.size * 8))
+        p = pay.copy()
+        p[b // 8] ^= np.uint8(1 << (b % 8))
+        gp = r.payload.clone()
+        gp[b // 8] ^= 1 << (b % 8)
+        r.unpack(payload=gp)
+        bm, nbad = cpu.unpack(t, C, p, sums, np.zeros(w.dst_arena_bytes, np.uint8))
+        assert r.bad_set() == set(cpu.bitmap_to_set(bm, nc)) and nbad >= 1
+    for _ in range(8):  # sums flips
+        c = int(rng.integers(0, nc))
+        gs = r.sums.clone()
+        gs[c, int(rng.integers(0, 2))] ^= 1 << int(rng.integers(0, 63))
+        r.unpack(sums=gs)
+        assert r.bad_set() == {c}
+    for _ in range(24):  # sender-side flips before pack (any of the 4 arrays)
+        b = int(rng.integers(0, src.size * 8))
+        s2 = src.copy()
+        s2[b // 8] ^= np.uint8(1 << (b % 8))
+        p, sm = cpu.pack(t, C, s2)
+        bm, _ = cpu.unpack(t, C, p, sm, np.zeros(w.dst_arena_bytes, np.uint8))
+        g2 = s.clone()
+        g2[b // 8] ^= 1 << (b % 8)
+        r.pack(g2)
+        r.unpack()
+        assert r.bad_set() == set(cpu.bitmap_to_set(bm, nc))
+
+
+def test_deterministic_across_grid_sizes():
+    w = W.make_workload(0)
+    src = to_dev(W.fill_state(w))
+    outs = []
+    old = os.environ.get("FLASHRESTORE_MAX_GRID")
+    try:
+        for g in ("1", "7", "300", ""):
+            os.environ["FLASHRESTORE_MAX_GRID"] = g
+            r = Restore(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
+            gp = None
+            r.pack(src)
+            gp = r.payload.clone()
+            gp[12345] ^= 4  # one bad chunk
+            r.unpack(payload=gp)
+            r.verify(src, r.dst)
+            torch.cuda.synchronize()
+            outs.append((r.payload.cpu(), r.sums.cpu(), r.dst.cpu(), r.bad.cpu(), r.n_bad.cpu(), r.diff.cpu()))
+    finally:
+        if old is None:
+            os.environ.pop("FLASHRESTORE_MAX_GRID", None)
+        else:
+            os.environ["FLASHRESTORE_MAX_GRID"] = old
+    for o in outs[1:]:
+        for x, y in zip(outs[0], o):
+            assert torch.equal(x, y)
+    assert int(outs[0][4].item()) >= 1
+
+
+def test_empty_and_zero_length_tables():
+    from paper_2509_03047_amd import flashrestore as F
+
+    for rows in ([], [(0, 0, 0, 1, -1), (16, 16, 0, 2, -1)]):
+        t = F.as_table(rows) if rows else np.zeros(0, dtype=F.DESC_DTYPE)
+        r = Restore(t, 64, 64, 64)
+        assert r.n_chunks == 0 and r.plan.payload_bytes == 0
+        src = torch.zeros(64, dtype=torch.uint8, device="cuda")
+        r.n_bad.fill_(77)
+        r.pack(src)
+        r.unpack()
+        r.verify(src, src)
+        r.checksum(src)
+        torch.cuda.synchronize()
+        assert int(r.n_bad.item()) == 0 and int(r.n_diff.item()) == 0
+        assert torch.all(r.dst == 0xA5)
