@@ -1,0 +1,262 @@
+#!/usr/bin/env python3
+"""Benchmark of the replica state-restore hot path on one MI355X.
+
+One step = one pass of the whole path over one rank's training state:
+  pack + checksum (donor) -> unpack + bf16 re-derive + verify (receiver)
+  -> replica compare (donor vs restored) -> checksum of the restored state.
+The workload is one rank's share of a Llama-3-8B-shaped state under tensor
+parallel 8 (1,004,015,616 params; bf16 param + fp32 master + fp32 Adam m, v =
+14,056,218,624 bytes; 64 KiB chunks), synthetic values, resident in HBM
+before timing starts.  The plan (descriptor validation and device tables) is
+built once, outside the timed region.
+
+Prints one JSON line: whole-step throughput in state GB/s, per-operation
+times and algorithmic HBM GB/s, a roofline entry for the dominant kernel and
+the CPU oracle's rate on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+METRIC = "state restore GB/s per GPU (pack+checksum, unpack+verify) and % of HBM peak"
+KERNEL_SOURCES = ("paper_2509_03047_amd/csrc/kernels.hip", "paper_2509_03047_amd/csrc/fr_internal.h")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+KERNEL_NAMES = {"pack": "k_pack", "unpack": "k_unpack", "verify": "k_verify", "checksum": "k_pack"}
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=1, help="workload: 0 toy, 1 8B share, 2 stress, 3 70B share")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time per baseline")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 4 GiB device copy (for counter scaling) and exit")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(info) -> dict:
+    """Bytes each operation must move at least (read + write), per launch."""
+    S, P, n = info["state_bytes"], info["payload_bytes"], info["n_chunks"]
+    words = info["bitmap_words"]
+    return {
+        "pack": S + P + 16 * n,
+        "unpack": P + 16 * n + S + 4 * words,
+        "verify": 2 * S + 4 * words,
+        "checksum": S + 16 * n,
+    }
+
+
+def copy_calibration():
+    import torch
+
+    n = 4 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    reps = 10
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"bytes_per_copy": 2 * n, "ms": ms, "gbs": 2 * n / ms / 1e6}
+
+
+def cpu_baseline(w, src_np, seconds: float):
+    """The oracle, as it stands, on a prefix of the same workload: the
+    embedding and the first layers (whole logical tensors)."""
+    import numpy as np
+
+    from oracle import cpu
+
+    t = w.table
+    # prefix of whole logical tensors (4 entries each) up to ~2 GB of state
+    es = np.where(t["dtype"] == 1, 4, 2).astype(np.int64) * t["numel"].astype(np.int64)
+    cum = np.cumsum(es)
+    n_ent = 4
+    while n_ent + 4 <= len(t) and cum[n_ent + 4 - 1] <= 2_100_000_000:
+        n_ent += 4
+    sub = t[:n_ent].copy()
+    end = int(sub["src_offset"][-1]) + int(es[n_ent - 1])
+    state = int(cum[n_ent - 1])
+    src = src_np[:end]
+    C = w.chunk_bytes
+    dst = np.empty(end, np.uint8)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        pay, sums = cpu.pack(sub, C, src)
+        bm, nbad = cpu.unpack(sub, C, pay, sums, dst)
+        vb, nd = cpu.verify(sub, C, src, dst)
+        cs = cpu.checksum(sub, C, dst)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or reps >= 20:
+            break
+    assert nbad == 0 and nd == 0
+    return {
+        "value": round(state * reps / el / 1e9, 4),
+        "unit": "GB/s",
+        "cores": cpu.threads(),
+        "kind": "oracle",
+        "sample": f"first {n_ent} of {len(t)} entries ({n_ent // 4} logical tensors, {state} state bytes), "
+                  f"{reps} full steps (pack+unpack+verify+checksum) in {el:.1f} s",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the restore shards per rank; see the sharding notes). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    if args.copy_calibration:
+        print(json.dumps({"copy_calibration": copy_calibration()}), flush=True)
+        return
+
+    from paper_2509_03047_amd import flashrestore as F
+    from paper_2509_03047_amd import workloads as W
+
+    w = W.make_workload(args.config)
+    t0 = time.perf_counter()
+    src_np = W.fill_state(w)
+    print(f"# generated {w.name}: {w.state_bytes} state bytes in {time.perf_counter() - t0:.1f} s",
+          file=sys.stderr, flush=True)
+    plan = F.Plan(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
+    info = plan.info
+    src = torch.from_numpy(src_np).to("cuda")
+    payload, sums = plan.empty_payload(), plan.empty_sums()
+    dst = torch.empty(w.dst_arena_bytes, dtype=torch.uint8, device="cuda")
+    bad, nbad = plan.empty_bitmap(), plan.empty_counter()
+    diff, ndiff = plan.empty_bitmap(), plan.empty_counter()
+    csum = plan.empty_sums()
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    ops = ("pack", "unpack", "verify", "checksum")
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        plan.pack(src, payload, sums, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        plan.unpack(payload, sums, dst, bad, nbad, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+        plan.verify_replicas(src, dst, diff, ndiff, stream=stream)
+        if ev is not None:
+            ev[3].record(stream)
+        plan.checksum_state(dst, csum, stream=stream)
+        if ev is not None:
+            ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for k in range(args.steps):
+        step(evs[k])
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(end)
+    per_op = {op: sum(e[i].elapsed_time(e[i + 1]) for e in evs) / args.steps for i, op in enumerate(ops)}
+
+    # the pass restored the state exactly: nothing flagged, receiver == sender
+    ok = int(nbad.item()) == 0 and int(ndiff.item()) == 0 and torch.equal(dst, src)
+    ok = ok and torch.equal(csum[: plan.n_chunks], sums[: plan.n_chunks])
+
+    ms_step = total_ms / args.steps
+    value = info["state_bytes"] / (ms_step * 1e-3) / 1e9
+    alg = algorithmic_bytes(info)
+    op_report = {}
+    for op in ops:
+        gbs = alg[op] / (per_op[op] * 1e-3) / 1e9
+        op_report[op] = {"ms": round(per_op[op], 4), "alg_bytes": alg[op], "hbm_gbs": round(gbs, 1),
+                         "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
+    restore_ms = per_op["pack"] + per_op["unpack"]
+    dom = max(ops, key=lambda o: per_op[o])
+    roof = {"bound": "hbm", "kernel": KERNEL_NAMES[dom], "op": dom,
+            "achieved": op_report[dom]["hbm_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": op_report[dom]["frac_of_peak"], "traffic": None}
+    try:
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("kernel_source_sha") == kernel_source_hash() and tr.get("config") == args.config:
+            roof["traffic"] = tr.get("ops", {}).get(dom, {}).get("bytes_per_launch")
+    except (OSError, ValueError):
+        pass
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32/u64",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "params": w.n_params,
+            "state_bytes": info["state_bytes"],
+            "payload_bytes": info["payload_bytes"],
+            "chunk_bytes": info["chunk_bytes"],
+            "n_chunks": info["n_chunks"],
+            "step": "pack+checksum -> unpack+derive+verify -> verify_replicas -> checksum_state",
+        },
+        "restore_gbs": round(info["state_bytes"] / (restore_ms * 1e-3) / 1e9, 2),
+        "ops": op_report,
+        "roofline": roof,
+        "parity_ok": bool(ok),
+        "wall_s_timed": round(wall, 4),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, src_np, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

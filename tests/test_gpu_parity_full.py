@@ -1,0 +1,235 @@
+"""GPU parity at full workload sizes, in the launch configuration the benchmark
+times (default plan, one workgroup per unit).
+
+* Llama-3-8B TP=8 rank share (14.06 GB state): the whole oracle runs on the
+  host; payload, sums, receiver arena and result sets are compared bit for bit.
+* 20,000-entry descriptor stress (7.6 GB): whole oracle, scattered layouts,
+  canaries in every receiver gap.
+* Llama-3-70B TP=8 x PP=4 first-stage share (31.8 GB): sampled chunks against
+  the oracle plus properties that hold at any size (exact round trip, nothing
+  flagged, checksum == pack sums, replica compare empty).
+* Replica compare on two copies of the 8B share with k in {0, 1, 64, 4096}
+  distinct random bit flips: the flagged set equals the closed form
+  {chunk of each flipped byte} and the oracle's set.
+"""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+from oracle import cpu  # noqa: E402
+from paper_2509_03047_amd import workloads as W  # noqa: E402
+
+from tests.gpu_util import Restore, log, sums_host, to_host  # noqa: E402
+
+
+@pytest.fixture(scope="module")
+def llama8b():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    w = W.make_workload(1)
+    import time
+
+    t0 = time.perf_counter()
+    src = W.fill_state(w)
+    log(f"generated {w.name} ({w.state_bytes} B) in {time.perf_counter() - t0:.1f} s")
+    return w, src
+
+
+def _upload(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(a).to("cuda")
+
+
+def _flip_on_device(t: torch.Tensor, bit_positions: np.ndarray):
+    """XOR distinct bit positions into a device byte tensor (bytes may repeat)."""
+    if bit_positions.size == 0:
+        return
+    by = (bit_positions // 8).astype(np.int64)
+    masks = (np.uint8(1) << (bit_positions % 8).astype(np.uint8)).astype(np.uint8)
+    order = np.argsort(by, kind="stable")
+    by, masks = by[order], masks[order]
+    uniq, start = np.unique(by, return_index=True)
+    comb = np.bitwise_or.reduceat(masks, start)
+    idx = torch.from_numpy(uniq).to("cuda")
+    m = torch.from_numpy(comb).to("cuda")
+    t[idx] = t[idx] ^ m
+
+
+def _expected_chunks(w, plan_base, bit_positions):
+    starts = w.table["src_offset"].astype(np.int64)
+    out = set()
+    for p in bit_positions:
+        byte = int(p) // 8
+        e = int(np.searchsorted(starts, byte, side="right") - 1)
+        out.add(int(plan_base[e]) + (byte - int(starts[e])) // w.chunk_bytes)
+    return out
+
+
+@pytest.mark.timeout(900)
+def test_llama8b_tp8_full_parity(llama8b):
+    w, src_np = llama8b
+    t, C = w.table, w.chunk_bytes
+    r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes, canary=0xA5)
+    src = _upload(src_np)
+    r.pack(src)
+    r.unpack()
+    r.verify(src, r.dst)
+    r.checksum(r.dst)
+    torch.cuda.synchronize()
+    log("gpu ops done")
+    pay, sums = cpu.pack(t, C, src_np)
+    log("oracle pack done")
+    nc = r.n_chunks
+    assert nc == 214_684 and pay.size == 12_048_187_392
+    assert np.array_equal(sums_host(r.sums, nc), sums)
+    g_pay = to_host(r.payload)
+    assert np.array_equal(g_pay[: pay.size], pay)
+    del g_pay
+    dst = np.full(w.dst_arena_bytes, 0xA5, np.uint8)
+    bm, nbad = cpu.unpack(t, C, pay, sums, dst)
+    log("oracle unpack done")
+    assert nbad == 0 and int(r.n_bad.item()) == 0 and r.bad_set() == set()
+    assert np.array_equal(to_host(r.dst), dst)
+    assert int(r.n_diff.item()) == 0 and r.diff_set() == set()
+    assert np.array_equal(sums_host(r.csum, nc), sums)
+
+
+@pytest.mark.timeout(900)
+def test_llama8b_replica_verify_flips(llama8b):
+    w, a_np = llama8b
+    t, C = w.table, w.chunk_bytes
+    r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes)
+    a = _upload(a_np)
+    b = a.clone()
+    base = cpu.plan(t, C)[1]
+    nc = r.n_chunks
+    ref_sums = cpu.checksum(t, C, a_np)
+    log("oracle checksum of A done")
+    for k in (0, 1, 64, 4096):
+        pos = W.flip_positions(a_np.size * 8, k, 4000 + k)
+        exp = _expected_chunks(w, base, pos)
+        _flip_on_device(b, pos)
+        sa, sb = r.plan.empty_sums(), r.plan.empty_sums()
+        r.verify(a, b, sa, sb)
+        got = r.diff_set()
+        assert got == exp, f"k={k}"
+        assert int(r.n_diff.item()) == len(exp)
+        # the oracle's exact compare on the same bytes
+        b_np = a_np.copy()
+        W.apply_flips(b_np, pos)
+        vb, nd = cpu.verify(t, C, a_np, b_np)
+        assert set(cpu.bitmap_to_set(vb, nc)) == exp and nd == len(exp)
+        # sums of A equal the oracle's; sums of B differ exactly on the set
+        g_sa, g_sb = sums_host(sa, nc), sums_host(sb, nc)
+        assert np.array_equal(g_sa, ref_sums)
+        ids = np.array(sorted(exp), dtype=np.uint64)
+        if ids.size:
+            assert np.array_equal(g_sb.reshape(-1, 2)[ids.astype(np.int64)].reshape(-1),
+                                  cpu.checksum_chunks(t, C, b_np, ids))
+        same = np.ones(nc, bool)
+        same[ids.astype(np.int64)] = False
+        assert np.array_equal(g_sb.reshape(-1, 2)[same], g_sa.reshape(-1, 2)[same])
+        del b_np
+        _flip_on_device(b, pos)  # restore B
+        log(f"replica verify k={k}: {len(exp)} chunks")
+    r.verify(a, b)
+    assert r.diff_set() == set()
+
+
+@pytest.mark.timeout(900)
+def test_descriptor_stress_full_parity():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    w = W.make_workload(2)
+    t, C = w.table, w.chunk_bytes
+    src_np = W.fill_state(w)
+    log(f"generated {w.name}: {len(t)} entries, {w.state_bytes} B")
+    r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes, canary=0xA5)
+    src = _upload(src_np)
+    r.pack(src)
+    r.unpack()
+    r.checksum(src)
+    torch.cuda.synchronize()
+    pay, sums = cpu.pack(t, C, src_np)
+    nc = r.n_chunks
+    assert np.array_equal(sums_host(r.sums, nc), sums)
+    assert np.array_equal(to_host(r.payload)[: pay.size], pay)
+    dst = np.full(w.dst_arena_bytes, 0xA5, np.uint8)
+    bm, nbad = cpu.unpack(t, C, pay, sums, dst)
+    assert nbad == 0 and r.bad_set() == set() and int(r.n_bad.item()) == 0
+    assert np.array_equal(to_host(r.dst), dst)
+    assert np.array_equal(sums_host(r.csum, nc), sums)
+    # a corrupted wire on this layout: three payload flips
+    rng = np.random.default_rng(5)
+    for _ in range(3):
+        bit = int(rng.integers(0, pay.size * 8))
+        pay[bit // 8] ^= np.uint8(1 << (bit % 8))
+        r.payload[bit // 8] ^= 1 << (bit % 8)
+    r.unpack()
+    dst = np.full(w.dst_arena_bytes, 0xA5, np.uint8)
+    bm, nbad = cpu.unpack(t, C, pay, sums, dst)
+    assert r.bad_set() == set(cpu.bitmap_to_set(bm, nc)) and int(r.n_bad.item()) == nbad
+
+
+@pytest.mark.timeout(900)
+def test_llama70b_stage0_sampled_parity():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    w = W.make_workload(3)
+    t, C = w.table, w.chunk_bytes
+    src_np = W.fill_state(w)
+    log(f"generated {w.name}: {w.state_bytes} B")
+    r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes)
+    src = _upload(src_np)
+    r.pack(src)
+    r.unpack()
+    r.verify(src, r.dst)
+    r.checksum(r.dst)
+    torch.cuda.synchronize()
+    nc = r.n_chunks
+    assert nc == 30_474
+    # properties at full size
+    assert int(r.n_bad.item()) == 0 and int(r.n_diff.item()) == 0
+    assert torch.equal(r.dst, src)
+    assert torch.equal(r.csum[:nc], r.sums[:nc])
+    # sampled chunks against the oracle, one by one
+    _, base, pay_off, pb = cpu.plan(t, C)
+    assert pb == r.plan.payload_bytes == 27_249_082_368
+    rng = np.random.default_rng(33)
+    ids = np.unique(np.concatenate([rng.integers(0, nc, 512), [0, nc - 1]])).astype(np.uint64)
+    exp = cpu.checksum_chunks(t, C, src_np, ids)
+    assert np.array_equal(sums_host(r.sums, nc).reshape(-1, 2)[ids.astype(np.int64)].reshape(-1), exp)
+    for c in ids[:64]:
+        c = int(c)
+        k = int(np.searchsorted(base, c, side="right") - 1)
+        j = c - int(base[k])
+        nb = int(t[k]["numel"]) * W.ESIZE[int(t[k]["dtype"])]
+        ln = min(C, nb - j * C)
+        so = int(t[k]["src_offset"]) + j * C
+        if int(t[k]["derive_from"]) < 0:
+            po = int(pay_off[k]) + j * C
+            assert np.array_equal(to_host(r.payload[po:po + ln]), src_np[so:so + ln])
+    # one flip on the wire is located in the 1 MiB-chunk layout: the master
+    # (or moment) chunk that holds it, plus the derived param chunk when the
+    # flipped master rounds to a different bf16 value
+    sent = [k for k in range(len(t)) if int(t[k]["derive_from"]) < 0]
+    starts = np.array([int(pay_off[k]) for k in sent], np.int64)
+    bit = int(rng.integers(0, pb * 8))
+    byte = bit // 8
+    k = sent[int(np.searchsorted(starts, byte, side="right") - 1)]
+    off = byte - int(pay_off[k])
+    exp = {int(base[k]) + off // C}
+    derived = [d for d in range(len(t)) if int(t[d]["derive_from"]) == k]
+    if derived:
+        d, el = derived[0], off // 4
+        mo = int(t[k]["src_offset"]) + 4 * el
+        m = src_np[mo:mo + 4].copy()
+        m[off % 4] ^= np.uint8(1 << (bit % 8))
+        po = int(t[d]["src_offset"]) + 2 * el
+        if W._bf16_round(m.view(np.float32)).tobytes() != src_np[po:po + 2].tobytes():
+            exp.add(int(base[d]) + (2 * el) // C)
+    r.payload[byte] ^= 1 << (bit % 8)
+    r.unpack()
+    assert r.bad_set() == exp
+    assert int(r.n_bad.item()) == len(exp)
