@@ -111,8 +111,8 @@ extern "C" int fr_pack_state(const fr_plan* plan, const void* src_base, void* pa
   const Region outs[] = {{payload, L.payload_bytes}, {sums, L.n_chunks * sizeof(fr_chunk_sum)}};
   const Region ins[] = {{src_base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 2, ins, 1));
-  return launch_result(launch_pack(plan->d_chunks, uint32_t(L.n_chunks), src_base, payload, sums,
-                                   plan->cfg, stream));
+  return launch_result(launch_pack(plan->d_chunks, uint32_t(L.n_chunks), L.C, src_base, payload,
+                                   sums, plan->scratch, plan->cfg, stream));
 }
 
 extern "C" int fr_unpack_state(const fr_plan* plan, const void* payload, const fr_chunk_sum* sums,
@@ -130,9 +130,21 @@ extern "C" int fr_unpack_state(const fr_plan* plan, const void* payload, const f
   const Region outs[] = {{dst_base, plan->dst_arena_bytes}, {bad_bitmap, words * 4}, {n_bad, 8}};
   const Region ins[] = {{payload, L.payload_bytes}, {sums, L.n_chunks * sizeof(fr_chunk_sum)}};
   FR_TRY(check_disjoint(outs, 3, ins, 2));
-  return launch_result(launch_unpack(plan->d_chunks, plan->d_units, plan->n_units, L.C, words,
-                                     payload, sums, dst_base, bad_bitmap, n_bad, plan->cfg,
-                                     stream));
+  UnpackArgs u;
+  u.chunks = plan->d_chunks;
+  u.derived = plan->d_derived;
+  u.n_derived = plan->n_derived;
+  u.plain = plan->d_plain;
+  u.n_plain = plan->n_plain;
+  u.n_chunks = uint32_t(L.n_chunks);
+  u.C = L.C;
+  u.payload = payload;
+  u.sums = sums;
+  u.dst = dst_base;
+  u.bitmap = bad_bitmap;
+  u.n_bad = n_bad;
+  u.scratch = plan->scratch;
+  return launch_result(launch_unpack(u, plan->cfg, stream));
 }
 
 extern "C" int fr_verify_replicas(const fr_plan* plan, const void* base_a, const void* base_b,
@@ -155,8 +167,9 @@ extern "C" int fr_verify_replicas(const fr_plan* plan, const void* base_a, const
   const Region outs[] = {{diff_bitmap, words * 4}, {n_diff, 8}, {sums_a, sb}, {sums_b, sb}};
   const Region ins[] = {{base_a, plan->src_arena_bytes}, {base_b, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 4, ins, 2));
-  return launch_result(launch_verify(plan->d_chunks, uint32_t(L.n_chunks), words, base_a, base_b,
-                                     diff_bitmap, n_diff, sums_a, sums_b, plan->cfg, stream));
+  return launch_result(launch_verify(plan->d_chunks, uint32_t(L.n_chunks), L.C, base_a, base_b,
+                                     diff_bitmap, n_diff, sums_a, sums_b, plan->scratch,
+                                     plan->cfg, stream));
 }
 
 extern "C" int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums,
@@ -170,7 +183,8 @@ extern "C" int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk
   const Region ins[] = {{base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 1, ins, 1));
   return launch_result(
-      launch_checksum(plan->d_chunks, uint32_t(L.n_chunks), base, sums, plan->cfg, stream));
+      launch_checksum(plan->d_chunks, uint32_t(L.n_chunks), L.C, base, sums, plan->scratch,
+                      plan->cfg, stream));
 }
 
 extern "C" const char* fr_strerror(int status) {

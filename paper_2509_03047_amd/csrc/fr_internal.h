@@ -36,25 +36,56 @@ struct Layout {
 int validate_and_layout(const fr_tensor_desc* table, uint32_t n, uint64_t C, uint64_t src_bytes,
                         uint64_t dst_bytes, Layout* out);
 
-// Launch configuration shared by all kernels.
+// Launch configuration of a plan.  A tile is B threads x U 16-byte vectors
+// per workgroup: 0 = 256x1, 1 = 512x1, 2 = 256x2, 3 = 256x4, 4 = 64x4,
+// 5 = 128x2, 6 = 64x2, 7 = 64x1, 8 = 128x1, 9 = 128x4, 10 = 64x8.
 struct LaunchCfg {
-  uint32_t max_grid;  // upper bound on workgroups per launch (grid-stride beyond)
+  uint32_t max_grid = 0;  // cap on workgroups per launch (0: hardware limit); grid-stride beyond
+  int tile_pack = 0, tile_unpack = 0, tile_verify = 0, tile_checksum = 0;
 };
+
+// Device scratch owned by a plan: per-chunk accumulators (G per chunk, see
+// accumulators_per_chunk), a second set for the replica compare's sums of
+// arena B, and one 32-bit flag per chunk.  Every operation clears what it
+// uses first, so operations on one plan must not overlap in time.
+struct Scratch {
+  fr_chunk_sum* acc = nullptr;
+  fr_chunk_sum* acc_b = nullptr;
+  uint32_t* flags = nullptr;
+};
+
+struct UnpackArgs {
+  const ChunkRec* chunks;
+  const uint32_t* derived;  // derived (bf16 param) chunk ids
+  uint32_t n_derived;
+  const uint32_t* plain;    // chunks copied as they are
+  uint32_t n_plain;
+  uint32_t n_chunks;
+  uint64_t C;
+  const void* payload;
+  const fr_chunk_sum* sums;
+  void* dst;
+  uint32_t* bitmap;
+  uint64_t* n_bad;
+  Scratch scratch;
+};
+
+// Bytes of one slice for a tile, and the accumulators a chunk of C bytes
+// needs with that tile (kernels.hip).
+uint32_t tile_bytes(int tile);
+uint64_t accumulators_per_chunk(uint64_t C, int tile);
 
 // Kernel launchers (kernels.hip).  They assume validated arguments, enqueue
 // on `stream` and return the hipError_t of the launches as an int.
-int launch_pack(const ChunkRec* chunks, uint32_t n_chunks, const void* src, void* payload,
-                fr_chunk_sum* sums, const LaunchCfg& cfg, void* stream);
-int launch_checksum(const ChunkRec* chunks, uint32_t n_chunks, const void* base,
-                    fr_chunk_sum* sums, const LaunchCfg& cfg, void* stream);
-int launch_unpack(const ChunkRec* chunks, const uint32_t* units, uint32_t n_units, uint64_t C,
-                  uint64_t bitmap_words, const void* payload, const fr_chunk_sum* sums,
-                  void* dst, uint32_t* bitmap, uint64_t* n_bad, const LaunchCfg& cfg,
-                  void* stream);
-int launch_verify(const ChunkRec* chunks, uint32_t n_chunks, uint64_t bitmap_words,
-                  const void* a, const void* b, uint32_t* bitmap, uint64_t* n_diff,
-                  fr_chunk_sum* sums_a, fr_chunk_sum* sums_b, const LaunchCfg& cfg,
-                  void* stream);
+int launch_pack(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* src,
+                void* payload, fr_chunk_sum* sums, const Scratch& scr, const LaunchCfg& cfg,
+                void* stream);
+int launch_checksum(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* base,
+                    fr_chunk_sum* sums, const Scratch& scr, const LaunchCfg& cfg, void* stream);
+int launch_unpack(const UnpackArgs& args, const LaunchCfg& cfg, void* stream);
+int launch_verify(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* a,
+                  const void* b, uint32_t* bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
+                  fr_chunk_sum* sums_b, const Scratch& scr, const LaunchCfg& cfg, void* stream);
 
 }  // namespace fr
 
@@ -64,7 +95,11 @@ struct fr_plan {
   fr::Layout layout;
   uint64_t src_arena_bytes = 0, dst_arena_bytes = 0;
   fr::ChunkRec* d_chunks = nullptr;  // n_chunks records
-  uint32_t* d_units = nullptr;       // unpack work list
-  uint32_t n_units = 0;
+  uint32_t* d_derived = nullptr;     // unpack units: derived chunk ids
+  uint32_t n_derived = 0;
+  uint32_t* d_plain = nullptr;       // unpack units: plain chunk ids
+  uint32_t n_plain = 0;
+  void* d_scratch = nullptr;         // one allocation holding `scratch`
+  fr::Scratch scratch{};
   fr::LaunchCfg cfg{};
 };

@@ -2,18 +2,31 @@
 // re-derive + verify, replica compare, checksum.
 //
 // All four are pure streaming (no reuse, integer arithmetic only), so the
-// bound is HBM bandwidth.  Layout of the work:
-//   * one unit = one chunk (or, for unpack, one bf16 parameter chunk together
-//     with the two fp32 master chunks it is rounded from), processed by one
-//     256-thread workgroup; units are taken in grid-stride order;
-//   * each thread moves 16-byte vectors with non-temporal loads and stores,
-//     kUnroll vectors in flight before the first is consumed;
-//   * FRSUM-128 partial sums live in 64-bit registers per lane; a unit's
-//     sums are folded across the wavefront with cross-lane shuffles and
-//     across the four wavefronts through LDS (double-buffered, so one
-//     barrier per unit);
-//   * result sets are written with 32-bit atomic OR and a 64-bit atomic add,
-//     whose outcome does not depend on the order of the units.
+// bound is HBM bandwidth, and what decides the achieved bandwidth is how the
+// waves' accesses are spread over memory.  Measured on MI355X: a copy in
+// which each workgroup streams its own 64 KiB region (thousands of
+// concurrent sequential streams) saturates near 5.3-5.5 TB/s, while the same
+// copy cut into 4-8 KiB slices, one slice per workgroup and workgroups
+// launched in address order, keeps the whole chip working inside one compact
+// window and reaches 6.5-6.7 TB/s.  So:
+//   * the unit of work is a slice of SL = min(tile, C) bytes of one chunk
+//     (tile = B threads x U vectors x 16 B); chunk c owns SPC = C / SL
+//     consecutive workgroup ids, so launch order is table (address) order;
+//   * each thread moves U 16-byte vectors with non-temporal loads/stores;
+//   * FRSUM-128 is additive over any split of a chunk when every word keeps
+//     its absolute index, so a slice sums its words with their chunk-relative
+//     indices, folds the totals over the workgroup (cross-lane shuffles, then
+//     LDS), and one thread adds them into 64-bit accumulators with atomics
+//     (order-independent, hence deterministic);
+//   * atomics on one address serialise, so no accumulator takes more than
+//     16 slices (32 for a bf16 parameter fed by master slices): a chunk of
+//     SPC slices owns G = max(1, SPC / 16) accumulators in the plan's
+//     scratch, cleared by a fill kernel launched first;
+//   * replica compare marks a differing chunk with a plain store of 1 to a
+//     per-chunk flag (idempotent, so no atomics on shared bitmap words);
+//   * a finalize kernel, one lane per chunk, folds the G accumulators into
+//     the chunk's sums (pack, checksum, compare) or compares them with the
+//     sums sent (unpack), and writes whole bitmap words from wave ballots.
 #include <hip/hip_runtime.h>
 
 #include "fr_internal.h"
@@ -24,10 +37,6 @@ namespace {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned long long u64;
-
-constexpr int kBlock = 256;
-constexpr int kWaves = kBlock / 64;
-constexpr int kUnroll = 8;
 
 __device__ __forceinline__ u32x4 ld_nt(const u32x4* p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void st_nt(u32x4 v, u32x4* p) { __builtin_nontemporal_store(v, p); }
@@ -91,12 +100,11 @@ __device__ __forceinline__ u32x4 mask_tail(const u32x4& x, uint32_t t) {
   return u32x4{o[0], o[1], o[2], o[3]};
 }
 
-// Sum K 64-bit values over the workgroup; every thread receives the totals.
-// `lds` holds two buffers; alternating `parity` per unit makes one barrier
-// enough (a buffer is rewritten only after the next unit's barrier, which all
-// readers of the previous use have passed).
-template <int K>
-__device__ __forceinline__ void block_sum(u64 (&v)[K], u64 (&lds)[2][kWaves][K], int parity) {
+// Sum K 64-bit values over the workgroup; thread 0 receives the totals.
+// `lds` holds two buffers; alternating `parity` per slice makes one barrier
+// per slice enough when a workgroup walks several slices.
+template <int B, int K>
+__device__ __forceinline__ void block_sum(u64 (&v)[K], u64 (&lds)[2][B / 64][K], int parity) {
 #pragma unroll
   for (int k = 0; k < K; k++) {
 #pragma unroll
@@ -108,338 +116,573 @@ __device__ __forceinline__ void block_sum(u64 (&v)[K], u64 (&lds)[2][kWaves][K],
     for (int k = 0; k < K; k++) lds[parity][wave][k] = v[k];
   }
   __syncthreads();
+  if (threadIdx.x == 0) {
 #pragma unroll
-  for (int k = 0; k < K; k++) {
-    u64 t = 0;
+    for (int k = 0; k < K; k++) {
+      u64 t = 0;
 #pragma unroll
-    for (int w = 0; w < kWaves; w++) t += lds[parity][w][k];
-    v[k] = t;
+      for (int w = 0; w < B / 64; w++) t += lds[parity][w][k];
+      v[k] = t;
+    }
   }
 }
 
-__device__ __forceinline__ void flag(uint32_t c, uint32_t* bitmap, u64* count) {
-  atomicOr(bitmap + (c >> 5), 1u << (c & 31));
-  atomicAdd(count, 1ull);
+__device__ __forceinline__ void add_sum(fr_chunk_sum* acc, u64 s, u64 ws) {
+  atomicAdd(reinterpret_cast<u64*>(&acc->sum), s);
+  atomicAdd(reinterpret_cast<u64*>(&acc->wsum), ws);
 }
 
-__device__ __forceinline__ bool differs(const fr_chunk_sum& want, u64 s, u64 ws) {
-  return want.sum != s || want.wsum != ws;
-}
+// Geometry of the slice walk shared by the kernels.
+struct Walk {
+  u64 n_slices;       // workgroup ids to cover (units << spc_shift)
+  uint32_t sl_vec;    // vectors per slice: SL / 16
+  uint32_t spc_shift; // log2(SPC), slices per chunk
+  uint32_t g_shift;   // log2(G), accumulators per chunk
+};
+
+constexpr uint32_t kAccSlicesShift = 4;  // 16 slices per accumulator
 
 // ------------------------------------------------------------------ pack
 
 // kStore: pack (copy non-derived chunks into the payload); otherwise
-// checksum only.  Every chunk's sums come from the bytes read at src.
-template <bool kStore>
-__global__ __launch_bounds__(kBlock) void k_pack(const ChunkRec* __restrict__ chunks,
-                                                 uint32_t n_chunks,
-                                                 const uint8_t* __restrict__ src,
-                                                 uint8_t* __restrict__ payload,
-                                                 fr_chunk_sum* __restrict__ sums) {
-  __shared__ u64 lds[2][kWaves][2];
+// checksum only.  Sums of the bytes read at src go to acc (zeroed), every
+// chunk's own accumulators; derived entries are read and summed only.
+template <int B, int U, bool kStore>
+__global__ __launch_bounds__(B) void k_pack(const ChunkRec* __restrict__ chunks, Walk wk,
+                                            const uint8_t* __restrict__ src,
+                                            uint8_t* __restrict__ payload,
+                                            fr_chunk_sum* __restrict__ acc_out) {
+  __shared__ u64 lds[2][B / 64][2];
   int parity = 0;
-  for (uint32_t c = blockIdx.x; c < n_chunks; c += gridDim.x, parity ^= 1) {
+  const uint32_t spc_mask = (1u << wk.spc_shift) - 1;
+  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
+    const uint32_t c = uint32_t(g >> wk.spc_shift);
+    const uint32_t j = uint32_t(g) & spc_mask;
     const ChunkRec r = chunks[c];
+    const uint32_t nvec = r.len >> 4, tail = r.len & 15;
+    const uint32_t v0 = j * wk.sl_vec;  // first vector of the slice
+    if (v0 > nvec || (v0 == nvec && tail == 0)) continue;  // slice past the chunk's end
     const u32x4* s = reinterpret_cast<const u32x4*>(src + r.src_off);
     const bool store = kStore && r.pay_off != kNoPayload;
     u32x4* d = reinterpret_cast<u32x4*>(payload + (store ? r.pay_off : 0));
-    const uint32_t nvec = r.len >> 4;
     u64 acc[2] = {0, 0};
-    uint32_t v = threadIdx.x;
-    for (; v + (kUnroll - 1) * kBlock < nvec; v += kUnroll * kBlock) {
-      u32x4 x[kUnroll];
+    u32x4 x[U];
 #pragma unroll
-      for (int q = 0; q < kUnroll; q++) x[q] = ld_nt(s + v + q * kBlock);
+    for (int q = 0; q < U; q++) {
+      const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+      if (l < wk.sl_vec && v < nvec) x[q] = ld_nt(s + v);
+    }
 #pragma unroll
-      for (int q = 0; q < kUnroll; q++) {
-        acc4(x[q], 4 * (v + q * kBlock), acc[0], acc[1]);
-        if (store) st_nt(x[q], d + v + q * kBlock);
+    for (int q = 0; q < U; q++) {
+      const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+      if (l < wk.sl_vec && v < nvec) {
+        acc4(x[q], 4 * v, acc[0], acc[1]);
+        if (store) st_nt(x[q], d + v);
       }
     }
-    for (; v < nvec; v += kBlock) {
-      const u32x4 x = ld_nt(s + v);
-      acc4(x, 4 * v, acc[0], acc[1]);
-      if (store) st_nt(x, d + v);
+    if (tail && nvec >= v0 && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
+      const u32x4 t = load_tail(reinterpret_cast<const uint8_t*>(s + nvec), tail);
+      acc4(t, 4 * nvec, acc[0], acc[1]);
+      if (store) d[nvec] = t;  // the segment's zero padding is written with it
     }
-    const uint32_t tail = r.len & 15;
-    if (tail && threadIdx.x == nvec % kBlock) {
-      const u32x4 x = load_tail(reinterpret_cast<const uint8_t*>(s + nvec), tail);
-      acc4(x, 4 * nvec, acc[0], acc[1]);
-      if (store) d[nvec] = x;  // the segment's zero padding is written with it
-    }
-    block_sum<2>(acc, lds, parity);
-    if (threadIdx.x == 0) {
-      sums[c].sum = acc[0];
-      sums[c].wsum = acc[1];
-    }
+    block_sum<B, 2>(acc, lds, parity);
+    if (threadIdx.x == 0)
+      add_sum(acc_out + ((u64(c) << wk.g_shift) + (j >> kAccSlicesShift)), acc[0], acc[1]);
   }
 }
 
 // ---------------------------------------------------------------- unpack
 
-__global__ __launch_bounds__(kBlock) void k_unpack(const ChunkRec* __restrict__ chunks,
-                                                   const uint32_t* __restrict__ units,
-                                                   uint32_t n_units, uint32_t cvec,
-                                                   const uint8_t* __restrict__ payload,
-                                                   const fr_chunk_sum* __restrict__ sums,
-                                                   uint8_t* __restrict__ dst,
-                                                   uint32_t* __restrict__ bitmap,
-                                                   u64* __restrict__ n_bad) {
-  __shared__ u64 lds[2][kWaves][6];
+// Two kinds of units, derived groups first:
+//   derived: bf16 parameter chunk c and the master chunks m0 = master(c) and
+//            m0 + 1 holding its 2 * len source bytes; walked in slices of
+//            master bytes (2 * SPC slices per unit), each slice inside one
+//            master chunk;
+//   plain:   a chunk of an entry that is neither derived nor a master with a
+//            derived image; SPC slices per unit.
+// Sums of the bytes written go to the accumulators `acc_out` (zeroed).
+template <int B, int U>
+__global__ __launch_bounds__(B) void k_unpack(const ChunkRec* __restrict__ chunks,
+                                              const uint32_t* __restrict__ derived,
+                                              const uint32_t* __restrict__ plain, Walk wk,
+                                              u64 n_derived_slices, uint32_t cvec,
+                                              const uint8_t* __restrict__ payload,
+                                              uint8_t* __restrict__ dst,
+                                              fr_chunk_sum* __restrict__ acc_out) {
+  __shared__ u64 lds[2][B / 64][4];
   int parity = 0;
-  for (uint32_t u = blockIdx.x; u < n_units; u += gridDim.x, parity ^= 1) {
-    const uint32_t c = units[u];
-    const ChunkRec r = chunks[c];
-    u64 acc[6] = {0, 0, 0, 0, 0, 0};
-    if (r.master == kNoMaster) {
-      // Plain chunk: copy, then check the bytes as written.
-      const u32x4* s = reinterpret_cast<const u32x4*>(payload + r.pay_off);
-      u32x4* d = reinterpret_cast<u32x4*>(dst + r.dst_off);
-      const uint32_t nvec = r.len >> 4;
-      uint32_t v = threadIdx.x;
-      for (; v + (kUnroll - 1) * kBlock < nvec; v += kUnroll * kBlock) {
-        u32x4 x[kUnroll];
-#pragma unroll
-        for (int q = 0; q < kUnroll; q++) x[q] = ld_nt(s + v + q * kBlock);
-#pragma unroll
-        for (int q = 0; q < kUnroll; q++) {
-          st_nt(x[q], d + v + q * kBlock);
-          acc4(x[q], 4 * (v + q * kBlock), acc[0], acc[1]);
-        }
-      }
-      for (; v < nvec; v += kBlock) {
-        const u32x4 x = ld_nt(s + v);
-        st_nt(x, d + v);
-        acc4(x, 4 * v, acc[0], acc[1]);
-      }
-      const uint32_t tail = r.len & 15;
-      if (tail && threadIdx.x == nvec % kBlock) {
-        // The payload segment is padded to 16 bytes, so the whole vector is
-        // readable; only the entry's bytes are written and summed.
-        const u32x4 x = mask_tail(s[nvec], tail);
-        store_tail(reinterpret_cast<uint8_t*>(d + nvec), x, tail);
-        acc4(x, 4 * nvec, acc[0], acc[1]);
-      }
-      block_sum<6>(acc, lds, parity);
-      if (threadIdx.x == 0 && differs(sums[c], acc[0], acc[1])) flag(c, bitmap, n_bad);
-    } else {
-      // Derived group: bf16 parameter chunk c (r.len bytes) and the master
-      // chunks m0 = r.master and m0 + 1 that hold its 2 * r.len source bytes.
+  const uint32_t spc_mask = (1u << wk.spc_shift) - 1;
+  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
+    u64 acc[4] = {0, 0, 0, 0};
+    if (g < n_derived_slices) {
+      const uint32_t c = derived[g >> (wk.spc_shift + 1)];
+      const uint32_t j = uint32_t(g) & (2 * spc_mask + 1);
+      const ChunkRec r = chunks[c];
+      const uint32_t mvec = (2 * r.len) >> 4;  // whole master vectors of the group
+      const uint32_t mtail = (2 * r.len) & 15;  // 0, 4, 8 or 12: whole fp32 values
+      const uint32_t v0 = j * wk.sl_vec;
+      if (v0 > mvec || (v0 == mvec && mtail == 0)) continue;
       const uint32_t m0 = r.master;
       const ChunkRec m = chunks[m0];
-      const uint32_t mbytes = 2 * r.len;
-      const uint32_t nvm = mbytes >> 4;
+      const uint32_t part = j >> wk.spc_shift;  // master chunk of this slice: m0 + part
+      const uint32_t wbase = part * cvec * 4;   // its first word in the group
       const u32x4* s = reinterpret_cast<const u32x4*>(payload + m.pay_off);
       u32x4* md = reinterpret_cast<u32x4*>(dst + m.dst_off);
       u32x2* pd = reinterpret_cast<u32x2*>(dst + r.dst_off);
-      // Vectors [0, cvec) belong to master chunk m0, [cvec, nvm) to m0 + 1.
+      u32x4 x[U];
 #pragma unroll
-      for (int part = 0; part < 2; part++) {
-        const uint32_t lo = part ? cvec : 0;
-        const uint32_t hi = part ? nvm : (nvm < cvec ? nvm : cvec);
-        u64& ms = acc[2 * part];
-        u64& mws = acc[2 * part + 1];
-        uint32_t v = lo + threadIdx.x;
-        for (; v + (kUnroll - 1) * kBlock < hi; v += kUnroll * kBlock) {
-          u32x4 x[kUnroll];
+      for (int q = 0; q < U; q++) {
+        const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+        if (l < wk.sl_vec && v < mvec) x[q] = ld_nt(s + v);
+      }
 #pragma unroll
-          for (int q = 0; q < kUnroll; q++) x[q] = ld_nt(s + v + q * kBlock);
-#pragma unroll
-          for (int q = 0; q < kUnroll; q++) {
-            const uint32_t vv = v + q * kBlock;
-            st_nt(x[q], md + vv);
-            acc4(x[q], 4 * (vv - lo), ms, mws);
-            const u32x2 p = rne4(x[q]);
-            st_nt2(p, pd + vv);
-            acc2(p, 2 * vv, acc[4], acc[5]);
-          }
-        }
-        for (; v < hi; v += kBlock) {
-          const u32x4 x = ld_nt(s + v);
-          st_nt(x, md + v);
-          acc4(x, 4 * (v - lo), ms, mws);
-          const u32x2 p = rne4(x);
+      for (int q = 0; q < U; q++) {
+        const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+        if (l < wk.sl_vec && v < mvec) {
+          st_nt(x[q], md + v);
+          acc4(x[q], 4 * v - wbase, acc[0], acc[1]);
+          const u32x2 p = rne4(x[q]);
           st_nt2(p, pd + v);
-          acc2(p, 2 * v, acc[4], acc[5]);
+          acc2(p, 2 * v, acc[2], acc[3]);
         }
       }
-      const uint32_t tail = mbytes & 15;  // 0, 4, 8 or 12: whole fp32 values
-      if (tail && threadIdx.x == nvm % kBlock) {
-        const u32x4 x = mask_tail(s[nvm], tail);  // padded segment: readable
-        uint8_t* mt = reinterpret_cast<uint8_t*>(md + nvm);
-        uint32_t* mw = reinterpret_cast<uint32_t*>(mt);
-        const uint32_t nf = tail >> 2;
-        if (nf > 0) mw[0] = x.x;
-        if (nf > 1) mw[1] = x.y;
-        if (nf > 2) mw[2] = x.z;
-        const int part = nvm < cvec ? 0 : 1;
-        const uint32_t lo = part ? cvec : 0;
-        acc4(x, 4 * (nvm - lo), acc[2 * part], acc[2 * part + 1]);
-        uint16_t* ph = reinterpret_cast<uint16_t*>(pd + nvm);
-        const uint32_t h0 = rne_bf16(x.x), h1 = rne_bf16(x.y), h2 = rne_bf16(x.z);
-        if (nf > 0) ph[0] = uint16_t(h0);
+      if (mtail && mvec >= v0 && mvec - v0 < wk.sl_vec && threadIdx.x == (mvec - v0) % B) {
+        const u32x4 t = mask_tail(s[mvec], mtail);  // padded segment: readable
+        uint32_t* mw = reinterpret_cast<uint32_t*>(md + mvec);
+        const uint32_t nf = mtail >> 2;
+        mw[0] = t.x;
+        if (nf > 1) mw[1] = t.y;
+        if (nf > 2) mw[2] = t.z;
+        acc4(t, 4 * mvec - wbase, acc[0], acc[1]);
+        uint16_t* ph = reinterpret_cast<uint16_t*>(pd + mvec);
+        const uint32_t h0 = rne_bf16(t.x), h1 = rne_bf16(t.y), h2 = rne_bf16(t.z);
+        ph[0] = uint16_t(h0);
         if (nf > 1) ph[1] = uint16_t(h1);
         if (nf > 2) ph[2] = uint16_t(h2);
         const u32x2 p{h0 | (nf > 1 ? h1 << 16 : 0u), nf > 2 ? h2 : 0u};
-        acc2(p, 2 * nvm, acc[4], acc[5]);
+        acc2(p, 2 * mvec, acc[2], acc[3]);
       }
-      block_sum<6>(acc, lds, parity);
+      block_sum<B, 4>(acc, lds, parity);
       if (threadIdx.x == 0) {
-        if (differs(sums[m0], acc[0], acc[1])) flag(m0, bitmap, n_bad);
-        if (mbytes > 16 * cvec && differs(sums[m0 + 1], acc[2], acc[3])) flag(m0 + 1, bitmap, n_bad);
-        if (differs(sums[c], acc[4], acc[5])) flag(c, bitmap, n_bad);
+        const uint32_t jj = j - (part << wk.spc_shift);  // slice within its master chunk
+        add_sum(acc_out + ((u64(m0 + part) << wk.g_shift) + (jj >> kAccSlicesShift)), acc[0],
+                acc[1]);
+        // a parameter accumulator covers 16 slices' worth of parameter bytes,
+        // which come from 32 master slices
+        add_sum(acc_out + ((u64(c) << wk.g_shift) + (j >> (kAccSlicesShift + 1))), acc[2],
+                acc[3]);
       }
+    } else {
+      const u64 h = g - n_derived_slices;
+      const uint32_t c = plain[h >> wk.spc_shift];
+      const uint32_t j = uint32_t(h) & spc_mask;
+      const ChunkRec r = chunks[c];
+      const uint32_t nvec = r.len >> 4, tail = r.len & 15;
+      const uint32_t v0 = j * wk.sl_vec;
+      if (v0 > nvec || (v0 == nvec && tail == 0)) continue;
+      const u32x4* s = reinterpret_cast<const u32x4*>(payload + r.pay_off);
+      u32x4* d = reinterpret_cast<u32x4*>(dst + r.dst_off);
+      u32x4 x[U];
+#pragma unroll
+      for (int q = 0; q < U; q++) {
+        const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+        if (l < wk.sl_vec && v < nvec) x[q] = ld_nt(s + v);
+      }
+#pragma unroll
+      for (int q = 0; q < U; q++) {
+        const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+        if (l < wk.sl_vec && v < nvec) {
+          st_nt(x[q], d + v);
+          acc4(x[q], 4 * v, acc[0], acc[1]);
+        }
+      }
+      if (tail && nvec >= v0 && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
+        // The payload segment is padded to 16 bytes, so the whole vector is
+        // readable; only the entry's bytes are written and summed.
+        const u32x4 t = mask_tail(s[nvec], tail);
+        store_tail(reinterpret_cast<uint8_t*>(d + nvec), t, tail);
+        acc4(t, 4 * nvec, acc[0], acc[1]);
+      }
+      block_sum<B, 4>(acc, lds, parity);
+      if (threadIdx.x == 0)
+        add_sum(acc_out + ((u64(c) << wk.g_shift) + (j >> kAccSlicesShift)), acc[0], acc[1]);
     }
   }
 }
 
 // ---------------------------------------------------------------- verify
 
-template <bool kSums>
-__global__ __launch_bounds__(kBlock) void k_verify(const ChunkRec* __restrict__ chunks,
-                                                   uint32_t n_chunks,
-                                                   const uint8_t* __restrict__ a,
-                                                   const uint8_t* __restrict__ b,
-                                                   uint32_t* __restrict__ bitmap,
-                                                   u64* __restrict__ n_diff,
-                                                   fr_chunk_sum* __restrict__ sums_a,
-                                                   fr_chunk_sum* __restrict__ sums_b) {
-  __shared__ u64 lds[2][kWaves][4];
-  constexpr int U = kSums ? kUnroll / 2 : kUnroll;
+// flags[c] <- 1 when any slice of chunk c differs (flags zeroed); with kSums
+// the sums of both arenas go to acc_a / acc_b (zeroed).
+template <int B, int U, bool kSums>
+__global__ __launch_bounds__(B) void k_verify(const ChunkRec* __restrict__ chunks, Walk wk,
+                                              const uint8_t* __restrict__ a,
+                                              const uint8_t* __restrict__ b,
+                                              uint32_t* __restrict__ flags,
+                                              fr_chunk_sum* __restrict__ acc_a,
+                                              fr_chunk_sum* __restrict__ acc_b) {
+  __shared__ u64 lds[2][B / 64][4];
   int parity = 0;
-  for (uint32_t c = blockIdx.x; c < n_chunks; c += gridDim.x, parity ^= 1) {
+  const uint32_t spc_mask = (1u << wk.spc_shift) - 1;
+  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
+    const uint32_t c = uint32_t(g >> wk.spc_shift);
+    const uint32_t j = uint32_t(g) & spc_mask;
     const ChunkRec r = chunks[c];
+    const uint32_t nvec = r.len >> 4, tail = r.len & 15;
+    const uint32_t v0 = j * wk.sl_vec;
+    if (v0 > nvec || (v0 == nvec && tail == 0)) continue;
     const u32x4* pa = reinterpret_cast<const u32x4*>(a + r.src_off);
     const u32x4* pb = reinterpret_cast<const u32x4*>(b + r.src_off);
-    const uint32_t nvec = r.len >> 4;
     u64 acc[4] = {0, 0, 0, 0};
     uint32_t diff = 0;
-    uint32_t v = threadIdx.x;
-    for (; v + (U - 1) * kBlock < nvec; v += U * kBlock) {
-      u32x4 xa[U], xb[U];
+    u32x4 xa[U], xb[U];
 #pragma unroll
-      for (int q = 0; q < U; q++) {
-        xa[q] = ld_nt(pa + v + q * kBlock);
-        xb[q] = ld_nt(pb + v + q * kBlock);
+    for (int q = 0; q < U; q++) {
+      const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+      if (l < wk.sl_vec && v < nvec) {
+        xa[q] = ld_nt(pa + v);
+        xb[q] = ld_nt(pb + v);
       }
+    }
 #pragma unroll
-      for (int q = 0; q < U; q++) {
+    for (int q = 0; q < U; q++) {
+      const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+      if (l < wk.sl_vec && v < nvec) {
         const u32x4 x = xa[q] ^ xb[q];
         diff |= x.x | x.y | x.z | x.w;
         if (kSums) {
-          acc4(xa[q], 4 * (v + q * kBlock), acc[0], acc[1]);
-          acc4(xb[q], 4 * (v + q * kBlock), acc[2], acc[3]);
+          acc4(xa[q], 4 * v, acc[0], acc[1]);
+          acc4(xb[q], 4 * v, acc[2], acc[3]);
         }
       }
     }
-    for (; v < nvec; v += kBlock) {
-      const u32x4 xa = ld_nt(pa + v), xb = ld_nt(pb + v);
-      const u32x4 x = xa ^ xb;
+    if (tail && nvec >= v0 && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
+      const u32x4 ta = load_tail(reinterpret_cast<const uint8_t*>(pa + nvec), tail);
+      const u32x4 tb = load_tail(reinterpret_cast<const uint8_t*>(pb + nvec), tail);
+      const u32x4 x = ta ^ tb;
       diff |= x.x | x.y | x.z | x.w;
       if (kSums) {
-        acc4(xa, 4 * v, acc[0], acc[1]);
-        acc4(xb, 4 * v, acc[2], acc[3]);
+        acc4(ta, 4 * nvec, acc[0], acc[1]);
+        acc4(tb, 4 * nvec, acc[2], acc[3]);
       }
     }
-    const uint32_t tail = r.len & 15;
-    if (tail && threadIdx.x == nvec % kBlock) {
-      const u32x4 xa = load_tail(reinterpret_cast<const uint8_t*>(pa + nvec), tail);
-      const u32x4 xb = load_tail(reinterpret_cast<const uint8_t*>(pb + nvec), tail);
-      const u32x4 x = xa ^ xb;
-      diff |= x.x | x.y | x.z | x.w;
-      if (kSums) {
-        acc4(xa, 4 * nvec, acc[0], acc[1]);
-        acc4(xb, 4 * nvec, acc[2], acc[3]);
-      }
-    }
-    // Any lane of any wave with a difference marks the chunk.
-    const int hit = __syncthreads_or(int(diff != 0));
-    if (kSums) block_sum<4>(acc, lds, parity);
-    if (threadIdx.x == 0) {
-      if (hit) flag(c, bitmap, n_diff);
-      if (kSums) {
-        sums_a[c].sum = acc[0];
-        sums_a[c].wsum = acc[1];
-        sums_b[c].sum = acc[2];
-        sums_b[c].wsum = acc[3];
+    // Any lane of the wave that differs marks the chunk; the store is
+    // idempotent, so several waves or slices may make it.
+    if (__ballot(diff != 0) != 0 && (threadIdx.x & 63) == 0) flags[c] = 1u;
+    if (kSums) {
+      block_sum<B, 4>(acc, lds, parity);
+      if (threadIdx.x == 0) {
+        const u64 i = (u64(c) << wk.g_shift) + (j >> kAccSlicesShift);
+        add_sum(acc_a + i, acc[0], acc[1]);
+        add_sum(acc_b + i, acc[2], acc[3]);
       }
     }
   }
 }
 
+// -------------------------------------------------------------- finalize
+
+// One lane per chunk.  Modes:
+//   kFold:    sums[c] = sum of its G accumulators              (pack, checksum)
+//   kCompare: bit c = (sum of its accumulators != sent[c])       (unpack)
+//   kFlags:   bit c = (flags[c] != 0); optional folds of two
+//             accumulator sets into sums_a / sums_b             (verify)
+// Bitmap words are written whole from wave ballots (lanes 0 and 32 each own
+// one 32-bit word), so the bitmap needs no clearing; the count takes one
+// atomic add per wave with a set bit.
+enum FinalMode { kFold = 0, kCompare = 1, kFlags = 2 };
+
+struct FinalArgs {
+  const fr_chunk_sum* acc;  // accumulators (A for kFlags)
+  const fr_chunk_sum* acc_b;
+  const fr_chunk_sum* sent;
+  const uint32_t* flags;
+  fr_chunk_sum* out;  // sums (A for kFlags)
+  fr_chunk_sum* out_b;
+  uint32_t* bitmap;
+  u64* count;
+  uint32_t n_chunks;
+  uint32_t g_shift;
+};
+
+__device__ __forceinline__ fr_chunk_sum fold(const fr_chunk_sum* acc, u64 c, uint32_t g_shift) {
+  u64 s = 0, ws = 0;
+  const u64 first = c << g_shift;
+  for (u64 i = first; i < first + (u64(1) << g_shift); i++) {
+    s += acc[i].sum;
+    ws += acc[i].wsum;
+  }
+  return fr_chunk_sum{s, ws};
+}
+
+template <int kMode>
+__global__ __launch_bounds__(256) void k_finalize(FinalArgs f) {
+  const uint32_t lane = threadIdx.x & 63;
+  const u64 stride = u64(gridDim.x) * blockDim.x;
+  for (u64 base = u64(blockIdx.x) * blockDim.x + (threadIdx.x & ~63u); base < f.n_chunks;
+       base += stride) {
+    const u64 c = base + lane;
+    const bool live = c < f.n_chunks;
+    bool bit = false;
+    if (kMode == kFold) {
+      if (live) f.out[c] = fold(f.acc, c, f.g_shift);
+      continue;
+    }
+    if (kMode == kCompare && live) {
+      const fr_chunk_sum got = fold(f.acc, c, f.g_shift);
+      bit = got.sum != f.sent[c].sum || got.wsum != f.sent[c].wsum;
+    }
+    if (kMode == kFlags && live) {
+      bit = f.flags[c] != 0;
+      if (f.out) {
+        f.out[c] = fold(f.acc, c, f.g_shift);
+        f.out_b[c] = fold(f.acc_b, c, f.g_shift);
+      }
+    }
+    const u64 mask = __ballot(bit);
+    const u64 w = base >> 5;  // base is a multiple of 64: two words per wave
+    if (lane == 0) f.bitmap[w] = uint32_t(mask);
+    if (lane == 32 && base + 32 < f.n_chunks) f.bitmap[w + 1] = uint32_t(mask >> 32);
+    if (lane == 0 && mask) atomicAdd(f.count, u64(__popcll(mask)));
+  }
+}
+
 // ------------------------------------------------------------- utilities
 
-// Clears a result bitmap and its counter (a kernel rather than a memset so
-// that the whole operation is made of kernel launches).
-__global__ void k_zero(uint32_t* __restrict__ bitmap, uint64_t words, u64* __restrict__ count) {
-  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
-  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < words; i += stride)
-    bitmap[i] = 0;
-  if (blockIdx.x == 0 && threadIdx.x == 0) *count = 0;
+// Clears up to four regions of 32-bit words (a kernel rather than a memset
+// so that an operation is made of kernel launches only).
+struct ZeroList {
+  uint32_t* p[4];
+  u64 words[4];
+};
+
+__global__ __launch_bounds__(256) void k_zero(ZeroList z) {
+  const u64 stride = u64(gridDim.x) * blockDim.x;
+#pragma unroll
+  for (int r = 0; r < 4; r++) {
+    uint32_t* p = z.p[r];
+    for (u64 i = u64(blockIdx.x) * blockDim.x + threadIdx.x; i < z.words[r]; i += stride) p[i] = 0;
+  }
 }
 
-inline uint32_t grid_for(uint64_t units, const LaunchCfg& cfg) {
-  return uint32_t(units < cfg.max_grid ? units : cfg.max_grid);
+struct Zeroes {
+  ZeroList z{};
+  int n = 0;
+  u64 total = 0;
+  void add(void* p, u64 bytes) {
+    if (!p || bytes == 0) return;
+    z.p[n] = static_cast<uint32_t*>(p);
+    z.words[n] = bytes / 4;
+    total += bytes / 4;
+    n++;
+  }
+  int launch(hipStream_t st) {
+    if (n == 0) return 0;
+    const u64 want = (total + 255) / 256;
+    const uint32_t blocks = uint32_t(want < 2048 ? (want ? want : 1) : 2048);
+    hipLaunchKernelGGL(k_zero, dim3(blocks), dim3(256), 0, st, z);
+    return int(hipGetLastError());
+  }
+};
+
+// Workgroups per launch: one per slice up to the configured cap and the
+// hardware limit of 2^32 work-items per grid; beyond that, grid-stride.
+template <int B>
+inline uint32_t grid_for(u64 units, const LaunchCfg& cfg) {
+  u64 cap = (u64(1) << 31) / B;
+  if (cfg.max_grid && cfg.max_grid < cap) cap = cfg.max_grid;
+  return uint32_t(units < cap ? units : cap);
 }
 
-inline int launch_zero(uint32_t* bitmap, uint64_t words, uint64_t* count, hipStream_t st) {
-  const uint32_t blocks = uint32_t(words / 256 + 1 < 1024 ? words / 256 + 1 : 1024);
-  hipLaunchKernelGGL(k_zero, dim3(blocks), dim3(256), 0, st, bitmap, words,
-                     reinterpret_cast<u64*>(count));
+// Slice geometry for `units` chunks (or derived groups, two chunks' worth of
+// master slices each) of C bytes and a tile of `tile_bytes`.
+inline Walk walk_for(u64 units, uint64_t C, uint32_t tile_bytes, bool derived_group = false) {
+  const uint64_t sl = C < tile_bytes ? C : tile_bytes;
+  uint32_t sh = 0;
+  while ((sl << sh) < C) sh++;
+  Walk w;
+  w.sl_vec = uint32_t(sl >> 4);
+  w.spc_shift = sh;
+  w.g_shift = sh > kAccSlicesShift ? sh - kAccSlicesShift : 0;
+  w.n_slices = units << (sh + (derived_group ? 1 : 0));
+  return w;
+}
+
+inline int launch_finalize(int mode, const FinalArgs& f, hipStream_t st) {
+  if (f.n_chunks == 0) return 0;
+  const u64 waves = (u64(f.n_chunks) + 63) / 64;
+  const u64 want = (waves + 3) / 4;
+  const dim3 grid(uint32_t(want < 8192 ? want : 8192));
+  if (mode == kFold) hipLaunchKernelGGL(k_finalize<kFold>, grid, dim3(256), 0, st, f);
+  else if (mode == kCompare) hipLaunchKernelGGL(k_finalize<kCompare>, grid, dim3(256), 0, st, f);
+  else hipLaunchKernelGGL(k_finalize<kFlags>, grid, dim3(256), 0, st, f);
   return int(hipGetLastError());
 }
+
+// Launch configurations: B threads x U vectors per slice.
+enum Tile {
+  T256x1 = 0, T512x1 = 1, T256x2 = 2, T256x4 = 3, T64x4 = 4, T128x2 = 5,
+  T64x2 = 6, T64x1 = 7, T128x1 = 8, T128x4 = 9, T64x8 = 10
+};
+
+template <int B, int U>
+int pack_impl(bool store, const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* src,
+              void* payload, fr_chunk_sum* sums, const Scratch& scr, const LaunchCfg& cfg,
+              hipStream_t st) {
+  if (n_chunks == 0) return 0;
+  const Walk wk = walk_for(n_chunks, C, B * U * 16);
+  const u64 n_acc = u64(n_chunks) << wk.g_shift;
+  Zeroes z;
+  z.add(scr.acc, n_acc * sizeof(fr_chunk_sum));
+  int e = z.launch(st);
+  if (e) return e;
+  const auto* s = static_cast<const uint8_t*>(src);
+  auto* p = static_cast<uint8_t*>(payload);
+  if (store)
+    hipLaunchKernelGGL((k_pack<B, U, true>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0, st,
+                       chunks, wk, s, p, scr.acc);
+  else
+    hipLaunchKernelGGL((k_pack<B, U, false>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0,
+                       st, chunks, wk, s, p, scr.acc);
+  e = int(hipGetLastError());
+  if (e) return e;
+  FinalArgs f{};
+  f.acc = scr.acc;
+  f.out = sums;
+  f.n_chunks = n_chunks;
+  f.g_shift = wk.g_shift;
+  return launch_finalize(kFold, f, st);
+}
+
+template <int B, int U>
+int unpack_impl(const UnpackArgs& u, const LaunchCfg& cfg, hipStream_t st) {
+  const Walk wd = walk_for(u.n_derived, u.C, B * U * 16, true);
+  Walk wk = walk_for(u.n_plain, u.C, B * U * 16);
+  const u64 n_acc = u64(u.n_chunks) << wk.g_shift;
+  Zeroes z;
+  z.add(u.scratch.acc, n_acc * sizeof(fr_chunk_sum));
+  z.add(u.n_bad, 8);
+  int e = z.launch(st);
+  if (e || u.n_chunks == 0) return e;
+  const u64 n_der = wd.n_slices;
+  wk.n_slices += n_der;
+  if (wk.n_slices) {
+    hipLaunchKernelGGL((k_unpack<B, U>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0, st,
+                       u.chunks, u.derived, u.plain, wk, n_der, uint32_t(u.C >> 4),
+                       static_cast<const uint8_t*>(u.payload), static_cast<uint8_t*>(u.dst),
+                       u.scratch.acc);
+    e = int(hipGetLastError());
+    if (e) return e;
+  }
+  FinalArgs f{};
+  f.acc = u.scratch.acc;
+  f.sent = u.sums;
+  f.bitmap = u.bitmap;
+  f.count = reinterpret_cast<u64*>(u.n_bad);
+  f.n_chunks = u.n_chunks;
+  f.g_shift = wk.g_shift;
+  return launch_finalize(kCompare, f, st);
+}
+
+template <int B, int U>
+int verify_impl(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* a,
+                const void* b, uint32_t* bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
+                fr_chunk_sum* sums_b, const Scratch& scr, const LaunchCfg& cfg, hipStream_t st) {
+  const Walk wk = walk_for(n_chunks, C, B * U * 16);
+  const u64 n_acc = u64(n_chunks) << wk.g_shift;
+  Zeroes z;
+  z.add(scr.flags, u64(n_chunks) * 4);
+  z.add(n_diff, 8);
+  if (sums_a) {
+    z.add(scr.acc, n_acc * sizeof(fr_chunk_sum));
+    z.add(scr.acc_b, n_acc * sizeof(fr_chunk_sum));
+  }
+  int e = z.launch(st);
+  if (e || n_chunks == 0) return e;
+  const auto* pa = static_cast<const uint8_t*>(a);
+  const auto* pb = static_cast<const uint8_t*>(b);
+  const dim3 grid(grid_for<B>(wk.n_slices, cfg));
+  if (sums_a)
+    hipLaunchKernelGGL((k_verify<B, U, true>), grid, dim3(B), 0, st, chunks, wk, pa, pb,
+                       scr.flags, scr.acc, scr.acc_b);
+  else
+    hipLaunchKernelGGL((k_verify<B, U, false>), grid, dim3(B), 0, st, chunks, wk, pa, pb,
+                       scr.flags, scr.acc, scr.acc_b);
+  e = int(hipGetLastError());
+  if (e) return e;
+  FinalArgs f{};
+  f.acc = scr.acc;
+  f.acc_b = scr.acc_b;
+  f.flags = scr.flags;
+  f.out = sums_a;
+  f.out_b = sums_b;
+  f.bitmap = bitmap;
+  f.count = reinterpret_cast<u64*>(n_diff);
+  f.n_chunks = n_chunks;
+  f.g_shift = wk.g_shift;
+  return launch_finalize(kFlags, f, st);
+}
+
+#define FR_DISPATCH(tile, fn, ...)                        \
+  switch (tile) {                                         \
+    case T512x1: return fn<512, 1>(__VA_ARGS__);          \
+    case T256x2: return fn<256, 2>(__VA_ARGS__);          \
+    case T256x4: return fn<256, 4>(__VA_ARGS__);          \
+    case T64x4: return fn<64, 4>(__VA_ARGS__);            \
+    case T128x2: return fn<128, 2>(__VA_ARGS__);          \
+    case T64x2: return fn<64, 2>(__VA_ARGS__);            \
+    case T64x1: return fn<64, 1>(__VA_ARGS__);            \
+    case T128x1: return fn<128, 1>(__VA_ARGS__);          \
+    case T128x4: return fn<128, 4>(__VA_ARGS__);          \
+    case T64x8: return fn<64, 8>(__VA_ARGS__);            \
+    default: return fn<256, 1>(__VA_ARGS__);              \
+  }
 
 }  // namespace
 
-int launch_pack(const ChunkRec* chunks, uint32_t n_chunks, const void* src, void* payload,
-                fr_chunk_sum* sums, const LaunchCfg& cfg, void* stream) {
-  if (n_chunks == 0) return 0;
-  hipLaunchKernelGGL(k_pack<true>, dim3(grid_for(n_chunks, cfg)), dim3(kBlock), 0,
-                     hipStream_t(stream), chunks, n_chunks,
-                     static_cast<const uint8_t*>(src), static_cast<uint8_t*>(payload), sums);
-  return int(hipGetLastError());
+uint32_t tile_bytes(int tile) {
+  switch (tile) {
+    case T512x1: return 512 * 16;
+    case T256x2: return 256 * 2 * 16;
+    case T256x4: return 256 * 4 * 16;
+    case T64x4: return 64 * 4 * 16;
+    case T128x2: return 128 * 2 * 16;
+    case T64x2: return 64 * 2 * 16;
+    case T64x1: return 64 * 16;
+    case T128x1: return 128 * 16;
+    case T128x4: return 128 * 4 * 16;
+    case T64x8: return 64 * 8 * 16;
+    default: return 256 * 16;
+  }
 }
 
-int launch_checksum(const ChunkRec* chunks, uint32_t n_chunks, const void* base,
-                    fr_chunk_sum* sums, const LaunchCfg& cfg, void* stream) {
-  if (n_chunks == 0) return 0;
-  hipLaunchKernelGGL(k_pack<false>, dim3(grid_for(n_chunks, cfg)), dim3(kBlock), 0,
-                     hipStream_t(stream), chunks, n_chunks,
-                     static_cast<const uint8_t*>(base), static_cast<uint8_t*>(nullptr), sums);
-  return int(hipGetLastError());
+uint64_t accumulators_per_chunk(uint64_t C, int tile) {
+  const Walk w = walk_for(1, C, tile_bytes(tile));
+  return uint64_t(1) << w.g_shift;
 }
 
-int launch_unpack(const ChunkRec* chunks, const uint32_t* units, uint32_t n_units, uint64_t C,
-                  uint64_t bitmap_words, const void* payload, const fr_chunk_sum* sums,
-                  void* dst, uint32_t* bitmap, uint64_t* n_bad, const LaunchCfg& cfg,
-                  void* stream) {
-  const hipStream_t st = hipStream_t(stream);
-  int e = launch_zero(bitmap, bitmap_words, n_bad, st);
-  if (e || n_units == 0) return e;
-  hipLaunchKernelGGL(k_unpack, dim3(grid_for(n_units, cfg)), dim3(kBlock), 0, st, chunks, units,
-                     n_units, uint32_t(C >> 4), static_cast<const uint8_t*>(payload), sums,
-                     static_cast<uint8_t*>(dst), bitmap, reinterpret_cast<u64*>(n_bad));
-  return int(hipGetLastError());
+int launch_pack(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* src,
+                void* payload, fr_chunk_sum* sums, const Scratch& scr, const LaunchCfg& cfg,
+                void* stream) {
+  FR_DISPATCH(cfg.tile_pack, pack_impl, true, chunks, n_chunks, C, src, payload, sums, scr, cfg,
+              hipStream_t(stream));
 }
 
-int launch_verify(const ChunkRec* chunks, uint32_t n_chunks, uint64_t bitmap_words,
-                  const void* a, const void* b, uint32_t* bitmap, uint64_t* n_diff,
-                  fr_chunk_sum* sums_a, fr_chunk_sum* sums_b, const LaunchCfg& cfg,
-                  void* stream) {
-  const hipStream_t st = hipStream_t(stream);
-  int e = launch_zero(bitmap, bitmap_words, n_diff, st);
-  if (e || n_chunks == 0) return e;
-  const dim3 grid(grid_for(n_chunks, cfg));
-  const auto* pa = static_cast<const uint8_t*>(a);
-  const auto* pb = static_cast<const uint8_t*>(b);
-  u64* nd = reinterpret_cast<u64*>(n_diff);
-  if (sums_a)
-    hipLaunchKernelGGL(k_verify<true>, grid, dim3(kBlock), 0, st, chunks, n_chunks, pa, pb,
-                       bitmap, nd, sums_a, sums_b);
-  else
-    hipLaunchKernelGGL(k_verify<false>, grid, dim3(kBlock), 0, st, chunks, n_chunks, pa, pb,
-                       bitmap, nd, sums_a, sums_b);
-  return int(hipGetLastError());
+int launch_checksum(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* base,
+                    fr_chunk_sum* sums, const Scratch& scr, const LaunchCfg& cfg, void* stream) {
+  FR_DISPATCH(cfg.tile_checksum, pack_impl, false, chunks, n_chunks, C, base, nullptr, sums, scr,
+              cfg, hipStream_t(stream));
+}
+
+int launch_unpack(const UnpackArgs& u, const LaunchCfg& cfg, void* stream) {
+  FR_DISPATCH(cfg.tile_unpack, unpack_impl, u, cfg, hipStream_t(stream));
+}
+
+int launch_verify(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* a,
+                  const void* b, uint32_t* bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
+                  fr_chunk_sum* sums_b, const Scratch& scr, const LaunchCfg& cfg, void* stream) {
+  FR_DISPATCH(cfg.tile_verify, verify_impl, chunks, n_chunks, C, a, b, bitmap, n_diff, sums_a,
+              sums_b, scr, cfg, hipStream_t(stream));
 }
 
 }  // namespace fr

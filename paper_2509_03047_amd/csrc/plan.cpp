@@ -15,6 +15,12 @@ namespace fr {
 
 thread_local int g_last_hip_error = 0;
 
+// Default tile of each operation (kernels.hip: 4 = 64 threads x 4 vectors,
+// 5 = 128 threads x 2 vectors; both 4 KiB slices), chosen by sweeping all
+// tiles on MI355X over the 8B and 70B rank-share workloads.
+constexpr uint32_t kDefaultTilePack = 4, kDefaultTileUnpack = 5, kDefaultTileVerify = 5,
+                   kDefaultTileChecksum = 4;
+
 static uint64_t esize(uint32_t dtype) { return dtype == FR_F32 ? 4 : 2; }
 static uint64_t align16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
 
@@ -131,6 +137,23 @@ static int hip_fail(hipError_t e) {
   return FR_E_DEVICE;
 }
 
+// Device copy of a host array (or an uninitialised buffer when src is NULL).
+static int upload(const void* src, size_t bytes, void** out) {
+  *out = nullptr;
+  if (bytes == 0) return FR_OK;
+  hipError_t e = hipMalloc(out, bytes);
+  if (e != hipSuccess) {
+    *out = nullptr;
+    (void)hipGetLastError();
+    return e == hipErrorOutOfMemory ? FR_E_NOMEM : hip_fail(e);
+  }
+  if (src) {
+    e = hipMemcpy(*out, src, bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  return FR_OK;
+}
+
 extern "C" int fr_plan_destroy(fr_plan* p) {
   if (!p) return FR_OK;
   int prev = -1;
@@ -139,7 +162,9 @@ extern "C" int fr_plan_destroy(fr_plan* p) {
     switched = hipSetDevice(p->device) == hipSuccess;
   }
   if (p->d_chunks) (void)hipFree(p->d_chunks);
-  if (p->d_units) (void)hipFree(p->d_units);
+  if (p->d_derived) (void)hipFree(p->d_derived);
+  if (p->d_plain) (void)hipFree(p->d_plain);
+  if (p->d_scratch) (void)hipFree(p->d_scratch);
   if (switched) (void)hipSetDevice(prev);
   delete p;
   return FR_OK;
@@ -167,9 +192,17 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
       return hip_fail(e);
     }
     p->device = dev;
-    // 0 = one workgroup per unit (capped by the hardware grid limit).
-    uint32_t mg = env_u32("FLASHRESTORE_MAX_GRID", 0);
-    p->cfg.max_grid = mg ? mg : (1u << 22);
+    // Launch tuning knobs (defaults measured on MI355X): workgroup cap
+    // (0 = one workgroup per slice) and the tile of each operation.
+    p->cfg.max_grid = env_u32("FLASHRESTORE_MAX_GRID", 0);
+    const uint32_t all = env_u32("FLASHRESTORE_TILE", ~0u);  // one tile for every operation
+    auto pick = [&](const char* name, uint32_t dflt) {
+      return int(env_u32(name, all != ~0u ? all : dflt));
+    };
+    p->cfg.tile_pack = pick("FLASHRESTORE_TILE_PACK", kDefaultTilePack);
+    p->cfg.tile_unpack = pick("FLASHRESTORE_TILE_UNPACK", kDefaultTileUnpack);
+    p->cfg.tile_verify = pick("FLASHRESTORE_TILE_VERIFY", kDefaultTileVerify);
+    p->cfg.tile_checksum = pick("FLASHRESTORE_TILE_CHECKSUM", kDefaultTileChecksum);
 
     const Layout& L = p->layout;
     std::vector<ChunkRec> recs(L.n_chunks);
@@ -198,36 +231,29 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
         }
       }
     }
-    // Unpack work list: the heavier derived groups first, then plain chunks.
-    std::vector<uint32_t> units;
-    units.reserve(units_derived.size() + units_plain.size());
-    units.insert(units.end(), units_derived.begin(), units_derived.end());
-    units.insert(units.end(), units_plain.begin(), units_plain.end());
-    p->n_units = uint32_t(units.size());
-
-    if (!recs.empty()) {
-      e = hipMalloc(&p->d_chunks, recs.size() * sizeof(ChunkRec));
-      if (e != hipSuccess) {
-        fr_plan_destroy(p);
-        return e == hipErrorOutOfMemory ? FR_E_NOMEM : hip_fail(e);
-      }
-      e = hipMemcpy(p->d_chunks, recs.data(), recs.size() * sizeof(ChunkRec), hipMemcpyHostToDevice);
-      if (e != hipSuccess) {
-        fr_plan_destroy(p);
-        return hip_fail(e);
-      }
+    // Unpack walks the derived groups first, then the plain chunks.
+    p->n_derived = uint32_t(units_derived.size());
+    p->n_plain = uint32_t(units_plain.size());
+    rc = upload(recs.data(), recs.size() * sizeof(ChunkRec), (void**)&p->d_chunks);
+    if (rc == FR_OK)
+      rc = upload(units_derived.data(), units_derived.size() * 4, (void**)&p->d_derived);
+    if (rc == FR_OK) rc = upload(units_plain.data(), units_plain.size() * 4, (void**)&p->d_plain);
+    // Scratch: accumulators for the largest G any configured tile needs.
+    uint64_t g = 1;
+    for (int t : {p->cfg.tile_pack, p->cfg.tile_unpack, p->cfg.tile_verify, p->cfg.tile_checksum})
+      g = std::max<uint64_t>(g, accumulators_per_chunk(C, t));
+    const uint64_t acc_bytes = L.n_chunks * g * sizeof(fr_chunk_sum);
+    const uint64_t flag_bytes = (L.n_chunks * 4 + 255) & ~uint64_t(255);
+    if (rc == FR_OK) rc = upload(nullptr, 2 * acc_bytes + flag_bytes, &p->d_scratch);
+    if (rc != FR_OK) {
+      fr_plan_destroy(p);
+      return rc;
     }
-    if (!units.empty()) {
-      e = hipMalloc(&p->d_units, units.size() * sizeof(uint32_t));
-      if (e != hipSuccess) {
-        fr_plan_destroy(p);
-        return e == hipErrorOutOfMemory ? FR_E_NOMEM : hip_fail(e);
-      }
-      e = hipMemcpy(p->d_units, units.data(), units.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
-      if (e != hipSuccess) {
-        fr_plan_destroy(p);
-        return hip_fail(e);
-      }
+    if (p->d_scratch) {
+      uint8_t* base = static_cast<uint8_t*>(p->d_scratch);
+      p->scratch.acc = reinterpret_cast<fr_chunk_sum*>(base);
+      p->scratch.acc_b = reinterpret_cast<fr_chunk_sum*>(base + acc_bytes);
+      p->scratch.flags = reinterpret_cast<uint32_t*>(base + 2 * acc_bytes);
     }
   } catch (const std::bad_alloc&) {
     if (p) fr_plan_destroy(p);

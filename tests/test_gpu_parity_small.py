@@ -188,3 +188,27 @@ def test_empty_and_zero_length_tables():
         torch.cuda.synchronize()
         assert int(r.n_bad.item()) == 0 and int(r.n_diff.item()) == 0
         assert torch.all(r.dst == 0xA5)
+
+
+@pytest.mark.parametrize("tile", list(range(11)))
+def test_every_tile_matches_oracle(tile):
+    """Each launch tile (threads x vectors per slice) gives the oracle's bytes."""
+    old = os.environ.get("FLASHRESTORE_TILE")
+    os.environ["FLASHRESTORE_TILE"] = str(tile)
+    try:
+        rng = np.random.default_rng(500 + tile)
+        for it in range(60):
+            t, sb, db = W.random_tiny_table(rng)
+            C = int(rng.choice([16, 64, 256, 1024, 4096]))
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"tile {tile} table {it} C={C}")
+        for it in range(5):
+            t, sb, db = W.random_tiny_table(rng, max_entries=8, max_numel=200_000)
+            C = int(rng.choice([4096, 16384, 65536, 1 << 20]))
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"tile {tile} multi {it} C={C}")
+    finally:
+        if old is None:
+            os.environ.pop("FLASHRESTORE_TILE", None)
+        else:
+            os.environ["FLASHRESTORE_TILE"] = old
