@@ -1,0 +1,128 @@
+"""Error behaviour of the operations on the GPU: each misuse returns its
+documented code, and nothing is enqueued or written (outputs prefilled with a
+pattern stay as they were)."""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+from paper_2509_03047_amd import flashrestore as F  # noqa: E402
+from paper_2509_03047_amd import workloads as W  # noqa: E402
+
+
+@pytest.fixture(scope="module")
+def setup():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    w = W.make_workload(0)
+    src = torch.from_numpy(W.fill_state(w)).to("cuda")
+    plan = F.Plan(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
+    return w, plan, src
+
+
+def _status(fn, *a, **k):
+    try:
+        fn(*a, **k)
+        return 0
+    except F.FlashRestoreError as e:
+        return e.status
+
+
+def test_pack_errors_touch_nothing(setup):
+    w, plan, src = setup
+    payload = torch.full((plan.payload_bytes + 64,), 7, dtype=torch.uint8, device="cuda")
+    sums = torch.full((plan.n_chunks, 2), 9, dtype=torch.int64, device="cuda")
+    base_p, base_s = payload.clone(), sums.clone()
+    cases = [
+        ((plan, src, payload, plan.payload_bytes - 1, sums), -3),          # payload too small
+        ((plan, src.data_ptr() + 8, payload, None, sums), -2),             # misaligned src
+        ((plan, src, payload.data_ptr() + 4, plan.payload_bytes, sums), -2),
+        ((plan, src, payload, None, sums.data_ptr() + 8), -2),
+        ((plan, None, payload, None, sums), -1),                           # null src
+        ((plan, src, payload, None, None), -1),                            # null sums
+        ((plan, src, src.data_ptr() + 1024, plan.payload_bytes, sums), -4),  # payload inside src
+    ]
+    host = np.zeros(w.src_arena_bytes + 64, np.uint8)
+    hp = (host.ctypes.data + 15) & ~15
+    cases.append(((plan, hp, payload, None, sums), -1))                    # host memory
+    for args, code in cases:
+        assert _status(F.fr_pack_state, *args) == code, (args[1:], code)
+    torch.cuda.synchronize()
+    assert torch.equal(payload, base_p) and torch.equal(sums, base_s)
+
+
+def test_unpack_and_verify_errors_touch_nothing(setup):
+    w, plan, src = setup
+    payload, sums = plan.empty_payload(), plan.empty_sums()
+    plan.pack(src, payload, sums)
+    dst = torch.full((w.dst_arena_bytes,), 0x5A, dtype=torch.uint8, device="cuda")
+    bad = torch.full((plan.bitmap_words,), -1, dtype=torch.int32, device="cuda")
+    nbad = torch.full((1,), 12345, dtype=torch.int64, device="cuda")
+    snap = (dst.clone(), bad.clone(), nbad.clone())
+    cases = [
+        (F.fr_unpack_state, (plan, payload, sums, dst, bad, None), -1),                 # null n_bad
+        (F.fr_unpack_state, (plan, payload, sums, dst.data_ptr() + 2, bad, nbad), -2),
+        (F.fr_unpack_state, (plan, payload, sums, dst, bad.data_ptr() + 2, nbad), -2),
+        (F.fr_unpack_state, (plan, payload, sums, dst, dst.data_ptr() + 4096, nbad), -4),  # bitmap in dst
+        (F.fr_unpack_state, (plan, dst, sums, dst, bad, nbad), -4),                     # payload in dst
+        (F.fr_verify_replicas, (plan, src, dst, bad, nbad, plan.empty_sums(), None), -1),  # one sums only
+        (F.fr_verify_replicas, (plan, src, dst, src.data_ptr() + 64, nbad), -4),         # bitmap in A
+        (F.fr_checksum_state, (plan, src, src.data_ptr() + 4096), -4),                  # sums in arena
+    ]
+    for fn, args, code in cases:
+        assert _status(fn, *args) == code, (fn.__name__, code)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, snap[0]) and torch.equal(bad, snap[1]) and torch.equal(nbad, snap[2])
+
+
+def test_buffer_past_its_allocation_is_rejected(setup):
+    """The arena must lie inside one device allocation (no faulting reads)."""
+    import ctypes
+
+    w, plan, src = setup
+    hip = ctypes.CDLL("libamdhip64.so")
+    p = ctypes.c_void_p()
+    assert hip.hipMalloc(ctypes.byref(p), ctypes.c_size_t(64 << 20)) == 0
+    try:
+        start = p.value + (64 << 20) - (1 << 20)  # 1 MiB left, the arena needs 51 MB
+        payload, sums = plan.empty_payload(), plan.empty_sums()
+        assert _status(F.fr_pack_state, plan, start, payload, None, sums) == -3
+        assert _status(F.fr_pack_state, plan, p.value, payload, None, sums) == 0
+        torch.cuda.synchronize()
+    finally:
+        hip.hipFree(p)
+
+
+def test_mismatch_is_data_not_an_error(setup):
+    w, plan, src = setup
+    payload, sums = plan.empty_payload(), plan.empty_sums()
+    plan.pack(src, payload, sums)
+    sums[0, 1] += 1
+    dst = torch.empty(w.dst_arena_bytes, dtype=torch.uint8, device="cuda")
+    bad, nbad = plan.empty_bitmap(), plan.empty_counter()
+    plan.unpack(payload, sums, dst, bad, nbad)  # returns normally
+    torch.cuda.synchronize()
+    assert int(nbad.item()) == 1 and list(F.bitmap_indices(bad, plan.n_chunks)) == [0]
+
+
+def test_explicit_stream_and_destroy(setup):
+    w, plan, src = setup
+    s = torch.cuda.Stream()
+    payload, sums = plan.empty_payload(), plan.empty_sums()
+    with torch.cuda.stream(s):
+        plan.pack(src, payload, sums, stream=s)
+    s.synchronize()
+    ref = plan.empty_sums()
+    plan.checksum_state(src, ref)
+    torch.cuda.synchronize()
+    assert torch.equal(ref[: plan.n_chunks], sums[: plan.n_chunks])
+    p2 = F.Plan(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
+    assert p2.chunk_of(3, 0) == plan.chunk_of(3, 0)
+    assert p2.entry_layout(1) == plan.entry_layout(1)
+    p2.destroy()
+    p2.destroy()  # idempotent in the binding
+    with pytest.raises(ValueError):
+        p2.pack(src, payload, sums)
+    with pytest.raises(F.FlashRestoreError):
+        plan.chunk_of(0, 10 ** 12)
