@@ -131,7 +131,6 @@ extern "C" int fr_unpack_state(const fr_plan* plan, const void* payload, const f
   const Region ins[] = {{payload, L.payload_bytes}, {sums, L.n_chunks * sizeof(fr_chunk_sum)}};
   FR_TRY(check_disjoint(outs, 3, ins, 2));
   UnpackArgs u;
-  u.chunks = plan->d_chunks;
   u.derived = plan->d_derived;
   u.n_derived = plan->n_derived;
   u.plain = plan->d_plain;

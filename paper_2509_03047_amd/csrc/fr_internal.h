@@ -23,6 +23,31 @@ struct alignas(16) ChunkRec {
 };
 static_assert(sizeof(ChunkRec) == 32, "ChunkRec is 32 bytes");
 
+// Unpack work units, one record each so that a workgroup needs a single
+// dependent load before it can address its data.
+// A derived group: bf16 parameter chunk j and the fp32 master chunks 2j and
+// 2j + 1 it is rounded from.
+struct alignas(16) DerivedUnit {
+  uint64_t m_pay_off;  // payload offset of master chunk 2j (the group's first master byte)
+  uint64_t m_dst_off;  // receiver offset of master chunk 2j
+  uint64_t p_dst_off;  // receiver offset of parameter chunk j
+  uint32_t len;        // parameter chunk bytes L (the group holds 2L master bytes)
+  uint32_t m0;         // global id of master chunk 2j
+  uint32_t c;          // global id of parameter chunk j
+  uint32_t pad_;
+};
+static_assert(sizeof(DerivedUnit) == 48, "DerivedUnit is 48 bytes");
+
+// A chunk copied as it is.
+struct alignas(16) PlainUnit {
+  uint64_t pay_off;
+  uint64_t dst_off;
+  uint32_t len;
+  uint32_t c;
+  uint64_t pad_;
+};
+static_assert(sizeof(PlainUnit) == 32, "PlainUnit is 32 bytes");
+
 // Host-side layout of a validated table.
 struct Layout {
   uint64_t C = 0;
@@ -55,10 +80,9 @@ struct Scratch {
 };
 
 struct UnpackArgs {
-  const ChunkRec* chunks;
-  const uint32_t* derived;  // derived (bf16 param) chunk ids
+  const DerivedUnit* derived;
   uint32_t n_derived;
-  const uint32_t* plain;    // chunks copied as they are
+  const PlainUnit* plain;
   uint32_t n_plain;
   uint32_t n_chunks;
   uint64_t C;
@@ -95,9 +119,9 @@ struct fr_plan {
   fr::Layout layout;
   uint64_t src_arena_bytes = 0, dst_arena_bytes = 0;
   fr::ChunkRec* d_chunks = nullptr;  // n_chunks records
-  uint32_t* d_derived = nullptr;     // unpack units: derived chunk ids
+  fr::DerivedUnit* d_derived = nullptr;  // unpack units: derived groups
   uint32_t n_derived = 0;
-  uint32_t* d_plain = nullptr;       // unpack units: plain chunk ids
+  fr::PlainUnit* d_plain = nullptr;      // unpack units: plain chunks
   uint32_t n_plain = 0;
   void* d_scratch = nullptr;         // one allocation holding `scratch`
   fr::Scratch scratch{};

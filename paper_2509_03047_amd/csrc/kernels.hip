@@ -100,16 +100,43 @@ __device__ __forceinline__ u32x4 mask_tail(const u32x4& x, uint32_t t) {
   return u32x4{o[0], o[1], o[2], o[3]};
 }
 
+// 64-bit value of lane (i op CTRL) for a DPP lane pattern, moved as two
+// 32-bit halves.
+template <int CTRL>
+__device__ __forceinline__ u64 dpp64(u64 v) {
+  const uint32_t lo = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(v)), CTRL, 0xF, 0xF, false));
+  const uint32_t hi = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(v >> 32)), CTRL, 0xF, 0xF, false));
+  return (u64(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ u64 readlane64(u64 v, int lane) {
+  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), lane));
+  const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v >> 32)), lane));
+  return (u64(hi) << 32) | lo;
+}
+
+// Sum of a 64-bit value over the 64 lanes of a wave (uniform result).
+// Within each row of 16 lanes: swap neighbours, swap pairs (quad_perm
+// [1,0,3,2] and [2,3,0,1]) then rotate the row by 4 and by 8, after which
+// every lane of a row holds the row's total; the four row totals are then
+// read into scalar registers and added.
+__device__ __forceinline__ u64 wave_sum(u64 v) {
+  v += dpp64<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp64<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp64<0x124>(v);  // row_ror:4
+  v += dpp64<0x128>(v);  // row_ror:8
+  return readlane64(v, 0) + readlane64(v, 16) + readlane64(v, 32) + readlane64(v, 48);
+}
+
 // Sum K 64-bit values over the workgroup; thread 0 receives the totals.
-// `lds` holds two buffers; alternating `parity` per slice makes one barrier
-// per slice enough when a workgroup walks several slices.
+// Several waves combine through LDS; `lds` holds two buffers, and
+// alternating `parity` per slice makes one barrier per slice enough when a
+// workgroup walks several slices.
 template <int B, int K>
 __device__ __forceinline__ void block_sum(u64 (&v)[K], u64 (&lds)[2][B / 64][K], int parity) {
 #pragma unroll
-  for (int k = 0; k < K; k++) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v[k] += __shfl_xor(v[k], o, 64);
-  }
+  for (int k = 0; k < K; k++) v[k] = wave_sum(v[k]);
+  if (B == 64) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (lane == 0) {
 #pragma unroll
@@ -202,33 +229,30 @@ __global__ __launch_bounds__(B) void k_pack(const ChunkRec* __restrict__ chunks,
 //            derived image; SPC slices per unit.
 // Sums of the bytes written go to the accumulators `acc_out` (zeroed).
 template <int B, int U>
-__global__ __launch_bounds__(B) void k_unpack(const ChunkRec* __restrict__ chunks,
-                                              const uint32_t* __restrict__ derived,
-                                              const uint32_t* __restrict__ plain, Walk wk,
+__global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ derived,
+                                              const PlainUnit* __restrict__ plain, Walk wk,
                                               u64 n_derived_slices, uint32_t cvec,
                                               const uint8_t* __restrict__ payload,
                                               uint8_t* __restrict__ dst,
                                               fr_chunk_sum* __restrict__ acc_out) {
   __shared__ u64 lds[2][B / 64][4];
+  __shared__ u64 lds2[2][B / 64][2];
   int parity = 0;
   const uint32_t spc_mask = (1u << wk.spc_shift) - 1;
   for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
     u64 acc[4] = {0, 0, 0, 0};
     if (g < n_derived_slices) {
-      const uint32_t c = derived[g >> (wk.spc_shift + 1)];
+      const DerivedUnit r = derived[g >> (wk.spc_shift + 1)];
       const uint32_t j = uint32_t(g) & (2 * spc_mask + 1);
-      const ChunkRec r = chunks[c];
       const uint32_t mvec = (2 * r.len) >> 4;  // whole master vectors of the group
       const uint32_t mtail = (2 * r.len) & 15;  // 0, 4, 8 or 12: whole fp32 values
       const uint32_t v0 = j * wk.sl_vec;
       if (v0 > mvec || (v0 == mvec && mtail == 0)) continue;
-      const uint32_t m0 = r.master;
-      const ChunkRec m = chunks[m0];
       const uint32_t part = j >> wk.spc_shift;  // master chunk of this slice: m0 + part
       const uint32_t wbase = part * cvec * 4;   // its first word in the group
-      const u32x4* s = reinterpret_cast<const u32x4*>(payload + m.pay_off);
-      u32x4* md = reinterpret_cast<u32x4*>(dst + m.dst_off);
-      u32x2* pd = reinterpret_cast<u32x2*>(dst + r.dst_off);
+      const u32x4* s = reinterpret_cast<const u32x4*>(payload + r.m_pay_off);
+      u32x4* md = reinterpret_cast<u32x4*>(dst + r.m_dst_off);
+      u32x2* pd = reinterpret_cast<u32x2*>(dst + r.p_dst_off);
       u32x4 x[U];
 #pragma unroll
       for (int q = 0; q < U; q++) {
@@ -265,18 +289,17 @@ __global__ __launch_bounds__(B) void k_unpack(const ChunkRec* __restrict__ chunk
       block_sum<B, 4>(acc, lds, parity);
       if (threadIdx.x == 0) {
         const uint32_t jj = j - (part << wk.spc_shift);  // slice within its master chunk
-        add_sum(acc_out + ((u64(m0 + part) << wk.g_shift) + (jj >> kAccSlicesShift)), acc[0],
+        add_sum(acc_out + ((u64(r.m0 + part) << wk.g_shift) + (jj >> kAccSlicesShift)), acc[0],
                 acc[1]);
         // a parameter accumulator covers 16 slices' worth of parameter bytes,
         // which come from 32 master slices
-        add_sum(acc_out + ((u64(c) << wk.g_shift) + (j >> (kAccSlicesShift + 1))), acc[2],
+        add_sum(acc_out + ((u64(r.c) << wk.g_shift) + (j >> (kAccSlicesShift + 1))), acc[2],
                 acc[3]);
       }
     } else {
       const u64 h = g - n_derived_slices;
-      const uint32_t c = plain[h >> wk.spc_shift];
+      const PlainUnit r = plain[h >> wk.spc_shift];
       const uint32_t j = uint32_t(h) & spc_mask;
-      const ChunkRec r = chunks[c];
       const uint32_t nvec = r.len >> 4, tail = r.len & 15;
       const uint32_t v0 = j * wk.sl_vec;
       if (v0 > nvec || (v0 == nvec && tail == 0)) continue;
@@ -303,9 +326,10 @@ __global__ __launch_bounds__(B) void k_unpack(const ChunkRec* __restrict__ chunk
         store_tail(reinterpret_cast<uint8_t*>(d + nvec), t, tail);
         acc4(t, 4 * nvec, acc[0], acc[1]);
       }
-      block_sum<B, 4>(acc, lds, parity);
+      u64 acc2v[2] = {acc[0], acc[1]};
+      block_sum<B, 2>(acc2v, lds2, parity);
       if (threadIdx.x == 0)
-        add_sum(acc_out + ((u64(c) << wk.g_shift) + (j >> kAccSlicesShift)), acc[0], acc[1]);
+        add_sum(acc_out + ((u64(r.c) << wk.g_shift) + (j >> kAccSlicesShift)), acc2v[0], acc2v[1]);
     }
   }
 }
@@ -568,7 +592,7 @@ int unpack_impl(const UnpackArgs& u, const LaunchCfg& cfg, hipStream_t st) {
   wk.n_slices += n_der;
   if (wk.n_slices) {
     hipLaunchKernelGGL((k_unpack<B, U>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0, st,
-                       u.chunks, u.derived, u.plain, wk, n_der, uint32_t(u.C >> 4),
+                       u.derived, u.plain, wk, n_der, uint32_t(u.C >> 4),
                        static_cast<const uint8_t*>(u.payload), static_cast<uint8_t*>(u.dst),
                        u.scratch.acc);
     e = int(hipGetLastError());

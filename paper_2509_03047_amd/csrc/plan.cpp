@@ -206,7 +206,6 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
 
     const Layout& L = p->layout;
     std::vector<ChunkRec> recs(L.n_chunks);
-    std::vector<uint32_t> units_derived, units_plain;
     std::vector<uint8_t> is_master(n, 0);
     for (uint32_t k = 0; k < n; k++)
       if (table[k].derive_from >= 0) is_master[table[k].derive_from] = 1;
@@ -215,29 +214,52 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
       uint64_t nb = d.numel * (d.dtype == FR_F32 ? 4 : 2);
       uint64_t nc = L.chunk_base[k + 1] - L.chunk_base[k];
       for (uint64_t j = 0; j < nc; j++) {
-        uint64_t c = L.chunk_base[k] + j;
-        ChunkRec& r = recs[c];
+        ChunkRec& r = recs[L.chunk_base[k] + j];
         r.src_off = d.src_offset + j * C;
         r.dst_off = d.dst_offset + j * C;
         r.pay_off = L.pay_off[k] == kNoPayload ? kNoPayload : L.pay_off[k] + j * C;
         r.len = uint32_t(std::min<uint64_t>(C, nb - j * C));
-        r.master = kNoMaster;
-        if (d.derive_from >= 0) {
-          // param chunk j covers master chunks 2j and 2j + 1
-          r.master = uint32_t(L.chunk_base[d.derive_from] + 2 * j);
-          units_derived.push_back(uint32_t(c));
-        } else if (!is_master[k]) {
-          units_plain.push_back(uint32_t(c));
-        }
+        // param chunk j covers master chunks 2j and 2j + 1
+        r.master = d.derive_from >= 0 ? uint32_t(L.chunk_base[d.derive_from] + 2 * j) : kNoMaster;
       }
     }
     // Unpack walks the derived groups first, then the plain chunks.
-    p->n_derived = uint32_t(units_derived.size());
-    p->n_plain = uint32_t(units_plain.size());
-    rc = upload(recs.data(), recs.size() * sizeof(ChunkRec), (void**)&p->d_chunks);
-    if (rc == FR_OK)
-      rc = upload(units_derived.data(), units_derived.size() * 4, (void**)&p->d_derived);
-    if (rc == FR_OK) rc = upload(units_plain.data(), units_plain.size() * 4, (void**)&p->d_plain);
+    std::vector<DerivedUnit> derived;
+    std::vector<PlainUnit> plain;
+    for (uint32_t k = 0; k < n; k++) {
+      const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];
+      if (table[k].derive_from >= 0) {
+        for (uint64_t c = c0; c < c1; c++) {
+          const ChunkRec& r = recs[c];
+          const ChunkRec& m = recs[r.master];
+          DerivedUnit u{};
+          u.m_pay_off = m.pay_off;
+          u.m_dst_off = m.dst_off;
+          u.p_dst_off = r.dst_off;
+          u.len = r.len;
+          u.m0 = r.master;
+          u.c = uint32_t(c);
+          derived.push_back(u);
+        }
+      } else if (!is_master[k]) {
+        for (uint64_t c = c0; c < c1; c++) {
+          PlainUnit u{};
+          u.pay_off = recs[c].pay_off;
+          u.dst_off = recs[c].dst_off;
+          u.len = recs[c].len;
+          u.c = uint32_t(c);
+          plain.push_back(u);
+        }
+      }
+    }
+    p->n_derived = uint32_t(derived.size());
+    p->n_plain = uint32_t(plain.size());
+    int rc2 = upload(recs.data(), recs.size() * sizeof(ChunkRec), (void**)&p->d_chunks);
+    if (rc2 == FR_OK)
+      rc2 = upload(derived.data(), derived.size() * sizeof(DerivedUnit), (void**)&p->d_derived);
+    if (rc2 == FR_OK)
+      rc2 = upload(plain.data(), plain.size() * sizeof(PlainUnit), (void**)&p->d_plain);
+    rc = rc2;
     // Scratch: accumulators for the largest G any configured tile needs.
     uint64_t g = 1;
     for (int t : {p->cfg.tile_pack, p->cfg.tile_unpack, p->cfg.tile_verify, p->cfg.tile_checksum})
