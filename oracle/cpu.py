@@ -41,8 +41,12 @@ def lib():
         l.oro_verify.argtypes = [P, u32, u64, P, P, P, P, P, P]
         l.oro_checksum.argtypes = [P, u32, u64, P, P]
         l.oro_checksum_chunks.argtypes = [P, u32, u64, P, P, u64, P]
+        l.oro_delta_layout.argtypes = [P, u32, u64, P, u64, P, P]
+        l.oro_pack_chunks.argtypes = [P, u32, u64, P, P, u64, P, P]
+        l.oro_unpack_chunks.argtypes = [P, u32, u64, P, P, P, u64, P, P, P]
         for f in ("oro_plan", "oro_pack", "oro_unpack", "oro_verify", "oro_checksum",
-                  "oro_checksum_chunks", "oro_selfcheck", "oro_threads"):
+                  "oro_checksum_chunks", "oro_selfcheck", "oro_threads", "oro_delta_layout",
+                  "oro_pack_chunks", "oro_unpack_chunks"):
             getattr(l, f).restype = C.c_int
         if l.oro_selfcheck() != 0:
             raise RuntimeError("oracle needs a little-endian host")
@@ -161,3 +165,44 @@ def checksum_chunks(t, C_, base: np.ndarray, ids: np.ndarray):
 def bitmap_to_set(bitmap: np.ndarray, n: int) -> list:
     bits = np.unpackbits(np.ascontiguousarray(bitmap, "<u4").view(np.uint8), bitorder="little")
     return [int(i) for i in np.nonzero(bits[:n])[0]]
+
+
+NO_PAYLOAD = (1 << 64) - 1
+
+
+def delta_layout(t, C_, ids):
+    """Per-list-position payload offsets (NO_PAYLOAD for derived) and payload bytes."""
+    t = _table(t)
+    ids = np.ascontiguousarray(ids, np.uint32)
+    off = np.zeros(max(ids.size, 1), np.uint64)
+    pb = np.zeros(1, np.uint64)
+    if lib().oro_delta_layout(_p(t), len(t), C_, _p(ids), ids.size, _p(off), _p(pb)) != 0:
+        raise ValueError("bad chunk list")
+    return off[: ids.size], int(pb[0])
+
+
+def pack_chunks(t, C_, src, ids):
+    t = _table(t)
+    ids = np.ascontiguousarray(ids, np.uint32)
+    _, pb = delta_layout(t, C_, ids)
+    payload = np.empty(max(pb, 1), np.uint8)
+    sums = np.empty(2 * max(ids.size, 1), np.uint64)
+    if lib().oro_pack_chunks(_p(t), len(t), C_, _p(src), _p(ids), ids.size, _p(payload), _p(sums)) != 0:
+        raise RuntimeError("oro_pack_chunks")
+    return payload[:pb], sums[: 2 * ids.size]
+
+
+def unpack_chunks(t, C_, payload, sums, ids, dst):
+    """Writes into dst in place; returns (bitmap over list positions, n_bad)."""
+    t = _table(t)
+    ids = np.ascontiguousarray(ids, np.uint32)
+    bitmap = np.zeros(max((ids.size + 31) // 32, 1), np.uint32)
+    nbad = np.zeros(1, np.uint64)
+    payload = np.ascontiguousarray(payload, np.uint8)
+    if payload.size == 0:
+        payload = np.zeros(1, np.uint8)
+    sums = np.ascontiguousarray(sums, np.uint64)
+    if lib().oro_unpack_chunks(_p(t), len(t), C_, _p(payload), _p(sums), _p(ids), ids.size, _p(dst),
+                               _p(bitmap), _p(nbad)) != 0:
+        raise RuntimeError("oro_unpack_chunks")
+    return bitmap[: (ids.size + 31) // 32], int(nbad[0])

@@ -297,6 +297,132 @@ int oro_checksum_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_
   return 0;
 }
 
+/* ------------------------------------------------------------ delta repair
+ *
+ * Re-sending only the chunks in which a replica diverged.  The caller lists
+ * global chunk ids in strictly increasing order.  Delta payload: the bytes of
+ * every listed chunk of a non-derived entry, in list order, each starting at
+ * a 16-aligned offset, every gap byte 0; listed chunks of a derived (bf16)
+ * entry send nothing.  sums[i] is the FRSUM of chunk ids[i] at the sender.
+ * At the receiver the sent chunks are written first; then each listed derived
+ * chunk is recomputed as RNE of the receiver's master bytes (which now hold
+ * every sent master chunk); then every listed chunk is checked, bit i of the
+ * result standing for list position i. */
+
+typedef struct {
+  uint32_t entry;
+  uint64_t j; /* chunk index within the entry */
+} chunk_loc;
+
+static chunk_loc locate(const layout* L, uint32_t n, uint64_t c) {
+  uint32_t lo = 0, hi = n; /* entry k with chunk_base[k] <= c < chunk_base[k+1] */
+  while (hi - lo > 1) {
+    uint32_t mid = lo + (hi - lo) / 2;
+    if (L->chunk_base[mid] <= c) lo = mid; else hi = mid;
+  }
+  chunk_loc r = {lo, c - L->chunk_base[lo]};
+  return r;
+}
+
+static int list_ok(const layout* L, uint32_t n, const uint32_t* ids, uint64_t n_ids) {
+  for (uint64_t i = 0; i < n_ids; i++) {
+    if (ids[i] >= L->chunk_base[n]) return 0;
+    if (i && ids[i] <= ids[i - 1]) return 0;
+  }
+  return 1;
+}
+
+int oro_delta_layout(const oro_entry* t, uint32_t n, uint64_t C, const uint32_t* ids,
+                     uint64_t n_ids, uint64_t* pay_off, uint64_t* payload_bytes) {
+  layout L;
+  if (make_layout(t, n, C, &L)) return -1;
+  if (!list_ok(&L, n, ids, n_ids)) { free_layout(&L); return -1; }
+  uint64_t pay = 0;
+  for (uint64_t i = 0; i < n_ids; i++) {
+    chunk_loc w = locate(&L, n, ids[i]);
+    if (t[w.entry].derive_from >= 0) {
+      pay_off[i] = ORO_NO_PAYLOAD;
+    } else {
+      uint64_t nb = t[w.entry].numel * esize_of(t[w.entry].dtype);
+      pay_off[i] = pay;
+      pay = align16(pay + chunk_len(nb, C, w.j));
+    }
+  }
+  *payload_bytes = pay;
+  free_layout(&L);
+  return 0;
+}
+
+int oro_pack_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* src,
+                    const uint32_t* ids, uint64_t n_ids, uint8_t* payload, uint64_t* sums) {
+  uint64_t* off = (uint64_t*)malloc(sizeof(uint64_t) * (n_ids ? n_ids : 1));
+  uint64_t pb;
+  if (!off || oro_delta_layout(t, n, C, ids, n_ids, off, &pb)) { free(off); return -1; }
+  layout L;
+  if (make_layout(t, n, C, &L)) { free(off); return -1; }
+  memset(payload, 0, pb);
+  for (uint64_t i = 0; i < n_ids; i++) {
+    chunk_loc w = locate(&L, n, ids[i]);
+    uint64_t nb = t[w.entry].numel * esize_of(t[w.entry].dtype);
+    uint64_t len = chunk_len(nb, C, w.j);
+    const uint8_t* from = src + t[w.entry].src_offset + w.j * C;
+    if (off[i] != ORO_NO_PAYLOAD) memcpy(payload + off[i], from, len);
+    oro_frsum(from, len, &sums[2 * i], &sums[2 * i + 1]);
+  }
+  free_layout(&L);
+  free(off);
+  return 0;
+}
+
+int oro_unpack_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* payload,
+                      const uint64_t* sums, const uint32_t* ids, uint64_t n_ids, uint8_t* dst,
+                      uint32_t* bitmap, uint64_t* n_bad) {
+  uint64_t* off = (uint64_t*)malloc(sizeof(uint64_t) * (n_ids ? n_ids : 1));
+  uint64_t pb;
+  if (!off || oro_delta_layout(t, n, C, ids, n_ids, off, &pb)) { free(off); return -1; }
+  layout L;
+  if (make_layout(t, n, C, &L)) { free(off); return -1; }
+  /* 1. the sent chunks */
+  for (uint64_t i = 0; i < n_ids; i++) {
+    if (off[i] == ORO_NO_PAYLOAD) continue;
+    chunk_loc w = locate(&L, n, ids[i]);
+    uint64_t nb = t[w.entry].numel * esize_of(t[w.entry].dtype);
+    memcpy(dst + t[w.entry].dst_offset + w.j * C, payload + off[i], chunk_len(nb, C, w.j));
+  }
+  /* 2. derived chunks from the receiver's masters */
+  for (uint64_t i = 0; i < n_ids; i++) {
+    if (off[i] != ORO_NO_PAYLOAD) continue;
+    chunk_loc w = locate(&L, n, ids[i]);
+    const oro_entry* e = &t[w.entry];
+    const oro_entry* m = &t[e->derive_from];
+    uint64_t len = chunk_len(e->numel * 2, C, w.j);
+    uint64_t first = w.j * C / 2; /* first element of the chunk */
+    for (uint64_t q = 0; q < len / 2; q++) {
+      uint32_t u;
+      memcpy(&u, dst + m->dst_offset + 4 * (first + q), 4);
+      uint16_t h = oro_rne_bf16(u);
+      memcpy(dst + e->dst_offset + 2 * (first + q), &h, 2);
+    }
+  }
+  /* 3. check every listed chunk as written */
+  memset(bitmap, 0, sizeof(uint32_t) * ((n_ids + 31) / 32));
+  uint64_t bad = 0;
+  for (uint64_t i = 0; i < n_ids; i++) {
+    chunk_loc w = locate(&L, n, ids[i]);
+    uint64_t nb = t[w.entry].numel * esize_of(t[w.entry].dtype);
+    uint64_t s, ws;
+    oro_frsum(dst + t[w.entry].dst_offset + w.j * C, chunk_len(nb, C, w.j), &s, &ws);
+    if (s != sums[2 * i] || ws != sums[2 * i + 1]) {
+      bitmap[i / 32] |= 1u << (i % 32);
+      bad++;
+    }
+  }
+  *n_bad = bad;
+  free_layout(&L);
+  free(off);
+  return 0;
+}
+
 int oro_selfcheck(void) { return host_is_little_endian() ? 0 : -1; }
 
 int oro_threads(void) {

@@ -46,6 +46,17 @@ int oro_checksum(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* base
 int oro_checksum_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* base,
                         const uint64_t* ids, uint64_t n_ids, uint64_t* sums);
 
+/* Delta repair over a strictly increasing list of global chunk ids (see
+ * fr_oracle.c).  pay_off[i] is ORO_NO_PAYLOAD for derived chunks; bitmap and
+ * sums are indexed by list position. */
+int oro_delta_layout(const oro_entry* t, uint32_t n, uint64_t C, const uint32_t* ids,
+                     uint64_t n_ids, uint64_t* pay_off, uint64_t* payload_bytes);
+int oro_pack_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* src,
+                    const uint32_t* ids, uint64_t n_ids, uint8_t* payload, uint64_t* sums);
+int oro_unpack_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* payload,
+                      const uint64_t* sums, const uint32_t* ids, uint64_t n_ids, uint8_t* dst,
+                      uint32_t* bitmap, uint64_t* n_bad);
+
 int oro_selfcheck(void);
 int oro_threads(void);
 

@@ -114,3 +114,60 @@ def verify(table, C, a: bytes, b: bytes):
     ca = dict(_chunks(table, C, a, "src_offset"))
     cb = dict(_chunks(table, C, b, "src_offset"))
     return {c for c in ca if ca[c] != cb[c]}
+
+
+def _chunk_map(table, C):
+    """Global chunk id -> (entry, index within entry)."""
+    out = []
+    for k, e in enumerate(table):
+        nb = int(e["numel"]) * _esize(int(e["dtype"]))
+        out += [(k, j) for j in range(-(-nb // C))]
+    return out
+
+
+def _chunk_bytes(table, C, k, j, arena, key):
+    e = table[k]
+    nb = int(e["numel"]) * _esize(int(e["dtype"]))
+    o = int(e[key]) + j * C
+    return o, min(C, nb - j * C)
+
+
+def pack_chunks(table, C, src: bytes, ids):
+    cmap = _chunk_map(table, C)
+    payload = bytearray()
+    sums = []
+    for c in ids:
+        k, j = cmap[c]
+        o, ln = _chunk_bytes(table, C, k, j, src, "src_offset")
+        if int(table[k]["derive_from"]) < 0:
+            payload += src[o:o + ln]
+            payload += bytes(-len(payload) % 16)
+        sums.append(frsum(src[o:o + ln]))
+    return bytes(payload), sums
+
+
+def unpack_chunks(table, C, payload: bytes, sums, ids, dst: bytearray):
+    cmap = _chunk_map(table, C)
+    pos = 0
+    for c in ids:
+        k, j = cmap[c]
+        if int(table[k]["derive_from"]) < 0:
+            o, ln = _chunk_bytes(table, C, k, j, dst, "dst_offset")
+            dst[o:o + ln] = payload[pos:pos + ln]
+            pos += -(-ln // 16) * 16
+    for c in ids:
+        k, j = cmap[c]
+        s = int(table[k]["derive_from"])
+        if s >= 0:
+            o, ln = _chunk_bytes(table, C, k, j, dst, "dst_offset")
+            mo = int(table[s]["dst_offset"]) + 2 * j * C
+            for q in range(ln // 2):
+                u = int.from_bytes(dst[mo + 4 * q:mo + 4 * q + 4], "little")
+                dst[o + 2 * q:o + 2 * q + 2] = rne_bf16(u).to_bytes(2, "little")
+    bad = set()
+    for i, c in enumerate(ids):
+        k, j = cmap[c]
+        o, ln = _chunk_bytes(table, C, k, j, dst, "dst_offset")
+        if frsum(bytes(dst[o:o + ln])) != tuple(sums[i]):
+            bad.add(i)
+    return bad

@@ -1,0 +1,152 @@
+"""Delta repair in the CPU oracle (CPU only): re-sending only the chunks in
+which a replica diverged.
+
+Pins: listing every chunk reproduces the full restore's payload and sums
+(closed form); a replica repaired from the chunks that the exact compare
+flags equals the donor byte for byte; the wire carries exactly the listed
+non-derived chunks; a flipped bit on the wire is flagged at its list
+position; the C oracle equals the pure-Python oracle on random tables and
+lists."""
+import numpy as np
+
+from oracle import cpu, mini
+from paper_2509_03047_amd import workloads as W
+
+
+def _all_ids(t, C):
+    return np.arange(cpu.n_chunks(t, C), dtype=np.uint32)
+
+
+def test_listing_every_chunk_is_the_full_restore():
+    rng = np.random.default_rng(61)
+    for _ in range(60):
+        t, sb, db = W.random_tiny_table(rng)
+        C = int(rng.choice([16, 32, 64, 256]))
+        src = W.random_tiny_state(t, sb, rng)
+        fp, fs = cpu.pack(t, C, src)
+        dp, ds = cpu.pack_chunks(t, C, src, _all_ids(t, C))
+        assert dp.tobytes() == fp.tobytes() and np.array_equal(ds, fs)
+    w = W.make_workload(0)
+    src = W.fill_state(w)
+    fp, fs = cpu.pack(w.table, w.chunk_bytes, src)
+    dp, ds = cpu.pack_chunks(w.table, w.chunk_bytes, src, _all_ids(w.table, w.chunk_bytes))
+    assert np.array_equal(dp, fp) and np.array_equal(ds, fs)
+
+
+def _repair(t, C, donor, receiver):
+    bm, nd = cpu.verify(t, C, donor, receiver)
+    ids = np.array(cpu.bitmap_to_set(bm, cpu.n_chunks(t, C)), dtype=np.uint32)
+    pay, sums = cpu.pack_chunks(t, C, donor, ids)
+    fixed = receiver.copy()
+    rb, nbad = cpu.unpack_chunks(t, C, pay, sums, ids, fixed)
+    return ids, pay, fixed, nbad
+
+
+def test_repair_from_the_flagged_chunks_restores_the_donor():
+    w = W.make_workload(0)
+    donor = W.fill_state(w)
+    t, C = w.table, w.chunk_bytes
+    sizes = np.where(t["dtype"] == 1, 4, 2) * t["numel"].astype(np.int64)
+    for k in (1, 7, 64, 500):
+        recv = donor.copy()
+        W.apply_flips(recv, W.flip_positions(donor.size * 8, k, 4000 + k))
+        ids, pay, fixed, nbad = _repair(t, C, donor, recv)
+        assert nbad == 0 and np.array_equal(fixed, donor)
+        # the wire holds exactly the listed chunks of sent (non-derived) entries
+        _, base, _, _ = cpu.plan(t, C)
+        expect = 0
+        for c in ids:
+            e = int(np.searchsorted(base, int(c), side="right") - 1)
+            if int(t[e]["derive_from"]) < 0:
+                j = int(c) - int(base[e])
+                expect += -(-min(C, int(sizes[e]) - j * C) // 16) * 16
+        assert pay.size == expect
+
+
+def test_param_only_divergence_sends_nothing_and_rederives():
+    w = W.make_workload(0)
+    donor = W.fill_state(w)
+    t, C = w.table, w.chunk_bytes
+    recv = donor.copy()
+    p0 = int(t[0]["src_offset"])  # entry 0 is the embedding's bf16 param
+    recv[p0 + 5] ^= 0x10
+    recv[p0 + 70000] ^= 0x01
+    ids, pay, fixed, nbad = _repair(t, C, donor, recv)
+    assert list(ids) == [0, 1] and pay.size == 0
+    assert nbad == 0 and np.array_equal(fixed, donor)
+
+
+def test_master_divergence_repairs_master_and_param():
+    w = W.make_workload(0)
+    donor = W.fill_state(w)
+    t, C = w.table, w.chunk_bytes
+    recv = donor.copy()
+    m0, p0 = int(t[1]["src_offset"]), int(t[0]["src_offset"])
+    recv[m0 + 3] ^= 0x40  # exponent bit of master element 0
+    recv[p0 + 1] ^= 0x40  # and its bf16 image
+    ids, pay, fixed, nbad = _repair(t, C, donor, recv)
+    assert nbad == 0 and np.array_equal(fixed, donor)
+
+
+def test_wire_flip_is_flagged_at_its_list_position():
+    w = W.make_workload(0)
+    donor = W.fill_state(w)
+    t, C = w.table, w.chunk_bytes
+    ids = np.array([2, 3, 10, 11, 40, 400, 803], dtype=np.uint32)
+    pay, sums = cpu.pack_chunks(t, C, donor, ids)
+    off, pb = cpu.delta_layout(t, C, ids)
+    _, base, _, _ = cpu.plan(t, C)
+    sizes = np.where(t["dtype"] == 1, 4, 2) * t["numel"].astype(np.int64)
+    lens = []
+    for c in ids:
+        e = int(np.searchsorted(base, int(c), side="right") - 1)
+        lens.append(min(C, int(sizes[e]) - (int(c) - int(base[e])) * C))
+    sent = [i for i in range(ids.size) if off[i] != cpu.NO_PAYLOAD]
+    assert sent  # the list mixes derived (not sent) and sent chunks
+    assert len(sent) < ids.size
+    rng = np.random.default_rng(62)
+    for _ in range(40):
+        b = int(rng.integers(0, pb * 8))
+        p = pay.copy()
+        p[b // 8] ^= np.uint8(1 << (b % 8))
+        recv = donor.copy()
+        bm, nbad = cpu.unpack_chunks(t, C, p, sums, ids, recv)
+        exp = {i for i in sent if off[i] <= b // 8 < off[i] + lens[i]}  # padding bytes are not data
+        assert set(cpu.bitmap_to_set(bm, ids.size)) == exp and nbad == len(exp)
+
+
+def test_bad_lists_are_rejected():
+    t, sb, db = W.random_tiny_table(np.random.default_rng(63), max_entries=3, max_numel=200)
+    n = cpu.n_chunks(t, 16)
+    for bad in ([1, 1], [2, 1], [n]):
+        try:
+            cpu.delta_layout(t, 16, np.array(bad, np.uint32))
+            raise AssertionError("accepted", bad)
+        except ValueError:
+            pass
+
+
+def test_c_oracle_equals_python_oracle_on_delta():
+    rng = np.random.default_rng(64)
+    for _ in range(400):
+        t, sb, db = W.random_tiny_table(rng, max_numel=150)
+        C = int(rng.choice([16, 32, 64, 256]))
+        nc = cpu.n_chunks(t, C)
+        if nc == 0:
+            continue
+        ids = np.sort(rng.choice(nc, size=int(rng.integers(1, nc + 1)), replace=False)).astype(np.uint32)
+        src = W.random_tiny_state(t, sb, rng)
+        pay, sums = cpu.pack_chunks(t, C, src, ids)
+        mp, ms = mini.pack_chunks(t, C, src.tobytes(), [int(i) for i in ids])
+        assert pay.tobytes() == mp
+        assert [tuple(int(x) for x in sums[2 * i:2 * i + 2]) for i in range(ids.size)] == ms
+        recv = rng.integers(0, 256, size=db, dtype=np.uint8)
+        mrecv = bytearray(recv.tobytes())
+        p = pay.copy()
+        if p.size and rng.random() < 0.5:
+            b = int(rng.integers(0, p.size * 8))
+            p[b // 8] ^= np.uint8(1 << (b % 8))
+        bm, nbad = cpu.unpack_chunks(t, C, p, sums, ids, recv)
+        mbad = mini.unpack_chunks(t, C, p.tobytes(), ms, [int(i) for i in ids], mrecv)
+        assert recv.tobytes() == bytes(mrecv)
+        assert set(cpu.bitmap_to_set(bm, ids.size)) == mbad and nbad == len(mbad)
