@@ -56,8 +56,11 @@
  *   `stream` (a hipStream_t; NULL is the null stream) and return without
  *   waiting; their outputs are valid once the stream reaches that point.
  *   On any error nothing is enqueued and no output is touched.  A checksum or
- *   compare mismatch is data (a set bit and a count), not an error.  Calls on
- *   one plan from several host threads at once are not supported.
+ *   compare mismatch is data (a set bit and a count), not an error.
+ *   Operations on one plan share the plan's device scratch: they must not run
+ *   concurrently (issue them on one stream, or order the streams), and one
+ *   plan must not be used from several host threads at once; use one plan per
+ *   concurrent stream.
  */
 #ifndef FLASHRESTORE_H
 #define FLASHRESTORE_H
@@ -200,6 +203,44 @@ int fr_verify_replicas(const fr_plan* plan, const void* base_a, const void* base
 /* sums[c] <- FRSUM-128 of chunk c of the arena at base (src offsets); equal
  * to the sums fr_pack_state produces for the same bytes. */
 int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums, void* stream);
+
+/* --------------------------------------------------------- delta repair */
+
+/* Re-sending only the chunks in which a replica diverged, for example the set
+ * fr_verify_replicas reports, instead of the whole state (the paper restores
+ * from a data-parallel replica, Section III-E; a replica that differs from
+ * its group in a few chunks needs only those).
+ *   chunk_ids  host array of n_ids global chunk ids, strictly increasing,
+ *              each < n_chunks (FR_E_INVAL otherwise); n_ids may be 0
+ * Delta payload: the bytes of every listed chunk of a non-derived entry, in
+ * list order, each starting at a 16-aligned offset, every gap byte 0; listed
+ * chunks of derived (bf16) entries send nothing.  With every chunk listed the
+ * delta payload and sums equal fr_pack_state's.
+ * All three take the list on the host; pack and unpack copy a small unit
+ * table to the device on `stream` before their kernels. */
+
+/* Bytes of the delta payload for a list.  Host only. */
+int fr_delta_layout(const fr_plan* plan, const uint32_t* chunk_ids, uint64_t n_ids,
+                    uint64_t* payload_bytes);
+
+/* Donor side: payload <- the listed chunks as defined above; sums[i] <-
+ * FRSUM-128 of chunk chunk_ids[i] read at src_base (derived chunks included).
+ *   payload   device, 16-byte aligned, payload_cap >= fr_delta_layout bytes
+ *   sums      device, 16-byte aligned, n_ids entries */
+int fr_pack_chunks(const fr_plan* plan, const void* src_base, const uint32_t* chunk_ids,
+                   uint64_t n_ids, void* payload, uint64_t payload_cap, fr_chunk_sum* sums,
+                   void* stream);
+
+/* Receiver side: write every sent chunk to dst_base; then recompute every
+ * listed derived chunk as RNE of the receiver's master bytes (which by then
+ * hold every sent master chunk); then set bit i of bad_bitmap iff FRSUM-128
+ * of chunk chunk_ids[i] as written differs from sums[i]; *n_bad = number of
+ * set bits.  Bytes outside the listed chunks are not written.
+ *   bad_bitmap  device, 4-byte aligned, ceil(n_ids / 32) words (NULL if n_ids == 0)
+ *   n_bad       device, 8-byte aligned, one uint64 */
+int fr_unpack_chunks(const fr_plan* plan, const void* payload, const fr_chunk_sum* sums,
+                     const uint32_t* chunk_ids, uint64_t n_ids, void* dst_base,
+                     uint32_t* bad_bitmap, uint64_t* n_bad, void* stream);
 
 /* ---------------------------------------------------------------- misc */
 

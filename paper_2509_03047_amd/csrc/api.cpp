@@ -3,7 +3,10 @@
 // touched unless every check passes.
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cstdint>
+#include <new>
+#include <vector>
 
 #include "fr_internal.h"
 
@@ -184,6 +187,198 @@ extern "C" int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk
   return launch_result(
       launch_checksum(plan->d_chunks, uint32_t(L.n_chunks), L.C, base, sums, plan->scratch,
                       plan->cfg, stream));
+}
+
+// ------------------------------------------------------------ delta repair
+
+namespace {
+
+int check_list(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids) {
+  if (n_ids == 0) return FR_OK;
+  if (!ids || n_ids > plan->layout.n_chunks) return FR_E_INVAL;
+  for (uint64_t i = 0; i < n_ids; i++) {
+    if (ids[i] >= plan->layout.n_chunks) return FR_E_INVAL;
+    if (i && ids[i] <= ids[i - 1]) return FR_E_INVAL;
+  }
+  return FR_OK;
+}
+
+struct Where {
+  uint32_t entry;
+  uint64_t j;    // chunk index within the entry
+  uint64_t len;  // chunk bytes
+};
+
+Where locate(const fr_plan* plan, uint32_t c) {
+  const std::vector<uint64_t>& base = plan->layout.chunk_base;
+  // the entry k with base[k] <= c < base[k + 1]
+  const auto it = std::upper_bound(base.begin(), base.end() - 1, uint64_t(c));
+  const uint32_t k = uint32_t(it - base.begin()) - 1;
+  const fr_tensor_desc& d = plan->table[k];
+  const uint64_t nb = d.numel * (d.dtype == FR_F32 ? 4 : 2);
+  const uint64_t j = c - base[k];
+  const uint64_t C = plan->layout.C;
+  return Where{k, j, std::min<uint64_t>(C, nb - j * C)};
+}
+
+uint64_t delta_bytes(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids) {
+  uint64_t pay = 0;
+  for (uint64_t i = 0; i < n_ids; i++) {
+    const Where w = locate(plan, ids[i]);
+    if (plan->table[w.entry].derive_from < 0) pay = (pay + w.len + 15) & ~uint64_t(15);
+  }
+  return pay;
+}
+
+// Device room for the unit records of a delta call (allocated once per plan,
+// sized for a list of every chunk).
+int ensure_delta_buffer(fr_plan* plan) {
+  const uint64_t need = std::max<uint64_t>(plan->layout.n_chunks, 1) * sizeof(DerivedUnit);
+  if (plan->d_delta && plan->delta_cap >= need) return FR_OK;
+  void* p = nullptr;
+  hipError_t e = hipMalloc(&p, need);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e == hipErrorOutOfMemory ? FR_E_NOMEM : device_error(e);
+  }
+  if (plan->d_delta) (void)hipFree(plan->d_delta);
+  plan->d_delta = p;
+  plan->delta_cap = need;
+  return FR_OK;
+}
+
+int upload_records(fr_plan* plan, size_t bytes, void* stream) {
+  if (bytes == 0) return FR_OK;
+  hipError_t e = hipMemcpyAsync(plan->d_delta, plan->delta_host.data(), bytes,
+                                hipMemcpyHostToDevice, hipStream_t(stream));
+  return e == hipSuccess ? FR_OK : device_error(e);
+}
+
+}  // namespace
+
+extern "C" int fr_delta_layout(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids,
+                               uint64_t* payload_bytes) {
+  if (!plan || !payload_bytes) return FR_E_INVAL;
+  FR_TRY(check_list(plan, ids, n_ids));
+  *payload_bytes = delta_bytes(plan, ids, n_ids);
+  return FR_OK;
+}
+
+extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const uint32_t* ids,
+                              uint64_t n_ids, void* payload, uint64_t payload_cap,
+                              fr_chunk_sum* sums, void* stream) {
+  if (!cplan) return FR_E_INVAL;
+  fr_plan* plan = const_cast<fr_plan*>(cplan);  // the plan's delta staging is mutable state
+  FR_TRY(check_list(plan, ids, n_ids));
+  const uint64_t pb = delta_bytes(plan, ids, n_ids);
+  if (payload_cap < pb) return FR_E_RANGE;
+  FR_TRY(check_device_and_stream(plan, stream));
+  FR_TRY(check_buffer(plan, src_base, plan->src_arena_bytes, 16));
+  FR_TRY(check_buffer(plan, payload, pb, 16));
+  FR_TRY(check_buffer(plan, sums, n_ids * sizeof(fr_chunk_sum), 16));
+  const Region outs[] = {{payload, pb}, {sums, n_ids * sizeof(fr_chunk_sum)}};
+  const Region ins[] = {{src_base, plan->src_arena_bytes}};
+  FR_TRY(check_disjoint(outs, 2, ins, 1));
+  if (n_ids == 0) return FR_OK;
+  FR_TRY(ensure_delta_buffer(plan));
+  const uint64_t C = plan->layout.C;
+  try {
+    plan->delta_host.resize(n_ids * sizeof(ChunkRec));
+  } catch (const std::bad_alloc&) {
+    return FR_E_NOMEM;
+  }
+  ChunkRec* recs = reinterpret_cast<ChunkRec*>(plan->delta_host.data());
+  uint64_t pay = 0;
+  for (uint64_t i = 0; i < n_ids; i++) {
+    const Where w = locate(plan, ids[i]);
+    const fr_tensor_desc& d = plan->table[w.entry];
+    ChunkRec& r = recs[i];
+    r.src_off = d.src_offset + w.j * C;
+    r.dst_off = d.dst_offset + w.j * C;
+    r.len = uint32_t(w.len);
+    r.master = kNoMaster;
+    if (d.derive_from >= 0) {
+      r.pay_off = kNoPayload;
+    } else {
+      r.pay_off = pay;
+      pay = (pay + w.len + 15) & ~uint64_t(15);
+    }
+  }
+  FR_TRY(upload_records(plan, n_ids * sizeof(ChunkRec), stream));
+  return launch_result(launch_pack(static_cast<const ChunkRec*>(plan->d_delta), uint32_t(n_ids), C,
+                                   src_base, payload, sums, plan->scratch, plan->cfg, stream));
+}
+
+extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
+                                const fr_chunk_sum* sums, const uint32_t* ids, uint64_t n_ids,
+                                void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad,
+                                void* stream) {
+  if (!cplan || !n_bad) return FR_E_INVAL;
+  fr_plan* plan = const_cast<fr_plan*>(cplan);
+  FR_TRY(check_list(plan, ids, n_ids));
+  const uint64_t pb = delta_bytes(plan, ids, n_ids);
+  const uint64_t words = (n_ids + 31) / 32;
+  FR_TRY(check_device_and_stream(plan, stream));
+  FR_TRY(check_buffer(plan, payload, pb, 16));
+  FR_TRY(check_buffer(plan, sums, n_ids * sizeof(fr_chunk_sum), 16));
+  FR_TRY(check_buffer(plan, dst_base, plan->dst_arena_bytes, 16));
+  FR_TRY(check_buffer(plan, bad_bitmap, words * 4, 4));
+  FR_TRY(check_buffer(plan, n_bad, 8, 8));
+  const Region outs[] = {{dst_base, plan->dst_arena_bytes}, {bad_bitmap, words * 4}, {n_bad, 8}};
+  const Region ins[] = {{payload, pb}, {sums, n_ids * sizeof(fr_chunk_sum)}};
+  FR_TRY(check_disjoint(outs, 3, ins, 2));
+  if (n_ids) FR_TRY(ensure_delta_buffer(plan));
+  const uint64_t C = plan->layout.C;
+  uint32_t n_plain = 0, n_derived = 0;
+  for (uint64_t i = 0; i < n_ids; i++)
+    (plan->table[locate(plan, ids[i]).entry].derive_from < 0 ? n_plain : n_derived)++;
+  try {
+    plan->delta_host.resize(n_plain * sizeof(PlainUnit) + n_derived * sizeof(DerivedUnit));
+  } catch (const std::bad_alloc&) {
+    return FR_E_NOMEM;
+  }
+  PlainUnit* pu = reinterpret_cast<PlainUnit*>(plan->delta_host.data());
+  DerivedUnit* du = reinterpret_cast<DerivedUnit*>(plan->delta_host.data() + n_plain * sizeof(PlainUnit));
+  uint64_t pay = 0;
+  uint32_t ip = 0, id = 0;
+  for (uint64_t i = 0; i < n_ids; i++) {
+    const Where w = locate(plan, ids[i]);
+    const fr_tensor_desc& d = plan->table[w.entry];
+    if (d.derive_from < 0) {
+      PlainUnit& u = pu[ip++];
+      u = PlainUnit{};
+      u.pay_off = pay;
+      u.dst_off = d.dst_offset + w.j * C;
+      u.len = uint32_t(w.len);
+      u.c = uint32_t(i);
+      pay = (pay + w.len + 15) & ~uint64_t(15);
+    } else {
+      const fr_tensor_desc& m = plan->table[d.derive_from];
+      DerivedUnit& u = du[id++];
+      u = DerivedUnit{};
+      u.m_pay_off = m.dst_offset + 2 * w.j * C;  // the receiver's master bytes of this chunk
+      u.m_dst_off = u.m_pay_off;
+      u.p_dst_off = d.dst_offset + w.j * C;
+      u.len = uint32_t(w.len);
+      u.c = uint32_t(i);
+    }
+  }
+  FR_TRY(upload_records(plan, plan->delta_host.size(), stream));
+  UnpackDeltaArgs a{};
+  a.plain = static_cast<const PlainUnit*>(plan->d_delta);
+  a.n_plain = n_plain;
+  a.derived = reinterpret_cast<const DerivedUnit*>(static_cast<const uint8_t*>(plan->d_delta) +
+                                                   n_plain * sizeof(PlainUnit));
+  a.n_derived = n_derived;
+  a.n_ids = uint32_t(n_ids);
+  a.C = C;
+  a.payload = payload;
+  a.sums = sums;
+  a.dst = dst_base;
+  a.bitmap = bad_bitmap;
+  a.n_bad = n_bad;
+  a.scratch = plan->scratch;
+  return launch_result(launch_unpack_delta(a, plan->cfg, stream));
 }
 
 extern "C" const char* fr_strerror(int status) {

@@ -94,6 +94,23 @@ struct UnpackArgs {
   Scratch scratch;
 };
 
+// A delta restore (a list of chunks) on the receiver: sent chunks first,
+// then derived chunks recomputed from the receiver's masters.
+struct UnpackDeltaArgs {
+  const PlainUnit* plain;      // sent chunks; c = list position
+  uint32_t n_plain;
+  const DerivedUnit* derived;  // derived chunks; m_pay_off = master's receiver offset, c = list position
+  uint32_t n_derived;
+  uint32_t n_ids;
+  uint64_t C;
+  const void* payload;
+  const fr_chunk_sum* sums;    // n_ids, list order
+  void* dst;
+  uint32_t* bitmap;
+  uint64_t* n_bad;
+  Scratch scratch;
+};
+
 // Bytes of one slice for a tile, and the accumulators a chunk of C bytes
 // needs with that tile (kernels.hip).
 uint32_t tile_bytes(int tile);
@@ -107,6 +124,7 @@ int launch_pack(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const voi
 int launch_checksum(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* base,
                     fr_chunk_sum* sums, const Scratch& scr, const LaunchCfg& cfg, void* stream);
 int launch_unpack(const UnpackArgs& args, const LaunchCfg& cfg, void* stream);
+int launch_unpack_delta(const UnpackDeltaArgs& args, const LaunchCfg& cfg, void* stream);
 int launch_verify(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* a,
                   const void* b, uint32_t* bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
                   fr_chunk_sum* sums_b, const Scratch& scr, const LaunchCfg& cfg, void* stream);
@@ -124,6 +142,9 @@ struct fr_plan {
   fr::PlainUnit* d_plain = nullptr;      // unpack units: plain chunks
   uint32_t n_plain = 0;
   void* d_scratch = nullptr;         // one allocation holding `scratch`
+  void* d_delta = nullptr;           // delta unit records, allocated on first use
+  uint64_t delta_cap = 0;            // bytes of d_delta
+  std::vector<uint8_t> delta_host;   // host staging of the unit records
   fr::Scratch scratch{};
   fr::LaunchCfg cfg{};
 };

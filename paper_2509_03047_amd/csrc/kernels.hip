@@ -228,6 +228,102 @@ __global__ __launch_bounds__(B) void k_pack(const ChunkRec* __restrict__ chunks,
 //   plain:   a chunk of an entry that is neither derived nor a master with a
 //            derived image; SPC slices per unit.
 // Sums of the bytes written go to the accumulators `acc_out` (zeroed).
+// One slice of a derived group: read master bytes from `msrc` (the payload,
+// or with kFromPayload = false the receiver's own masters), write the bf16
+// images to the parameter chunk, and with kFromPayload also write the master
+// bytes to the receiver.  acc[0..1] get the master words' sums (relative to
+// master chunk m0 + part), acc[2..3] the parameter words'.  Returns false
+// for a slice past the group's end.
+template <int B, int U, bool kFromPayload>
+__device__ __forceinline__ bool derived_slice(const DerivedUnit& r, uint32_t j, const Walk& wk,
+                                              uint32_t cvec, const uint8_t* msrc, uint8_t* dst,
+                                              u64 (&acc)[4], uint32_t& part) {
+  const uint32_t mvec = (2 * r.len) >> 4;  // whole master vectors of the group
+  const uint32_t mtail = (2 * r.len) & 15;  // 0, 4, 8 or 12: whole fp32 values
+  const uint32_t v0 = j * wk.sl_vec;
+  if (v0 > mvec || (v0 == mvec && mtail == 0)) return false;
+  part = j >> wk.spc_shift;                 // master chunk of this slice: m0 + part
+  const uint32_t wbase = part * cvec * 4;   // its first word in the group
+  const u32x4* s = reinterpret_cast<const u32x4*>(msrc + r.m_pay_off);
+  u32x4* md = reinterpret_cast<u32x4*>(dst + r.m_dst_off);
+  u32x2* pd = reinterpret_cast<u32x2*>(dst + r.p_dst_off);
+  u32x4 x[U];
+#pragma unroll
+  for (int q = 0; q < U; q++) {
+    const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+    if (l < wk.sl_vec && v < mvec) x[q] = ld_nt(s + v);
+  }
+#pragma unroll
+  for (int q = 0; q < U; q++) {
+    const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+    if (l < wk.sl_vec && v < mvec) {
+      if (kFromPayload) {
+        st_nt(x[q], md + v);
+        acc4(x[q], 4 * v - wbase, acc[0], acc[1]);
+      }
+      const u32x2 p = rne4(x[q]);
+      st_nt2(p, pd + v);
+      acc2(p, 2 * v, acc[2], acc[3]);
+    }
+  }
+  if (mtail && mvec >= v0 && mvec - v0 < wk.sl_vec && threadIdx.x == (mvec - v0) % B) {
+    // A payload segment is padded to 16 bytes, so its whole last vector is
+    // readable; the receiver's master is read only up to its last value.
+    const u32x4 t = kFromPayload ? mask_tail(s[mvec], mtail)
+                                 : load_tail(reinterpret_cast<const uint8_t*>(s + mvec), mtail);
+    const uint32_t nf = mtail >> 2;
+    if (kFromPayload) {
+      uint32_t* mw = reinterpret_cast<uint32_t*>(md + mvec);
+      mw[0] = t.x;
+      if (nf > 1) mw[1] = t.y;
+      if (nf > 2) mw[2] = t.z;
+      acc4(t, 4 * mvec - wbase, acc[0], acc[1]);
+    }
+    uint16_t* ph = reinterpret_cast<uint16_t*>(pd + mvec);
+    const uint32_t h0 = rne_bf16(t.x), h1 = rne_bf16(t.y), h2 = rne_bf16(t.z);
+    ph[0] = uint16_t(h0);
+    if (nf > 1) ph[1] = uint16_t(h1);
+    if (nf > 2) ph[2] = uint16_t(h2);
+    const u32x2 p{h0 | (nf > 1 ? h1 << 16 : 0u), nf > 2 ? h2 : 0u};
+    acc2(p, 2 * mvec, acc[2], acc[3]);
+  }
+  return true;
+}
+
+// One slice of a plain chunk: copy, and sum the bytes as written.
+template <int B, int U>
+__device__ __forceinline__ bool plain_slice(const PlainUnit& r, uint32_t j, const Walk& wk,
+                                            const uint8_t* payload, uint8_t* dst,
+                                            u64 (&acc)[2]) {
+  const uint32_t nvec = r.len >> 4, tail = r.len & 15;
+  const uint32_t v0 = j * wk.sl_vec;
+  if (v0 > nvec || (v0 == nvec && tail == 0)) return false;
+  const u32x4* s = reinterpret_cast<const u32x4*>(payload + r.pay_off);
+  u32x4* d = reinterpret_cast<u32x4*>(dst + r.dst_off);
+  u32x4 x[U];
+#pragma unroll
+  for (int q = 0; q < U; q++) {
+    const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+    if (l < wk.sl_vec && v < nvec) x[q] = ld_nt(s + v);
+  }
+#pragma unroll
+  for (int q = 0; q < U; q++) {
+    const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+    if (l < wk.sl_vec && v < nvec) {
+      st_nt(x[q], d + v);
+      acc4(x[q], 4 * v, acc[0], acc[1]);
+    }
+  }
+  if (tail && nvec >= v0 && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
+    // The payload segment is padded to 16 bytes, so the whole vector is
+    // readable; only the entry's bytes are written and summed.
+    const u32x4 t = mask_tail(s[nvec], tail);
+    store_tail(reinterpret_cast<uint8_t*>(d + nvec), t, tail);
+    acc4(t, 4 * nvec, acc[0], acc[1]);
+  }
+  return true;
+}
+
 template <int B, int U>
 __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ derived,
                                               const PlainUnit* __restrict__ plain, Walk wk,
@@ -240,52 +336,12 @@ __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ de
   int parity = 0;
   const uint32_t spc_mask = (1u << wk.spc_shift) - 1;
   for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
-    u64 acc[4] = {0, 0, 0, 0};
     if (g < n_derived_slices) {
       const DerivedUnit r = derived[g >> (wk.spc_shift + 1)];
       const uint32_t j = uint32_t(g) & (2 * spc_mask + 1);
-      const uint32_t mvec = (2 * r.len) >> 4;  // whole master vectors of the group
-      const uint32_t mtail = (2 * r.len) & 15;  // 0, 4, 8 or 12: whole fp32 values
-      const uint32_t v0 = j * wk.sl_vec;
-      if (v0 > mvec || (v0 == mvec && mtail == 0)) continue;
-      const uint32_t part = j >> wk.spc_shift;  // master chunk of this slice: m0 + part
-      const uint32_t wbase = part * cvec * 4;   // its first word in the group
-      const u32x4* s = reinterpret_cast<const u32x4*>(payload + r.m_pay_off);
-      u32x4* md = reinterpret_cast<u32x4*>(dst + r.m_dst_off);
-      u32x2* pd = reinterpret_cast<u32x2*>(dst + r.p_dst_off);
-      u32x4 x[U];
-#pragma unroll
-      for (int q = 0; q < U; q++) {
-        const uint32_t l = q * B + threadIdx.x, v = v0 + l;
-        if (l < wk.sl_vec && v < mvec) x[q] = ld_nt(s + v);
-      }
-#pragma unroll
-      for (int q = 0; q < U; q++) {
-        const uint32_t l = q * B + threadIdx.x, v = v0 + l;
-        if (l < wk.sl_vec && v < mvec) {
-          st_nt(x[q], md + v);
-          acc4(x[q], 4 * v - wbase, acc[0], acc[1]);
-          const u32x2 p = rne4(x[q]);
-          st_nt2(p, pd + v);
-          acc2(p, 2 * v, acc[2], acc[3]);
-        }
-      }
-      if (mtail && mvec >= v0 && mvec - v0 < wk.sl_vec && threadIdx.x == (mvec - v0) % B) {
-        const u32x4 t = mask_tail(s[mvec], mtail);  // padded segment: readable
-        uint32_t* mw = reinterpret_cast<uint32_t*>(md + mvec);
-        const uint32_t nf = mtail >> 2;
-        mw[0] = t.x;
-        if (nf > 1) mw[1] = t.y;
-        if (nf > 2) mw[2] = t.z;
-        acc4(t, 4 * mvec - wbase, acc[0], acc[1]);
-        uint16_t* ph = reinterpret_cast<uint16_t*>(pd + mvec);
-        const uint32_t h0 = rne_bf16(t.x), h1 = rne_bf16(t.y), h2 = rne_bf16(t.z);
-        ph[0] = uint16_t(h0);
-        if (nf > 1) ph[1] = uint16_t(h1);
-        if (nf > 2) ph[2] = uint16_t(h2);
-        const u32x2 p{h0 | (nf > 1 ? h1 << 16 : 0u), nf > 2 ? h2 : 0u};
-        acc2(p, 2 * mvec, acc[2], acc[3]);
-      }
+      u64 acc[4] = {0, 0, 0, 0};
+      uint32_t part = 0;
+      if (!derived_slice<B, U, true>(r, j, wk, cvec, payload, dst, acc, part)) continue;
       block_sum<B, 4>(acc, lds, parity);
       if (threadIdx.x == 0) {
         const uint32_t jj = j - (part << wk.spc_shift);  // slice within its master chunk
@@ -300,37 +356,34 @@ __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ de
       const u64 h = g - n_derived_slices;
       const PlainUnit r = plain[h >> wk.spc_shift];
       const uint32_t j = uint32_t(h) & spc_mask;
-      const uint32_t nvec = r.len >> 4, tail = r.len & 15;
-      const uint32_t v0 = j * wk.sl_vec;
-      if (v0 > nvec || (v0 == nvec && tail == 0)) continue;
-      const u32x4* s = reinterpret_cast<const u32x4*>(payload + r.pay_off);
-      u32x4* d = reinterpret_cast<u32x4*>(dst + r.dst_off);
-      u32x4 x[U];
-#pragma unroll
-      for (int q = 0; q < U; q++) {
-        const uint32_t l = q * B + threadIdx.x, v = v0 + l;
-        if (l < wk.sl_vec && v < nvec) x[q] = ld_nt(s + v);
-      }
-#pragma unroll
-      for (int q = 0; q < U; q++) {
-        const uint32_t l = q * B + threadIdx.x, v = v0 + l;
-        if (l < wk.sl_vec && v < nvec) {
-          st_nt(x[q], d + v);
-          acc4(x[q], 4 * v, acc[0], acc[1]);
-        }
-      }
-      if (tail && nvec >= v0 && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
-        // The payload segment is padded to 16 bytes, so the whole vector is
-        // readable; only the entry's bytes are written and summed.
-        const u32x4 t = mask_tail(s[nvec], tail);
-        store_tail(reinterpret_cast<uint8_t*>(d + nvec), t, tail);
-        acc4(t, 4 * nvec, acc[0], acc[1]);
-      }
-      u64 acc2v[2] = {acc[0], acc[1]};
-      block_sum<B, 2>(acc2v, lds2, parity);
+      u64 acc[2] = {0, 0};
+      if (!plain_slice<B, U>(r, j, wk, payload, dst, acc)) continue;
+      block_sum<B, 2>(acc, lds2, parity);
       if (threadIdx.x == 0)
-        add_sum(acc_out + ((u64(r.c) << wk.g_shift) + (j >> kAccSlicesShift)), acc2v[0], acc2v[1]);
+        add_sum(acc_out + ((u64(r.c) << wk.g_shift) + (j >> kAccSlicesShift)), acc[0], acc[1]);
     }
+  }
+}
+
+// Delta restore, second phase: recompute listed bf16 parameter chunks from
+// the receiver's own master bytes (m_pay_off holds the master's receiver
+// offset); parameter sums go to the list position r.c.
+template <int B, int U>
+__global__ __launch_bounds__(B) void k_rederive(const DerivedUnit* __restrict__ derived, Walk wk,
+                                                uint32_t cvec, uint8_t* dst,
+                                                fr_chunk_sum* __restrict__ acc_out) {
+  __shared__ u64 lds[2][B / 64][4];
+  int parity = 0;
+  const uint32_t gmask = (2u << wk.spc_shift) - 1;
+  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
+    const DerivedUnit r = derived[g >> (wk.spc_shift + 1)];
+    const uint32_t j = uint32_t(g) & gmask;
+    u64 acc[4] = {0, 0, 0, 0};
+    uint32_t part = 0;
+    if (!derived_slice<B, U, false>(r, j, wk, cvec, dst, dst, acc, part)) continue;
+    block_sum<B, 4>(acc, lds, parity);
+    if (threadIdx.x == 0)
+      add_sum(acc_out + ((u64(r.c) << wk.g_shift) + (j >> (kAccSlicesShift + 1))), acc[2], acc[3]);
   }
 }
 
@@ -609,6 +662,41 @@ int unpack_impl(const UnpackArgs& u, const LaunchCfg& cfg, hipStream_t st) {
 }
 
 template <int B, int U>
+int unpack_delta_impl(const UnpackDeltaArgs& u, const LaunchCfg& cfg, hipStream_t st) {
+  const Walk wd = walk_for(u.n_derived, u.C, B * U * 16, true);
+  const Walk wp = walk_for(u.n_plain, u.C, B * U * 16);
+  const u64 n_acc = u64(u.n_ids) << wp.g_shift;
+  Zeroes z;
+  z.add(u.scratch.acc, n_acc * sizeof(fr_chunk_sum));
+  z.add(u.n_bad, 8);
+  int e = z.launch(st);
+  if (e || u.n_ids == 0) return e;
+  const uint32_t cvec = uint32_t(u.C >> 4);
+  if (wp.n_slices) {  // sent chunks first: the masters the second phase reads
+    hipLaunchKernelGGL((k_unpack<B, U>), dim3(grid_for<B>(wp.n_slices, cfg)), dim3(B), 0, st,
+                       static_cast<const DerivedUnit*>(nullptr), u.plain, wp, u64(0), cvec,
+                       static_cast<const uint8_t*>(u.payload), static_cast<uint8_t*>(u.dst),
+                       u.scratch.acc);
+    e = int(hipGetLastError());
+    if (e) return e;
+  }
+  if (wd.n_slices) {
+    hipLaunchKernelGGL((k_rederive<B, U>), dim3(grid_for<B>(wd.n_slices, cfg)), dim3(B), 0, st,
+                       u.derived, wd, cvec, static_cast<uint8_t*>(u.dst), u.scratch.acc);
+    e = int(hipGetLastError());
+    if (e) return e;
+  }
+  FinalArgs f{};
+  f.acc = u.scratch.acc;
+  f.sent = u.sums;
+  f.bitmap = u.bitmap;
+  f.count = reinterpret_cast<u64*>(u.n_bad);
+  f.n_chunks = u.n_ids;
+  f.g_shift = wp.g_shift;
+  return launch_finalize(kCompare, f, st);
+}
+
+template <int B, int U>
 int verify_impl(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* a,
                 const void* b, uint32_t* bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
                 fr_chunk_sum* sums_b, const Scratch& scr, const LaunchCfg& cfg, hipStream_t st) {
@@ -700,6 +788,10 @@ int launch_checksum(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const
 
 int launch_unpack(const UnpackArgs& u, const LaunchCfg& cfg, void* stream) {
   FR_DISPATCH(cfg.tile_unpack, unpack_impl, u, cfg, hipStream_t(stream));
+}
+
+int launch_unpack_delta(const UnpackDeltaArgs& u, const LaunchCfg& cfg, void* stream) {
+  FR_DISPATCH(cfg.tile_unpack, unpack_delta_impl, u, cfg, hipStream_t(stream));
 }
 
 int launch_verify(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* a,

@@ -165,6 +165,7 @@ extern "C" int fr_plan_destroy(fr_plan* p) {
   if (p->d_derived) (void)hipFree(p->d_derived);
   if (p->d_plain) (void)hipFree(p->d_plain);
   if (p->d_scratch) (void)hipFree(p->d_scratch);
+  if (p->d_delta) (void)hipFree(p->d_delta);
   if (switched) (void)hipSetDevice(prev);
   delete p;
   return FR_OK;

@@ -84,6 +84,9 @@ def _load():
         "fr_unpack_state": [P, P, P, P, P, P, P],
         "fr_verify_replicas": [P, P, P, P, P, P, P, P],
         "fr_checksum_state": [P, P, P, P],
+        "fr_delta_layout": [P, P, u64, C.POINTER(u64)],
+        "fr_pack_chunks": [P, P, P, u64, P, u64, P, P],
+        "fr_unpack_chunks": [P, P, P, P, u64, P, P, P, P],
         "fr_strerror": [i32],
         "fr_last_hip_error": [],
         "fr_abi_version": [],
@@ -103,8 +106,8 @@ _lib = _load()
 EXPORTED = (
     "fr_plan_create", "fr_plan_get_info", "fr_plan_chunk_of", "fr_plan_entry_layout",
     "fr_plan_destroy", "fr_layout_query", "fr_pack_state", "fr_unpack_state",
-    "fr_verify_replicas", "fr_checksum_state", "fr_strerror", "fr_last_hip_error",
-    "fr_abi_version",
+    "fr_verify_replicas", "fr_checksum_state", "fr_delta_layout", "fr_pack_chunks",
+    "fr_unpack_chunks", "fr_strerror", "fr_last_hip_error", "fr_abi_version",
 )
 
 
@@ -246,6 +249,15 @@ class Plan:
     def checksum_state(self, base, sums, stream=None):
         return fr_checksum_state(self, base, sums, stream)
 
+    def delta_layout(self, chunk_ids) -> int:
+        return fr_delta_layout(self, chunk_ids)
+
+    def pack_chunks(self, src, chunk_ids, payload, sums, stream=None, payload_cap=None):
+        return fr_pack_chunks(self, src, chunk_ids, payload, payload_cap, sums, stream)
+
+    def unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream=None):
+        return fr_unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream)
+
 
 def _nbytes(x):
     if x is None or isinstance(x, int):
@@ -285,6 +297,35 @@ def fr_verify_replicas(plan: Plan, base_a, base_b, diff_bitmap, n_diff, sums_a=N
 def fr_checksum_state(plan: Plan, base, sums, stream=None) -> None:
     _check(_lib.fr_checksum_state(plan.handle, _ptr(base), _ptr(sums), _stream(stream)),
            "fr_checksum_state")
+
+
+def _ids(chunk_ids) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(chunk_ids, dtype=np.uint32).reshape(-1))
+
+
+def fr_delta_layout(plan: Plan, chunk_ids) -> int:
+    ids = _ids(chunk_ids)
+    out = C.c_uint64()
+    _check(_lib.fr_delta_layout(plan.handle, ids.ctypes.data if ids.size else None, ids.size,
+                                C.byref(out)), "fr_delta_layout")
+    return out.value
+
+
+def fr_pack_chunks(plan: Plan, src, chunk_ids, payload, payload_cap, sums, stream=None) -> None:
+    ids = _ids(chunk_ids)
+    if payload_cap is None:
+        payload_cap = _nbytes(payload)
+        if payload_cap is None:
+            payload_cap = fr_delta_layout(plan, ids)
+    _check(_lib.fr_pack_chunks(plan.handle, _ptr(src), ids.ctypes.data if ids.size else None, ids.size,
+                               _ptr(payload), payload_cap, _ptr(sums), _stream(stream)), "fr_pack_chunks")
+
+
+def fr_unpack_chunks(plan: Plan, payload, sums, chunk_ids, dst, bad_bitmap, n_bad, stream=None) -> None:
+    ids = _ids(chunk_ids)
+    _check(_lib.fr_unpack_chunks(plan.handle, _ptr(payload), _ptr(sums), ids.ctypes.data if ids.size else None,
+                                 ids.size, _ptr(dst), _ptr(bad_bitmap), _ptr(n_bad), _stream(stream)),
+           "fr_unpack_chunks")
 
 
 def fr_strerror(status: int) -> str:

@@ -1,0 +1,150 @@
+"""GPU parity of delta repair (re-sending only the diverged chunks) against the
+CPU oracle, through the C ABI: payload, sums, receiver arena and result sets
+bit for bit on random tables and lists, every tile, and a full-size repair of
+the Llama-3-8B TP=8 rank share from the chunks the replica compare flags."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+from oracle import cpu  # noqa: E402
+from paper_2509_03047_amd import flashrestore as F  # noqa: E402
+from paper_2509_03047_amd import workloads as W  # noqa: E402
+
+from tests.gpu_util import log, sums_host, to_dev, to_host  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _one(t, C, src_np, recv_np, ids, rng, tag):
+    plan = F.Plan(t, C, max(src_np.size, 16), max(recv_np.size, 16))
+    src = to_dev(src_np) if src_np.size else torch.zeros(16, dtype=torch.uint8, device="cuda")
+    dst = to_dev(recv_np) if recv_np.size else torch.zeros(16, dtype=torch.uint8, device="cuda")
+    pb = plan.delta_layout(ids)
+    off, opb = cpu.delta_layout(t, C, ids)
+    assert pb == opb, tag
+    payload = torch.empty(max(pb, 16), dtype=torch.uint8, device="cuda")
+    sums = torch.empty(max(ids.size, 1), 2, dtype=torch.int64, device="cuda")
+    plan.pack_chunks(src, ids, payload, sums)
+    opay, osums = cpu.pack_chunks(t, C, src_np, ids)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(payload)[:pb], opay), f"payload {tag}"
+    assert np.array_equal(sums_host(sums, ids.size), osums), f"sums {tag}"
+    if pb and rng.random() < 0.4:  # corrupt the wire
+        b = int(rng.integers(0, pb * 8))
+        opay[b // 8] ^= np.uint8(1 << (b % 8))
+        payload[b // 8] ^= 1 << (b % 8)
+    bad = torch.empty(max((ids.size + 31) // 32, 1), dtype=torch.int32, device="cuda")
+    nbad = torch.empty(1, dtype=torch.int64, device="cuda")
+    plan.unpack_chunks(payload, sums, ids, dst, bad, nbad)
+    orecv = recv_np.copy()
+    obm, onbad = cpu.unpack_chunks(t, C, opay, osums, ids, orecv)
+    torch.cuda.synchronize()
+    if recv_np.size:
+        assert np.array_equal(to_host(dst)[: recv_np.size], orecv), f"dst {tag}"
+    assert set(F.bitmap_indices(bad, ids.size).tolist()) == set(cpu.bitmap_to_set(obm, ids.size)), tag
+    assert int(nbad.item()) == onbad
+
+
+def test_delta_bruteforce_tiny_tables():
+    rng = np.random.default_rng(71)
+    for it in range(400):
+        t, sb, db = W.random_tiny_table(rng)
+        C = int(rng.choice([16, 32, 64, 256]))
+        nc = cpu.n_chunks(t, C)
+        k = int(rng.integers(0, nc + 1))
+        ids = np.sort(rng.choice(nc, size=k, replace=False)).astype(np.uint32) if nc else np.zeros(0, np.uint32)
+        src = W.random_tiny_state(t, sb, rng)
+        recv = rng.integers(0, 256, size=db, dtype=np.uint8)
+        _one(t, C, src, recv, ids, rng, f"table {it} C={C} ids={ids.size}")
+        if it % 100 == 0:
+            log(f"delta tiny {it}")
+
+
+@pytest.mark.parametrize("tile", [0, 2, 4, 5, 9])
+def test_delta_every_tile(tile):
+    old = os.environ.get("FLASHRESTORE_TILE")
+    os.environ["FLASHRESTORE_TILE"] = str(tile)
+    try:
+        rng = np.random.default_rng(80 + tile)
+        for it in range(20):
+            t, sb, db = W.random_tiny_table(rng, max_entries=8, max_numel=100_000)
+            C = int(rng.choice([256, 4096, 16384, 65536]))
+            nc = cpu.n_chunks(t, C)
+            ids = np.sort(rng.choice(nc, size=int(rng.integers(0, nc + 1)), replace=False)).astype(np.uint32) \
+                if nc else np.zeros(0, np.uint32)
+            src = W.random_tiny_state(t, sb, rng)
+            recv = rng.integers(0, 256, size=db, dtype=np.uint8)
+            _one(t, C, src, recv, ids, rng, f"tile {tile} table {it}")
+    finally:
+        if old is None:
+            os.environ.pop("FLASHRESTORE_TILE", None)
+        else:
+            os.environ["FLASHRESTORE_TILE"] = old
+
+
+def test_listing_every_chunk_equals_the_full_pack():
+    w = W.make_workload(0)
+    src = to_dev(W.fill_state(w))
+    plan = F.Plan(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
+    ids = np.arange(plan.n_chunks, dtype=np.uint32)
+    assert plan.delta_layout(ids) == plan.payload_bytes
+    p1, s1 = plan.empty_payload(), plan.empty_sums()
+    p2, s2 = plan.empty_payload(), plan.empty_sums()
+    plan.pack(src, p1, s1)
+    plan.pack_chunks(src, ids, p2, s2)
+    torch.cuda.synchronize()
+    assert torch.equal(p1[: plan.payload_bytes], p2[: plan.payload_bytes]) and torch.equal(s1, s2)
+
+
+def test_delta_list_errors():
+    w = W.make_workload(0)
+    plan = F.Plan(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
+    for bad in ([3, 3], [5, 4], [plan.n_chunks]):
+        with pytest.raises(F.FlashRestoreError) as ei:
+            plan.delta_layout(np.array(bad, np.uint32))
+        assert ei.value.status == -1
+
+
+@pytest.mark.timeout(600)
+def test_repair_llama8b_share_from_the_flagged_chunks():
+    """Donor and a replica with 4096 random flips: compare, re-send only the
+    flagged chunks, and the replica equals the donor again."""
+    w = W.make_workload(1)
+    t, C = w.table, w.chunk_bytes
+    donor_np = W.fill_state(w)
+    log("generated", w.name)
+    plan = F.Plan(t, C, w.src_arena_bytes, w.dst_arena_bytes)
+    donor = to_dev(donor_np)
+    recv = donor.clone()
+    pos = W.flip_positions(donor_np.size * 8, 4096, 4000 + 4096)
+    by = (pos // 8).astype(np.int64)
+    masks = (np.uint8(1) << (pos % 8).astype(np.uint8)).astype(np.uint8)
+    uniq, start = np.unique(by, return_index=True)
+    idx = torch.from_numpy(uniq).to("cuda")
+    recv[idx] = recv[idx] ^ torch.from_numpy(np.bitwise_or.reduceat(masks, start)).to("cuda")
+    diff, ndiff = plan.empty_bitmap(), plan.empty_counter()
+    plan.verify_replicas(donor, recv, diff, ndiff)
+    ids = F.bitmap_indices(diff, plan.n_chunks).astype(np.uint32)
+    assert ids.size == int(ndiff.item()) == 4060
+    pb = plan.delta_layout(ids)
+    payload = torch.empty(pb, dtype=torch.uint8, device="cuda")
+    sums = torch.empty(ids.size, 2, dtype=torch.int64, device="cuda")
+    plan.pack_chunks(donor, ids, payload, sums)
+    opay, osums = cpu.pack_chunks(t, C, donor_np, ids)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(payload), opay) and np.array_equal(sums_host(sums, ids.size), osums)
+    bad = torch.empty((ids.size + 31) // 32, dtype=torch.int32, device="cuda")
+    nbad = torch.empty(1, dtype=torch.int64, device="cuda")
+    plan.unpack_chunks(payload, sums, ids, recv, bad, nbad)
+    plan.verify_replicas(donor, recv, diff, ndiff)
+    torch.cuda.synchronize()
+    assert int(nbad.item()) == 0 and int(ndiff.item()) == 0 and torch.equal(recv, donor)
+    log(f"repaired {ids.size} chunks with {pb} payload bytes")
