@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=1, help="workload: 0 toy, 1 8B share, 2 stress, 3 70B share")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-delta", action="store_true", help="skip the delta-repair measurement")
+    ap.add_argument("--delta-flips", type=int, default=4096)
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time per baseline")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 4 GiB device copy (for counter scaling) and exit")
@@ -126,6 +128,53 @@ def cpu_baseline(w, src_np, seconds: float):
         "kind": "oracle",
         "sample": f"first {n_ent} of {len(t)} entries ({n_ent // 4} logical tensors, {state} state bytes), "
                   f"{reps} full steps (pack+unpack+verify+checksum) in {el:.1f} s",
+    }
+
+
+def delta_repair(plan, donor, replica, info, k, stream, reps=5):
+    """Repair of a replica that diverged in k random bits: compare, read the
+    flagged set back, re-send only those chunks.  Times the GPU work of the
+    two delta operations (HIP events) and the whole repair on the host clock."""
+    import numpy as np
+    import torch
+
+    from paper_2509_03047_amd import flashrestore as F
+    from paper_2509_03047_amd import workloads as W
+
+    pos = W.flip_positions(info["src_arena_bytes"] * 8, k, 4000 + k)
+    by = (pos // 8).astype(np.int64)
+    masks = (np.uint8(1) << (pos % 8).astype(np.uint8)).astype(np.uint8)
+    uniq, start = np.unique(by, return_index=True)
+    idx = torch.from_numpy(uniq).to("cuda")
+    xor = torch.from_numpy(np.bitwise_or.reduceat(masks, start)).to("cuda")
+    diff, ndiff = plan.empty_bitmap(), plan.empty_counter()
+    bad, nbad = plan.empty_bitmap(), plan.empty_counter()
+    payload = plan.empty_payload()
+    sums = plan.empty_sums()
+    gpu_ms, wall_ms = [], []
+    for _ in range(reps):
+        replica[idx] = replica[idx] ^ xor  # diverge
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        plan.verify_replicas(donor, replica, diff, ndiff, stream=stream)
+        ids = F.bitmap_indices(diff, plan.n_chunks).astype(np.uint32)  # synchronises
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        plan.pack_chunks(donor, ids, payload, sums, stream=stream)
+        plan.unpack_chunks(payload, sums, ids, replica, bad, nbad, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wall_ms.append((time.perf_counter() - t0) * 1e3)
+        gpu_ms.append(e0.elapsed_time(e1))
+    ok = int(nbad.item()) == 0 and torch.equal(replica, donor)
+    return {
+        "flips": k,
+        "chunks_resent": int(ids.size),
+        "payload_bytes": int(plan.delta_layout(ids)),
+        "gpu_ms_pack_unpack": round(float(np.median(gpu_ms)), 4),
+        "wall_ms_compare_to_repaired": round(float(np.median(wall_ms)), 3),
+        "full_restore_ms": None,
+        "ok": bool(ok),
     }
 
 
@@ -253,6 +302,9 @@ def main():
         "parity_ok": bool(ok),
         "wall_s_timed": round(wall, 4),
     }
+    if not args.no_delta:
+        out["delta_repair"] = delta_repair(plan, src, dst, info, args.delta_flips, stream)
+        out["delta_repair"]["full_restore_ms"] = round(restore_ms, 4)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, src_np, args.cpu_seconds)
     print(json.dumps(out), flush=True)
