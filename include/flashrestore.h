@@ -242,6 +242,65 @@ int fr_unpack_chunks(const fr_plan* plan, const void* payload, const fr_chunk_su
                      const uint32_t* chunk_ids, uint64_t n_ids, void* dst_base,
                      uint32_t* bad_bitmap, uint64_t* n_bad, void* stream);
 
+/* ------------------------------------------------- step tags and donors */
+
+/* Host-only controller logic that decides *which* state a restore copies and
+ * *when* the normal ranks may be stopped (Section III-E, "Step i or step i+1
+ * to resume?" and "The moment to stop, clean and reset").  Every rank tags
+ * itself i when forward of step i starts, -1 when its optimizer step starts
+ * and i+1 when that ends, and reports the tag with its heartbeat
+ * (Section III-C).  A barrier merged into the gradient all-reduce keeps the
+ * ranks in one phase, so once every normal rank reports the same tag T >= 0
+ * the replicas hold the state at the start of step T: stop, restore the
+ * failed ranks from replicas at step T, roll the data iterator back to T.
+ * Readings where the paper is silent: a normal rank's tag counts only if it
+ * was reported after the last failure was detected (an older report may show
+ * i from a rank already inside its optimizer step); a rank silent for longer
+ * than the timeout counts as failed, detected at last heartbeat + timeout;
+ * fresh tags that are neither all equal nor -1 are inconsistent with the
+ * barrier; a data-parallel group with no live rank leaves no replica, so the
+ * answer is a checkpoint (Section III-G).  Times are seconds on any monotonic
+ * clock; the timeout must exceed the heartbeat period. */
+
+typedef struct fr_tracker fr_tracker; /* opaque, owned by the library */
+
+enum fr_action {
+  FR_ACT_CONTINUE = 0,            /* no failed rank */
+  FR_ACT_WAIT = 1,                /* a normal rank is in its optimizer step or has not
+                                     reported since the last failure was detected */
+  FR_ACT_STOP_AND_RESTORE = 2,    /* stop, clean, reset; resume at resume_step */
+  FR_ACT_CHECKPOINT_FALLBACK = 3, /* some data-parallel group has no live rank */
+  FR_ACT_INCONSISTENT = 4         /* fresh normal tags disagree */
+};
+
+typedef struct fr_decision {
+  int64_t resume_step; /* valid for FR_ACT_STOP_AND_RESTORE, else -1 */
+  int32_t action;      /* enum fr_action */
+  uint32_t n_failed;   /* ranks counted as failed */
+  uint32_t n_waiting;  /* normal ranks the decision waits for */
+  uint32_t reserved;
+} fr_decision;
+
+/* n_ranks > 0; dp_group[r] < n_ranks is the data-parallel group of rank r
+ * (host array, copied; NULL puts every rank in group 0); timeout_s > 0. */
+int fr_tracker_create(uint32_t n_ranks, const uint32_t* dp_group, double timeout_s, double now_s,
+                      fr_tracker** out);
+int fr_tracker_destroy(fr_tracker* t);
+/* A heartbeat of `rank` carrying its tag (>= 0, or -1 in the optimizer step). */
+int fr_tracker_heartbeat(fr_tracker* t, uint32_t rank, int64_t step_tag, double now_s);
+/* A failure of `rank` reported by a monitor or device plugin at now_s. */
+int fr_tracker_report_failure(fr_tracker* t, uint32_t rank, double now_s);
+int fr_tracker_decide(const fr_tracker* t, double now_s, fr_decision* out);
+/* The failed ranks in increasing order; FR_E_RANGE (with *n_failed set) if
+ * more than cap. */
+int fr_tracker_failed_ranks(const fr_tracker* t, double now_s, uint32_t* ranks, uint32_t cap,
+                            uint32_t* n_failed);
+/* donor[r] (n_ranks entries): for a failed rank, the live rank of its
+ * data-parallel group whose state restores it (failed ranks of a group are
+ * spread over its live ranks in rank order; Section III-D stage 3); -1 for
+ * live ranks and for ranks whose group has no live rank. */
+int fr_tracker_donors(const fr_tracker* t, double now_s, int32_t* donor);
+
 /* ---------------------------------------------------------------- misc */
 
 const char* fr_strerror(int status);

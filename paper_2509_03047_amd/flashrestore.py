@@ -55,6 +55,19 @@ class fr_plan_info(C.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_}
 
 
+class fr_decision(C.Structure):
+    _fields_ = [
+        ("resume_step", C.c_int64),
+        ("action", C.c_int32),
+        ("n_failed", C.c_uint32),
+        ("n_waiting", C.c_uint32),
+        ("reserved", C.c_uint32),
+    ]
+
+
+ACTIONS = {0: "continue", 1: "wait", 2: "stop_and_restore", 3: "checkpoint_fallback", 4: "inconsistent"}
+
+
 class FlashRestoreError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
@@ -87,6 +100,13 @@ def _load():
         "fr_delta_layout": [P, P, u64, C.POINTER(u64)],
         "fr_pack_chunks": [P, P, P, u64, P, u64, P, P],
         "fr_unpack_chunks": [P, P, P, P, u64, P, P, P, P],
+        "fr_tracker_create": [u32, P, C.c_double, C.c_double, C.POINTER(P)],
+        "fr_tracker_destroy": [P],
+        "fr_tracker_heartbeat": [P, u32, C.c_int64, C.c_double],
+        "fr_tracker_report_failure": [P, u32, C.c_double],
+        "fr_tracker_decide": [P, C.c_double, C.POINTER(fr_decision)],
+        "fr_tracker_failed_ranks": [P, C.c_double, P, u32, C.POINTER(u32)],
+        "fr_tracker_donors": [P, C.c_double, P],
         "fr_strerror": [i32],
         "fr_last_hip_error": [],
         "fr_abi_version": [],
@@ -107,7 +127,9 @@ EXPORTED = (
     "fr_plan_create", "fr_plan_get_info", "fr_plan_chunk_of", "fr_plan_entry_layout",
     "fr_plan_destroy", "fr_layout_query", "fr_pack_state", "fr_unpack_state",
     "fr_verify_replicas", "fr_checksum_state", "fr_delta_layout", "fr_pack_chunks",
-    "fr_unpack_chunks", "fr_strerror", "fr_last_hip_error", "fr_abi_version",
+    "fr_unpack_chunks", "fr_tracker_create", "fr_tracker_destroy", "fr_tracker_heartbeat",
+    "fr_tracker_report_failure", "fr_tracker_decide", "fr_tracker_failed_ranks", "fr_tracker_donors",
+    "fr_strerror", "fr_last_hip_error", "fr_abi_version",
 )
 
 
@@ -326,6 +348,48 @@ def fr_unpack_chunks(plan: Plan, payload, sums, chunk_ids, dst, bad_bitmap, n_ba
     _check(_lib.fr_unpack_chunks(plan.handle, _ptr(payload), _ptr(sums), ids.ctypes.data if ids.size else None,
                                  ids.size, _ptr(dst), _ptr(bad_bitmap), _ptr(n_bad), _stream(stream)),
            "fr_unpack_chunks")
+
+
+class Tracker:
+    """Step-tag tracker of the controller (``fr_tracker_*``; host only)."""
+
+    def __init__(self, n_ranks: int, dp_group=None, timeout_s: float = 10.0, now_s: float = 0.0):
+        self._h = None
+        self.n_ranks = n_ranks
+        g = None if dp_group is None else np.ascontiguousarray(dp_group, dtype=np.uint32)
+        h = C.c_void_p()
+        _check(_lib.fr_tracker_create(n_ranks, None if g is None else g.ctypes.data, timeout_s, now_s,
+                                      C.byref(h)), "fr_tracker_create")
+        self._h = h
+
+    def __del__(self):
+        if getattr(self, "_h", None) is not None:
+            _lib.fr_tracker_destroy(self._h)
+            self._h = None
+
+    def heartbeat(self, rank: int, step_tag: int, now_s: float):
+        _check(_lib.fr_tracker_heartbeat(self._h, rank, step_tag, now_s), "fr_tracker_heartbeat")
+
+    def report_failure(self, rank: int, now_s: float):
+        _check(_lib.fr_tracker_report_failure(self._h, rank, now_s), "fr_tracker_report_failure")
+
+    def decide(self, now_s: float) -> dict:
+        d = fr_decision()
+        _check(_lib.fr_tracker_decide(self._h, now_s, C.byref(d)), "fr_tracker_decide")
+        return {"action": ACTIONS[d.action], "resume_step": d.resume_step, "n_failed": d.n_failed,
+                "n_waiting": d.n_waiting}
+
+    def failed_ranks(self, now_s: float) -> list:
+        out = np.zeros(self.n_ranks, np.uint32)
+        n = C.c_uint32()
+        _check(_lib.fr_tracker_failed_ranks(self._h, now_s, out.ctypes.data, self.n_ranks, C.byref(n)),
+               "fr_tracker_failed_ranks")
+        return [int(x) for x in out[: n.value]]
+
+    def donors(self, now_s: float) -> list:
+        out = np.zeros(self.n_ranks, np.int32)
+        _check(_lib.fr_tracker_donors(self._h, now_s, out.ctypes.data), "fr_tracker_donors")
+        return [int(x) for x in out]
 
 
 def fr_strerror(status: int) -> str:
