@@ -301,6 +301,56 @@ int fr_tracker_failed_ranks(const fr_tracker* t, double now_s, uint32_t* ranks, 
  * live ranks and for ranks whose group has no live rank. */
 int fr_tracker_donors(const fr_tracker* t, double now_s, int32_t* donor);
 
+/* ------------------------------------------ parallel layouts and donors */
+
+/* Restore planning for data x tensor x pipeline parallel training with ZeRO
+ * sharding (Section III-A lists DP, PP, TP and ZeRO/FSDP and their
+ * combination; Section III-E restores vanilla DP, ZeRO/FSDP and combined
+ * layouts from replicas).  Host only.  The paper fixes no rank order or shard
+ * layout; this library's:
+ *   world = tp * dp * pp; rank = t + tp * (d + dp * p) for tensor index t,
+ *   data index d, pipeline index p.  The data-parallel group of a (t, p)
+ *   slice is split into dp / shard replica groups of `shard` ranks:
+ *   d = s + shard * q for shard index s and replica index q.
+ *   zero_stage 0: vanilla DP (shard must be 1), every rank holds bf16
+ *     params, fp32 master, m, v of every tensor of its slice;
+ *   zero_stage 1 or 2: the slice's tensors are flattened in order into N
+ *     elements, padded with zeros to a multiple of 8 * shard; shard s owns
+ *     elements [s E, (s+1) E), E = N_pad / shard, of master, m and v; bf16
+ *     params are kept whole;
+ *   zero_stage 3: params are sharded like the optimizer state.
+ * Ranks with equal (t, p, s) hold identical state and are each other's
+ * replicas; a failed rank is restored from a live one of them. */
+typedef struct fr_layout3d {
+  uint32_t tp, pp, dp; /* parallel degrees, each >= 1 */
+  uint32_t shard;      /* ranks a ZeRO shard group spans; divides dp */
+  uint32_t zero_stage; /* 0, 1, 2 or 3 */
+  uint32_t reserved;   /* 0 */
+} fr_layout3d;
+
+/* coords[5] <- (t, p, d, s, q) of `rank`. */
+int fr_layout_rank_coords(const fr_layout3d* layout, uint32_t rank, uint32_t* coords);
+
+/* failed[world] (0/1) -> donor[world]: for each failed rank a live replica
+ * (failed ranks of a replica class are spread over its live ranks in rank
+ * order), -1 for live ranks and for failed ranks with no live replica (those
+ * need a checkpoint, Section III-G). */
+int fr_layout_donors(const fr_layout3d* layout, const uint8_t* failed, int32_t* donor);
+
+/* The tensor table of `rank`'s state arena (identical on all replicas of the
+ * rank, so the donor packs and the new rank unpacks with the same plan):
+ *   numel[n_tensors]  element counts of the slice's logical tensors
+ * stage 0: per tensor [param bf16 (derived from the next), master, m, v];
+ * stage 1/2: [param before the shard, param shard (derived from the master
+ * shard), param after the shard, master shard, m shard, v shard];
+ * stage 3: [param shard (derived), master shard, m shard, v shard].
+ * Entries are contiguous, 16-aligned, src and dst offsets equal;
+ * *arena_bytes = the arena size.  With table == NULL only *n_entries and
+ * *arena_bytes are set; FR_E_RANGE if cap < *n_entries. */
+int fr_layout_state_table(const fr_layout3d* layout, uint32_t rank, const uint64_t* numel,
+                          uint32_t n_tensors, fr_tensor_desc* table, uint32_t cap,
+                          uint32_t* n_entries, uint64_t* arena_bytes);
+
 /* ---------------------------------------------------------------- misc */
 
 const char* fr_strerror(int status);

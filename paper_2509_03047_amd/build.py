@@ -12,7 +12,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libflashrestore.so")
-SOURCES = ["plan.cpp", "api.cpp", "steptag.cpp", "kernels.hip"]
+SOURCES = ["plan.cpp", "api.cpp", "steptag.cpp", "layout.cpp", "kernels.hip"]
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 

@@ -65,6 +65,11 @@ class fr_decision(C.Structure):
     ]
 
 
+class fr_layout3d(C.Structure):
+    _fields_ = [("tp", C.c_uint32), ("pp", C.c_uint32), ("dp", C.c_uint32), ("shard", C.c_uint32),
+                ("zero_stage", C.c_uint32), ("reserved", C.c_uint32)]
+
+
 ACTIONS = {0: "continue", 1: "wait", 2: "stop_and_restore", 3: "checkpoint_fallback", 4: "inconsistent"}
 
 
@@ -107,6 +112,9 @@ def _load():
         "fr_tracker_decide": [P, C.c_double, C.POINTER(fr_decision)],
         "fr_tracker_failed_ranks": [P, C.c_double, P, u32, C.POINTER(u32)],
         "fr_tracker_donors": [P, C.c_double, P],
+        "fr_layout_rank_coords": [P, u32, P],
+        "fr_layout_donors": [P, P, P],
+        "fr_layout_state_table": [P, u32, P, u32, P, u32, C.POINTER(u32), C.POINTER(u64)],
         "fr_strerror": [i32],
         "fr_last_hip_error": [],
         "fr_abi_version": [],
@@ -129,6 +137,7 @@ EXPORTED = (
     "fr_verify_replicas", "fr_checksum_state", "fr_delta_layout", "fr_pack_chunks",
     "fr_unpack_chunks", "fr_tracker_create", "fr_tracker_destroy", "fr_tracker_heartbeat",
     "fr_tracker_report_failure", "fr_tracker_decide", "fr_tracker_failed_ranks", "fr_tracker_donors",
+    "fr_layout_rank_coords", "fr_layout_donors", "fr_layout_state_table",
     "fr_strerror", "fr_last_hip_error", "fr_abi_version",
 )
 
@@ -390,6 +399,39 @@ class Tracker:
         out = np.zeros(self.n_ranks, np.int32)
         _check(_lib.fr_tracker_donors(self._h, now_s, out.ctypes.data), "fr_tracker_donors")
         return [int(x) for x in out]
+
+
+class Layout3D:
+    """A data x tensor x pipeline parallel layout with ZeRO sharding
+    (``fr_layout_*``; host only)."""
+
+    def __init__(self, tp=1, pp=1, dp=1, shard=1, zero_stage=0):
+        self.s = fr_layout3d(tp, pp, dp, shard, zero_stage, 0)
+        self.world = tp * pp * dp
+
+    def coords(self, rank: int) -> tuple:
+        out = np.zeros(5, np.uint32)
+        _check(_lib.fr_layout_rank_coords(C.byref(self.s), rank, out.ctypes.data), "fr_layout_rank_coords")
+        return tuple(int(x) for x in out)
+
+    def donors(self, failed) -> list:
+        f = np.zeros(self.world, np.uint8)
+        f[list(failed)] = 1
+        out = np.zeros(self.world, np.int32)
+        _check(_lib.fr_layout_donors(C.byref(self.s), f.ctypes.data, out.ctypes.data), "fr_layout_donors")
+        return [int(x) for x in out]
+
+    def state_table(self, rank: int, numel):
+        """(table as a DESC_DTYPE array, arena bytes) of `rank`'s state."""
+        n = np.ascontiguousarray(numel, np.uint64)
+        ne, ab = C.c_uint32(), C.c_uint64()
+        ptr = n.ctypes.data if n.size else None
+        _check(_lib.fr_layout_state_table(C.byref(self.s), rank, ptr, n.size, None, 0, C.byref(ne), C.byref(ab)),
+               "fr_layout_state_table")
+        t = np.zeros(ne.value, DESC_DTYPE)
+        _check(_lib.fr_layout_state_table(C.byref(self.s), rank, ptr, n.size, t.ctypes.data, ne.value,
+                                          C.byref(ne), C.byref(ab)), "fr_layout_state_table")
+        return t, ab.value
 
 
 def fr_strerror(status: int) -> str:
