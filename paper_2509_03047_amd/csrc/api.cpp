@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <cstring>
 #include <new>
 #include <vector>
 
@@ -94,6 +95,16 @@ int launch_result(int hip_rc) {
   return device_error(hipError_t(hip_rc));
 }
 
+// The plan's pack / checksum / compare walk at the slice size of `tile`
+// (the plan builds one for each tile it is configured with, so this finds
+// one for the plan's own tiles).
+const SlotTable* src_walk(const fr_plan* plan, int tile) {
+  const uint32_t sl = slice_bytes(plan->layout.C, tile);
+  for (const auto& w : plan->src_walks)
+    if (w.sl == sl) return &w.t;
+  return nullptr;
+}
+
 #define FR_TRY(expr)            \
   do {                          \
     const int rc_ = (expr);     \
@@ -114,8 +125,10 @@ extern "C" int fr_pack_state(const fr_plan* plan, const void* src_base, void* pa
   const Region outs[] = {{payload, L.payload_bytes}, {sums, L.n_chunks * sizeof(fr_chunk_sum)}};
   const Region ins[] = {{src_base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 2, ins, 1));
-  return launch_result(launch_pack(plan->d_chunks, uint32_t(L.n_chunks), L.C, src_base, payload,
-                                   sums, plan->scratch, plan->cfg, stream));
+  const SlotTable* walk = src_walk(plan, plan->cfg.tile_pack);
+  if (!walk) return FR_E_INVAL;
+  return launch_result(launch_pack(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, src_base,
+                                   payload, sums, plan->scratch, plan->cfg, stream));
 }
 
 extern "C" int fr_unpack_state(const fr_plan* plan, const void* payload, const fr_chunk_sum* sums,
@@ -138,6 +151,7 @@ extern "C" int fr_unpack_state(const fr_plan* plan, const void* payload, const f
   u.n_derived = plan->n_derived;
   u.plain = plan->d_plain;
   u.n_plain = plan->n_plain;
+  u.slots = plan->unpack_walk.t;
   u.n_chunks = uint32_t(L.n_chunks);
   u.C = L.C;
   u.payload = payload;
@@ -169,8 +183,10 @@ extern "C" int fr_verify_replicas(const fr_plan* plan, const void* base_a, const
   const Region outs[] = {{diff_bitmap, words * 4}, {n_diff, 8}, {sums_a, sb}, {sums_b, sb}};
   const Region ins[] = {{base_a, plan->src_arena_bytes}, {base_b, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 4, ins, 2));
-  return launch_result(launch_verify(plan->d_chunks, uint32_t(L.n_chunks), L.C, base_a, base_b,
-                                     diff_bitmap, n_diff, sums_a, sums_b, plan->scratch,
+  const SlotTable* walk = src_walk(plan, plan->cfg.tile_verify);
+  if (!walk) return FR_E_INVAL;
+  return launch_result(launch_verify(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, base_a,
+                                     base_b, diff_bitmap, n_diff, sums_a, sums_b, plan->scratch,
                                      plan->cfg, stream));
 }
 
@@ -184,9 +200,10 @@ extern "C" int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk
   const Region outs[] = {{sums, L.n_chunks * sizeof(fr_chunk_sum)}};
   const Region ins[] = {{base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 1, ins, 1));
-  return launch_result(
-      launch_checksum(plan->d_chunks, uint32_t(L.n_chunks), L.C, base, sums, plan->scratch,
-                      plan->cfg, stream));
+  const SlotTable* walk = src_walk(plan, plan->cfg.tile_checksum);
+  if (!walk) return FR_E_INVAL;
+  return launch_result(launch_checksum(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, base,
+                                       sums, plan->scratch, plan->cfg, stream));
 }
 
 // ------------------------------------------------------------ delta repair
@@ -232,8 +249,9 @@ uint64_t delta_bytes(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids) {
 
 // Device room for the unit records of a delta call (allocated once per plan,
 // sized for a list of every chunk).
-int ensure_delta_buffer(fr_plan* plan) {
-  const uint64_t need = std::max<uint64_t>(plan->layout.n_chunks, 1) * sizeof(DerivedUnit);
+// Device buffer for a delta call's records and slot tables (grows on demand;
+// hipFree waits for work still using the old one).
+int ensure_delta_buffer(fr_plan* plan, uint64_t need) {
   if (plan->d_delta && plan->delta_cap >= need) return FR_OK;
   void* p = nullptr;
   hipError_t e = hipMalloc(&p, need);
@@ -280,32 +298,44 @@ extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const 
   const Region ins[] = {{src_base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 2, ins, 1));
   if (n_ids == 0) return FR_OK;
-  FR_TRY(ensure_delta_buffer(plan));
   const uint64_t C = plan->layout.C;
+  // device image: [n_ids SrcUnit records][slot table]
+  SlotBuilder b;
+  b.sl = slice_bytes(C, plan->cfg.tile_pack);
+  uint64_t tab_off = 0;
   try {
-    plan->delta_host.resize(n_ids * sizeof(ChunkRec));
+    std::vector<SrcUnit> recs(n_ids);
+    uint64_t pay = 0;
+    for (uint64_t i = 0; i < n_ids; i++) {
+      const Where w = locate(plan, ids[i]);
+      const fr_tensor_desc& d = plan->table[w.entry];
+      SrcUnit& r = recs[i];
+      r.src_off = d.src_offset + w.j * C;
+      r.len = uint32_t(w.len);
+      r.c = uint32_t(i);
+      if (d.derive_from >= 0) {
+        r.pay_off = kNoPayload;
+      } else {
+        r.pay_off = pay;
+        pay = (pay + w.len + 15) & ~uint64_t(15);
+      }
+      b.add(uint32_t(i), w.len, 0);
+    }
+    tab_off = n_ids * sizeof(SrcUnit);
+    plan->delta_host.resize(tab_off + 8 * b.stride() * sizeof(uint64_t));
+    std::memcpy(plan->delta_host.data(), recs.data(), tab_off);
+    b.xcd_major(reinterpret_cast<uint64_t*>(plan->delta_host.data() + tab_off));
   } catch (const std::bad_alloc&) {
     return FR_E_NOMEM;
   }
-  ChunkRec* recs = reinterpret_cast<ChunkRec*>(plan->delta_host.data());
-  uint64_t pay = 0;
-  for (uint64_t i = 0; i < n_ids; i++) {
-    const Where w = locate(plan, ids[i]);
-    const fr_tensor_desc& d = plan->table[w.entry];
-    ChunkRec& r = recs[i];
-    r.src_off = d.src_offset + w.j * C;
-    r.dst_off = d.dst_offset + w.j * C;
-    r.len = uint32_t(w.len);
-    r.master = kNoMaster;
-    if (d.derive_from >= 0) {
-      r.pay_off = kNoPayload;
-    } else {
-      r.pay_off = pay;
-      pay = (pay + w.len + 15) & ~uint64_t(15);
-    }
-  }
-  FR_TRY(upload_records(plan, n_ids * sizeof(ChunkRec), stream));
-  return launch_result(launch_pack(static_cast<const ChunkRec*>(plan->d_delta), uint32_t(n_ids), C,
+  FR_TRY(ensure_delta_buffer(plan, plan->delta_host.size()));
+  FR_TRY(upload_records(plan, plan->delta_host.size(), stream));
+  const uint8_t* dev = static_cast<const uint8_t*>(plan->d_delta);
+  SlotTable t;
+  t.d = reinterpret_cast<const uint64_t*>(dev + tab_off);
+  t.n = b.lin.size();
+  t.stride = b.stride();
+  return launch_result(launch_pack(reinterpret_cast<const SrcUnit*>(dev), t, uint32_t(n_ids), C,
                                    src_base, payload, sums, plan->scratch, plan->cfg, stream));
 }
 
@@ -327,49 +357,67 @@ extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
   const Region outs[] = {{dst_base, plan->dst_arena_bytes}, {bad_bitmap, words * 4}, {n_bad, 8}};
   const Region ins[] = {{payload, pb}, {sums, n_ids * sizeof(fr_chunk_sum)}};
   FR_TRY(check_disjoint(outs, 3, ins, 2));
-  if (n_ids) FR_TRY(ensure_delta_buffer(plan));
   const uint64_t C = plan->layout.C;
-  uint32_t n_plain = 0, n_derived = 0;
-  for (uint64_t i = 0; i < n_ids; i++)
-    (plan->table[locate(plan, ids[i]).entry].derive_from < 0 ? n_plain : n_derived)++;
+  // device image: [plain units][derived units][plain slots][derived slots]
+  SlotBuilder bp, bd;
+  bp.sl = bd.sl = slice_bytes(C, plan->cfg.tile_unpack);
+  uint64_t off_d = 0, off_sp = 0, off_sd = 0;
   try {
-    plan->delta_host.resize(n_plain * sizeof(PlainUnit) + n_derived * sizeof(DerivedUnit));
+    std::vector<PlainUnit> pu;
+    std::vector<DerivedUnit> du;
+    uint64_t pay = 0;
+    for (uint64_t i = 0; i < n_ids; i++) {
+      const Where w = locate(plan, ids[i]);
+      const fr_tensor_desc& d = plan->table[w.entry];
+      if (d.derive_from < 0) {
+        PlainUnit u{};
+        u.pay_off = pay;
+        u.dst_off = d.dst_offset + w.j * C;
+        u.len = uint32_t(w.len);
+        u.c = uint32_t(i);
+        bp.add(uint32_t(pu.size()), w.len, 0);
+        pu.push_back(u);
+        pay = (pay + w.len + 15) & ~uint64_t(15);
+      } else {
+        const fr_tensor_desc& m = plan->table[d.derive_from];
+        DerivedUnit u{};
+        u.m_pay_off = m.dst_offset + 2 * w.j * C;  // the receiver's master bytes of this chunk
+        u.m_dst_off = u.m_pay_off;
+        u.p_dst_off = d.dst_offset + w.j * C;
+        u.len = uint32_t(w.len);
+        u.c = uint32_t(i);
+        bd.add(uint32_t(du.size()), 2 * w.len, kSlotDerived);
+        du.push_back(u);
+      }
+    }
+    off_d = pu.size() * sizeof(PlainUnit);
+    off_sp = off_d + du.size() * sizeof(DerivedUnit);
+    off_sd = off_sp + 8 * bp.stride() * sizeof(uint64_t);
+    plan->delta_host.resize(off_sd + 8 * bd.stride() * sizeof(uint64_t));
+    uint8_t* h = plan->delta_host.data();
+    if (!pu.empty()) std::memcpy(h, pu.data(), off_d);
+    if (!du.empty()) std::memcpy(h + off_d, du.data(), off_sp - off_d);
+    bp.xcd_major(reinterpret_cast<uint64_t*>(h + off_sp));
+    bd.xcd_major(reinterpret_cast<uint64_t*>(h + off_sd));
   } catch (const std::bad_alloc&) {
     return FR_E_NOMEM;
   }
-  PlainUnit* pu = reinterpret_cast<PlainUnit*>(plan->delta_host.data());
-  DerivedUnit* du = reinterpret_cast<DerivedUnit*>(plan->delta_host.data() + n_plain * sizeof(PlainUnit));
-  uint64_t pay = 0;
-  uint32_t ip = 0, id = 0;
-  for (uint64_t i = 0; i < n_ids; i++) {
-    const Where w = locate(plan, ids[i]);
-    const fr_tensor_desc& d = plan->table[w.entry];
-    if (d.derive_from < 0) {
-      PlainUnit& u = pu[ip++];
-      u = PlainUnit{};
-      u.pay_off = pay;
-      u.dst_off = d.dst_offset + w.j * C;
-      u.len = uint32_t(w.len);
-      u.c = uint32_t(i);
-      pay = (pay + w.len + 15) & ~uint64_t(15);
-    } else {
-      const fr_tensor_desc& m = plan->table[d.derive_from];
-      DerivedUnit& u = du[id++];
-      u = DerivedUnit{};
-      u.m_pay_off = m.dst_offset + 2 * w.j * C;  // the receiver's master bytes of this chunk
-      u.m_dst_off = u.m_pay_off;
-      u.p_dst_off = d.dst_offset + w.j * C;
-      u.len = uint32_t(w.len);
-      u.c = uint32_t(i);
-    }
+  if (n_ids) {
+    FR_TRY(ensure_delta_buffer(plan, plan->delta_host.size()));
+    FR_TRY(upload_records(plan, plan->delta_host.size(), stream));
   }
-  FR_TRY(upload_records(plan, plan->delta_host.size(), stream));
+  const uint8_t* dev = static_cast<const uint8_t*>(plan->d_delta);
   UnpackDeltaArgs a{};
-  a.plain = static_cast<const PlainUnit*>(plan->d_delta);
-  a.n_plain = n_plain;
-  a.derived = reinterpret_cast<const DerivedUnit*>(static_cast<const uint8_t*>(plan->d_delta) +
-                                                   n_plain * sizeof(PlainUnit));
-  a.n_derived = n_derived;
+  a.plain = reinterpret_cast<const PlainUnit*>(dev);
+  a.n_plain = uint32_t(off_d / sizeof(PlainUnit));
+  a.derived = reinterpret_cast<const DerivedUnit*>(dev + off_d);
+  a.n_derived = uint32_t((off_sp - off_d) / sizeof(DerivedUnit));
+  a.plain_slots.d = reinterpret_cast<const uint64_t*>(dev + off_sp);
+  a.plain_slots.n = bp.lin.size();
+  a.plain_slots.stride = bp.stride();
+  a.derived_slots.d = reinterpret_cast<const uint64_t*>(dev + off_sd);
+  a.derived_slots.n = bd.lin.size();
+  a.derived_slots.stride = bd.stride();
   a.n_ids = uint32_t(n_ids);
   a.C = C;
   a.payload = payload;

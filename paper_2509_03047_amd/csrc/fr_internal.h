@@ -12,8 +12,8 @@ namespace fr {
 constexpr uint64_t kNoPayload = ~uint64_t(0);
 constexpr uint32_t kNoMaster = 0xFFFFFFFFu;
 
-// One record per global chunk id, uploaded once per plan.  Every kernel reads
-// the record of the unit it works on with uniform (scalar) loads.
+// One record per global chunk id (host side; the device tables are built
+// from these).
 struct alignas(16) ChunkRec {
   uint64_t src_off;  // chunk start in the sender / replica arena
   uint64_t pay_off;  // chunk start in the payload; kNoPayload for derived entries
@@ -23,8 +23,22 @@ struct alignas(16) ChunkRec {
 };
 static_assert(sizeof(ChunkRec) == 32, "ChunkRec is 32 bytes");
 
-// Unpack work units, one record each so that a workgroup needs a single
-// dependent load before it can address its data.
+// Device unit records.  A workgroup reads its slot (see SlotTable), then the
+// record of the unit it works on, with uniform (scalar) loads, and needs
+// nothing else to address its data.
+
+// Unit of pack, checksum and replica compare: one chunk of the sender (or
+// replica) arena.
+struct alignas(16) SrcUnit {
+  uint64_t src_off;  // chunk start in the sender / replica arena
+  uint64_t pay_off;  // chunk start in the payload; kNoPayload: read and summed only
+  uint32_t len;      // bytes in this chunk (<= C, even)
+  uint32_t c;        // its sums slot: global chunk id, or list position for a delta
+  uint64_t pad_;
+};
+static_assert(sizeof(SrcUnit) == 32, "SrcUnit is 32 bytes");
+
+// Unpack units.
 // A derived group: bf16 parameter chunk j and the fp32 master chunks 2j and
 // 2j + 1 it is rounded from.
 struct alignas(16) DerivedUnit {
@@ -47,6 +61,34 @@ struct alignas(16) PlainUnit {
   uint64_t pad_;
 };
 static_assert(sizeof(PlainUnit) == 32, "PlainUnit is 32 bytes");
+
+// A walk: one 64-bit slot per workgroup id, (unit << 32) | j with j the
+// slice of that unit, bytes [j * SL, (j + 1) * SL) of it (for unpack,
+// kSlotDerived in the low word marks a derived group).  Units are listed in
+// address order and a unit of b bytes has ceil(b / SL) slots, so no
+// workgroup of a launch is idle.  (Giving every unit C / SL slots instead
+// leaves the slots past a short chunk's end idle: a few thousand idle
+// workgroups among two million cost 4 % of the bandwidth, and moving the
+// short chunks to the end of the launch costs as much, since they are then
+// read scattered.)  The table is stored XCD-major: the
+// dispatcher hands workgroup g to XCD g mod 8, and slot g sits at
+// (g mod 8) * stride + g / 8, so each XCD reads its own slots contiguously.
+constexpr uint32_t kSlotDerived = 0x80000000u;
+
+struct SlotTable {
+  const uint64_t* d = nullptr;
+  uint64_t n = 0;       // slots (workgroups to launch)
+  uint64_t stride = 0;  // ceil(n / 8); the table holds 8 * stride entries
+};
+
+// Host builder of a slot table (plan.cpp).
+struct SlotBuilder {
+  std::vector<uint64_t> lin;  // slots in walk order
+  uint32_t sl = 0;            // slice bytes
+  void add(uint32_t unit, uint64_t bytes, uint32_t flag);
+  uint64_t stride() const { return (lin.size() + 7) / 8; }
+  void xcd_major(uint64_t* out) const;  // writes 8 * stride() entries
+};
 
 // Host-side layout of a validated table.
 struct Layout {
@@ -84,6 +126,7 @@ struct UnpackArgs {
   uint32_t n_derived;
   const PlainUnit* plain;
   uint32_t n_plain;
+  SlotTable slots;  // derived groups and plain chunks in payload order
   uint32_t n_chunks;
   uint64_t C;
   const void* payload;
@@ -101,6 +144,7 @@ struct UnpackDeltaArgs {
   uint32_t n_plain;
   const DerivedUnit* derived;  // derived chunks; m_pay_off = master's receiver offset, c = list position
   uint32_t n_derived;
+  SlotTable plain_slots, derived_slots;
   uint32_t n_ids;
   uint64_t C;
   const void* payload;
@@ -114,20 +158,28 @@ struct UnpackDeltaArgs {
 // Bytes of one slice for a tile, and the accumulators a chunk of C bytes
 // needs with that tile (kernels.hip).
 uint32_t tile_bytes(int tile);
+inline uint32_t slice_bytes(uint64_t C, int tile) {
+  const uint32_t t = tile_bytes(tile);
+  return C < t ? uint32_t(C) : t;
+}
 uint64_t accumulators_per_chunk(uint64_t C, int tile);
 
 // Kernel launchers (kernels.hip).  They assume validated arguments, enqueue
 // on `stream` and return the hipError_t of the launches as an int.
-int launch_pack(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* src,
-                void* payload, fr_chunk_sum* sums, const Scratch& scr, const LaunchCfg& cfg,
-                void* stream);
-int launch_checksum(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* base,
-                    fr_chunk_sum* sums, const Scratch& scr, const LaunchCfg& cfg, void* stream);
+// `units` holds n_chunks records whose sums slots c cover [0, n_chunks);
+// `slots` walks them at the slice size of the operation's tile.
+int launch_pack(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks, uint64_t C,
+                const void* src, void* payload, fr_chunk_sum* sums, const Scratch& scr,
+                const LaunchCfg& cfg, void* stream);
+int launch_checksum(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks, uint64_t C,
+                    const void* base, fr_chunk_sum* sums, const Scratch& scr,
+                    const LaunchCfg& cfg, void* stream);
 int launch_unpack(const UnpackArgs& args, const LaunchCfg& cfg, void* stream);
 int launch_unpack_delta(const UnpackDeltaArgs& args, const LaunchCfg& cfg, void* stream);
-int launch_verify(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* a,
-                  const void* b, uint32_t* bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
-                  fr_chunk_sum* sums_b, const Scratch& scr, const LaunchCfg& cfg, void* stream);
+int launch_verify(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks, uint64_t C,
+                  const void* a, const void* b, uint32_t* bitmap, uint64_t* n_diff,
+                  fr_chunk_sum* sums_a, fr_chunk_sum* sums_b, const Scratch& scr,
+                  const LaunchCfg& cfg, void* stream);
 
 }  // namespace fr
 
@@ -136,7 +188,16 @@ struct fr_plan {
   std::vector<fr_tensor_desc> table;
   fr::Layout layout;
   uint64_t src_arena_bytes = 0, dst_arena_bytes = 0;
-  fr::ChunkRec* d_chunks = nullptr;  // n_chunks records
+  fr::SrcUnit* d_units = nullptr;    // n_chunks records, chunk order
+  // slot tables of the walks: pack / checksum / compare (one per slice size
+  // their tiles use) and unpack
+  struct Walk {
+    uint32_t sl = 0;
+    fr::SlotTable t{};
+    uint64_t* mem = nullptr;
+  };
+  std::vector<Walk> src_walks;
+  Walk unpack_walk;
   fr::DerivedUnit* d_derived = nullptr;  // unpack units: derived groups
   uint32_t n_derived = 0;
   fr::PlainUnit* d_plain = nullptr;      // unpack units: plain chunks

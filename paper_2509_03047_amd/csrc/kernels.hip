@@ -10,8 +10,10 @@
 // launched in address order, keeps the whole chip working inside one compact
 // window and reaches 6.5-6.7 TB/s.  So:
 //   * the unit of work is a slice of SL = min(tile, C) bytes of one chunk
-//     (tile = B threads x U vectors x 16 B); chunk c owns SPC = C / SL
-//     consecutive workgroup ids, so launch order is table (address) order;
+//     (tile = B threads x U vectors x 16 B); a slot table lists the slices
+//     of every unit in address order, one per workgroup id, so launch order
+//     is table (address) order and no workgroup is idle (a workgroup reads
+//     its slot, then its unit's record, then its data);
 //   * each thread moves U 16-byte vectors with non-temporal loads/stores;
 //   * FRSUM-128 is additive over any split of a chunk when every word keeps
 //     its absolute index, so a slice sums its words with their chunk-relative
@@ -161,11 +163,18 @@ __device__ __forceinline__ void add_sum(fr_chunk_sum* acc, u64 s, u64 ws) {
 
 // Geometry of the slice walk shared by the kernels.
 struct Walk {
-  u64 n_slices;       // workgroup ids to cover (units << spc_shift)
+  const u64* slots;   // slot table, XCD-major (see SlotTable)
+  u64 n_slices;       // workgroup ids to cover: slots in the table
+  u64 stride;         // entries per XCD in the table
   uint32_t sl_vec;    // vectors per slice: SL / 16
   uint32_t spc_shift; // log2(SPC), slices per chunk
   uint32_t g_shift;   // log2(G), accumulators per chunk
 };
+
+// Slot of workgroup id g: (unit << 32) | j.
+__device__ __forceinline__ u64 slot_of(const Walk& wk, u64 g) {
+  return wk.slots[(g & 7) * wk.stride + (g >> 3)];
+}
 
 constexpr uint32_t kAccSlicesShift = 4;  // 16 slices per accumulator
 
@@ -175,20 +184,19 @@ constexpr uint32_t kAccSlicesShift = 4;  // 16 slices per accumulator
 // checksum only.  Sums of the bytes read at src go to acc (zeroed), every
 // chunk's own accumulators; derived entries are read and summed only.
 template <int B, int U, bool kStore>
-__global__ __launch_bounds__(B) void k_pack(const ChunkRec* __restrict__ chunks, Walk wk,
+__global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, Walk wk,
                                             const uint8_t* __restrict__ src,
                                             uint8_t* __restrict__ payload,
                                             fr_chunk_sum* __restrict__ acc_out) {
   __shared__ u64 lds[2][B / 64][2];
   int parity = 0;
-  const uint32_t spc_mask = (1u << wk.spc_shift) - 1;
   for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
-    const uint32_t c = uint32_t(g >> wk.spc_shift);
-    const uint32_t j = uint32_t(g) & spc_mask;
-    const ChunkRec r = chunks[c];
+    const u64 e = slot_of(wk, g);
+    const SrcUnit r = units[e >> 32];
+    const uint32_t c = r.c, j = uint32_t(e);
     const uint32_t nvec = r.len >> 4, tail = r.len & 15;
     const uint32_t v0 = j * wk.sl_vec;  // first vector of the slice
-    if (v0 > nvec || (v0 == nvec && tail == 0)) continue;  // slice past the chunk's end
+    if (v0 > nvec || (v0 == nvec && tail == 0)) continue;  // guard: no listed slot is empty
     const u32x4* s = reinterpret_cast<const u32x4*>(src + r.src_off);
     const bool store = kStore && r.pay_off != kNoPayload;
     u32x4* d = reinterpret_cast<u32x4*>(payload + (store ? r.pay_off : 0));
@@ -327,18 +335,17 @@ __device__ __forceinline__ bool plain_slice(const PlainUnit& r, uint32_t j, cons
 template <int B, int U>
 __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ derived,
                                               const PlainUnit* __restrict__ plain, Walk wk,
-                                              u64 n_derived_slices, uint32_t cvec,
-                                              const uint8_t* __restrict__ payload,
+                                              uint32_t cvec, const uint8_t* __restrict__ payload,
                                               uint8_t* __restrict__ dst,
                                               fr_chunk_sum* __restrict__ acc_out) {
   __shared__ u64 lds[2][B / 64][4];
   __shared__ u64 lds2[2][B / 64][2];
   int parity = 0;
-  const uint32_t spc_mask = (1u << wk.spc_shift) - 1;
   for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
-    if (g < n_derived_slices) {
-      const DerivedUnit r = derived[g >> (wk.spc_shift + 1)];
-      const uint32_t j = uint32_t(g) & (2 * spc_mask + 1);
+    const u64 e = slot_of(wk, g);
+    if (uint32_t(e) & kSlotDerived) {
+      const DerivedUnit r = derived[e >> 32];
+      const uint32_t j = uint32_t(e) & ~kSlotDerived;
       u64 acc[4] = {0, 0, 0, 0};
       uint32_t part = 0;
       if (!derived_slice<B, U, true>(r, j, wk, cvec, payload, dst, acc, part)) continue;
@@ -353,9 +360,8 @@ __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ de
                 acc[3]);
       }
     } else {
-      const u64 h = g - n_derived_slices;
-      const PlainUnit r = plain[h >> wk.spc_shift];
-      const uint32_t j = uint32_t(h) & spc_mask;
+      const PlainUnit r = plain[e >> 32];
+      const uint32_t j = uint32_t(e);
       u64 acc[2] = {0, 0};
       if (!plain_slice<B, U>(r, j, wk, payload, dst, acc)) continue;
       block_sum<B, 2>(acc, lds2, parity);
@@ -374,10 +380,10 @@ __global__ __launch_bounds__(B) void k_rederive(const DerivedUnit* __restrict__ 
                                                 fr_chunk_sum* __restrict__ acc_out) {
   __shared__ u64 lds[2][B / 64][4];
   int parity = 0;
-  const uint32_t gmask = (2u << wk.spc_shift) - 1;
   for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
-    const DerivedUnit r = derived[g >> (wk.spc_shift + 1)];
-    const uint32_t j = uint32_t(g) & gmask;
+    const u64 e = slot_of(wk, g);
+    const DerivedUnit r = derived[e >> 32];
+    const uint32_t j = uint32_t(e) & ~kSlotDerived;
     u64 acc[4] = {0, 0, 0, 0};
     uint32_t part = 0;
     if (!derived_slice<B, U, false>(r, j, wk, cvec, dst, dst, acc, part)) continue;
@@ -392,7 +398,7 @@ __global__ __launch_bounds__(B) void k_rederive(const DerivedUnit* __restrict__ 
 // flags[c] <- 1 when any slice of chunk c differs (flags zeroed); with kSums
 // the sums of both arenas go to acc_a / acc_b (zeroed).
 template <int B, int U, bool kSums>
-__global__ __launch_bounds__(B) void k_verify(const ChunkRec* __restrict__ chunks, Walk wk,
+__global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units, Walk wk,
                                               const uint8_t* __restrict__ a,
                                               const uint8_t* __restrict__ b,
                                               uint32_t* __restrict__ flags,
@@ -400,11 +406,10 @@ __global__ __launch_bounds__(B) void k_verify(const ChunkRec* __restrict__ chunk
                                               fr_chunk_sum* __restrict__ acc_b) {
   __shared__ u64 lds[2][B / 64][4];
   int parity = 0;
-  const uint32_t spc_mask = (1u << wk.spc_shift) - 1;
   for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
-    const uint32_t c = uint32_t(g >> wk.spc_shift);
-    const uint32_t j = uint32_t(g) & spc_mask;
-    const ChunkRec r = chunks[c];
+    const u64 e = slot_of(wk, g);
+    const SrcUnit r = units[e >> 32];
+    const uint32_t c = r.c, j = uint32_t(e);
     const uint32_t nvec = r.len >> 4, tail = r.len & 15;
     const uint32_t v0 = j * wk.sl_vec;
     if (v0 > nvec || (v0 == nvec && tail == 0)) continue;
@@ -571,17 +576,19 @@ inline uint32_t grid_for(u64 units, const LaunchCfg& cfg) {
   return uint32_t(units < cap ? units : cap);
 }
 
-// Slice geometry for `units` chunks (or derived groups, two chunks' worth of
-// master slices each) of C bytes and a tile of `tile_bytes`.
-inline Walk walk_for(u64 units, uint64_t C, uint32_t tile_bytes, bool derived_group = false) {
+// Slice geometry for chunks of C bytes and a tile of `tile_bytes`, walked by
+// the slot table `t` (built for that slice size).
+inline Walk walk_for(uint64_t C, uint32_t tile_bytes, const SlotTable& t) {
   const uint64_t sl = C < tile_bytes ? C : tile_bytes;
   uint32_t sh = 0;
   while ((sl << sh) < C) sh++;
   Walk w;
+  w.slots = reinterpret_cast<const u64*>(t.d);
+  w.n_slices = t.n;
+  w.stride = t.stride;
   w.sl_vec = uint32_t(sl >> 4);
   w.spc_shift = sh;
   w.g_shift = sh > kAccSlicesShift ? sh - kAccSlicesShift : 0;
-  w.n_slices = units << (sh + (derived_group ? 1 : 0));
   return w;
 }
 
@@ -603,11 +610,11 @@ enum Tile {
 };
 
 template <int B, int U>
-int pack_impl(bool store, const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* src,
-              void* payload, fr_chunk_sum* sums, const Scratch& scr, const LaunchCfg& cfg,
-              hipStream_t st) {
+int pack_impl(bool store, const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks,
+              uint64_t C, const void* src, void* payload, fr_chunk_sum* sums, const Scratch& scr,
+              const LaunchCfg& cfg, hipStream_t st) {
   if (n_chunks == 0) return 0;
-  const Walk wk = walk_for(n_chunks, C, B * U * 16);
+  const Walk wk = walk_for(C, B * U * 16, slots);
   const u64 n_acc = u64(n_chunks) << wk.g_shift;
   Zeroes z;
   z.add(scr.acc, n_acc * sizeof(fr_chunk_sum));
@@ -617,10 +624,10 @@ int pack_impl(bool store, const ChunkRec* chunks, uint32_t n_chunks, uint64_t C,
   auto* p = static_cast<uint8_t*>(payload);
   if (store)
     hipLaunchKernelGGL((k_pack<B, U, true>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0, st,
-                       chunks, wk, s, p, scr.acc);
+                       units, wk, s, p, scr.acc);
   else
     hipLaunchKernelGGL((k_pack<B, U, false>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0,
-                       st, chunks, wk, s, p, scr.acc);
+                       st, units, wk, s, p, scr.acc);
   e = int(hipGetLastError());
   if (e) return e;
   FinalArgs f{};
@@ -633,19 +640,16 @@ int pack_impl(bool store, const ChunkRec* chunks, uint32_t n_chunks, uint64_t C,
 
 template <int B, int U>
 int unpack_impl(const UnpackArgs& u, const LaunchCfg& cfg, hipStream_t st) {
-  const Walk wd = walk_for(u.n_derived, u.C, B * U * 16, true);
-  Walk wk = walk_for(u.n_plain, u.C, B * U * 16);
+  const Walk wk = walk_for(u.C, B * U * 16, u.slots);
   const u64 n_acc = u64(u.n_chunks) << wk.g_shift;
   Zeroes z;
   z.add(u.scratch.acc, n_acc * sizeof(fr_chunk_sum));
   z.add(u.n_bad, 8);
   int e = z.launch(st);
   if (e || u.n_chunks == 0) return e;
-  const u64 n_der = wd.n_slices;
-  wk.n_slices += n_der;
   if (wk.n_slices) {
     hipLaunchKernelGGL((k_unpack<B, U>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0, st,
-                       u.derived, u.plain, wk, n_der, uint32_t(u.C >> 4),
+                       u.derived, u.plain, wk, uint32_t(u.C >> 4),
                        static_cast<const uint8_t*>(u.payload), static_cast<uint8_t*>(u.dst),
                        u.scratch.acc);
     e = int(hipGetLastError());
@@ -663,8 +667,8 @@ int unpack_impl(const UnpackArgs& u, const LaunchCfg& cfg, hipStream_t st) {
 
 template <int B, int U>
 int unpack_delta_impl(const UnpackDeltaArgs& u, const LaunchCfg& cfg, hipStream_t st) {
-  const Walk wd = walk_for(u.n_derived, u.C, B * U * 16, true);
-  const Walk wp = walk_for(u.n_plain, u.C, B * U * 16);
+  const Walk wd = walk_for(u.C, B * U * 16, u.derived_slots);
+  const Walk wp = walk_for(u.C, B * U * 16, u.plain_slots);
   const u64 n_acc = u64(u.n_ids) << wp.g_shift;
   Zeroes z;
   z.add(u.scratch.acc, n_acc * sizeof(fr_chunk_sum));
@@ -674,7 +678,7 @@ int unpack_delta_impl(const UnpackDeltaArgs& u, const LaunchCfg& cfg, hipStream_
   const uint32_t cvec = uint32_t(u.C >> 4);
   if (wp.n_slices) {  // sent chunks first: the masters the second phase reads
     hipLaunchKernelGGL((k_unpack<B, U>), dim3(grid_for<B>(wp.n_slices, cfg)), dim3(B), 0, st,
-                       static_cast<const DerivedUnit*>(nullptr), u.plain, wp, u64(0), cvec,
+                       static_cast<const DerivedUnit*>(nullptr), u.plain, wp, cvec,
                        static_cast<const uint8_t*>(u.payload), static_cast<uint8_t*>(u.dst),
                        u.scratch.acc);
     e = int(hipGetLastError());
@@ -697,10 +701,11 @@ int unpack_delta_impl(const UnpackDeltaArgs& u, const LaunchCfg& cfg, hipStream_
 }
 
 template <int B, int U>
-int verify_impl(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* a,
-                const void* b, uint32_t* bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
-                fr_chunk_sum* sums_b, const Scratch& scr, const LaunchCfg& cfg, hipStream_t st) {
-  const Walk wk = walk_for(n_chunks, C, B * U * 16);
+int verify_impl(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks, uint64_t C,
+                const void* a, const void* b, uint32_t* bitmap, uint64_t* n_diff,
+                fr_chunk_sum* sums_a, fr_chunk_sum* sums_b, const Scratch& scr,
+                const LaunchCfg& cfg, hipStream_t st) {
+  const Walk wk = walk_for(C, B * U * 16, slots);
   const u64 n_acc = u64(n_chunks) << wk.g_shift;
   Zeroes z;
   z.add(scr.flags, u64(n_chunks) * 4);
@@ -715,10 +720,10 @@ int verify_impl(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const voi
   const auto* pb = static_cast<const uint8_t*>(b);
   const dim3 grid(grid_for<B>(wk.n_slices, cfg));
   if (sums_a)
-    hipLaunchKernelGGL((k_verify<B, U, true>), grid, dim3(B), 0, st, chunks, wk, pa, pb,
+    hipLaunchKernelGGL((k_verify<B, U, true>), grid, dim3(B), 0, st, units, wk, pa, pb,
                        scr.flags, scr.acc, scr.acc_b);
   else
-    hipLaunchKernelGGL((k_verify<B, U, false>), grid, dim3(B), 0, st, chunks, wk, pa, pb,
+    hipLaunchKernelGGL((k_verify<B, U, false>), grid, dim3(B), 0, st, units, wk, pa, pb,
                        scr.flags, scr.acc, scr.acc_b);
   e = int(hipGetLastError());
   if (e) return e;
@@ -769,21 +774,22 @@ uint32_t tile_bytes(int tile) {
 }
 
 uint64_t accumulators_per_chunk(uint64_t C, int tile) {
-  const Walk w = walk_for(1, C, tile_bytes(tile));
+  const Walk w = walk_for(C, tile_bytes(tile), SlotTable{});
   return uint64_t(1) << w.g_shift;
 }
 
-int launch_pack(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* src,
-                void* payload, fr_chunk_sum* sums, const Scratch& scr, const LaunchCfg& cfg,
-                void* stream) {
-  FR_DISPATCH(cfg.tile_pack, pack_impl, true, chunks, n_chunks, C, src, payload, sums, scr, cfg,
-              hipStream_t(stream));
+int launch_pack(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks, uint64_t C,
+                const void* src, void* payload, fr_chunk_sum* sums, const Scratch& scr,
+                const LaunchCfg& cfg, void* stream) {
+  FR_DISPATCH(cfg.tile_pack, pack_impl, true, units, slots, n_chunks, C, src, payload, sums, scr,
+              cfg, hipStream_t(stream));
 }
 
-int launch_checksum(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* base,
-                    fr_chunk_sum* sums, const Scratch& scr, const LaunchCfg& cfg, void* stream) {
-  FR_DISPATCH(cfg.tile_checksum, pack_impl, false, chunks, n_chunks, C, base, nullptr, sums, scr,
-              cfg, hipStream_t(stream));
+int launch_checksum(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks, uint64_t C,
+                    const void* base, fr_chunk_sum* sums, const Scratch& scr,
+                    const LaunchCfg& cfg, void* stream) {
+  FR_DISPATCH(cfg.tile_checksum, pack_impl, false, units, slots, n_chunks, C, base, nullptr, sums,
+              scr, cfg, hipStream_t(stream));
 }
 
 int launch_unpack(const UnpackArgs& u, const LaunchCfg& cfg, void* stream) {
@@ -794,11 +800,12 @@ int launch_unpack_delta(const UnpackDeltaArgs& u, const LaunchCfg& cfg, void* st
   FR_DISPATCH(cfg.tile_unpack, unpack_delta_impl, u, cfg, hipStream_t(stream));
 }
 
-int launch_verify(const ChunkRec* chunks, uint32_t n_chunks, uint64_t C, const void* a,
-                  const void* b, uint32_t* bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
-                  fr_chunk_sum* sums_b, const Scratch& scr, const LaunchCfg& cfg, void* stream) {
-  FR_DISPATCH(cfg.tile_verify, verify_impl, chunks, n_chunks, C, a, b, bitmap, n_diff, sums_a,
-              sums_b, scr, cfg, hipStream_t(stream));
+int launch_verify(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks, uint64_t C,
+                  const void* a, const void* b, uint32_t* bitmap, uint64_t* n_diff,
+                  fr_chunk_sum* sums_a, fr_chunk_sum* sums_b, const Scratch& scr,
+                  const LaunchCfg& cfg, void* stream) {
+  FR_DISPATCH(cfg.tile_verify, verify_impl, units, slots, n_chunks, C, a, b, bitmap, n_diff,
+              sums_a, sums_b, scr, cfg, hipStream_t(stream));
 }
 
 }  // namespace fr

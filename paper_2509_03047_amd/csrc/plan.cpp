@@ -1,6 +1,7 @@
 // Plan: validation of a tensor table, the chunk / payload layout, and the
-// device tables the kernels walk (one ChunkRec per chunk, plus the unpack
-// work list).
+// device tables the kernels walk: unit records (one SrcUnit per chunk for
+// pack, checksum and replica compare; derived groups and plain chunks for
+// unpack) and the slot tables that walk them.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -154,6 +155,37 @@ static int upload(const void* src, size_t bytes, void** out) {
   return FR_OK;
 }
 
+namespace fr {
+
+void SlotBuilder::add(uint32_t unit, uint64_t bytes, uint32_t flag) {
+  const uint64_t ns = (bytes + sl - 1) / sl;
+  for (uint64_t j = 0; j < ns; j++) lin.push_back((uint64_t(unit) << 32) | flag | j);
+}
+
+void SlotBuilder::xcd_major(uint64_t* out) const {
+  const uint64_t st = stride();
+  std::fill(out, out + 8 * st, uint64_t(0));
+  for (uint64_t g = 0; g < lin.size(); g++) out[(g & 7) * st + (g >> 3)] = lin[g];
+}
+
+}  // namespace fr
+
+namespace {
+
+// Uploads a slot table built by `b` into `w`.
+int upload_walk(const SlotBuilder& b, fr_plan::Walk& w) {
+  std::vector<uint64_t> img(8 * b.stride());
+  b.xcd_major(img.data());
+  w.sl = b.sl;
+  w.t.n = b.lin.size();
+  w.t.stride = b.stride();
+  const int rc = upload(img.data(), img.size() * sizeof(uint64_t), (void**)&w.mem);
+  w.t.d = w.mem;
+  return rc;
+}
+
+}  // namespace
+
 extern "C" int fr_plan_destroy(fr_plan* p) {
   if (!p) return FR_OK;
   int prev = -1;
@@ -161,7 +193,10 @@ extern "C" int fr_plan_destroy(fr_plan* p) {
   if (p->device >= 0 && hipGetDevice(&prev) == hipSuccess && prev != p->device) {
     switched = hipSetDevice(p->device) == hipSuccess;
   }
-  if (p->d_chunks) (void)hipFree(p->d_chunks);
+  if (p->d_units) (void)hipFree(p->d_units);
+  for (auto& w : p->src_walks)
+    if (w.mem) (void)hipFree(w.mem);
+  if (p->unpack_walk.mem) (void)hipFree(p->unpack_walk.mem);
   if (p->d_derived) (void)hipFree(p->d_derived);
   if (p->d_plain) (void)hipFree(p->d_plain);
   if (p->d_scratch) (void)hipFree(p->d_scratch);
@@ -255,7 +290,45 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
     }
     p->n_derived = uint32_t(derived.size());
     p->n_plain = uint32_t(plain.size());
-    int rc2 = upload(recs.data(), recs.size() * sizeof(ChunkRec), (void**)&p->d_chunks);
+    std::vector<SrcUnit> units(recs.size());
+    for (uint64_t c = 0; c < recs.size(); c++) {
+      units[c].src_off = recs[c].src_off;
+      units[c].pay_off = recs[c].pay_off;
+      units[c].len = recs[c].len;
+      units[c].c = uint32_t(c);
+    }
+    int rc2 = upload(units.data(), units.size() * sizeof(SrcUnit), (void**)&p->d_units);
+    // Walks of pack / checksum / compare: every chunk in order, one table per
+    // slice size their tiles use.
+    for (int t : {p->cfg.tile_pack, p->cfg.tile_checksum, p->cfg.tile_verify}) {
+      const uint32_t sl = slice_bytes(C, t);
+      bool have = false;
+      for (const auto& w : p->src_walks) have = have || w.sl == sl;
+      if (have || rc2 != FR_OK) continue;
+      SlotBuilder b;
+      b.sl = sl;
+      b.lin.reserve(L.state_bytes / sl + L.n_chunks);
+      for (uint64_t c = 0; c < recs.size(); c++) b.add(uint32_t(c), recs[c].len, 0);
+      p->src_walks.emplace_back();
+      rc2 = upload_walk(b, p->src_walks.back());
+    }
+    // Walk of unpack, in payload (table) order: a derived entry's groups
+    // (their master bytes) where the entry stands, plain chunks where theirs.
+    if (rc2 == FR_OK) {
+      SlotBuilder b;
+      b.sl = slice_bytes(C, p->cfg.tile_unpack);
+      b.lin.reserve(L.payload_bytes / b.sl + L.n_chunks);
+      uint32_t id = 0, ip = 0;
+      for (uint32_t k = 0; k < n; k++) {
+        const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];
+        if (table[k].derive_from >= 0) {
+          for (uint64_t c = c0; c < c1; c++) b.add(id++, 2 * uint64_t(recs[c].len), kSlotDerived);
+        } else if (!is_master[k]) {
+          for (uint64_t c = c0; c < c1; c++) b.add(ip++, recs[c].len, 0);
+        }
+      }
+      rc2 = upload_walk(b, p->unpack_walk);
+    }
     if (rc2 == FR_OK)
       rc2 = upload(derived.data(), derived.size() * sizeof(DerivedUnit), (void**)&p->d_derived);
     if (rc2 == FR_OK)

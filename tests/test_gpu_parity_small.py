@@ -212,3 +212,35 @@ def test_every_tile_matches_oracle(tile):
             os.environ.pop("FLASHRESTORE_TILE", None)
         else:
             os.environ["FLASHRESTORE_TILE"] = old
+
+
+def test_short_last_chunks_every_slot_count():
+    """Entries whose last chunk holds every possible number of 4 KiB slices
+    (and ragged tails inside them), for plain chunks and for bf16 parameter
+    chunks derived from masters, with the receiver laid out differently from
+    the sender: the walk lists only the slices a short chunk has."""
+    from paper_2509_03047_amd import flashrestore as F
+
+    rng = np.random.default_rng(77)
+    C = 1 << 14  # four slices per chunk at the default tiles
+    numels = [1, 3, 511, 512, 513, 1023, 1024, 1025, 2047, 2048, 3071, 4095, 4096, 4097,
+              6143, 8191, 8193, 12289, 16383]
+    rows, so, do = [], 0, 0
+    for n in numels:
+        for dtype, derive in ((F.FR_BF16, len(rows) + 1), (F.FR_F32, -1), (F.FR_F32, -1)):
+            nb = n * (4 if dtype == F.FR_F32 else 2)
+            gap = 16 * int(rng.integers(0, 5))
+            rows.append((so, do + gap, n, dtype, derive))
+            so += (nb + 15) // 16 * 16
+            do += gap + (nb + 15) // 16 * 16
+    t = F.as_table(rows)
+    src = np.zeros(so, np.uint8)
+    for k, (s_off, _, n, dtype, derive) in enumerate(rows):
+        if dtype == F.FR_F32:
+            src[s_off:s_off + 4 * n] = rng.standard_normal(n).astype(np.float32).view(np.uint8)
+    for k, (s_off, _, n, dtype, derive) in enumerate(rows):
+        if derive >= 0:
+            m_off = rows[derive][0]
+            master = src[m_off:m_off + 4 * n].view(np.float32)
+            src[s_off:s_off + 2 * n] = W._bf16_round(master).view(np.uint8)
+    _check_against_oracle(t, C, src, so, do, corrupt_rng=rng, tag="short chunks")
