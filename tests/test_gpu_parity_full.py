@@ -130,6 +130,12 @@ def test_llama8b_replica_verify_flips(llama8b):
         same = np.ones(nc, bool)
         same[ids.astype(np.int64)] = False
         assert np.array_equal(g_sb.reshape(-1, 2)[same], g_sa.reshape(-1, 2)[same])
+        # a compare of sums alone would find the same set: no flipped chunk's
+        # (sum, wsum) is unchanged
+        if ids.size:
+            ii = ids.astype(np.int64)
+            moved = (g_sb.reshape(-1, 2)[ii] != g_sa.reshape(-1, 2)[ii]).any(axis=1)
+            assert moved.all(), f"checksum collisions at k={k}: {ids[~moved].tolist()}"
         del b_np
         _flip_on_device(b, pos)  # restore B
         log(f"replica verify k={k}: {len(exp)} chunks")
