@@ -216,8 +216,11 @@ int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums,
  * list order, each starting at a 16-aligned offset, every gap byte 0; listed
  * chunks of derived (bf16) entries send nothing.  With every chunk listed the
  * delta payload and sums equal fr_pack_state's.
- * All three take the list on the host; pack and unpack copy a small unit
- * table to the device on `stream` before their kernels. */
+ * All three take the list on the host.  Pack and unpack copy the list's unit
+ * records (32 or 48 bytes per chunk) to a device buffer the plan keeps, on
+ * `stream`, before their kernels; a list that needs more room than the
+ * buffer has makes the call first synchronise the device and reallocate it
+ * (an allocation: such a call cannot be captured into a graph). */
 
 /* Bytes of the delta payload for a list.  Host only. */
 int fr_delta_layout(const fr_plan* plan, const uint32_t* chunk_ids, uint64_t n_ids,

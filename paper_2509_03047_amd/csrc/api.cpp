@@ -247,22 +247,38 @@ uint64_t delta_bytes(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids) {
   return pay;
 }
 
-// Device room for the unit records of a delta call (allocated once per plan,
-// sized for a list of every chunk).
-// Device buffer for a delta call's records and slot tables (grows on demand;
-// hipFree waits for work still using the old one).
+// Device buffer for a delta call's records and slot tables.  It grows on
+// demand; before the old one is freed, the device is synchronised, since
+// work enqueued by earlier calls (on any stream) may still read it.
 int ensure_delta_buffer(fr_plan* plan, uint64_t need) {
   if (plan->d_delta && plan->delta_cap >= need) return FR_OK;
+  if (plan->d_delta) {
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return device_error(e);
+    (void)hipFree(plan->d_delta);
+    plan->d_delta = nullptr;
+    plan->delta_cap = 0;
+  }
   void* p = nullptr;
   hipError_t e = hipMalloc(&p, need);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return e == hipErrorOutOfMemory ? FR_E_NOMEM : device_error(e);
   }
-  if (plan->d_delta) (void)hipFree(plan->d_delta);
   plan->d_delta = p;
   plan->delta_cap = need;
   return FR_OK;
+}
+
+// Implicit walk over `units` chunks (derived groups: two chunks' worth of
+// master slices each) at the slice size of `tile`.
+SlotTable implicit_walk(uint64_t units, uint64_t C, int tile, bool derived) {
+  uint32_t sh = 0;
+  while ((uint64_t(slice_bytes(C, tile)) << sh) < C) sh++;
+  SlotTable t;
+  t.implicit_shift = sh + (derived ? 1 : 0);
+  t.n = units << t.implicit_shift;
+  return t;
 }
 
 int upload_records(fr_plan* plan, size_t bytes, void* stream) {
@@ -299,44 +315,34 @@ extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const 
   FR_TRY(check_disjoint(outs, 2, ins, 1));
   if (n_ids == 0) return FR_OK;
   const uint64_t C = plan->layout.C;
-  // device image: [n_ids SrcUnit records][slot table]
-  SlotBuilder b;
-  b.sl = slice_bytes(C, plan->cfg.tile_pack);
-  uint64_t tab_off = 0;
   try {
-    std::vector<SrcUnit> recs(n_ids);
-    uint64_t pay = 0;
-    for (uint64_t i = 0; i < n_ids; i++) {
-      const Where w = locate(plan, ids[i]);
-      const fr_tensor_desc& d = plan->table[w.entry];
-      SrcUnit& r = recs[i];
-      r.src_off = d.src_offset + w.j * C;
-      r.len = uint32_t(w.len);
-      r.c = uint32_t(i);
-      if (d.derive_from >= 0) {
-        r.pay_off = kNoPayload;
-      } else {
-        r.pay_off = pay;
-        pay = (pay + w.len + 15) & ~uint64_t(15);
-      }
-      b.add(uint32_t(i), w.len, 0);
-    }
-    tab_off = n_ids * sizeof(SrcUnit);
-    plan->delta_host.resize(tab_off + 8 * b.stride() * sizeof(uint64_t));
-    std::memcpy(plan->delta_host.data(), recs.data(), tab_off);
-    b.xcd_major(reinterpret_cast<uint64_t*>(plan->delta_host.data() + tab_off));
+    plan->delta_host.resize(n_ids * sizeof(SrcUnit));
   } catch (const std::bad_alloc&) {
     return FR_E_NOMEM;
   }
+  SrcUnit* recs = reinterpret_cast<SrcUnit*>(plan->delta_host.data());
+  uint64_t pay = 0;
+  for (uint64_t i = 0; i < n_ids; i++) {
+    const Where w = locate(plan, ids[i]);
+    const fr_tensor_desc& d = plan->table[w.entry];
+    SrcUnit& r = recs[i];
+    r = SrcUnit{};
+    r.src_off = d.src_offset + w.j * C;
+    r.len = uint32_t(w.len);
+    r.c = uint32_t(i);
+    if (d.derive_from >= 0) {
+      r.pay_off = kNoPayload;
+    } else {
+      r.pay_off = pay;
+      pay = (pay + w.len + 15) & ~uint64_t(15);
+    }
+  }
   FR_TRY(ensure_delta_buffer(plan, plan->delta_host.size()));
   FR_TRY(upload_records(plan, plan->delta_host.size(), stream));
-  const uint8_t* dev = static_cast<const uint8_t*>(plan->d_delta);
-  SlotTable t;
-  t.d = reinterpret_cast<const uint64_t*>(dev + tab_off);
-  t.n = b.lin.size();
-  t.stride = b.stride();
-  return launch_result(launch_pack(reinterpret_cast<const SrcUnit*>(dev), t, uint32_t(n_ids), C,
-                                   src_base, payload, sums, plan->scratch, plan->cfg, stream));
+  return launch_result(launch_pack(static_cast<const SrcUnit*>(plan->d_delta),
+                                   implicit_walk(n_ids, C, plan->cfg.tile_pack, false),
+                                   uint32_t(n_ids), C, src_base, payload, sums, plan->scratch,
+                                   plan->cfg, stream));
 }
 
 extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
@@ -358,66 +364,53 @@ extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
   const Region ins[] = {{payload, pb}, {sums, n_ids * sizeof(fr_chunk_sum)}};
   FR_TRY(check_disjoint(outs, 3, ins, 2));
   const uint64_t C = plan->layout.C;
-  // device image: [plain units][derived units][plain slots][derived slots]
-  SlotBuilder bp, bd;
-  bp.sl = bd.sl = slice_bytes(C, plan->cfg.tile_unpack);
-  uint64_t off_d = 0, off_sp = 0, off_sd = 0;
+  uint32_t n_plain = 0, n_derived = 0;
+  for (uint64_t i = 0; i < n_ids; i++)
+    (plan->table[locate(plan, ids[i]).entry].derive_from < 0 ? n_plain : n_derived)++;
   try {
-    std::vector<PlainUnit> pu;
-    std::vector<DerivedUnit> du;
-    uint64_t pay = 0;
-    for (uint64_t i = 0; i < n_ids; i++) {
-      const Where w = locate(plan, ids[i]);
-      const fr_tensor_desc& d = plan->table[w.entry];
-      if (d.derive_from < 0) {
-        PlainUnit u{};
-        u.pay_off = pay;
-        u.dst_off = d.dst_offset + w.j * C;
-        u.len = uint32_t(w.len);
-        u.c = uint32_t(i);
-        bp.add(uint32_t(pu.size()), w.len, 0);
-        pu.push_back(u);
-        pay = (pay + w.len + 15) & ~uint64_t(15);
-      } else {
-        const fr_tensor_desc& m = plan->table[d.derive_from];
-        DerivedUnit u{};
-        u.m_pay_off = m.dst_offset + 2 * w.j * C;  // the receiver's master bytes of this chunk
-        u.m_dst_off = u.m_pay_off;
-        u.p_dst_off = d.dst_offset + w.j * C;
-        u.len = uint32_t(w.len);
-        u.c = uint32_t(i);
-        bd.add(uint32_t(du.size()), 2 * w.len, kSlotDerived);
-        du.push_back(u);
-      }
-    }
-    off_d = pu.size() * sizeof(PlainUnit);
-    off_sp = off_d + du.size() * sizeof(DerivedUnit);
-    off_sd = off_sp + 8 * bp.stride() * sizeof(uint64_t);
-    plan->delta_host.resize(off_sd + 8 * bd.stride() * sizeof(uint64_t));
-    uint8_t* h = plan->delta_host.data();
-    if (!pu.empty()) std::memcpy(h, pu.data(), off_d);
-    if (!du.empty()) std::memcpy(h + off_d, du.data(), off_sp - off_d);
-    bp.xcd_major(reinterpret_cast<uint64_t*>(h + off_sp));
-    bd.xcd_major(reinterpret_cast<uint64_t*>(h + off_sd));
+    plan->delta_host.resize(n_plain * sizeof(PlainUnit) + n_derived * sizeof(DerivedUnit));
   } catch (const std::bad_alloc&) {
     return FR_E_NOMEM;
+  }
+  // device image: [plain units][derived units]
+  PlainUnit* pu = reinterpret_cast<PlainUnit*>(plan->delta_host.data());
+  DerivedUnit* du = reinterpret_cast<DerivedUnit*>(plan->delta_host.data() + n_plain * sizeof(PlainUnit));
+  uint64_t pay = 0;
+  uint32_t ip = 0, id = 0;
+  for (uint64_t i = 0; i < n_ids; i++) {
+    const Where w = locate(plan, ids[i]);
+    const fr_tensor_desc& d = plan->table[w.entry];
+    if (d.derive_from < 0) {
+      PlainUnit& u = pu[ip++];
+      u = PlainUnit{};
+      u.pay_off = pay;
+      u.dst_off = d.dst_offset + w.j * C;
+      u.len = uint32_t(w.len);
+      u.c = uint32_t(i);
+      pay = (pay + w.len + 15) & ~uint64_t(15);
+    } else {
+      const fr_tensor_desc& m = plan->table[d.derive_from];
+      DerivedUnit& u = du[id++];
+      u = DerivedUnit{};
+      u.m_pay_off = m.dst_offset + 2 * w.j * C;  // the receiver's master bytes of this chunk
+      u.m_dst_off = u.m_pay_off;
+      u.p_dst_off = d.dst_offset + w.j * C;
+      u.len = uint32_t(w.len);
+      u.c = uint32_t(i);
+    }
   }
   if (n_ids) {
     FR_TRY(ensure_delta_buffer(plan, plan->delta_host.size()));
     FR_TRY(upload_records(plan, plan->delta_host.size(), stream));
   }
-  const uint8_t* dev = static_cast<const uint8_t*>(plan->d_delta);
   UnpackDeltaArgs a{};
-  a.plain = reinterpret_cast<const PlainUnit*>(dev);
-  a.n_plain = uint32_t(off_d / sizeof(PlainUnit));
-  a.derived = reinterpret_cast<const DerivedUnit*>(dev + off_d);
-  a.n_derived = uint32_t((off_sp - off_d) / sizeof(DerivedUnit));
-  a.plain_slots.d = reinterpret_cast<const uint64_t*>(dev + off_sp);
-  a.plain_slots.n = bp.lin.size();
-  a.plain_slots.stride = bp.stride();
-  a.derived_slots.d = reinterpret_cast<const uint64_t*>(dev + off_sd);
-  a.derived_slots.n = bd.lin.size();
-  a.derived_slots.stride = bd.stride();
+  a.plain = static_cast<const PlainUnit*>(plan->d_delta);
+  a.n_plain = n_plain;
+  a.derived = reinterpret_cast<const DerivedUnit*>(static_cast<const uint8_t*>(plan->d_delta) +
+                                                   n_plain * sizeof(PlainUnit));
+  a.n_derived = n_derived;
+  a.plain_slots = implicit_walk(n_plain, C, plan->cfg.tile_unpack, false);
+  a.derived_slots = implicit_walk(n_derived, C, plan->cfg.tile_unpack, true);
   a.n_ids = uint32_t(n_ids);
   a.C = C;
   a.payload = payload;

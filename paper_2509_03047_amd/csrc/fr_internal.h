@@ -76,9 +76,14 @@ static_assert(sizeof(PlainUnit) == 32, "PlainUnit is 32 bytes");
 constexpr uint32_t kSlotDerived = 0x80000000u;
 
 struct SlotTable {
-  const uint64_t* d = nullptr;
+  const uint64_t* d = nullptr;  // NULL: implicit walk (below)
   uint64_t n = 0;       // slots (workgroups to launch)
   uint64_t stride = 0;  // ceil(n / 8); the table holds 8 * stride entries
+  // Implicit walk, for the scattered chunk lists of a delta call, which
+  // would gain nothing from a table: every unit has 2^implicit_shift slots
+  // and slot g is (g >> implicit_shift, g mod 2^implicit_shift); slots past
+  // a short unit's end do nothing.
+  uint32_t implicit_shift = 0;
 };
 
 // Host builder of a slot table (plan.cpp).

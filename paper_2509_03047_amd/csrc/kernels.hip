@@ -163,9 +163,10 @@ __device__ __forceinline__ void add_sum(fr_chunk_sum* acc, u64 s, u64 ws) {
 
 // Geometry of the slice walk shared by the kernels.
 struct Walk {
-  const u64* slots;   // slot table, XCD-major (see SlotTable)
-  u64 n_slices;       // workgroup ids to cover: slots in the table
+  const u64* slots;   // slot table, XCD-major (see SlotTable); NULL: implicit
+  u64 n_slices;       // workgroup ids to cover: slots in the walk
   u64 stride;         // entries per XCD in the table
+  uint32_t imp_shift; // implicit walk: log2 of the slots per unit
   uint32_t sl_vec;    // vectors per slice: SL / 16
   uint32_t spc_shift; // log2(SPC), slices per chunk
   uint32_t g_shift;   // log2(G), accumulators per chunk
@@ -173,7 +174,8 @@ struct Walk {
 
 // Slot of workgroup id g: (unit << 32) | j.
 __device__ __forceinline__ u64 slot_of(const Walk& wk, u64 g) {
-  return wk.slots[(g & 7) * wk.stride + (g >> 3)];
+  if (wk.slots) return wk.slots[(g & 7) * wk.stride + (g >> 3)];
+  return ((g >> wk.imp_shift) << 32) | (g & ((u64(1) << wk.imp_shift) - 1));
 }
 
 constexpr uint32_t kAccSlicesShift = 4;  // 16 slices per accumulator
@@ -586,6 +588,7 @@ inline Walk walk_for(uint64_t C, uint32_t tile_bytes, const SlotTable& t) {
   w.slots = reinterpret_cast<const u64*>(t.d);
   w.n_slices = t.n;
   w.stride = t.stride;
+  w.imp_shift = t.implicit_shift;
   w.sl_vec = uint32_t(sl >> 4);
   w.spc_shift = sh;
   w.g_shift = sh > kAccSlicesShift ? sh - kAccSlicesShift : 0;
