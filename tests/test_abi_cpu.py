@@ -175,3 +175,15 @@ def test_binding_refuses_to_run_without_the_library(tmp_path, monkeypatch):
     monkeypatch.setattr(os.path, "exists", lambda p: False if p.endswith("libflashrestore.so") else True)
     with pytest.raises(ImportError):
         spec.loader.exec_module(mod)
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """One GPU only: bench.py with --gpus above 1 exits with a message before
+    touching any device."""
+    import sys
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    p = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert p.returncode == 2
+    assert "one GPU" in p.stderr and p.stdout == ""
