@@ -244,3 +244,28 @@ def test_short_last_chunks_every_slot_count():
             master = src[m_off:m_off + 4 * n].view(np.float32)
             src[s_off:s_off + 2 * n] = W._bf16_round(master).view(np.uint8)
     _check_against_oracle(t, C, src, so, do, corrupt_rng=rng, tag="short chunks")
+
+
+def test_mixed_tiles_per_operation():
+    """Each operation with its own tile (so one plan holds several walks of
+    different slice sizes) still gives the oracle's bytes."""
+    names = ("FLASHRESTORE_TILE_PACK", "FLASHRESTORE_TILE_UNPACK", "FLASHRESTORE_TILE_VERIFY",
+             "FLASHRESTORE_TILE_CHECKSUM")
+    old = {k: os.environ.get(k) for k in names}
+    rng = np.random.default_rng(91)
+    try:
+        for combo in ((7, 1, 3, 10), (3, 7, 10, 6), (10, 8, 7, 2)):
+            for k, v in zip(names, combo):
+                os.environ[k] = str(v)
+            for it in range(4):
+                t, sb, db = W.random_tiny_table(rng, max_entries=8, max_numel=100_000)
+                C = int(rng.choice([4096, 16384, 65536]))
+                src = W.random_tiny_state(t, sb, rng)
+                _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng,
+                                      tag=f"tiles {combo} table {it} C={C}")
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
