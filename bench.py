@@ -134,6 +134,66 @@ def cpu_baseline(w, src_np, seconds: float):
     }
 
 
+def control_plane(reps=21):
+    """Host rows at the paper's cluster scale, 4,800 ranks (TP 8 x PP 4 x
+    DP 150, a 70B-class layout): step-tag tracker and restore planner
+    latencies through the Python binding (medians; microseconds).  The 8
+    ranks of one node fail in forward of step 41; every normal rank then
+    reports 41."""
+    import statistics
+
+    import numpy as np
+
+    from paper_2509_03047_amd import flashrestore as F
+    from paper_2509_03047_amd import workloads as W
+
+    tp, pp, dp = 8, 4, 150
+    layout = F.Layout3D(tp, pp, dp, 1, 0)
+    world = layout.world
+    group = [c[1] * tp + c[0] for c in (layout.coords(r) for r in range(world))]
+    failed = list(range(8 * 37, 8 * 38))  # one tensor-parallel group: a node
+    failed_set = set(failed)
+
+    def med_us(fn):
+        ts = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            fn()
+            ts.append(time.perf_counter() - t0)
+        return round(statistics.median(ts) * 1e6, 1)
+
+    tr = F.Tracker(world, group, 10.0, 0.0)
+    t0 = time.perf_counter()
+    for r in range(world):
+        tr.heartbeat(r, 41, 1.0)
+    hb_us = (time.perf_counter() - t0) / world * 1e6
+    for r in failed:
+        tr.report_failure(r, 2.0)
+    for r in range(world):
+        if r not in failed_set:
+            tr.heartbeat(r, 41, 3.0)
+    d = tr.decide(3.5)
+    donors = tr.donors(3.5)
+    ok = (d["action"] == "stop_and_restore" and d["resume_step"] == 41
+          and all(donors[r] >= 0 and group[donors[r]] == group[r] for r in failed))
+    numel = [n for _, n in W.llama3_70b_tp8_pp4_stage0_tensors()]
+    zero1 = F.Layout3D(tp, pp, dp, 6, 1)
+    out = np.zeros(world, np.int32)
+    mask = np.zeros(world, np.uint8)
+    mask[failed] = 1
+    return {
+        "ranks": world,
+        "layout": "tp8 x pp4 x dp150",
+        "tracker_heartbeat_us": round(hb_us, 2),
+        "tracker_decide_us": med_us(lambda: tr.decide(3.5)),
+        "tracker_donors_us": med_us(lambda: tr.donors_into(3.5, out)),
+        "planner_donors_us": med_us(lambda: layout.donors_into(mask, out)),
+        "planner_state_table_us": med_us(lambda: layout.state_table(failed[0], numel)),
+        "planner_state_table_zero1_us": med_us(lambda: zero1.state_table(failed[0], numel)),
+        "ok": bool(ok),
+    }
+
+
 def delta_repair(plan, donor, replica, info, k, stream, reps=5):
     """Repair of a replica that diverged in k random bits: compare, read the
     flagged set back, re-send only those chunks.  Times the GPU work of the
@@ -329,8 +389,9 @@ def main():
         "wall_s_timed": round(wall, 4),
     }
     if not args.no_delta:
-        out["delta_repair"] = delta_repair(plan, src, dst, info, args.delta_flips, stream)
+        out["delta_repair"] = delta_repair(plan, src, replica, info, args.delta_flips, stream)
         out["delta_repair"]["full_restore_ms"] = round(restore_ms, 4)
+    out["control_plane"] = control_plane()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, src_np, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -397,8 +397,14 @@ class Tracker:
 
     def donors(self, now_s: float) -> list:
         out = np.zeros(self.n_ranks, np.int32)
-        _check(_lib.fr_tracker_donors(self._h, now_s, out.ctypes.data), "fr_tracker_donors")
+        self.donors_into(now_s, out)
         return [int(x) for x in out]
+
+    def donors_into(self, now_s: float, out: np.ndarray) -> np.ndarray:
+        """donors() into a caller-owned contiguous int32 array of n_ranks."""
+        assert out.dtype == np.int32 and out.size == self.n_ranks and out.flags.c_contiguous
+        _check(_lib.fr_tracker_donors(self._h, now_s, out.ctypes.data), "fr_tracker_donors")
+        return out
 
 
 class Layout3D:
@@ -418,8 +424,17 @@ class Layout3D:
         f = np.zeros(self.world, np.uint8)
         f[list(failed)] = 1
         out = np.zeros(self.world, np.int32)
-        _check(_lib.fr_layout_donors(C.byref(self.s), f.ctypes.data, out.ctypes.data), "fr_layout_donors")
-        return [int(x) for x in out]
+        return [int(x) for x in self.donors_into(f, out)]
+
+    def donors_into(self, failed_mask: np.ndarray, out: np.ndarray) -> np.ndarray:
+        """donors() from a uint8 mask of failed ranks into a caller-owned
+        int32 array (both contiguous, one element per rank)."""
+        assert failed_mask.dtype == np.uint8 and failed_mask.size == self.world
+        assert out.dtype == np.int32 and out.size == self.world
+        assert failed_mask.flags.c_contiguous and out.flags.c_contiguous
+        _check(_lib.fr_layout_donors(C.byref(self.s), failed_mask.ctypes.data, out.ctypes.data),
+               "fr_layout_donors")
+        return out
 
     def state_table(self, rank: int, numel):
         """(table as a DESC_DTYPE array, arena bytes) of `rank`'s state."""

@@ -100,3 +100,12 @@ def test_layout_errors():
         F.Layout3D(1, 1, 4, 1, 4).coords(0)   # no ZeRO stage 4
     with pytest.raises(F.FlashRestoreError):
         F.Layout3D(2, 2, 2, 1, 0).coords(8)   # rank past the world
+
+
+def test_donors_into_equals_donors():
+    L = F.Layout3D(2, 2, 4, 2, 1)
+    failed = [0, 5, 9]
+    mask = np.zeros(L.world, np.uint8)
+    mask[failed] = 1
+    out = np.full(L.world, 99, np.int32)
+    assert L.donors_into(mask, out).tolist() == L.donors(failed)

@@ -242,3 +242,13 @@ def test_library_equals_plain_rules_on_random_events():
             assert (d["action"], d["resume_step"]) == oc.decide(now)
             assert t.failed_ranks(now) == oc.failed(now)
             assert t.donors(now) == oc.donors(now)
+
+
+def test_donors_into_equals_donors():
+    t = F.Tracker(6, [0, 0, 0, 1, 1, 1], 5.0, 0.0)
+    for r in range(6):
+        t.heartbeat(r, 2, 0.1)
+    t.report_failure(1, 0.2)
+    t.report_failure(4, 0.2)
+    out = np.full(6, 99, np.int32)
+    assert t.donors_into(0.3, out).tolist() == t.donors(0.3)
