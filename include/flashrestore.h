@@ -43,10 +43,13 @@
  *     the result is (u >> 16) | 0x0040, otherwise the nearer bf16 neighbour
  *     with ties to an even last bit, overflow to infinity, denormals rounded
  *     exactly (no flush to zero).
- *   Payload.  The bytes of every non-derived entry in table order; segment k
- *     starts at the 16-byte-aligned end of the previous one (0 for the
- *     first); every byte between segments and after the last is 0;
- *     payload_bytes = the 16-aligned end of the last segment.
+ *   Payload.  The bytes of every non-derived entry in table order; the
+ *     segment of each non-empty one starts at the first multiple of 4096 at
+ *     or after the end of the previous segment (0 for the first); an empty
+ *     entry has no segment (its offset is the end so far rounded up to 16);
+ *     payload_bytes = the end of the last segment rounded up to 16; every
+ *     byte outside the segments is 0.  (Segments on 4 KiB boundaries let
+ *     pack and unpack move whole aligned slices of the payload.)
  *   Bitmaps.  Bit c of a result set lives in 32-bit word c / 32 at bit c % 32.
  *
  * Conventions
@@ -213,9 +216,11 @@ int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums,
  *   chunk_ids  host array of n_ids global chunk ids, strictly increasing,
  *              each < n_chunks (FR_E_INVAL otherwise); n_ids may be 0
  * Delta payload: the bytes of every listed chunk of a non-derived entry, in
- * list order, each starting at a 16-aligned offset, every gap byte 0; listed
- * chunks of derived (bf16) entries send nothing.  With every chunk listed the
- * delta payload and sums equal fr_pack_state's.
+ * list order; a chunk that directly follows the previous sent chunk of its
+ * entry starts where that one ends, any other at the first multiple of 4096
+ * at or after it; the payload ends at the last chunk's end rounded up to 16;
+ * every gap byte 0.  Listed chunks of derived (bf16) entries send nothing.
+ * With every chunk listed the delta payload and sums equal fr_pack_state's.
  * All three take the list on the host.  Pack and unpack copy the list's unit
  * records (32 or 48 bytes per chunk) to a device buffer the plan keeps, on
  * `stream`, before their kernels; a list that needs more room than the

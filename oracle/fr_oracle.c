@@ -22,7 +22,10 @@
  *              (missing tail bytes read as 0);  sum = sum_i w_i mod 2^64,
  *              wsum = sum_i (i+1) w_i mod 2^64.
  *   payload    the bytes of every non-derived entry in table order, each
- *              segment starting at a multiple of 16, every gap byte 0.
+ *              segment starting at the next multiple of 4096 bytes after
+ *              the previous one ends (an empty entry has no segment), the
+ *              payload ending at the last segment's end rounded up to 16,
+ *              every gap byte 0.
  *              A bf16 entry that derives from an fp32 master is not sent;
  *              its chunk sums are.
  *   RNE        fp32 -> bf16: the nearer of the two neighbouring bf16 values,
@@ -47,6 +50,10 @@
 
 static uint64_t esize_of(uint32_t dtype) { return dtype == ORO_F32 ? 4u : 2u; }
 static uint64_t align16(uint64_t x) { return (x + 15u) & ~(uint64_t)15u; }
+/* a payload segment starts at a multiple of ORO_SEGMENT_ALIGN */
+static uint64_t align_segment(uint64_t x) {
+  return (x + ORO_SEGMENT_ALIGN - 1) & ~(uint64_t)(ORO_SEGMENT_ALIGN - 1);
+}
 
 static int host_is_little_endian(void) {
   const uint32_t one = 1;
@@ -60,7 +67,7 @@ static int host_is_little_endian(void) {
 int oro_plan(const oro_entry* t, uint32_t n, uint64_t C, uint64_t* nchunks,
              uint64_t* chunk_base, uint64_t* pay_off, uint64_t* payload_bytes) {
   if (C == 0 || (C & (C - 1)) != 0) return -1;
-  uint64_t base = 0, pay = 0;
+  uint64_t base = 0, end = 0; /* end: where the last segment so far ends */
   for (uint32_t k = 0; k < n; k++) {
     uint64_t nb = t[k].numel * esize_of(t[k].dtype);
     uint64_t nc = (nb + C - 1) / C;
@@ -69,13 +76,15 @@ int oro_plan(const oro_entry* t, uint32_t n, uint64_t C, uint64_t* nchunks,
     base += nc;
     if (t[k].derive_from >= 0) {
       pay_off[k] = ORO_NO_PAYLOAD; /* derived entries are not sent */
+    } else if (nb == 0) {
+      pay_off[k] = align16(end); /* an empty entry occupies no segment */
     } else {
-      pay_off[k] = pay; /* pay is always a multiple of 16 here */
-      pay = align16(pay + nb);
+      pay_off[k] = align_segment(end);
+      end = pay_off[k] + nb;
     }
   }
   chunk_base[n] = base;
-  *payload_bytes = pay;
+  *payload_bytes = align16(end);
   return 0;
 }
 
@@ -301,8 +310,11 @@ int oro_checksum_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_
  *
  * Re-sending only the chunks in which a replica diverged.  The caller lists
  * global chunk ids in strictly increasing order.  Delta payload: the bytes of
- * every listed chunk of a non-derived entry, in list order, each starting at
- * a 16-aligned offset, every gap byte 0; listed chunks of a derived (bf16)
+ * every listed chunk of a non-derived entry, in list order; a chunk that
+ * directly follows the previous sent chunk in its entry starts where that one
+ * ends, any other at the next multiple of ORO_SEGMENT_ALIGN; the payload ends
+ * at the last chunk's end rounded up to 16; every gap byte 0.  (With every
+ * chunk listed this is the full payload.)  Listed chunks of a derived (bf16)
  * entry send nothing.  sums[i] is the FRSUM of chunk ids[i] at the sender.
  * At the receiver the sent chunks are written first; then each listed derived
  * chunk is recomputed as RNE of the receiver's master bytes (which now hold
@@ -337,18 +349,23 @@ int oro_delta_layout(const oro_entry* t, uint32_t n, uint64_t C, const uint32_t*
   layout L;
   if (make_layout(t, n, C, &L)) return -1;
   if (!list_ok(&L, n, ids, n_ids)) { free_layout(&L); return -1; }
-  uint64_t pay = 0;
+  uint64_t end = 0;
+  int have_prev = 0;
+  chunk_loc prev = {0, 0};
   for (uint64_t i = 0; i < n_ids; i++) {
     chunk_loc w = locate(&L, n, ids[i]);
     if (t[w.entry].derive_from >= 0) {
       pay_off[i] = ORO_NO_PAYLOAD;
     } else {
       uint64_t nb = t[w.entry].numel * esize_of(t[w.entry].dtype);
-      pay_off[i] = pay;
-      pay = align16(pay + chunk_len(nb, C, w.j));
+      int follows = have_prev && prev.entry == w.entry && prev.j + 1 == w.j;
+      pay_off[i] = follows ? end : align_segment(end);
+      end = pay_off[i] + chunk_len(nb, C, w.j);
+      prev = w;
+      have_prev = 1;
     }
   }
-  *payload_bytes = pay;
+  *payload_bytes = align16(end);
   free_layout(&L);
   return 0;
 }

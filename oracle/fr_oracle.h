@@ -14,6 +14,12 @@ extern "C" {
 
 enum { ORO_F32 = 1, ORO_BF16 = 2 };
 #define ORO_NO_PAYLOAD UINT64_MAX
+/* Payload layout (a reading: the paper fixes no wire format): the sent
+ * entries' bytes in table order, each non-empty one starting at the next
+ * multiple of ORO_SEGMENT_ALIGN bytes after the previous one ends, the whole
+ * payload ending at the last entry's end rounded up to 16; every other byte
+ * 0.  An empty entry's offset is the end so far rounded up to 16. */
+#define ORO_SEGMENT_ALIGN 4096u
 
 typedef struct {
   uint64_t src_offset; /* byte offset in the sender / replica arena */

@@ -10,6 +10,11 @@ from __future__ import annotations
 from fractions import Fraction
 
 M64 = (1 << 64) - 1
+SEGMENT = 4096  # a payload segment starts at a multiple of this
+
+
+def _up(x, a):
+    return -(-x // a) * a
 
 
 def frsum(b: bytes):
@@ -57,17 +62,19 @@ def _esize(dt):
 
 def plan(table, C):
     nch, base, pay = [], [0], []
-    p = 0
+    end = 0
     for e in table:
         nb = int(e["numel"]) * _esize(int(e["dtype"]))
         nch.append(-(-nb // C))
         base.append(base[-1] + nch[-1])
         if int(e["derive_from"]) >= 0:
             pay.append(None)
+        elif nb == 0:
+            pay.append(_up(end, 16))  # an empty entry occupies no segment
         else:
-            pay.append(p)
-            p += -(-nb // 16) * 16
-    return nch, base, pay, p
+            pay.append(_up(end, SEGMENT))
+            end = pay[-1] + nb
+    return nch, base, pay, _up(end, 16)
 
 
 def _chunks(table, C, arena: bytes, key):
@@ -132,29 +139,46 @@ def _chunk_bytes(table, C, k, j, arena, key):
     return o, min(C, nb - j * C)
 
 
-def pack_chunks(table, C, src: bytes, ids):
+def _delta_offsets(table, C, ids):
+    """Payload offset of each listed chunk (None if derived) and the payload
+    size: a chunk right after the previous sent chunk of its entry follows it,
+    any other starts at the next segment boundary."""
     cmap = _chunk_map(table, C)
-    payload = bytearray()
-    sums = []
+    offs, end, prev = [], 0, None
     for c in ids:
         k, j = cmap[c]
+        if int(table[k]["derive_from"]) >= 0:
+            offs.append(None)
+            continue
+        _, ln = _chunk_bytes(table, C, k, j, None, "src_offset")
+        offs.append(end if prev == (k, j - 1) else _up(end, SEGMENT))
+        end = offs[-1] + ln
+        prev = (k, j)
+    return offs, _up(end, 16)
+
+
+def pack_chunks(table, C, src: bytes, ids):
+    cmap = _chunk_map(table, C)
+    offs, size = _delta_offsets(table, C, ids)
+    payload = bytearray(size)
+    sums = []
+    for c, off in zip(ids, offs):
+        k, j = cmap[c]
         o, ln = _chunk_bytes(table, C, k, j, src, "src_offset")
-        if int(table[k]["derive_from"]) < 0:
-            payload += src[o:o + ln]
-            payload += bytes(-len(payload) % 16)
+        if off is not None:
+            payload[off:off + ln] = src[o:o + ln]
         sums.append(frsum(src[o:o + ln]))
     return bytes(payload), sums
 
 
 def unpack_chunks(table, C, payload: bytes, sums, ids, dst: bytearray):
     cmap = _chunk_map(table, C)
-    pos = 0
-    for c in ids:
+    offs, _ = _delta_offsets(table, C, ids)
+    for c, off in zip(ids, offs):
         k, j = cmap[c]
-        if int(table[k]["derive_from"]) < 0:
+        if off is not None:
             o, ln = _chunk_bytes(table, C, k, j, dst, "dst_offset")
-            dst[o:o + ln] = payload[pos:pos + ln]
-            pos += -(-ln // 16) * 16
+            dst[o:o + ln] = payload[off:off + ln]
     for c in ids:
         k, j = cmap[c]
         s = int(table[k]["derive_from"])

@@ -238,13 +238,29 @@ Where locate(const fr_plan* plan, uint32_t c) {
   return Where{k, j, std::min<uint64_t>(C, nb - j * C)};
 }
 
-uint64_t delta_bytes(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids) {
-  uint64_t pay = 0;
+// Delta payload layout: the listed chunks of sent entries in list order; a
+// chunk right after the previous sent chunk of its entry follows it (that
+// one is whole, so it ends on a multiple of C), any other starts at the next
+// segment boundary; the payload ends at the last chunk's end rounded up to
+// 16.  Returns the payload bytes; with `off`, each list position's offset
+// (kNoPayload for a derived chunk).
+uint64_t delta_layout(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids,
+                      std::vector<uint64_t>* off) {
+  uint64_t end = 0;
+  bool have_prev = false;
+  Where prev{};
+  if (off) off->assign(n_ids, kNoPayload);
   for (uint64_t i = 0; i < n_ids; i++) {
     const Where w = locate(plan, ids[i]);
-    if (plan->table[w.entry].derive_from < 0) pay = (pay + w.len + 15) & ~uint64_t(15);
+    if (plan->table[w.entry].derive_from >= 0) continue;
+    const bool follows = have_prev && prev.entry == w.entry && prev.j + 1 == w.j;
+    const uint64_t at = follows ? end : (end + kSegmentAlign - 1) & ~(kSegmentAlign - 1);
+    if (off) (*off)[i] = at;
+    end = at + w.len;
+    prev = w;
+    have_prev = true;
   }
-  return pay;
+  return (end + 15) & ~uint64_t(15);
 }
 
 // Device buffer for a delta call's records and slot tables.  It grows on
@@ -294,7 +310,7 @@ extern "C" int fr_delta_layout(const fr_plan* plan, const uint32_t* ids, uint64_
                                uint64_t* payload_bytes) {
   if (!plan || !payload_bytes) return FR_E_INVAL;
   FR_TRY(check_list(plan, ids, n_ids));
-  *payload_bytes = delta_bytes(plan, ids, n_ids);
+  *payload_bytes = delta_layout(plan, ids, n_ids, nullptr);
   return FR_OK;
 }
 
@@ -304,7 +320,7 @@ extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const 
   if (!cplan) return FR_E_INVAL;
   fr_plan* plan = const_cast<fr_plan*>(cplan);  // the plan's delta staging is mutable state
   FR_TRY(check_list(plan, ids, n_ids));
-  const uint64_t pb = delta_bytes(plan, ids, n_ids);
+  const uint64_t pb = delta_layout(plan, ids, n_ids, nullptr);
   if (payload_cap < pb) return FR_E_RANGE;
   FR_TRY(check_device_and_stream(plan, stream));
   FR_TRY(check_buffer(plan, src_base, plan->src_arena_bytes, 16));
@@ -315,14 +331,15 @@ extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const 
   FR_TRY(check_disjoint(outs, 2, ins, 1));
   if (n_ids == 0) return FR_OK;
   const uint64_t C = plan->layout.C;
+  std::vector<uint64_t> off;
   try {
+    delta_layout(plan, ids, n_ids, &off);
     plan->delta_host.resize(n_ids * sizeof(SrcUnit));
   } catch (const std::bad_alloc&) {
     return FR_E_NOMEM;
   }
   SrcUnit* recs = reinterpret_cast<SrcUnit*>(plan->delta_host.data());
-  uint64_t pay = 0;
-  for (uint64_t i = 0; i < n_ids; i++) {
+  for (uint64_t i = 0, last_sent = n_ids; i < n_ids; i++) {
     const Where w = locate(plan, ids[i]);
     const fr_tensor_desc& d = plan->table[w.entry];
     SrcUnit& r = recs[i];
@@ -330,12 +347,13 @@ extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const 
     r.src_off = d.src_offset + w.j * C;
     r.len = uint32_t(w.len);
     r.c = uint32_t(i);
-    if (d.derive_from >= 0) {
-      r.pay_off = kNoPayload;
-    } else {
-      r.pay_off = pay;
-      pay = (pay + w.len + 15) & ~uint64_t(15);
+    r.pay_off = off[i];
+    if (off[i] == kNoPayload) continue;
+    if (last_sent < n_ids) {  // the previous sent chunk zero-fills up to this one
+      SrcUnit& p = recs[last_sent];
+      p.gap_v = uint32_t((off[i] - ((p.pay_off + p.len + 15) & ~uint64_t(15))) >> 4);
     }
+    last_sent = i;
   }
   FR_TRY(ensure_delta_buffer(plan, plan->delta_host.size()));
   FR_TRY(upload_records(plan, plan->delta_host.size(), stream));
@@ -352,7 +370,7 @@ extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
   if (!cplan || !n_bad) return FR_E_INVAL;
   fr_plan* plan = const_cast<fr_plan*>(cplan);
   FR_TRY(check_list(plan, ids, n_ids));
-  const uint64_t pb = delta_bytes(plan, ids, n_ids);
+  const uint64_t pb = delta_layout(plan, ids, n_ids, nullptr);
   const uint64_t words = (n_ids + 31) / 32;
   FR_TRY(check_device_and_stream(plan, stream));
   FR_TRY(check_buffer(plan, payload, pb, 16));
@@ -365,9 +383,10 @@ extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
   FR_TRY(check_disjoint(outs, 3, ins, 2));
   const uint64_t C = plan->layout.C;
   uint32_t n_plain = 0, n_derived = 0;
-  for (uint64_t i = 0; i < n_ids; i++)
-    (plan->table[locate(plan, ids[i]).entry].derive_from < 0 ? n_plain : n_derived)++;
+  std::vector<uint64_t> off;
   try {
+    delta_layout(plan, ids, n_ids, &off);
+    for (uint64_t i = 0; i < n_ids; i++) (off[i] == kNoPayload ? n_derived : n_plain)++;
     plan->delta_host.resize(n_plain * sizeof(PlainUnit) + n_derived * sizeof(DerivedUnit));
   } catch (const std::bad_alloc&) {
     return FR_E_NOMEM;
@@ -375,7 +394,6 @@ extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
   // device image: [plain units][derived units]
   PlainUnit* pu = reinterpret_cast<PlainUnit*>(plan->delta_host.data());
   DerivedUnit* du = reinterpret_cast<DerivedUnit*>(plan->delta_host.data() + n_plain * sizeof(PlainUnit));
-  uint64_t pay = 0;
   uint32_t ip = 0, id = 0;
   for (uint64_t i = 0; i < n_ids; i++) {
     const Where w = locate(plan, ids[i]);
@@ -383,11 +401,10 @@ extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
     if (d.derive_from < 0) {
       PlainUnit& u = pu[ip++];
       u = PlainUnit{};
-      u.pay_off = pay;
+      u.pay_off = off[i];
       u.dst_off = d.dst_offset + w.j * C;
       u.len = uint32_t(w.len);
       u.c = uint32_t(i);
-      pay = (pay + w.len + 15) & ~uint64_t(15);
     } else {
       const fr_tensor_desc& m = plan->table[d.derive_from];
       DerivedUnit& u = du[id++];

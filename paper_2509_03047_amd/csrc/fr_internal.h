@@ -10,6 +10,11 @@
 namespace fr {
 
 constexpr uint64_t kNoPayload = ~uint64_t(0);
+// A payload segment (an entry, or a run of consecutive chunks of a delta
+// list) starts at a multiple of kSegmentAlign bytes: the slices of a segment
+// then start at 4 KiB boundaries of the payload, which on MI355X makes pack
+// up to a fifth faster on tables of many small or oddly placed tensors.
+constexpr uint64_t kSegmentAlign = 4096;
 constexpr uint32_t kNoMaster = 0xFFFFFFFFu;
 
 // One record per global chunk id (host side; the device tables are built
@@ -34,7 +39,8 @@ struct alignas(16) SrcUnit {
   uint64_t pay_off;  // chunk start in the payload; kNoPayload: read and summed only
   uint32_t len;      // bytes in this chunk (<= C, even)
   uint32_t c;        // its sums slot: global chunk id, or list position for a delta
-  uint64_t pad_;
+  uint32_t gap_v;    // zero vectors pack writes after the chunk's 16-byte-padded end
+  uint32_t pad_;     //   (the gap up to the next segment; < kSegmentAlign / 16)
 };
 static_assert(sizeof(SrcUnit) == 32, "SrcUnit is 32 bytes");
 

@@ -222,6 +222,12 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
       acc4(t, 4 * nvec, acc[0], acc[1]);
       if (store) d[nvec] = t;  // the segment's zero padding is written with it
     }
+    // The chunk's last slice zero-fills the gap up to the next payload
+    // segment (fewer than 256 vectors).
+    const uint32_t endv = nvec + (tail ? 1u : 0u);
+    if (store && r.gap_v && v0 + wk.sl_vec >= endv) {
+      for (uint32_t v = endv + threadIdx.x; v < endv + r.gap_v; v += B) st_nt(u32x4{0, 0, 0, 0}, d + v);
+    }
     block_sum<B, 2>(acc, lds, parity);
     if (threadIdx.x == 0)
       add_sum(acc_out + ((u64(c) << wk.g_shift) + (j >> kAccSlicesShift)), acc[0], acc[1]);

@@ -24,6 +24,7 @@ constexpr uint32_t kDefaultTilePack = 4, kDefaultTileUnpack = 5, kDefaultTileVer
 
 static uint64_t esize(uint32_t dtype) { return dtype == FR_F32 ? 4 : 2; }
 static uint64_t align16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
+static uint64_t align_segment(uint64_t x) { return (x + kSegmentAlign - 1) & ~(kSegmentAlign - 1); }
 
 int validate_and_layout(const fr_tensor_desc* t, uint32_t n, uint64_t C, uint64_t src_bytes,
                         uint64_t dst_bytes, Layout* L) {
@@ -70,22 +71,24 @@ int validate_and_layout(const fr_tensor_desc* t, uint32_t n, uint64_t C, uint64_
   L->C = C;
   L->pay_off.assign(n, 0);
   L->chunk_base.assign(size_t(n) + 1, 0);
-  uint64_t base = 0, pay = 0;
+  uint64_t base = 0, end = 0;  // end of the last payload segment so far
   for (uint32_t k = 0; k < n; k++) {
     uint64_t nb = t[k].numel * esize(t[k].dtype);
     L->chunk_base[k] = base;
     base += (nb + C - 1) / C;
     if (t[k].derive_from >= 0) {
       L->pay_off[k] = kNoPayload;
+    } else if (nb == 0) {
+      L->pay_off[k] = align16(end);  // an empty entry occupies no segment
     } else {
-      L->pay_off[k] = pay;
-      pay = align16(pay + nb);
+      L->pay_off[k] = align_segment(end);
+      end = L->pay_off[k] + nb;
     }
   }
   L->chunk_base[n] = base;
   if (base > 0xFFFFFFFFull) return FR_E_RANGE;  // chunk ids are 32-bit
   L->n_chunks = base;
-  L->payload_bytes = pay;
+  L->payload_bytes = align16(end);
   L->state_bytes = state;
   return FR_OK;
 }
@@ -296,6 +299,15 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
       units[c].pay_off = recs[c].pay_off;
       units[c].len = recs[c].len;
       units[c].c = uint32_t(c);
+    }
+    // The last chunk of each sent entry zero-fills the gap to the next one.
+    for (uint32_t k = 0, prev = UINT32_MAX; k < n; k++) {
+      if (L.pay_off[k] == kNoPayload || L.chunk_base[k + 1] == L.chunk_base[k]) continue;
+      if (prev != UINT32_MAX) {
+        SrcUnit& u = units[L.chunk_base[prev + 1] - 1];
+        u.gap_v = uint32_t((L.pay_off[k] - align16(u.pay_off + u.len)) >> 4);
+      }
+      prev = k;
     }
     int rc2 = upload(units.data(), units.size() * sizeof(SrcUnit), (void**)&p->d_units);
     // Walks of pack / checksum / compare: every chunk in order, one table per

@@ -52,15 +52,20 @@ def test_repair_from_the_flagged_chunks_restores_the_donor():
         W.apply_flips(recv, W.flip_positions(donor.size * 8, k, 4000 + k))
         ids, pay, fixed, nbad = _repair(t, C, donor, recv)
         assert nbad == 0 and np.array_equal(fixed, donor)
-        # the wire holds exactly the listed chunks of sent (non-derived) entries
+        # the wire holds exactly the listed chunks of sent (non-derived)
+        # entries: a chunk right after the previous sent chunk of its entry
+        # follows it, any other starts at a 4 KiB boundary; the end is
+        # rounded up to 16
         _, base, _, _ = cpu.plan(t, C)
-        expect = 0
+        end, prev = 0, None
         for c in ids:
             e = int(np.searchsorted(base, int(c), side="right") - 1)
             if int(t[e]["derive_from"]) < 0:
                 j = int(c) - int(base[e])
-                expect += -(-min(C, int(sizes[e]) - j * C) // 16) * 16
-        assert pay.size == expect
+                start = end if prev == (e, j - 1) else -(-end // 4096) * 4096
+                end = start + min(C, int(sizes[e]) - j * C)
+                prev = (e, j)
+        assert pay.size == -(-end // 16) * 16
 
 
 def test_param_only_divergence_sends_nothing_and_rederives():

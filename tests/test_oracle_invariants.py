@@ -33,11 +33,14 @@ def toy():
 
 def test_toy_sizes_closed_form(toy):
     w, src = toy
-    # 3,671,296 params; 14 B of state and 12 B of payload per param
+    # 3,671,296 params; 14 B of state and 12 B of payload per param, the
+    # payload's 3 x 28 sent tensors each starting at a multiple of 4 KiB:
+    # the five 256-element norms (1 KiB per array) leave 3 KiB gaps, except
+    # after the last entry (the final norm's v, ending the payload)
     assert w.n_params == 3_671_296
     assert w.state_bytes == 14 * w.n_params == w.src_arena_bytes
     nch, base, pay, pb = cpu.plan(w.table, w.chunk_bytes)
-    assert pb == 12 * w.n_params
+    assert pb == 12 * w.n_params + (5 * 3 - 1) * 3072
     assert int(base[-1]) == 804
 
 
@@ -64,8 +67,10 @@ def test_payload_is_concatenation_with_zero_padding():
             if int(e["derive_from"]) >= 0:
                 continue
             o, n = int(e["src_offset"]), _nbytes(e)
-            exp += src[o:o + n].tobytes()
-            exp += bytes(-len(exp) % 16)
+            if n:  # each non-empty segment at a 4 KiB boundary
+                exp += bytes(-len(exp) % 4096)
+                exp += src[o:o + n].tobytes()
+        exp += bytes(-len(exp) % 16)
         assert payload.tobytes() == bytes(exp)
 
 
