@@ -226,41 +226,43 @@ struct Where {
   uint64_t len;  // chunk bytes
 };
 
-Where locate(const fr_plan* plan, uint32_t c) {
-  const std::vector<uint64_t>& base = plan->layout.chunk_base;
-  // the entry k with base[k] <= c < base[k + 1]
-  const auto it = std::upper_bound(base.begin(), base.end() - 1, uint64_t(c));
-  const uint32_t k = uint32_t(it - base.begin()) - 1;
-  const fr_tensor_desc& d = plan->table[k];
-  const uint64_t nb = d.numel * (d.dtype == FR_F32 ? 4 : 2);
-  const uint64_t j = c - base[k];
-  const uint64_t C = plan->layout.C;
-  return Where{k, j, std::min<uint64_t>(C, nb - j * C)};
-}
-
 // Delta payload layout: the listed chunks of sent entries in list order; a
 // chunk right after the previous sent chunk of its entry follows it (that
 // one is whole, so it ends on a multiple of C), any other starts at the next
 // segment boundary; the payload ends at the last chunk's end rounded up to
-// 16.  Returns the payload bytes; with `off`, each list position's offset
-// (kNoPayload for a derived chunk).
-uint64_t delta_layout(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids,
-                      std::vector<uint64_t>* off) {
+// 16.  Ids are strictly increasing (checked before), so one pass over the
+// entries locates them all.
+struct DeltaList {
+  std::vector<Where> where;   // per list position
+  std::vector<uint64_t> off;  // payload offset per list position (kNoPayload: derived)
+  uint64_t bytes = 0;         // payload bytes
+};
+
+void delta_layout(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids, DeltaList* out) {
+  const std::vector<uint64_t>& base = plan->layout.chunk_base;
+  const uint64_t C = plan->layout.C;
+  out->where.resize(n_ids);
+  out->off.assign(n_ids, kNoPayload);
   uint64_t end = 0;
   bool have_prev = false;
   Where prev{};
-  if (off) off->assign(n_ids, kNoPayload);
+  uint32_t k = 0;
   for (uint64_t i = 0; i < n_ids; i++) {
-    const Where w = locate(plan, ids[i]);
-    if (plan->table[w.entry].derive_from >= 0) continue;
+    while (base[k + 1] <= ids[i]) k++;  // the entry with base[k] <= id < base[k + 1]
+    const fr_tensor_desc& d = plan->table[k];
+    const uint64_t nb = d.numel * (d.dtype == FR_F32 ? 4 : 2);
+    const uint64_t j = ids[i] - base[k];
+    const Where w{k, j, std::min<uint64_t>(C, nb - j * C)};
+    out->where[i] = w;
+    if (d.derive_from >= 0) continue;
     const bool follows = have_prev && prev.entry == w.entry && prev.j + 1 == w.j;
     const uint64_t at = follows ? end : (end + kSegmentAlign - 1) & ~(kSegmentAlign - 1);
-    if (off) (*off)[i] = at;
+    out->off[i] = at;
     end = at + w.len;
     prev = w;
     have_prev = true;
   }
-  return (end + 15) & ~uint64_t(15);
+  out->bytes = (end + 15) & ~uint64_t(15);
 }
 
 // Device buffer for a delta call's records and slot tables.  It grows on
@@ -310,7 +312,13 @@ extern "C" int fr_delta_layout(const fr_plan* plan, const uint32_t* ids, uint64_
                                uint64_t* payload_bytes) {
   if (!plan || !payload_bytes) return FR_E_INVAL;
   FR_TRY(check_list(plan, ids, n_ids));
-  *payload_bytes = delta_layout(plan, ids, n_ids, nullptr);
+  DeltaList dl;
+  try {
+    delta_layout(plan, ids, n_ids, &dl);
+  } catch (const std::bad_alloc&) {
+    return FR_E_NOMEM;
+  }
+  *payload_bytes = dl.bytes;
   return FR_OK;
 }
 
@@ -320,7 +328,13 @@ extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const 
   if (!cplan) return FR_E_INVAL;
   fr_plan* plan = const_cast<fr_plan*>(cplan);  // the plan's delta staging is mutable state
   FR_TRY(check_list(plan, ids, n_ids));
-  const uint64_t pb = delta_layout(plan, ids, n_ids, nullptr);
+  DeltaList dl;
+  try {
+    delta_layout(plan, ids, n_ids, &dl);
+  } catch (const std::bad_alloc&) {
+    return FR_E_NOMEM;
+  }
+  const uint64_t pb = dl.bytes;
   if (payload_cap < pb) return FR_E_RANGE;
   FR_TRY(check_device_and_stream(plan, stream));
   FR_TRY(check_buffer(plan, src_base, plan->src_arena_bytes, 16));
@@ -331,27 +345,24 @@ extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const 
   FR_TRY(check_disjoint(outs, 2, ins, 1));
   if (n_ids == 0) return FR_OK;
   const uint64_t C = plan->layout.C;
-  std::vector<uint64_t> off;
   try {
-    delta_layout(plan, ids, n_ids, &off);
     plan->delta_host.resize(n_ids * sizeof(SrcUnit));
   } catch (const std::bad_alloc&) {
     return FR_E_NOMEM;
   }
   SrcUnit* recs = reinterpret_cast<SrcUnit*>(plan->delta_host.data());
   for (uint64_t i = 0, last_sent = n_ids; i < n_ids; i++) {
-    const Where w = locate(plan, ids[i]);
-    const fr_tensor_desc& d = plan->table[w.entry];
+    const Where& w = dl.where[i];
     SrcUnit& r = recs[i];
     r = SrcUnit{};
-    r.src_off = d.src_offset + w.j * C;
+    r.src_off = plan->table[w.entry].src_offset + w.j * C;
     r.len = uint32_t(w.len);
     r.c = uint32_t(i);
-    r.pay_off = off[i];
-    if (off[i] == kNoPayload) continue;
+    r.pay_off = dl.off[i];
+    if (dl.off[i] == kNoPayload) continue;
     if (last_sent < n_ids) {  // the previous sent chunk zero-fills up to this one
       SrcUnit& p = recs[last_sent];
-      p.gap_v = uint32_t((off[i] - ((p.pay_off + p.len + 15) & ~uint64_t(15))) >> 4);
+      p.gap_v = uint32_t((dl.off[i] - ((p.pay_off + p.len + 15) & ~uint64_t(15))) >> 4);
     }
     last_sent = i;
   }
@@ -370,7 +381,13 @@ extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
   if (!cplan || !n_bad) return FR_E_INVAL;
   fr_plan* plan = const_cast<fr_plan*>(cplan);
   FR_TRY(check_list(plan, ids, n_ids));
-  const uint64_t pb = delta_layout(plan, ids, n_ids, nullptr);
+  DeltaList dl;
+  try {
+    delta_layout(plan, ids, n_ids, &dl);
+  } catch (const std::bad_alloc&) {
+    return FR_E_NOMEM;
+  }
+  const uint64_t pb = dl.bytes;
   const uint64_t words = (n_ids + 31) / 32;
   FR_TRY(check_device_and_stream(plan, stream));
   FR_TRY(check_buffer(plan, payload, pb, 16));
@@ -383,10 +400,8 @@ extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
   FR_TRY(check_disjoint(outs, 3, ins, 2));
   const uint64_t C = plan->layout.C;
   uint32_t n_plain = 0, n_derived = 0;
-  std::vector<uint64_t> off;
+  for (uint64_t i = 0; i < n_ids; i++) (dl.off[i] == kNoPayload ? n_derived : n_plain)++;
   try {
-    delta_layout(plan, ids, n_ids, &off);
-    for (uint64_t i = 0; i < n_ids; i++) (off[i] == kNoPayload ? n_derived : n_plain)++;
     plan->delta_host.resize(n_plain * sizeof(PlainUnit) + n_derived * sizeof(DerivedUnit));
   } catch (const std::bad_alloc&) {
     return FR_E_NOMEM;
@@ -396,12 +411,12 @@ extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
   DerivedUnit* du = reinterpret_cast<DerivedUnit*>(plan->delta_host.data() + n_plain * sizeof(PlainUnit));
   uint32_t ip = 0, id = 0;
   for (uint64_t i = 0; i < n_ids; i++) {
-    const Where w = locate(plan, ids[i]);
+    const Where& w = dl.where[i];
     const fr_tensor_desc& d = plan->table[w.entry];
     if (d.derive_from < 0) {
       PlainUnit& u = pu[ip++];
       u = PlainUnit{};
-      u.pay_off = off[i];
+      u.pay_off = dl.off[i];
       u.dst_off = d.dst_offset + w.j * C;
       u.len = uint32_t(w.len);
       u.c = uint32_t(i);
