@@ -35,7 +35,8 @@ class Restore:
     def __init__(self, table, chunk_bytes, src_bytes, dst_bytes, canary=0xA5):
         self.plan = F.Plan(table, chunk_bytes, src_bytes, dst_bytes)
         self.src_bytes, self.dst_bytes = src_bytes, dst_bytes
-        self.payload = self.plan.empty_payload()
+        # pack must write every payload byte, padding and gaps included
+        self.payload = self.plan.empty_payload().fill_(0xEE)
         self.sums = self.plan.empty_sums()
         self.dst = torch.full((max(dst_bytes, 1),), canary, dtype=torch.uint8, device="cuda")
         self.bad = self.plan.empty_bitmap()

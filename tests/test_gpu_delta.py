@@ -30,7 +30,7 @@ def _one(t, C, src_np, recv_np, ids, rng, tag):
     pb = plan.delta_layout(ids)
     off, opb = cpu.delta_layout(t, C, ids)
     assert pb == opb, tag
-    payload = torch.empty(max(pb, 16), dtype=torch.uint8, device="cuda")
+    payload = torch.full((max(pb, 16),), 0xEE, dtype=torch.uint8, device="cuda")  # gaps must be written
     sums = torch.empty(max(ids.size, 1), 2, dtype=torch.int64, device="cuda")
     plan.pack_chunks(src, ids, payload, sums)
     opay, osums = cpu.pack_chunks(t, C, src_np, ids)
@@ -96,8 +96,8 @@ def test_listing_every_chunk_equals_the_full_pack():
     plan = F.Plan(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
     ids = np.arange(plan.n_chunks, dtype=np.uint32)
     assert plan.delta_layout(ids) == plan.payload_bytes
-    p1, s1 = plan.empty_payload(), plan.empty_sums()
-    p2, s2 = plan.empty_payload(), plan.empty_sums()
+    p1, s1 = plan.empty_payload().fill_(0xEE), plan.empty_sums()
+    p2, s2 = plan.empty_payload().fill_(0x11), plan.empty_sums()
     plan.pack(src, p1, s1)
     plan.pack_chunks(src, ids, p2, s2)
     torch.cuda.synchronize()
@@ -135,7 +135,7 @@ def test_repair_llama8b_share_from_the_flagged_chunks():
     ids = F.bitmap_indices(diff, plan.n_chunks).astype(np.uint32)
     assert ids.size == int(ndiff.item()) == 4060
     pb = plan.delta_layout(ids)
-    payload = torch.empty(pb, dtype=torch.uint8, device="cuda")
+    payload = torch.full((pb,), 0xEE, dtype=torch.uint8, device="cuda")
     sums = torch.empty(ids.size, 2, dtype=torch.int64, device="cuda")
     plan.pack_chunks(donor, ids, payload, sums)
     opay, osums = cpu.pack_chunks(t, C, donor_np, ids)

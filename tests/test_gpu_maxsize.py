@@ -38,7 +38,7 @@ def test_one_gib_chunks():
     plan = F.Plan(t, C, arena, arena)
     assert plan.n_chunks == 2 + 1 + 1
     src = torch.from_numpy(src_np).to("cuda")
-    payload, sums = plan.empty_payload(), plan.empty_sums()
+    payload, sums = plan.empty_payload().fill_(0xEE), plan.empty_sums()
     dst = torch.full((arena,), 0x3C, dtype=torch.uint8, device="cuda")
     bad, nbad = plan.empty_bitmap(), plan.empty_counter()
     plan.pack(src, payload, sums)
