@@ -11,8 +11,8 @@
  * instead of from a checkpoint (Section III-B item 3; Section III-E,
  * "Model states Restoration"), and the restored replica must be consistent
  * with the others again (Section III-A: data parallelism keeps model copies
- * consistent).  The paper fixes nothing below the level of "copy the
- * replica's state"; every format detail here is a reading, listed in the
+ * consistent).  The paper fixes nothing below the level of copying the
+ * replica's state; every format detail here is a reading, listed in the
  * design notes:
  *
  *   chunking   each tensor entry is cut into ceil(nbytes / C) byte chunks,
