@@ -131,7 +131,7 @@ extern "C" int fr_layout_query(const fr_tensor_desc* table, uint32_t n, uint64_t
   }
   if (rc != FR_OK) return rc;
   fill_info(L, n, src_bytes, dst_bytes, -1, info);
-  if (payload_offset) std::memcpy(payload_offset, L.pay_off.data(), sizeof(uint64_t) * n);
+  if (payload_offset && n) std::memcpy(payload_offset, L.pay_off.data(), sizeof(uint64_t) * n);
   if (chunk_base) std::memcpy(chunk_base, L.chunk_base.data(), sizeof(uint64_t) * (size_t(n) + 1));
   return FR_OK;
 }
