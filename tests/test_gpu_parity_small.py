@@ -269,3 +269,53 @@ def test_mixed_tiles_per_operation():
                 os.environ.pop(k, None)
             else:
                 os.environ[k] = v
+
+
+def test_random_midsize_tables_restore_compare_and_delta():
+    """Mid-size random tables (up to 300 entries, chunks of many slices,
+    derived groups, scattered layouts): whole restore and compare against the
+    oracle, then a delta repair of random chunks, also against the oracle."""
+    from paper_2509_03047_amd import flashrestore as F
+
+    rng = np.random.default_rng(1234)
+    for it in range(6):
+        t, sb, db = W.random_tiny_table(rng, max_entries=300, max_numel=60_000)
+        C = int(rng.choice([1024, 4096, 16384, 65536, 1 << 18]))
+        src = W.random_tiny_state(t, sb, rng)
+        log(f"midsize table {it}: {len(t)} entries, C={C}, {sb} bytes")
+        _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"midsize {it} C={C}")
+        # delta: re-send a random subset of chunks into a receiver holding the
+        # oracle's full restore with those chunks scrambled
+        plan = F.Plan(t, C, sb, db)
+        n = plan.n_chunks
+        if n == 0:
+            continue
+        ids = np.sort(rng.choice(n, size=int(rng.integers(1, n + 1)), replace=False)).astype(np.uint32)
+        opay, osums = cpu.pack(t, C, src)
+        recv = np.full(max(db, 1), 0xA5, np.uint8)
+        cpu.unpack(t, C, opay, osums, recv)
+        expect = recv.copy()
+        nch, base, _, _ = cpu.plan(t, C)
+        for c in ids:  # scramble the listed chunks at the receiver
+            k = int(np.searchsorted(base, int(c), side="right") - 1)
+            j = int(c) - int(base[k])
+            nb = int(t[k]["numel"]) * (4 if int(t[k]["dtype"]) == 1 else 2)
+            o = int(t[k]["dst_offset"]) + j * C
+            ln = min(C, nb - j * C)
+            recv[o:o + ln] = rng.integers(0, 256, ln, dtype=np.uint8)
+        dpay, dsums = cpu.pack_chunks(t, C, src, ids)
+        g_src, g_recv = to_dev(src), to_dev(recv)
+        pb = plan.delta_layout(ids)
+        assert pb == dpay.size
+        payload = torch.full((max(pb, 16),), 0xEE, dtype=torch.uint8, device="cuda")
+        sums = torch.empty(ids.size, 2, dtype=torch.int64, device="cuda")
+        bad, nbad = torch.empty((ids.size + 31) // 32, dtype=torch.int32, device="cuda"), plan.empty_counter()
+        plan.pack_chunks(g_src, ids, payload, sums)
+        plan.unpack_chunks(payload, sums, ids, g_recv, bad, nbad)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host(payload)[:pb], dpay), f"delta payload {it}"
+        assert np.array_equal(sums_host(sums, ids.size), dsums), f"delta sums {it}"
+        orecv = recv.copy()
+        obm, onbad = cpu.unpack_chunks(t, C, dpay, dsums, ids, orecv)
+        assert np.array_equal(to_host(g_recv), orecv) and int(nbad.item()) == onbad == 0, f"delta {it}"
+        assert np.array_equal(orecv, expect), f"delta repair {it}"
