@@ -59,13 +59,26 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_bytes(info) -> dict:
-    """Bytes each operation must move at least (read + write), per launch."""
+def segment_bytes(table) -> int:
+    """Bytes of the payload's segments: every sent (non-derived) entry padded
+    to 16 bytes; the zero gaps between segments are not counted."""
+    import numpy as np
+
+    sent = table["derive_from"] < 0
+    nb = table["numel"].astype(np.uint64) * np.where(table["dtype"] == 1, 4, 2).astype(np.uint64)
+    return int(((nb[sent] + 15) // 16 * 16).sum())
+
+
+def algorithmic_bytes(info, table=None) -> dict:
+    """Bytes each operation must move at least (read + write), per launch.
+    Pack writes the whole payload, zero gaps included; unpack reads only its
+    segments (the whole payload when no table is given)."""
     S, P, n = info["state_bytes"], info["payload_bytes"], info["n_chunks"]
+    R = P if table is None else segment_bytes(table)
     words = info["bitmap_words"]
     return {
         "pack": S + P + 16 * n,
-        "unpack": P + 16 * n + S + 4 * words,
+        "unpack": R + 16 * n + S + 4 * words,
         "verify": 2 * S + 4 * words,
         "checksum": S + 16 * n,
     }
@@ -341,7 +354,7 @@ def main():
 
     ms_step = total_ms / args.steps
     value = info["state_bytes"] / (ms_step * 1e-3) / 1e9
-    alg = algorithmic_bytes(info)
+    alg = algorithmic_bytes(info, w.table)
     op_report = {}
     for op in ops:
         gbs = alg[op] / (per_op[op] * 1e-3) / 1e9
