@@ -207,18 +207,28 @@ def control_plane(reps=21):
     }
 
 
-def delta_repair(plan, donor, replica, info, k, stream, reps=5):
-    """Repair of a replica that diverged in k random bits: compare, read the
-    flagged set back, re-send only those chunks.  Times the GPU work of the
-    two delta operations (HIP events) and the whole repair on the host clock."""
+def delta_repair(plan, table, donor, replica, info, k, stream, reps=5):
+    """Repair of a replica that diverged in k random bits of its tensors:
+    compare, read the flagged set back, re-send only those chunks.  `plan`
+    has the donor's layout on both sides (replicas of one group share it).
+    Times the GPU work of the two delta operations (HIP events) and the whole
+    repair on the host clock."""
     import numpy as np
     import torch
 
     from paper_2509_03047_amd import flashrestore as F
     from paper_2509_03047_amd import workloads as W
 
-    pos = W.flip_positions(info["src_arena_bytes"] * 8, k, 4000 + k)
-    by = (pos // 8).astype(np.int64)
+    # bit positions over the table-order concatenation of the tensors' bytes,
+    # mapped to arena offsets (gaps between tensors belong to no chunk)
+    nb = table["numel"].astype(np.int64) * np.where(table["dtype"] == W.F32, 4, 2)
+    starts = np.concatenate([[0], np.cumsum(nb)])
+    pos = W.flip_positions(int(starts[-1]) * 8, k, 4000 + k).astype(np.int64)
+    cat = pos // 8
+    e = np.searchsorted(starts, cat, side="right") - 1
+    by = table["src_offset"].astype(np.int64)[e] + (cat - starts[e])
+    order = np.argsort(by, kind="stable")
+    by, pos = by[order], pos[order]
     masks = (np.uint8(1) << (pos % 8).astype(np.uint8)).astype(np.uint8)
     uniq, start = np.unique(by, return_index=True)
     idx = torch.from_numpy(uniq).to("cuda")
@@ -234,6 +244,9 @@ def delta_repair(plan, donor, replica, info, k, stream, reps=5):
         t0 = time.perf_counter()
         plan.verify_replicas(donor, replica, diff, ndiff, stream=stream)
         ids = F.bitmap_indices(diff, plan.n_chunks).astype(np.uint32)  # synchronises
+        need = plan.delta_layout(ids)
+        if payload.numel() < need:  # a sparse list of chunks under 4 KiB can outgrow the full payload
+            payload = torch.empty(need, dtype=torch.uint8, device="cuda")
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         plan.pack_chunks(donor, ids, payload, sums, stream=stream)
@@ -402,7 +415,12 @@ def main():
         "wall_s_timed": round(wall, 4),
     }
     if not args.no_delta:
-        out["delta_repair"] = delta_repair(plan, src, replica, info, args.delta_flips, stream)
+        rplan, rtable = plan, w.table
+        if not same_layout:  # repair within the donor's layout
+            rtable = w.table.copy()
+            rtable["dst_offset"] = rtable["src_offset"]
+            rplan = F.Plan(rtable, w.chunk_bytes, w.src_arena_bytes, w.src_arena_bytes)
+        out["delta_repair"] = delta_repair(rplan, rtable, src, replica, rplan.info, args.delta_flips, stream)
         out["delta_repair"]["full_restore_ms"] = round(restore_ms, 4)
     out["control_plane"] = control_plane()
     if not args.no_cpu_baseline:

@@ -227,7 +227,10 @@ int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums,
  * buffer has makes the call first synchronise the device and reallocate it
  * (an allocation: such a call cannot be captured into a graph). */
 
-/* Bytes of the delta payload for a list.  Host only. */
+/* Bytes of the delta payload for a list.  Host only.  (With C below 4096 a
+ * sparse list can need more than the full payload's payload_bytes, since
+ * each chunk that does not continue the previous one starts on a 4 KiB
+ * boundary.) */
 int fr_delta_layout(const fr_plan* plan, const uint32_t* chunk_ids, uint64_t n_ids,
                     uint64_t* payload_bytes);
 
