@@ -107,42 +107,51 @@ def copy_calibration():
 
 
 def cpu_baseline(w, src_np, seconds: float):
-    """The oracle, as it stands, on a prefix of the same workload: the
-    embedding and the first layers (whole logical tensors)."""
+    """The oracle, as it stands, on a prefix of the same workload: the first
+    entries of the table (whole logical tensors for the model-shaped ones, the
+    embedding and the first layers) up to about 2 GB of state."""
     import numpy as np
 
     from oracle import cpu
 
     t = w.table
-    # prefix of whole logical tensors (4 entries each) up to ~2 GB of state
     es = np.where(t["dtype"] == 1, 4, 2).astype(np.int64) * t["numel"].astype(np.int64)
     cum = np.cumsum(es)
-    n_ent = 4
-    while n_ent + 4 <= len(t) and cum[n_ent + 4 - 1] <= 2_100_000_000:
-        n_ent += 4
+    step = 4 if w.tensors is not None else 1  # 4 entries per logical tensor
+    n_ent = step
+    while n_ent + step <= len(t) and cum[n_ent + step - 1] <= 2_100_000_000:
+        n_ent += step
     sub = t[:n_ent].copy()
-    end = int(sub["src_offset"][-1]) + int(es[n_ent - 1])
     state = int(cum[n_ent - 1])
-    src = src_np[:end]
+    same_layout = (w.src_arena_bytes == w.dst_arena_bytes
+                   and np.array_equal(t["src_offset"], t["dst_offset"]))
+    if same_layout and w.tensors is not None:
+        # entries are contiguous from 0: only the prefix's bytes are needed
+        end = int(sub["src_offset"][-1]) + int(es[n_ent - 1])
+        src, dst = src_np[:end], np.empty(end, np.uint8)
+    else:
+        src, dst = src_np, np.empty(w.dst_arena_bytes, np.uint8)
+    # the compare and the checksum take an arena in the donor's layout
+    replica = dst if same_layout else src
     C = w.chunk_bytes
-    dst = np.empty(end, np.uint8)
     reps, t0 = 0, time.perf_counter()
     while True:
         pay, sums = cpu.pack(sub, C, src)
         bm, nbad = cpu.unpack(sub, C, pay, sums, dst)
-        vb, nd = cpu.verify(sub, C, src, dst)
-        cs = cpu.checksum(sub, C, dst)
+        vb, nd = cpu.verify(sub, C, src, replica)
+        cs = cpu.checksum(sub, C, replica)
         reps += 1
         el = time.perf_counter() - t0
         if el >= seconds or reps >= 20:
             break
-    assert nbad == 0 and nd == 0
+    assert nbad == 0 and nd == 0 and np.array_equal(cs, sums)
+    what = f"{n_ent // 4} logical tensors" if step == 4 else "entries in table order"
     return {
         "value": round(state * reps / el / 1e9, 4),
         "unit": "GB/s",
         "cores": cpu.threads(),
         "kind": "oracle",
-        "sample": f"first {n_ent} of {len(t)} entries ({n_ent // 4} logical tensors, {state} state bytes), "
+        "sample": f"first {n_ent} of {len(t)} entries ({what}, {state} state bytes), "
                   f"{reps} full steps (pack+unpack+verify+checksum) in {el:.1f} s",
     }
 
