@@ -1,0 +1,43 @@
+"""bench.py end to end on small runs: the one JSON line it prints carries the
+contract's fields, and the pass, the delta repair and the control-plane
+checks all report success (toy decoder; descriptor stress, whose receiver
+layout differs from the sender's)."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("config,extra", [(0, ["--cpu-seconds", "0.5"]), (2, ["--no-cpu-baseline"])])
+def test_bench_json_line(config, extra):
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--config", str(config),
+                        "--steps", "2", "--warmup", "1", *extra],
+                       cwd=ROOT, capture_output=True, text=True, timeout=500)
+    assert p.returncode == 0, p.stderr[-3000:]
+    lines = [ln for ln in p.stdout.splitlines() if ln.strip()]
+    assert len(lines) == 1
+    d = json.loads(lines[0])
+    for k in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+              "scaling", "vs_baseline", "dtype", "data", "config", "roofline", "ops"):
+        assert k in d, k
+    assert d["n_gpus"] == 1 and d["steps"] == 2 and d["warmup"] == 1 and d["higher_is_better"] is True
+    assert d["value"] > 0 and d["config"]["workload"]
+    r = d["roofline"]
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert abs(r["frac"] - r["achieved"] / r["peak"]) < 1e-3
+    assert d["parity_ok"] is True
+    assert d["delta_repair"]["ok"] is True and d["control_plane"]["ok"] is True
+    if "--no-cpu-baseline" not in extra:
+        cb = d["cpu_baseline"]
+        assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1 and cb["sample"]
