@@ -17,10 +17,11 @@ namespace fr {
 thread_local int g_last_hip_error = 0;
 
 // Default tile of each operation (kernels.hip: 4 = 64 threads x 4 vectors,
-// 5 = 128 threads x 2 vectors; both 4 KiB slices), chosen by sweeping all
-// tiles on MI355X over the 8B and 70B rank-share workloads.
+// 5 = 128 threads x 2 vectors, both 4 KiB slices; 3 = 256 threads x 4
+// vectors, 16 KiB slices), chosen by sweeping all tiles on MI355X over the
+// 8B and 70B rank shares and the descriptor stress table.
 constexpr uint32_t kDefaultTilePack = 4, kDefaultTileUnpack = 5, kDefaultTileVerify = 5,
-                   kDefaultTileChecksum = 4;
+                   kDefaultTileChecksum = 3;
 
 static uint64_t esize(uint32_t dtype) { return dtype == FR_F32 ? 4 : 2; }
 static uint64_t align16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
