@@ -226,7 +226,8 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
     // segment (fewer than 256 vectors).
     const uint32_t endv = nvec + (tail ? 1u : 0u);
     if (store && r.gap_v && v0 + wk.sl_vec >= endv) {
-      for (uint32_t v = endv + threadIdx.x; v < endv + r.gap_v; v += B) st_nt(u32x4{0, 0, 0, 0}, d + v);
+      for (uint32_t v = endv + threadIdx.x; v < endv + r.gap_v; v += B)
+        st_nt(u32x4{0, 0, 0, 0}, d + v);
     }
     block_sum<B, 2>(acc, lds, parity);
     if (threadIdx.x == 0)
@@ -236,13 +237,14 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
 
 // ---------------------------------------------------------------- unpack
 
-// Two kinds of units, derived groups first:
+// Two kinds of units, listed by the walk in payload order (a derived group
+// where its entry stands in the table):
 //   derived: bf16 parameter chunk c and the master chunks m0 = master(c) and
 //            m0 + 1 holding its 2 * len source bytes; walked in slices of
-//            master bytes (2 * SPC slices per unit), each slice inside one
+//            master bytes (at most 2 * SPC per unit), each slice inside one
 //            master chunk;
 //   plain:   a chunk of an entry that is neither derived nor a master with a
-//            derived image; SPC slices per unit.
+//            derived image; at most SPC slices per unit.
 // Sums of the bytes written go to the accumulators `acc_out` (zeroed).
 // One slice of a derived group: read master bytes from `msrc` (the payload,
 // or with kFromPayload = false the receiver's own masters), write the bf16
