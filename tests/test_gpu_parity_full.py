@@ -5,9 +5,11 @@ times (default plan, one workgroup per unit).
   host; payload, sums, receiver arena and result sets are compared bit for bit.
 * 20,000-entry descriptor stress (7.6 GB): whole oracle, scattered layouts,
   canaries in every receiver gap.
-* Llama-3-70B TP=8 x PP=4 first-stage share (31.8 GB): sampled chunks against
-  the oracle plus properties that hold at any size (exact round trip, nothing
-  flagged, checksum == pack sums, replica compare empty).
+* Llama-3-70B TP=8 x PP=4 first-stage share (31.8 GB): the whole oracle on
+  the host (payload, sums and receiver arena compared slice by slice), plus
+  sampled chunks, a located wire flip and properties that hold at any size
+  (exact round trip, nothing flagged, checksum == pack sums, replica compare
+  empty).
 * Replica compare on two copies of the 8B share with k in {0, 1, 64, 4096}
   distinct random bit flips: the flagged set equals the closed form
   {chunk of each flipped byte} and the oracle's set.
@@ -178,14 +180,56 @@ def test_descriptor_stress_full_parity():
     assert r.bad_set() == set(cpu.bitmap_to_set(bm, nc)) and int(r.n_bad.item()) == nbad
 
 
-@pytest.mark.timeout(900)
-def test_llama70b_stage0_sampled_parity():
+@pytest.fixture(scope="module")
+def llama70b():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     w = W.make_workload(3)
-    t, C = w.table, w.chunk_bytes
-    src_np = W.fill_state(w)
+    src = W.fill_state(w)
     log(f"generated {w.name}: {w.state_bytes} B")
+    return w, src
+
+
+def _equal_in_slices(dev: torch.Tensor, host: np.ndarray, step: int = 1 << 30) -> bool:
+    """Device bytes equal host bytes, copied back one slice at a time."""
+    if dev.numel() < host.size:
+        return False
+    for a in range(0, host.size, step):
+        b = min(a + step, host.size)
+        if not np.array_equal(to_host(dev[a:b]), host[a:b]):
+            log(f"mismatch in bytes [{a}, {b})")
+            return False
+    return True
+
+
+@pytest.mark.timeout(900)
+def test_llama70b_stage0_whole_oracle_parity(llama70b):
+    w, src_np = llama70b
+    t, C = w.table, w.chunk_bytes
+    r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes)
+    r.pack(_upload(src_np))
+    r.unpack()
+    torch.cuda.synchronize()
+    nc = r.n_chunks
+    opay, osums = cpu.pack(t, C, src_np)
+    log("oracle pack done")
+    assert opay.size == r.plan.payload_bytes
+    assert np.array_equal(sums_host(r.sums, nc), osums)
+    assert _equal_in_slices(r.payload, opay)
+    log("payload and sums equal the oracle's")
+    odst = np.full(w.dst_arena_bytes, 0xA5, np.uint8)
+    obm, onbad = cpu.unpack(t, C, opay, osums, odst)
+    del opay
+    log("oracle unpack done")
+    assert onbad == 0 and int(r.n_bad.item()) == 0 and r.bad_set() == set()
+    assert _equal_in_slices(r.dst, odst)
+    log("receiver arena equals the oracle's")
+
+
+@pytest.mark.timeout(900)
+def test_llama70b_stage0_sampled_parity(llama70b):
+    w, src_np = llama70b
+    t, C = w.table, w.chunk_bytes
     r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes)
     src = _upload(src_np)
     r.pack(src)
