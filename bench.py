@@ -319,7 +319,9 @@ def main():
     src_np = W.fill_state(w)
     print(f"# generated {w.name}: {w.state_bytes} state bytes in {time.perf_counter() - t0:.1f} s",
           file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
     plan = F.Plan(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
+    plan_ms = (time.perf_counter() - t0) * 1e3  # validation, walks, device tables (once per rank)
     info = plan.info
     src = torch.from_numpy(src_np).to("cuda")
     payload, sums = plan.empty_payload(), plan.empty_sums()
@@ -418,6 +420,7 @@ def main():
             "step": "pack+checksum -> unpack+derive+verify -> verify_replicas -> checksum_state",
         },
         "restore_gbs": round(info["state_bytes"] / (restore_ms * 1e-3) / 1e9, 2),
+        "plan_ms": round(plan_ms, 2),
         "ops": op_report,
         "roofline": roof,
         "parity_ok": bool(ok),
