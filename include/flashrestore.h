@@ -136,7 +136,13 @@ typedef struct fr_plan_info {
  * (FR_E_OVERLAP; sender ranges may), the chunk count must be < 2^32
  * (FR_E_RANGE).  Synchronous: the plan's device tables are uploaded before
  * return.  The plan is immutable and bound to the device current at
- * creation. */
+ * creation.  Launch shapes are read from the environment at creation, and
+ * results never depend on them: FLASHRESTORE_TILE (every operation) or
+ * FLASHRESTORE_TILE_PACK / _UNPACK / _VERIFY / _CHECKSUM select a tile
+ * 0-10 (threads x 16-byte vectors per workgroup: 256x1, 512x1, 256x2,
+ * 256x4, 64x4, 128x2, 64x2, 64x1, 128x1, 128x4, 64x8; defaults pack 64x4,
+ * unpack and compare 128x2, checksum 256x4), FLASHRESTORE_MAX_GRID caps the
+ * workgroups per launch (0 or unset: one per slice). */
 int fr_plan_create(const fr_tensor_desc* table, uint32_t n_entries, uint64_t chunk_bytes,
                    uint64_t src_arena_bytes, uint64_t dst_arena_bytes, fr_plan** out);
 
