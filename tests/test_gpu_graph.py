@@ -1,4 +1,4 @@
-"""A whole restore step captured in a HIP graph (the operations are kernel
+"""Streams and graphs.  A whole restore step captured in a HIP graph (the operations are kernel
 launches only: no memsets, no host work on the stream) and replayed several
 times, with eager work and synchronisation between replays; every replay is
 checked against the eager result."""
@@ -70,3 +70,52 @@ def test_captured_restore_step_replays_correctly():
     torch.cuda.synchronize()
     assert torch.equal(payload, ref[0]) and torch.equal(sums, ref[1])
     assert torch.equal(dst, ref[2]) and torch.equal(csum, ref[3])
+
+
+def test_two_plans_on_two_streams_run_concurrently():
+    """One plan per concurrent stream: two plans' whole restore steps, queued
+    on two streams without ordering between them, give the same results as
+    each plan run alone."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    rng = np.random.default_rng(5)
+    runs = []
+    for seed in (0, 1):
+        t, sb, db = W.random_tiny_table(rng, max_entries=40, max_numel=200_000)
+        src = torch.from_numpy(W.random_tiny_state(t, sb, rng)).to("cuda")
+        plan = F.Plan(t, 4096, sb, db)
+        bufs = dict(payload=plan.empty_payload(), sums=plan.empty_sums(),
+                    dst=torch.full((max(db, 1),), 0x5A, dtype=torch.uint8, device="cuda"),
+                    bad=plan.empty_bitmap(), nbad=plan.empty_counter(), csum=plan.empty_sums())
+        runs.append((plan, src, bufs))
+
+    def step(plan, src, b, stream):
+        plan.pack(src, b["payload"], b["sums"], stream=stream)
+        plan.unpack(b["payload"], b["sums"], b["dst"], b["bad"], b["nbad"], stream=stream)
+        plan.checksum_state(src, b["csum"], stream=stream)
+
+    def view(plan, b):  # the bytes a step defines (the receiver's gaps keep their canary)
+        return {"payload": b["payload"][: plan.payload_bytes], "sums": b["sums"][: plan.n_chunks],
+                "dst": b["dst"], "bad": b["bad"], "nbad": b["nbad"], "csum": b["csum"][: plan.n_chunks]}
+
+    # each alone, on the current stream
+    ref = []
+    for plan, src, b in runs:
+        step(plan, src, b, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        ref.append({k: v.clone() for k, v in view(plan, b).items()})
+        for k, v in b.items():
+            v.fill_(0x5A if k == "dst" else 0x33)
+    # both at once, on two streams
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for i in range(3):
+        for (plan, src, b), s in zip(runs, streams):
+            with torch.cuda.stream(s):
+                step(plan, src, b, s)
+    torch.cuda.synchronize()
+    for (plan, src, b), r in zip(runs, ref):
+        got = view(plan, b)
+        for k in got:
+            assert torch.equal(got[k], r[k]), k
+        assert int(b["nbad"].item()) == 0
