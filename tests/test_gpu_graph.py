@@ -1,7 +1,8 @@
-"""Streams and graphs.  A whole restore step captured in a HIP graph (the operations are kernel
-launches only: no memsets, no host work on the stream) and replayed several
-times, with eager work and synchronisation between replays; every replay is
-checked against the eager result."""
+"""Streams and graphs.  A whole restore step captured in a HIP graph (the
+operations are kernel launches only: no memsets, no host work on the stream)
+and replayed several times, with eager work and synchronisation between
+replays, every replay checked against the eager result; and two plans run
+concurrently on two streams."""
 import numpy as np
 import pytest
 import torch
