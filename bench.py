@@ -319,6 +319,8 @@ def main():
     src_np = W.fill_state(w)
     print(f"# generated {w.name}: {w.state_bytes} state bytes in {time.perf_counter() - t0:.1f} s",
           file=sys.stderr, flush=True)
+    torch.zeros(1, device="cuda")  # HIP runtime set-up, which the first plan would otherwise pay
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
     plan = F.Plan(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
     plan_ms = (time.perf_counter() - t0) * 1e3  # validation, walks, device tables (once per rank)

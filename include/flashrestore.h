@@ -74,7 +74,7 @@
 extern "C" {
 #endif
 
-#define FR_ABI_VERSION 1
+#define FR_ABI_VERSION 2
 
 enum fr_dtype { FR_F32 = 1, FR_BF16 = 2 };
 
@@ -253,11 +253,16 @@ int fr_pack_chunks(const fr_plan* plan, const void* src_base, const uint32_t* ch
  * hold every sent master chunk); then set bit i of bad_bitmap iff FRSUM-128
  * of chunk chunk_ids[i] as written differs from sums[i]; *n_bad = number of
  * set bits.  Bytes outside the listed chunks are not written.
- *   bad_bitmap  device, 4-byte aligned, ceil(n_ids / 32) words (NULL if n_ids == 0)
- *   n_bad       device, 8-byte aligned, one uint64 */
-int fr_unpack_chunks(const fr_plan* plan, const void* payload, const fr_chunk_sum* sums,
-                     const uint32_t* chunk_ids, uint64_t n_ids, void* dst_base,
-                     uint32_t* bad_bitmap, uint64_t* n_bad, void* stream);
+ *   payload        device, 16-byte aligned, as fr_pack_chunks wrote it for the
+ *                  same list
+ *   payload_bytes  bytes readable at payload; FR_E_RANGE if below the
+ *                  fr_delta_layout bytes of the list
+ *   sums           device, 16-byte aligned, n_ids entries
+ *   bad_bitmap     device, 4-byte aligned, ceil(n_ids / 32) words (NULL if n_ids == 0)
+ *   n_bad          device, 8-byte aligned, one uint64 */
+int fr_unpack_chunks(const fr_plan* plan, const void* payload, uint64_t payload_bytes,
+                     const fr_chunk_sum* sums, const uint32_t* chunk_ids, uint64_t n_ids,
+                     void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad, void* stream);
 
 /* ------------------------------------------------- step tags and donors */
 

@@ -375,9 +375,9 @@ extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const 
 }
 
 extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
-                                const fr_chunk_sum* sums, const uint32_t* ids, uint64_t n_ids,
-                                void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad,
-                                void* stream) {
+                                uint64_t payload_bytes, const fr_chunk_sum* sums,
+                                const uint32_t* ids, uint64_t n_ids, void* dst_base,
+                                uint32_t* bad_bitmap, uint64_t* n_bad, void* stream) {
   if (!cplan || !n_bad) return FR_E_INVAL;
   fr_plan* plan = const_cast<fr_plan*>(cplan);
   FR_TRY(check_list(plan, ids, n_ids));
@@ -388,6 +388,7 @@ extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
     return FR_E_NOMEM;
   }
   const uint64_t pb = dl.bytes;
+  if (payload_bytes < pb) return FR_E_RANGE;
   const uint64_t words = (n_ids + 31) / 32;
   FR_TRY(check_device_and_stream(plan, stream));
   FR_TRY(check_buffer(plan, payload, pb, 16));

@@ -104,7 +104,7 @@ def _load():
         "fr_checksum_state": [P, P, P, P],
         "fr_delta_layout": [P, P, u64, C.POINTER(u64)],
         "fr_pack_chunks": [P, P, P, u64, P, u64, P, P],
-        "fr_unpack_chunks": [P, P, P, P, u64, P, P, P, P],
+        "fr_unpack_chunks": [P, P, u64, P, P, u64, P, P, P, P],
         "fr_tracker_create": [u32, P, C.c_double, C.c_double, C.POINTER(P)],
         "fr_tracker_destroy": [P],
         "fr_tracker_heartbeat": [P, u32, C.c_int64, C.c_double],
@@ -124,7 +124,7 @@ def _load():
         f.argtypes = args
         f.restype = C.c_int
     lib.fr_strerror.restype = C.c_char_p
-    if lib.fr_abi_version() != 1:
+    if lib.fr_abi_version() != 2:
         raise ImportError("libflashrestore ABI version mismatch")
     return lib
 
@@ -164,6 +164,25 @@ def _ptr(x) -> int | None:
         return None
     if isinstance(x, int):
         return x
+    return x.data_ptr()
+
+
+def _dev(x, need: int, name: str) -> int | None:
+    """Address of a device buffer argument that the call accesses for `need`
+    bytes.  The library checks that a buffer lies inside one HIP allocation,
+    but torch carves many tensors out of one allocation, so a tensor's own
+    extent is checked here: it must be a contiguous CUDA tensor of at least
+    `need` bytes (ValueError otherwise).  An int is a raw device address whose
+    extent the caller vouches for; None is NULL."""
+    if x is None or isinstance(x, int):
+        return x
+    if not x.is_cuda:
+        raise ValueError(f"{name}: not a device tensor")
+    if not x.is_contiguous():
+        raise ValueError(f"{name}: not contiguous")
+    nb = x.numel() * x.element_size()
+    if nb < need:
+        raise ValueError(f"{name}: {nb} bytes, the call accesses {need}")
     return x.data_ptr()
 
 
@@ -286,8 +305,8 @@ class Plan:
     def pack_chunks(self, src, chunk_ids, payload, sums, stream=None, payload_cap=None):
         return fr_pack_chunks(self, src, chunk_ids, payload, payload_cap, sums, stream)
 
-    def unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream=None):
-        return fr_unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream)
+    def unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream=None, payload_bytes=None):
+        return fr_unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream, payload_bytes)
 
 
 def _nbytes(x):
@@ -309,24 +328,38 @@ def fr_pack_state(plan: Plan, src, payload, payload_cap, sums, stream=None) -> N
         payload_cap = _nbytes(payload)
         if payload_cap is None:
             payload_cap = plan.payload_bytes
-    _check(_lib.fr_pack_state(plan.handle, _ptr(src), _ptr(payload), payload_cap, _ptr(sums),
-                              _stream(stream)), "fr_pack_state")
+    i = plan.info
+    # pack writes payload_bytes (a smaller cap is the library's FR_E_RANGE)
+    _check(_lib.fr_pack_state(plan.handle, _dev(src, i["src_arena_bytes"], "src"),
+                              _dev(payload, min(payload_cap, i["payload_bytes"]), "payload"), payload_cap,
+                              _dev(sums, SUM_BYTES * i["n_chunks"], "sums"), _stream(stream)),
+           "fr_pack_state")
 
 
 def fr_unpack_state(plan: Plan, payload, sums, dst, bad_bitmap, n_bad, stream=None) -> None:
-    _check(_lib.fr_unpack_state(plan.handle, _ptr(payload), _ptr(sums), _ptr(dst), _ptr(bad_bitmap),
-                                _ptr(n_bad), _stream(stream)), "fr_unpack_state")
+    i = plan.info
+    _check(_lib.fr_unpack_state(plan.handle, _dev(payload, i["payload_bytes"], "payload"),
+                                _dev(sums, SUM_BYTES * i["n_chunks"], "sums"),
+                                _dev(dst, i["dst_arena_bytes"], "dst"),
+                                _dev(bad_bitmap, 4 * i["bitmap_words"], "bad_bitmap"),
+                                _dev(n_bad, 8, "n_bad"), _stream(stream)), "fr_unpack_state")
 
 
 def fr_verify_replicas(plan: Plan, base_a, base_b, diff_bitmap, n_diff, sums_a=None, sums_b=None,
                        stream=None) -> None:
-    _check(_lib.fr_verify_replicas(plan.handle, _ptr(base_a), _ptr(base_b), _ptr(diff_bitmap),
-                                   _ptr(n_diff), _ptr(sums_a), _ptr(sums_b), _stream(stream)),
-           "fr_verify_replicas")
+    i = plan.info
+    sb = SUM_BYTES * i["n_chunks"]
+    _check(_lib.fr_verify_replicas(plan.handle, _dev(base_a, i["src_arena_bytes"], "base_a"),
+                                   _dev(base_b, i["src_arena_bytes"], "base_b"),
+                                   _dev(diff_bitmap, 4 * i["bitmap_words"], "diff_bitmap"),
+                                   _dev(n_diff, 8, "n_diff"), _dev(sums_a, sb, "sums_a"),
+                                   _dev(sums_b, sb, "sums_b"), _stream(stream)), "fr_verify_replicas")
 
 
 def fr_checksum_state(plan: Plan, base, sums, stream=None) -> None:
-    _check(_lib.fr_checksum_state(plan.handle, _ptr(base), _ptr(sums), _stream(stream)),
+    i = plan.info
+    _check(_lib.fr_checksum_state(plan.handle, _dev(base, i["src_arena_bytes"], "base"),
+                                  _dev(sums, SUM_BYTES * i["n_chunks"], "sums"), _stream(stream)),
            "fr_checksum_state")
 
 
@@ -348,15 +381,30 @@ def fr_pack_chunks(plan: Plan, src, chunk_ids, payload, payload_cap, sums, strea
         payload_cap = _nbytes(payload)
         if payload_cap is None:
             payload_cap = fr_delta_layout(plan, ids)
-    _check(_lib.fr_pack_chunks(plan.handle, _ptr(src), ids.ctypes.data if ids.size else None, ids.size,
-                               _ptr(payload), payload_cap, _ptr(sums), _stream(stream)), "fr_pack_chunks")
+    # the library refuses a cap below the list's payload and writes no more
+    # than that, so a tensor of payload_cap bytes is enough
+    _check(_lib.fr_pack_chunks(plan.handle, _dev(src, plan.info["src_arena_bytes"], "src"),
+                               ids.ctypes.data if ids.size else None, ids.size,
+                               _dev(payload, payload_cap, "payload"), payload_cap,
+                               _dev(sums, SUM_BYTES * ids.size, "sums"), _stream(stream)), "fr_pack_chunks")
 
 
-def fr_unpack_chunks(plan: Plan, payload, sums, chunk_ids, dst, bad_bitmap, n_bad, stream=None) -> None:
+def fr_unpack_chunks(plan: Plan, payload, sums, chunk_ids, dst, bad_bitmap, n_bad, stream=None,
+                     payload_bytes=None) -> None:
+    """payload_bytes: bytes readable at payload (default: the tensor's size,
+    else the list's fr_delta_layout bytes); the library refuses less than the
+    list needs."""
     ids = _ids(chunk_ids)
-    _check(_lib.fr_unpack_chunks(plan.handle, _ptr(payload), _ptr(sums), ids.ctypes.data if ids.size else None,
-                                 ids.size, _ptr(dst), _ptr(bad_bitmap), _ptr(n_bad), _stream(stream)),
-           "fr_unpack_chunks")
+    if payload_bytes is None:
+        payload_bytes = _nbytes(payload)
+        if payload_bytes is None:
+            payload_bytes = fr_delta_layout(plan, ids)
+    _check(_lib.fr_unpack_chunks(plan.handle, _dev(payload, payload_bytes, "payload"), payload_bytes,
+                                 _dev(sums, SUM_BYTES * ids.size, "sums"),
+                                 ids.ctypes.data if ids.size else None, ids.size,
+                                 _dev(dst, plan.info["dst_arena_bytes"], "dst"),
+                                 _dev(bad_bitmap, 4 * ((ids.size + 31) // 32), "bad_bitmap"),
+                                 _dev(n_bad, 8, "n_bad"), _stream(stream)), "fr_unpack_chunks")
 
 
 class Tracker:

@@ -126,3 +126,45 @@ def test_explicit_stream_and_destroy(setup):
         p2.pack(src, payload, sums)
     with pytest.raises(F.FlashRestoreError):
         plan.chunk_of(0, 10 ** 12)
+
+
+def test_binding_rejects_short_or_strided_tensors(setup):
+    """torch sub-allocates tensors from one HIP allocation, where the
+    library's own allocation check cannot see a tensor's end: the binding
+    refuses a tensor shorter than the call accesses, or not contiguous,
+    before anything is enqueued."""
+    w, plan, src = setup
+    payload, sums = plan.empty_payload(), plan.empty_sums()
+    dst = torch.full((w.dst_arena_bytes,), 0x5A, dtype=torch.uint8, device="cuda")
+    bad, nbad = plan.empty_bitmap(), plan.empty_counter()
+    snap = dst.clone()
+    short = [
+        (F.fr_pack_state, (plan, src[:-16], payload, None, sums)),
+        (F.fr_pack_state, (plan, src, payload[: plan.payload_bytes - 16], plan.payload_bytes, sums)),
+        (F.fr_pack_state, (plan, src, payload, None, sums[:-1])),
+        (F.fr_unpack_state, (plan, payload[:-16], sums, dst, bad, nbad)),
+        (F.fr_unpack_state, (plan, payload, sums, dst[:-16], bad, nbad)),
+        (F.fr_unpack_state, (plan, payload, sums, dst, bad[:-1], nbad)),
+        (F.fr_verify_replicas, (plan, src, dst[:-16], bad, nbad)),
+        (F.fr_checksum_state, (plan, src, sums[:-1])),
+        (F.fr_checksum_state, (plan, src.cpu(), sums)),
+    ]
+    wide = torch.empty(w.src_arena_bytes, 2, dtype=torch.uint8, device="cuda")
+    short.append((F.fr_checksum_state, (plan, wide[:, 0], sums)))  # strided view
+    for fn, args in short:
+        with pytest.raises(ValueError):
+            fn(*args)
+    ids = np.arange(0, plan.n_chunks, 3, dtype=np.uint32)
+    need = plan.delta_layout(ids)
+    dsums = torch.empty(ids.size, 2, dtype=torch.int64, device="cuda")
+    dbad = torch.empty((ids.size + 31) // 32, dtype=torch.int32, device="cuda")
+    with pytest.raises(ValueError):
+        plan.pack_chunks(src, ids, payload[: need - 16], dsums, payload_cap=need)
+    plan.pack_chunks(src, ids, payload, dsums)
+    # a tensor, or a raw address with a stated extent, below the list's
+    # payload: the library's own check
+    assert _status(plan.unpack_chunks, payload[: need - 16], dsums, ids, dst, dbad, nbad) == -3
+    assert _status(F.fr_unpack_chunks, plan, payload.data_ptr(), dsums, ids, dst, dbad, nbad,
+                   None, need - 16) == -3
+    torch.cuda.synchronize()
+    assert torch.equal(dst, snap)
