@@ -214,17 +214,15 @@ def test_every_tile_matches_oracle(tile):
             os.environ["FLASHRESTORE_TILE"] = old
 
 
-def test_short_last_chunks_every_slot_count():
-    """Entries whose last chunk holds every possible number of 4 KiB slices
-    (and ragged tails inside them), for plain chunks and for bf16 parameter
-    chunks derived from masters, with the receiver laid out differently from
-    the sender: the walk lists only the slices a short chunk has."""
+def _short_chunk_table(rng, scale=1):
+    """Entries (bf16 parameter derived from its master, two plain fp32) whose
+    last chunk of C = 16 KiB * scale holds every number of 4 KiB * scale
+    slices, with ragged tails; the receiver gaps differ from the sender's."""
     from paper_2509_03047_amd import flashrestore as F
 
-    rng = np.random.default_rng(77)
-    C = 1 << 14  # four slices per chunk at the default tiles
     numels = [1, 3, 511, 512, 513, 1023, 1024, 1025, 2047, 2048, 3071, 4095, 4096, 4097,
               6143, 8191, 8193, 12289, 16383]
+    numels = [n * scale + (scale - 1) * (k % 3) for k, n in enumerate(numels)]
     rows, so, do = [], 0, 0
     for n in numels:
         for dtype, derive in ((F.FR_BF16, len(rows) + 1), (F.FR_F32, -1), (F.FR_F32, -1)):
@@ -243,7 +241,78 @@ def test_short_last_chunks_every_slot_count():
             m_off = rows[derive][0]
             master = src[m_off:m_off + 4 * n].view(np.float32)
             src[s_off:s_off + 2 * n] = W._bf16_round(master).view(np.uint8)
+    return t, src, so, do
+
+
+def test_short_last_chunks_every_slot_count():
+    """Entries whose last chunk holds every possible number of 4 KiB slices
+    (and ragged tails inside them), for plain chunks and for bf16 parameter
+    chunks derived from masters, with the receiver laid out differently from
+    the sender: the walk lists only the slices a short chunk has."""
+    rng = np.random.default_rng(77)
+    t, src, so, do = _short_chunk_table(rng)
+    C = 1 << 14  # four slices per chunk at the default tiles
     _check_against_oracle(t, C, src, so, do, corrupt_rng=rng, tag="short chunks")
+
+
+def _slice_count_table(rng, C, SL):
+    """Triples (bf16 parameter derived from its master, the master, a plain
+    fp32 entry) of one whole chunk plus a short chunk of every slice count
+    1 .. C / SL, ending on a slice boundary or ragged inside its last slice
+    (12 bytes short, half a slice past); the derived group then walks every
+    count SPC + k.  The receiver gaps differ from the sender's."""
+    from paper_2509_03047_amd import flashrestore as F
+
+    rows, so, do = [], 0, 0
+    for k in range(1, C // SL + 1):
+        for short in sorted({0, 12, SL // 2 - 4}):
+            n = (C + k * SL - short) // 4
+            for dtype, derive in ((F.FR_BF16, len(rows) + 1), (F.FR_F32, -1), (F.FR_F32, -1)):
+                nb = n * (4 if dtype == F.FR_F32 else 2)
+                gap = 16 * int(rng.integers(0, 5))
+                rows.append((so, do + gap, n, dtype, derive))
+                so += (nb + 15) // 16 * 16
+                do += gap + (nb + 15) // 16 * 16
+    t = F.as_table(rows)
+    src = np.zeros(so, np.uint8)
+    for s_off, _, n, dtype, derive in rows:
+        if dtype == F.FR_F32:
+            src[s_off:s_off + 4 * n] = rng.standard_normal(n).astype(np.float32).view(np.uint8)
+    for s_off, _, n, dtype, derive in rows:
+        if derive >= 0:
+            m_off = rows[derive][0]
+            src[s_off:s_off + 2 * n] = W._bf16_round(src[m_off:m_off + 4 * n].view(np.float32)).view(np.uint8)
+    return t, src, so, do
+
+
+# slice bytes of the tiles: 3: 16 KiB, 4: 4 KiB, 5: 4 KiB, 7: 1 KiB, 10: 8 KiB
+SLICE_BYTES = {3: 16384, 4: 4096, 5: 4096, 7: 1024, 10: 8192}
+
+
+@pytest.mark.parametrize("tile", sorted(SLICE_BYTES))
+def test_every_slice_count_per_tile(tile):
+    """For each tile: a table whose short chunks hold every slice count (plain
+    and derived), random tables with C up to 1 MiB, and delta lists (implicit
+    walks) give the oracle's bytes."""
+    old = os.environ.get("FLASHRESTORE_TILE")
+    os.environ["FLASHRESTORE_TILE"] = str(tile)
+    rng = np.random.default_rng(600 + tile)
+    try:
+        C = 1 << 16
+        t, src, so, do = _slice_count_table(rng, C, SLICE_BYTES[tile])
+        _check_against_oracle(t, C, src, so, do, corrupt_rng=rng, tag=f"tile {tile} slice counts")
+        _delta_against_oracle(t, C, src, so, do, rng, f"tile {tile} slice counts")
+        for it in range(4):
+            t, sb, db = W.random_tiny_table(rng, max_entries=8, max_numel=200_000)
+            C = int(rng.choice([4096, 16384, 65536, 1 << 20]))
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"tile {tile} multi {it}")
+            _delta_against_oracle(t, C, src, sb, db, rng, f"tile {tile} multi {it}")
+    finally:
+        if old is None:
+            os.environ.pop("FLASHRESTORE_TILE", None)
+        else:
+            os.environ["FLASHRESTORE_TILE"] = old
 
 
 def test_mixed_tiles_per_operation():
@@ -284,38 +353,45 @@ def test_random_midsize_tables_restore_compare_and_delta():
         src = W.random_tiny_state(t, sb, rng)
         log(f"midsize table {it}: {len(t)} entries, C={C}, {sb} bytes")
         _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"midsize {it} C={C}")
-        # delta: re-send a random subset of chunks into a receiver holding the
-        # oracle's full restore with those chunks scrambled
-        plan = F.Plan(t, C, sb, db)
-        n = plan.n_chunks
-        if n == 0:
-            continue
-        ids = np.sort(rng.choice(n, size=int(rng.integers(1, n + 1)), replace=False)).astype(np.uint32)
-        opay, osums = cpu.pack(t, C, src)
-        recv = np.full(max(db, 1), 0xA5, np.uint8)
-        cpu.unpack(t, C, opay, osums, recv)
-        expect = recv.copy()
-        nch, base, _, _ = cpu.plan(t, C)
-        for c in ids:  # scramble the listed chunks at the receiver
-            k = int(np.searchsorted(base, int(c), side="right") - 1)
-            j = int(c) - int(base[k])
-            nb = int(t[k]["numel"]) * (4 if int(t[k]["dtype"]) == 1 else 2)
-            o = int(t[k]["dst_offset"]) + j * C
-            ln = min(C, nb - j * C)
-            recv[o:o + ln] = rng.integers(0, 256, ln, dtype=np.uint8)
-        dpay, dsums = cpu.pack_chunks(t, C, src, ids)
-        g_src, g_recv = to_dev(src), to_dev(recv)
-        pb = plan.delta_layout(ids)
-        assert pb == dpay.size
-        payload = torch.full((max(pb, 16),), 0xEE, dtype=torch.uint8, device="cuda")
-        sums = torch.empty(ids.size, 2, dtype=torch.int64, device="cuda")
-        bad, nbad = torch.empty((ids.size + 31) // 32, dtype=torch.int32, device="cuda"), plan.empty_counter()
-        plan.pack_chunks(g_src, ids, payload, sums)
-        plan.unpack_chunks(payload, sums, ids, g_recv, bad, nbad)
-        torch.cuda.synchronize()
-        assert np.array_equal(to_host(payload)[:pb], dpay), f"delta payload {it}"
-        assert np.array_equal(sums_host(sums, ids.size), dsums), f"delta sums {it}"
-        orecv = recv.copy()
-        obm, onbad = cpu.unpack_chunks(t, C, dpay, dsums, ids, orecv)
-        assert np.array_equal(to_host(g_recv), orecv) and int(nbad.item()) == onbad == 0, f"delta {it}"
-        assert np.array_equal(orecv, expect), f"delta repair {it}"
+        _delta_against_oracle(t, C, src, sb, db, rng, f"midsize {it}")
+
+
+def _delta_against_oracle(t, C, src, sb, db, rng, tag):
+    """Re-send a random subset of chunks into a receiver holding the oracle's
+    full restore with those chunks scrambled; payload, sums, receiver and
+    count must be the oracle's, and the receiver must be repaired."""
+    from paper_2509_03047_amd import flashrestore as F
+
+    plan = F.Plan(t, C, sb, db)
+    n = plan.n_chunks
+    if n == 0:
+        return
+    ids = np.sort(rng.choice(n, size=int(rng.integers(1, n + 1)), replace=False)).astype(np.uint32)
+    opay, osums = cpu.pack(t, C, src)
+    recv = np.full(max(db, 1), 0xA5, np.uint8)
+    cpu.unpack(t, C, opay, osums, recv)
+    expect = recv.copy()
+    nch, base, _, _ = cpu.plan(t, C)
+    for c in ids:  # scramble the listed chunks at the receiver
+        k = int(np.searchsorted(base, int(c), side="right") - 1)
+        j = int(c) - int(base[k])
+        nb = int(t[k]["numel"]) * (4 if int(t[k]["dtype"]) == 1 else 2)
+        o = int(t[k]["dst_offset"]) + j * C
+        ln = min(C, nb - j * C)
+        recv[o:o + ln] = rng.integers(0, 256, ln, dtype=np.uint8)
+    dpay, dsums = cpu.pack_chunks(t, C, src, ids)
+    g_src, g_recv = to_dev(src), to_dev(recv)
+    pb = plan.delta_layout(ids)
+    assert pb == dpay.size
+    payload = torch.full((max(pb, 16),), 0xEE, dtype=torch.uint8, device="cuda")
+    sums = torch.empty(ids.size, 2, dtype=torch.int64, device="cuda")
+    bad, nbad = torch.empty((ids.size + 31) // 32, dtype=torch.int32, device="cuda"), plan.empty_counter()
+    plan.pack_chunks(g_src, ids, payload, sums)
+    plan.unpack_chunks(payload, sums, ids, g_recv, bad, nbad)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(payload)[:pb], dpay), f"delta payload {tag}"
+    assert np.array_equal(sums_host(sums, ids.size), dsums), f"delta sums {tag}"
+    orecv = recv.copy()
+    obm, onbad = cpu.unpack_chunks(t, C, dpay, dsums, ids, orecv)
+    assert np.array_equal(to_host(g_recv), orecv) and int(nbad.item()) == onbad == 0, f"delta {tag}"
+    assert np.array_equal(orecv, expect), f"delta repair {tag}"
