@@ -148,3 +148,36 @@ def test_repair_llama8b_share_from_the_flagged_chunks():
     torch.cuda.synchronize()
     assert int(nbad.item()) == 0 and int(ndiff.item()) == 0 and torch.equal(recv, donor)
     log(f"repaired {ids.size} chunks with {pb} payload bytes")
+
+
+@pytest.mark.parametrize("k", [1, 3, 8])
+def test_striped_transfer_restores_like_one_payload(k):
+    """Multi-donor striping on one GPU: contiguous chunk ranges packed
+    separately (C >= 4 KiB) are byte slices of the full payload, and placed
+    at their offsets they form a buffer that one fr_unpack_state restores to
+    the oracle's receiver arena; the gaps between segments are never read."""
+    from tests.gpu_util import striped_payload, stripe_ranges
+
+    rng = np.random.default_rng(900 + k)
+    cases = []
+    for _ in range(4):
+        t, sb, db = W.random_tiny_table(rng, max_entries=10, max_numel=60_000)
+        cases.append((t, int(rng.choice([4096, 16384, 65536])), W.random_tiny_state(t, sb, rng), sb, db))
+    w = W.make_workload(0)
+    cases.append((w.table, w.chunk_bytes, W.fill_state(w), w.src_arena_bytes, w.dst_arena_bytes))
+    for t, C, src_np, sb, db in cases:
+        plan = F.Plan(t, C, sb, db)
+        src = to_dev(src_np) if src_np.size else torch.empty(16, dtype=torch.uint8, device="cuda")
+        recv, sums, parts = striped_payload(plan, t, src, stripe_ranges(plan.n_chunks, k))
+        opay, osums = cpu.pack(t, C, src_np)
+        for (a, b), off, sp, ss in parts:
+            assert np.array_equal(sums_host(ss, b - a), osums[2 * a:2 * b])
+            if off is not None:
+                assert np.array_equal(to_host(sp), opay[off:off + sp.numel()]), (a, b)
+        dst = torch.full((max(db, 1),), 0x5A, dtype=torch.uint8, device="cuda")
+        bad, nbad = plan.empty_bitmap(), plan.empty_counter()
+        plan.unpack(recv, sums, dst, bad, nbad)
+        odst = np.full(max(db, 1), 0x5A, np.uint8)
+        cpu.unpack(t, C, opay, osums, odst)
+        torch.cuda.synchronize()
+        assert int(nbad.item()) == 0 and np.array_equal(to_host(dst), odst)

@@ -283,3 +283,27 @@ def test_llama70b_stage0_sampled_parity(llama70b):
     r.unpack()
     assert r.bad_set() == exp
     assert int(r.n_bad.item()) == len(exp)
+
+
+@pytest.mark.timeout(900)
+def test_llama8b_striped_transfer_properties(llama8b):
+    """The 8B share sent as 7 stripes (one per donor over the seven xGMI
+    links of a node), each packed on its own: every stripe is the slice of
+    the whole pack's payload at its first chunk's offset with the whole
+    pack's sums, and the assembled buffer restores the state exactly."""
+    from tests.gpu_util import striped_payload, stripe_ranges
+
+    w, src_np = llama8b
+    t, C = w.table, w.chunk_bytes
+    r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes, canary=0xA5)
+    src = _upload(src_np)
+    r.pack(src)
+    recv, sums, parts = striped_payload(r.plan, t, src, stripe_ranges(r.n_chunks, 7))
+    torch.cuda.synchronize()
+    log("stripes packed")
+    for (a, b), off, sp, ss in parts:
+        assert torch.equal(ss, r.sums[a:b]), (a, b)
+        assert off is not None and torch.equal(sp, r.payload[off:off + sp.numel()]), (a, b)
+    r.unpack(payload=recv, sums=sums)
+    torch.cuda.synchronize()
+    assert int(r.n_bad.item()) == 0 and torch.equal(r.dst, src)

@@ -155,3 +155,71 @@ def test_c_oracle_equals_python_oracle_on_delta():
         mbad = mini.unpack_chunks(t, C, p.tobytes(), ms, [int(i) for i in ids], mrecv)
         assert recv.tobytes() == bytes(mrecv)
         assert set(cpu.bitmap_to_set(bm, ids.size)) == mbad and nbad == len(mbad)
+
+
+def _stripe_cuts(n, k, rng):
+    """k contiguous chunk ranges covering [0, n) (some may be empty)."""
+    cuts = np.sort(rng.integers(0, n + 1, size=k - 1)) if n else np.zeros(k - 1, np.int64)
+    edges = [0] + [int(c) for c in cuts] + [n]
+    return list(zip(edges[:-1], edges[1:]))
+
+
+def _chunk_payload_offset(t, C, c):
+    """Full-payload offset of global chunk c (None for a derived chunk)."""
+    _, base, pay, _ = cpu.plan(t, C)
+    k = int(np.searchsorted(base, c, side="right") - 1)
+    if int(t[k]["derive_from"]) >= 0:
+        return None
+    return int(pay[k]) + (c - int(base[k])) * C
+
+
+def test_stripes_are_slices_of_the_full_payload():
+    """With C >= 4 KiB every chunk starts on a 4 KiB boundary of the full
+    payload, so the delta payload of a contiguous chunk range (a stripe)
+    is the full payload's bytes from the range's first sent chunk on, and
+    its sums are the full sums of the range: stripes packed separately (one
+    per donor) and placed at those offsets form a buffer that a whole
+    unpack restores exactly (it never reads the gaps between segments)."""
+    rng = np.random.default_rng(313)
+    cases = []
+    for _ in range(20):
+        t, sb, db = W.random_tiny_table(rng, max_entries=10, max_numel=60_000)
+        cases.append((t, int(rng.choice([4096, 16384, 65536])), W.random_tiny_state(t, sb, rng), db))
+    w = W.make_workload(0)
+    cases.append((w.table, w.chunk_bytes, W.fill_state(w), w.dst_arena_bytes))
+    for t, C, src, db in cases:
+        fp, fs = cpu.pack(t, C, src)
+        n = cpu.n_chunks(t, C)
+        buf = np.full(fp.size, 0xEE, np.uint8)  # gap bytes never written
+        got_sums = np.zeros_like(fs)
+        for a, b in _stripe_cuts(n, int(rng.integers(1, 9)), rng):
+            ids = np.arange(a, b, dtype=np.uint32)
+            dp, ds = cpu.pack_chunks(t, C, src, ids)
+            assert np.array_equal(ds, fs[2 * a:2 * b])
+            got_sums[2 * a:2 * b] = ds
+            offs = [o for o in (_chunk_payload_offset(t, C, int(c)) for c in ids) if o is not None]
+            if not offs:  # only derived chunks: nothing on the wire
+                assert dp.size == 0
+                continue
+            assert np.array_equal(dp, fp[offs[0]:offs[0] + dp.size]), (a, b)
+            buf[offs[0]:offs[0] + dp.size] = dp
+        ref = np.zeros(max(db, 1), np.uint8)
+        cpu.unpack(t, C, fp, fs, ref)
+        dst = np.zeros(max(db, 1), np.uint8)
+        bm, nbad = cpu.unpack(t, C, buf, got_sums, dst)
+        assert nbad == 0 and np.array_equal(dst, ref)
+
+
+def test_stripes_below_4k_chunks_are_not_slices():
+    """The slice property needs C >= 4 KiB: with smaller chunks a stripe
+    starting inside an entry is not 4 KiB-aligned in the full payload, so
+    the next entry's segment lands elsewhere (the reading is checked, not
+    assumed)."""
+    t = np.array([(0, 0, 3000, W.F32, -1), (12288, 12288, 3000, W.F32, -1)], dtype=W.TABLE_DTYPE)
+    C = 1024
+    src = np.arange(24576, dtype=np.uint32).astype(np.uint8)
+    fp, _ = cpu.pack(t, C, src)
+    ids = np.arange(1, cpu.n_chunks(t, C), dtype=np.uint32)  # from chunk 1 of entry 0
+    dp, _ = cpu.pack_chunks(t, C, src, ids)
+    off = _chunk_payload_offset(t, C, 1)
+    assert off == 1024 and not np.array_equal(dp, fp[off:off + dp.size])
