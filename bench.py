@@ -23,6 +23,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -162,8 +163,6 @@ def control_plane(reps=21):
     latencies through the Python binding (medians; microseconds).  The 8
     ranks of one node fail in forward of step 41; every normal rank then
     reports 41."""
-    import statistics
-
     import numpy as np
 
     from paper_2509_03047_amd import flashrestore as F
@@ -371,7 +370,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     total_ms = start.elapsed_time(end)
-    per_op = {op: sum(e[i].elapsed_time(e[i + 1]) for e in evs) / args.steps for i, op in enumerate(ops)}
+    op_ms = {op: [e[i].elapsed_time(e[i + 1]) for e in evs] for i, op in enumerate(ops)}
+    per_op = {op: sum(v) / len(v) for op, v in op_ms.items()}
 
     # the pass restored the state exactly: nothing flagged, receiver == sender
     ok = int(nbad.item()) == 0 and int(ndiff.item()) == 0
@@ -384,8 +384,9 @@ def main():
     op_report = {}
     for op in ops:
         gbs = alg[op] / (per_op[op] * 1e-3) / 1e9
-        op_report[op] = {"ms": round(per_op[op], 4), "alg_bytes": alg[op], "hbm_gbs": round(gbs, 1),
-                         "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
+        op_report[op] = {"ms": round(per_op[op], 4), "ms_median": round(statistics.median(op_ms[op]), 4),
+                         "ms_min": round(min(op_ms[op]), 4), "alg_bytes": alg[op],
+                         "hbm_gbs": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
     restore_ms = per_op["pack"] + per_op["unpack"]
     dom = max(ops, key=lambda o: per_op[o])
     roof = {"bound": "hbm", "kernel": KERNEL_NAMES[dom], "op": dom,

@@ -480,8 +480,10 @@ __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units,
 //   kFlags:   bit c = (flags[c] != 0); optional folds of two
 //             accumulator sets into sums_a / sums_b             (verify)
 // Bitmap words are written whole from wave ballots (lanes 0 and 32 each own
-// one 32-bit word), so the bitmap needs no clearing; the count takes one
-// atomic add per wave with a set bit.
+// one 32-bit word), so the bitmap needs no clearing.  The count is summed
+// per workgroup and added with one atomic per workgroup with a set bit
+// (one per wave serialises on the counter when many chunks differ: 30 us
+// for 4,096 flipped chunks of the 8B share).
 enum FinalMode { kFold = 0, kCompare = 1, kFlags = 2 };
 
 struct FinalArgs {
@@ -507,10 +509,14 @@ __device__ __forceinline__ fr_chunk_sum fold(const fr_chunk_sum* acc, u64 c, uin
   return fr_chunk_sum{s, ws};
 }
 
+constexpr int kFinalThreads = 1024;
+
 template <int kMode>
-__global__ __launch_bounds__(256) void k_finalize(FinalArgs f) {
+__global__ __launch_bounds__(kFinalThreads) void k_finalize(FinalArgs f) {
+  __shared__ u64 wave_count[kFinalThreads / 64];
   const uint32_t lane = threadIdx.x & 63;
   const u64 stride = u64(gridDim.x) * blockDim.x;
+  u64 count = 0;  // set bits seen by this wave (uniform)
   for (u64 base = u64(blockIdx.x) * blockDim.x + (threadIdx.x & ~63u); base < f.n_chunks;
        base += stride) {
     const u64 c = base + lane;
@@ -535,7 +541,16 @@ __global__ __launch_bounds__(256) void k_finalize(FinalArgs f) {
     const u64 w = base >> 5;  // base is a multiple of 64: two words per wave
     if (lane == 0) f.bitmap[w] = uint32_t(mask);
     if (lane == 32 && base + 32 < f.n_chunks) f.bitmap[w + 1] = uint32_t(mask >> 32);
-    if (lane == 0 && mask) atomicAdd(f.count, u64(__popcll(mask)));
+    count += u64(__popcll(mask));
+  }
+  if (kMode == kFold) return;  // uniform over the grid
+  if (lane == 0) wave_count[threadIdx.x >> 6] = count;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    u64 t = 0;
+#pragma unroll
+    for (int i = 0; i < kFinalThreads / 64; i++) t += wave_count[i];
+    if (t) atomicAdd(f.count, t);
   }
 }
 
@@ -606,11 +621,11 @@ inline Walk walk_for(uint64_t C, uint32_t tile_bytes, const SlotTable& t) {
 inline int launch_finalize(int mode, const FinalArgs& f, hipStream_t st) {
   if (f.n_chunks == 0) return 0;
   const u64 waves = (u64(f.n_chunks) + 63) / 64;
-  const u64 want = (waves + 3) / 4;
-  const dim3 grid(uint32_t(want < 8192 ? want : 8192));
-  if (mode == kFold) hipLaunchKernelGGL(k_finalize<kFold>, grid, dim3(256), 0, st, f);
-  else if (mode == kCompare) hipLaunchKernelGGL(k_finalize<kCompare>, grid, dim3(256), 0, st, f);
-  else hipLaunchKernelGGL(k_finalize<kFlags>, grid, dim3(256), 0, st, f);
+  const u64 want = (waves + kFinalThreads / 64 - 1) / (kFinalThreads / 64);
+  const dim3 grid(uint32_t(want < 2048 ? want : 2048)), block(kFinalThreads);
+  if (mode == kFold) hipLaunchKernelGGL(k_finalize<kFold>, grid, block, 0, st, f);
+  else if (mode == kCompare) hipLaunchKernelGGL(k_finalize<kCompare>, grid, block, 0, st, f);
+  else hipLaunchKernelGGL(k_finalize<kFlags>, grid, block, 0, st, f);
   return int(hipGetLastError());
 }
 
