@@ -290,11 +290,11 @@ class Plan:
     def pack(self, src, payload, sums, stream=None, payload_cap=None):
         return fr_pack_state(self, src, payload, payload_cap, sums, stream)
 
-    def unpack(self, payload, sums, dst, bitmap, n_bad, stream=None):
-        return fr_unpack_state(self, payload, sums, dst, bitmap, n_bad, stream)
+    def unpack(self, payload, sums, dst, bitmap, n_bad, stream=None, sync=False):
+        return fr_unpack_state(self, payload, sums, dst, bitmap, n_bad, stream, sync)
 
-    def verify_replicas(self, a, b, bitmap, n_diff, sums_a=None, sums_b=None, stream=None):
-        return fr_verify_replicas(self, a, b, bitmap, n_diff, sums_a, sums_b, stream)
+    def verify_replicas(self, a, b, bitmap, n_diff, sums_a=None, sums_b=None, stream=None, sync=False):
+        return fr_verify_replicas(self, a, b, bitmap, n_diff, sums_a, sums_b, stream, sync)
 
     def checksum_state(self, base, sums, stream=None):
         return fr_checksum_state(self, base, sums, stream)
@@ -305,8 +305,28 @@ class Plan:
     def pack_chunks(self, src, chunk_ids, payload, sums, stream=None, payload_cap=None):
         return fr_pack_chunks(self, src, chunk_ids, payload, payload_cap, sums, stream)
 
-    def unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream=None, payload_bytes=None):
-        return fr_unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream, payload_bytes)
+    def unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream=None, payload_bytes=None,
+                      sync=False):
+        return fr_unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream, payload_bytes, sync)
+
+
+def _synced_bits(bitmap, n: int, stream) -> np.ndarray:
+    """Wait for `stream` (None: the current stream; an int handle: the whole
+    device), then return the sorted indices of the set bits of `bitmap`.
+    The ``sync=True`` form of the operations that produce a bitmap."""
+    import torch
+
+    if n == 0:
+        return np.zeros(0, dtype=np.int64)
+    if not hasattr(bitmap, "detach"):
+        raise ValueError("sync=True needs the bitmap as a tensor")
+    if stream is None:
+        torch.cuda.current_stream().synchronize()
+    elif isinstance(stream, int):
+        torch.cuda.synchronize()
+    else:
+        stream.synchronize()
+    return bitmap_indices(bitmap, n)
 
 
 def _nbytes(x):
@@ -336,17 +356,22 @@ def fr_pack_state(plan: Plan, src, payload, payload_cap, sums, stream=None) -> N
            "fr_pack_state")
 
 
-def fr_unpack_state(plan: Plan, payload, sums, dst, bad_bitmap, n_bad, stream=None) -> None:
+def fr_unpack_state(plan: Plan, payload, sums, dst, bad_bitmap, n_bad, stream=None, sync=False):
+    """Enqueue the unpack; with sync=True wait for it and return the sorted
+    ids of the chunks that failed verification (else None)."""
     i = plan.info
     _check(_lib.fr_unpack_state(plan.handle, _dev(payload, i["payload_bytes"], "payload"),
                                 _dev(sums, SUM_BYTES * i["n_chunks"], "sums"),
                                 _dev(dst, i["dst_arena_bytes"], "dst"),
                                 _dev(bad_bitmap, 4 * i["bitmap_words"], "bad_bitmap"),
                                 _dev(n_bad, 8, "n_bad"), _stream(stream)), "fr_unpack_state")
+    return _synced_bits(bad_bitmap, i["n_chunks"], stream) if sync else None
 
 
 def fr_verify_replicas(plan: Plan, base_a, base_b, diff_bitmap, n_diff, sums_a=None, sums_b=None,
-                       stream=None) -> None:
+                       stream=None, sync=False):
+    """Enqueue the replica compare; with sync=True wait for it and return the
+    sorted ids of the chunks that differ (else None)."""
     i = plan.info
     sb = SUM_BYTES * i["n_chunks"]
     _check(_lib.fr_verify_replicas(plan.handle, _dev(base_a, i["src_arena_bytes"], "base_a"),
@@ -354,6 +379,7 @@ def fr_verify_replicas(plan: Plan, base_a, base_b, diff_bitmap, n_diff, sums_a=N
                                    _dev(diff_bitmap, 4 * i["bitmap_words"], "diff_bitmap"),
                                    _dev(n_diff, 8, "n_diff"), _dev(sums_a, sb, "sums_a"),
                                    _dev(sums_b, sb, "sums_b"), _stream(stream)), "fr_verify_replicas")
+    return _synced_bits(diff_bitmap, i["n_chunks"], stream) if sync else None
 
 
 def fr_checksum_state(plan: Plan, base, sums, stream=None) -> None:
@@ -390,10 +416,11 @@ def fr_pack_chunks(plan: Plan, src, chunk_ids, payload, payload_cap, sums, strea
 
 
 def fr_unpack_chunks(plan: Plan, payload, sums, chunk_ids, dst, bad_bitmap, n_bad, stream=None,
-                     payload_bytes=None) -> None:
+                     payload_bytes=None, sync=False):
     """payload_bytes: bytes readable at payload (default: the tensor's size,
     else the list's fr_delta_layout bytes); the library refuses less than the
-    list needs."""
+    list needs.  With sync=True wait and return the sorted list positions
+    that failed verification (else None)."""
     ids = _ids(chunk_ids)
     if payload_bytes is None:
         payload_bytes = _nbytes(payload)
@@ -405,6 +432,7 @@ def fr_unpack_chunks(plan: Plan, payload, sums, chunk_ids, dst, bad_bitmap, n_ba
                                  _dev(dst, plan.info["dst_arena_bytes"], "dst"),
                                  _dev(bad_bitmap, 4 * ((ids.size + 31) // 32), "bad_bitmap"),
                                  _dev(n_bad, 8, "n_bad"), _stream(stream)), "fr_unpack_chunks")
+    return _synced_bits(bad_bitmap, ids.size, stream) if sync else None
 
 
 class Tracker:

@@ -168,3 +168,47 @@ def test_binding_rejects_short_or_strided_tensors(setup):
                    None, need - 16) == -3
     torch.cuda.synchronize()
     assert torch.equal(dst, snap)
+
+
+def test_sync_returns_the_sorted_flagged_chunks(setup):
+    """sync=True waits for the operation (on its own stream too) and returns
+    the sorted ids of the flagged chunks: unpack, replica compare and delta
+    unpack (list positions)."""
+    w, plan, src = setup
+    payload, sums = plan.empty_payload(), plan.empty_sums()
+    plan.pack(src, payload, sums)
+    rng = np.random.default_rng(5)
+    bits = rng.choice(plan.payload_bytes * 8, size=6, replace=False)
+    for b in bits:
+        payload[int(b) // 8] ^= 1 << (int(b) % 8)
+    dst = torch.empty(w.dst_arena_bytes, dtype=torch.uint8, device="cuda")
+    bad, nbad = plan.empty_bitmap(), plan.empty_counter()
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        got = plan.unpack(payload, sums, dst, bad, nbad, stream=s, sync=True)
+    expect = F.bitmap_indices(bad, plan.n_chunks)
+    # a flipped master byte also flags the parameter chunk re-derived from it
+    assert list(got) == sorted(set(int(x) for x in expect)) and 1 <= len(got) <= 12
+    assert plan.unpack(payload, sums, dst, bad, nbad) is None  # without sync: nothing returned
+    replica = src.clone()
+    replica[123457] ^= 4
+    replica[9_000_001] ^= 1
+    diff, nd = plan.empty_bitmap(), plan.empty_counter()
+    got = plan.verify_replicas(src, replica, diff, nd, sync=True)
+    assert list(got) == sorted({plan.chunk_of(*_entry_byte(w, 123457)), plan.chunk_of(*_entry_byte(w, 9_000_001))})
+    ids = np.array(got, dtype=np.uint32)
+    dp = torch.empty(max(plan.delta_layout(ids), 16), dtype=torch.uint8, device="cuda")
+    ds = torch.empty(ids.size, 2, dtype=torch.int64, device="cuda")
+    plan.pack_chunks(src, ids, dp, ds)
+    ds[ids.size - 1, 1] ^= 1  # the last listed chunk's sums no longer match
+    db = torch.empty(1, dtype=torch.int32, device="cuda")
+    assert list(plan.unpack_chunks(dp, ds, ids, replica, db, nd, sync=True)) == [ids.size - 1]
+    assert list(plan.unpack_chunks(dp, ds, ids[:0], replica, None, nd, sync=True)) == []
+
+
+def _entry_byte(w, arena_byte):
+    """(entry, byte in entry) of a sender-arena byte."""
+    starts = w.table["src_offset"].astype(np.int64)
+    e = int(np.searchsorted(starts, arena_byte, side="right") - 1)
+    return e, arena_byte - int(starts[e])
