@@ -143,7 +143,7 @@ def cpu_baseline(w, src_np, seconds: float):
         cs = cpu.checksum(sub, C, replica)
         reps += 1
         el = time.perf_counter() - t0
-        if el >= seconds or reps >= 20:
+        if el >= seconds or reps >= 100:
             break
     assert nbad == 0 and nd == 0 and np.array_equal(cs, sums)
     what = f"{n_ent // 4} logical tensors" if step == 4 else "entries in table order"
