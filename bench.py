@@ -295,9 +295,9 @@ def restored_equals(w, src, dst) -> bool:
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the restore shards per rank; see the sharding notes). Run with --gpus 1.",
-              file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU transport "
+              "(a restore shards per rank: each GPU packs or unpacks its own share). "
+              "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
