@@ -64,6 +64,11 @@
  *   concurrently (issue them on one stream, or order the streams), and one
  *   plan must not be used from several host threads at once; use one plan per
  *   concurrent stream.
+ *   Graph capture.  The four whole-state operations enqueue kernel launches
+ *   only (no memset, no host copy), so a capture of them into a HIP graph
+ *   replays the same work.  The delta calls below copy per-call unit records
+ *   from the plan's host staging, which the next delta call overwrites: they
+ *   are not for capture.
  */
 #ifndef FLASHRESTORE_H
 #define FLASHRESTORE_H
