@@ -2,7 +2,8 @@
  * A plain C program that drives libflashrestore through its C ABI with raw
  * HIP device memory and a HIP stream (no Python, no torch): restore a small
  * state across differing sender and receiver layouts, compare two replicas,
- * checksum, and check every output byte against the C oracle.  Test
+ * checksum, repair the diverged replica by a delta, and check every output
+ * byte against the C oracle.  Test
  * infrastructure: built by the package build, run by
  * tests/test_gpu_c_abi.py.
  */
@@ -189,13 +190,62 @@ int main(void) {
   for (uint64_t c = 0; c < n; c++)
     CHECK(((g_bm[c / 32] >> (c % 32)) & 1u) == (c == chunk), "the flipped chunk is flagged");
 
+  /* delta repair: re-send the flagged chunk and a derived parameter chunk
+   * (recomputed from the receiver's master) into the diverged replica.
+   * Replicas share the donor's layout, so the repair plan's receiver layout
+   * is the sender's (chunk ids are the same in both plans). */
+  fr_tensor_desc t2[N_ENTRIES];
+  oro_entry o2[N_ENTRIES];
+  memcpy(t2, t, sizeof t);
+  memcpy(o2, o, sizeof o);
+  for (int e = 0; e < N_ENTRIES; e++) t2[e].dst_offset = o2[e].dst_offset = t[e].src_offset;
+  fr_plan* rplan = NULL;
+  FR(fr_plan_create(t2, N_ENTRIES, C, src_bytes, src_bytes, &rplan));
+  const uint32_t ids[2] = {0u, (uint32_t)chunk};
+  uint64_t dpb = 0, o_dpb = 0, o_doff[2];
+  FR(fr_delta_layout(rplan, ids, 2, &dpb));
+  CHECK(oro_delta_layout(o2, N_ENTRIES, C, ids, 2, o_doff, &o_dpb) == 0 && dpb == o_dpb,
+        "delta payload size equals the oracle's");
+  uint8_t* o_dpay = calloc(dpb, 1);
+  uint64_t o_dsums[4];
+  CHECK(o_dpay && oro_pack_chunks(o2, N_ENTRIES, C, src, ids, 2, o_dpay, o_dsums) == 0,
+        "oracle delta pack");
+  void* d_dpay;
+  fr_chunk_sum* d_dsums;
+  uint32_t* d_dbm;
+  HIP(hipMalloc(&d_dpay, dpb));
+  HIP(hipMalloc((void**)&d_dsums, 2 * sizeof(fr_chunk_sum)));
+  HIP(hipMalloc((void**)&d_dbm, 4));
+  CHECK(fr_unpack_chunks(plan, d_dpay, dpb, d_dsums, ids, 2, d_rep, d_dbm, d_nbad, s) ==
+            FR_E_RANGE, "a replica arena smaller than the plan's receiver arena");
+  CHECK(fr_unpack_chunks(rplan, d_dpay, dpb - 16, d_dsums, ids, 2, d_rep, d_dbm, d_nbad, s) ==
+            FR_E_RANGE, "delta payload shorter than the list needs");
+  FR(fr_pack_chunks(rplan, d_src, ids, 2, d_dpay, dpb, d_dsums, s));
+  FR(fr_unpack_chunks(rplan, d_dpay, dpb, d_dsums, ids, 2, d_rep, d_dbm, d_nbad, s));
+  HIP(hipStreamSynchronize(s));
+  uint8_t* g_dpay = malloc(dpb);
+  uint64_t g_dsums[4];
+  uint8_t* g_rep = malloc(src_bytes);
+  CHECK(g_dpay && g_rep, "host allocation");
+  HIP(hipMemcpy(g_dpay, d_dpay, dpb, hipMemcpyDeviceToHost));
+  HIP(hipMemcpy(g_dsums, d_dsums, 32, hipMemcpyDeviceToHost));
+  HIP(hipMemcpy(g_rep, d_rep, src_bytes, hipMemcpyDeviceToHost));
+  HIP(hipMemcpy(&g_nbad, d_nbad, 8, hipMemcpyDeviceToHost));
+  CHECK(memcmp(g_dpay, o_dpay, dpb) == 0 && memcmp(g_dsums, o_dsums, 32) == 0,
+        "delta payload and sums equal the oracle's");
+  CHECK(g_nbad == 0 && memcmp(g_rep, src, src_bytes) == 0, "the replica is repaired");
+  FR(fr_plan_destroy(rplan));
+  hipFree(d_dpay), hipFree(d_dsums), hipFree(d_dbm);
+  free(o_dpay), free(g_dpay), free(g_rep);
+
   FR(fr_plan_destroy(plan));
   HIP(hipStreamDestroy(s));
   hipFree(d_src), hipFree(d_rep), hipFree(d_dst), hipFree(d_pay), hipFree(d_sums);
   hipFree(d_csum), hipFree(d_bm), hipFree(d_diff), hipFree(d_nbad), hipFree(d_ndiff);
   free(src), free(o_pay), free(o_sums), free(o_dst), free(o_bm);
   free(g_pay), free(g_sums), free(g_csum), free(g_dst), free(g_bm);
-  printf("c abi ok: %llu chunks, %llu payload bytes, chunk %llu located\n", (unsigned long long)n,
-         (unsigned long long)pb, (unsigned long long)chunk);
+  printf("c abi ok: %llu chunks, %llu payload bytes, chunk %llu located and repaired (%llu delta bytes)\n",
+         (unsigned long long)n, (unsigned long long)pb, (unsigned long long)chunk,
+         (unsigned long long)dpb);
   return 0;
 }
