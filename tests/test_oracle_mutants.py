@@ -1,0 +1,288 @@
+"""Planted mistakes in the oracle are caught by its pins (CPU only).
+
+Each mutant is a fresh copy of the Python oracle (``oracle/mini.py``) with
+one plausible mistake planted in it: a dropped or shifted term, a wrong
+index, a byte order, a modulus, a rounding rule, a layout constant, padding
+left dirty.  The pins that fix the oracle from outside it (hand-worked
+values in tests/golden, closed forms, numpy's modular sums, torch's bf16
+cast, exhaustive detection properties, independently built payloads, the
+restore round trip) must accept the unmodified oracle and reject every
+mutant: no plausible single mistake survives them."""
+import importlib.util
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import mini
+from paper_2509_03047_amd import workloads as W
+
+from tests.test_oracle_pins import _golden_frsum, _golden_rne
+
+M64 = (1 << 64) - 1
+MINI_PATH = mini.__file__
+
+
+def _fresh_mini(tag):
+    spec = importlib.util.spec_from_file_location(f"mini_mutant_{tag}", MINI_PATH)
+    m = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(m)
+    return m
+
+
+# ---------------------------------------------------------------- pins
+
+def frsum_pins(f, golden_dir):
+    """Names of the FRSUM pins that `f` (bytes -> (sum, wsum)) fails."""
+    failed = []
+    if any(f(d) != (s, ws) for d, s, ws in _golden_frsum(golden_dir) if len(d) <= 65536):
+        failed.append("golden")
+    rng = np.random.default_rng(11)
+    for n_words in (1, 3, 64, 1000):
+        w = rng.integers(0, 1 << 32, size=n_words, dtype=np.uint64)
+        with np.errstate(over="ignore"):
+            s = int(np.sum(w, dtype=np.uint64))
+            ws = int(np.sum(w * np.arange(1, n_words + 1, dtype=np.uint64), dtype=np.uint64))
+        if f(w.astype("<u4").tobytes()) != (s, ws):
+            failed.append("numpy")
+            break
+    n = 131072  # wsum of all-ones words wraps past 2^64 here
+    if f(b"\xff" * (4 * n)) != ((n * 0xFFFFFFFF) & M64, (0xFFFFFFFF * n * (n + 1) // 2) & M64):
+        failed.append("closed form")
+    x = rng.integers(0, 256, size=200, dtype=np.uint8).tobytes()
+    s0, ws0 = f(x)
+    if f(bytes(20) + x) != (s0, (ws0 + 5 * s0) & M64):
+        failed.append("shift law")
+    if f(x[:198]) != f(x[:198] + b"\0\0") or f(b"\x80\x3f") != (16256, 16256):
+        failed.append("bf16 tail")
+    base = rng.integers(0, 256, size=16, dtype=np.uint8)
+    ref = f(base.tobytes())
+    for a in range(128):
+        va = base.copy()
+        va[a // 8] ^= np.uint8(1 << (a % 8))
+        if f(va.tobytes())[0] == ref[0]:
+            failed.append("single flips")
+            break
+        if any(f(_flip(va, b).tobytes()) == ref for b in range(a + 1, 128)):
+            failed.append("double flips")
+            break
+    return failed
+
+
+def _flip(v, bit):
+    v = v.copy()
+    v[bit // 8] ^= np.uint8(1 << (bit % 8))
+    return v
+
+
+def rne_pins(r, golden_dir):
+    """Names of the rounding pins that `r` (fp32 bits -> bf16 bits) fails."""
+    failed = []
+    if any(r(u) != h for u, h in _golden_rne(golden_dir)):
+        failed.append("golden")
+    rng = np.random.default_rng(18)
+    u = rng.integers(0, 1 << 32, size=4000, dtype=np.uint64).astype(np.uint32)
+    # ties, denormals and values near overflow are rare among random
+    # patterns: add them
+    ties = (rng.integers(0, 1 << 16, size=500, dtype=np.uint64).astype(np.uint32) << np.uint32(16)) | np.uint32(0x8000)
+    den = rng.integers(0, 1 << 23, size=500, dtype=np.uint64).astype(np.uint32)
+    big = rng.integers(0x7F7F0000, 0x7F800000, size=500, dtype=np.uint64).astype(np.uint32)  # near overflow
+    u = np.concatenate([u, ties, den, den | np.uint32(0x80000000), big, big | np.uint32(0x80000000)])
+    u = u[(u & np.uint32(0x7FFFFFFF)) <= np.uint32(0x7F800000)]  # non-NaN
+    ref = torch.from_numpy(u.view(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    if any(r(int(a)) != int(b) for a, b in zip(u, ref)):
+        failed.append("torch cast")
+    nan = [0x7F800001, 0xFF800001, 0x7FC00000, 0x7FFFFFFF, 0xFFA00000]
+    if any(r(x) != ((x >> 16) | 0x40) for x in nan):
+        failed.append("NaN reading")
+    return failed
+
+
+def layout_pins(m):
+    """Names of the plan / pack / unpack pins that module `m` fails."""
+    failed = []
+    w = W.make_workload(0)  # table only: its closed forms need no state
+    _, base, _, pb = m.plan(w.table, w.chunk_bytes)
+    if pb != 12 * w.n_params + (5 * 3 - 1) * 3072 or base[-1] != 804:
+        failed.append("toy closed form")
+    rng = np.random.default_rng(21)
+    for _ in range(20):
+        t, sb, db = W.random_tiny_table(rng)
+        src = W.random_tiny_state(t, sb, rng).tobytes()
+        payload, _ = m.pack(t, 64, src)
+        exp = bytearray()
+        for e in t:
+            if int(e["derive_from"]) >= 0:
+                continue
+            o, n = int(e["src_offset"]), int(e["numel"]) * W.ESIZE[int(e["dtype"])]
+            if n:
+                exp += bytes(-len(exp) % 4096)
+                exp += src[o:o + n]
+        exp += bytes(-len(exp) % 16)
+        if bytes(payload) != bytes(exp):
+            failed.append("concatenation")
+            break
+    t, nb = W.state_table([("a", 40), ("b", 3), ("c", 17)])
+    src = W.random_tiny_state(t, nb, np.random.default_rng(23)).tobytes()
+    payload, sums = m.pack(t, 32, src)
+    dst = bytearray(nb)
+    bad = m.unpack(t, 32, payload, sums, dst)
+    if bad or bytes(dst) != src:
+        failed.append("round trip")
+    return failed
+
+
+# ------------------------------------------------------------- mutants
+
+def _frsum_with(word, weight, mask_s=M64, mask_ws=M64, tail=True, swap=False):
+    def f(b):
+        s = ws = 0
+        step = 4
+        n = len(b) if tail else len(b) - len(b) % 4
+        for i in range(0, n, step):
+            w = word(b[i:i + 4].ljust(4, b"\0"))
+            s += w
+            ws += weight(i) * w
+        out = (s & mask_s, ws & mask_ws)
+        return out[::-1] if swap else out
+    return f
+
+
+LE = lambda c: int.from_bytes(c, "little")  # noqa: E731
+FRSUM_MUTANTS = {
+    "weight is the 0-based index": _frsum_with(LE, lambda i: i // 4),
+    "weight is the byte offset + 1": _frsum_with(LE, lambda i: i + 1),
+    "big-endian words": _frsum_with(lambda c: int.from_bytes(c, "big"), lambda i: i // 4 + 1),
+    "sum kept mod 2^32": _frsum_with(LE, lambda i: i // 4 + 1, mask_s=0xFFFFFFFF),
+    "no wrap mod 2^64": _frsum_with(LE, lambda i: i // 4 + 1, mask_s=-1, mask_ws=-1),
+    "short last word dropped": _frsum_with(LE, lambda i: i // 4 + 1, tail=False),
+    "outputs swapped": _frsum_with(LE, lambda i: i // 4 + 1, swap=True),
+    "16-bit words": lambda b: _frsum16(b),
+}
+
+
+def _frsum16(b):
+    s = ws = 0
+    for i in range(0, len(b), 2):
+        w = int.from_bytes(b[i:i + 2].ljust(2, b"\0"), "little")
+        s += w
+        ws += (i // 2 + 1) * w
+    return s & M64, ws & M64
+
+
+def _nan_rule(u, h):
+    return ((u >> 16) | 0x40) if (u & 0x7FFFFFFF) > 0x7F800000 else h
+
+
+RNE_MUTANTS = {
+    "truncation": lambda u: _nan_rule(u, u >> 16),
+    "ties away from zero": lambda u: _nan_rule(u, (u + 0x8000) >> 16),
+    "ties to odd": lambda u: _nan_rule(u, (u + 0x7FFF + (1 - ((u >> 16) & 1))) >> 16),
+    "denormals flushed": lambda u: _nan_rule(
+        u, (u >> 16) & 0x8000 if (u & 0x7F800000) == 0 else (u + 0x7FFF + ((u >> 16) & 1)) >> 16),
+    "overflow saturates": lambda u: _nan_rule(u, min((u + 0x7FFF + ((u >> 16) & 1)) >> 16, 0x7F7F | (u >> 16 & 0x8000))
+                                              if (u & 0x7FFFFFFF) < 0x7F800000 else u >> 16),
+    "canonical NaN": lambda u: 0x7FC0 if (u & 0x7FFFFFFF) > 0x7F800000 else (u + 0x7FFF + ((u >> 16) & 1)) >> 16,
+    "NaN not quieted": lambda u: (u >> 16) if (u & 0x7FFFFFFF) > 0x7F800000 else (u + 0x7FFF + ((u >> 16) & 1)) >> 16,
+}
+
+
+def _mutant_segment_16(m):
+    m.SEGMENT = 16
+
+
+def _mutant_floor_chunks(m):
+    orig = m.plan
+
+    def plan(table, C):
+        nch, base, pay, pb = orig(table, C)
+        nch = [int(e["numel"]) * m._esize(int(e["dtype"])) // C for e in table]
+        base = [0]
+        for x in nch:
+            base.append(base[-1] + x)
+        return nch, base, pay, pb
+    m.plan = plan
+
+
+def _mutant_derived_sent(m):
+    def plan(table, C):
+        nch, base, pay = [], [0], []
+        end = 0
+        for e in table:
+            nb = int(e["numel"]) * m._esize(int(e["dtype"]))
+            nch.append(-(-nb // C))
+            base.append(base[-1] + nch[-1])
+            pay.append(m._up(end, m.SEGMENT) if nb else m._up(end, 16))
+            end = pay[-1] + nb if nb else end
+        return nch, base, pay, m._up(end, 16)
+    m.plan = plan
+
+
+def _mutant_dirty_padding(m):
+    orig = m.pack
+
+    def pack(table, C, src):
+        payload, sums = orig(table, C, src)
+        p = bytearray(payload)
+        _, _, pay, _ = m.plan(table, C)
+        used = bytearray(len(p))
+        for k, e in enumerate(table):
+            if pay[k] is not None:
+                nb = int(e["numel"]) * m._esize(int(e["dtype"]))
+                used[pay[k]:pay[k] + nb] = b"\1" * nb
+        for i in range(len(p)):
+            if not used[i]:
+                p[i] = 0xFF
+        return bytes(p), sums
+    m.pack = pack
+
+
+def _mutant_unrounded_end(m):
+    orig = m.plan
+
+    def plan(table, C):
+        nch, base, pay, pb = orig(table, C)
+        end = max([p + int(e["numel"]) * m._esize(int(e["dtype"]))
+                   for p, e in zip(pay, table) if p is not None] + [0])
+        return nch, base, pay, end
+    m.plan = plan
+
+
+def _mutant_truncating_rederive(m):
+    m.rne_bf16 = lambda u: u >> 16
+
+
+LAYOUT_MUTANTS = {
+    "segments on 16-byte boundaries": _mutant_segment_16,
+    "chunk count rounded down": _mutant_floor_chunks,
+    "derived entries sent": _mutant_derived_sent,
+    "padding not zeroed": _mutant_dirty_padding,
+    "payload end not rounded to 16": _mutant_unrounded_end,
+    "parameters re-derived by truncation": _mutant_truncating_rederive,
+}
+
+
+# --------------------------------------------------------------- tests
+
+def test_pins_accept_the_oracle(golden_dir):
+    assert frsum_pins(mini.frsum, golden_dir) == []
+    assert rne_pins(mini.rne_bf16, golden_dir) == []
+    assert layout_pins(_fresh_mini("clean")) == []
+
+
+@pytest.mark.parametrize("name", sorted(FRSUM_MUTANTS))
+def test_frsum_mutant_is_caught(name, golden_dir):
+    assert frsum_pins(FRSUM_MUTANTS[name], golden_dir), name
+
+
+@pytest.mark.parametrize("name", sorted(RNE_MUTANTS))
+def test_rne_mutant_is_caught(name, golden_dir):
+    assert rne_pins(RNE_MUTANTS[name], golden_dir), name
+
+
+@pytest.mark.parametrize("name", sorted(LAYOUT_MUTANTS))
+def test_layout_mutant_is_caught(name):
+    m = _fresh_mini(name.replace(" ", "_"))
+    LAYOUT_MUTANTS[name](m)
+    assert layout_pins(m), name
