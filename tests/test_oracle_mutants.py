@@ -3,7 +3,7 @@
 Each mutant is a fresh copy of the Python oracle (``oracle/mini.py``) with
 one plausible mistake planted in it: a dropped or shifted term, a wrong
 index, a byte order, a modulus, a rounding rule, a layout constant, padding
-left dirty.  The pins that fix the oracle from outside it (hand-worked
+left dirty, a delta layout or re-derivation order.  The pins that fix the oracle from outside it (hand-worked
 values in tests/golden, closed forms, numpy's modular sums, torch's bf16
 cast, exhaustive detection properties, independently built payloads, the
 restore round trip) must accept the unmodified oracle and reject every
@@ -286,3 +286,107 @@ def test_layout_mutant_is_caught(name):
     m = _fresh_mini(name.replace(" ", "_"))
     LAYOUT_MUTANTS[name](m)
     assert layout_pins(m), name
+
+
+# ----------------------------------------------------------- delta repair
+
+def delta_pins(m):
+    """Names of the delta-repair pins that module `m` fails."""
+    failed = []
+    rng = np.random.default_rng(61)
+    for _ in range(30):
+        t, sb, db = W.random_tiny_table(rng, max_numel=120)
+        C = int(rng.choice([16, 32, 64]))
+        src = W.random_tiny_state(t, sb, rng).tobytes()
+        n = len(m._chunk_map(t, C))
+        fp, fs = m.pack(t, C, src)
+        dp, ds = m.pack_chunks(t, C, src, list(range(n)))
+        if dp != fp or [tuple(x) for x in ds] != [tuple(x) for x in fs]:
+            failed.append("full list is the full pack")
+            break
+    # repair of a replica whose master, its bf16 image and a moment diverged
+    t, nb = W.state_table([("a", 40), ("b", 3), ("c", 17)])
+    donor = W.random_tiny_state(t, nb, np.random.default_rng(23)).tobytes()
+    recv = bytearray(donor)
+    m0, p0, v0 = int(t[1]["src_offset"]), int(t[0]["src_offset"]), int(t[3]["src_offset"])
+    for o, x in ((m0 + 67, 0x40), (p0 + 33, 0x01), (v0 + 5, 0x80), (m0 + 3, 0x02)):
+        recv[o] ^= x
+    for C in (16, 32, 64):
+        r = bytearray(recv)
+        ids = sorted(m.verify(t, C, donor, bytes(r)))
+        pay, sums = m.pack_chunks(t, C, donor, ids)
+        bad = m.unpack_chunks(t, C, pay, sums, ids, r)
+        if bad or bytes(r) != donor:
+            failed.append("repair restores the donor")
+            break
+    return failed
+
+
+def _delta_offsets_with(m, rule):
+    def offsets(table, C, ids):
+        cmap = m._chunk_map(table, C)
+        offs, end, prev = [], 0, None
+        for c in ids:
+            k, j = cmap[c]
+            if int(table[k]["derive_from"]) >= 0:
+                offs.append(None)
+                continue
+            _, ln = m._chunk_bytes(table, C, k, j, None, "src_offset")
+            offs.append(rule(end, prev == (k, j - 1)))
+            end = offs[-1] + ln
+            prev = (k, j)
+        return offs, m._up(end, 16)
+    m._delta_offsets = offsets
+
+
+def _unpack_chunks_with(m, derive_first=False, master_index=2):
+    def unpack_chunks(table, C, payload, sums, ids, dst):
+        cmap = m._chunk_map(table, C)
+        offs, _ = m._delta_offsets(table, C, ids)
+
+        def sent():
+            for c, off in zip(ids, offs):
+                k, j = cmap[c]
+                if off is not None:
+                    o, ln = m._chunk_bytes(table, C, k, j, dst, "dst_offset")
+                    dst[o:o + ln] = payload[off:off + ln]
+
+        def derived():
+            for c in ids:
+                k, j = cmap[c]
+                s = int(table[k]["derive_from"])
+                if s >= 0:
+                    o, ln = m._chunk_bytes(table, C, k, j, dst, "dst_offset")
+                    mo = int(table[s]["dst_offset"]) + master_index * j * C
+                    for q in range(ln // 2):
+                        u = int.from_bytes(dst[mo + 4 * q:mo + 4 * q + 4], "little")
+                        dst[o + 2 * q:o + 2 * q + 2] = m.rne_bf16(u).to_bytes(2, "little")
+        for step in ((derived, sent) if derive_first else (sent, derived)):
+            step()
+        bad = set()
+        for i, c in enumerate(ids):
+            k, j = cmap[c]
+            o, ln = m._chunk_bytes(table, C, k, j, dst, "dst_offset")
+            if m.frsum(bytes(dst[o:o + ln])) != tuple(sums[i]):
+                bad.add(i)
+        return bad
+    m.unpack_chunks = unpack_chunks
+
+
+DELTA_MUTANTS = {
+    "every chunk on a new segment": lambda m: _delta_offsets_with(m, lambda end, cont: m._up(end, m.SEGMENT)),
+    "no segment boundaries": lambda m: _delta_offsets_with(m, lambda end, cont: end),
+    "parameters re-derived before the masters land": lambda m: _unpack_chunks_with(m, derive_first=True),
+    "parameter chunk j read from master chunk j": lambda m: _unpack_chunks_with(m, master_index=1),
+}
+
+
+def test_delta_pins_accept_the_oracle():
+    assert delta_pins(_fresh_mini("delta_clean")) == []
+
+
+@pytest.mark.parametrize("name", sorted(DELTA_MUTANTS))
+def test_delta_mutant_is_caught(name):
+    m = _fresh_mini("delta_" + name.replace(" ", "_"))
+    DELTA_MUTANTS[name](m)
+    assert delta_pins(m), name
