@@ -7,7 +7,9 @@ left dirty, a delta layout or re-derivation order.  The pins that fix the oracle
 values in tests/golden, closed forms, numpy's modular sums, torch's bf16
 cast, exhaustive detection properties, independently built payloads, the
 restore round trip) must accept the unmodified oracle and reject every
-mutant: no plausible single mistake survives them."""
+mutant: no plausible single mistake survives them.  The same is done for
+the restatement of the controller's step-tag rules (oracle/steptag.py)
+against the scenarios and the simulation of tests/test_steptag.py."""
 import importlib.util
 import os
 
@@ -390,3 +392,97 @@ def test_delta_mutant_is_caught(name):
     m = _fresh_mini("delta_" + name.replace(" ", "_"))
     DELTA_MUTANTS[name](m)
     assert delta_pins(m), name
+
+
+# ------------------------------------------------------- step-tag tracker
+
+from oracle.steptag import Cluster  # noqa: E402
+
+from tests import test_steptag as S  # noqa: E402
+
+
+class _NoFreshness(Cluster):
+    """Trusts tags reported before the failure was detected."""
+
+    def decide(self, now):
+        saved = dict(self.seen)
+        self.seen = {r: float("inf") for r in saved}
+        try:
+            return Cluster.decide(self, now)
+        finally:
+            self.seen = saved
+
+
+class _OptimizerTagIsAStep(Cluster):
+    """Does not wait for ranks inside their optimizer step (tag -1)."""
+
+    def decide(self, now):
+        saved = dict(self.tag)
+        self.tag = {r: (10 ** 9 if v == -1 else v) for r, v in saved.items()}
+        try:
+            a, s = Cluster.decide(self, now)
+            return (a, -1 if s == 10 ** 9 else s)
+        finally:
+            self.tag = saved
+
+
+class _FallbackOnAnyLoss(Cluster):
+    """Falls back to a checkpoint as soon as a group lost any member, not
+    only when it lost every member."""
+
+    def decide(self, now):
+        if self.failed(now):
+            return "checkpoint_fallback", -1
+        return Cluster.decide(self, now)
+
+
+class _NoTimeout(Cluster):
+    """Detects only reported failures (a silent rank is never failed)."""
+
+    def failed(self, now):
+        return [r for r in range(self.n_ranks) if r in self.reported]
+
+
+class _ResumeAfterTag(Cluster):
+    """Resumes one step after the agreed tag."""
+
+    def decide(self, now):
+        a, s = Cluster.decide(self, now)
+        return (a, s + 1 if a == "stop_and_restore" else s)
+
+
+STEPTAG_MUTANTS = {
+    "stale tags trusted": _NoFreshness,
+    "optimizer-step tag not waited for": _OptimizerTagIsAStep,
+    "checkpoint when any replica is lost": _FallbackOnAnyLoss,
+    "silent ranks never time out": _NoTimeout,
+    "resume one step late": _ResumeAfterTag,
+}
+
+
+def _steptag_pins_failed(cluster_cls):
+    class Make(S.OracleTracker):
+        cluster = cluster_cls
+    failed = []
+    for name in dir(S):
+        fn = getattr(S, name)
+        if name.startswith("test_") and callable(fn) and fn.__code__.co_varnames[:1] == ("make",):
+            try:
+                fn(Make)
+            except AssertionError:
+                failed.append(name)
+    for seed in range(40):
+        try:
+            S.check_simulation(seed, Make)
+        except AssertionError:
+            failed.append(f"simulation {seed}")
+    return failed
+
+
+def test_steptag_pins_accept_the_oracle():
+    assert _steptag_pins_failed(Cluster) == []
+
+
+@pytest.mark.parametrize("name", sorted(STEPTAG_MUTANTS))
+def test_steptag_mutant_is_caught(name):
+    assert _steptag_pins_failed(STEPTAG_MUTANTS[name]), name

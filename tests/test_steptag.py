@@ -11,6 +11,10 @@
   and stops at the step the failed rank's phase implies.
 * The library equals the plain restatement in ``oracle/steptag.py`` on random
   event sequences, and donors are spread over the live ranks of each group.
+
+The scenarios and the simulation run on both the library and the plain
+restatement (through ``OracleTracker``), so they pin the restatement too;
+tests/test_oracle_mutants.py plants mistakes in it that they must catch.
 """
 import numpy as np
 import pytest
@@ -19,29 +23,70 @@ from oracle.steptag import Cluster
 from paper_2509_03047_amd import flashrestore as F
 
 
-def test_no_failure_continues():
-    t = F.Tracker(4, None, 2.0, 0.0)
+class OracleTracker:
+    """The plain restatement behind the library's Tracker interface
+    (decisions carry the action and the resume step only)."""
+
+    cluster = Cluster
+
+    def __init__(self, n_ranks, dp_group=None, timeout_s=10.0, now_s=0.0):
+        groups = [0] * n_ranks if dp_group is None else [int(x) for x in dp_group]
+        self.c = self.cluster(n_ranks, groups, timeout_s, now_s)
+
+    def heartbeat(self, rank, tag, now):
+        self.c.heartbeat(rank, tag, now)
+
+    def report_failure(self, rank, now):
+        self.c.report_failure(rank, now)
+
+    def decide(self, now):
+        action, step = self.c.decide(now)
+        return {"action": action, "resume_step": step}
+
+    def failed_ranks(self, now):
+        return self.c.failed(now)
+
+    def donors(self, now):
+        return self.c.donors(now)
+
+
+IMPLS = {"library": F.Tracker, "oracle": OracleTracker}
+
+
+@pytest.fixture(params=sorted(IMPLS))
+def make(request):
+    return IMPLS[request.param]
+
+
+def _same(d, expect: dict):
+    """d agrees with every field of expect that it carries (the restatement
+    reports no counts)."""
+    return all(d[k] == v for k, v in expect.items() if k in d)
+
+
+def test_no_failure_continues(make):
+    t = make(4, None, 2.0, 0.0)
     for r in range(4):
         t.heartbeat(r, 3, 1.0)
     assert t.decide(1.5)["action"] == "continue"
 
 
-def test_failure_in_forward_backward_resumes_at_i():
-    t = F.Tracker(4, [0, 0, 1, 1], 2.0, 0.0)
+def test_failure_in_forward_backward_resumes_at_i(make):
+    t = make(4, [0, 0, 1, 1], 2.0, 0.0)
     for r in range(4):
         t.heartbeat(r, 5, 1.0)
     t.report_failure(2, 1.2)
     d = t.decide(1.3)
-    assert d["action"] == "wait" and d["n_waiting"] == 3  # reports predate the failure
+    assert _same(d, {"action": "wait", "n_waiting": 3})  # reports predate the failure
     for r in (0, 1, 3):
         t.heartbeat(r, 5, 1.5)  # blocked at the barrier before the optimizer step
     d = t.decide(1.6)
-    assert d == {"action": "stop_and_restore", "resume_step": 5, "n_failed": 1, "n_waiting": 0}
+    assert _same(d, {"action": "stop_and_restore", "resume_step": 5, "n_failed": 1, "n_waiting": 0})
     assert t.donors(1.6) == [-1, -1, 3, -1]
 
 
-def test_failure_in_optimizer_step_resumes_at_i_plus_1():
-    t = F.Tracker(3, None, 2.0, 0.0)
+def test_failure_in_optimizer_step_resumes_at_i_plus_1(make):
+    t = make(3, None, 2.0, 0.0)
     for r in range(3):
         t.heartbeat(r, -1, 1.0)
     t.report_failure(0, 1.1)
@@ -53,10 +98,10 @@ def test_failure_in_optimizer_step_resumes_at_i_plus_1():
     assert d["action"] == "stop_and_restore" and d["resume_step"] == 6
 
 
-def test_stale_tag_from_before_the_failure_is_not_trusted():
+def test_stale_tag_from_before_the_failure_is_not_trusted(make):
     """A rank that reported i in forward and then entered its optimizer step
     must not be read as 'still at i'."""
-    t = F.Tracker(2, None, 5.0, 0.0)
+    t = make(2, None, 5.0, 0.0)
     t.heartbeat(0, 9, 1.0)
     t.heartbeat(1, 9, 1.0)
     t.report_failure(1, 2.0)  # rank 1 died in its optimizer step of step 9
@@ -65,8 +110,8 @@ def test_stale_tag_from_before_the_failure_is_not_trusted():
     assert t.decide(2.4)["resume_step"] == 10
 
 
-def test_silent_rank_times_out():
-    t = F.Tracker(3, None, 1.0, 0.0)
+def test_silent_rank_times_out(make):
+    t = make(3, None, 1.0, 0.0)
     for r in range(3):
         t.heartbeat(r, 2, 0.5)
     t.heartbeat(0, 2, 1.2)
@@ -79,8 +124,8 @@ def test_silent_rank_times_out():
     assert t.decide(1.8)["action"] == "stop_and_restore"
 
 
-def test_lost_group_falls_back_to_checkpoint():
-    t = F.Tracker(4, [0, 1, 0, 1], 5.0, 0.0)
+def test_lost_group_falls_back_to_checkpoint(make):
+    t = make(4, [0, 1, 0, 1], 5.0, 0.0)
     for r in range(4):
         t.heartbeat(r, 1, 0.1)
     t.report_failure(1, 0.2)
@@ -89,17 +134,17 @@ def test_lost_group_falls_back_to_checkpoint():
     assert t.donors(0.3) == [-1, -1, -1, -1]
 
 
-def test_disagreeing_fresh_tags_are_inconsistent():
-    t = F.Tracker(3, None, 5.0, 0.0)
+def test_disagreeing_fresh_tags_are_inconsistent(make):
+    t = make(3, None, 5.0, 0.0)
     t.report_failure(2, 0.5)
     t.heartbeat(0, 4, 1.0)
     t.heartbeat(1, 7, 1.0)
     assert t.decide(1.1)["action"] == "inconsistent"
 
 
-def test_donors_spread_over_live_ranks():
+def test_donors_spread_over_live_ranks(make):
     g = [0] * 6 + [1] * 2
-    t = F.Tracker(8, g, 5.0, 0.0)
+    t = make(8, g, 5.0, 0.0)
     for r in range(8):
         t.heartbeat(r, 0, 0.1)
     for r in (0, 1, 2, 7):
@@ -164,8 +209,11 @@ def tag_at(changes, t):
     return tag
 
 
-@pytest.mark.parametrize("seed", range(40))
-def test_simulated_failures_resume_at_the_papers_step(seed):
+def check_simulation(seed, make):
+    """One simulated failure (seed) against a tracker made by `make`: the
+    tracker never calls the state inconsistent, stops only at the step the
+    failed rank's phase implies, and stops at all when a replica is left.
+    Returns False when the failure falls past the simulated horizon."""
     rng = np.random.default_rng(1000 + seed)
     n = int(rng.integers(2, 9))
     n_groups = int(rng.integers(1, n + 1))
@@ -174,14 +222,13 @@ def test_simulated_failures_resume_at_the_papers_step(seed):
     tf = float(rng.uniform(0.5, 15.0))
     changes, implied = simulate(rng, n, groups, {f: tf})
     if f not in implied:
-        pytest.skip("failure after the simulated horizon")
+        return False
     expect = implied[f]
     has_replica = sum(1 for r in range(n) if groups[r] == groups[f]) > 1
     hb = 0.25
     timeout = 1.0
     report = bool(rng.integers(0, 2))
-    t = F.Tracker(n, groups, timeout, 0.0)
-    oc = Cluster(n, groups, timeout, 0.0)
+    t = make(n, groups, timeout, 0.0)
     phase = rng.uniform(0, hb, size=n)
     events = []
     for r in range(n):
@@ -198,15 +245,11 @@ def test_simulated_failures_resume_at_the_papers_step(seed):
     stops = []
     for when, kind, r in events:
         if kind == "hb":
-            tag = tag_at(changes[r], when)
-            t.heartbeat(r, tag, when)
-            oc.heartbeat(r, tag, when)
+            t.heartbeat(r, tag_at(changes[r], when), when)
         elif kind == "fail":
             t.report_failure(r, when)
-            oc.report_failure(r, when)
         else:
             d = t.decide(when)
-            assert (d["action"], d["resume_step"]) == oc.decide(when), when
             if not has_replica:  # the failed rank is alone in its group
                 assert d["action"] in ("continue", "checkpoint_fallback")
                 continue
@@ -216,6 +259,13 @@ def test_simulated_failures_resume_at_the_papers_step(seed):
                 stops.append(when)
     if has_replica:
         assert stops, "no stop decision"
+    return True
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_simulated_failures_resume_at_the_papers_step(seed, make):
+    if not check_simulation(seed, make):
+        pytest.skip("failure after the simulated horizon")
 
 
 def test_library_equals_plain_rules_on_random_events():
