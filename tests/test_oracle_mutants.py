@@ -486,3 +486,119 @@ def test_steptag_pins_accept_the_oracle():
 @pytest.mark.parametrize("name", sorted(STEPTAG_MUTANTS))
 def test_steptag_mutant_is_caught(name):
     assert _steptag_pins_failed(STEPTAG_MUTANTS[name]), name
+
+
+# ------------------------------------------------------- restore planner
+
+from oracle import planner as _planner  # noqa: E402
+
+
+def _fresh_planner(tag):
+    spec = importlib.util.spec_from_file_location(f"planner_mutant_{tag}", _planner.__file__)
+    m = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(m)
+    return m
+
+
+PLANNER_LAYOUTS = [(1, 1, 4, 1), (2, 1, 4, 1), (2, 2, 4, 2), (1, 2, 8, 4), (2, 2, 4, 4), (4, 1, 2, 2),
+                   (2, 3, 6, 2)]
+
+
+def planner_pins(P):
+    """Names of the planner pins that module P fails.  Replica classes must
+    partition the ranks into groups of dp / shard ranks holding identical
+    state (equal tensor-parallel index, pipeline stage and shard); a donor
+    must be a live member of the failed rank's class, -1 when none is left,
+    and donors spread evenly over a class's live members."""
+    failed = []
+    rng = np.random.default_rng(5)
+    for tp, pp, dp, shard in PLANNER_LAYOUTS:
+        world = tp * pp * dp
+        state = {r: (lambda c: (c[0], c[1], c[3]))(_planner.coords(tp, pp, dp, shard, r)) for r in range(world)}
+        for r in range(world):
+            reps = P.replicas(tp, pp, dp, shard, r)
+            if (r not in reps or len(set(reps)) != dp // shard
+                    or any(not 0 <= x < world or state[x] != state[r] for x in reps)):
+                failed.append("replica classes")
+                return failed
+        for _ in range(20):
+            dead = set(int(x) for x in rng.choice(world, size=int(rng.integers(0, world + 1)), replace=False))
+            d = P.donors(tp, pp, dp, shard, dead)
+            loads = {}
+            for r in range(world):
+                live = [x for x in range(world) if state[x] == state[r] and x not in dead]
+                if r not in dead or not live:
+                    if d[r] != -1:
+                        failed.append("donor for a live or unservable rank")
+                        return failed
+                    continue
+                if d[r] not in live:
+                    failed.append("donor is a live replica")
+                    return failed
+                loads.setdefault(state[r], []).append(d[r])
+            for cls, used in loads.items():
+                live = [x for x in range(world) if state[x] == cls and x not in dead]
+                counts = [used.count(x) for x in live]
+                if max(counts) - min(counts) > 1:
+                    failed.append("even spread")
+                    return failed
+    return failed
+
+
+def _pl_replicas_no_stage(P):
+    def replicas(tp, pp, dp, shard, rank):
+        t, p, d, s, q = P.coords(tp, pp, dp, shard, rank)
+        return [t + tp * (s + shard * qq) for qq in range(dp // shard)]
+    P.replicas = replicas
+
+
+def _pl_replicas_over_shards(P):
+    def replicas(tp, pp, dp, shard, rank):
+        t, p, d, s, q = P.coords(tp, pp, dp, shard, rank)
+        return [t + tp * (ss + shard * q + dp * p) for ss in range(shard)] if shard > 1 else \
+            [t + tp * (s + shard * qq + dp * p) for qq in range(dp)]
+    P.replicas = replicas
+
+
+def _pl_first_live_donor(P):
+    def donors(tp, pp, dp, shard, failed):
+        out = [-1] * (tp * pp * dp)
+        for r in failed:
+            live = [x for x in sorted(P.replicas(tp, pp, dp, shard, r)) if x not in failed]
+            if live:
+                out[r] = live[0]
+        return out
+    P.donors = donors
+
+
+def _pl_failed_donor(P):
+    def donors(tp, pp, dp, shard, failed):
+        out = [-1] * (tp * pp * dp)
+        served = {}
+        for r in sorted(failed):
+            reps = sorted(P.replicas(tp, pp, dp, shard, r))
+            if any(x not in failed for x in reps):
+                k = served.get(tuple(reps), 0)
+                out[r] = reps[k % len(reps)]
+                served[tuple(reps)] = k + 1
+        return out
+    P.donors = donors
+
+
+PLANNER_MUTANTS = {
+    "replicas ignore the pipeline stage": _pl_replicas_no_stage,
+    "replicas run over the shard index": _pl_replicas_over_shards,
+    "always the first live replica": _pl_first_live_donor,
+    "failed ranks may donate": _pl_failed_donor,
+}
+
+
+def test_planner_pins_accept_the_oracle():
+    assert planner_pins(_fresh_planner("clean")) == []
+
+
+@pytest.mark.parametrize("name", sorted(PLANNER_MUTANTS))
+def test_planner_mutant_is_caught(name):
+    P = _fresh_planner(name.replace(" ", "_"))
+    PLANNER_MUTANTS[name](P)
+    assert planner_pins(P), name
