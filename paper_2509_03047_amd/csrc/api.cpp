@@ -95,13 +95,14 @@ int launch_result(int hip_rc) {
   return device_error(hipError_t(hip_rc));
 }
 
-// The plan's pack / checksum / compare walk at the slice size of `tile`
-// (the plan builds one for each tile it is configured with, so this finds
-// one for the plan's own tiles).
-const SlotTable* src_walk(const fr_plan* plan, int tile) {
+// The plan's pack / checksum / compare walk at the slice size of `tile`,
+// line-aligned or not (the plan builds one for each configuration its
+// operations use, so this finds one for the plan's own).
+const SlotTable* src_walk(const fr_plan* plan, int tile, bool line) {
   const uint32_t sl = slice_bytes(plan->layout.C, tile);
+  const uint32_t shift = line_walk(plan, tile, line) ? 1u : 0u;
   for (const auto& w : plan->src_walks)
-    if (w.sl == sl) return &w.t;
+    if (w.sl == sl && w.t.shift == shift) return &w.t;
   return nullptr;
 }
 
@@ -125,7 +126,7 @@ extern "C" int fr_pack_state(const fr_plan* plan, const void* src_base, void* pa
   const Region outs[] = {{payload, L.payload_bytes}, {sums, L.n_chunks * sizeof(fr_chunk_sum)}};
   const Region ins[] = {{src_base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 2, ins, 1));
-  const SlotTable* walk = src_walk(plan, plan->cfg.tile_pack);
+  const SlotTable* walk = src_walk(plan, plan->cfg.tile_pack, plan->cfg.line_pack);
   if (!walk) return FR_E_INVAL;
   return launch_result(launch_pack(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, src_base,
                                    payload, sums, plan->scratch, plan->cfg, stream));
@@ -183,7 +184,7 @@ extern "C" int fr_verify_replicas(const fr_plan* plan, const void* base_a, const
   const Region outs[] = {{diff_bitmap, words * 4}, {n_diff, 8}, {sums_a, sb}, {sums_b, sb}};
   const Region ins[] = {{base_a, plan->src_arena_bytes}, {base_b, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 4, ins, 2));
-  const SlotTable* walk = src_walk(plan, plan->cfg.tile_verify);
+  const SlotTable* walk = src_walk(plan, plan->cfg.tile_verify, plan->cfg.line_verify);
   if (!walk) return FR_E_INVAL;
   return launch_result(launch_verify(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, base_a,
                                      base_b, diff_bitmap, n_diff, sums_a, sums_b, plan->scratch,
@@ -200,7 +201,7 @@ extern "C" int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk
   const Region outs[] = {{sums, L.n_chunks * sizeof(fr_chunk_sum)}};
   const Region ins[] = {{base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 1, ins, 1));
-  const SlotTable* walk = src_walk(plan, plan->cfg.tile_checksum);
+  const SlotTable* walk = src_walk(plan, plan->cfg.tile_checksum, plan->cfg.line_checksum);
   if (!walk) return FR_E_INVAL;
   return launch_result(launch_checksum(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, base,
                                        sums, plan->scratch, plan->cfg, stream));

@@ -16,6 +16,7 @@ constexpr uint64_t kNoPayload = ~uint64_t(0);
 // up to a fifth faster on tables of many small or oddly placed tensors.
 constexpr uint64_t kSegmentAlign = 4096;
 constexpr uint32_t kNoMaster = 0xFFFFFFFFu;
+constexpr uint32_t kLine = 128;  // L2 cache line (bytes)
 
 // One record per global chunk id (host side; the device tables are built
 // from these).
@@ -40,7 +41,8 @@ struct alignas(16) SrcUnit {
   uint32_t len;      // bytes in this chunk (<= C, even)
   uint32_t c;        // its sums slot: global chunk id, or list position for a delta
   uint32_t gap_v;    // zero vectors pack writes after the chunk's 16-byte-padded end
-  uint32_t pad_;     //   (the gap up to the next segment; < kSegmentAlign / 16)
+                     //   (the gap up to the next segment; < kSegmentAlign / 16)
+  uint32_t lead;     // src_off mod kLine: how far into a cache line the chunk starts
 };
 static_assert(sizeof(SrcUnit) == 32, "SrcUnit is 32 bytes");
 
@@ -90,6 +92,12 @@ struct SlotTable {
   // and slot g is (g >> implicit_shift, g mod 2^implicit_shift); slots past
   // a short unit's end do nothing.
   uint32_t implicit_shift = 0;
+  // Line-aligned walk (SrcUnit walks only): slice j of a chunk covers chunk
+  // bytes [j SL - lead, (j + 1) SL - lead), so every cut between slices falls
+  // on a cache-line boundary of the arena read and no line is fetched by two
+  // workgroups; a chunk has ceil((lead + len) / SL) slices (one more than a
+  // plain walk's when it starts inside a line and ends near a slice end).
+  uint32_t shift = 0;
 };
 
 // Host builder of a slot table (plan.cpp).
@@ -120,6 +128,8 @@ int validate_and_layout(const fr_tensor_desc* table, uint32_t n, uint64_t C, uin
 struct LaunchCfg {
   uint32_t max_grid = 0;  // cap on workgroups per launch (0: hardware limit); grid-stride beyond
   int tile_pack = 0, tile_unpack = 0, tile_verify = 0, tile_checksum = 0;
+  // line-aligned walks (SlotTable::shift) per operation
+  bool line_pack = false, line_verify = false, line_checksum = false;
 };
 
 // Device scratch owned by a plan: per-chunk accumulators (G per chunk, see
@@ -175,6 +185,11 @@ inline uint32_t slice_bytes(uint64_t C, int tile) {
 }
 uint64_t accumulators_per_chunk(uint64_t C, int tile);
 
+// Whether an operation with this tile and line setting walks line-aligned:
+// only when some chunk starts inside a line and a slice spans at least two
+// lines (otherwise the plain walk is the same thing).
+inline bool line_walk(const fr_plan* p, int tile, bool line);
+
 // Kernel launchers (kernels.hip).  They assume validated arguments, enqueue
 // on `stream` and return the hipError_t of the launches as an int.
 // `units` holds n_chunks records whose sums slots c cover [0, n_chunks);
@@ -204,9 +219,10 @@ struct fr_plan {
   // their tiles use) and unpack
   struct Walk {
     uint32_t sl = 0;
-    fr::SlotTable t{};
+    fr::SlotTable t{};  // t.shift: line-aligned
     uint64_t* mem = nullptr;
   };
+  bool any_lead = false;             // some chunk starts inside a cache line
   std::vector<Walk> src_walks;
   Walk unpack_walk;
   fr::DerivedUnit* d_derived = nullptr;  // unpack units: derived groups
@@ -220,3 +236,7 @@ struct fr_plan {
   fr::Scratch scratch{};
   fr::LaunchCfg cfg{};
 };
+
+inline bool fr::line_walk(const fr_plan* p, int tile, bool line) {
+  return line && p->any_lead && slice_bytes(p->layout.C, tile) >= 2 * kLine;
+}

@@ -170,6 +170,7 @@ struct Walk {
   uint32_t sl_vec;    // vectors per slice: SL / 16
   uint32_t spc_shift; // log2(SPC), slices per chunk
   uint32_t g_shift;   // log2(G), accumulators per chunk
+  uint32_t line;      // 1: line-aligned walk (SlotTable::shift)
 };
 
 // Slot of workgroup id g: (unit << 32) | j.
@@ -179,6 +180,13 @@ __device__ __forceinline__ u64 slot_of(const Walk& wk, u64 g) {
 }
 
 constexpr uint32_t kAccSlicesShift = 4;  // 16 slices per accumulator
+
+// Accumulator of slice j of chunk c.  A line-aligned walk can give a chunk
+// one slice more than SPC; that slice shares the chunk's last accumulator.
+__device__ __forceinline__ u64 acc_index(const Walk& wk, uint32_t c, uint32_t j) {
+  const uint32_t a = j >> kAccSlicesShift, last = (1u << wk.g_shift) - 1;
+  return (u64(c) << wk.g_shift) + (a < last ? a : last);
+}
 
 // ------------------------------------------------------------------ pack
 
@@ -197,8 +205,13 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
     const SrcUnit r = units[e >> 32];
     const uint32_t c = r.c, j = uint32_t(e);
     const uint32_t nvec = r.len >> 4, tail = r.len & 15;
-    const uint32_t v0 = j * wk.sl_vec;  // first vector of the slice
-    if (v0 > nvec || (v0 == nvec && tail == 0)) continue;  // guard: no listed slot is empty
+    const uint32_t endv = nvec + (tail ? 1u : 0u);
+    // First vector of the slice; a line-aligned walk starts it lead_v
+    // vectors early (the first slice's leading lanes then come before the
+    // chunk: their unsigned index wraps past nvec and they do nothing).
+    const uint32_t lead_v = wk.line ? r.lead >> 4 : 0u;
+    const uint32_t v0 = j * wk.sl_vec - lead_v;
+    if (j * wk.sl_vec >= endv + lead_v) continue;  // guard: no listed slot is empty
     const u32x4* s = reinterpret_cast<const u32x4*>(src + r.src_off);
     const bool store = kStore && r.pay_off != kNoPayload;
     u32x4* d = reinterpret_cast<u32x4*>(payload + (store ? r.pay_off : 0));
@@ -217,21 +230,19 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
         if (store) st_nt(x[q], d + v);
       }
     }
-    if (tail && nvec >= v0 && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
+    if (tail && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
       const u32x4 t = load_tail(reinterpret_cast<const uint8_t*>(s + nvec), tail);
       acc4(t, 4 * nvec, acc[0], acc[1]);
       if (store) d[nvec] = t;  // the segment's zero padding is written with it
     }
     // The chunk's last slice zero-fills the gap up to the next payload
     // segment (fewer than 256 vectors).
-    const uint32_t endv = nvec + (tail ? 1u : 0u);
-    if (store && r.gap_v && v0 + wk.sl_vec >= endv) {
+    if (store && r.gap_v && (j + 1) * wk.sl_vec >= endv + lead_v) {
       for (uint32_t v = endv + threadIdx.x; v < endv + r.gap_v; v += B)
         st_nt(u32x4{0, 0, 0, 0}, d + v);
     }
     block_sum<B, 2>(acc, lds, parity);
-    if (threadIdx.x == 0)
-      add_sum(acc_out + ((u64(c) << wk.g_shift) + (j >> kAccSlicesShift)), acc[0], acc[1]);
+    if (threadIdx.x == 0) add_sum(acc_out + acc_index(wk, c, j), acc[0], acc[1]);
   }
 }
 
@@ -421,8 +432,9 @@ __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units,
     const SrcUnit r = units[e >> 32];
     const uint32_t c = r.c, j = uint32_t(e);
     const uint32_t nvec = r.len >> 4, tail = r.len & 15;
-    const uint32_t v0 = j * wk.sl_vec;
-    if (v0 > nvec || (v0 == nvec && tail == 0)) continue;
+    const uint32_t lead_v = wk.line ? r.lead >> 4 : 0u;  // as in k_pack
+    const uint32_t v0 = j * wk.sl_vec - lead_v;
+    if (j * wk.sl_vec >= nvec + (tail ? 1u : 0u) + lead_v) continue;
     const u32x4* pa = reinterpret_cast<const u32x4*>(a + r.src_off);
     const u32x4* pb = reinterpret_cast<const u32x4*>(b + r.src_off);
     u64 acc[4] = {0, 0, 0, 0};
@@ -448,7 +460,7 @@ __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units,
         }
       }
     }
-    if (tail && nvec >= v0 && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
+    if (tail && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
       const u32x4 ta = load_tail(reinterpret_cast<const uint8_t*>(pa + nvec), tail);
       const u32x4 tb = load_tail(reinterpret_cast<const uint8_t*>(pb + nvec), tail);
       const u32x4 x = ta ^ tb;
@@ -464,7 +476,7 @@ __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units,
     if (kSums) {
       block_sum<B, 4>(acc, lds, parity);
       if (threadIdx.x == 0) {
-        const u64 i = (u64(c) << wk.g_shift) + (j >> kAccSlicesShift);
+        const u64 i = acc_index(wk, c, j);
         add_sum(acc_a + i, acc[0], acc[1]);
         add_sum(acc_b + i, acc[2], acc[3]);
       }
@@ -613,6 +625,7 @@ inline Walk walk_for(uint64_t C, uint32_t tile_bytes, const SlotTable& t) {
   w.stride = t.stride;
   w.imp_shift = t.implicit_shift;
   w.sl_vec = uint32_t(sl >> 4);
+  w.line = t.shift;
   w.spc_shift = sh;
   w.g_shift = sh > kAccSlicesShift ? sh - kAccSlicesShift : 0;
   return w;

@@ -8,6 +8,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <new>
+#include <utility>
 #include <vector>
 
 #include "fr_internal.h"
@@ -22,6 +23,7 @@ thread_local int g_last_hip_error = 0;
 // 8B and 70B rank shares and the descriptor stress table.
 constexpr uint32_t kDefaultTilePack = 4, kDefaultTileUnpack = 5, kDefaultTileVerify = 5,
                    kDefaultTileChecksum = 3;
+constexpr bool kDefaultLinePack = false, kDefaultLineVerify = true, kDefaultLineChecksum = false;
 
 static uint64_t esize(uint32_t dtype) { return dtype == FR_F32 ? 4 : 2; }
 static uint64_t align16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
@@ -243,6 +245,14 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
     p->cfg.tile_unpack = pick("FLASHRESTORE_TILE_UNPACK", kDefaultTileUnpack);
     p->cfg.tile_verify = pick("FLASHRESTORE_TILE_VERIFY", kDefaultTileVerify);
     p->cfg.tile_checksum = pick("FLASHRESTORE_TILE_CHECKSUM", kDefaultTileChecksum);
+    // line-aligned walks: 1 on, 0 off (FLASHRESTORE_LINE sets all three)
+    const uint32_t lall = env_u32("FLASHRESTORE_LINE", ~0u);
+    auto lpick = [&](const char* name, bool dflt) {
+      return env_u32(name, lall != ~0u ? lall : uint32_t(dflt)) != 0;
+    };
+    p->cfg.line_pack = lpick("FLASHRESTORE_LINE_PACK", kDefaultLinePack);
+    p->cfg.line_verify = lpick("FLASHRESTORE_LINE_VERIFY", kDefaultLineVerify);
+    p->cfg.line_checksum = lpick("FLASHRESTORE_LINE_CHECKSUM", kDefaultLineChecksum);
 
     const Layout& L = p->layout;
     std::vector<ChunkRec> recs(L.n_chunks);
@@ -300,6 +310,8 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
       units[c].pay_off = recs[c].pay_off;
       units[c].len = recs[c].len;
       units[c].c = uint32_t(c);
+      units[c].lead = uint32_t(recs[c].src_off % kLine);
+      p->any_lead = p->any_lead || units[c].lead != 0;
     }
     // The last chunk of each sent entry zero-fills the gap to the next one.
     for (uint32_t k = 0, prev = UINT32_MAX; k < n; k++) {
@@ -312,18 +324,25 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
     }
     int rc2 = upload(units.data(), units.size() * sizeof(SrcUnit), (void**)&p->d_units);
     // Walks of pack / checksum / compare: every chunk in order, one table per
-    // slice size their tiles use.
-    for (int t : {p->cfg.tile_pack, p->cfg.tile_checksum, p->cfg.tile_verify}) {
-      const uint32_t sl = slice_bytes(C, t);
+    // slice size and alignment their configurations use (a line-aligned walk
+    // is the plain one when every chunk starts on a line).
+    const std::pair<int, bool> walks[] = {{p->cfg.tile_pack, p->cfg.line_pack},
+                                          {p->cfg.tile_checksum, p->cfg.line_checksum},
+                                          {p->cfg.tile_verify, p->cfg.line_verify}};
+    for (const auto& tw : walks) {
+      const uint32_t sl = slice_bytes(C, tw.first);
+      const uint32_t shift = line_walk(p, tw.first, tw.second) ? 1u : 0u;
       bool have = false;
-      for (const auto& w : p->src_walks) have = have || w.sl == sl;
+      for (const auto& w : p->src_walks) have = have || (w.sl == sl && w.t.shift == shift);
       if (have || rc2 != FR_OK) continue;
       SlotBuilder b;
       b.sl = sl;
-      b.lin.reserve(L.state_bytes / sl + L.n_chunks);
-      for (uint64_t c = 0; c < recs.size(); c++) b.add(uint32_t(c), recs[c].len, 0);
+      b.lin.reserve(L.state_bytes / sl + 2 * L.n_chunks);
+      for (uint64_t c = 0; c < recs.size(); c++)
+        b.add(uint32_t(c), recs[c].len + (shift ? units[c].lead : 0), 0);
       p->src_walks.emplace_back();
       rc2 = upload_walk(b, p->src_walks.back());
+      p->src_walks.back().t.shift = shift;
     }
     // Walk of unpack, in payload (table) order: a derived entry's groups
     // (their master bytes) where the entry stands, plain chunks where theirs.

@@ -315,6 +315,40 @@ def test_every_slice_count_per_tile(tile):
             os.environ["FLASHRESTORE_TILE"] = old
 
 
+@pytest.mark.parametrize("tile", [0, 3, 4, 5, 7, 10])
+def test_line_aligned_walks_match_oracle(tile):
+    """Line-aligned walks (every slice cut at a 128-byte line of the arena
+    read, one more slice for a chunk that starts inside a line) for pack,
+    compare and checksum give the oracle's bytes: random tables at random
+    16-byte offsets, chunks from 16 B (several chunks per line) to 1 MiB,
+    and short chunks of every slice count."""
+    names = ("FLASHRESTORE_TILE", "FLASHRESTORE_LINE")
+    old = {k: os.environ.get(k) for k in names}
+    os.environ["FLASHRESTORE_TILE"], os.environ["FLASHRESTORE_LINE"] = str(tile), "1"
+    rng = np.random.default_rng(700 + tile)
+    try:
+        for it in range(40):
+            t, sb, db = W.random_tiny_table(rng)
+            C = int(rng.choice([16, 32, 64, 256, 1024]))
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"line tile {tile} table {it} C={C}")
+        for it in range(6):
+            t, sb, db = W.random_tiny_table(rng, max_entries=8, max_numel=200_000)
+            C = int(rng.choice([4096, 16384, 65536, 1 << 20]))
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"line tile {tile} multi {it} C={C}")
+            _delta_against_oracle(t, C, src, sb, db, rng, f"line tile {tile} multi {it}")
+        if tile in SLICE_BYTES:
+            t, src, so, do = _slice_count_table(rng, 1 << 16, SLICE_BYTES[tile])
+            _check_against_oracle(t, 1 << 16, src, so, do, corrupt_rng=rng, tag=f"line tile {tile} slice counts")
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
 def test_mixed_tiles_per_operation():
     """Each operation with its own tile (so one plan holds several walks of
     different slice sizes) still gives the oracle's bytes."""
