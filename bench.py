@@ -37,11 +37,28 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 KERNEL_NAMES = {"pack": "k_pack", "unpack": "k_unpack", "verify": "k_verify", "checksum": "k_pack"}
 
 
-def kernel_source_hash() -> str:
+def _code_only(text: str) -> str:
+    """C++ source without comments and with whitespace collapsed, so that a
+    comment edit does not count as a kernel change (string literals in these
+    sources hold no comment markers)."""
+    import re
+
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
+def kernel_source_hash(read=None) -> str:
+    """Hash of the kernel sources' code (comments excluded); `read(path)`
+    supplies a file's text (default: the working tree)."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        if read is None:
+            with open(os.path.join(ROOT, p), encoding="utf-8") as f:
+                text = f.read()
+        else:
+            text = read(p)
+        h.update(_code_only(text).encode())
     return h.hexdigest()[:16]
 
 

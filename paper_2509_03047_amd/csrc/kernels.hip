@@ -25,7 +25,10 @@
 //     SPC slices owns G = max(1, SPC / 16) accumulators in the plan's
 //     scratch, cleared by a fill kernel launched first;
 //   * replica compare marks a differing chunk with a plain store of 1 to a
-//     per-chunk flag (idempotent, so no atomics on shared bitmap words);
+//     per-chunk flag (idempotent, so no atomics on shared bitmap words), and
+//     by default walks line-aligned: for tensors that start inside a cache
+//     line its cuts fall on lines of the arenas, so no line is fetched
+//     twice (pack and checksum measured slower that way, see SlotTable);
 //   * a finalize kernel, one lane per chunk, folds the G accumulators into
 //     the chunk's sums (pack, checksum, compare) or compares them with the
 //     sums sent (unpack), and writes whole bitmap words from wave ballots.
