@@ -4,7 +4,8 @@ times (default plan, one workgroup per unit).
 * Llama-3-8B TP=8 rank share (14.06 GB state): the whole oracle runs on the
   host; payload, sums, receiver arena and result sets are compared bit for bit.
 * 20,000-entry descriptor stress (7.6 GB): whole oracle, scattered layouts,
-  canaries in every receiver gap.
+  canaries in every receiver gap; its replica compare (line-aligned, since
+  its tensors start inside cache lines) with flips at chunk and line edges.
 * Llama-3-70B TP=8 x PP=4 first-stage share (31.8 GB): the whole oracle on
   the host (payload, sums and receiver arena compared slice by slice), plus
   sampled chunks, a located wire flip and properties that hold at any size
@@ -178,6 +179,55 @@ def test_descriptor_stress_full_parity():
     dst = np.full(w.dst_arena_bytes, 0xA5, np.uint8)
     bm, nbad = cpu.unpack(t, C, pay, sums, dst)
     assert r.bad_set() == set(cpu.bitmap_to_set(bm, nc)) and int(r.n_bad.item()) == nbad
+
+
+@pytest.mark.timeout(900)
+def test_descriptor_stress_replica_compare():
+    """The replica compare on the stress table, whose tensors start inside
+    cache lines (the compare walks line-aligned there): bits flipped at chunk
+    starts and ends, next to line boundaries and at random give the oracle's
+    set and both arenas' sums, and the set is the closed form {chunk of each
+    flipped byte inside a tensor}."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    w = W.make_workload(2)
+    t, C = w.table, w.chunk_bytes
+    src_np = W.fill_state(w)
+    rng = np.random.default_rng(11)
+    nb = t["numel"].astype(np.int64) * np.where(t["dtype"] == W.F32, 4, 2)
+    so = t["src_offset"].astype(np.int64)
+    picks = []
+    for e in rng.choice(len(t), size=200, replace=False):
+        e = int(e)
+        n = int(nb[e])
+        j = int(rng.integers(0, -(-n // C)))
+        lo, hi = j * C, min((j + 1) * C, n)
+        line = (-(int(so[e]) + lo)) % 128  # first line boundary inside the chunk
+        for off in (lo, lo + 1, lo + line, lo + line - 1, hi - 1, int(rng.integers(lo, hi))):
+            if lo <= off < hi:
+                picks.append(int(so[e]) + off)
+    pos = np.unique(np.array(picks, np.int64)) * 8 + rng.integers(0, 8, size=len(set(picks)))
+    b_np = src_np.copy()
+    W.apply_flips(b_np, pos)
+    a, b = _upload(src_np), _upload(b_np)
+    plan = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes).plan
+    diff, nd = plan.empty_bitmap(), plan.empty_counter()
+    sa, sb = plan.empty_sums(), plan.empty_sums()
+    got = plan.verify_replicas(a, b, diff, nd, sa, sb, sync=True)
+    vbm, ond, osa, osb = cpu.verify(t, C, src_np, b_np, with_sums=True)
+    nc = plan.n_chunks
+    assert set(int(x) for x in got) == set(cpu.bitmap_to_set(vbm, nc)) and int(nd.item()) == ond
+    assert np.array_equal(sums_host(sa, nc), osa) and np.array_equal(sums_host(sb, nc), osb)
+    _, base, _, _ = cpu.plan(t, C)
+    order = np.argsort(so, kind="stable")  # the table is shuffled over the arena
+    exp = set()
+    for byte in pos // 8:
+        i = int(np.searchsorted(so[order], byte, side="right") - 1)
+        e = int(order[i]) if i >= 0 else -1
+        if e >= 0 and byte - so[e] < nb[e]:
+            exp.add(int(base[e]) + int(byte - so[e]) // C)
+    assert set(int(x) for x in got) == exp
+    log(f"stress compare: {len(pos)} flips, {len(exp)} chunks flagged")
 
 
 @pytest.fixture(scope="module")
