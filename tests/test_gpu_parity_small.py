@@ -322,23 +322,27 @@ def test_line_aligned_walks_match_oracle(tile):
     compare and checksum give the oracle's bytes: random tables at random
     16-byte offsets, chunks from 16 B (several chunks per line) to 1 MiB,
     and short chunks of every slice count."""
-    names = ("FLASHRESTORE_TILE", "FLASHRESTORE_LINE")
+    names = ("FLASHRESTORE_TILE", "FLASHRESTORE_LINE", "FLASHRESTORE_MAX_GRID")
     old = {k: os.environ.get(k) for k in names}
     os.environ["FLASHRESTORE_TILE"], os.environ["FLASHRESTORE_LINE"] = str(tile), "1"
     rng = np.random.default_rng(700 + tile)
     try:
         for it in range(40):
+            # grid-stride launches too (a capped grid walks several slices per workgroup)
+            os.environ["FLASHRESTORE_MAX_GRID"] = str(int(rng.choice([0, 1, 7, 300])))
             t, sb, db = W.random_tiny_table(rng)
             C = int(rng.choice([16, 32, 64, 256, 1024]))
             src = W.random_tiny_state(t, sb, rng)
             _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"line tile {tile} table {it} C={C}")
         for it in range(6):
+            os.environ["FLASHRESTORE_MAX_GRID"] = str(int(rng.choice([0, 7, 300])))
             t, sb, db = W.random_tiny_table(rng, max_entries=8, max_numel=200_000)
             C = int(rng.choice([4096, 16384, 65536, 1 << 20]))
             src = W.random_tiny_state(t, sb, rng)
             _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"line tile {tile} multi {it} C={C}")
             _delta_against_oracle(t, C, src, sb, db, rng, f"line tile {tile} multi {it}")
         if tile in SLICE_BYTES:
+            os.environ["FLASHRESTORE_MAX_GRID"] = "0"
             t, src, so, do = _slice_count_table(rng, 1 << 16, SLICE_BYTES[tile])
             _check_against_oracle(t, 1 << 16, src, so, do, corrupt_rng=rng, tag=f"line tile {tile} slice counts")
     finally:
