@@ -212,6 +212,181 @@ extern "C" int fr_plan_destroy(fr_plan* p) {
   return FR_OK;
 }
 
+namespace {
+
+// Launch tuning knobs, read from the environment (defaults measured on
+// MI355X): workgroup cap (0 = one workgroup per slice), the tile of each
+// operation and its line-aligned walks.
+LaunchCfg launch_config() {
+  LaunchCfg cfg;
+  cfg.max_grid = env_u32("FLASHRESTORE_MAX_GRID", 0);
+  const uint32_t all = env_u32("FLASHRESTORE_TILE", ~0u);  // one tile for every operation
+  auto pick = [&](const char* name, uint32_t dflt) {
+    return int(env_u32(name, all != ~0u ? all : dflt));
+  };
+  cfg.tile_pack = pick("FLASHRESTORE_TILE_PACK", kDefaultTilePack);
+  cfg.tile_unpack = pick("FLASHRESTORE_TILE_UNPACK", kDefaultTileUnpack);
+  cfg.tile_verify = pick("FLASHRESTORE_TILE_VERIFY", kDefaultTileVerify);
+  cfg.tile_checksum = pick("FLASHRESTORE_TILE_CHECKSUM", kDefaultTileChecksum);
+  // line-aligned walks: 1 on, 0 off (FLASHRESTORE_LINE sets all three)
+  const uint32_t lall = env_u32("FLASHRESTORE_LINE", ~0u);
+  auto lpick = [&](const char* name, bool dflt) {
+    return env_u32(name, lall != ~0u ? lall : uint32_t(dflt)) != 0;
+  };
+  cfg.line_pack = lpick("FLASHRESTORE_LINE_PACK", kDefaultLinePack);
+  cfg.line_verify = lpick("FLASHRESTORE_LINE_VERIFY", kDefaultLineVerify);
+  cfg.line_checksum = lpick("FLASHRESTORE_LINE_CHECKSUM", kDefaultLineChecksum);
+  return cfg;
+}
+
+// One record per global chunk.
+std::vector<ChunkRec> chunk_records(const fr_tensor_desc* table, uint32_t n, const Layout& L) {
+  const uint64_t C = L.C;
+  std::vector<ChunkRec> recs(L.n_chunks);
+  for (uint32_t k = 0; k < n; k++) {
+    const fr_tensor_desc& d = table[k];
+    const uint64_t nb = d.numel * esize(d.dtype);
+    const uint64_t nc = L.chunk_base[k + 1] - L.chunk_base[k];
+    for (uint64_t j = 0; j < nc; j++) {
+      ChunkRec& r = recs[L.chunk_base[k] + j];
+      r.src_off = d.src_offset + j * C;
+      r.dst_off = d.dst_offset + j * C;
+      r.pay_off = L.pay_off[k] == kNoPayload ? kNoPayload : L.pay_off[k] + j * C;
+      r.len = uint32_t(std::min<uint64_t>(C, nb - j * C));
+      // param chunk j covers master chunks 2j and 2j + 1
+      r.master = d.derive_from >= 0 ? uint32_t(L.chunk_base[d.derive_from] + 2 * j) : kNoMaster;
+    }
+  }
+  return recs;
+}
+
+// Pack / checksum / compare units: every chunk, in chunk order.  The last
+// chunk of each sent entry zero-fills the payload gap up to the next one.
+std::vector<SrcUnit> src_units(const std::vector<ChunkRec>& recs, uint32_t n, const Layout& L,
+                               bool* any_lead) {
+  std::vector<SrcUnit> units(recs.size());
+  *any_lead = false;
+  for (uint64_t c = 0; c < recs.size(); c++) {
+    units[c].src_off = recs[c].src_off;
+    units[c].pay_off = recs[c].pay_off;
+    units[c].len = recs[c].len;
+    units[c].c = uint32_t(c);
+    units[c].lead = uint32_t(recs[c].src_off % kLine);
+    *any_lead = *any_lead || units[c].lead != 0;
+  }
+  for (uint32_t k = 0, prev = UINT32_MAX; k < n; k++) {
+    if (L.pay_off[k] == kNoPayload || L.chunk_base[k + 1] == L.chunk_base[k]) continue;
+    if (prev != UINT32_MAX) {
+      SrcUnit& u = units[L.chunk_base[prev + 1] - 1];
+      u.gap_v = uint32_t((L.pay_off[k] - align16(u.pay_off + u.len)) >> 4);
+    }
+    prev = k;
+  }
+  return units;
+}
+
+// Unpack units: a derived group per parameter chunk of a derived entry (its
+// master chunks travel in it), a plain unit per chunk of every other entry
+// that is not such a master.  is_master[k]: entry k feeds a derived entry.
+void unpack_units(const fr_tensor_desc* table, uint32_t n, const Layout& L,
+                  const std::vector<ChunkRec>& recs, const std::vector<uint8_t>& is_master,
+                  std::vector<DerivedUnit>* derived, std::vector<PlainUnit>* plain) {
+  for (uint32_t k = 0; k < n; k++) {
+    const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];
+    if (table[k].derive_from >= 0) {
+      for (uint64_t c = c0; c < c1; c++) {
+        const ChunkRec& r = recs[c];
+        const ChunkRec& m = recs[r.master];
+        DerivedUnit u{};
+        u.m_pay_off = m.pay_off;
+        u.m_dst_off = m.dst_off;
+        u.p_dst_off = r.dst_off;
+        u.len = r.len;
+        u.m0 = r.master;
+        u.c = uint32_t(c);
+        derived->push_back(u);
+      }
+    } else if (!is_master[k]) {
+      for (uint64_t c = c0; c < c1; c++) {
+        PlainUnit u{};
+        u.pay_off = recs[c].pay_off;
+        u.dst_off = recs[c].dst_off;
+        u.len = recs[c].len;
+        u.c = uint32_t(c);
+        plain->push_back(u);
+      }
+    }
+  }
+}
+
+// Walks of pack / checksum / compare: every chunk in order, one table per
+// slice size and alignment their configurations use (a line-aligned walk is
+// the plain one when every chunk starts on a line).
+int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units) {
+  const Layout& L = p->layout;
+  const std::pair<int, bool> walks[] = {{p->cfg.tile_pack, p->cfg.line_pack},
+                                        {p->cfg.tile_checksum, p->cfg.line_checksum},
+                                        {p->cfg.tile_verify, p->cfg.line_verify}};
+  for (const auto& tw : walks) {
+    const uint32_t sl = slice_bytes(L.C, tw.first);
+    const uint32_t shift = line_walk(p, tw.first, tw.second) ? 1u : 0u;
+    bool have = false;
+    for (const auto& w : p->src_walks) have = have || (w.sl == sl && w.t.shift == shift);
+    if (have) continue;
+    SlotBuilder b;
+    b.sl = sl;
+    b.lin.reserve(L.state_bytes / sl + 2 * L.n_chunks);
+    for (uint64_t c = 0; c < units.size(); c++)
+      b.add(uint32_t(c), units[c].len + (shift ? units[c].lead : 0), 0);
+    p->src_walks.emplace_back();
+    const int rc = upload_walk(b, p->src_walks.back());
+    p->src_walks.back().t.shift = shift;
+    if (rc != FR_OK) return rc;
+  }
+  return FR_OK;
+}
+
+// Walk of unpack, in payload (table) order: a derived entry's groups (their
+// master bytes) where the entry stands, plain chunks where theirs.
+int build_unpack_walk(fr_plan* p, const std::vector<ChunkRec>& recs,
+                      const std::vector<uint8_t>& is_master) {
+  const Layout& L = p->layout;
+  SlotBuilder b;
+  b.sl = slice_bytes(L.C, p->cfg.tile_unpack);
+  b.lin.reserve(L.payload_bytes / b.sl + L.n_chunks);
+  uint32_t id = 0, ip = 0;
+  for (uint32_t k = 0; k < p->table.size(); k++) {
+    const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];
+    if (p->table[k].derive_from >= 0) {
+      for (uint64_t c = c0; c < c1; c++) b.add(id++, 2 * uint64_t(recs[c].len), kSlotDerived);
+    } else if (!is_master[k]) {
+      for (uint64_t c = c0; c < c1; c++) b.add(ip++, recs[c].len, 0);
+    }
+  }
+  return upload_walk(b, p->unpack_walk);
+}
+
+// Scratch: accumulators for the largest G any configured tile needs, for two
+// arenas, and one flag per chunk.
+int build_scratch(fr_plan* p) {
+  const Layout& L = p->layout;
+  uint64_t g = 1;
+  for (int t : {p->cfg.tile_pack, p->cfg.tile_unpack, p->cfg.tile_verify, p->cfg.tile_checksum})
+    g = std::max<uint64_t>(g, accumulators_per_chunk(L.C, t));
+  const uint64_t acc_bytes = L.n_chunks * g * sizeof(fr_chunk_sum);
+  const uint64_t flag_bytes = (L.n_chunks * 4 + 255) & ~uint64_t(255);
+  const int rc = upload(nullptr, 2 * acc_bytes + flag_bytes, &p->d_scratch);
+  if (rc == FR_OK && p->d_scratch) {
+    uint8_t* base = static_cast<uint8_t*>(p->d_scratch);
+    p->scratch.acc = reinterpret_cast<fr_chunk_sum*>(base);
+    p->scratch.acc_b = reinterpret_cast<fr_chunk_sum*>(base + acc_bytes);
+    p->scratch.flags = reinterpret_cast<uint32_t*>(base + 2 * acc_bytes);
+  }
+  return rc;
+}
+
+}  // namespace
+
 extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t C,
                               uint64_t src_bytes, uint64_t dst_bytes, fr_plan** out) {
   if (!out) return FR_E_INVAL;
@@ -226,162 +401,38 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
     p->table.assign(table, table + n);
     p->src_arena_bytes = src_bytes;
     p->dst_arena_bytes = dst_bytes;
-
     int dev = -1;
-    hipError_t e = hipGetDevice(&dev);
+    const hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) {
       delete p;
       return hip_fail(e);
     }
     p->device = dev;
-    // Launch tuning knobs (defaults measured on MI355X): workgroup cap
-    // (0 = one workgroup per slice) and the tile of each operation.
-    p->cfg.max_grid = env_u32("FLASHRESTORE_MAX_GRID", 0);
-    const uint32_t all = env_u32("FLASHRESTORE_TILE", ~0u);  // one tile for every operation
-    auto pick = [&](const char* name, uint32_t dflt) {
-      return int(env_u32(name, all != ~0u ? all : dflt));
-    };
-    p->cfg.tile_pack = pick("FLASHRESTORE_TILE_PACK", kDefaultTilePack);
-    p->cfg.tile_unpack = pick("FLASHRESTORE_TILE_UNPACK", kDefaultTileUnpack);
-    p->cfg.tile_verify = pick("FLASHRESTORE_TILE_VERIFY", kDefaultTileVerify);
-    p->cfg.tile_checksum = pick("FLASHRESTORE_TILE_CHECKSUM", kDefaultTileChecksum);
-    // line-aligned walks: 1 on, 0 off (FLASHRESTORE_LINE sets all three)
-    const uint32_t lall = env_u32("FLASHRESTORE_LINE", ~0u);
-    auto lpick = [&](const char* name, bool dflt) {
-      return env_u32(name, lall != ~0u ? lall : uint32_t(dflt)) != 0;
-    };
-    p->cfg.line_pack = lpick("FLASHRESTORE_LINE_PACK", kDefaultLinePack);
-    p->cfg.line_verify = lpick("FLASHRESTORE_LINE_VERIFY", kDefaultLineVerify);
-    p->cfg.line_checksum = lpick("FLASHRESTORE_LINE_CHECKSUM", kDefaultLineChecksum);
+    p->cfg = launch_config();
 
     const Layout& L = p->layout;
-    std::vector<ChunkRec> recs(L.n_chunks);
+    const std::vector<ChunkRec> recs = chunk_records(table, n, L);
     std::vector<uint8_t> is_master(n, 0);
     for (uint32_t k = 0; k < n; k++)
       if (table[k].derive_from >= 0) is_master[table[k].derive_from] = 1;
-    for (uint32_t k = 0; k < n; k++) {
-      const fr_tensor_desc& d = table[k];
-      uint64_t nb = d.numel * (d.dtype == FR_F32 ? 4 : 2);
-      uint64_t nc = L.chunk_base[k + 1] - L.chunk_base[k];
-      for (uint64_t j = 0; j < nc; j++) {
-        ChunkRec& r = recs[L.chunk_base[k] + j];
-        r.src_off = d.src_offset + j * C;
-        r.dst_off = d.dst_offset + j * C;
-        r.pay_off = L.pay_off[k] == kNoPayload ? kNoPayload : L.pay_off[k] + j * C;
-        r.len = uint32_t(std::min<uint64_t>(C, nb - j * C));
-        // param chunk j covers master chunks 2j and 2j + 1
-        r.master = d.derive_from >= 0 ? uint32_t(L.chunk_base[d.derive_from] + 2 * j) : kNoMaster;
-      }
-    }
-    // Unpack walks the derived groups first, then the plain chunks.
     std::vector<DerivedUnit> derived;
     std::vector<PlainUnit> plain;
-    for (uint32_t k = 0; k < n; k++) {
-      const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];
-      if (table[k].derive_from >= 0) {
-        for (uint64_t c = c0; c < c1; c++) {
-          const ChunkRec& r = recs[c];
-          const ChunkRec& m = recs[r.master];
-          DerivedUnit u{};
-          u.m_pay_off = m.pay_off;
-          u.m_dst_off = m.dst_off;
-          u.p_dst_off = r.dst_off;
-          u.len = r.len;
-          u.m0 = r.master;
-          u.c = uint32_t(c);
-          derived.push_back(u);
-        }
-      } else if (!is_master[k]) {
-        for (uint64_t c = c0; c < c1; c++) {
-          PlainUnit u{};
-          u.pay_off = recs[c].pay_off;
-          u.dst_off = recs[c].dst_off;
-          u.len = recs[c].len;
-          u.c = uint32_t(c);
-          plain.push_back(u);
-        }
-      }
-    }
+    unpack_units(table, n, L, recs, is_master, &derived, &plain);
     p->n_derived = uint32_t(derived.size());
     p->n_plain = uint32_t(plain.size());
-    std::vector<SrcUnit> units(recs.size());
-    for (uint64_t c = 0; c < recs.size(); c++) {
-      units[c].src_off = recs[c].src_off;
-      units[c].pay_off = recs[c].pay_off;
-      units[c].len = recs[c].len;
-      units[c].c = uint32_t(c);
-      units[c].lead = uint32_t(recs[c].src_off % kLine);
-      p->any_lead = p->any_lead || units[c].lead != 0;
-    }
-    // The last chunk of each sent entry zero-fills the gap to the next one.
-    for (uint32_t k = 0, prev = UINT32_MAX; k < n; k++) {
-      if (L.pay_off[k] == kNoPayload || L.chunk_base[k + 1] == L.chunk_base[k]) continue;
-      if (prev != UINT32_MAX) {
-        SrcUnit& u = units[L.chunk_base[prev + 1] - 1];
-        u.gap_v = uint32_t((L.pay_off[k] - align16(u.pay_off + u.len)) >> 4);
-      }
-      prev = k;
-    }
-    int rc2 = upload(units.data(), units.size() * sizeof(SrcUnit), (void**)&p->d_units);
-    // Walks of pack / checksum / compare: every chunk in order, one table per
-    // slice size and alignment their configurations use (a line-aligned walk
-    // is the plain one when every chunk starts on a line).
-    const std::pair<int, bool> walks[] = {{p->cfg.tile_pack, p->cfg.line_pack},
-                                          {p->cfg.tile_checksum, p->cfg.line_checksum},
-                                          {p->cfg.tile_verify, p->cfg.line_verify}};
-    for (const auto& tw : walks) {
-      const uint32_t sl = slice_bytes(C, tw.first);
-      const uint32_t shift = line_walk(p, tw.first, tw.second) ? 1u : 0u;
-      bool have = false;
-      for (const auto& w : p->src_walks) have = have || (w.sl == sl && w.t.shift == shift);
-      if (have || rc2 != FR_OK) continue;
-      SlotBuilder b;
-      b.sl = sl;
-      b.lin.reserve(L.state_bytes / sl + 2 * L.n_chunks);
-      for (uint64_t c = 0; c < recs.size(); c++)
-        b.add(uint32_t(c), recs[c].len + (shift ? units[c].lead : 0), 0);
-      p->src_walks.emplace_back();
-      rc2 = upload_walk(b, p->src_walks.back());
-      p->src_walks.back().t.shift = shift;
-    }
-    // Walk of unpack, in payload (table) order: a derived entry's groups
-    // (their master bytes) where the entry stands, plain chunks where theirs.
-    if (rc2 == FR_OK) {
-      SlotBuilder b;
-      b.sl = slice_bytes(C, p->cfg.tile_unpack);
-      b.lin.reserve(L.payload_bytes / b.sl + L.n_chunks);
-      uint32_t id = 0, ip = 0;
-      for (uint32_t k = 0; k < n; k++) {
-        const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];
-        if (table[k].derive_from >= 0) {
-          for (uint64_t c = c0; c < c1; c++) b.add(id++, 2 * uint64_t(recs[c].len), kSlotDerived);
-        } else if (!is_master[k]) {
-          for (uint64_t c = c0; c < c1; c++) b.add(ip++, recs[c].len, 0);
-        }
-      }
-      rc2 = upload_walk(b, p->unpack_walk);
-    }
-    if (rc2 == FR_OK)
-      rc2 = upload(derived.data(), derived.size() * sizeof(DerivedUnit), (void**)&p->d_derived);
-    if (rc2 == FR_OK)
-      rc2 = upload(plain.data(), plain.size() * sizeof(PlainUnit), (void**)&p->d_plain);
-    rc = rc2;
-    // Scratch: accumulators for the largest G any configured tile needs.
-    uint64_t g = 1;
-    for (int t : {p->cfg.tile_pack, p->cfg.tile_unpack, p->cfg.tile_verify, p->cfg.tile_checksum})
-      g = std::max<uint64_t>(g, accumulators_per_chunk(C, t));
-    const uint64_t acc_bytes = L.n_chunks * g * sizeof(fr_chunk_sum);
-    const uint64_t flag_bytes = (L.n_chunks * 4 + 255) & ~uint64_t(255);
-    if (rc == FR_OK) rc = upload(nullptr, 2 * acc_bytes + flag_bytes, &p->d_scratch);
+    const std::vector<SrcUnit> units = src_units(recs, n, L, &p->any_lead);
+
+    rc = upload(units.data(), units.size() * sizeof(SrcUnit), (void**)&p->d_units);
+    if (rc == FR_OK) rc = build_src_walks(p, units);
+    if (rc == FR_OK) rc = build_unpack_walk(p, recs, is_master);
+    if (rc == FR_OK)
+      rc = upload(derived.data(), derived.size() * sizeof(DerivedUnit), (void**)&p->d_derived);
+    if (rc == FR_OK)
+      rc = upload(plain.data(), plain.size() * sizeof(PlainUnit), (void**)&p->d_plain);
+    if (rc == FR_OK) rc = build_scratch(p);
     if (rc != FR_OK) {
       fr_plan_destroy(p);
       return rc;
-    }
-    if (p->d_scratch) {
-      uint8_t* base = static_cast<uint8_t*>(p->d_scratch);
-      p->scratch.acc = reinterpret_cast<fr_chunk_sum*>(base);
-      p->scratch.acc_b = reinterpret_cast<fr_chunk_sum*>(base + acc_bytes);
-      p->scratch.flags = reinterpret_cast<uint32_t*>(base + 2 * acc_bytes);
     }
   } catch (const std::bad_alloc&) {
     if (p) fr_plan_destroy(p);
