@@ -13,7 +13,8 @@ times (default plan, one workgroup per unit).
   empty).
 * Replica compare on two copies of the 8B share with k in {0, 1, 64, 4096}
   distinct random bit flips: the flagged set equals the closed form
-  {chunk of each flipped byte} and the oracle's set.
+  {chunk of each flipped byte} and the oracle's set; the 4,096-flip replica
+  repaired by a delta (payload and sums against the oracle).
 """
 import numpy as np
 import pytest
@@ -357,3 +358,35 @@ def test_llama8b_striped_transfer_properties(llama8b):
     r.unpack(payload=recv, sums=sums)
     torch.cuda.synchronize()
     assert int(r.n_bad.item()) == 0 and torch.equal(r.dst, src)
+
+
+@pytest.mark.timeout(900)
+def test_llama8b_delta_repair(llama8b):
+    """A replica of the 8B share with 4,096 random bit flips is repaired by
+    re-sending only the chunks the compare flags: the delta payload and sums
+    equal the oracle's for that list, nothing is flagged on arrival, and the
+    replica equals the donor byte for byte."""
+    import paper_2509_03047_amd.flashrestore as F
+
+    w, src_np = llama8b
+    t, C = w.table, w.chunk_bytes
+    plan = F.Plan(t, C, w.src_arena_bytes, w.dst_arena_bytes)
+    donor = _upload(src_np)
+    replica = donor.clone()
+    pos = W.flip_positions(src_np.size * 8, 4096, 4000 + 4096)
+    _flip_on_device(replica, pos)
+    diff, nd = plan.empty_bitmap(), plan.empty_counter()
+    ids = plan.verify_replicas(donor, replica, diff, nd, sync=True).astype(np.uint32)
+    _, base, _, _ = cpu.plan(t, C)
+    assert set(int(x) for x in ids) == _expected_chunks(w, base, pos)
+    pb = plan.delta_layout(ids)
+    payload = torch.full((pb,), 0xEE, dtype=torch.uint8, device="cuda")
+    sums = torch.empty(ids.size, 2, dtype=torch.int64, device="cuda")
+    plan.pack_chunks(donor, ids, payload, sums)
+    bad, nbad = torch.empty((ids.size + 31) // 32, dtype=torch.int32, device="cuda"), plan.empty_counter()
+    flagged = plan.unpack_chunks(payload, sums, ids, replica, bad, nbad, sync=True)
+    opay, osums = cpu.pack_chunks(t, C, src_np, ids)
+    assert np.array_equal(to_host(payload), opay) and np.array_equal(sums_host(sums, ids.size), osums)
+    assert len(flagged) == 0 and int(nbad.item()) == 0
+    assert torch.equal(replica, donor)
+    log(f"delta repair: {ids.size} chunks, {pb} payload bytes")
