@@ -441,7 +441,9 @@ class Tracker:
     def __init__(self, n_ranks: int, dp_group=None, timeout_s: float = 10.0, now_s: float = 0.0):
         self._h = None
         self.n_ranks = n_ranks
-        g = None if dp_group is None else np.ascontiguousarray(dp_group, dtype=np.uint32)
+        g = None if dp_group is None else np.ascontiguousarray(dp_group, dtype=np.uint32).reshape(-1)
+        if g is not None and g.size != n_ranks:
+            raise ValueError(f"dp_group has {g.size} entries for {n_ranks} ranks")
         h = C.c_void_p()
         _check(_lib.fr_tracker_create(n_ranks, None if g is None else g.ctypes.data, timeout_s, now_s,
                                       C.byref(h)), "fr_tracker_create")
@@ -478,7 +480,9 @@ class Tracker:
 
     def donors_into(self, now_s: float, out: np.ndarray) -> np.ndarray:
         """donors() into a caller-owned contiguous int32 array of n_ranks."""
-        assert out.dtype == np.int32 and out.size == self.n_ranks and out.flags.c_contiguous
+        if not (isinstance(out, np.ndarray) and out.dtype == np.int32 and out.size == self.n_ranks
+                and out.flags.c_contiguous):
+            raise ValueError("out must be a contiguous int32 array with one element per rank")
         _check(_lib.fr_tracker_donors(self._h, now_s, out.ctypes.data), "fr_tracker_donors")
         return out
 
@@ -505,9 +509,9 @@ class Layout3D:
     def donors_into(self, failed_mask: np.ndarray, out: np.ndarray) -> np.ndarray:
         """donors() from a uint8 mask of failed ranks into a caller-owned
         int32 array (both contiguous, one element per rank)."""
-        assert failed_mask.dtype == np.uint8 and failed_mask.size == self.world
-        assert out.dtype == np.int32 and out.size == self.world
-        assert failed_mask.flags.c_contiguous and out.flags.c_contiguous
+        for a, dt, name in ((failed_mask, np.uint8, "failed_mask"), (out, np.int32, "out")):
+            if not (isinstance(a, np.ndarray) and a.dtype == dt and a.size == self.world and a.flags.c_contiguous):
+                raise ValueError(f"{name} must be a contiguous {np.dtype(dt).name} array with one element per rank")
         _check(_lib.fr_layout_donors(C.byref(self.s), failed_mask.ctypes.data, out.ctypes.data),
                "fr_layout_donors")
         return out

@@ -302,3 +302,20 @@ def test_donors_into_equals_donors():
     t.report_failure(4, 0.2)
     out = np.full(6, 99, np.int32)
     assert t.donors_into(0.3, out).tolist() == t.donors(0.3)
+
+
+def test_binding_checks_host_arrays():
+    """The binding refuses host arrays of the wrong length or type before
+    the library reads them."""
+    with pytest.raises(ValueError):
+        F.Tracker(4, [0, 1], 1.0, 0.0)  # group array shorter than the ranks
+    t = F.Tracker(3, None, 1.0, 0.0)
+    with pytest.raises(ValueError):
+        t.donors_into(0.0, np.zeros(2, np.int32))
+    with pytest.raises(ValueError):
+        t.donors_into(0.0, np.zeros(3, np.int64))
+    L = F.Layout3D(2, 1, 2, 1, 0)
+    with pytest.raises(ValueError):
+        L.donors_into(np.zeros(4, np.uint8), np.zeros(3, np.int32))
+    with pytest.raises(ValueError):
+        L.donors_into(np.zeros(4, np.int32), np.zeros(4, np.int32))
