@@ -162,7 +162,8 @@ def cpu_baseline(w, src_np, seconds: float):
         el = time.perf_counter() - t0
         if el >= seconds or reps >= 100:
             break
-    assert nbad == 0 and nd == 0 and np.array_equal(cs, sums)
+    if not (nbad == 0 and nd == 0 and np.array_equal(cs, sums)):
+        raise RuntimeError("the oracle's own restore of the sample is not exact")
     what = f"{n_ent // 4} logical tensors" if step == 4 else "entries in table order"
     return {
         "value": round(state * reps / el / 1e9, 4),

@@ -251,7 +251,8 @@ def fill_state(w: Workload, arena: np.ndarray | None = None, threads: int | None
     """
     if arena is None:
         arena = np.zeros(w.src_arena_bytes, dtype=np.uint8)
-    assert arena.dtype == np.uint8 and arena.size >= w.src_arena_bytes
+    if arena.dtype != np.uint8 or arena.size < w.src_arena_bytes:
+        raise ValueError("arena must be a uint8 array of at least src_arena_bytes")
     t = w.table
     jobs = []
     if w.tensors is not None:
