@@ -276,8 +276,8 @@ int fr_unpack_chunks(const fr_plan* plan, const void* payload, uint64_t payload_
 /* ------------------------------------------------- step tags and donors */
 
 /* Host-only controller logic that decides *which* state a restore copies and
- * *when* the normal ranks may be stopped (Section III-E, "Step i or step i+1
- * to resume?" and "The moment to stop, clean and reset").  Every rank tags
+ * *when* the normal ranks may be stopped (Section III-E: its parts on the
+ * step to resume from and on when to stop the normal processes).  Every rank tags
  * itself i when forward of step i starts, -1 when its optimizer step starts
  * and i+1 when that ends, and reports the tag with its heartbeat
  * (Section III-C).  A barrier merged into the gradient all-reduce keeps the

@@ -1,6 +1,6 @@
 // Step-tag tracker: when may the controller stop the normal ranks, and from
-// which step's state does recovery resume (Section III-E, "Step i or step
-// i+1 to resume?" and "The moment to stop, clean and reset").
+// which step's state does recovery resume (Section III-E: its parts on the
+// step to resume from and on when to stop the normal processes).
 //
 // Every training process sets its tag to i when forward of step i starts,
 // to -1 when its optimizer step starts, and to i+1 when the optimizer step
