@@ -212,3 +212,17 @@ def _entry_byte(w, arena_byte):
     starts = w.table["src_offset"].astype(np.int64)
     e = int(np.searchsorted(starts, arena_byte, side="right") - 1)
     return e, arena_byte - int(starts[e])
+
+
+def test_compare_of_an_arena_with_itself_is_empty(setup):
+    """base_a == base_b is legal: nothing differs and both sums equal the
+    pack sums."""
+    w, plan, src = setup
+    payload, sums = plan.empty_payload(), plan.empty_sums()
+    plan.pack(src, payload, sums)
+    diff, nd = plan.empty_bitmap(), plan.empty_counter()
+    sa, sb = plan.empty_sums(), plan.empty_sums()
+    assert list(plan.verify_replicas(src, src, diff, nd, sa, sb, sync=True)) == []
+    assert int(nd.item()) == 0
+    n = plan.n_chunks
+    assert torch.equal(sa[:n], sums[:n]) and torch.equal(sb[:n], sums[:n])
