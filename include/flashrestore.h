@@ -5,7 +5,7 @@
  * recreated process's model state -- parameters, optimizer state and other
  * training state -- from a healthy replica in its data-parallel group rather
  * than from a checkpoint, by collective communication (Section III-B item 3;
- * Section III-E, "Model states Restoration").  Data parallelism is what makes
+ * Section III-E, its part on restoring the model states).  Data parallelism is what makes
  * the replicas exist and keeps them identical (Section III-A).  This library
  * is the per-GPU data path of that restore:
  *

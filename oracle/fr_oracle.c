@@ -8,8 +8,8 @@
  *
  * What is computed.  The paper restores the model state of a recreated
  * process from a healthy data-parallel replica by collective communication
- * instead of from a checkpoint (Section III-B item 3; Section III-E,
- * "Model states Restoration"), and the restored replica must be consistent
+ * instead of from a checkpoint (Section III-B item 3; Section III-E, its
+ * part on restoring the model states), and the restored replica must be consistent
  * with the others again (Section III-A: data parallelism keeps model copies
  * consistent).  The paper fixes nothing below the level of copying the
  * replica's state; every format detail here is a reading, listed in the
