@@ -186,3 +186,45 @@ def test_rne_mini_agrees_on_random_patterns():
     got = cpu.rne_bf16_array(u)
     for x, g in zip(u, got):
         assert mini.rne_bf16(int(x)) == int(g)
+
+
+def test_pack_worked_example(golden_dir):
+    """A three-entry pack worked by hand (tests/golden/pack_worked.txt):
+    payload bytes, segment placement, zero gaps and every chunk's sums, for
+    both oracles; the restore of it reproduces the arena."""
+    from paper_2509_03047_amd import workloads as W
+
+    rows, src, segs, sums, C, ab, pb = [], {}, {}, [], 0, 0, 0
+    with open(os.path.join(golden_dir, "pack_worked.txt")) as f:
+        for line in f:
+            p = line.split()
+            if not p or p[0].startswith("#"):
+                continue
+            if p[0] == "entry":
+                rows.append(tuple(int(x) for x in p[1:]))
+            elif p[0] == "chunk_bytes":
+                C = int(p[1])
+            elif p[0] == "arena_bytes":
+                ab = int(p[1])
+            elif p[0] == "src":
+                src[int(p[1])] = bytes.fromhex(p[2])
+            elif p[0] == "payload_bytes":
+                pb = int(p[1])
+            elif p[0] == "segment":
+                segs[int(p[1])] = bytes.fromhex(p[2])
+            elif p[0] == "sums":
+                sums += [int(p[1]), int(p[2])]
+    t = np.array(rows, dtype=W.TABLE_DTYPE)
+    arena = np.zeros(ab, np.uint8)
+    for o, b in src.items():
+        arena[o:o + len(b)] = np.frombuffer(b, np.uint8)
+    expect = np.zeros(pb, np.uint8)
+    for o, b in segs.items():
+        expect[o:o + len(b)] = np.frombuffer(b, np.uint8)
+    pay, s = cpu.pack(t, C, arena)
+    assert np.array_equal(pay, expect) and [int(x) for x in s] == sums
+    mp, ms = mini.pack(t, C, arena.tobytes())
+    assert mp == expect.tobytes() and [x for pair in ms for x in pair] == sums
+    dst = np.zeros(ab, np.uint8)
+    bm, nbad = cpu.unpack(t, C, pay, s, dst)
+    assert nbad == 0 and np.array_equal(dst, arena)
