@@ -194,7 +194,7 @@ def test_pack_worked_example(golden_dir):
     both oracles; the restore of it reproduces the arena."""
     from paper_2509_03047_amd import workloads as W
 
-    rows, src, segs, sums, C, ab, pb = [], {}, {}, [], 0, 0, 0
+    rows, src, segs, sums, C, ab, pb, deltas = [], {}, {}, [], 0, 0, 0, []
     with open(os.path.join(golden_dir, "pack_worked.txt")) as f:
         for line in f:
             p = line.split()
@@ -214,6 +214,9 @@ def test_pack_worked_example(golden_dir):
                 segs[int(p[1])] = bytes.fromhex(p[2])
             elif p[0] == "sums":
                 sums += [int(p[1]), int(p[2])]
+            elif p[0] == "delta":
+                deltas.append(([int(x) for x in p[1].split(",")],
+                               [None if x == "-" else int(x) for x in p[2].split(",")], int(p[3])))
     t = np.array(rows, dtype=W.TABLE_DTYPE)
     arena = np.zeros(ab, np.uint8)
     for o, b in src.items():
@@ -228,3 +231,19 @@ def test_pack_worked_example(golden_dir):
     dst = np.zeros(ab, np.uint8)
     bm, nbad = cpu.unpack(t, C, pay, s, dst)
     assert nbad == 0 and np.array_equal(dst, arena)
+    # delta lists: offsets, sizes, and the bytes at those offsets
+    assert len(deltas) == 4
+    for ids, offs, size in deltas:
+        ia = np.array(ids, np.uint32)
+        off, got_size = cpu.delta_layout(t, C, ia)
+        assert got_size == size and [None if o == cpu.NO_PAYLOAD else int(o) for o in off] == offs
+        dp, ds = cpu.pack_chunks(t, C, arena, ia)
+        assert dp.size == size and [int(x) for x in ds] == [v for c in ids for v in sums[2 * c:2 * c + 2]]
+        _, base, _, _ = cpu.plan(t, C)
+        for c, o in zip(ids, offs):
+            if o is None:
+                continue
+            k = int(np.searchsorted(base, c, side="right") - 1)
+            so = int(t[k]["src_offset"]) + (c - int(base[k])) * C
+            ln = min(C, int(t[k]["numel"]) * (4 if int(t[k]["dtype"]) == 1 else 2) - (c - int(base[k])) * C)
+            assert np.array_equal(dp[o:o + ln], arena[so:so + ln])
