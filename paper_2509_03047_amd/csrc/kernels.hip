@@ -28,7 +28,8 @@
 //     per-chunk flag (idempotent, so no atomics on shared bitmap words), and
 //     by default walks line-aligned: for tensors that start inside a cache
 //     line its cuts fall on lines of the arenas, so no line is fetched
-//     twice (pack and checksum measured slower that way, see SlotTable);
+//     twice (pack and checksum measured slower that way; the plan's
+//     launch configuration sets it per operation, see LaunchCfg);
 //   * a finalize kernel, one lane per chunk, folds the G accumulators into
 //     the chunk's sums (pack, checksum, compare) or compares them with the
 //     sums sent (unpack), and writes whole bitmap words from wave ballots.
