@@ -235,7 +235,10 @@ int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums,
  * entry starts where that one ends, any other at the first multiple of 4096
  * at or after it; the payload ends at the last chunk's end rounded up to 16;
  * every gap byte 0.  Listed chunks of derived (bf16) entries send nothing.
- * With every chunk listed the delta payload and sums equal fr_pack_state's.
+ * With every chunk listed the delta payload and sums equal fr_pack_state's;
+ * with C >= 4096 the delta payload of a contiguous range of chunk ids (a
+ * stripe) is fr_pack_state's payload from the range's first sent chunk on,
+ * so stripes packed by several donors assemble into one payload.
  * All three take the list on the host.  Pack and unpack copy the list's unit
  * records (32 or 48 bytes per chunk) to a device buffer the plan keeps, on
  * `stream`, before their kernels; a list that needs more room than the
