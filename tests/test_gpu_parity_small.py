@@ -433,3 +433,34 @@ def _delta_against_oracle(t, C, src, sb, db, rng, tag):
     obm, onbad = cpu.unpack_chunks(t, C, dpay, dsums, ids, orecv)
     assert np.array_equal(to_host(g_recv), orecv) and int(nbad.item()) == onbad == 0, f"delta {tag}"
     assert np.array_equal(orecv, expect), f"delta repair {tag}"
+
+
+def test_payload_gaps_and_padding_are_never_read():
+    """Unpack reads only the entries' bytes of the payload: with every gap
+    byte between segments and every padding byte after a segment's last
+    value overwritten, nothing is flagged and the receiver arena is the same
+    as from the clean payload (the oracle reads only those bytes too)."""
+    from paper_2509_03047_amd import flashrestore as F
+
+    rng = np.random.default_rng(31)
+    for it in range(20):
+        t, sb, db = W.random_tiny_table(rng, max_entries=10, max_numel=3000)
+        C = int(rng.choice([16, 64, 256, 4096]))
+        src = W.random_tiny_state(t, sb, rng)
+        r = Restore(t, C, sb, db)
+        r.pack(to_dev(src) if src.size else torch.empty(16, dtype=torch.uint8, device="cuda"))
+        r.unpack()
+        torch.cuda.synchronize()
+        clean = r.dst.clone()
+        used = np.zeros(r.plan.payload_bytes, bool)
+        for k in range(len(t)):
+            off, _, _ = r.plan.entry_layout(k)
+            nb = int(t[k]["numel"]) * (4 if int(t[k]["dtype"]) == F.FR_F32 else 2)
+            if off != F.NO_PAYLOAD and nb:
+                used[off:off + nb] = True
+        junk = torch.from_numpy(np.where(used, 0, rng.integers(1, 256, used.size)).astype(np.uint8)).to("cuda")
+        r.payload[: used.size] ^= junk  # only bytes outside the entries change
+        r.dst.fill_(0xA5)
+        r.unpack()
+        torch.cuda.synchronize()
+        assert r.bad_set() == set() and torch.equal(r.dst, clean), f"table {it} C={C}"
