@@ -233,6 +233,62 @@ def control_plane(reps=21):
     }
 
 
+def flips(table, C, k):
+    """k distinct random bit flips over the table-order concatenation of the
+    tensors' bytes (seed 4000 + k), mapped to arena offsets: (byte indices,
+    XOR masks) as device tensors, and the set of chunks they fall in."""
+    import numpy as np
+    import torch
+
+    from paper_2509_03047_amd import workloads as W
+
+    nb = table["numel"].astype(np.int64) * np.where(table["dtype"] == W.F32, 4, 2)
+    starts = np.concatenate([[0], np.cumsum(nb)])
+    nch = -(-nb // C)
+    base = np.concatenate([[0], np.cumsum(nch)])
+    pos = W.flip_positions(int(starts[-1]) * 8, k, 4000 + k).astype(np.int64)
+    cat = pos // 8
+    e = np.searchsorted(starts, cat, side="right") - 1
+    chunks = set(int(x) for x in base[e] + (cat - starts[e]) // C)
+    by = table["src_offset"].astype(np.int64)[e] + (cat - starts[e])
+    order = np.argsort(by, kind="stable")
+    by, pos = by[order], pos[order]
+    masks = (np.uint8(1) << (pos % 8).astype(np.uint8)).astype(np.uint8)
+    uniq, start = np.unique(by, return_index=True)
+    idx = torch.from_numpy(uniq).to("cuda")
+    xor = torch.from_numpy(np.bitwise_or.reduceat(masks, start)).to("cuda")
+    return idx, xor, chunks
+
+
+def replica_compare(plan, table, donor, replica, stream, ks=(0, 1, 64, 4096), reps=5):
+    """The replica compare on two copies of the state with k distinct random
+    bit flips in the second: median time (HIP events) and whether the flagged
+    set is exactly {chunk of each flipped byte}.  The copy is restored after
+    each k by flipping the same bits back."""
+    import numpy as np
+    import torch
+
+    diff, ndiff = plan.empty_bitmap(), plan.empty_counter()
+    out = {}
+    for k in ks:
+        idx, xor, expect = flips(table, plan.info["chunk_bytes"], k)
+        replica[idx] ^= xor
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            plan.verify_replicas(donor, replica, diff, ndiff, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        got = plan.verify_replicas(donor, replica, diff, ndiff, stream=stream, sync=True)
+        replica[idx] ^= xor
+        out[str(k)] = {"ms": round(float(np.median(ts)), 4), "n_diff": int(ndiff.item()),
+                       "exact": set(int(x) for x in got) == expect}
+    torch.cuda.synchronize()
+    return out
+
+
 def delta_repair(plan, table, donor, replica, info, k, stream, reps=5):
     """Repair of a replica that diverged in k random bits of its tensors:
     compare, read the flagged set back, re-send only those chunks.  `plan`
@@ -243,22 +299,8 @@ def delta_repair(plan, table, donor, replica, info, k, stream, reps=5):
     import torch
 
     from paper_2509_03047_amd import flashrestore as F
-    from paper_2509_03047_amd import workloads as W
 
-    # bit positions over the table-order concatenation of the tensors' bytes,
-    # mapped to arena offsets (gaps between tensors belong to no chunk)
-    nb = table["numel"].astype(np.int64) * np.where(table["dtype"] == W.F32, 4, 2)
-    starts = np.concatenate([[0], np.cumsum(nb)])
-    pos = W.flip_positions(int(starts[-1]) * 8, k, 4000 + k).astype(np.int64)
-    cat = pos // 8
-    e = np.searchsorted(starts, cat, side="right") - 1
-    by = table["src_offset"].astype(np.int64)[e] + (cat - starts[e])
-    order = np.argsort(by, kind="stable")
-    by, pos = by[order], pos[order]
-    masks = (np.uint8(1) << (pos % 8).astype(np.uint8)).astype(np.uint8)
-    uniq, start = np.unique(by, return_index=True)
-    idx = torch.from_numpy(uniq).to("cuda")
-    xor = torch.from_numpy(np.bitwise_or.reduceat(masks, start)).to("cuda")
+    idx, xor, _ = flips(table, plan.info["chunk_bytes"], k)
     diff, ndiff = plan.empty_bitmap(), plan.empty_counter()
     bad, nbad = plan.empty_bitmap(), plan.empty_counter()
     payload = plan.empty_payload()
@@ -467,6 +509,7 @@ def main():
             rtable = w.table.copy()
             rtable["dst_offset"] = rtable["src_offset"]
             rplan = F.Plan(rtable, w.chunk_bytes, w.src_arena_bytes, w.src_arena_bytes)
+        out["replica_compare"] = replica_compare(rplan, rtable, src, replica, stream)
         out["delta_repair"] = delta_repair(rplan, rtable, src, replica, rplan.info, args.delta_flips, stream)
         out["delta_repair"]["full_restore_ms"] = round(restore_ms, 4)
     out["control_plane"] = control_plane()
