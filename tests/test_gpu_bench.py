@@ -38,6 +38,9 @@ def test_bench_json_line(config, extra):
     assert abs(r["frac"] - r["achieved"] / r["peak"]) < 1e-3
     assert d["parity_ok"] is True
     assert d["delta_repair"]["ok"] is True and d["control_plane"]["ok"] is True
+    rc = d["replica_compare"]
+    assert set(rc) == {"0", "1", "64", "4096"} and all(v["exact"] for v in rc.values())
+    assert rc["0"]["n_diff"] == 0 and rc["1"]["n_diff"] == 1
     if "--no-cpu-baseline" not in extra:
         cb = d["cpu_baseline"]
         assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1 and cb["sample"]
