@@ -124,23 +124,31 @@ def copy_calibration():
     return {"bytes_per_copy": 2 * n, "ms": ms, "gbs": 2 * n / ms / 1e6}
 
 
-def cpu_baseline(w, src_np, seconds: float):
-    """The oracle, as it stands, on a prefix of the same workload: the first
-    entries of the table (whole logical tensors for the model-shaped ones, the
-    embedding and the first layers) up to about 2 GB of state."""
-    import numpy as np
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
-    from oracle import cpu
+
+def _oracle_sample(w, src_np, max_bytes: int):
+    """The first entries of the table (whole logical tensors for the
+    model-shaped ones) up to about max_bytes of state, with the arenas the
+    oracle reads and writes for them."""
+    import numpy as np
 
     t = w.table
     es = np.where(t["dtype"] == 1, 4, 2).astype(np.int64) * t["numel"].astype(np.int64)
     cum = np.cumsum(es)
     step = 4 if w.tensors is not None else 1  # 4 entries per logical tensor
     n_ent = step
-    while n_ent + step <= len(t) and cum[n_ent + step - 1] <= 2_100_000_000:
+    while n_ent + step <= len(t) and cum[n_ent + step - 1] <= max_bytes:
         n_ent += step
     sub = t[:n_ent].copy()
-    state = int(cum[n_ent - 1])
     same_layout = (w.src_arena_bytes == w.dst_arena_bytes
                    and np.array_equal(t["src_offset"], t["dst_offset"]))
     if same_layout and w.tensors is not None:
@@ -151,28 +159,69 @@ def cpu_baseline(w, src_np, seconds: float):
         src, dst = src_np, np.empty(w.dst_arena_bytes, np.uint8)
     # the compare and the checksum take an arena in the donor's layout
     replica = dst if same_layout else src
-    C = w.chunk_bytes
+    what = f"{n_ent // 4} logical tensors" if step == 4 else "entries in table order"
+    return sub, int(cum[n_ent - 1]), src, dst, replica, f"first {n_ent} of {len(t)} entries ({what}"
+
+
+def _oracle_steps(sub, C, src, dst, replica, seconds: float, max_reps: int):
+    """Full oracle steps until `seconds` pass: (steps, elapsed, seconds per op)."""
+    import numpy as np
+
+    from oracle import cpu
+
+    ops = {"pack": 0.0, "unpack": 0.0, "verify": 0.0, "checksum": 0.0}
     reps, t0 = 0, time.perf_counter()
     while True:
+        a = time.perf_counter()
         pay, sums = cpu.pack(sub, C, src)
+        b = time.perf_counter()
         bm, nbad = cpu.unpack(sub, C, pay, sums, dst)
+        c = time.perf_counter()
         vb, nd = cpu.verify(sub, C, src, replica)
+        d = time.perf_counter()
         cs = cpu.checksum(sub, C, replica)
+        e = time.perf_counter()
+        for k, dt in zip(ops, (b - a, c - b, d - c, e - d)):
+            ops[k] += dt
         reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds or reps >= 100:
+        if e - t0 >= seconds or reps >= max_reps:
             break
     if not (nbad == 0 and nd == 0 and np.array_equal(cs, sums)):
         raise RuntimeError("the oracle's own restore of the sample is not exact")
-    what = f"{n_ent // 4} logical tensors" if step == 4 else "entries in table order"
-    return {
+    return reps, time.perf_counter() - t0, ops
+
+
+def cpu_baseline(w, src_np, seconds: float):
+    """The oracle, as it stands, on a prefix of the same workload: the first
+    entries of the table (the embedding and the first layers for the
+    model-shaped ones) up to about 2 GB of state, on every host thread; and a
+    smaller prefix (about 256 MB) on one thread.  Rates are state bytes per
+    second: the whole step, and each operation alone."""
+    from oracle import cpu
+
+    C = w.chunk_bytes
+    cores = cpu.threads()
+    sub, state, src, dst, replica, what = _oracle_sample(w, src_np, 2_100_000_000)
+    reps, el, ops = _oracle_steps(sub, C, src, dst, replica, seconds, 100)
+    out = {
         "value": round(state * reps / el / 1e9, 4),
         "unit": "GB/s",
-        "cores": cpu.threads(),
+        "cores": cores,
         "kind": "oracle",
-        "sample": f"first {n_ent} of {len(t)} entries ({what}, {state} state bytes), "
-                  f"{reps} full steps (pack+unpack+verify+checksum) in {el:.1f} s",
+        "sample": f"{what}, {state} state bytes), {reps} full steps (pack+unpack+verify+checksum) "
+                  f"in {el:.1f} s",
+        "ops_gbs": {k: round(state * reps / v / 1e9, 4) for k, v in ops.items()},
+        "cpu_model": _cpu_model(),
     }
+    sub1, state1, src1, dst1, rep1, what1 = _oracle_sample(w, src_np, 270_000_000)
+    cpu.set_threads(1)
+    try:
+        r1, el1, _ = _oracle_steps(sub1, C, src1, dst1, rep1, max(1.0, seconds / 4), 20)
+    finally:
+        cpu.set_threads(cores)
+    out["one_thread"] = {"value": round(state1 * r1 / el1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+                         "sample": f"{what1}, {state1} state bytes), {r1} full steps in {el1:.1f} s"}
+    return out
 
 
 def control_plane(reps=21):

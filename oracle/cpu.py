@@ -48,6 +48,8 @@ def lib():
                   "oro_checksum_chunks", "oro_selfcheck", "oro_threads", "oro_delta_layout",
                   "oro_pack_chunks", "oro_unpack_chunks"):
             getattr(l, f).restype = C.c_int
+        l.oro_set_threads.argtypes = [C.c_int]
+        l.oro_set_threads.restype = None
         if l.oro_selfcheck() != 0:
             raise RuntimeError("oracle needs a little-endian host")
         _lib = l
@@ -69,6 +71,11 @@ def _p(a) -> int:
 
 def threads() -> int:
     return lib().oro_threads()
+
+
+def set_threads(n: int) -> None:
+    """OpenMP threads of the following oracle calls (timing only)."""
+    lib().oro_set_threads(int(n))
 
 
 def plan(t: np.ndarray, C_: int):

@@ -449,3 +449,12 @@ int oro_threads(void) {
   return 1;
 #endif
 }
+
+/* Threads for the following calls (timing only; results never depend on it). */
+void oro_set_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}

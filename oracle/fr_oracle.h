@@ -65,6 +65,7 @@ int oro_unpack_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t*
 
 int oro_selfcheck(void);
 int oro_threads(void);
+void oro_set_threads(int n);
 
 #ifdef __cplusplus
 }
