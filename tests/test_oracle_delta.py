@@ -223,3 +223,35 @@ def test_stripes_below_4k_chunks_are_not_slices():
     dp, _ = cpu.pack_chunks(t, C, src, ids)
     off = _chunk_payload_offset(t, C, 1)
     assert off == 1024 and not np.array_equal(dp, fp[off:off + dp.size])
+
+
+def _subset_table():
+    """Ten chunks of 64 bytes: a bf16 parameter (2 chunks) derived from its
+    master (4 chunks), a plain fp32 entry of 2 chunks and 1 ragged one, an
+    empty entry, and a bf16 entry of one short chunk."""
+    t = np.array([(0, 0, 60, W.BF16, 1), (128, 128, 60, W.F32, -1), (384, 400, 40, W.F32, -1),
+                  (544, 560, 0, W.F32, -1), (544, 576, 5, W.BF16, -1)], dtype=W.TABLE_DTYPE)
+    return t, 64, 560, 608
+
+
+def test_every_delta_subset_of_a_small_table():
+    """All 1,024 lists of the ten chunks: the C oracle's delta layout,
+    payload, sums and repair equal the pure-Python oracle's."""
+    t, C, sb, db = _subset_table()
+    n = cpu.n_chunks(t, C)
+    assert n == 10
+    rng = np.random.default_rng(65)
+    src = W.random_tiny_state(t, sb, rng)
+    recv0 = rng.integers(0, 256, size=db, dtype=np.uint8)
+    for mask in range(1 << n):
+        ids = np.array([c for c in range(n) if mask >> c & 1], dtype=np.uint32)
+        off, pb = cpu.delta_layout(t, C, ids)
+        moff, mpb = mini._delta_offsets(t, C, [int(i) for i in ids])
+        assert pb == mpb and [None if o == cpu.NO_PAYLOAD else int(o) for o in off] == moff, mask
+        pay, sums = cpu.pack_chunks(t, C, src, ids)
+        mp, ms = mini.pack_chunks(t, C, src.tobytes(), [int(i) for i in ids])
+        assert pay.tobytes() == mp and [tuple(int(x) for x in sums[2 * i:2 * i + 2]) for i in range(ids.size)] == ms
+        recv, mrecv = recv0.copy(), bytearray(recv0.tobytes())
+        bm, nbad = cpu.unpack_chunks(t, C, pay, sums, ids, recv)
+        mbad = mini.unpack_chunks(t, C, pay.tobytes(), ms, [int(i) for i in ids], mrecv)
+        assert recv.tobytes() == bytes(mrecv) and set(cpu.bitmap_to_set(bm, ids.size)) == mbad, mask
