@@ -181,3 +181,42 @@ def test_striped_transfer_restores_like_one_payload(k):
         cpu.unpack(t, C, opay, osums, odst)
         torch.cuda.synchronize()
         assert int(nbad.item()) == 0 and np.array_equal(to_host(dst), odst)
+
+
+def test_delta_every_subset_of_a_small_table():
+    """All 1,024 lists of a ten-chunk table with a derived parameter, a
+    ragged entry, an empty entry and a short bf16 entry, through one plan:
+    payload, sums, receiver arena and result set equal the oracle's."""
+    from tests.test_oracle_delta import _subset_table
+
+    t, C, sb, db = _subset_table()
+    n = cpu.n_chunks(t, C)
+    rng = np.random.default_rng(66)
+    src_np = W.random_tiny_state(t, sb, rng)
+    recv0 = rng.integers(0, 256, size=db, dtype=np.uint8)
+    plan = F.Plan(t, C, sb, db)
+    src = to_dev(src_np)
+    lists = [np.array([c for c in range(n) if mask >> c & 1], dtype=np.uint32) for mask in range(1 << n)]
+    # a list with gaps starts a 4 KiB segment per run of chunks, so it can
+    # need more room than the full payload
+    payload = torch.empty(max(plan.delta_layout(ids) for ids in lists), dtype=torch.uint8, device="cuda")
+    sums = torch.empty(n, 2, dtype=torch.int64, device="cuda")
+    bad = torch.empty(1, dtype=torch.int32, device="cuda")
+    nbad = torch.empty(1, dtype=torch.int64, device="cuda")
+    for mask, ids in enumerate(lists):
+        pb = plan.delta_layout(ids)
+        payload.fill_(0xEE)
+        plan.pack_chunks(src, ids, payload, sums)
+        opay, osums = cpu.pack_chunks(t, C, src_np, ids)
+        assert pb == opay.size
+        assert np.array_equal(to_host(payload)[:pb], opay), mask
+        assert np.array_equal(sums_host(sums, ids.size), osums), mask
+        dst = to_dev(recv0)
+        plan.unpack_chunks(payload, sums, ids, dst, bad, nbad)
+        orecv = recv0.copy()
+        obm, onbad = cpu.unpack_chunks(t, C, opay, osums, ids, orecv)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host(dst), orecv), mask
+        assert set(F.bitmap_indices(bad, ids.size).tolist()) == set(cpu.bitmap_to_set(obm, ids.size)), mask
+        assert int(nbad.item()) == onbad, mask
+    log(f"delta subsets {1 << n}")
