@@ -300,6 +300,9 @@ SlotTable implicit_walk(uint64_t units, uint64_t C, int tile, bool derived) {
   return t;
 }
 
+// The staging vector is pageable memory, and HIP performs an async copy from
+// pageable memory synchronously: the records have left the vector when this
+// returns, so the next delta call may refill or reallocate it at once.
 int upload_records(fr_plan* plan, size_t bytes, void* stream) {
   if (bytes == 0) return FR_OK;
   hipError_t e = hipMemcpyAsync(plan->d_delta, plan->delta_host.data(), bytes,
