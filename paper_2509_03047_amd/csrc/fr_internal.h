@@ -100,13 +100,17 @@ struct SlotTable {
   uint32_t shift = 0;
 };
 
-// Host builder of a slot table (plan.cpp).
-struct SlotBuilder {
-  std::vector<uint64_t> lin;  // slots in walk order
-  uint32_t sl = 0;            // slice bytes
-  void add(uint32_t unit, uint64_t bytes, uint32_t flag);
-  uint64_t stride() const { return (lin.size() + 7) / 8; }
-  void xcd_major(uint64_t* out) const;  // writes 8 * stride() entries
+// A slot table as runs, built on the host (plan.cpp) and expanded on the
+// device (launch_expand_slots): run r holds the slots base[r] | 0,
+// base[r] | 1, ..., base[r] | (first[r + 1] - first[r] - 1), runs in walk
+// order, none empty.
+struct SlotRuns {
+  std::vector<uint64_t> first{0};  // n_runs + 1 entries: prefix of slot counts
+  std::vector<uint64_t> base;      // n_runs entries: (unit << 32) | flag
+  uint32_t sl = 0;                 // slice bytes
+  void add(uint32_t unit, uint64_t bytes, uint32_t flag);  // ceil(bytes / sl) slots
+  uint64_t n() const { return first.back(); }
+  uint64_t stride() const { return (n() + 7) / 8; }
 };
 
 // Host-side layout of a validated table.
@@ -206,6 +210,11 @@ int launch_verify(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunk
                   const void* a, const void* b, uint32_t* bitmap, uint64_t* n_diff,
                   fr_chunk_sum* sums_a, fr_chunk_sum* sums_b, const Scratch& scr,
                   const LaunchCfg& cfg, void* stream);
+// Writes the XCD-major image (8 * stride entries, zero past slot n - 1) of
+// the slot table whose runs are first[0 .. n_runs] and base[0 .. n_runs - 1]
+// (device arrays; first[0] = 0, first[n_runs] = n, no empty run).
+int launch_expand_slots(const uint64_t* first, const uint64_t* base, uint64_t n_runs, uint64_t n,
+                        uint64_t stride, uint64_t* out, void* stream);
 
 }  // namespace fr
 

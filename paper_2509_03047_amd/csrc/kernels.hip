@@ -572,6 +572,31 @@ __global__ __launch_bounds__(kFinalThreads) void k_finalize(FinalArgs f) {
 
 // ------------------------------------------------------------- utilities
 
+// Expands a slot table from runs (plan creation).  Thread o writes entry o
+// of the XCD-major image, which holds slot g = (o mod stride) * 8 +
+// o / stride, so consecutive threads store consecutive words; slot g belongs
+// to the last run whose first slot is <= g (binary search: first[0] = 0 <=
+// g < n = first[n_runs], and no run is empty).
+__global__ __launch_bounds__(256) void k_expand_slots(const u64* __restrict__ first,
+                                                      const u64* __restrict__ base, u64 n_runs,
+                                                      u64 n, u64 stride, u64* __restrict__ out) {
+  const u64 total = 8 * stride, step = u64(gridDim.x) * blockDim.x;
+  for (u64 o = u64(blockIdx.x) * blockDim.x + threadIdx.x; o < total; o += step) {
+    const u64 g = (o % stride) * 8 + o / stride;
+    u64 v = 0;
+    if (g < n) {
+      u64 lo = 0, hi = n_runs;  // first[lo] <= g < first[hi]
+      while (hi - lo > 1) {
+        const u64 mid = lo + (hi - lo) / 2;
+        if (first[mid] <= g) lo = mid;
+        else hi = mid;
+      }
+      v = base[lo] | (g - first[lo]);
+    }
+    out[o] = v;
+  }
+}
+
 // Clears up to four regions of 32-bit words (a kernel rather than a memset
 // so that an operation is made of kernel launches only).
 struct ZeroList {
@@ -799,6 +824,18 @@ int verify_impl(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks,
   }
 
 }  // namespace
+
+int launch_expand_slots(const uint64_t* first, const uint64_t* base, uint64_t n_runs, uint64_t n,
+                        uint64_t stride, uint64_t* out, void* stream) {
+  const u64 total = 8 * stride;
+  if (total == 0) return 0;
+  const u64 want = (total + 255) / 256;
+  const uint32_t blocks = uint32_t(want < 65536 ? want : 65536);
+  hipLaunchKernelGGL(k_expand_slots, dim3(blocks), dim3(256), 0, hipStream_t(stream),
+                     reinterpret_cast<const u64*>(first), reinterpret_cast<const u64*>(base),
+                     u64(n_runs), u64(n), u64(stride), reinterpret_cast<u64*>(out));
+  return int(hipGetLastError());
+}
 
 uint32_t tile_bytes(int tile) {
   switch (tile) {

@@ -163,31 +163,41 @@ static int upload(const void* src, size_t bytes, void** out) {
 
 namespace fr {
 
-void SlotBuilder::add(uint32_t unit, uint64_t bytes, uint32_t flag) {
+void SlotRuns::add(uint32_t unit, uint64_t bytes, uint32_t flag) {
   const uint64_t ns = (bytes + sl - 1) / sl;
-  for (uint64_t j = 0; j < ns; j++) lin.push_back((uint64_t(unit) << 32) | flag | j);
-}
-
-void SlotBuilder::xcd_major(uint64_t* out) const {
-  const uint64_t st = stride();
-  std::fill(out, out + 8 * st, uint64_t(0));
-  for (uint64_t g = 0; g < lin.size(); g++) out[(g & 7) * st + (g >> 3)] = lin[g];
+  if (ns == 0) return;
+  base.push_back((uint64_t(unit) << 32) | flag);
+  first.push_back(first.back() + ns);
 }
 
 }  // namespace fr
 
 namespace {
 
-// Uploads a slot table built by `b` into `w`.
-int upload_walk(const SlotBuilder& b, fr_plan::Walk& w) {
-  std::vector<uint64_t> img(8 * b.stride());
-  b.xcd_major(img.data());
-  w.sl = b.sl;
-  w.t.n = b.lin.size();
-  w.t.stride = b.stride();
-  const int rc = upload(img.data(), img.size() * sizeof(uint64_t), (void**)&w.mem);
+// Allocates the slot table of `r` on the device and expands it there: the
+// host uploads one (first slot, base) pair per run instead of every slot.
+int upload_walk(const SlotRuns& r, fr_plan::Walk& w) {
+  w.sl = r.sl;
+  w.t.n = r.n();
+  w.t.stride = r.stride();
+  int rc = upload(nullptr, 8 * r.stride() * sizeof(uint64_t), (void**)&w.mem);
   w.t.d = w.mem;
-  return rc;
+  if (rc != FR_OK || !w.mem) return rc;
+  const uint64_t n_runs = r.base.size();
+  void* runs = nullptr;
+  rc = upload(nullptr, (2 * n_runs + 1) * sizeof(uint64_t), &runs);
+  if (rc != FR_OK) return rc;
+  uint64_t* d_first = static_cast<uint64_t*>(runs);
+  uint64_t* d_base = d_first + n_runs + 1;
+  hipError_t e = hipMemcpy(d_first, r.first.data(), (n_runs + 1) * sizeof(uint64_t),
+                           hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy(d_base, r.base.data(), n_runs * sizeof(uint64_t), hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipError_t(launch_expand_slots(d_first, d_base, n_runs, r.n(), r.stride(), w.mem, nullptr));
+  if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+  (void)hipFree(runs);
+  return e == hipSuccess ? FR_OK : hip_fail(e);
 }
 
 }  // namespace
@@ -333,9 +343,10 @@ int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units) {
     bool have = false;
     for (const auto& w : p->src_walks) have = have || (w.sl == sl && w.t.shift == shift);
     if (have) continue;
-    SlotBuilder b;
+    SlotRuns b;
     b.sl = sl;
-    b.lin.reserve(L.state_bytes / sl + 2 * L.n_chunks);
+    b.first.reserve(units.size() + 1);
+    b.base.reserve(units.size());
     for (uint64_t c = 0; c < units.size(); c++)
       b.add(uint32_t(c), units[c].len + (shift ? units[c].lead : 0), 0);
     p->src_walks.emplace_back();
@@ -351,9 +362,10 @@ int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units) {
 int build_unpack_walk(fr_plan* p, const std::vector<ChunkRec>& recs,
                       const std::vector<uint8_t>& is_master) {
   const Layout& L = p->layout;
-  SlotBuilder b;
+  SlotRuns b;
   b.sl = slice_bytes(L.C, p->cfg.tile_unpack);
-  b.lin.reserve(L.payload_bytes / b.sl + L.n_chunks);
+  b.first.reserve(L.n_chunks + 1);
+  b.base.reserve(L.n_chunks);
   uint32_t id = 0, ip = 0;
   for (uint32_t k = 0; k < p->table.size(); k++) {
     const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];

@@ -32,6 +32,8 @@ int launch_unpack_delta(const UnpackDeltaArgs&, const LaunchCfg&, void*) { retur
 int launch_verify(const SrcUnit*, const SlotTable&, uint32_t, uint64_t, const void*, const void*,
                   uint32_t*, uint64_t*, fr_chunk_sum*, fr_chunk_sum*, const Scratch&,
                   const LaunchCfg&, void*) { return 1; }
+int launch_expand_slots(const uint64_t*, const uint64_t*, uint64_t, uint64_t, uint64_t, uint64_t*,
+                        void*) { return 1; }
 }  // namespace fr
 
 namespace {
