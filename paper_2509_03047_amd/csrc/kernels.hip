@@ -33,6 +33,8 @@
 //   * a finalize kernel, one lane per chunk, folds the G accumulators into
 //     the chunk's sums (pack, checksum, compare) or compares them with the
 //     sums sent (unpack), and writes whole bitmap words from wave ballots.
+// Plan creation uses one more kernel: the host describes each slot table as
+// one run of slots per unit and k_expand_slots writes the table itself.
 #include <hip/hip_runtime.h>
 
 #include "fr_internal.h"
