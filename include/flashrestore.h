@@ -139,8 +139,10 @@ typedef struct fr_plan_info {
  * Entries must lie inside their arenas (FR_E_RANGE), offsets must be
  * multiples of 16 (FR_E_ALIGN), receiver ranges must not overlap
  * (FR_E_OVERLAP; sender ranges may), the chunk count must be < 2^32
- * (FR_E_RANGE).  Synchronous: the plan's device tables are uploaded before
- * return.  The plan is immutable and bound to the device current at
+ * (FR_E_RANGE).  Synchronous: the plan's device tables are complete before
+ * return (they are partly built by a kernel on the null stream, which this
+ * call waits for; so create plans outside graph capture, as the allocations
+ * also require).  The plan is immutable and bound to the device current at
  * creation.  Launch shapes are read from the environment at creation, and
  * results never depend on them: FLASHRESTORE_TILE (every operation) or
  * FLASHRESTORE_TILE_PACK / _UNPACK / _VERIFY / _CHECKSUM select a tile
