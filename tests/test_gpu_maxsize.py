@@ -1,6 +1,9 @@
-"""Largest chunk size the ABI allows (C = 2^30): a chunk then spans 2^18
+"""The chunk-size extremes the ABI allows.  C = 2^30: a chunk spans 2^18
 slices and 2^14 sub-chunk accumulators, and a derived group spans two 1 GiB
-master chunks.  Whole-oracle parity on a 1.8 GB state with ragged tails."""
+master chunks (whole-oracle parity on a 1.8 GB state with ragged tails).
+C = 16: 20 million chunks and slots, so the plan's slot expansion, the
+finalize kernel and the 256- and 128-thread launches all loop over more
+work than one grid covers."""
 import numpy as np
 import pytest
 import torch
@@ -63,3 +66,23 @@ def test_one_gib_chunks():
     torch.cuda.synchronize()
     got = set(F.bitmap_indices(bad, plan.n_chunks).tolist())
     assert got == set(cpu.bitmap_to_set(obm, plan.n_chunks)) and 2 in got
+
+
+@pytest.mark.timeout(600)
+def test_twenty_million_sixteen_byte_chunks():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from tests.test_gpu_parity_small import _check_against_oracle
+
+    n = 40_000_000
+    # a bf16 parameter and its master, and an fp32 array with a ragged tail
+    t = np.array([(0, 0, n, W.BF16, 1), (2 * n, 2 * n, n, W.F32, -1),
+                  (6 * n, 6 * n, n // 2 + 3, W.F32, -1)], dtype=W.TABLE_DTYPE)
+    arena = (6 * n + 4 * (n // 2 + 3) + 15) // 16 * 16
+    C = 16
+    assert cpu.n_chunks(t, C) == 20_000_001  # slots of the pack walk: past 65,536 x 256
+    src = W.random_tiny_state(t, arena, np.random.default_rng(17))
+    log("state built")
+    _check_against_oracle(t, C, src, arena, arena, corrupt_rng=np.random.default_rng(18),
+                          tag="C=16, 20M chunks")
+    log("20M chunks: parity")
