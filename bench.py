@@ -33,7 +33,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 METRIC = "state restore GB/s per GPU (pack+checksum, unpack+verify) and % of HBM peak"
 KERNEL_SOURCES = ("paper_2509_03047_amd/csrc/kernels.hip", "paper_2509_03047_amd/csrc/fr_internal.h")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama8b_tp8.json")
 KERNEL_NAMES = {"pack": "k_pack", "unpack": "k_unpack", "verify": "k_verify", "checksum": "k_pack"}
 
 
