@@ -71,6 +71,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-delta", action="store_true", help="skip the delta-repair measurement")
     ap.add_argument("--delta-flips", type=int, default=4096)
+    ap.add_argument("--segment-align", type=int, default=None,
+                    help="payload segment alignment (default: the library's, 16)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time per baseline")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 4 GiB device copy (for counter scaling) and exit")
@@ -444,7 +446,7 @@ def main():
     torch.zeros(1, device="cuda")  # HIP runtime set-up, which the first plan would otherwise pay
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    plan = F.Plan(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
+    plan = F.Plan(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes, args.segment_align)
     plan_ms = (time.perf_counter() - t0) * 1e3  # validation, walks, device tables (once per rank)
     info = plan.info
     src = torch.from_numpy(src_np).to("cuda")
@@ -542,6 +544,7 @@ def main():
             "state_bytes": info["state_bytes"],
             "payload_bytes": info["payload_bytes"],
             "chunk_bytes": info["chunk_bytes"],
+            "segment_align": info["segment_align"],
             "n_chunks": info["n_chunks"],
             "step": "pack+checksum -> unpack+derive+verify -> verify_replicas -> checksum_state",
         },
@@ -557,7 +560,7 @@ def main():
         if not same_layout:  # repair within the donor's layout
             rtable = w.table.copy()
             rtable["dst_offset"] = rtable["src_offset"]
-            rplan = F.Plan(rtable, w.chunk_bytes, w.src_arena_bytes, w.src_arena_bytes)
+            rplan = F.Plan(rtable, w.chunk_bytes, w.src_arena_bytes, w.src_arena_bytes, args.segment_align)
         out["replica_compare"] = replica_compare(rplan, rtable, src, replica, stream)
         out["delta_repair"] = delta_repair(rplan, rtable, src, replica, rplan.info, args.delta_flips, stream)
         out["delta_repair"]["full_restore_ms"] = round(restore_ms, 4)

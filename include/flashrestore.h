@@ -44,12 +44,17 @@
  *     with ties to an even last bit, overflow to infinity, denormals rounded
  *     exactly (no flush to zero).
  *   Payload.  The bytes of every non-derived entry in table order; the
- *     segment of each non-empty one starts at the first multiple of 4096 at
- *     or after the end of the previous segment (0 for the first); an empty
- *     entry has no segment (its offset is the end so far rounded up to 16);
- *     payload_bytes = the end of the last segment rounded up to 16; every
- *     byte outside the segments is 0.  (Segments on 4 KiB boundaries let
- *     pack and unpack move whole aligned slices of the payload.)
+ *     segment of each non-empty one starts at the first multiple of the
+ *     plan's segment alignment A at or after the end of the previous segment
+ *     (0 for the first); an empty entry has no segment (its offset is the end
+ *     so far rounded up to 16); payload_bytes = the end of the last segment
+ *     rounded up to 16; every byte outside the segments is 0.  A = 16 by
+ *     default: the segments follow each other at 16-byte alignment.  A
+ *     larger A (fr_plan_create_ex; both sides of a transfer must use the
+ *     same) leaves wider zero gaps: with A = 4096, tensors at scattered
+ *     offsets pack and unpack faster, since every segment then starts on a
+ *     4 KiB boundary.  Tables whose sent tensors are multiples of A bytes get
+ *     the same payload for every A up to that size.
  *   Bitmaps.  Bit c of a result set lives in 32-bit word c / 32 at bit c % 32.
  *
  * Conventions
@@ -79,7 +84,7 @@
 extern "C" {
 #endif
 
-#define FR_ABI_VERSION 2
+#define FR_ABI_VERSION 3
 
 enum fr_dtype { FR_F32 = 1, FR_BF16 = 2 };
 
@@ -126,6 +131,7 @@ typedef struct fr_plan_info {
   uint64_t dst_arena_bytes;
   uint64_t state_bytes;     /* sum of nbytes over all entries */
   int64_t device;           /* HIP device the plan is bound to; -1 for a layout query */
+  uint64_t segment_align;   /* A: payload segments start at multiples of it */
 } fr_plan_info;
 
 /* ---------------------------------------------------------------- plans */
@@ -157,6 +163,14 @@ typedef struct fr_plan_info {
 int fr_plan_create(const fr_tensor_desc* table, uint32_t n_entries, uint64_t chunk_bytes,
                    uint64_t src_arena_bytes, uint64_t dst_arena_bytes, fr_plan** out);
 
+/* fr_plan_create with the payload segment alignment A given: a power of two
+ * in [16, 2^20] (FR_E_INVAL otherwise).  fr_plan_create is A = 16.  The
+ * payload (its size and every offset) depends on A, the sums and the
+ * restored state do not. */
+int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n_entries, uint64_t chunk_bytes,
+                      uint64_t src_arena_bytes, uint64_t dst_arena_bytes, uint64_t segment_align,
+                      fr_plan** out);
+
 /* Sizes of a plan.  Host only. */
 int fr_plan_get_info(const fr_plan* plan, fr_plan_info* out);
 
@@ -173,13 +187,13 @@ int fr_plan_entry_layout(const fr_plan* plan, uint32_t entry, uint64_t* payload_
  * destroy a plan while work that uses it is still pending on a stream. */
 int fr_plan_destroy(fr_plan* plan);
 
-/* The same validation and layout as fr_plan_create, on the host only, with no
- * device and no plan: fills `info` (device = -1) and, when non-NULL,
+/* The same validation and layout as fr_plan_create_ex, on the host only,
+ * with no device and no plan: fills `info` (device = -1) and, when non-NULL,
  * payload_offset[n_entries] (UINT64_MAX for derived entries) and
  * chunk_base[n_entries + 1]. */
 int fr_layout_query(const fr_tensor_desc* table, uint32_t n_entries, uint64_t chunk_bytes,
-                    uint64_t src_arena_bytes, uint64_t dst_arena_bytes, fr_plan_info* info,
-                    uint64_t* payload_offset, uint64_t* chunk_base);
+                    uint64_t src_arena_bytes, uint64_t dst_arena_bytes, uint64_t segment_align,
+                    fr_plan_info* info, uint64_t* payload_offset, uint64_t* chunk_base);
 
 /* ----------------------------------------------------------- operations */
 
@@ -234,23 +248,24 @@ int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums,
  *              each < n_chunks (FR_E_INVAL otherwise); n_ids may be 0
  * Delta payload: the bytes of every listed chunk of a non-derived entry, in
  * list order; a chunk that directly follows the previous sent chunk of its
- * entry starts where that one ends, any other at the first multiple of 4096
- * at or after it; the payload ends at the last chunk's end rounded up to 16;
- * every gap byte 0.  Listed chunks of derived (bf16) entries send nothing.
- * With every chunk listed the delta payload and sums equal fr_pack_state's;
- * with C >= 4096 the delta payload of a contiguous range of chunk ids (a
- * stripe) is fr_pack_state's payload from the range's first sent chunk on,
- * so stripes packed by several donors assemble into one payload.
+ * entry starts where that one ends, any other at the first multiple of the
+ * plan's segment alignment A at or after it; the payload ends at the last
+ * chunk's end rounded up to 16; every gap byte 0.  Listed chunks of derived
+ * (bf16) entries send nothing.  With every chunk listed the delta payload and
+ * sums equal fr_pack_state's; with C >= A the delta payload of a contiguous
+ * range of chunk ids (a stripe) is fr_pack_state's payload from the range's
+ * first sent chunk on, so stripes packed by several donors assemble into one
+ * payload.
  * All three take the list on the host.  Pack and unpack copy the list's unit
  * records (32 or 48 bytes per chunk) to a device buffer the plan keeps, on
  * `stream`, before their kernels; a list that needs more room than the
  * buffer has makes the call first synchronise the device and reallocate it
  * (an allocation: such a call cannot be captured into a graph). */
 
-/* Bytes of the delta payload for a list.  Host only.  (With C below 4096 a
+/* Bytes of the delta payload for a list.  Host only.  (With C below A a
  * sparse list can need more than the full payload's payload_bytes, since
- * each chunk that does not continue the previous one starts on a 4 KiB
- * boundary.) */
+ * each chunk that does not continue the previous one starts on a multiple
+ * of A.) */
 int fr_delta_layout(const fr_plan* plan, const uint32_t* chunk_ids, uint64_t n_ids,
                     uint64_t* payload_bytes);
 

@@ -31,19 +31,19 @@ def lib():
         l = C.CDLL(LIB)
         P = C.c_void_p
         u32, u64 = C.c_uint32, C.c_uint64
-        l.oro_plan.argtypes = [P, u32, u64, P, P, P, P]
+        l.oro_plan.argtypes = [P, u32, u64, u64, P, P, P, P]
         l.oro_frsum.argtypes = [P, u64, P, P]
         l.oro_rne_bf16.argtypes = [u32]
         l.oro_rne_bf16.restype = C.c_uint16
         l.oro_rne_bf16_array.argtypes = [P, P, u64]
-        l.oro_pack.argtypes = [P, u32, u64, P, P, P]
-        l.oro_unpack.argtypes = [P, u32, u64, P, P, P, P, P]
+        l.oro_pack.argtypes = [P, u32, u64, u64, P, P, P]
+        l.oro_unpack.argtypes = [P, u32, u64, u64, P, P, P, P, P]
         l.oro_verify.argtypes = [P, u32, u64, P, P, P, P, P, P]
         l.oro_checksum.argtypes = [P, u32, u64, P, P]
         l.oro_checksum_chunks.argtypes = [P, u32, u64, P, P, u64, P]
-        l.oro_delta_layout.argtypes = [P, u32, u64, P, u64, P, P]
-        l.oro_pack_chunks.argtypes = [P, u32, u64, P, P, u64, P, P]
-        l.oro_unpack_chunks.argtypes = [P, u32, u64, P, P, P, u64, P, P, P]
+        l.oro_delta_layout.argtypes = [P, u32, u64, u64, P, u64, P, P]
+        l.oro_pack_chunks.argtypes = [P, u32, u64, u64, P, P, u64, P, P]
+        l.oro_unpack_chunks.argtypes = [P, u32, u64, u64, P, P, P, u64, P, P, P]
         for f in ("oro_plan", "oro_pack", "oro_unpack", "oro_verify", "oro_checksum",
                   "oro_checksum_chunks", "oro_selfcheck", "oro_threads", "oro_delta_layout",
                   "oro_pack_chunks", "oro_unpack_chunks"):
@@ -78,7 +78,13 @@ def set_threads(n: int) -> None:
     lib().oro_set_threads(int(n))
 
 
-def plan(t: np.ndarray, C_: int):
+# Payload segment alignment: 16 packs the sent entries back to back (the
+# default reading of the payload layout); any larger power of two is the
+# same rule with wider zero gaps.
+SEGMENT = 16
+
+
+def plan(t: np.ndarray, C_: int, seg: int = SEGMENT):
     """Per-entry chunk counts, chunk bases (n+1), payload offsets, payload bytes."""
     t = _table(t)
     n = len(t)
@@ -86,8 +92,8 @@ def plan(t: np.ndarray, C_: int):
     base = np.zeros(n + 1, np.uint64)
     pay = np.zeros(n + 1, np.uint64)
     pb = np.zeros(1, np.uint64)
-    if lib().oro_plan(_p(t), n, C_, _p(nch), _p(base), _p(pay), _p(pb)) != 0:
-        raise ValueError("bad chunk size")
+    if lib().oro_plan(_p(t), n, C_, seg, _p(nch), _p(base), _p(pay), _p(pb)) != 0:
+        raise ValueError("bad chunk size or segment alignment")
     return nch[:n], base, pay[:n], int(pb[0])
 
 
@@ -113,25 +119,26 @@ def n_chunks(t, C_):
     return int(plan(t, C_)[1][-1])
 
 
-def pack(t, C_, src: np.ndarray):
+def pack(t, C_, src: np.ndarray, seg: int = SEGMENT):
     t = _table(t)
-    _, base, _, pb = plan(t, C_)
+    _, base, _, pb = plan(t, C_, seg)
     nc = int(base[-1])
     payload = np.empty(pb, np.uint8)
     sums = np.empty(2 * max(nc, 1), np.uint64)
-    if lib().oro_pack(_p(t), len(t), C_, _p(src), _p(payload), _p(sums)) != 0:
+    if lib().oro_pack(_p(t), len(t), C_, seg, _p(src), _p(payload), _p(sums)) != 0:
         raise RuntimeError("oro_pack")
     return payload, sums[: 2 * nc]
 
 
-def unpack(t, C_, payload: np.ndarray, sums: np.ndarray, dst: np.ndarray):
+def unpack(t, C_, payload: np.ndarray, sums: np.ndarray, dst: np.ndarray, seg: int = SEGMENT):
     """Writes into dst in place; returns (bitmap, n_bad)."""
     t = _table(t)
     nc = n_chunks(t, C_)
     bitmap = np.zeros(max((nc + 31) // 32, 1), np.uint32)
     nbad = np.zeros(1, np.uint64)
     sums = np.ascontiguousarray(sums, np.uint64)
-    if lib().oro_unpack(_p(t), len(t), C_, _p(payload), _p(sums), _p(dst), _p(bitmap), _p(nbad)) != 0:
+    if lib().oro_unpack(_p(t), len(t), C_, seg, _p(payload), _p(sums), _p(dst), _p(bitmap),
+                        _p(nbad)) != 0:
         raise RuntimeError("oro_unpack")
     return bitmap[: (nc + 31) // 32], int(nbad[0])
 
@@ -177,29 +184,30 @@ def bitmap_to_set(bitmap: np.ndarray, n: int) -> list:
 NO_PAYLOAD = (1 << 64) - 1
 
 
-def delta_layout(t, C_, ids):
+def delta_layout(t, C_, ids, seg: int = SEGMENT):
     """Per-list-position payload offsets (NO_PAYLOAD for derived) and payload bytes."""
     t = _table(t)
     ids = np.ascontiguousarray(ids, np.uint32)
     off = np.zeros(max(ids.size, 1), np.uint64)
     pb = np.zeros(1, np.uint64)
-    if lib().oro_delta_layout(_p(t), len(t), C_, _p(ids), ids.size, _p(off), _p(pb)) != 0:
+    if lib().oro_delta_layout(_p(t), len(t), C_, seg, _p(ids), ids.size, _p(off), _p(pb)) != 0:
         raise ValueError("bad chunk list")
     return off[: ids.size], int(pb[0])
 
 
-def pack_chunks(t, C_, src, ids):
+def pack_chunks(t, C_, src, ids, seg: int = SEGMENT):
     t = _table(t)
     ids = np.ascontiguousarray(ids, np.uint32)
-    _, pb = delta_layout(t, C_, ids)
+    _, pb = delta_layout(t, C_, ids, seg)
     payload = np.empty(max(pb, 1), np.uint8)
     sums = np.empty(2 * max(ids.size, 1), np.uint64)
-    if lib().oro_pack_chunks(_p(t), len(t), C_, _p(src), _p(ids), ids.size, _p(payload), _p(sums)) != 0:
+    if lib().oro_pack_chunks(_p(t), len(t), C_, seg, _p(src), _p(ids), ids.size, _p(payload),
+                             _p(sums)) != 0:
         raise RuntimeError("oro_pack_chunks")
     return payload[:pb], sums[: 2 * ids.size]
 
 
-def unpack_chunks(t, C_, payload, sums, ids, dst):
+def unpack_chunks(t, C_, payload, sums, ids, dst, seg: int = SEGMENT):
     """Writes into dst in place; returns (bitmap over list positions, n_bad)."""
     t = _table(t)
     ids = np.ascontiguousarray(ids, np.uint32)
@@ -209,7 +217,7 @@ def unpack_chunks(t, C_, payload, sums, ids, dst):
     if payload.size == 0:
         payload = np.zeros(1, np.uint8)
     sums = np.ascontiguousarray(sums, np.uint64)
-    if lib().oro_unpack_chunks(_p(t), len(t), C_, _p(payload), _p(sums), _p(ids), ids.size, _p(dst),
-                               _p(bitmap), _p(nbad)) != 0:
+    if lib().oro_unpack_chunks(_p(t), len(t), C_, seg, _p(payload), _p(sums), _p(ids), ids.size,
+                               _p(dst), _p(bitmap), _p(nbad)) != 0:
         raise RuntimeError("oro_unpack_chunks")
     return bitmap[: (ids.size + 31) // 32], int(nbad[0])

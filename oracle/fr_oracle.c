@@ -22,10 +22,12 @@
  *              (missing tail bytes read as 0);  sum = sum_i w_i mod 2^64,
  *              wsum = sum_i (i+1) w_i mod 2^64.
  *   payload    the bytes of every non-derived entry in table order, each
- *              segment starting at the next multiple of 4096 bytes after
- *              the previous one ends (an empty entry has no segment), the
- *              payload ending at the last segment's end rounded up to 16,
- *              every gap byte 0.
+ *              segment starting at the first multiple of the segment
+ *              alignment `seg` (a power of two >= 16) at or after the end of
+ *              the previous one (an empty entry has no segment), the payload
+ *              ending at the last segment's end rounded up to 16, every gap
+ *              byte 0.  seg = 16 packs the segments back to back; a larger
+ *              seg (e.g. 4096) is the same rule with wider gaps.
  *              A bf16 entry that derives from an fp32 master is not sent;
  *              its chunk sums are.
  *   RNE        fp32 -> bf16: the nearer of the two neighbouring bf16 values,
@@ -50,10 +52,9 @@
 
 static uint64_t esize_of(uint32_t dtype) { return dtype == ORO_F32 ? 4u : 2u; }
 static uint64_t align16(uint64_t x) { return (x + 15u) & ~(uint64_t)15u; }
-/* a payload segment starts at a multiple of ORO_SEGMENT_ALIGN */
-static uint64_t align_segment(uint64_t x) {
-  return (x + ORO_SEGMENT_ALIGN - 1) & ~(uint64_t)(ORO_SEGMENT_ALIGN - 1);
-}
+/* a payload segment starts at a multiple of seg (a power of two) */
+static uint64_t align_segment(uint64_t x, uint64_t seg) { return (x + seg - 1) & ~(seg - 1); }
+static int seg_ok(uint64_t seg) { return seg >= 16 && (seg & (seg - 1)) == 0; }
 
 static int host_is_little_endian(void) {
   const uint32_t one = 1;
@@ -64,9 +65,9 @@ static int host_is_little_endian(void) {
 
 /* ------------------------------------------------------------------ plan */
 
-int oro_plan(const oro_entry* t, uint32_t n, uint64_t C, uint64_t* nchunks,
+int oro_plan(const oro_entry* t, uint32_t n, uint64_t C, uint64_t seg, uint64_t* nchunks,
              uint64_t* chunk_base, uint64_t* pay_off, uint64_t* payload_bytes) {
-  if (C == 0 || (C & (C - 1)) != 0) return -1;
+  if (C == 0 || (C & (C - 1)) != 0 || !seg_ok(seg)) return -1;
   uint64_t base = 0, end = 0; /* end: where the last segment so far ends */
   for (uint32_t k = 0; k < n; k++) {
     uint64_t nb = t[k].numel * esize_of(t[k].dtype);
@@ -79,7 +80,7 @@ int oro_plan(const oro_entry* t, uint32_t n, uint64_t C, uint64_t* nchunks,
     } else if (nb == 0) {
       pay_off[k] = align16(end); /* an empty entry occupies no segment */
     } else {
-      pay_off[k] = align_segment(end);
+      pay_off[k] = align_segment(end, seg);
       end = pay_off[k] + nb;
     }
   }
@@ -178,12 +179,12 @@ typedef struct {
   uint64_t payload_bytes;
 } layout;
 
-static int make_layout(const oro_entry* t, uint32_t n, uint64_t C, layout* L) {
+static int make_layout(const oro_entry* t, uint32_t n, uint64_t C, uint64_t seg, layout* L) {
   L->nchunks = (uint64_t*)malloc(sizeof(uint64_t) * (n + 1));
   L->chunk_base = (uint64_t*)malloc(sizeof(uint64_t) * (n + 1));
   L->pay_off = (uint64_t*)malloc(sizeof(uint64_t) * (n + 1));
   if (!L->nchunks || !L->chunk_base || !L->pay_off) return -1;
-  return oro_plan(t, n, C, L->nchunks, L->chunk_base, L->pay_off, &L->payload_bytes);
+  return oro_plan(t, n, C, seg, L->nchunks, L->chunk_base, L->pay_off, &L->payload_bytes);
 }
 
 static void free_layout(layout* L) {
@@ -192,10 +193,10 @@ static void free_layout(layout* L) {
   free(L->pay_off);
 }
 
-int oro_pack(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* src, uint8_t* payload,
-             uint64_t* sums) {
+int oro_pack(const oro_entry* t, uint32_t n, uint64_t C, uint64_t seg, const uint8_t* src,
+             uint8_t* payload, uint64_t* sums) {
   layout L;
-  if (make_layout(t, n, C, &L)) return -1;
+  if (make_layout(t, n, C, seg, &L)) return -1;
   memset(payload, 0, L.payload_bytes);
   for (uint32_t k = 0; k < n; k++) {
     if (t[k].derive_from >= 0) continue;
@@ -206,10 +207,10 @@ int oro_pack(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* src, uin
   return 0;
 }
 
-int oro_unpack(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* payload,
+int oro_unpack(const oro_entry* t, uint32_t n, uint64_t C, uint64_t seg, const uint8_t* payload,
                const uint64_t* sums, uint8_t* dst, uint32_t* bitmap, uint64_t* n_bad) {
   layout L;
-  if (make_layout(t, n, C, &L)) return -1;
+  if (make_layout(t, n, C, seg, &L)) return -1;
   uint64_t total = L.chunk_base[n];
   for (uint32_t k = 0; k < n; k++) {
     if (t[k].derive_from >= 0) continue;
@@ -248,7 +249,7 @@ int oro_unpack(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* payloa
 int oro_verify(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* a, const uint8_t* b,
                uint32_t* bitmap, uint64_t* n_diff, uint64_t* sums_a, uint64_t* sums_b) {
   layout L;
-  if (make_layout(t, n, C, &L)) return -1;
+  if (make_layout(t, n, C, 16, &L)) return -1;  /* chunk map only */
   uint64_t total = L.chunk_base[n];
   uint8_t* differs = (uint8_t*)calloc(total ? total : 1, 1);
   if (!differs) return -1;
@@ -279,7 +280,7 @@ int oro_verify(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* a, con
 
 int oro_checksum(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* base, uint64_t* sums) {
   layout L;
-  if (make_layout(t, n, C, &L)) return -1;
+  if (make_layout(t, n, C, 16, &L)) return -1;  /* chunk map only */
   sums_of_arena(t, n, C, base, 0, L.chunk_base, sums);
   free_layout(&L);
   return 0;
@@ -290,7 +291,7 @@ int oro_checksum(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* base
 int oro_checksum_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* base,
                         const uint64_t* ids, uint64_t n_ids, uint64_t* sums) {
   layout L;
-  if (make_layout(t, n, C, &L)) return -1;
+  if (make_layout(t, n, C, 16, &L)) return -1;  /* chunk map only */
   for (uint64_t q = 0; q < n_ids; q++) {
     uint64_t c = ids[q];
     uint32_t lo = 0, hi = n; /* entry k with chunk_base[k] <= c < chunk_base[k+1] */
@@ -312,7 +313,7 @@ int oro_checksum_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_
  * global chunk ids in strictly increasing order.  Delta payload: the bytes of
  * every listed chunk of a non-derived entry, in list order; a chunk that
  * directly follows the previous sent chunk in its entry starts where that one
- * ends, any other at the next multiple of ORO_SEGMENT_ALIGN; the payload ends
+ * ends, any other at the next multiple of the segment alignment; the payload ends
  * at the last chunk's end rounded up to 16; every gap byte 0.  (With every
  * chunk listed this is the full payload.)  Listed chunks of a derived (bf16)
  * entry send nothing.  sums[i] is the FRSUM of chunk ids[i] at the sender.
@@ -344,10 +345,10 @@ static int list_ok(const layout* L, uint32_t n, const uint32_t* ids, uint64_t n_
   return 1;
 }
 
-int oro_delta_layout(const oro_entry* t, uint32_t n, uint64_t C, const uint32_t* ids,
+int oro_delta_layout(const oro_entry* t, uint32_t n, uint64_t C, uint64_t seg, const uint32_t* ids,
                      uint64_t n_ids, uint64_t* pay_off, uint64_t* payload_bytes) {
   layout L;
-  if (make_layout(t, n, C, &L)) return -1;
+  if (make_layout(t, n, C, seg, &L)) return -1;
   if (!list_ok(&L, n, ids, n_ids)) { free_layout(&L); return -1; }
   uint64_t end = 0;
   int have_prev = 0;
@@ -359,7 +360,7 @@ int oro_delta_layout(const oro_entry* t, uint32_t n, uint64_t C, const uint32_t*
     } else {
       uint64_t nb = t[w.entry].numel * esize_of(t[w.entry].dtype);
       int follows = have_prev && prev.entry == w.entry && prev.j + 1 == w.j;
-      pay_off[i] = follows ? end : align_segment(end);
+      pay_off[i] = follows ? end : align_segment(end, seg);
       end = pay_off[i] + chunk_len(nb, C, w.j);
       prev = w;
       have_prev = 1;
@@ -370,13 +371,13 @@ int oro_delta_layout(const oro_entry* t, uint32_t n, uint64_t C, const uint32_t*
   return 0;
 }
 
-int oro_pack_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* src,
+int oro_pack_chunks(const oro_entry* t, uint32_t n, uint64_t C, uint64_t seg, const uint8_t* src,
                     const uint32_t* ids, uint64_t n_ids, uint8_t* payload, uint64_t* sums) {
   uint64_t* off = (uint64_t*)malloc(sizeof(uint64_t) * (n_ids ? n_ids : 1));
   uint64_t pb;
-  if (!off || oro_delta_layout(t, n, C, ids, n_ids, off, &pb)) { free(off); return -1; }
+  if (!off || oro_delta_layout(t, n, C, seg, ids, n_ids, off, &pb)) { free(off); return -1; }
   layout L;
-  if (make_layout(t, n, C, &L)) { free(off); return -1; }
+  if (make_layout(t, n, C, seg, &L)) { free(off); return -1; }
   memset(payload, 0, pb);
   for (uint64_t i = 0; i < n_ids; i++) {
     chunk_loc w = locate(&L, n, ids[i]);
@@ -391,14 +392,15 @@ int oro_pack_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* s
   return 0;
 }
 
-int oro_unpack_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* payload,
+int oro_unpack_chunks(const oro_entry* t, uint32_t n, uint64_t C, uint64_t seg,
+                      const uint8_t* payload,
                       const uint64_t* sums, const uint32_t* ids, uint64_t n_ids, uint8_t* dst,
                       uint32_t* bitmap, uint64_t* n_bad) {
   uint64_t* off = (uint64_t*)malloc(sizeof(uint64_t) * (n_ids ? n_ids : 1));
   uint64_t pb;
-  if (!off || oro_delta_layout(t, n, C, ids, n_ids, off, &pb)) { free(off); return -1; }
+  if (!off || oro_delta_layout(t, n, C, seg, ids, n_ids, off, &pb)) { free(off); return -1; }
   layout L;
-  if (make_layout(t, n, C, &L)) { free(off); return -1; }
+  if (make_layout(t, n, C, seg, &L)) { free(off); return -1; }
   /* 1. the sent chunks */
   for (uint64_t i = 0; i < n_ids; i++) {
     if (off[i] == ORO_NO_PAYLOAD) continue;

@@ -10,7 +10,7 @@ from __future__ import annotations
 from fractions import Fraction
 
 M64 = (1 << 64) - 1
-SEGMENT = 4096  # a payload segment starts at a multiple of this
+SEGMENT = 16  # default: a payload segment starts at a multiple of this
 
 
 def _up(x, a):
@@ -60,7 +60,7 @@ def _esize(dt):
     return 4 if dt == 1 else 2
 
 
-def plan(table, C):
+def plan(table, C, seg=SEGMENT):
     nch, base, pay = [], [0], []
     end = 0
     for e in table:
@@ -72,7 +72,7 @@ def plan(table, C):
         elif nb == 0:
             pay.append(_up(end, 16))  # an empty entry occupies no segment
         else:
-            pay.append(_up(end, SEGMENT))
+            pay.append(_up(end, seg))
             end = pay[-1] + nb
     return nch, base, pay, _up(end, 16)
 
@@ -88,8 +88,8 @@ def _chunks(table, C, arena: bytes, key):
             c += 1
 
 
-def pack(table, C, src: bytes):
-    _, base, pay, pb = plan(table, C)
+def pack(table, C, src: bytes, seg=SEGMENT):
+    _, base, pay, pb = plan(table, C, seg)
     payload = bytearray(pb)
     for k, e in enumerate(table):
         if pay[k] is not None:
@@ -100,8 +100,8 @@ def pack(table, C, src: bytes):
     return bytes(payload), sums
 
 
-def unpack(table, C, payload: bytes, sums, dst: bytearray):
-    _, base, pay, _ = plan(table, C)
+def unpack(table, C, payload: bytes, sums, dst: bytearray, seg=SEGMENT):
+    _, base, pay, _ = plan(table, C, seg)
     for k, e in enumerate(table):
         nb = int(e["numel"]) * _esize(int(e["dtype"]))
         o = int(e["dst_offset"])
@@ -139,7 +139,7 @@ def _chunk_bytes(table, C, k, j, arena, key):
     return o, min(C, nb - j * C)
 
 
-def _delta_offsets(table, C, ids):
+def _delta_offsets(table, C, ids, seg=SEGMENT):
     """Payload offset of each listed chunk (None if derived) and the payload
     size: a chunk right after the previous sent chunk of its entry follows it,
     any other starts at the next segment boundary."""
@@ -151,15 +151,15 @@ def _delta_offsets(table, C, ids):
             offs.append(None)
             continue
         _, ln = _chunk_bytes(table, C, k, j, None, "src_offset")
-        offs.append(end if prev == (k, j - 1) else _up(end, SEGMENT))
+        offs.append(end if prev == (k, j - 1) else _up(end, seg))
         end = offs[-1] + ln
         prev = (k, j)
     return offs, _up(end, 16)
 
 
-def pack_chunks(table, C, src: bytes, ids):
+def pack_chunks(table, C, src: bytes, ids, seg=SEGMENT):
     cmap = _chunk_map(table, C)
-    offs, size = _delta_offsets(table, C, ids)
+    offs, size = _delta_offsets(table, C, ids, seg)
     payload = bytearray(size)
     sums = []
     for c, off in zip(ids, offs):
@@ -171,9 +171,9 @@ def pack_chunks(table, C, src: bytes, ids):
     return bytes(payload), sums
 
 
-def unpack_chunks(table, C, payload: bytes, sums, ids, dst: bytearray):
+def unpack_chunks(table, C, payload: bytes, sums, ids, dst: bytearray, seg=SEGMENT):
     cmap = _chunk_map(table, C)
-    offs, _ = _delta_offsets(table, C, ids)
+    offs, _ = _delta_offsets(table, C, ids, seg)
     for c, off in zip(ids, offs):
         k, j = cmap[c]
         if off is not None:

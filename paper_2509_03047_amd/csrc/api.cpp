@@ -257,7 +257,8 @@ void delta_layout(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids, Delt
     out->where[i] = w;
     if (d.derive_from >= 0) continue;
     const bool follows = have_prev && prev.entry == w.entry && prev.j + 1 == w.j;
-    const uint64_t at = follows ? end : (end + kSegmentAlign - 1) & ~(kSegmentAlign - 1);
+    const uint64_t seg = plan->layout.seg;
+    const uint64_t at = follows ? end : (end + seg - 1) & ~(seg - 1);
     out->off[i] = at;
     end = at + w.len;
     prev = w;

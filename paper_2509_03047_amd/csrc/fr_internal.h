@@ -11,10 +11,12 @@ namespace fr {
 
 constexpr uint64_t kNoPayload = ~uint64_t(0);
 // A payload segment (an entry, or a run of consecutive chunks of a delta
-// list) starts at a multiple of kSegmentAlign bytes: the slices of a segment
-// then start at 4 KiB boundaries of the payload, which on MI355X makes pack
-// up to a fifth faster on tables of many small or oddly placed tensors.
-constexpr uint64_t kSegmentAlign = 4096;
+// list) starts at a multiple of the plan's segment alignment: 16 by default
+// (segments back to back), up to kMaxSegmentAlign.  With 4096 the slices of
+// a segment start at 4 KiB boundaries of the payload, which on MI355X makes
+// pack up to a fifth faster on tables of many small or oddly placed tensors.
+constexpr uint64_t kDefaultSegmentAlign = 16;
+constexpr uint64_t kMaxSegmentAlign = uint64_t(1) << 20;
 constexpr uint32_t kNoMaster = 0xFFFFFFFFu;
 constexpr uint32_t kLine = 128;  // L2 cache line (bytes)
 
@@ -41,7 +43,7 @@ struct alignas(16) SrcUnit {
   uint32_t len;      // bytes in this chunk (<= C, even)
   uint32_t c;        // its sums slot: global chunk id, or list position for a delta
   uint32_t gap_v;    // zero vectors pack writes after the chunk's 16-byte-padded end
-                     //   (the gap up to the next segment; < kSegmentAlign / 16)
+                     //   (the gap up to the next segment; < segment alignment / 16)
   uint32_t lead;     // src_off mod kLine: how far into a cache line the chunk starts
 };
 static_assert(sizeof(SrcUnit) == 32, "SrcUnit is 32 bytes");
@@ -116,6 +118,7 @@ struct SlotRuns {
 // Host-side layout of a validated table.
 struct Layout {
   uint64_t C = 0;
+  uint64_t seg = 0;  // payload segment alignment
   uint64_t n_chunks = 0;
   uint64_t payload_bytes = 0;
   uint64_t state_bytes = 0;
@@ -123,8 +126,8 @@ struct Layout {
   std::vector<uint64_t> chunk_base;  // n_entries + 1
 };
 
-int validate_and_layout(const fr_tensor_desc* table, uint32_t n, uint64_t C, uint64_t src_bytes,
-                        uint64_t dst_bytes, Layout* out);
+int validate_and_layout(const fr_tensor_desc* table, uint32_t n, uint64_t C, uint64_t seg,
+                        uint64_t src_bytes, uint64_t dst_bytes, Layout* out);
 
 // Launch configuration of a plan.  A tile is B threads x U 16-byte vectors
 // per workgroup: 0 = 256x1, 1 = 512x1, 2 = 256x2, 3 = 256x4, 4 = 64x4,

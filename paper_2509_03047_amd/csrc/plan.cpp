@@ -27,13 +27,14 @@ constexpr bool kDefaultLinePack = false, kDefaultLineVerify = true, kDefaultLine
 
 static uint64_t esize(uint32_t dtype) { return dtype == FR_F32 ? 4 : 2; }
 static uint64_t align16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
-static uint64_t align_segment(uint64_t x) { return (x + kSegmentAlign - 1) & ~(kSegmentAlign - 1); }
+static uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) & ~(a - 1); }
 
-int validate_and_layout(const fr_tensor_desc* t, uint32_t n, uint64_t C, uint64_t src_bytes,
-                        uint64_t dst_bytes, Layout* L) {
+int validate_and_layout(const fr_tensor_desc* t, uint32_t n, uint64_t C, uint64_t seg,
+                        uint64_t src_bytes, uint64_t dst_bytes, Layout* L) {
   if (n > 0 && t == nullptr) return FR_E_INVAL;
   if (n > 0x7FFFFFFFu) return FR_E_INVAL;
   if (C < 16 || C > (uint64_t(1) << 30) || (C & (C - 1)) != 0) return FR_E_INVAL;
+  if (seg < 16 || seg > kMaxSegmentAlign || (seg & (seg - 1)) != 0) return FR_E_INVAL;
   // Field checks, in an order that makes the reported error deterministic:
   // dtype and derive_from first (INVAL), then alignment, then ranges.
   std::vector<uint8_t> used_as_master(n, 0);
@@ -72,6 +73,7 @@ int validate_and_layout(const fr_tensor_desc* t, uint32_t n, uint64_t C, uint64_
     if (ranges[i].first < ranges[i - 1].second) return FR_E_OVERLAP;
 
   L->C = C;
+  L->seg = seg;
   L->pay_off.assign(n, 0);
   L->chunk_base.assign(size_t(n) + 1, 0);
   uint64_t base = 0, end = 0;  // end of the last payload segment so far
@@ -84,7 +86,7 @@ int validate_and_layout(const fr_tensor_desc* t, uint32_t n, uint64_t C, uint64_
     } else if (nb == 0) {
       L->pay_off[k] = align16(end);  // an empty entry occupies no segment
     } else {
-      L->pay_off[k] = align_segment(end);
+      L->pay_off[k] = align_up(end, seg);
       end = L->pay_off[k] + nb;
     }
   }
@@ -107,6 +109,7 @@ static void fill_info(const Layout& L, uint32_t n, uint64_t src, uint64_t dst, i
   info->dst_arena_bytes = dst;
   info->state_bytes = L.state_bytes;
   info->device = dev;
+  info->segment_align = L.seg;
 }
 
 static uint32_t env_u32(const char* name, uint32_t dflt) {
@@ -122,13 +125,14 @@ static uint32_t env_u32(const char* name, uint32_t dflt) {
 using namespace fr;
 
 extern "C" int fr_layout_query(const fr_tensor_desc* table, uint32_t n, uint64_t C,
-                               uint64_t src_bytes, uint64_t dst_bytes, fr_plan_info* info,
-                               uint64_t* payload_offset, uint64_t* chunk_base) {
+                               uint64_t src_bytes, uint64_t dst_bytes, uint64_t seg,
+                               fr_plan_info* info, uint64_t* payload_offset,
+                               uint64_t* chunk_base) {
   if (!info) return FR_E_INVAL;
   Layout L;
   int rc;
   try {
-    rc = validate_and_layout(table, n, C, src_bytes, dst_bytes, &L);
+    rc = validate_and_layout(table, n, C, seg, src_bytes, dst_bytes, &L);
   } catch (const std::bad_alloc&) {
     return FR_E_NOMEM;
   }
@@ -399,13 +403,14 @@ int build_scratch(fr_plan* p) {
 
 }  // namespace
 
-extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t C,
-                              uint64_t src_bytes, uint64_t dst_bytes, fr_plan** out) {
+extern "C" int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n, uint64_t C,
+                                 uint64_t src_bytes, uint64_t dst_bytes, uint64_t seg,
+                                 fr_plan** out) {
   if (!out) return FR_E_INVAL;
   fr_plan* p = nullptr;
   try {
     p = new fr_plan();
-    int rc = validate_and_layout(table, n, C, src_bytes, dst_bytes, &p->layout);
+    int rc = validate_and_layout(table, n, C, seg, src_bytes, dst_bytes, &p->layout);
     if (rc != FR_OK) {
       delete p;
       return rc;
@@ -452,6 +457,11 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
   }
   *out = p;
   return FR_OK;
+}
+
+extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t C,
+                              uint64_t src_bytes, uint64_t dst_bytes, fr_plan** out) {
+  return fr_plan_create_ex(table, n, C, src_bytes, dst_bytes, kDefaultSegmentAlign, out);
 }
 
 extern "C" int fr_plan_get_info(const fr_plan* p, fr_plan_info* info) {

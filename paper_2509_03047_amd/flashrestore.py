@@ -49,6 +49,7 @@ class fr_plan_info(C.Structure):
         ("dst_arena_bytes", C.c_uint64),
         ("state_bytes", C.c_uint64),
         ("device", C.c_int64),
+        ("segment_align", C.c_uint64),
     ]
 
     def as_dict(self):
@@ -93,11 +94,12 @@ def _load():
     P, u32, u64, i32 = C.c_void_p, C.c_uint32, C.c_uint64, C.c_int
     sig = {
         "fr_plan_create": [P, u32, u64, u64, u64, C.POINTER(P)],
+        "fr_plan_create_ex": [P, u32, u64, u64, u64, u64, C.POINTER(P)],
         "fr_plan_get_info": [P, C.POINTER(fr_plan_info)],
         "fr_plan_chunk_of": [P, u32, u64, C.POINTER(u64)],
         "fr_plan_entry_layout": [P, u32, C.POINTER(u64), C.POINTER(u64), C.POINTER(u64)],
         "fr_plan_destroy": [P],
-        "fr_layout_query": [P, u32, u64, u64, u64, C.POINTER(fr_plan_info), P, P],
+        "fr_layout_query": [P, u32, u64, u64, u64, u64, C.POINTER(fr_plan_info), P, P],
         "fr_pack_state": [P, P, P, u64, P, P],
         "fr_unpack_state": [P, P, P, P, P, P, P],
         "fr_verify_replicas": [P, P, P, P, P, P, P, P],
@@ -124,7 +126,7 @@ def _load():
         f.argtypes = args
         f.restype = C.c_int
     lib.fr_strerror.restype = C.c_char_p
-    if lib.fr_abi_version() != 2:
+    if lib.fr_abi_version() != 3:
         raise ImportError("libflashrestore ABI version mismatch")
     return lib
 
@@ -132,7 +134,7 @@ def _load():
 _lib = _load()
 
 EXPORTED = (
-    "fr_plan_create", "fr_plan_get_info", "fr_plan_chunk_of", "fr_plan_entry_layout",
+    "fr_plan_create", "fr_plan_create_ex", "fr_plan_get_info", "fr_plan_chunk_of", "fr_plan_entry_layout",
     "fr_plan_destroy", "fr_layout_query", "fr_pack_state", "fr_unpack_state",
     "fr_verify_replicas", "fr_checksum_state", "fr_delta_layout", "fr_pack_chunks",
     "fr_unpack_chunks", "fr_tracker_create", "fr_tracker_destroy", "fr_tracker_heartbeat",
@@ -196,28 +198,41 @@ def _stream(stream) -> int | None:
     return stream.cuda_stream or None
 
 
-def fr_layout_query(table, chunk_bytes: int, src_arena_bytes: int, dst_arena_bytes: int):
+# Default payload segment alignment (fr_plan_create): segments back to back
+# at 16-byte alignment.
+SEGMENT_ALIGN = 16
+
+
+def fr_layout_query(table, chunk_bytes: int, src_arena_bytes: int, dst_arena_bytes: int,
+                    segment_align: int = SEGMENT_ALIGN):
     """Host-only validation and layout: (info dict, payload offsets, chunk bases)."""
     t = as_table(table)
     info = fr_plan_info()
     pay = np.zeros(max(len(t), 1), np.uint64)
     base = np.zeros(len(t) + 1, np.uint64)
     rc = _lib.fr_layout_query(t.ctypes.data if len(t) else None, len(t), chunk_bytes,
-                              src_arena_bytes, dst_arena_bytes, C.byref(info),
+                              src_arena_bytes, dst_arena_bytes, segment_align, C.byref(info),
                               pay.ctypes.data, base.ctypes.data)
     _check(rc, "fr_layout_query")
     return info.as_dict(), pay[: len(t)], base
 
 
 class Plan:
-    """A plan bound to the current HIP device (``fr_plan_create``)."""
+    """A plan bound to the current HIP device: ``fr_plan_create``, or
+    ``fr_plan_create_ex`` when a payload segment alignment is given."""
 
-    def __init__(self, table, chunk_bytes: int, src_arena_bytes: int, dst_arena_bytes: int):
+    def __init__(self, table, chunk_bytes: int, src_arena_bytes: int, dst_arena_bytes: int,
+                 segment_align: int | None = None):
         self._h = None
         self.table = as_table(table)
         h = C.c_void_p()
-        rc = _lib.fr_plan_create(self.table.ctypes.data if len(self.table) else None, len(self.table),
-                                 chunk_bytes, src_arena_bytes, dst_arena_bytes, C.byref(h))
+        tp = self.table.ctypes.data if len(self.table) else None
+        if segment_align is None:
+            rc = _lib.fr_plan_create(tp, len(self.table), chunk_bytes, src_arena_bytes, dst_arena_bytes,
+                                     C.byref(h))
+        else:
+            rc = _lib.fr_plan_create_ex(tp, len(self.table), chunk_bytes, src_arena_bytes,
+                                        dst_arena_bytes, segment_align, C.byref(h))
         _check(rc, "fr_plan_create")
         self._h = h
         info = fr_plan_info()
@@ -337,6 +352,10 @@ def _nbytes(x):
 
 def fr_plan_create(table, chunk_bytes, src_arena_bytes, dst_arena_bytes) -> Plan:
     return Plan(table, chunk_bytes, src_arena_bytes, dst_arena_bytes)
+
+
+def fr_plan_create_ex(table, chunk_bytes, src_arena_bytes, dst_arena_bytes, segment_align) -> Plan:
+    return Plan(table, chunk_bytes, src_arena_bytes, dst_arena_bytes, segment_align)
 
 
 def fr_plan_destroy(plan: Plan) -> None:

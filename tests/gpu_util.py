@@ -32,8 +32,8 @@ def sums_host(t: torch.Tensor, n: int) -> np.ndarray:
 class Restore:
     """Buffers and calls of one pack -> unpack -> verify -> checksum pass."""
 
-    def __init__(self, table, chunk_bytes, src_bytes, dst_bytes, canary=0xA5):
-        self.plan = F.Plan(table, chunk_bytes, src_bytes, dst_bytes)
+    def __init__(self, table, chunk_bytes, src_bytes, dst_bytes, canary=0xA5, seg=None):
+        self.plan = F.Plan(table, chunk_bytes, src_bytes, dst_bytes, seg)
         self.src_bytes, self.dst_bytes = src_bytes, dst_bytes
         # pack must write every payload byte, padding and gaps included
         self.payload = self.plan.empty_payload().fill_(0xEE)

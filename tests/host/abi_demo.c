@@ -101,7 +101,7 @@ int main(void) {
 
   /* the oracle's outputs */
   uint64_t nch[N_ENTRIES], base[N_ENTRIES + 1], pay[N_ENTRIES], pb = 0;
-  CHECK(oro_plan(o, N_ENTRIES, C, nch, base, pay, &pb) == 0, "oracle plan");
+  CHECK(oro_plan(o, N_ENTRIES, C, 16, nch, base, pay, &pb) == 0, "oracle plan");
   const uint64_t n = base[N_ENTRIES];
   uint8_t* o_pay = calloc(pb ? pb : 1, 1);
   uint64_t* o_sums = calloc(2 * n, 8);
@@ -110,8 +110,8 @@ int main(void) {
   uint64_t o_nbad = 0;
   CHECK(o_pay && o_sums && o_dst && o_bm, "host allocation");
   memset(o_dst, 0x5A, dst_bytes);
-  CHECK(oro_pack(o, N_ENTRIES, C, src, o_pay, o_sums) == 0, "oracle pack");
-  CHECK(oro_unpack(o, N_ENTRIES, C, o_pay, o_sums, o_dst, o_bm, &o_nbad) == 0 && o_nbad == 0,
+  CHECK(oro_pack(o, N_ENTRIES, C, 16, src, o_pay, o_sums) == 0, "oracle pack");
+  CHECK(oro_unpack(o, N_ENTRIES, C, 16, o_pay, o_sums, o_dst, o_bm, &o_nbad) == 0 && o_nbad == 0,
         "oracle unpack");
 
   /* device buffers and a stream of default priority */
@@ -193,22 +193,23 @@ int main(void) {
   /* delta repair: re-send the flagged chunk and a derived parameter chunk
    * (recomputed from the receiver's master) into the diverged replica.
    * Replicas share the donor's layout, so the repair plan's receiver layout
-   * is the sender's (chunk ids are the same in both plans). */
+   * is the sender's (chunk ids are the same in both plans).  This plan
+   * places payload segments on 4 KiB boundaries, the main one packs them. */
   fr_tensor_desc t2[N_ENTRIES];
   oro_entry o2[N_ENTRIES];
   memcpy(t2, t, sizeof t);
   memcpy(o2, o, sizeof o);
   for (int e = 0; e < N_ENTRIES; e++) t2[e].dst_offset = o2[e].dst_offset = t[e].src_offset;
   fr_plan* rplan = NULL;
-  FR(fr_plan_create(t2, N_ENTRIES, C, src_bytes, src_bytes, &rplan));
+  FR(fr_plan_create_ex(t2, N_ENTRIES, C, src_bytes, src_bytes, 4096, &rplan));
   const uint32_t ids[2] = {0u, (uint32_t)chunk};
   uint64_t dpb = 0, o_dpb = 0, o_doff[2];
   FR(fr_delta_layout(rplan, ids, 2, &dpb));
-  CHECK(oro_delta_layout(o2, N_ENTRIES, C, ids, 2, o_doff, &o_dpb) == 0 && dpb == o_dpb,
+  CHECK(oro_delta_layout(o2, N_ENTRIES, C, 4096, ids, 2, o_doff, &o_dpb) == 0 && dpb == o_dpb,
         "delta payload size equals the oracle's");
   uint8_t* o_dpay = calloc(dpb, 1);
   uint64_t o_dsums[4];
-  CHECK(o_dpay && oro_pack_chunks(o2, N_ENTRIES, C, src, ids, 2, o_dpay, o_dsums) == 0,
+  CHECK(o_dpay && oro_pack_chunks(o2, N_ENTRIES, C, 4096, src, ids, 2, o_dpay, o_dsums) == 0,
         "oracle delta pack");
   void* d_dpay;
   fr_chunk_sum* d_dsums;

@@ -97,7 +97,8 @@ void tracker_and_planner() {
       fr_layout_state_table(&L, r, numel.data(), uint32_t(numel.size()), tab.data(), ne, &ne, &ab);
       fr_plan_info info;
       std::vector<uint64_t> po(ne + 1), cb(ne + 2);
-      fr_layout_query(tab.data(), ne, 1ull << (4 + U(12)), ab, ab, &info, po.data(), cb.data());
+      fr_layout_query(tab.data(), ne, 1ull << (4 + U(12)), ab, ab, 16ull << U(9), &info, po.data(),
+                      cb.data());
     }
   }
 }
@@ -126,7 +127,8 @@ void table_validation() {
     fr_plan_info info;
     std::vector<uint64_t> po(n + 1), cb(n + 2);
     const uint64_t C = U(8) == 0 ? U(1 << 20) : (1ull << (4 + U(27)));
-    fr_layout_query(n ? t.data() : nullptr, n, C, arena, arena, &info, po.data(), cb.data());
+    const uint64_t seg = U(8) == 0 ? U(1 << 22) : (16ull << U(17));  // sometimes invalid
+    fr_layout_query(n ? t.data() : nullptr, n, C, arena, arena, seg, &info, po.data(), cb.data());
   }
 }
 
@@ -153,8 +155,9 @@ int delta_layout_vs_oracle() {
       off += (t[k].numel * (t[k].dtype == FR_F32 ? 4 : 2) + 15) & ~15ull;
     }
     const uint64_t C = 1ull << (4 + U(14));
+    const uint64_t seg = 16ull << U(10);
     fr_plan p;
-    if (fr::validate_and_layout(t.data(), n, C, off, off, &p.layout) != FR_OK) continue;
+    if (fr::validate_and_layout(t.data(), n, C, seg, off, off, &p.layout) != FR_OK) continue;
     p.table = t;
     p.src_arena_bytes = p.dst_arena_bytes = off;
     std::vector<uint32_t> ids;
@@ -166,7 +169,7 @@ int delta_layout_vs_oracle() {
     for (uint32_t k = 0; k < n; k++)
       ot[k] = oro_entry{t[k].src_offset, t[k].dst_offset, t[k].numel, t[k].dtype, t[k].derive_from};
     std::vector<uint64_t> oo(ids.size() + 1);
-    if (oro_delta_layout(ot.data(), n, C, ids.data(), ids.size(), oo.data(), &exp) != 0) return 1;
+    if (oro_delta_layout(ot.data(), n, C, seg, ids.data(), ids.size(), oo.data(), &exp) != 0) return 1;
     if (got != exp) bad++;
     std::vector<uint32_t> all(p.layout.n_chunks);
     for (uint64_t c = 0; c < all.size(); c++) all[c] = uint32_t(c);

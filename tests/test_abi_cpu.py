@@ -49,15 +49,16 @@ def test_library_is_gfx950_only():
 
 
 def test_version_and_strerror():
-    assert F.fr_abi_version() == 2
+    assert F.fr_abi_version() == 3
     msgs = {c: F.fr_strerror(c) for c in range(-7, 1)}
     assert msgs[0] == "ok" and len(set(msgs.values())) == 8
     assert F.fr_strerror(-99) == "unknown status"
 
 
-def _check_layout(t, C, sb, db):
-    info, pay, base = F.fr_layout_query(t, C, sb, db)
-    nch, obase, opay, opb = cpu.plan(t, C)
+def _check_layout(t, C, sb, db, seg=16):
+    info, pay, base = F.fr_layout_query(t, C, sb, db, seg)
+    nch, obase, opay, opb = cpu.plan(t, C, seg)
+    assert info["segment_align"] == seg
     assert info["payload_bytes"] == opb
     assert info["n_chunks"] == int(obase[-1])
     assert info["bitmap_words"] == (int(obase[-1]) + 31) // 32
@@ -74,12 +75,19 @@ def _check_layout(t, C, sb, db):
 def test_layout_matches_oracle_on_workloads(config):
     w = W.make_workload(config)
     info = _check_layout(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
-    # toy: 12 B per param plus 14 gaps of 3 KiB after its 1 KiB norm arrays
-    # (segments start at 4 KiB boundaries); the 8B and 70B shares have none
-    exp = {0: (804, 44_098_560), 1: (214_684, 12_048_187_392), 3: (30_474, 27_249_082_368)}
+    # 12 payload bytes per param, segments back to back
+    exp = {0: (804, 44_055_552), 1: (214_684, 12_048_187_392), 3: (30_474, 27_249_082_368)}
     if config in exp:
         assert (info["n_chunks"], info["payload_bytes"]) == exp[config]
+        assert info["payload_bytes"] == 12 * w.n_params
         assert info["state_bytes"] == 14 * w.n_params
+    # 4 KiB segments: the toy gains 14 gaps of 3 KiB after its 1 KiB norm
+    # arrays; the 8B and 70B shares, whose tensors are whole multiples of
+    # 4 KiB, keep the same payload
+    info4 = _check_layout(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes, 4096)
+    exp4 = {0: 44_098_560, 1: 12_048_187_392, 3: 27_249_082_368}
+    if config in exp4:
+        assert info4["payload_bytes"] == exp4[config]
 
 
 def test_layout_matches_both_oracles_on_random_tables():
@@ -87,9 +95,10 @@ def test_layout_matches_both_oracles_on_random_tables():
     for _ in range(300):
         t, sb, db = W.random_tiny_table(rng)
         C = int(rng.choice([16, 32, 64, 256, 4096]))
-        _check_layout(t, C, sb, db)
-        _, mbase, mpay, mpb = mini.plan(t, C)
-        info, pay, base = F.fr_layout_query(t, C, sb, db)
+        seg = int(rng.choice([16, 32, 256, 4096, 1 << 20]))
+        _check_layout(t, C, sb, db, seg)
+        _, mbase, mpay, mpb = mini.plan(t, C, seg)
+        info, pay, base = F.fr_layout_query(t, C, sb, db, seg)
         assert list(base) == mbase and info["payload_bytes"] == mpb
 
 
@@ -151,6 +160,17 @@ def test_sender_ranges_may_overlap_and_empty_entries_are_fine():
 @pytest.mark.parametrize("C, code", [(0, -1), (8, -1), (48, -1), (1 << 31, -1), (16, 0), (1 << 30, 0)])
 def test_chunk_size_rule(C, code):
     assert _q(_rows(), C=C) == code
+
+
+@pytest.mark.parametrize("seg, code", [(0, -1), (8, -1), (48, -1), (1 << 21, -1), (16, 0), (4096, 0),
+                                       (1 << 20, 0)])
+def test_segment_alignment_rule(seg, code):
+    try:
+        F.fr_layout_query(_rows(), 64, 4096, 4096, seg)
+        rc = 0
+    except F.FlashRestoreError as e:
+        rc = e.status
+    assert rc == code
 
 
 def test_chunk_id_limit():

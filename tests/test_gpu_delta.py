@@ -23,17 +23,18 @@ def _gpu():
         pytest.skip("no GPU")
 
 
-def _one(t, C, src_np, recv_np, ids, rng, tag):
-    plan = F.Plan(t, C, max(src_np.size, 16), max(recv_np.size, 16))
+def _one(t, C, src_np, recv_np, ids, rng, tag, seg=None):
+    plan = F.Plan(t, C, max(src_np.size, 16), max(recv_np.size, 16), seg)
+    oseg = cpu.SEGMENT if seg is None else seg
     src = to_dev(src_np) if src_np.size else torch.zeros(16, dtype=torch.uint8, device="cuda")
     dst = to_dev(recv_np) if recv_np.size else torch.zeros(16, dtype=torch.uint8, device="cuda")
     pb = plan.delta_layout(ids)
-    off, opb = cpu.delta_layout(t, C, ids)
+    off, opb = cpu.delta_layout(t, C, ids, oseg)
     assert pb == opb, tag
     payload = torch.full((max(pb, 16),), 0xEE, dtype=torch.uint8, device="cuda")  # gaps must be written
     sums = torch.empty(max(ids.size, 1), 2, dtype=torch.int64, device="cuda")
     plan.pack_chunks(src, ids, payload, sums)
-    opay, osums = cpu.pack_chunks(t, C, src_np, ids)
+    opay, osums = cpu.pack_chunks(t, C, src_np, ids, oseg)
     torch.cuda.synchronize()
     assert np.array_equal(to_host(payload)[:pb], opay), f"payload {tag}"
     assert np.array_equal(sums_host(sums, ids.size), osums), f"sums {tag}"
@@ -45,7 +46,7 @@ def _one(t, C, src_np, recv_np, ids, rng, tag):
     nbad = torch.empty(1, dtype=torch.int64, device="cuda")
     plan.unpack_chunks(payload, sums, ids, dst, bad, nbad)
     orecv = recv_np.copy()
-    obm, onbad = cpu.unpack_chunks(t, C, opay, osums, ids, orecv)
+    obm, onbad = cpu.unpack_chunks(t, C, opay, osums, ids, orecv, oseg)
     torch.cuda.synchronize()
     if recv_np.size:
         assert np.array_equal(to_host(dst)[: recv_np.size], orecv), f"dst {tag}"
@@ -66,6 +67,22 @@ def test_delta_bruteforce_tiny_tables():
         _one(t, C, src, recv, ids, rng, f"table {it} C={C} ids={ids.size}")
         if it % 100 == 0:
             log(f"delta tiny {it}")
+
+
+def test_delta_segment_alignments():
+    """Delta lists on plans with explicit segment alignments 16 to 2^20."""
+    rng = np.random.default_rng(72)
+    for it in range(150):
+        seg = int(rng.choice([16, 64, 4096, 1 << 20]))
+        t, sb, db = W.random_tiny_table(rng)
+        C = int(rng.choice([16, 32, 64, 256]))
+        nc = cpu.n_chunks(t, C)
+        k = int(rng.integers(0, nc + 1))
+        ids = np.sort(rng.choice(nc, size=k, replace=False)).astype(np.uint32) if nc else np.zeros(0, np.uint32)
+        src = W.random_tiny_state(t, sb, rng)
+        recv = rng.integers(0, 256, size=db, dtype=np.uint8)
+        _one(t, C, src, recv, ids, rng, f"seg {seg} table {it} C={C} ids={ids.size}", seg)
+    log("delta segment alignments")
 
 
 @pytest.mark.parametrize("tile", [0, 2, 4, 5, 9])
@@ -150,10 +167,12 @@ def test_repair_llama8b_share_from_the_flagged_chunks():
     log(f"repaired {ids.size} chunks with {pb} payload bytes")
 
 
+@pytest.mark.parametrize("seg", [None, 4096])
 @pytest.mark.parametrize("k", [1, 3, 8])
-def test_striped_transfer_restores_like_one_payload(k):
+def test_striped_transfer_restores_like_one_payload(k, seg):
     """Multi-donor striping on one GPU: contiguous chunk ranges packed
-    separately (C >= 4 KiB) are byte slices of the full payload, and placed
+    separately (C >= the segment alignment) are byte slices of the full
+    payload, and placed
     at their offsets they form a buffer that one fr_unpack_state restores to
     the oracle's receiver arena; the gaps between segments are never read."""
     from tests.gpu_util import striped_payload, stripe_ranges
@@ -162,14 +181,16 @@ def test_striped_transfer_restores_like_one_payload(k):
     cases = []
     for _ in range(4):
         t, sb, db = W.random_tiny_table(rng, max_entries=10, max_numel=60_000)
-        cases.append((t, int(rng.choice([4096, 16384, 65536])), W.random_tiny_state(t, sb, rng), sb, db))
+        cs = [256, 4096, 16384, 65536] if seg is None else [4096, 16384, 65536]
+        cases.append((t, int(rng.choice(cs)), W.random_tiny_state(t, sb, rng), sb, db))
     w = W.make_workload(0)
     cases.append((w.table, w.chunk_bytes, W.fill_state(w), w.src_arena_bytes, w.dst_arena_bytes))
+    oseg = cpu.SEGMENT if seg is None else seg
     for t, C, src_np, sb, db in cases:
-        plan = F.Plan(t, C, sb, db)
+        plan = F.Plan(t, C, sb, db, seg)
         src = to_dev(src_np) if src_np.size else torch.empty(16, dtype=torch.uint8, device="cuda")
         recv, sums, parts = striped_payload(plan, t, src, stripe_ranges(plan.n_chunks, k))
-        opay, osums = cpu.pack(t, C, src_np)
+        opay, osums = cpu.pack(t, C, src_np, oseg)
         for (a, b), off, sp, ss in parts:
             assert np.array_equal(sums_host(ss, b - a), osums[2 * a:2 * b])
             if off is not None:
@@ -178,7 +199,7 @@ def test_striped_transfer_restores_like_one_payload(k):
         bad, nbad = plan.empty_bitmap(), plan.empty_counter()
         plan.unpack(recv, sums, dst, bad, nbad)
         odst = np.full(max(db, 1), 0x5A, np.uint8)
-        cpu.unpack(t, C, opay, osums, odst)
+        cpu.unpack(t, C, opay, osums, odst, oseg)
         torch.cuda.synchronize()
         assert int(nbad.item()) == 0 and np.array_equal(to_host(dst), odst)
 
@@ -197,8 +218,7 @@ def test_delta_every_subset_of_a_small_table():
     plan = F.Plan(t, C, sb, db)
     src = to_dev(src_np)
     lists = [np.array([c for c in range(n) if mask >> c & 1], dtype=np.uint32) for mask in range(1 << n)]
-    # a list with gaps starts a 4 KiB segment per run of chunks, so it can
-    # need more room than the full payload
+    # the largest of the lists' payloads
     payload = torch.empty(max(plan.delta_layout(ids) for ids in lists), dtype=torch.uint8, device="cuda")
     sums = torch.empty(n, 2, dtype=torch.int64, device="cuda")
     bad = torch.empty(1, dtype=torch.int32, device="cuda")

@@ -22,11 +22,13 @@ def _gpu():
     from paper_2509_03047_amd import flashrestore  # noqa: F401  (fails loudly if unbuilt)
 
 
-def _check_against_oracle(t, C, src_np, src_bytes, dst_bytes, corrupt_rng=None, tag=""):
-    r = Restore(t, C, src_bytes, dst_bytes)
+def _check_against_oracle(t, C, src_np, src_bytes, dst_bytes, corrupt_rng=None, tag="", seg=None):
+    """seg: payload segment alignment (None: the default, 16)."""
+    r = Restore(t, C, src_bytes, dst_bytes, seg=seg)
+    oseg = cpu.SEGMENT if seg is None else seg
     src = to_dev(src_np) if src_np.size else torch.empty(1, dtype=torch.uint8, device="cuda")
     r.pack(src)
-    pay, sums = cpu.pack(t, C, src_np)
+    pay, sums = cpu.pack(t, C, src_np, oseg)
     nc = r.n_chunks
     g_pay = to_host(r.payload)[: pay.size]
     g_sums = sums_host(r.sums, nc)
@@ -43,7 +45,7 @@ def _check_against_oracle(t, C, src_np, src_bytes, dst_bytes, corrupt_rng=None, 
         r.sums[c, 0] ^= 1
     r.unpack()
     dst = np.full(max(dst_bytes, 1), 0xA5, np.uint8)
-    bm, nbad = cpu.unpack(t, C, pay, sums, dst)
+    bm, nbad = cpu.unpack(t, C, pay, sums, dst, oseg)
     torch.cuda.synchronize()
     assert np.array_equal(to_host(r.dst), dst), f"dst {tag}"
     assert r.bad_set() == set(cpu.bitmap_to_set(bm, nc)), f"bad set {tag}"
@@ -88,6 +90,25 @@ def test_bruteforce_multi_tile_ragged():
         C = int(rng.choice([4096, 16384, 65536, 1 << 20]))
         src = W.random_tiny_state(t, sb, rng)
         _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"multi {it} C={C}")
+
+
+@pytest.mark.parametrize("seg", [16, 32, 256, 4096, 1 << 20])
+def test_segment_alignments_match_oracle(seg):
+    """Plans with an explicit payload segment alignment (fr_plan_create_ex):
+    tiny tables and multi-slice tables with ragged tails, bit for bit
+    against the oracle at the same alignment."""
+    rng = np.random.default_rng(500 + seg.bit_length())
+    for it in range(120):
+        t, sb, db = W.random_tiny_table(rng)
+        C = int(rng.choice([16, 32, 64, 256]))
+        src = W.random_tiny_state(t, sb, rng)
+        _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"seg {seg} table {it} C={C}", seg=seg)
+    for it in range(8):
+        t, sb, db = W.random_tiny_table(rng, max_entries=8, max_numel=300_000)
+        C = int(rng.choice([4096, 16384, 65536, 1 << 20]))
+        src = W.random_tiny_state(t, sb, rng)
+        _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"seg {seg} multi {it} C={C}", seg=seg)
+    log(f"segment alignment {seg}")
 
 
 def test_toy_decoder_full_parity():

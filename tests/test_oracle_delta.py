@@ -8,6 +8,7 @@ non-derived chunks; a flipped bit on the wire is flagged at its list
 position; the C oracle equals the pure-Python oracle on random tables and
 lists."""
 import numpy as np
+import pytest
 
 from oracle import cpu, mini
 from paper_2509_03047_amd import workloads as W
@@ -164,18 +165,20 @@ def _stripe_cuts(n, k, rng):
     return list(zip(edges[:-1], edges[1:]))
 
 
-def _chunk_payload_offset(t, C, c):
+def _chunk_payload_offset(t, C, c, seg=cpu.SEGMENT):
     """Full-payload offset of global chunk c (None for a derived chunk)."""
-    _, base, pay, _ = cpu.plan(t, C)
+    _, base, pay, _ = cpu.plan(t, C, seg)
     k = int(np.searchsorted(base, c, side="right") - 1)
     if int(t[k]["derive_from"]) >= 0:
         return None
     return int(pay[k]) + (c - int(base[k])) * C
 
 
-def test_stripes_are_slices_of_the_full_payload():
-    """With C >= 4 KiB every chunk starts on a 4 KiB boundary of the full
-    payload, so the delta payload of a contiguous chunk range (a stripe)
+@pytest.mark.parametrize("seg", [16, 4096])
+def test_stripes_are_slices_of_the_full_payload(seg):
+    """With C >= the segment alignment every chunk starts on a segment
+    boundary of the full payload, so the delta payload of a contiguous chunk
+    range (a stripe)
     is the full payload's bytes from the range's first sent chunk on, and
     its sums are the full sums of the range: stripes packed separately (one
     per donor) and placed at those offsets form a buffer that a whole
@@ -184,45 +187,50 @@ def test_stripes_are_slices_of_the_full_payload():
     cases = []
     for _ in range(20):
         t, sb, db = W.random_tiny_table(rng, max_entries=10, max_numel=60_000)
-        cases.append((t, int(rng.choice([4096, 16384, 65536])), W.random_tiny_state(t, sb, rng), db))
+        cs = [16, 256, 4096, 65536] if seg == 16 else [4096, 16384, 65536]
+        cases.append((t, int(rng.choice(cs)), W.random_tiny_state(t, sb, rng), db))
     w = W.make_workload(0)
     cases.append((w.table, w.chunk_bytes, W.fill_state(w), w.dst_arena_bytes))
     for t, C, src, db in cases:
-        fp, fs = cpu.pack(t, C, src)
+        fp, fs = cpu.pack(t, C, src, seg)
         n = cpu.n_chunks(t, C)
         buf = np.full(fp.size, 0xEE, np.uint8)  # gap bytes never written
         got_sums = np.zeros_like(fs)
         for a, b in _stripe_cuts(n, int(rng.integers(1, 9)), rng):
             ids = np.arange(a, b, dtype=np.uint32)
-            dp, ds = cpu.pack_chunks(t, C, src, ids)
+            dp, ds = cpu.pack_chunks(t, C, src, ids, seg)
             assert np.array_equal(ds, fs[2 * a:2 * b])
             got_sums[2 * a:2 * b] = ds
-            offs = [o for o in (_chunk_payload_offset(t, C, int(c)) for c in ids) if o is not None]
+            offs = [o for o in (_chunk_payload_offset(t, C, int(c), seg) for c in ids) if o is not None]
             if not offs:  # only derived chunks: nothing on the wire
                 assert dp.size == 0
                 continue
             assert np.array_equal(dp, fp[offs[0]:offs[0] + dp.size]), (a, b)
             buf[offs[0]:offs[0] + dp.size] = dp
         ref = np.zeros(max(db, 1), np.uint8)
-        cpu.unpack(t, C, fp, fs, ref)
+        cpu.unpack(t, C, fp, fs, ref, seg)
         dst = np.zeros(max(db, 1), np.uint8)
-        bm, nbad = cpu.unpack(t, C, buf, got_sums, dst)
+        bm, nbad = cpu.unpack(t, C, buf, got_sums, dst, seg)
         assert nbad == 0 and np.array_equal(dst, ref)
 
 
-def test_stripes_below_4k_chunks_are_not_slices():
-    """The slice property needs C >= 4 KiB: with smaller chunks a stripe
-    starting inside an entry is not 4 KiB-aligned in the full payload, so
-    the next entry's segment lands elsewhere (the reading is checked, not
-    assumed)."""
+def test_stripes_below_the_segment_alignment_are_not_slices():
+    """The slice property needs C >= the segment alignment: with 1 KiB chunks
+    and 4 KiB segments a stripe starting inside an entry is not 4 KiB-aligned
+    in the full payload, so the next entry's segment lands elsewhere (the
+    reading is checked, not assumed); with 16-byte segments it holds."""
     t = np.array([(0, 0, 3000, W.F32, -1), (12288, 12288, 3000, W.F32, -1)], dtype=W.TABLE_DTYPE)
     C = 1024
     src = np.arange(24576, dtype=np.uint32).astype(np.uint8)
-    fp, _ = cpu.pack(t, C, src)
     ids = np.arange(1, cpu.n_chunks(t, C), dtype=np.uint32)  # from chunk 1 of entry 0
+    fp, _ = cpu.pack(t, C, src, 4096)
+    dp, _ = cpu.pack_chunks(t, C, src, ids, 4096)
+    off = _chunk_payload_offset(t, C, 1, 4096)
+    assert off == 1024 and not np.array_equal(dp, fp[off:off + dp.size])
+    fp, _ = cpu.pack(t, C, src)
     dp, _ = cpu.pack_chunks(t, C, src, ids)
     off = _chunk_payload_offset(t, C, 1)
-    assert off == 1024 and not np.array_equal(dp, fp[off:off + dp.size])
+    assert off == 1024 and np.array_equal(dp, fp[off:off + dp.size])
 
 
 def _subset_table():

@@ -34,14 +34,17 @@ def toy():
 def test_toy_sizes_closed_form(toy):
     w, src = toy
     # 3,671,296 params; 14 B of state and 12 B of payload per param, the
-    # payload's 3 x 28 sent tensors each starting at a multiple of 4 KiB:
-    # the five 256-element norms (1 KiB per array) leave 3 KiB gaps, except
-    # after the last entry (the final norm's v, ending the payload)
+    # payload's 3 x 28 sent tensors back to back
     assert w.n_params == 3_671_296
     assert w.state_bytes == 14 * w.n_params == w.src_arena_bytes
     nch, base, pay, pb = cpu.plan(w.table, w.chunk_bytes)
-    assert pb == 12 * w.n_params + (5 * 3 - 1) * 3072
+    assert pb == 12 * w.n_params == 44_055_552
     assert int(base[-1]) == 804
+    # with 4 KiB segments each sent tensor starts at a multiple of 4 KiB: the
+    # five 256-element norms (1 KiB per array) leave 3 KiB gaps, except after
+    # the last entry (the final norm's v, ending the payload)
+    nch, base, pay, pb = cpu.plan(w.table, w.chunk_bytes, 4096)
+    assert pb == 12 * w.n_params + (5 * 3 - 1) * 3072
 
 
 def test_toy_round_trip(toy):
@@ -58,17 +61,18 @@ def test_toy_round_trip(toy):
 
 def test_payload_is_concatenation_with_zero_padding():
     rng = np.random.default_rng(21)
-    for _ in range(50):
+    for it in range(60):
+        seg = (16, 128, 4096)[it % 3]
         t, sb, db = W.random_tiny_table(rng)
         src = W.random_tiny_state(t, sb, rng)
-        payload, _ = cpu.pack(t, 64, src)
+        payload, _ = cpu.pack(t, 64, src, seg)
         exp = bytearray()
         for e in t:
             if int(e["derive_from"]) >= 0:
                 continue
             o, n = int(e["src_offset"]), _nbytes(e)
-            if n:  # each non-empty segment at a 4 KiB boundary
-                exp += bytes(-len(exp) % 4096)
+            if n:  # each non-empty segment at a multiple of seg
+                exp += bytes(-len(exp) % seg)
                 exp += src[o:o + n].tobytes()
         exp += bytes(-len(exp) % 16)
         assert payload.tobytes() == bytes(exp)

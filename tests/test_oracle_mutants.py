@@ -106,24 +106,31 @@ def layout_pins(m):
     failed = []
     w = W.make_workload(0)  # table only: its closed forms need no state
     _, base, _, pb = m.plan(w.table, w.chunk_bytes)
-    if pb != 12 * w.n_params + (5 * 3 - 1) * 3072 or base[-1] != 804:
+    if pb != 12 * w.n_params or base[-1] != 804:
         failed.append("toy closed form")
+    # 4 KiB segments: 14 gaps of 3 KiB after the 1 KiB norm arrays
+    _, base, _, pb = m.plan(w.table, w.chunk_bytes, 4096)
+    if pb != 12 * w.n_params + (5 * 3 - 1) * 3072 or base[-1] != 804:
+        failed.append("toy closed form, 4 KiB segments")
     rng = np.random.default_rng(21)
-    for _ in range(20):
-        t, sb, db = W.random_tiny_table(rng)
-        src = W.random_tiny_state(t, sb, rng).tobytes()
-        payload, _ = m.pack(t, 64, src)
-        exp = bytearray()
-        for e in t:
-            if int(e["derive_from"]) >= 0:
-                continue
-            o, n = int(e["src_offset"]), int(e["numel"]) * W.ESIZE[int(e["dtype"])]
-            if n:
-                exp += bytes(-len(exp) % 4096)
-                exp += src[o:o + n]
-        exp += bytes(-len(exp) % 16)
-        if bytes(payload) != bytes(exp):
-            failed.append("concatenation")
+    for seg in (16, 256, 4096):
+        for _ in range(20):
+            t, sb, db = W.random_tiny_table(rng)
+            src = W.random_tiny_state(t, sb, rng).tobytes()
+            payload, _ = m.pack(t, 64, src, seg)
+            exp = bytearray()
+            for e in t:
+                if int(e["derive_from"]) >= 0:
+                    continue
+                o, n = int(e["src_offset"]), int(e["numel"]) * W.ESIZE[int(e["dtype"])]
+                if n:
+                    exp += bytes(-len(exp) % seg)
+                    exp += src[o:o + n]
+            exp += bytes(-len(exp) % 16)
+            if bytes(payload) != bytes(exp):
+                failed.append("concatenation")
+                break
+        if "concatenation" in failed:
             break
     t, nb = W.state_table([("a", 40), ("b", 3), ("c", 17)])
     src = W.random_tiny_state(t, nb, np.random.default_rng(23)).tobytes()
@@ -190,15 +197,18 @@ RNE_MUTANTS = {
 }
 
 
-def _mutant_segment_16(m):
-    m.SEGMENT = 16
+def _mutant_segment_fixed(a):
+    def mutate(m):
+        orig = m.plan
+        m.plan = lambda table, C, seg=16: orig(table, C, a)
+    return mutate
 
 
 def _mutant_floor_chunks(m):
     orig = m.plan
 
-    def plan(table, C):
-        nch, base, pay, pb = orig(table, C)
+    def plan(table, C, seg=16):
+        nch, base, pay, pb = orig(table, C, seg)
         nch = [int(e["numel"]) * m._esize(int(e["dtype"])) // C for e in table]
         base = [0]
         for x in nch:
@@ -208,14 +218,14 @@ def _mutant_floor_chunks(m):
 
 
 def _mutant_derived_sent(m):
-    def plan(table, C):
+    def plan(table, C, seg=16):
         nch, base, pay = [], [0], []
         end = 0
         for e in table:
             nb = int(e["numel"]) * m._esize(int(e["dtype"]))
             nch.append(-(-nb // C))
             base.append(base[-1] + nch[-1])
-            pay.append(m._up(end, m.SEGMENT) if nb else m._up(end, 16))
+            pay.append(m._up(end, seg) if nb else m._up(end, 16))
             end = pay[-1] + nb if nb else end
         return nch, base, pay, m._up(end, 16)
     m.plan = plan
@@ -224,10 +234,10 @@ def _mutant_derived_sent(m):
 def _mutant_dirty_padding(m):
     orig = m.pack
 
-    def pack(table, C, src):
-        payload, sums = orig(table, C, src)
+    def pack(table, C, src, seg=16):
+        payload, sums = orig(table, C, src, seg)
         p = bytearray(payload)
-        _, _, pay, _ = m.plan(table, C)
+        _, _, pay, _ = m.plan(table, C, seg)
         used = bytearray(len(p))
         for k, e in enumerate(table):
             if pay[k] is not None:
@@ -243,8 +253,8 @@ def _mutant_dirty_padding(m):
 def _mutant_unrounded_end(m):
     orig = m.plan
 
-    def plan(table, C):
-        nch, base, pay, pb = orig(table, C)
+    def plan(table, C, seg=16):
+        nch, base, pay, pb = orig(table, C, seg)
         end = max([p + int(e["numel"]) * m._esize(int(e["dtype"]))
                    for p, e in zip(pay, table) if p is not None] + [0])
         return nch, base, pay, end
@@ -256,7 +266,8 @@ def _mutant_truncating_rederive(m):
 
 
 LAYOUT_MUTANTS = {
-    "segments on 16-byte boundaries": _mutant_segment_16,
+    "segments always on 4 KiB boundaries": _mutant_segment_fixed(4096),
+    "segment alignment ignored (always 16)": _mutant_segment_fixed(16),
     "chunk count rounded down": _mutant_floor_chunks,
     "derived entries sent": _mutant_derived_sent,
     "padding not zeroed": _mutant_dirty_padding,
@@ -296,16 +307,27 @@ def delta_pins(m):
     """Names of the delta-repair pins that module `m` fails."""
     failed = []
     rng = np.random.default_rng(61)
-    for _ in range(30):
+    for it in range(60):
         t, sb, db = W.random_tiny_table(rng, max_numel=120)
         C = int(rng.choice([16, 32, 64]))
+        seg = (16, 64, 4096)[it % 3]
         src = W.random_tiny_state(t, sb, rng).tobytes()
         n = len(m._chunk_map(t, C))
-        fp, fs = m.pack(t, C, src)
-        dp, ds = m.pack_chunks(t, C, src, list(range(n)))
+        fp, fs = m.pack(t, C, src, seg)
+        dp, ds = m.pack_chunks(t, C, src, list(range(n)), seg)
         if dp != fp or [tuple(x) for x in ds] != [tuple(x) for x in fs]:
             failed.append("full list is the full pack")
             break
+    # a list with gaps, worked by hand (16-byte chunks, 64-byte segments):
+    # chunk 0 at 0; chunks 2-3 (a run) at 64; chunk 9 at 128; chunk 10 (the
+    # next entry's first) at 192; payload 208 bytes
+    t = np.array([(0, 0, 40, W.F32, -1), (160, 160, 8, W.F32, -1)], dtype=W.TABLE_DTYPE)
+    src = bytes(range(192))
+    pay, _ = m.pack_chunks(t, 16, src, [0, 2, 3, 9, 10], 64)
+    exp = (src[0:16] + bytes(48) + src[32:64] + bytes(32) + src[144:160] + bytes(48)
+           + src[160:176])
+    if pay != exp:
+        failed.append("runs start segments")
     # repair of a replica whose master, its bf16 image and a moment diverged
     t, nb = W.state_table([("a", 40), ("b", 3), ("c", 17)])
     donor = W.random_tiny_state(t, nb, np.random.default_rng(23)).tobytes()
@@ -325,7 +347,7 @@ def delta_pins(m):
 
 
 def _delta_offsets_with(m, rule):
-    def offsets(table, C, ids):
+    def offsets(table, C, ids, seg=16):
         cmap = m._chunk_map(table, C)
         offs, end, prev = [], 0, None
         for c in ids:
@@ -334,7 +356,7 @@ def _delta_offsets_with(m, rule):
                 offs.append(None)
                 continue
             _, ln = m._chunk_bytes(table, C, k, j, None, "src_offset")
-            offs.append(rule(end, prev == (k, j - 1)))
+            offs.append(rule(end, prev == (k, j - 1), seg))
             end = offs[-1] + ln
             prev = (k, j)
         return offs, m._up(end, 16)
@@ -342,9 +364,9 @@ def _delta_offsets_with(m, rule):
 
 
 def _unpack_chunks_with(m, derive_first=False, master_index=2):
-    def unpack_chunks(table, C, payload, sums, ids, dst):
+    def unpack_chunks(table, C, payload, sums, ids, dst, seg=16):
         cmap = m._chunk_map(table, C)
-        offs, _ = m._delta_offsets(table, C, ids)
+        offs, _ = m._delta_offsets(table, C, ids, seg)
 
         def sent():
             for c, off in zip(ids, offs):
@@ -376,8 +398,11 @@ def _unpack_chunks_with(m, derive_first=False, master_index=2):
 
 
 DELTA_MUTANTS = {
-    "every chunk on a new segment": lambda m: _delta_offsets_with(m, lambda end, cont: m._up(end, m.SEGMENT)),
-    "no segment boundaries": lambda m: _delta_offsets_with(m, lambda end, cont: end),
+    "every chunk on a new segment": lambda m: _delta_offsets_with(
+        m, lambda end, cont, seg: m._up(end, seg)),
+    "no segment boundaries": lambda m: _delta_offsets_with(m, lambda end, cont, seg: end),
+    "segments on 16-byte boundaries whatever the alignment": lambda m: _delta_offsets_with(
+        m, lambda end, cont, seg: end if cont else m._up(end, 16)),
     "parameters re-derived before the masters land": lambda m: _unpack_chunks_with(m, derive_first=True),
     "parameter chunk j read from master chunk j": lambda m: _unpack_chunks_with(m, master_index=1),
 }

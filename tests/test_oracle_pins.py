@@ -188,14 +188,16 @@ def test_rne_mini_agrees_on_random_patterns():
         assert mini.rne_bf16(int(x)) == int(g)
 
 
-def test_pack_worked_example(golden_dir):
-    """A three-entry pack worked by hand (tests/golden/pack_worked.txt):
-    payload bytes, segment placement, zero gaps and every chunk's sums, for
-    both oracles; the restore of it reproduces the arena."""
+@pytest.mark.parametrize("name", ["pack_worked.txt", "pack_worked_packed.txt"])
+def test_pack_worked_example(golden_dir, name):
+    """A three-entry pack worked by hand (tests/golden/pack_worked*.txt, with
+    4 KiB and 16-byte payload segments): payload bytes, segment placement,
+    zero gaps and every chunk's sums, for both oracles; the restore of it
+    reproduces the arena."""
     from paper_2509_03047_amd import workloads as W
 
-    rows, src, segs, sums, C, ab, pb, deltas = [], {}, {}, [], 0, 0, 0, []
-    with open(os.path.join(golden_dir, "pack_worked.txt")) as f:
+    rows, src, segs, sums, C, ab, pb, deltas, seg = [], {}, {}, [], 0, 0, 0, [], 0
+    with open(os.path.join(golden_dir, name)) as f:
         for line in f:
             p = line.split()
             if not p or p[0].startswith("#"):
@@ -204,6 +206,8 @@ def test_pack_worked_example(golden_dir):
                 rows.append(tuple(int(x) for x in p[1:]))
             elif p[0] == "chunk_bytes":
                 C = int(p[1])
+            elif p[0] == "segment_align":
+                seg = int(p[1])
             elif p[0] == "arena_bytes":
                 ab = int(p[1])
             elif p[0] == "src":
@@ -224,22 +228,23 @@ def test_pack_worked_example(golden_dir):
     expect = np.zeros(pb, np.uint8)
     for o, b in segs.items():
         expect[o:o + len(b)] = np.frombuffer(b, np.uint8)
-    pay, s = cpu.pack(t, C, arena)
+    assert seg in (16, 4096)
+    pay, s = cpu.pack(t, C, arena, seg)
     assert np.array_equal(pay, expect) and [int(x) for x in s] == sums
-    mp, ms = mini.pack(t, C, arena.tobytes())
+    mp, ms = mini.pack(t, C, arena.tobytes(), seg)
     assert mp == expect.tobytes() and [x for pair in ms for x in pair] == sums
     dst = np.zeros(ab, np.uint8)
-    bm, nbad = cpu.unpack(t, C, pay, s, dst)
+    bm, nbad = cpu.unpack(t, C, pay, s, dst, seg)
     assert nbad == 0 and np.array_equal(dst, arena)
     # delta lists: offsets, sizes, and the bytes at those offsets
     assert len(deltas) == 4
     for ids, offs, size in deltas:
         ia = np.array(ids, np.uint32)
-        off, got_size = cpu.delta_layout(t, C, ia)
+        off, got_size = cpu.delta_layout(t, C, ia, seg)
         assert got_size == size and [None if o == cpu.NO_PAYLOAD else int(o) for o in off] == offs
-        dp, ds = cpu.pack_chunks(t, C, arena, ia)
+        dp, ds = cpu.pack_chunks(t, C, arena, ia, seg)
         assert dp.size == size and [int(x) for x in ds] == [v for c in ids for v in sums[2 * c:2 * c + 2]]
-        _, base, _, _ = cpu.plan(t, C)
+        _, base, _, _ = cpu.plan(t, C, seg)
         for c, o in zip(ids, offs):
             if o is None:
                 continue

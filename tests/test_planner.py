@@ -67,12 +67,15 @@ def test_state_tables(tp, pp, dp, shard, stage):
             assert len(t) == 4 * len(numel)
             assert info["state_bytes"] == 14 * sum(numel)
             # master, m and v of every tensor are sent, each segment at a
-            # 4 KiB boundary, the payload ending 16-aligned
-            end = 0
-            for n in numel:
-                for _ in range(3):
-                    end = -(-end // 4096) * 4096 + 4 * n
-            assert info["payload_bytes"] == -(-end // 16) * 16
+            # 16-byte boundary (4 KiB with 4 KiB segments), the payload
+            # ending 16-aligned
+            for seg in (16, 4096):
+                end = 0
+                for n in numel:
+                    for _ in range(3):
+                        end = -(-end // seg) * seg + 4 * n
+                got = F.fr_layout_query(t, 256, ab, ab, seg)[0]["payload_bytes"]
+                assert got == -(-end // 16) * 16
         else:
             lo, hi, npad = planner.shard_range(numel, shard, s)
             e = hi - lo
