@@ -155,10 +155,11 @@ typedef struct fr_plan_info {
  * 0-10 (threads x 16-byte vectors per workgroup: 256x1, 512x1, 256x2,
  * 256x4, 64x4, 128x2, 64x2, 64x1, 128x1, 128x4, 64x8; defaults pack 64x4,
  * unpack and compare 128x2, checksum 256x4), FLASHRESTORE_LINE (every
- * operation) or FLASHRESTORE_LINE_PACK / _VERIFY / _CHECKSUM = 1 or 0 turn
- * line-aligned slices on or off (each workgroup's share of a chunk cut at
- * 128-byte lines of the arena read, for tensors placed inside lines;
- * default: on for the compare only), FLASHRESTORE_MAX_GRID caps the
+ * operation) or FLASHRESTORE_LINE_PACK / _VERIFY / _CHECKSUM choose
+ * line-aligned slices (each workgroup's share of a chunk cut at 128-byte
+ * lines, for data placed inside lines): 0 off, 1 at lines of the arena
+ * read, 2 (pack only; 1 elsewhere) at lines of the payload written;
+ * defaults pack 2, compare 1, checksum 0.  FLASHRESTORE_MAX_GRID caps the
  * workgroups per launch (0 or unset: one per slice). */
 int fr_plan_create(const fr_tensor_desc* table, uint32_t n_entries, uint64_t chunk_bytes,
                    uint64_t src_arena_bytes, uint64_t dst_arena_bytes, fr_plan** out);

@@ -98,9 +98,9 @@ int launch_result(int hip_rc) {
 // The plan's pack / checksum / compare walk at the slice size of `tile`,
 // line-aligned or not (the plan builds one for each configuration its
 // operations use, so this finds one for the plan's own).
-const SlotTable* src_walk(const fr_plan* plan, int tile, bool line) {
+const SlotTable* src_walk(const fr_plan* plan, int tile, int line) {
   const uint32_t sl = slice_bytes(plan->layout.C, tile);
-  const uint32_t shift = line_walk(plan, tile, line) ? 1u : 0u;
+  const uint32_t shift = line_walk(plan, tile, line);
   for (const auto& w : plan->src_walks)
     if (w.sl == sl && w.t.shift == shift) return &w.t;
   return nullptr;

@@ -44,7 +44,8 @@ struct alignas(16) SrcUnit {
   uint32_t c;        // its sums slot: global chunk id, or list position for a delta
   uint32_t gap_v;    // zero vectors pack writes after the chunk's 16-byte-padded end
                      //   (the gap up to the next segment; < segment alignment / 16)
-  uint32_t lead;     // src_off mod kLine: how far into a cache line the chunk starts
+  uint16_t lead;     // src_off mod kLine: how far into a cache line the chunk starts
+  uint16_t plead;    // pay_off mod kLine (0 without payload): the same in the payload
 };
 static_assert(sizeof(SrcUnit) == 32, "SrcUnit is 32 bytes");
 
@@ -96,9 +97,11 @@ struct SlotTable {
   uint32_t implicit_shift = 0;
   // Line-aligned walk (SrcUnit walks only): slice j of a chunk covers chunk
   // bytes [j SL - lead, (j + 1) SL - lead), so every cut between slices falls
-  // on a cache-line boundary of the arena read and no line is fetched by two
+  // on a cache-line boundary and no line is fetched or written by two
   // workgroups; a chunk has ceil((lead + len) / SL) slices (one more than a
   // plain walk's when it starts inside a line and ends near a slice end).
+  // shift 1 takes lead from the arena read (SrcUnit::lead), 2 from the
+  // payload written (SrcUnit::plead).
   uint32_t shift = 0;
 };
 
@@ -136,7 +139,9 @@ struct LaunchCfg {
   uint32_t max_grid = 0;  // cap on workgroups per launch (0: hardware limit); grid-stride beyond
   int tile_pack = 0, tile_unpack = 0, tile_verify = 0, tile_checksum = 0;
   // line-aligned walks (SlotTable::shift) per operation
-  bool line_pack = false, line_verify = false, line_checksum = false;
+  // line-aligned walks: 0 off, 1 cut at lines of the arena read, 2 (pack
+  // only) cut at lines of the payload written
+  int line_pack = 0, line_verify = 0, line_checksum = 0;
 };
 
 // Device scratch owned by a plan: per-chunk accumulators (G per chunk, see
@@ -192,10 +197,11 @@ inline uint32_t slice_bytes(uint64_t C, int tile) {
 }
 uint64_t accumulators_per_chunk(uint64_t C, int tile);
 
-// Whether an operation with this tile and line setting walks line-aligned:
-// only when some chunk starts inside a line and a slice spans at least two
-// lines (otherwise the plain walk is the same thing).
-inline bool line_walk(const fr_plan* p, int tile, bool line);
+// The line-aligned mode an operation with this tile and line setting walks
+// in: the setting when some chunk starts inside a line of the side it keys
+// on and a slice spans at least two lines, else 0 (the plain walk is then
+// the same thing).
+inline uint32_t line_walk(const fr_plan* p, int tile, int line);
 
 // Kernel launchers (kernels.hip).  They assume validated arguments, enqueue
 // on `stream` and return the hipError_t of the launches as an int.
@@ -231,10 +237,11 @@ struct fr_plan {
   // their tiles use) and unpack
   struct Walk {
     uint32_t sl = 0;
-    fr::SlotTable t{};  // t.shift: line-aligned
+    fr::SlotTable t{};  // t.shift: the line-aligned mode (0 off, 1 arena lines, 2 payload lines)
     uint64_t* mem = nullptr;
   };
   bool any_lead = false;             // some chunk starts inside a cache line
+  bool any_plead = false;            // some chunk starts inside a payload line
   std::vector<Walk> src_walks;
   Walk unpack_walk;
   fr::DerivedUnit* d_derived = nullptr;  // unpack units: derived groups
@@ -249,6 +256,7 @@ struct fr_plan {
   fr::LaunchCfg cfg{};
 };
 
-inline bool fr::line_walk(const fr_plan* p, int tile, bool line) {
-  return line && p->any_lead && slice_bytes(p->layout.C, tile) >= 2 * kLine;
+inline uint32_t fr::line_walk(const fr_plan* p, int tile, int line) {
+  const bool some = line == 1 ? p->any_lead : line == 2 ? p->any_plead : false;
+  return some && slice_bytes(p->layout.C, tile) >= 2 * kLine ? uint32_t(line) : 0u;
 }

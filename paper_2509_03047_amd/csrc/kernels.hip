@@ -176,8 +176,13 @@ struct Walk {
   uint32_t sl_vec;    // vectors per slice: SL / 16
   uint32_t spc_shift; // log2(SPC), slices per chunk
   uint32_t g_shift;   // log2(G), accumulators per chunk
-  uint32_t line;      // 1: line-aligned walk (SlotTable::shift)
+  uint32_t line;      // line-aligned walk: 1 at arena lines, 2 at payload lines (SlotTable::shift)
 };
+
+// Vectors a line-aligned walk starts a unit's slices early (0 for a plain walk).
+__device__ __forceinline__ uint32_t lead_vectors(const Walk& wk, const SrcUnit& r) {
+  return wk.line == 1 ? uint32_t(r.lead) >> 4 : wk.line == 2 ? uint32_t(r.plead) >> 4 : 0u;
+}
 
 // Slot of workgroup id g: (unit << 32) | j.
 __device__ __forceinline__ u64 slot_of(const Walk& wk, u64 g) {
@@ -215,7 +220,7 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
     // First vector of the slice; a line-aligned walk starts it lead_v
     // vectors early (the first slice's leading lanes then come before the
     // chunk: their unsigned index wraps past nvec and they do nothing).
-    const uint32_t lead_v = wk.line ? r.lead >> 4 : 0u;
+    const uint32_t lead_v = lead_vectors(wk, r);
     const uint32_t v0 = j * wk.sl_vec - lead_v;
     if (j * wk.sl_vec >= endv + lead_v) continue;  // guard: no listed slot is empty
     const u32x4* s = reinterpret_cast<const u32x4*>(src + r.src_off);
@@ -242,7 +247,7 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
       if (store) d[nvec] = t;  // the segment's zero padding is written with it
     }
     // The chunk's last slice zero-fills the gap up to the next payload
-    // segment (fewer than 256 vectors).
+    // segment (fewer than segment alignment / 16 vectors).
     if (store && r.gap_v && (j + 1) * wk.sl_vec >= endv + lead_v) {
       for (uint32_t v = endv + threadIdx.x; v < endv + r.gap_v; v += B)
         st_nt(u32x4{0, 0, 0, 0}, d + v);
@@ -438,7 +443,7 @@ __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units,
     const SrcUnit r = units[e >> 32];
     const uint32_t c = r.c, j = uint32_t(e);
     const uint32_t nvec = r.len >> 4, tail = r.len & 15;
-    const uint32_t lead_v = wk.line ? r.lead >> 4 : 0u;  // as in k_pack
+    const uint32_t lead_v = lead_vectors(wk, r);  // as in k_pack
     const uint32_t v0 = j * wk.sl_vec - lead_v;
     if (j * wk.sl_vec >= nvec + (tail ? 1u : 0u) + lead_v) continue;
     const u32x4* pa = reinterpret_cast<const u32x4*>(a + r.src_off);

@@ -23,7 +23,9 @@ thread_local int g_last_hip_error = 0;
 // 8B and 70B rank shares and the descriptor stress table.
 constexpr uint32_t kDefaultTilePack = 4, kDefaultTileUnpack = 5, kDefaultTileVerify = 5,
                    kDefaultTileChecksum = 3;
-constexpr bool kDefaultLinePack = false, kDefaultLineVerify = true, kDefaultLineChecksum = false;
+// Line-aligned walks (0 off, 1 at lines of the arena read, 2 at lines of the
+// payload written): pack cuts at payload lines, the compare at arena lines.
+constexpr int kDefaultLinePack = 2, kDefaultLineVerify = 1, kDefaultLineChecksum = 0;
 
 static uint64_t esize(uint32_t dtype) { return dtype == FR_F32 ? 4 : 2; }
 static uint64_t align16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
@@ -242,14 +244,16 @@ LaunchCfg launch_config() {
   cfg.tile_unpack = pick("FLASHRESTORE_TILE_UNPACK", kDefaultTileUnpack);
   cfg.tile_verify = pick("FLASHRESTORE_TILE_VERIFY", kDefaultTileVerify);
   cfg.tile_checksum = pick("FLASHRESTORE_TILE_CHECKSUM", kDefaultTileChecksum);
-  // line-aligned walks: 1 on, 0 off (FLASHRESTORE_LINE sets all three)
+  // line-aligned walks: 0 off, 1 arena lines, 2 payload lines (pack only;
+  // elsewhere any nonzero value means 1); FLASHRESTORE_LINE sets all three
   const uint32_t lall = env_u32("FLASHRESTORE_LINE", ~0u);
-  auto lpick = [&](const char* name, bool dflt) {
-    return env_u32(name, lall != ~0u ? lall : uint32_t(dflt)) != 0;
+  auto lpick = [&](const char* name, int dflt, bool payload_side) {
+    const uint32_t v = env_u32(name, lall != ~0u ? lall : uint32_t(dflt));
+    return v == 0 ? 0 : (v == 2 && payload_side) ? 2 : 1;
   };
-  cfg.line_pack = lpick("FLASHRESTORE_LINE_PACK", kDefaultLinePack);
-  cfg.line_verify = lpick("FLASHRESTORE_LINE_VERIFY", kDefaultLineVerify);
-  cfg.line_checksum = lpick("FLASHRESTORE_LINE_CHECKSUM", kDefaultLineChecksum);
+  cfg.line_pack = lpick("FLASHRESTORE_LINE_PACK", kDefaultLinePack, true);
+  cfg.line_verify = lpick("FLASHRESTORE_LINE_VERIFY", kDefaultLineVerify, false);
+  cfg.line_checksum = lpick("FLASHRESTORE_LINE_CHECKSUM", kDefaultLineChecksum, false);
   return cfg;
 }
 
@@ -277,16 +281,18 @@ std::vector<ChunkRec> chunk_records(const fr_tensor_desc* table, uint32_t n, con
 // Pack / checksum / compare units: every chunk, in chunk order.  The last
 // chunk of each sent entry zero-fills the payload gap up to the next one.
 std::vector<SrcUnit> src_units(const std::vector<ChunkRec>& recs, uint32_t n, const Layout& L,
-                               bool* any_lead) {
+                               bool* any_lead, bool* any_plead) {
   std::vector<SrcUnit> units(recs.size());
-  *any_lead = false;
+  *any_lead = *any_plead = false;
   for (uint64_t c = 0; c < recs.size(); c++) {
     units[c].src_off = recs[c].src_off;
     units[c].pay_off = recs[c].pay_off;
     units[c].len = recs[c].len;
     units[c].c = uint32_t(c);
-    units[c].lead = uint32_t(recs[c].src_off % kLine);
+    units[c].lead = uint16_t(recs[c].src_off % kLine);
+    units[c].plead = recs[c].pay_off == kNoPayload ? 0 : uint16_t(recs[c].pay_off % kLine);
     *any_lead = *any_lead || units[c].lead != 0;
+    *any_plead = *any_plead || units[c].plead != 0;
   }
   for (uint32_t k = 0, prev = UINT32_MAX; k < n; k++) {
     if (L.pay_off[k] == kNoPayload || L.chunk_base[k + 1] == L.chunk_base[k]) continue;
@@ -338,12 +344,12 @@ void unpack_units(const fr_tensor_desc* table, uint32_t n, const Layout& L,
 // the plain one when every chunk starts on a line).
 int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units) {
   const Layout& L = p->layout;
-  const std::pair<int, bool> walks[] = {{p->cfg.tile_pack, p->cfg.line_pack},
+  const std::pair<int, int> walks[] = {{p->cfg.tile_pack, p->cfg.line_pack},
                                         {p->cfg.tile_checksum, p->cfg.line_checksum},
                                         {p->cfg.tile_verify, p->cfg.line_verify}};
   for (const auto& tw : walks) {
     const uint32_t sl = slice_bytes(L.C, tw.first);
-    const uint32_t shift = line_walk(p, tw.first, tw.second) ? 1u : 0u;
+    const uint32_t shift = line_walk(p, tw.first, tw.second);
     bool have = false;
     for (const auto& w : p->src_walks) have = have || (w.sl == sl && w.t.shift == shift);
     if (have) continue;
@@ -352,7 +358,7 @@ int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units) {
     b.first.reserve(units.size() + 1);
     b.base.reserve(units.size());
     for (uint64_t c = 0; c < units.size(); c++)
-      b.add(uint32_t(c), units[c].len + (shift ? units[c].lead : 0), 0);
+      b.add(uint32_t(c), units[c].len + (shift == 1 ? units[c].lead : shift == 2 ? units[c].plead : 0), 0);
     p->src_walks.emplace_back();
     const int rc = upload_walk(b, p->src_walks.back());
     p->src_walks.back().t.shift = shift;
@@ -437,7 +443,7 @@ extern "C" int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n, uint64
     unpack_units(table, n, L, recs, is_master, &derived, &plain);
     p->n_derived = uint32_t(derived.size());
     p->n_plain = uint32_t(plain.size());
-    const std::vector<SrcUnit> units = src_units(recs, n, L, &p->any_lead);
+    const std::vector<SrcUnit> units = src_units(recs, n, L, &p->any_lead, &p->any_plead);
 
     rc = upload(units.data(), units.size() * sizeof(SrcUnit), (void**)&p->d_units);
     if (rc == FR_OK) rc = build_src_walks(p, units);

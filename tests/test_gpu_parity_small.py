@@ -337,16 +337,20 @@ def test_every_slice_count_per_tile(tile):
 
 
 @pytest.mark.parametrize("tile", [0, 3, 4, 5, 7, 10])
-def test_line_aligned_walks_match_oracle(tile):
-    """Line-aligned walks (every slice cut at a 128-byte line of the arena
-    read, one more slice for a chunk that starts inside a line) for pack,
-    compare and checksum give the oracle's bytes: random tables at random
-    16-byte offsets, chunks from 16 B (several chunks per line) to 1 MiB,
-    and short chunks of every slice count."""
+@pytest.mark.parametrize("line", ["1", "2"])
+def test_line_aligned_walks_match_oracle(tile, line):
+    """Line-aligned walks (every slice cut at a 128-byte line, one more
+    slice for a chunk that starts inside a line) give the oracle's bytes:
+    line 1 cuts pack, compare and checksum at lines of the arena read, line 2
+    cuts pack at lines of the payload it writes (the compare and checksum at
+    arena lines).  Random tables at random 16-byte offsets (16-byte payload
+    segments, so payload chunks start inside lines too), chunks from 16 B
+    (several chunks per line) to 1 MiB, and short chunks of every slice
+    count."""
     names = ("FLASHRESTORE_TILE", "FLASHRESTORE_LINE", "FLASHRESTORE_MAX_GRID")
     old = {k: os.environ.get(k) for k in names}
-    os.environ["FLASHRESTORE_TILE"], os.environ["FLASHRESTORE_LINE"] = str(tile), "1"
-    rng = np.random.default_rng(700 + tile)
+    os.environ["FLASHRESTORE_TILE"], os.environ["FLASHRESTORE_LINE"] = str(tile), line
+    rng = np.random.default_rng(700 + tile + 50 * int(line))
     try:
         for it in range(40):
             # grid-stride launches too (a capped grid walks several slices per workgroup)
