@@ -137,9 +137,14 @@ __device__ __forceinline__ u64 wave_sum(u64 v) {
 }
 
 // Sum K 64-bit values over the workgroup; thread 0 receives the totals.
-// Several waves combine through LDS; `lds` holds two buffers, and
-// alternating `parity` per slice makes one barrier per slice enough when a
-// workgroup walks several slices.
+// Several waves combine through LDS; `lds` holds two buffers, and callers
+// flip `parity` after every call, so that one barrier per call is enough
+// when a workgroup walks several slices: a wave writes buffer p again only
+// after the barrier of the call in between, which thread 0 passes only once
+// it has read buffer p.  (Flipping per loop iteration instead would break
+// this when an iteration skips its call: two calls in a row would then use
+// the same buffer with no barrier between thread 0's reads and the next
+// writes.)
 template <int B, int K>
 __device__ __forceinline__ void block_sum(u64 (&v)[K], u64 (&lds)[2][B / 64][K], int parity) {
 #pragma unroll
@@ -211,7 +216,7 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
                                             fr_chunk_sum* __restrict__ acc_out) {
   __shared__ u64 lds[2][B / 64][2];
   int parity = 0;
-  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
+  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x) {
     const u64 e = slot_of(wk, g);
     const SrcUnit r = units[e >> 32];
     const uint32_t c = r.c, j = uint32_t(e);
@@ -253,6 +258,7 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
         st_nt(u32x4{0, 0, 0, 0}, d + v);
     }
     block_sum<B, 2>(acc, lds, parity);
+    parity ^= 1;
     if (threadIdx.x == 0) add_sum(acc_out + acc_index(wk, c, j), acc[0], acc[1]);
   }
 }
@@ -373,7 +379,7 @@ __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ de
   __shared__ u64 lds[2][B / 64][4];
   __shared__ u64 lds2[2][B / 64][2];
   int parity = 0;
-  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
+  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x) {
     const u64 e = slot_of(wk, g);
     if (uint32_t(e) & kSlotDerived) {
       const DerivedUnit r = derived[e >> 32];
@@ -382,6 +388,7 @@ __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ de
       uint32_t part = 0;
       if (!derived_slice<B, U, true>(r, j, wk, cvec, payload, dst, acc, part)) continue;
       block_sum<B, 4>(acc, lds, parity);
+      parity ^= 1;
       if (threadIdx.x == 0) {
         const uint32_t jj = j - (part << wk.spc_shift);  // slice within its master chunk
         add_sum(acc_out + ((u64(r.m0 + part) << wk.g_shift) + (jj >> kAccSlicesShift)), acc[0],
@@ -397,6 +404,7 @@ __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ de
       u64 acc[2] = {0, 0};
       if (!plain_slice<B, U>(r, j, wk, payload, dst, acc)) continue;
       block_sum<B, 2>(acc, lds2, parity);
+      parity ^= 1;
       if (threadIdx.x == 0)
         add_sum(acc_out + ((u64(r.c) << wk.g_shift) + (j >> kAccSlicesShift)), acc[0], acc[1]);
     }
@@ -412,7 +420,7 @@ __global__ __launch_bounds__(B) void k_rederive(const DerivedUnit* __restrict__ 
                                                 fr_chunk_sum* __restrict__ acc_out) {
   __shared__ u64 lds[2][B / 64][4];
   int parity = 0;
-  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
+  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x) {
     const u64 e = slot_of(wk, g);
     const DerivedUnit r = derived[e >> 32];
     const uint32_t j = uint32_t(e) & ~kSlotDerived;
@@ -420,6 +428,7 @@ __global__ __launch_bounds__(B) void k_rederive(const DerivedUnit* __restrict__ 
     uint32_t part = 0;
     if (!derived_slice<B, U, false>(r, j, wk, cvec, dst, dst, acc, part)) continue;
     block_sum<B, 4>(acc, lds, parity);
+    parity ^= 1;
     if (threadIdx.x == 0)
       add_sum(acc_out + ((u64(r.c) << wk.g_shift) + (j >> (kAccSlicesShift + 1))), acc[2], acc[3]);
   }
@@ -438,7 +447,7 @@ __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units,
                                               fr_chunk_sum* __restrict__ acc_b) {
   __shared__ u64 lds[2][B / 64][4];
   int parity = 0;
-  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x, parity ^= 1) {
+  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x) {
     const u64 e = slot_of(wk, g);
     const SrcUnit r = units[e >> 32];
     const uint32_t c = r.c, j = uint32_t(e);
@@ -486,6 +495,7 @@ __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units,
     if (__ballot(diff != 0) != 0 && (threadIdx.x & 63) == 0) flags[c] = 1u;
     if (kSums) {
       block_sum<B, 4>(acc, lds, parity);
+      parity ^= 1;
       if (threadIdx.x == 0) {
         const u64 i = acc_index(wk, c, j);
         add_sum(acc_a + i, acc[0], acc[1]);

@@ -107,6 +107,35 @@ def test_delta_every_tile(tile):
             os.environ["FLASHRESTORE_TILE"] = old
 
 
+@pytest.mark.parametrize("tile", [0, 1, 2, 3, 5, 8, 9])
+def test_delta_capped_grid_multiwave_tiles(tile):
+    """Delta calls walk every listed chunk with C / SL workgroup ids, so short
+    chunks leave ids that do nothing; under a capped grid one workgroup then
+    walks working and idle ids in turn.  With more than one wave per
+    workgroup the LDS combine must stay correct across such runs."""
+    names = ("FLASHRESTORE_TILE", "FLASHRESTORE_MAX_GRID")
+    old = {k: os.environ.get(k) for k in names}
+    os.environ["FLASHRESTORE_TILE"] = str(tile)
+    try:
+        rng = np.random.default_rng(180 + tile)
+        for it in range(24):
+            os.environ["FLASHRESTORE_MAX_GRID"] = str(int(rng.choice([1, 2, 3, 7, 64])))
+            t, sb, db = W.random_tiny_table(rng, max_entries=10, max_numel=40_000)
+            C = int(rng.choice([4096, 16384, 65536]))
+            nc = cpu.n_chunks(t, C)
+            ids = np.sort(rng.choice(nc, size=int(rng.integers(0, nc + 1)), replace=False)).astype(np.uint32) \
+                if nc else np.zeros(0, np.uint32)
+            src = W.random_tiny_state(t, sb, rng)
+            recv = rng.integers(0, 256, size=db, dtype=np.uint8)
+            _one(t, C, src, recv, ids, rng, f"tile {tile} grid {os.environ['FLASHRESTORE_MAX_GRID']} table {it}")
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
 def test_listing_every_chunk_equals_the_full_pack():
     w = W.make_workload(0)
     src = to_dev(W.fill_state(w))
