@@ -123,6 +123,42 @@ def verify(table, C, a: bytes, b: bytes):
     return {c for c in ca if ca[c] != cb[c]}
 
 
+def checksum(table, C, arena: bytes):
+    """FRSUM of every chunk of one replica's arena, read at the sender
+    offsets: what a healthy replica would send for each chunk."""
+    return [frsum(b) for _, b in _chunks(table, C, arena, "src_offset")]
+
+
+def verify_with_sums(table, C, a: bytes, b: bytes):
+    """The replica compare together with both arenas' chunk sums."""
+    return verify(table, C, a, b), checksum(table, C, a), checksum(table, C, b)
+
+
+def _entry_of(base, c):
+    """Entry k with base[k] <= c < base[k + 1] (base: prefix of chunk counts,
+    n + 1 values); empty entries (base[k] == base[k + 1]) hold no chunk, so
+    the search takes the last entry whose first chunk is <= c."""
+    lo, hi = 0, len(base) - 1
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        if base[mid] <= c:
+            lo = mid
+        else:
+            hi = mid
+    return lo
+
+
+def checksum_chunks(table, C, arena: bytes, ids):
+    """FRSUM of the listed chunks (global ids, any order) at sender offsets."""
+    _, base, _, _ = plan(table, C)
+    out = []
+    for c in ids:
+        k = _entry_of(base, int(c))
+        o, ln = _chunk_bytes(table, C, k, int(c) - base[k], arena, "src_offset")
+        out.append(frsum(arena[o:o + ln]))
+    return out
+
+
 def _chunk_map(table, C):
     """Global chunk id -> (entry, index within entry)."""
     out = []

@@ -3,7 +3,8 @@
 Each mutant is a fresh copy of the Python oracle (``oracle/mini.py``) with
 one plausible mistake planted in it: a dropped or shifted term, a wrong
 index, a byte order, a modulus, a rounding rule, a layout constant, padding
-left dirty, a delta layout or re-derivation order.  The pins that fix the oracle from outside it (hand-worked
+left dirty, a delta layout or re-derivation order, the side a checksum reads or
+the search that maps a chunk id to its tensor.  The pins that fix the oracle from outside it (hand-worked
 values in tests/golden, closed forms, numpy's modular sums, torch's bf16
 cast, exhaustive detection properties, independently built payloads, the
 restore round trip) must accept the unmodified oracle and reject every
@@ -299,6 +300,83 @@ def test_layout_mutant_is_caught(name):
     m = _fresh_mini(name.replace(" ", "_"))
     LAYOUT_MUTANTS[name](m)
     assert layout_pins(m), name
+
+
+# ------------------------------------------------------ checksum paths
+
+def checksum_pins(m):
+    """Names of the checksum-path pins (one replica's checksum, the replica
+    compare's sums, the checksum of a chunk list) that module `m` fails: the
+    hand-worked scattered table, and the location of single flipped bits on
+    random scattered tables with empty entries, walked in the test."""
+    from tests.test_oracle_checksum import (_chunk_of_byte, _edge_ids, load_checksum_golden,
+                                            with_empty_entries)
+
+    failed = []
+    t, C, a, sums, ids, list_sums, b, diff, sums_b = load_checksum_golden()
+    ab, bb = a.tobytes(), b.tobytes()
+    if m.checksum(t, C, ab) != sums:
+        failed.append("worked checksum")
+    if m.verify_with_sums(t, C, ab, bb) != (diff, sums, sums_b):
+        failed.append("worked compare sums")
+    if m.checksum_chunks(t, C, ab, ids) != list_sums:
+        failed.append("worked chunk list")
+    rng = np.random.default_rng(91)
+    for _ in range(40):
+        t0, sb, db = W.random_tiny_table(rng, max_entries=5, max_numel=120)
+        t = with_empty_entries(t0, sb, db, rng)
+        C = int(rng.choice([16, 32, 64]))
+        x = W.random_tiny_state(t, sb, rng)
+        ref = m.checksum(t, C, x.tobytes())
+        if sb:
+            p = int(rng.integers(0, sb))
+            y = x.copy()
+            y[p] ^= np.uint8(1)
+            got = m.checksum(t, C, y.tobytes())
+            c = _chunk_of_byte(t, C, p)
+            changed = {i for i, (u, v) in enumerate(zip(ref, got)) if u != v}
+            if changed != (set() if c is None else {c}):
+                failed.append("flip location")
+                break
+        edge = _edge_ids(t, C)
+        if m.checksum_chunks(t, C, x.tobytes(), edge) != [ref[i] for i in edge]:
+            failed.append("chunk list next to empty entries")
+            break
+    return failed
+
+
+def _mutant_sums_at_dst(m):
+    m.checksum = lambda table, C, arena: [m.frsum(b) for _, b in m._chunks(table, C, arena, "dst_offset")]
+
+
+def _mutant_search_off_by_one(m):
+    def entry_of(base, c):
+        lo, hi = 0, len(base) - 1
+        while hi - lo > 1:
+            mid = (lo + hi) // 2
+            if base[mid] < c:
+                lo = mid
+            else:
+                hi = mid
+        return lo
+    m._entry_of = entry_of
+
+
+CHECKSUM_MUTANTS = {
+    "sums read at dst offsets": _mutant_sums_at_dst,
+    "chunk search off by one": _mutant_search_off_by_one,
+}
+
+
+def test_checksum_pins_accept_the_oracle():
+    assert checksum_pins(_fresh_mini("checksum_clean")) == []
+
+
+@pytest.mark.parametrize("name", sorted(CHECKSUM_MUTANTS))
+def test_checksum_mutant_is_caught(name):
+    m = _fresh_mini(name.replace(" ", "_"))
+    CHECKSUM_MUTANTS[name](m)
+    assert checksum_pins(m), name
 
 
 # ----------------------------------------------------------- delta repair
