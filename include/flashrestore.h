@@ -80,11 +80,16 @@
 
 #include <stdint.h>
 
+/* hipStream_t.  Like every HIP host header this needs the HIP platform
+ * (hipcc defines it; a plain C or C++ compiler is given
+ * -D__HIP_PLATFORM_AMD__ and the ROCm include directory). */
+#include <hip/hip_runtime_api.h>
+
 #ifdef __cplusplus
 extern "C" {
 #endif
 
-#define FR_ABI_VERSION 3
+#define FR_ABI_VERSION 4
 
 enum fr_dtype { FR_F32 = 1, FR_BF16 = 2 };
 
@@ -136,7 +141,11 @@ typedef struct fr_plan_info {
 
 /* ---------------------------------------------------------------- plans */
 
-/* Validate a tensor table and build a plan on the current HIP device.
+/* Validate a tensor table and build a plan on the current HIP device.  The
+ * table lists the model state a restore copies (Section II: parameters,
+ * optimizer states and the rest of what training needs; Section III-E, its
+ * part on restoring the model states); the plan fixes its chunks and payload
+ * layout for every operation below.
  *   table            n_entries descriptors (host memory; copied)
  *   chunk_bytes      C: a power of two in [16, 2^30]
  *   src_arena_bytes  size of every sender / replica arena the plan will see
@@ -172,19 +181,23 @@ int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n_entries, uint64_t 
                       uint64_t src_arena_bytes, uint64_t dst_arena_bytes, uint64_t segment_align,
                       fr_plan** out);
 
-/* Sizes of a plan.  Host only. */
+/* Sizes of a plan (the buffers a restore of Section III-E needs).  Host only. */
 int fr_plan_get_info(const fr_plan* plan, fr_plan_info* out);
 
-/* Global id of the chunk holding byte `byte_in_entry` of entry `entry`.
- * FR_E_RANGE if the entry or byte does not exist.  Host only. */
+/* Global id of the chunk holding byte `byte_in_entry` of entry `entry`: the
+ * chunk map that turns a flagged chunk back into (tensor, byte range), for a
+ * restore check or replica compare (Sections III-A, III-E).  FR_E_RANGE if the
+ * entry or byte does not exist.  Host only. */
 int fr_plan_chunk_of(const fr_plan* plan, uint32_t entry, uint64_t byte_in_entry, uint64_t* chunk);
 
 /* Payload offset of entry `entry` (UINT64_MAX for derived entries) and its
- * first chunk id.  Host only. */
+ * first chunk id: where a tensor's bytes travel in a restore (Section III-E),
+ * e.g. to place stripes packed by several donors.  Host only. */
 int fr_plan_entry_layout(const fr_plan* plan, uint32_t entry, uint64_t* payload_offset,
                          uint64_t* first_chunk, uint64_t* n_chunks);
 
-/* Free a plan and its device tables.  NULL is a no-op.  The caller must not
+/* Free a plan and its device tables (the end of the restore set-up of
+ * fr_plan_create, Section III-E).  NULL is a no-op.  The caller must not
  * destroy a plan while work that uses it is still pending on a stream. */
 int fr_plan_destroy(fr_plan* plan);
 
@@ -207,7 +220,7 @@ int fr_layout_query(const fr_tensor_desc* table, uint32_t n_entries, uint64_t ch
  *   sums         device, 16-byte aligned, n_chunks entries
  * src, payload and sums must not overlap (FR_E_OVERLAP). */
 int fr_pack_state(const fr_plan* plan, const void* src_base, void* payload, uint64_t payload_cap,
-                  fr_chunk_sum* sums, void* stream);
+                  fr_chunk_sum* sums, hipStream_t stream);
 
 /* Receiver side of a restore (Section III-E): for each non-derived entry copy
  * its payload segment to dst_base + dst_offset; for each derived entry write
@@ -223,7 +236,7 @@ int fr_pack_state(const fr_plan* plan, const void* src_base, void* payload, uint
  *   n_bad        device, 8-byte aligned, one uint64; zeroed by the call
  * The receiver arena must not overlap any other argument. */
 int fr_unpack_state(const fr_plan* plan, const void* payload, const fr_chunk_sum* sums,
-                    void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad, void* stream);
+                    void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad, hipStream_t stream);
 
 /* Replica-consistency compare (Section III-A: data-parallel replicas must
  * hold the same state): bit c of diff_bitmap is set iff the bytes of chunk c
@@ -233,11 +246,15 @@ int fr_unpack_state(const fr_plan* plan, const void* payload, const fr_chunk_sum
  * is allowed (empty result).  Outputs must not overlap inputs or each other. */
 int fr_verify_replicas(const fr_plan* plan, const void* base_a, const void* base_b,
                        uint32_t* diff_bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
-                       fr_chunk_sum* sums_b, void* stream);
+                       fr_chunk_sum* sums_b, hipStream_t stream);
 
-/* sums[c] <- FRSUM-128 of chunk c of the arena at base (src offsets); equal
- * to the sums fr_pack_state produces for the same bytes. */
-int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums, void* stream);
+/* Checksum of one replica's state (Section III-A: the replicas of a
+ * data-parallel group hold the same state; Section III-E: a restore copies a
+ * replica's state): sums[c] <- FRSUM-128 of chunk c of the arena at base
+ * (src offsets); equal to the sums fr_pack_state produces for the same
+ * bytes, so ranks can compare replicas, or check a restored state, by sums
+ * alone. */
+int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums, hipStream_t stream);
 
 /* --------------------------------------------------------- delta repair */
 
@@ -276,7 +293,7 @@ int fr_delta_layout(const fr_plan* plan, const uint32_t* chunk_ids, uint64_t n_i
  *   sums      device, 16-byte aligned, n_ids entries */
 int fr_pack_chunks(const fr_plan* plan, const void* src_base, const uint32_t* chunk_ids,
                    uint64_t n_ids, void* payload, uint64_t payload_cap, fr_chunk_sum* sums,
-                   void* stream);
+                   hipStream_t stream);
 
 /* Receiver side: write every sent chunk to dst_base; then recompute every
  * listed derived chunk as RNE of the receiver's master bytes (which by then
@@ -292,7 +309,7 @@ int fr_pack_chunks(const fr_plan* plan, const void* src_base, const uint32_t* ch
  *   n_bad          device, 8-byte aligned, one uint64 */
 int fr_unpack_chunks(const fr_plan* plan, const void* payload, uint64_t payload_bytes,
                      const fr_chunk_sum* sums, const uint32_t* chunk_ids, uint64_t n_ids,
-                     void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad, void* stream);
+                     void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad, hipStream_t stream);
 
 /* ------------------------------------------------- step tags and donors */
 

@@ -29,7 +29,7 @@ int device_error(hipError_t e) {
   return FR_E_DEVICE;
 }
 
-int check_device_and_stream(const fr_plan* plan, void* stream) {
+int check_device_and_stream(const fr_plan* plan, hipStream_t stream) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return device_error(e);
@@ -115,7 +115,7 @@ const SlotTable* src_walk(const fr_plan* plan, int tile, int line) {
 }  // namespace
 
 extern "C" int fr_pack_state(const fr_plan* plan, const void* src_base, void* payload,
-                             uint64_t payload_cap, fr_chunk_sum* sums, void* stream) {
+                             uint64_t payload_cap, fr_chunk_sum* sums, hipStream_t stream) {
   if (!plan) return FR_E_INVAL;
   const Layout& L = plan->layout;
   if (payload_cap < L.payload_bytes) return FR_E_RANGE;
@@ -134,7 +134,7 @@ extern "C" int fr_pack_state(const fr_plan* plan, const void* src_base, void* pa
 
 extern "C" int fr_unpack_state(const fr_plan* plan, const void* payload, const fr_chunk_sum* sums,
                                void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad,
-                               void* stream) {
+                               hipStream_t stream) {
   if (!plan || !n_bad) return FR_E_INVAL;
   const Layout& L = plan->layout;
   const uint64_t words = (L.n_chunks + 31) / 32;
@@ -166,7 +166,7 @@ extern "C" int fr_unpack_state(const fr_plan* plan, const void* payload, const f
 
 extern "C" int fr_verify_replicas(const fr_plan* plan, const void* base_a, const void* base_b,
                                   uint32_t* diff_bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
-                                  fr_chunk_sum* sums_b, void* stream) {
+                                  fr_chunk_sum* sums_b, hipStream_t stream) {
   if (!plan || !n_diff) return FR_E_INVAL;
   if ((sums_a == nullptr) != (sums_b == nullptr)) return FR_E_INVAL;
   const Layout& L = plan->layout;
@@ -192,7 +192,7 @@ extern "C" int fr_verify_replicas(const fr_plan* plan, const void* base_a, const
 }
 
 extern "C" int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums,
-                                 void* stream) {
+                                 hipStream_t stream) {
   if (!plan) return FR_E_INVAL;
   const Layout& L = plan->layout;
   FR_TRY(check_device_and_stream(plan, stream));
@@ -304,7 +304,7 @@ SlotTable implicit_walk(uint64_t units, uint64_t C, int tile, bool derived) {
 // The staging vector is pageable memory, and HIP performs an async copy from
 // pageable memory synchronously: the records have left the vector when this
 // returns, so the next delta call may refill or reallocate it at once.
-int upload_records(fr_plan* plan, size_t bytes, void* stream) {
+int upload_records(fr_plan* plan, size_t bytes, hipStream_t stream) {
   if (bytes == 0) return FR_OK;
   hipError_t e = hipMemcpyAsync(plan->d_delta, plan->delta_host.data(), bytes,
                                 hipMemcpyHostToDevice, hipStream_t(stream));
@@ -329,7 +329,7 @@ extern "C" int fr_delta_layout(const fr_plan* plan, const uint32_t* ids, uint64_
 
 extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const uint32_t* ids,
                               uint64_t n_ids, void* payload, uint64_t payload_cap,
-                              fr_chunk_sum* sums, void* stream) {
+                              fr_chunk_sum* sums, hipStream_t stream) {
   if (!cplan) return FR_E_INVAL;
   fr_plan* plan = const_cast<fr_plan*>(cplan);  // the plan's delta staging is mutable state
   FR_TRY(check_list(plan, ids, n_ids));
@@ -382,7 +382,7 @@ extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const 
 extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
                                 uint64_t payload_bytes, const fr_chunk_sum* sums,
                                 const uint32_t* ids, uint64_t n_ids, void* dst_base,
-                                uint32_t* bad_bitmap, uint64_t* n_bad, void* stream) {
+                                uint32_t* bad_bitmap, uint64_t* n_bad, hipStream_t stream) {
   if (!cplan || !n_bad) return FR_E_INVAL;
   fr_plan* plan = const_cast<fr_plan*>(cplan);
   FR_TRY(check_list(plan, ids, n_ids));

@@ -126,7 +126,7 @@ def _load():
         f.argtypes = args
         f.restype = C.c_int
     lib.fr_strerror.restype = C.c_char_p
-    if lib.fr_abi_version() != 3:
+    if lib.fr_abi_version() != 4:
         raise ImportError("libflashrestore ABI version mismatch")
     return lib
 
