@@ -13,9 +13,13 @@ parallel 8 (1,004,015,616 params; bf16 param + fp32 master + fp32 Adam m, v =
 before timing starts.  The plan (descriptor validation and device tables) is
 built once, outside the timed region.
 
-Prints one JSON line: whole-step throughput in state GB/s, per-operation
-times and algorithmic HBM GB/s, a roofline entry for the dominant kernel and
-the CPU oracle's rate on a bounded sample of the same workload.
+Prints one JSON line.  `value` is the restore rate the metric names: state
+bytes over the time of pack + checksum and unpack + verify (the two
+operations of a restore); `step_gbs` is the state over the whole step's
+time.  Also: per-operation times, algorithmic HBM GB/s, fractions of the HBM
+peak and of the copy / read-only ceilings measured in the same process with
+plain streaming kernels, a roofline entry for the dominant kernel, and the
+CPU oracle's rates on a stated sample of the same workload.
 """
 from __future__ import annotations
 
@@ -73,7 +77,9 @@ def parse():
     ap.add_argument("--delta-flips", type=int, default=4096)
     ap.add_argument("--segment-align", type=int, default=None,
                     help="payload segment alignment (default: the library's, 16)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time per baseline")
+    ap.add_argument("--cpu-sample-bytes", type=int, default=4_200_000_000,
+                    help="state bytes of the oracle's sample (a prefix of the table)")
+    ap.add_argument("--no-ceilings", action="store_true", help="skip the copy / read ceiling kernels")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 4 GiB device copy (for counter scaling) and exit")
     return ap.parse_args()
@@ -126,6 +132,61 @@ def copy_calibration():
     return {"bytes_per_copy": 2 * n, "ms": ms, "gbs": 2 * n / ms / 1e6}
 
 
+def ceilings(reps: int = 10, nbytes: int = 4 << 30):
+    """Copy, read-only and write-only rates of plain streaming kernels on
+    this GPU (libfrceil: 16-byte non-temporal accesses, 64-lane workgroups in
+    address order, 1 KiB per workgroup for the copy and 4 KiB for the
+    others): median GB/s over `reps` launches of `nbytes` each (a copy counts
+    its reads and writes), timed with HIP events on the launch stream."""
+    import ctypes
+
+    import torch
+
+    from paper_2509_03047_amd import build as B
+
+    lib = ctypes.CDLL(B.CEIL_LIB)
+    P, u64, u32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32
+    lib.frc_copy.argtypes = [P, P, u64, P]
+    lib.frc_read.argtypes = [P, u64, u32, P, P]
+    lib.frc_write.argtypes = [P, u64, u32, P]
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    b = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(64, dtype=torch.int32, device="cuda")
+    a.fill_(0x5A)
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    # the XOR of 16 words of 0x5A5A5A5A is 0, so 1 never occurs
+    runs = {
+        "copy": (2 * nbytes, lambda: lib.frc_copy(b.data_ptr(), a.data_ptr(), nbytes, sp)),
+        "read": (nbytes, lambda: lib.frc_read(a.data_ptr(), nbytes, 1, sink.data_ptr(), sp)),
+        "write": (nbytes, lambda: lib.frc_write(b.data_ptr(), nbytes, 7, sp)),
+    }
+    out = {}
+    for name, (moved, fn) in runs.items():
+        ts = []
+        for i in range(reps + 3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            rc = fn()
+            e1.record(stream)
+            if rc != 0:
+                raise RuntimeError(f"ceiling kernel {name}: HIP error {rc}")
+            torch.cuda.synchronize()
+            if i >= 3:
+                ts.append(e0.elapsed_time(e1))
+        out[name + "_gbs"] = round(moved / (statistics.median(ts) * 1e-3) / 1e9, 1)
+    if int(sink.abs().sum().item()) != 0:
+        raise RuntimeError("read ceiling: the sink was written")
+    del a, b
+    torch.cuda.empty_cache()
+    out["bytes"] = nbytes
+    return out
+
+
+# the ceiling each operation's traffic mix is measured against
+CEILING_OF = {"pack": "copy", "unpack": "copy", "verify": "read", "checksum": "read"}
+
+
 def _cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -165,15 +226,14 @@ def _oracle_sample(w, src_np, max_bytes: int):
     return sub, int(cum[n_ent - 1]), src, dst, replica, f"first {n_ent} of {len(t)} entries ({what}"
 
 
-def _oracle_steps(sub, C, src, dst, replica, seconds: float, max_reps: int):
-    """Full oracle steps until `seconds` pass: (steps, elapsed, seconds per op)."""
+def _oracle_ops(sub, C, src, dst, replica, reps: int):
+    """`reps` full oracle steps; per operation the median seconds."""
     import numpy as np
 
     from oracle import cpu
 
-    ops = {"pack": 0.0, "unpack": 0.0, "verify": 0.0, "checksum": 0.0}
-    reps, t0 = 0, time.perf_counter()
-    while True:
+    ops = {"pack": [], "unpack": [], "verify": [], "checksum": []}
+    for _ in range(reps):
         a = time.perf_counter()
         pay, sums = cpu.pack(sub, C, src)
         b = time.perf_counter()
@@ -184,46 +244,54 @@ def _oracle_steps(sub, C, src, dst, replica, seconds: float, max_reps: int):
         cs = cpu.checksum(sub, C, replica)
         e = time.perf_counter()
         for k, dt in zip(ops, (b - a, c - b, d - c, e - d)):
-            ops[k] += dt
-        reps += 1
-        if e - t0 >= seconds or reps >= max_reps:
-            break
-    if not (nbad == 0 and nd == 0 and np.array_equal(cs, sums)):
-        raise RuntimeError("the oracle's own restore of the sample is not exact")
-    return reps, time.perf_counter() - t0, ops
+            ops[k].append(dt)
+        if not (nbad == 0 and nd == 0 and np.array_equal(cs, sums)):
+            raise RuntimeError("the oracle's own restore of the sample is not exact")
+    return {k: statistics.median(v) for k, v in ops.items()}
 
 
-def cpu_baseline(w, src_np, seconds: float):
+def cpu_baseline(w, src_np, max_bytes: int = 4_200_000_000, reps: int = 3):
     """The oracle, as it stands, on a prefix of the same workload: the first
     entries of the table (the embedding and the first layers for the
-    model-shaped ones) up to about 2 GB of state, on every host thread; and a
-    smaller prefix (about 256 MB) on one thread.  Rates are state bytes per
-    second: the whole step, and each operation alone."""
+    model-shaped ones) up to about `max_bytes` of state, on every host
+    thread and on one thread.  Each operation's time is the median of
+    `reps` full steps.  `value` is the restore rate in the unit of the
+    benchmark's value: sample state bytes over the median pack plus the
+    median unpack time; `ops_gbs` are state bytes per second of each
+    operation alone."""
     from oracle import cpu
 
     C = w.chunk_bytes
     cores = cpu.threads()
-    sub, state, src, dst, replica, what = _oracle_sample(w, src_np, 2_100_000_000)
-    reps, el, ops = _oracle_steps(sub, C, src, dst, replica, seconds, 100)
-    out = {
-        "value": round(state * reps / el / 1e9, 4),
+    sub, state, src, dst, replica, what = _oracle_sample(w, src_np, max_bytes)
+
+    def rates(med):
+        return {"value": round(state / (med["pack"] + med["unpack"]) / 1e9, 4),
+                "ops_gbs": {k: round(state / v / 1e9, 4) for k, v in med.items()},
+                "ops_s": {k: round(v, 4) for k, v in med.items()}}
+
+    t0 = time.perf_counter()
+    many = rates(_oracle_ops(sub, C, src, dst, replica, reps))
+    cpu.set_threads(1)
+    try:
+        one = rates(_oracle_ops(sub, C, src, dst, replica, reps))
+    finally:
+        cpu.set_threads(cores)
+    pct = 100.0 * state / w.state_bytes
+    return {
+        "value": many["value"],
         "unit": "GB/s",
         "cores": cores,
         "kind": "oracle",
-        "sample": f"{what}, {state} state bytes), {reps} full steps (pack+unpack+verify+checksum) "
-                  f"in {el:.1f} s",
-        "ops_gbs": {k: round(state * reps / v / 1e9, 4) for k, v in ops.items()},
+        "sample": f"{what}, {state} state bytes = {pct:.1f} % of the workload's {w.state_bytes}); "
+                  f"median of {reps} full steps (pack+unpack+verify+checksum) per operation, "
+                  f"value = sample bytes / (pack + unpack); {time.perf_counter() - t0:.1f} s in all",
+        "ops_gbs": many["ops_gbs"],
+        "ops_s": many["ops_s"],
         "cpu_model": _cpu_model(),
+        "one_thread": {"value": one["value"], "unit": "GB/s", "cores": 1, "ops_gbs": one["ops_gbs"],
+                       "ops_s": one["ops_s"], "sample": "the same"},
     }
-    sub1, state1, src1, dst1, rep1, what1 = _oracle_sample(w, src_np, 270_000_000)
-    cpu.set_threads(1)
-    try:
-        r1, el1, _ = _oracle_steps(sub1, C, src1, dst1, rep1, max(1.0, seconds / 4), 20)
-    finally:
-        cpu.set_threads(cores)
-    out["one_thread"] = {"value": round(state1 * r1 / el1 / 1e9, 4), "unit": "GB/s", "cores": 1,
-                         "sample": f"{what1}, {state1} state bytes), {r1} full steps in {el1:.1f} s"}
-    return out
 
 
 def control_plane(reps=21):
@@ -504,7 +572,8 @@ def main():
     ok = ok and (torch.equal(dst, src) if same_layout else restored_equals(w, src, dst))
 
     ms_step = total_ms / args.steps
-    value = info["state_bytes"] / (ms_step * 1e-3) / 1e9
+    restore_ms = per_op["pack"] + per_op["unpack"]
+    value = info["state_bytes"] / (restore_ms * 1e-3) / 1e9  # the metric: pack + unpack
     alg = algorithmic_bytes(info, w.table)
     op_report = {}
     for op in ops:
@@ -512,7 +581,6 @@ def main():
         op_report[op] = {"ms": round(per_op[op], 4), "ms_median": round(statistics.median(op_ms[op]), 4),
                          "ms_min": round(min(op_ms[op]), 4), "alg_bytes": alg[op],
                          "hbm_gbs": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
-    restore_ms = per_op["pack"] + per_op["unpack"]
     dom = max(ops, key=lambda o: per_op[o])
     roof = {"bound": "hbm", "kernel": KERNEL_NAMES[dom], "op": dom,
             "achieved": op_report[dom]["hbm_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -548,7 +616,8 @@ def main():
             "n_chunks": info["n_chunks"],
             "step": "pack+checksum -> unpack+derive+verify -> verify_replicas -> checksum_state",
         },
-        "restore_gbs": round(info["state_bytes"] / (restore_ms * 1e-3) / 1e9, 2),
+        "restore_ms": round(restore_ms, 4),
+        "step_gbs": round(info["state_bytes"] / (ms_step * 1e-3) / 1e9, 2),
         "plan_ms": round(plan_ms, 2),
         "ops": op_report,
         "roofline": roof,
@@ -564,9 +633,16 @@ def main():
         out["replica_compare"] = replica_compare(rplan, rtable, src, replica, stream)
         out["delta_repair"] = delta_repair(rplan, rtable, src, replica, rplan.info, args.delta_flips, stream)
         out["delta_repair"]["full_restore_ms"] = round(restore_ms, 4)
+    if not args.no_ceilings:
+        ceil = ceilings()
+        out["ceilings"] = ceil
+        for op in ops:
+            c = ceil[CEILING_OF[op] + "_gbs"]
+            out["ops"][op]["ceiling"] = CEILING_OF[op]
+            out["ops"][op]["frac_of_ceiling"] = round(out["ops"][op]["hbm_gbs"] / c, 4)
     out["control_plane"] = control_plane()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, src_np, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, src_np, args.cpu_sample_bytes)
     print(json.dumps(out), flush=True)
 
 

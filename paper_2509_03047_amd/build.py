@@ -1,7 +1,9 @@
-"""Build of the gfx950 shared library ``libflashrestore.so`` (in-tree).
+"""Build of the gfx950 shared library ``libflashrestore.so`` (in-tree), and of
+``libfrceil.so``, the plain streaming kernels the benchmark measures the
+chip's copy and read ceilings with (not part of the library).
 
-One hipcc invocation compiles the host sources and the kernels for gfx950
-only.  Packed fp32 instructions are disabled for all device code.
+One hipcc invocation per library compiles the host sources and the kernels
+for gfx950 only.  Packed fp32 instructions are disabled for all device code.
 """
 from __future__ import annotations
 
@@ -13,10 +15,12 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libflashrestore.so")
 SOURCES = ["plan.cpp", "api.cpp", "steptag.cpp", "layout.cpp", "kernels.hip"]
+CEIL_LIB = os.path.join(PKG, "libfrceil.so")
+CEIL_SOURCES = ["ceilings.hip"]
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 
-def hipcc_command(out: str = LIB, extra=()):
+def hipcc_command(out: str = LIB, extra=(), sources=SOURCES):
     return [
         os.path.join(ROCM, "bin", "hipcc"),
         "--offload-arch=gfx950",
@@ -27,7 +31,7 @@ def hipcc_command(out: str = LIB, extra=()):
         "-Wall",
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
         "-I", os.path.join(ROOT, "include"),
-        *[os.path.join(CSRC, s) for s in SOURCES],
+        *[os.path.join(CSRC, s) for s in sources],
         "-o", out,
         f"-Wl,-rpath,{ROCM}/lib",
         *extra,
@@ -35,12 +39,13 @@ def hipcc_command(out: str = LIB, extra=()):
 
 
 def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = hipcc_command(tmp)
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    for lib, sources in ((LIB, SOURCES), (CEIL_LIB, CEIL_SOURCES)):
+        tmp = lib + ".tmp"
+        cmd = hipcc_command(tmp, sources=sources)
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, lib)
     return LIB
 
 

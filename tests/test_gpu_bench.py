@@ -15,7 +15,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("config,extra", [(0, ["--cpu-seconds", "0.5"]), (2, ["--no-cpu-baseline"])])
+@pytest.mark.parametrize("config,extra", [(0, ["--cpu-sample-bytes", "20000000"]), (2, ["--no-cpu-baseline"])])
 def test_bench_json_line(config, extra):
     import torch
 
@@ -33,6 +33,15 @@ def test_bench_json_line(config, extra):
         assert k in d, k
     assert d["n_gpus"] == 1 and d["steps"] == 2 and d["warmup"] == 1 and d["higher_is_better"] is True
     assert d["value"] > 0 and d["config"]["workload"]
+    # value is the restore rate: state bytes over pack + unpack time
+    restore_ms = d["ops"]["pack"]["ms"] + d["ops"]["unpack"]["ms"]
+    assert abs(d["value"] - d["config"]["state_bytes"] / (restore_ms * 1e-3) / 1e9) < 0.01 * d["value"]
+    assert d["step_gbs"] < d["value"]
+    ce = d["ceilings"]
+    assert ce["copy_gbs"] > 0 and ce["read_gbs"] > 0 and ce["write_gbs"] > 0
+    for op, o in d["ops"].items():
+        assert o["ceiling"] in ("copy", "read")
+        assert abs(o["frac_of_ceiling"] - o["hbm_gbs"] / ce[o["ceiling"] + "_gbs"]) < 1e-3
     r = d["roofline"]
     assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
     assert abs(r["frac"] - r["achieved"] / r["peak"]) < 1e-3
@@ -44,3 +53,5 @@ def test_bench_json_line(config, extra):
     if "--no-cpu-baseline" not in extra:
         cb = d["cpu_baseline"]
         assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1 and cb["sample"]
+        assert cb["one_thread"]["cores"] == 1 and cb["one_thread"]["value"] > 0
+        assert set(cb["ops_gbs"]) == {"pack", "unpack", "verify", "checksum"}
