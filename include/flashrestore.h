@@ -248,6 +248,26 @@ int fr_verify_replicas(const fr_plan* plan, const void* base_a, const void* base
                        uint32_t* diff_bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
                        fr_chunk_sum* sums_b, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the replica
+ * compare of fr_verify_replicas, with the same arguments, checks and outputs,
+ * whose per-chunk flags and accumulators live in a static device array of
+ * FR_STATIC_SCRATCH_BYTES that each GPU holds until the process ends, instead
+ * of the plan's scratch.  The call allocates nothing (no hipMalloc, no
+ * hipFree, no allocating library routine; the plan was built before).  Its
+ * need is 4 * n_chunks bytes rounded up to 256, plus, when sums_a / sums_b
+ * are requested, 32 * G * n_chunks bytes for G accumulators per chunk (G = 1
+ * for chunks of up to 16 compare slices, C / (16 * slice bytes) above that);
+ * a plan that needs more gets FR_E_RANGE with nothing enqueued.  Every such
+ * call on one GPU shares that GPU's array, whatever its plan: calls that
+ * overlap in time on one GPU (two streams, two threads) race and give wrong
+ * results, so order them.  Each call clears what it uses first, so the
+ * contents a previous call left do not matter. */
+#define FR_STATIC_SCRATCH_BYTES (32ull << 20)
+int fr_verify_replicas_noalloc(const fr_plan* plan, const void* base_a, const void* base_b,
+                               uint32_t* diff_bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
+                               fr_chunk_sum* sums_b, hipStream_t stream);
+
 /* Checksum of one replica's state (Section III-A: the replicas of a
  * data-parallel group hold the same state; Section III-E: a restore copies a
  * replica's state): sums[c] <- FRSUM-128 of chunk c of the arena at base

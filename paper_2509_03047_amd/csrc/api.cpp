@@ -164,9 +164,13 @@ extern "C" int fr_unpack_state(const fr_plan* plan, const void* payload, const f
   return launch_result(launch_unpack(u, plan->cfg, stream));
 }
 
-extern "C" int fr_verify_replicas(const fr_plan* plan, const void* base_a, const void* base_b,
-                                  uint32_t* diff_bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
-                                  fr_chunk_sum* sums_b, hipStream_t stream) {
+namespace {
+
+// Argument checks of the replica compare (both entry points); on success
+// *walk is the plan's compare walk.
+int verify_checks(const fr_plan* plan, const void* base_a, const void* base_b,
+                  uint32_t* diff_bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
+                  fr_chunk_sum* sums_b, hipStream_t stream, const SlotTable** walk) {
   if (!plan || !n_diff) return FR_E_INVAL;
   if ((sums_a == nullptr) != (sums_b == nullptr)) return FR_E_INVAL;
   const Layout& L = plan->layout;
@@ -184,11 +188,48 @@ extern "C" int fr_verify_replicas(const fr_plan* plan, const void* base_a, const
   const Region outs[] = {{diff_bitmap, words * 4}, {n_diff, 8}, {sums_a, sb}, {sums_b, sb}};
   const Region ins[] = {{base_a, plan->src_arena_bytes}, {base_b, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 4, ins, 2));
-  const SlotTable* walk = src_walk(plan, plan->cfg.tile_verify, plan->cfg.line_verify);
-  if (!walk) return FR_E_INVAL;
+  *walk = src_walk(plan, plan->cfg.tile_verify, plan->cfg.line_verify);
+  return *walk ? FR_OK : FR_E_INVAL;
+}
+
+}  // namespace
+
+extern "C" int fr_verify_replicas(const fr_plan* plan, const void* base_a, const void* base_b,
+                                  uint32_t* diff_bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
+                                  fr_chunk_sum* sums_b, hipStream_t stream) {
+  const SlotTable* walk = nullptr;
+  FR_TRY(verify_checks(plan, base_a, base_b, diff_bitmap, n_diff, sums_a, sums_b, stream, &walk));
+  const Layout& L = plan->layout;
   return launch_result(launch_verify(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, base_a,
                                      base_b, diff_bitmap, n_diff, sums_a, sums_b, plan->scratch,
                                      plan->cfg, stream));
+}
+
+extern "C" int fr_verify_replicas_noalloc(const fr_plan* plan, const void* base_a,
+                                          const void* base_b, uint32_t* diff_bitmap,
+                                          uint64_t* n_diff, fr_chunk_sum* sums_a,
+                                          fr_chunk_sum* sums_b, hipStream_t stream) {
+  const SlotTable* walk = nullptr;
+  FR_TRY(verify_checks(plan, base_a, base_b, diff_bitmap, n_diff, sums_a, sums_b, stream, &walk));
+  const Layout& L = plan->layout;
+  // the same carving of the scratch as the plan's: flags, then the two
+  // accumulator sets (only with sums)
+  const uint64_t flag_bytes = (L.n_chunks * 4 + 255) & ~uint64_t(255);
+  const uint64_t acc_bytes =
+      sums_a ? L.n_chunks * accumulators_per_chunk(L.C, plan->cfg.tile_verify) * sizeof(fr_chunk_sum) : 0;
+  if (flag_bytes > kStaticScratchBytes || 2 * acc_bytes > kStaticScratchBytes - flag_bytes)
+    return FR_E_RANGE;
+  void* base = nullptr;
+  const int e = static_scratch_address(plan->device, &base);  // the plan's device is current
+  if (e != 0) return device_error(hipError_t(e));
+  uint8_t* p = static_cast<uint8_t*>(base);
+  Scratch scr;
+  scr.flags = reinterpret_cast<uint32_t*>(p);
+  scr.acc = reinterpret_cast<fr_chunk_sum*>(p + flag_bytes);
+  scr.acc_b = reinterpret_cast<fr_chunk_sum*>(p + flag_bytes + acc_bytes);
+  return launch_result(launch_verify(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, base_a,
+                                     base_b, diff_bitmap, n_diff, sums_a, sums_b, scr, plan->cfg,
+                                     stream));
 }
 
 extern "C" int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums,

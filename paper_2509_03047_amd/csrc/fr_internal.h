@@ -19,6 +19,9 @@ constexpr uint64_t kDefaultSegmentAlign = 16;
 constexpr uint64_t kMaxSegmentAlign = uint64_t(1) << 20;
 constexpr uint32_t kNoMaster = 0xFFFFFFFFu;
 constexpr uint32_t kLine = 128;  // L2 cache line (bytes)
+// Bytes of the static device array the no-allocation calls use as scratch
+// (kernels.hip); the public limit FR_STATIC_SCRATCH_BYTES.
+constexpr uint64_t kStaticScratchBytes = FR_STATIC_SCRATCH_BYTES;
 
 // One record per global chunk id (host side; the device tables are built
 // from these).
@@ -219,6 +222,10 @@ int launch_verify(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunk
                   const void* a, const void* b, uint32_t* bitmap, uint64_t* n_diff,
                   fr_chunk_sum* sums_a, fr_chunk_sum* sums_b, const Scratch& scr,
                   const LaunchCfg& cfg, void* stream);
+// Device address of the static scratch array (kStaticScratchBytes, 256-byte
+// aligned) on `device`, which must be the current device; resolved on the
+// first call per device.  Returns a hipError_t as an int.
+int static_scratch_address(int device, void** out);
 // Writes the XCD-major image (8 * stride entries, zero past slot n - 1) of
 // the slot table whose runs are first[0 .. n_runs] and base[0 .. n_runs - 1]
 // (device arrays; first[0] = 0, first[n_runs] = n, no empty run).

@@ -37,6 +37,8 @@
 // one run of slots per unit and k_expand_slots writes the table itself.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "fr_internal.h"
 
 namespace fr {
@@ -903,6 +905,32 @@ int launch_verify(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunk
                   const LaunchCfg& cfg, void* stream) {
   FR_DISPATCH(cfg.tile_verify, verify_impl, units, slots, n_chunks, C, a, b, bitmap, n_diff,
               sums_a, sums_b, scr, cfg, hipStream_t(stream));
+}
+
+// ------------------------------------------------------- static scratch
+
+// Device memory for the calls that allocate nothing (fr_verify_replicas_noalloc):
+// their flags and accumulators live here instead of in the plan's scratch.
+// Every GPU the library runs on holds its own copy at its own address until
+// the process ends.  In host code `scratch` names a host-side stand-in, not
+// device memory: host code uses only the address hipGetSymbolAddress returns
+// for the current device, resolved once per device below.
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+int static_scratch_address(int device, void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  if (device < 0 || device >= kMaxDevices) return int(hipErrorInvalidDevice);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));  // current device's copy
+    if (e != hipSuccess) return int(e);
+    addr[device] = p;
+  }
+  *out = addr[device];
+  return 0;
 }
 
 }  // namespace fr

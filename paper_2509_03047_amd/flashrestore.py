@@ -103,6 +103,7 @@ def _load():
         "fr_pack_state": [P, P, P, u64, P, P],
         "fr_unpack_state": [P, P, P, P, P, P, P],
         "fr_verify_replicas": [P, P, P, P, P, P, P, P],
+        "fr_verify_replicas_noalloc": [P, P, P, P, P, P, P, P],
         "fr_checksum_state": [P, P, P, P],
         "fr_delta_layout": [P, P, u64, C.POINTER(u64)],
         "fr_pack_chunks": [P, P, P, u64, P, u64, P, P],
@@ -136,7 +137,7 @@ _lib = _load()
 EXPORTED = (
     "fr_plan_create", "fr_plan_create_ex", "fr_plan_get_info", "fr_plan_chunk_of", "fr_plan_entry_layout",
     "fr_plan_destroy", "fr_layout_query", "fr_pack_state", "fr_unpack_state",
-    "fr_verify_replicas", "fr_checksum_state", "fr_delta_layout", "fr_pack_chunks",
+    "fr_verify_replicas", "fr_verify_replicas_noalloc", "fr_checksum_state", "fr_delta_layout", "fr_pack_chunks",
     "fr_unpack_chunks", "fr_tracker_create", "fr_tracker_destroy", "fr_tracker_heartbeat",
     "fr_tracker_report_failure", "fr_tracker_decide", "fr_tracker_failed_ranks", "fr_tracker_donors",
     "fr_layout_rank_coords", "fr_layout_donors", "fr_layout_state_table",
@@ -311,6 +312,10 @@ class Plan:
     def verify_replicas(self, a, b, bitmap, n_diff, sums_a=None, sums_b=None, stream=None, sync=False):
         return fr_verify_replicas(self, a, b, bitmap, n_diff, sums_a, sums_b, stream, sync)
 
+    def verify_replicas_noalloc(self, a, b, bitmap, n_diff, sums_a=None, sums_b=None, stream=None,
+                                sync=False):
+        return fr_verify_replicas_noalloc(self, a, b, bitmap, n_diff, sums_a, sums_b, stream, sync)
+
     def checksum_state(self, base, sums, stream=None):
         return fr_checksum_state(self, base, sums, stream)
 
@@ -398,6 +403,21 @@ def fr_verify_replicas(plan: Plan, base_a, base_b, diff_bitmap, n_diff, sums_a=N
                                    _dev(diff_bitmap, 4 * i["bitmap_words"], "diff_bitmap"),
                                    _dev(n_diff, 8, "n_diff"), _dev(sums_a, sb, "sums_a"),
                                    _dev(sums_b, sb, "sums_b"), _stream(stream)), "fr_verify_replicas")
+    return _synced_bits(diff_bitmap, i["n_chunks"], stream) if sync else None
+
+
+def fr_verify_replicas_noalloc(plan: Plan, base_a, base_b, diff_bitmap, n_diff, sums_a=None, sums_b=None,
+                               stream=None, sync=False):
+    """fr_verify_replicas with the library's static device scratch instead of
+    the plan's (the call allocates nothing); same arguments and results."""
+    i = plan.info
+    sb = SUM_BYTES * i["n_chunks"]
+    _check(_lib.fr_verify_replicas_noalloc(plan.handle, _dev(base_a, i["src_arena_bytes"], "base_a"),
+                                           _dev(base_b, i["src_arena_bytes"], "base_b"),
+                                           _dev(diff_bitmap, 4 * i["bitmap_words"], "diff_bitmap"),
+                                           _dev(n_diff, 8, "n_diff"), _dev(sums_a, sb, "sums_a"),
+                                           _dev(sums_b, sb, "sums_b"), _stream(stream)),
+           "fr_verify_replicas_noalloc")
     return _synced_bits(diff_bitmap, i["n_chunks"], stream) if sync else None
 
 
