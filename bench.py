@@ -408,47 +408,82 @@ def replica_compare(plan, table, donor, replica, stream, ks=(0, 1, 64, 4096), re
     return out
 
 
-def delta_repair(plan, table, donor, replica, info, k, stream, reps=5):
-    """Repair of a replica that diverged in k random bits of its tensors:
-    compare, read the flagged set back, re-send only those chunks.  `plan`
-    has the donor's layout on both sides (replicas of one group share it).
-    Times the GPU work of the two delta operations (HIP events) and the whole
-    repair on the host clock."""
+def delta_repair(plan, table, donor, replica, k, stream, reps=5):
+    """Repair of a replica that diverged in k random bits of its tensors.
+    Device-resident: compare, then the delta pack and unpack driven by the
+    compare's bitmap (the list and its layout built on the device), all
+    stream-ordered with no host round trip; timed with HIP events (compare,
+    repair) and on the host clock from the compare's launch to the repaired
+    replica.  For comparison, the repair through a host list (the flagged set
+    read back, the list passed to the host-list calls).  `plan` has the
+    donor's layout on both sides (replicas of one group share it)."""
     import numpy as np
     import torch
 
     from paper_2509_03047_amd import flashrestore as F
 
-    idx, xor, _ = flips(table, plan.info["chunk_bytes"], k)
+    idx, xor, expect = flips(table, plan.info["chunk_bytes"], k)
     diff, ndiff = plan.empty_bitmap(), plan.empty_counter()
     bad, nbad = plan.empty_bitmap(), plan.empty_counter()
-    payload = plan.empty_payload()
-    sums = plan.empty_sums()
-    gpu_ms, wall_ms = [], []
+    pay, sums = plan.empty_delta_payload(), plan.empty_sums()
+    counts = torch.empty(2, dtype=torch.int64, device="cuda")
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    cmp_ms, rep_ms, wall_ms, over_ms = [], [], [], []
+    ok = True
     for _ in range(reps):
         replica[idx] = replica[idx] ^ xor  # diverge
+        torch.cuda.synchronize()
+        e0, e1, e2 = ev(), ev(), ev()
+        t0 = time.perf_counter()
+        e0.record(stream)
+        plan.verify_replicas(donor, replica, diff, ndiff, stream=stream)
+        e1.record(stream)
+        plan.pack_flagged(donor, diff, pay, sums, counts, stream=stream)
+        plan.unpack_flagged(pay, sums, diff, replica, bad, nbad, stream=stream, payload_bytes=pay.numel())
+        e2.record(stream)
+        stream.synchronize()
+        wall = (time.perf_counter() - t0) * 1e3
+        cmp_ms.append(e0.elapsed_time(e1))
+        rep_ms.append(e1.elapsed_time(e2))
+        wall_ms.append(wall)
+        over_ms.append(wall - e0.elapsed_time(e1))
+        ok = ok and int(nbad.item()) == 0 and int(ndiff.item()) == len(expect)
+    ok = ok and torch.equal(replica, donor)
+    n_ids, pbytes = (int(x) for x in counts.tolist())
+
+    # the same repair through a host list
+    payload = torch.empty(max(pbytes, 16), dtype=torch.uint8, device="cuda")
+    lsums = plan.empty_sums()
+    list_gpu, list_wall = [], []
+    for _ in range(reps):
+        replica[idx] = replica[idx] ^ xor
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         plan.verify_replicas(donor, replica, diff, ndiff, stream=stream)
         ids = F.bitmap_indices(diff, plan.n_chunks).astype(np.uint32)  # synchronises
-        need = plan.delta_layout(ids)
-        if payload.numel() < need:  # a sparse list of chunks under 4 KiB can outgrow the full payload
-            payload = torch.empty(need, dtype=torch.uint8, device="cuda")
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0, e1 = ev(), ev()
         e0.record(stream)
-        plan.pack_chunks(donor, ids, payload, sums, stream=stream)
-        plan.unpack_chunks(payload, sums, ids, replica, bad, nbad, stream=stream)
+        plan.pack_chunks(donor, ids, payload, lsums, stream=stream)
+        plan.unpack_chunks(payload, lsums, ids, replica, bad, nbad, stream=stream)
         e1.record(stream)
-        torch.cuda.synchronize()
-        wall_ms.append((time.perf_counter() - t0) * 1e3)
-        gpu_ms.append(e0.elapsed_time(e1))
-    ok = int(nbad.item()) == 0 and torch.equal(replica, donor)
+        stream.synchronize()
+        list_wall.append((time.perf_counter() - t0) * 1e3)
+        list_gpu.append(e0.elapsed_time(e1))
+        ok = ok and int(nbad.item()) == 0 and ids.size == n_ids
+    ok = ok and torch.equal(replica, donor)
+    med = lambda v: round(float(np.median(v)), 4)  # noqa: E731
     return {
         "flips": k,
-        "chunks_resent": int(ids.size),
-        "payload_bytes": int(plan.delta_layout(ids)),
-        "gpu_ms_pack_unpack": round(float(np.median(gpu_ms)), 4),
-        "wall_ms_compare_to_repaired": round(float(np.median(wall_ms)), 3),
+        "chunks_resent": n_ids,
+        "payload_bytes": pbytes,
+        "gpu_ms_compare": med(cmp_ms),
+        "gpu_ms_repair": med(rep_ms),
+        "wall_ms_compare_to_repaired": med(wall_ms),
+        "wall_ms_beyond_compare": med(over_ms),
+        "host_list": {"gpu_ms_pack_unpack": med(list_gpu), "wall_ms_compare_to_repaired": med(list_wall)},
         "full_restore_ms": None,
         "ok": bool(ok),
     }
@@ -631,7 +666,7 @@ def main():
             rtable["dst_offset"] = rtable["src_offset"]
             rplan = F.Plan(rtable, w.chunk_bytes, w.src_arena_bytes, w.src_arena_bytes, args.segment_align)
         out["replica_compare"] = replica_compare(rplan, rtable, src, replica, stream)
-        out["delta_repair"] = delta_repair(rplan, rtable, src, replica, rplan.info, args.delta_flips, stream)
+        out["delta_repair"] = delta_repair(rplan, rtable, src, replica, args.delta_flips, stream)
         out["delta_repair"]["full_restore_ms"] = round(restore_ms, 4)
     if not args.no_ceilings:
         ceil = ceilings()

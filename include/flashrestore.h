@@ -69,10 +69,10 @@
  *   concurrently (issue them on one stream, or order the streams), and one
  *   plan must not be used from several host threads at once; use one plan per
  *   concurrent stream.
- *   Graph capture.  The four whole-state operations enqueue kernel launches
- *   only (no memset, no host copy), so a capture of them into a HIP graph
- *   replays the same work.  The delta calls below copy per-call unit records
- *   from the plan's host staging, which the next delta call overwrites: they
+ *   Graph capture.  The four whole-state operations and the flagged delta
+ *   calls enqueue kernel launches only (no memset, no host copy, no
+ *   allocation), so a capture of them into a HIP graph replays the same
+ *   work.  The host-list delta calls copy the list from host memory: they
  *   are not for capture.
  */
 #ifndef FLASHRESTORE_H
@@ -137,6 +137,10 @@ typedef struct fr_plan_info {
   uint64_t state_bytes;     /* sum of nbytes over all entries */
   int64_t device;           /* HIP device the plan is bound to; -1 for a layout query */
   uint64_t segment_align;   /* A: payload segments start at multiples of it */
+  uint64_t delta_payload_max; /* the largest delta payload any list of chunks can
+                                 need: payload_bytes when chunk_bytes >= A, else
+                                 the sent bytes plus A per sent chunk, rounded up
+                                 to 16 */
 } fr_plan_info;
 
 /* ---------------------------------------------------------------- plans */
@@ -294,11 +298,17 @@ int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk_sum* sums,
  * range of chunk ids (a stripe) is fr_pack_state's payload from the range's
  * first sent chunk on, so stripes packed by several donors assemble into one
  * payload.
- * All three take the list on the host.  Pack and unpack copy the list's unit
- * records (32 or 48 bytes per chunk) to a device buffer the plan keeps, on
- * `stream`, before their kernels; a list that needs more room than the
- * buffer has makes the call first synchronise the device and reallocate it
- * (an allocation: such a call cannot be captured into a graph). */
+ * fr_delta_layout, fr_pack_chunks and fr_unpack_chunks take the list on the
+ * host; fr_pack_flagged and fr_unpack_flagged take it as a device bitmap over
+ * the chunk ids (bit c of word c / 32 set: chunk c listed; the list is the
+ * set bits in increasing order), for example fr_verify_replicas's output, so
+ * that a repair needs no host round trip.  Either way the device builds the
+ * list's layout and unit records itself, in memory the plan allocated at
+ * creation: no delta call allocates.  A host list is first copied to the
+ * device on `stream` through pinned staging the plan owns (the call waits
+ * until the previous copy from that staging has completed before refilling
+ * it), so the host-list calls are not for graph capture; the flagged calls
+ * enqueue kernel launches only and may be captured. */
 
 /* Bytes of the delta payload for a list.  Host only.  (With C below A a
  * sparse list can need more than the full payload's payload_bytes, since
@@ -330,6 +340,35 @@ int fr_pack_chunks(const fr_plan* plan, const void* src_base, const uint32_t* ch
 int fr_unpack_chunks(const fr_plan* plan, const void* payload, uint64_t payload_bytes,
                      const fr_chunk_sum* sums, const uint32_t* chunk_ids, uint64_t n_ids,
                      void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad, hipStream_t stream);
+
+/* Donor side of a repair from a device bitmap (the list is its set bits):
+ * payload and sums as fr_pack_chunks for that list; sums[i] for list
+ * position i < the list's length, rows past it untouched.
+ *   flagged   device, 4-byte aligned, bitmap_words words (bits past n_chunks ignored)
+ *   payload   device, 16-byte aligned, payload_cap >= delta_payload_max of the
+ *             plan (fr_plan_get_info; FR_E_RANGE otherwise): the largest
+ *             delta payload any list can need
+ *   sums      device, 16-byte aligned, n_chunks entries
+ *   counts    NULL, or device, 8-byte aligned, two uint64: the list's length
+ *             and its delta payload bytes (what the transfer must carry) */
+int fr_pack_flagged(const fr_plan* plan, const void* src_base, const uint32_t* flagged,
+                    void* payload, uint64_t payload_cap, fr_chunk_sum* sums, uint64_t* counts,
+                    hipStream_t stream);
+
+/* Receiver side of a repair from a device bitmap: as fr_unpack_chunks for
+ * the list of its set bits, with bits of bad_bitmap indexed by list
+ * position; words past the list's end are written as 0.  A listed chunk
+ * whose bytes lie past payload_bytes (the bytes readable at payload; pass
+ * the donor's reported delta payload bytes or more) is neither read nor
+ * written and its bit is set.
+ *   payload     device, 16-byte aligned, payload_bytes long (0 allowed)
+ *   sums        device, 16-byte aligned, n_chunks entries (as packed)
+ *   flagged     device, 4-byte aligned, bitmap_words words: the same set as packed
+ *   bad_bitmap  device, 4-byte aligned, bitmap_words words
+ *   n_bad       device, 8-byte aligned, one uint64 */
+int fr_unpack_flagged(const fr_plan* plan, const void* payload, uint64_t payload_bytes,
+                      const fr_chunk_sum* sums, const uint32_t* flagged, void* dst_base,
+                      uint32_t* bad_bitmap, uint64_t* n_bad, hipStream_t stream);
 
 /* ------------------------------------------------- step tags and donors */
 

@@ -262,94 +262,121 @@ int check_list(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids) {
   return FR_OK;
 }
 
-struct Where {
-  uint32_t entry;
-  uint64_t j;    // chunk index within the entry
-  uint64_t len;  // chunk bytes
-};
-
-// Delta payload layout: the listed chunks of sent entries in list order; a
-// chunk right after the previous sent chunk of its entry follows it (that
-// one is whole, so it ends on a multiple of C), any other starts at the next
-// segment boundary; the payload ends at the last chunk's end rounded up to
-// 16.  Ids are strictly increasing (checked before), so one pass over the
-// entries locates them all.
-struct DeltaList {
-  std::vector<Where> where;   // per list position
-  std::vector<uint64_t> off;  // payload offset per list position (kNoPayload: derived)
-  uint64_t bytes = 0;         // payload bytes
-};
-
-void delta_layout(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids, DeltaList* out) {
+// Bytes of the delta payload of a host list: the listed chunks of sent
+// entries in list order; a chunk right after the previous sent chunk of its
+// entry follows it (that one is whole, so it ends on a multiple of C), any
+// other starts at the next segment boundary; the end rounded up to 16.  Ids
+// are strictly increasing (checked before), so one pass over the entries
+// locates them all.
+uint64_t delta_bytes(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids) {
   const std::vector<uint64_t>& base = plan->layout.chunk_base;
-  const uint64_t C = plan->layout.C;
-  out->where.resize(n_ids);
-  out->off.assign(n_ids, kNoPayload);
-  uint64_t end = 0;
-  bool have_prev = false;
-  Where prev{};
+  const uint64_t C = plan->layout.C, seg = plan->layout.seg;
+  uint64_t end = 0, prev = ~uint64_t(0);  // the previous sent chunk's id
   uint32_t k = 0;
   for (uint64_t i = 0; i < n_ids; i++) {
     while (base[k + 1] <= ids[i]) k++;  // the entry with base[k] <= id < base[k + 1]
     const fr_tensor_desc& d = plan->table[k];
-    const uint64_t nb = d.numel * (d.dtype == FR_F32 ? 4 : 2);
-    const uint64_t j = ids[i] - base[k];
-    const Where w{k, j, std::min<uint64_t>(C, nb - j * C)};
-    out->where[i] = w;
     if (d.derive_from >= 0) continue;
-    const bool follows = have_prev && prev.entry == w.entry && prev.j + 1 == w.j;
-    const uint64_t seg = plan->layout.seg;
+    const uint64_t j = ids[i] - base[k];
+    const uint64_t nb = d.numel * (d.dtype == FR_F32 ? 4 : 2);
+    const bool follows = j > 0 && prev == ids[i] - 1;
     const uint64_t at = follows ? end : (end + seg - 1) & ~(seg - 1);
-    out->off[i] = at;
-    end = at + w.len;
-    prev = w;
-    have_prev = true;
+    end = at + std::min<uint64_t>(C, nb - j * C);
+    prev = ids[i];
   }
-  out->bytes = (end + 15) & ~uint64_t(15);
+  return (end + 15) & ~uint64_t(15);
 }
 
-// Device buffer for a delta call's records and slot tables.  It grows on
-// demand; before the old one is freed, the device is synchronised, since
-// work enqueued by earlier calls (on any stream) may still read it.
-int ensure_delta_buffer(fr_plan* plan, uint64_t need) {
-  if (plan->d_delta && plan->delta_cap >= need) return FR_OK;
-  if (plan->d_delta) {
-    hipError_t e = hipDeviceSynchronize();
-    if (e != hipSuccess) return device_error(e);
-    (void)hipFree(plan->d_delta);
-    plan->d_delta = nullptr;
-    plan->delta_cap = 0;
-  }
-  void* p = nullptr;
-  hipError_t e = hipMalloc(&p, need);
-  if (e != hipSuccess) {
-    (void)hipGetLastError();
-    return e == hipErrorOutOfMemory ? FR_E_NOMEM : device_error(e);
-  }
-  plan->d_delta = p;
-  plan->delta_cap = need;
-  return FR_OK;
-}
-
-// Implicit walk over `units` chunks (derived groups: two chunks' worth of
-// master slices each) at the slice size of `tile`.
-SlotTable implicit_walk(uint64_t units, uint64_t C, int tile, bool derived) {
+// Implicit walk over a list of at most `bound` units whose length the device
+// holds at *count (derived groups: two chunks' worth of master slices each),
+// at the slice size of `tile`.
+SlotTable list_walk(uint64_t bound, const uint64_t* count, uint64_t C, int tile, bool derived) {
   uint32_t sh = 0;
   while ((uint64_t(slice_bytes(C, tile)) << sh) < C) sh++;
   SlotTable t;
   t.implicit_shift = sh + (derived ? 1 : 0);
-  t.n = units << t.implicit_shift;
+  t.n = bound << t.implicit_shift;
+  t.count = count;
   return t;
 }
 
-// The staging vector is pageable memory, and HIP performs an async copy from
-// pageable memory synchronously: the records have left the vector when this
-// returns, so the next delta call may refill or reallocate it at once.
-int upload_records(fr_plan* plan, size_t bytes, hipStream_t stream) {
-  if (bytes == 0) return FR_OK;
-  hipError_t e = hipMemcpyAsync(plan->d_delta, plan->delta_host.data(), bytes,
-                                hipMemcpyHostToDevice, hipStream_t(stream));
-  return e == hipSuccess ? FR_OK : device_error(e);
+// Enqueues the upload of a host list into the plan's device list and its
+// bitmap.  The list goes through the plan's pinned staging; the staging is
+// refilled only after the previous upload from it has completed (an event
+// recorded behind each copy).
+int upload_list(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids, hipStream_t stream) {
+  hipError_t e = hipEventSynchronize(plan->delta_ids_copied);
+  if (e != hipSuccess) return device_error(e);
+  std::memcpy(plan->h_delta_ids, ids, n_ids * sizeof(uint32_t));
+  e = hipMemcpyAsync(plan->d_delta_ids, plan->h_delta_ids, n_ids * sizeof(uint32_t),
+                     hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess) e = hipEventRecord(plan->delta_ids_copied, stream);
+  if (e != hipSuccess) return device_error(e);
+  const uint64_t words = (plan->layout.n_chunks + 31) / 32;
+  return launch_result(launch_ids_to_bits(plan->d_delta_ids, n_ids, plan->d_delta_bits, words, stream));
+}
+
+DeltaBuild delta_build(const fr_plan* plan, const uint32_t* bits, uint64_t* user_counts,
+                       uint64_t payload_limit) {
+  DeltaBuild b{};
+  b.t = plan->delta_tables;
+  b.bits = bits;
+  b.n_chunks = plan->layout.n_chunks;
+  b.agg = plan->d_delta_agg;
+  b.pre = plan->d_delta_pre;
+  b.counts = plan->d_delta_counts;
+  b.user_counts = user_counts;
+  b.src_units = plan->d_delta_src;
+  b.plain = plan->d_delta_plain;
+  b.derived = plan->d_delta_derived;
+  b.bad = plan->scratch.flags;
+  b.payload_limit = payload_limit;
+  return b;
+}
+
+// The device half of a delta pack: build the list's records from `bits`,
+// then pack them (at most `bound` units).
+int pack_list(const fr_plan* plan, const void* src_base, const uint32_t* bits, uint64_t bound,
+              void* payload, uint64_t payload_cap, fr_chunk_sum* sums, uint64_t* user_counts,
+              hipStream_t stream) {
+  FR_TRY(launch_result(launch_delta_build(delta_build(plan, bits, user_counts, payload_cap), true, stream)));
+  const uint64_t C = plan->layout.C;
+  return launch_result(launch_pack(plan->d_delta_src,
+                                   list_walk(bound, plan->d_delta_counts + kDeltaIds, C,
+                                             plan->cfg.tile_pack, false),
+                                   uint32_t(bound), C, src_base, payload, sums, plan->scratch,
+                                   plan->cfg, stream));
+}
+
+// The device half of a delta unpack: build the list's records from `bits`,
+// write the sent chunks, re-derive the listed parameters from the
+// receiver's masters, check every listed chunk (at most `bound`).
+int unpack_list(const fr_plan* plan, const void* payload, uint64_t payload_bytes,
+                const fr_chunk_sum* sums, const uint32_t* bits, uint64_t bound, void* dst_base,
+                uint32_t* bad_bitmap, uint64_t* n_bad, hipStream_t stream) {
+  if (bound) {
+    FR_TRY(launch_result(
+        launch_delta_build(delta_build(plan, bits, nullptr, payload_bytes), false, stream)));
+  }
+  const uint64_t C = plan->layout.C;
+  UnpackDeltaArgs a{};
+  a.plain = plan->d_delta_plain;
+  a.n_plain = 0;
+  a.derived = plan->d_delta_derived;
+  a.n_derived = 0;
+  a.plain_slots = list_walk(bound, plan->d_delta_counts + kDeltaSent, C, plan->cfg.tile_unpack, false);
+  a.derived_slots = list_walk(bound, plan->d_delta_counts + kDeltaDerived, C, plan->cfg.tile_unpack, true);
+  a.n_ids = uint32_t(bound);
+  a.C = C;
+  a.payload = payload;
+  a.sums = sums;
+  a.dst = dst_base;
+  a.bitmap = bad_bitmap;
+  a.n_bad = n_bad;
+  a.scratch = plan->scratch;
+  a.live = plan->d_delta_counts + kDeltaIds;
+  a.bad = plan->scratch.flags;
+  return launch_result(launch_unpack_delta(a, plan->cfg, stream));
 }
 
 }  // namespace
@@ -358,29 +385,16 @@ extern "C" int fr_delta_layout(const fr_plan* plan, const uint32_t* ids, uint64_
                                uint64_t* payload_bytes) {
   if (!plan || !payload_bytes) return FR_E_INVAL;
   FR_TRY(check_list(plan, ids, n_ids));
-  DeltaList dl;
-  try {
-    delta_layout(plan, ids, n_ids, &dl);
-  } catch (const std::bad_alloc&) {
-    return FR_E_NOMEM;
-  }
-  *payload_bytes = dl.bytes;
+  *payload_bytes = delta_bytes(plan, ids, n_ids);
   return FR_OK;
 }
 
-extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const uint32_t* ids,
+extern "C" int fr_pack_chunks(const fr_plan* plan, const void* src_base, const uint32_t* ids,
                               uint64_t n_ids, void* payload, uint64_t payload_cap,
                               fr_chunk_sum* sums, hipStream_t stream) {
-  if (!cplan) return FR_E_INVAL;
-  fr_plan* plan = const_cast<fr_plan*>(cplan);  // the plan's delta staging is mutable state
+  if (!plan) return FR_E_INVAL;
   FR_TRY(check_list(plan, ids, n_ids));
-  DeltaList dl;
-  try {
-    delta_layout(plan, ids, n_ids, &dl);
-  } catch (const std::bad_alloc&) {
-    return FR_E_NOMEM;
-  }
-  const uint64_t pb = dl.bytes;
+  const uint64_t pb = delta_bytes(plan, ids, n_ids);
   if (payload_cap < pb) return FR_E_RANGE;
   FR_TRY(check_device_and_stream(plan, stream));
   FR_TRY(check_buffer(plan, src_base, plan->src_arena_bytes, 16));
@@ -390,50 +404,17 @@ extern "C" int fr_pack_chunks(const fr_plan* cplan, const void* src_base, const 
   const Region ins[] = {{src_base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 2, ins, 1));
   if (n_ids == 0) return FR_OK;
-  const uint64_t C = plan->layout.C;
-  try {
-    plan->delta_host.resize(n_ids * sizeof(SrcUnit));
-  } catch (const std::bad_alloc&) {
-    return FR_E_NOMEM;
-  }
-  SrcUnit* recs = reinterpret_cast<SrcUnit*>(plan->delta_host.data());
-  for (uint64_t i = 0, last_sent = n_ids; i < n_ids; i++) {
-    const Where& w = dl.where[i];
-    SrcUnit& r = recs[i];
-    r = SrcUnit{};
-    r.src_off = plan->table[w.entry].src_offset + w.j * C;
-    r.len = uint32_t(w.len);
-    r.c = uint32_t(i);
-    r.pay_off = dl.off[i];
-    if (dl.off[i] == kNoPayload) continue;
-    if (last_sent < n_ids) {  // the previous sent chunk zero-fills up to this one
-      SrcUnit& p = recs[last_sent];
-      p.gap_v = uint32_t((dl.off[i] - ((p.pay_off + p.len + 15) & ~uint64_t(15))) >> 4);
-    }
-    last_sent = i;
-  }
-  FR_TRY(ensure_delta_buffer(plan, plan->delta_host.size()));
-  FR_TRY(upload_records(plan, plan->delta_host.size(), stream));
-  return launch_result(launch_pack(static_cast<const SrcUnit*>(plan->d_delta),
-                                   implicit_walk(n_ids, C, plan->cfg.tile_pack, false),
-                                   uint32_t(n_ids), C, src_base, payload, sums, plan->scratch,
-                                   plan->cfg, stream));
+  FR_TRY(upload_list(plan, ids, n_ids, stream));
+  return pack_list(plan, src_base, plan->d_delta_bits, n_ids, payload, pb, sums, nullptr, stream);
 }
 
-extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
-                                uint64_t payload_bytes, const fr_chunk_sum* sums,
-                                const uint32_t* ids, uint64_t n_ids, void* dst_base,
-                                uint32_t* bad_bitmap, uint64_t* n_bad, hipStream_t stream) {
-  if (!cplan || !n_bad) return FR_E_INVAL;
-  fr_plan* plan = const_cast<fr_plan*>(cplan);
+extern "C" int fr_unpack_chunks(const fr_plan* plan, const void* payload, uint64_t payload_bytes,
+                                const fr_chunk_sum* sums, const uint32_t* ids, uint64_t n_ids,
+                                void* dst_base, uint32_t* bad_bitmap, uint64_t* n_bad,
+                                hipStream_t stream) {
+  if (!plan || !n_bad) return FR_E_INVAL;
   FR_TRY(check_list(plan, ids, n_ids));
-  DeltaList dl;
-  try {
-    delta_layout(plan, ids, n_ids, &dl);
-  } catch (const std::bad_alloc&) {
-    return FR_E_NOMEM;
-  }
-  const uint64_t pb = dl.bytes;
+  const uint64_t pb = delta_bytes(plan, ids, n_ids);
   if (payload_bytes < pb) return FR_E_RANGE;
   const uint64_t words = (n_ids + 31) / 32;
   FR_TRY(check_device_and_stream(plan, stream));
@@ -445,60 +426,49 @@ extern "C" int fr_unpack_chunks(const fr_plan* cplan, const void* payload,
   const Region outs[] = {{dst_base, plan->dst_arena_bytes}, {bad_bitmap, words * 4}, {n_bad, 8}};
   const Region ins[] = {{payload, pb}, {sums, n_ids * sizeof(fr_chunk_sum)}};
   FR_TRY(check_disjoint(outs, 3, ins, 2));
-  const uint64_t C = plan->layout.C;
-  uint32_t n_plain = 0, n_derived = 0;
-  for (uint64_t i = 0; i < n_ids; i++) (dl.off[i] == kNoPayload ? n_derived : n_plain)++;
-  try {
-    plan->delta_host.resize(n_plain * sizeof(PlainUnit) + n_derived * sizeof(DerivedUnit));
-  } catch (const std::bad_alloc&) {
-    return FR_E_NOMEM;
-  }
-  // device image: [plain units][derived units]
-  PlainUnit* pu = reinterpret_cast<PlainUnit*>(plan->delta_host.data());
-  DerivedUnit* du = reinterpret_cast<DerivedUnit*>(plan->delta_host.data() + n_plain * sizeof(PlainUnit));
-  uint32_t ip = 0, id = 0;
-  for (uint64_t i = 0; i < n_ids; i++) {
-    const Where& w = dl.where[i];
-    const fr_tensor_desc& d = plan->table[w.entry];
-    if (d.derive_from < 0) {
-      PlainUnit& u = pu[ip++];
-      u = PlainUnit{};
-      u.pay_off = dl.off[i];
-      u.dst_off = d.dst_offset + w.j * C;
-      u.len = uint32_t(w.len);
-      u.c = uint32_t(i);
-    } else {
-      const fr_tensor_desc& m = plan->table[d.derive_from];
-      DerivedUnit& u = du[id++];
-      u = DerivedUnit{};
-      u.m_pay_off = m.dst_offset + 2 * w.j * C;  // the receiver's master bytes of this chunk
-      u.m_dst_off = u.m_pay_off;
-      u.p_dst_off = d.dst_offset + w.j * C;
-      u.len = uint32_t(w.len);
-      u.c = uint32_t(i);
-    }
-  }
-  if (n_ids) {
-    FR_TRY(ensure_delta_buffer(plan, plan->delta_host.size()));
-    FR_TRY(upload_records(plan, plan->delta_host.size(), stream));
-  }
-  UnpackDeltaArgs a{};
-  a.plain = static_cast<const PlainUnit*>(plan->d_delta);
-  a.n_plain = n_plain;
-  a.derived = reinterpret_cast<const DerivedUnit*>(static_cast<const uint8_t*>(plan->d_delta) +
-                                                   n_plain * sizeof(PlainUnit));
-  a.n_derived = n_derived;
-  a.plain_slots = implicit_walk(n_plain, C, plan->cfg.tile_unpack, false);
-  a.derived_slots = implicit_walk(n_derived, C, plan->cfg.tile_unpack, true);
-  a.n_ids = uint32_t(n_ids);
-  a.C = C;
-  a.payload = payload;
-  a.sums = sums;
-  a.dst = dst_base;
-  a.bitmap = bad_bitmap;
-  a.n_bad = n_bad;
-  a.scratch = plan->scratch;
-  return launch_result(launch_unpack_delta(a, plan->cfg, stream));
+  if (n_ids) FR_TRY(upload_list(plan, ids, n_ids, stream));
+  return unpack_list(plan, payload, pb, sums, plan->d_delta_bits, n_ids, dst_base, bad_bitmap,
+                     n_bad, stream);
+}
+
+extern "C" int fr_pack_flagged(const fr_plan* plan, const void* src_base, const uint32_t* flagged,
+                               void* payload, uint64_t payload_cap, fr_chunk_sum* sums,
+                               uint64_t* counts, hipStream_t stream) {
+  if (!plan) return FR_E_INVAL;
+  const Layout& L = plan->layout;
+  const uint64_t words = (L.n_chunks + 31) / 32, pmax = L.delta_payload_max;
+  if (payload_cap < pmax) return FR_E_RANGE;
+  FR_TRY(check_device_and_stream(plan, stream));
+  FR_TRY(check_buffer(plan, src_base, plan->src_arena_bytes, 16));
+  FR_TRY(check_buffer(plan, flagged, words * 4, 4));
+  FR_TRY(check_buffer(plan, payload, pmax, 16));
+  FR_TRY(check_buffer(plan, sums, L.n_chunks * sizeof(fr_chunk_sum), 16));
+  if (counts) FR_TRY(check_buffer(plan, counts, 16, 8));
+  const Region outs[] = {{payload, pmax}, {sums, L.n_chunks * sizeof(fr_chunk_sum)}, {counts, counts ? 16u : 0u}};
+  const Region ins[] = {{src_base, plan->src_arena_bytes}, {flagged, words * 4}};
+  FR_TRY(check_disjoint(outs, 3, ins, 2));
+  return pack_list(plan, src_base, flagged, L.n_chunks, payload, pmax, sums, counts, stream);
+}
+
+extern "C" int fr_unpack_flagged(const fr_plan* plan, const void* payload, uint64_t payload_bytes,
+                                 const fr_chunk_sum* sums, const uint32_t* flagged, void* dst_base,
+                                 uint32_t* bad_bitmap, uint64_t* n_bad, hipStream_t stream) {
+  if (!plan || !n_bad) return FR_E_INVAL;
+  const Layout& L = plan->layout;
+  const uint64_t words = (L.n_chunks + 31) / 32;
+  FR_TRY(check_device_and_stream(plan, stream));
+  if (payload_bytes) FR_TRY(check_buffer(plan, payload, payload_bytes, 16));
+  FR_TRY(check_buffer(plan, sums, L.n_chunks * sizeof(fr_chunk_sum), 16));
+  FR_TRY(check_buffer(plan, flagged, words * 4, 4));
+  FR_TRY(check_buffer(plan, dst_base, plan->dst_arena_bytes, 16));
+  FR_TRY(check_buffer(plan, bad_bitmap, words * 4, 4));
+  FR_TRY(check_buffer(plan, n_bad, 8, 8));
+  const Region outs[] = {{dst_base, plan->dst_arena_bytes}, {bad_bitmap, words * 4}, {n_bad, 8}};
+  const Region ins[] = {{payload, payload_bytes}, {sums, L.n_chunks * sizeof(fr_chunk_sum)},
+                        {flagged, words * 4}};
+  FR_TRY(check_disjoint(outs, 3, ins, 3));
+  return unpack_list(plan, payload, payload_bytes, sums, flagged, L.n_chunks, dst_base, bad_bitmap,
+                     n_bad, stream);
 }
 
 extern "C" const char* fr_strerror(int status) {

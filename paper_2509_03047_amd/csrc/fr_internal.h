@@ -106,6 +106,9 @@ struct SlotTable {
   // shift 1 takes lead from the arena read (SrcUnit::lead), 2 from the
   // payload written (SrcUnit::plead).
   uint32_t shift = 0;
+  // Implicit walk over a list built on the device: n covers the longest
+  // list, and only the slots of the first *count units work.
+  const uint64_t* count = nullptr;
 };
 
 // A slot table as runs, built on the host (plan.cpp) and expanded on the
@@ -128,6 +131,8 @@ struct Layout {
   uint64_t n_chunks = 0;
   uint64_t payload_bytes = 0;
   uint64_t state_bytes = 0;
+  uint64_t n_sent_chunks = 0;       // chunks of non-derived entries
+  uint64_t delta_payload_max = 0;   // the largest delta payload any list of chunks can need
   std::vector<uint64_t> pay_off;     // per entry; kNoPayload for derived
   std::vector<uint64_t> chunk_base;  // n_entries + 1
 };
@@ -140,6 +145,7 @@ int validate_and_layout(const fr_tensor_desc* table, uint32_t n, uint64_t C, uin
 // 5 = 128x2, 6 = 64x2, 7 = 64x1, 8 = 128x1, 9 = 128x4, 10 = 64x8.
 struct LaunchCfg {
   uint32_t max_grid = 0;  // cap on workgroups per launch (0: hardware limit); grid-stride beyond
+  uint32_t delta_grid = 0;  // cap on workgroups walking a list built on the device (0: none)
   int tile_pack = 0, tile_unpack = 0, tile_verify = 0, tile_checksum = 0;
   // line-aligned walks (SlotTable::shift) per operation
   // line-aligned walks: 0 off, 1 cut at lines of the arena read, 2 (pack
@@ -189,6 +195,47 @@ struct UnpackDeltaArgs {
   uint32_t* bitmap;
   uint64_t* n_bad;
   Scratch scratch;
+  const uint64_t* live = nullptr;  // list built on the device: its length (n_ids is the bound)
+  const uint32_t* bad = nullptr;   // per list position: 1 = flag it whatever its sums
+};
+
+// Device tables of a plan for lists of chunks built on the device.
+struct DeltaTables {
+  const fr_tensor_desc* desc;   // the tensor table
+  const uint64_t* chunk_base;   // n_entries + 1: prefix of the entries' chunk counts
+  uint32_t n_entries;
+  uint64_t C;
+  uint64_t seg;                 // payload segment alignment A
+};
+
+// Scan element of a delta list: the map x -> x + q (has = 0) or
+// x -> align_A(x + p) + q (has = 1) of the payload end over some chunks,
+// with their counts of sent (ns) and derived (nd) chunks.
+struct DeltaAgg {
+  uint32_t ns, nd, has, pad_;
+  uint64_t p, q;
+};
+// Before a bitmap word: the payload end and the counts.
+struct DeltaPre {
+  uint64_t end;
+  uint32_t ns, nd;
+};
+// Totals of a list built on the device (plan-owned device words).
+enum DeltaCount { kDeltaIds = 0, kDeltaSent = 1, kDeltaDerived = 2, kDeltaEnd = 3 };
+
+struct DeltaBuild {
+  DeltaTables t;
+  const uint32_t* bits;      // the list: bit c set = chunk c listed
+  uint64_t n_chunks;         // the plan's chunks (bits past them are ignored)
+  DeltaAgg* agg;             // per bitmap word
+  DeltaPre* pre;             // per bitmap word
+  uint64_t* counts;          // [kDeltaIds, kDeltaSent, kDeltaDerived, kDeltaEnd]
+  uint64_t* user_counts;     // NULL or the caller's [list length, payload bytes]
+  SrcUnit* src_units;        // pack: one per listed chunk, list order
+  PlainUnit* plain;          // unpack: sent chunks
+  DerivedUnit* derived;      // unpack: derived chunks (re-derived from the receiver's masters)
+  uint32_t* bad;             // unpack: per list position, 1 = beyond the readable payload
+  uint64_t payload_limit;    // pack: payload capacity; unpack: readable payload bytes
 };
 
 // Bytes of one slice for a tile, and the accumulators a chunk of C bytes
@@ -222,6 +269,12 @@ int launch_verify(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunk
                   const void* a, const void* b, uint32_t* bitmap, uint64_t* n_diff,
                   fr_chunk_sum* sums_a, fr_chunk_sum* sums_b, const Scratch& scr,
                   const LaunchCfg& cfg, void* stream);
+// The unit records of a delta list given as a bitmap, built on the device:
+// pack's SrcUnit list, or unpack's plain and derived lists, and the counts.
+int launch_delta_build(const DeltaBuild& b, bool for_pack, void* stream);
+// bits[0 .. words) <- the bitmap of ids[0 .. n) (ids < 32 * words).
+int launch_ids_to_bits(const uint32_t* ids, uint64_t n, uint32_t* bits, uint64_t words,
+                       void* stream);
 // Device address of the static scratch array (kStaticScratchBytes, 256-byte
 // aligned) on `device`, which must be the current device; resolved on the
 // first call per device.  Returns a hipError_t as an int.
@@ -256,9 +309,19 @@ struct fr_plan {
   fr::PlainUnit* d_plain = nullptr;      // unpack units: plain chunks
   uint32_t n_plain = 0;
   void* d_scratch = nullptr;         // one allocation holding `scratch`
-  void* d_delta = nullptr;           // delta unit records, allocated on first use
-  uint64_t delta_cap = 0;            // bytes of d_delta
-  std::vector<uint8_t> delta_host;   // host staging of the unit records
+  // Delta lists, built on the device (one allocation, carved at creation):
+  void* d_delta = nullptr;
+  fr::DeltaTables delta_tables{};     // the table and chunk bases
+  fr::SrcUnit* d_delta_src = nullptr; // pack records; shares its bytes with the two below
+  fr::PlainUnit* d_delta_plain = nullptr;
+  fr::DerivedUnit* d_delta_derived = nullptr;
+  fr::DeltaAgg* d_delta_agg = nullptr;
+  fr::DeltaPre* d_delta_pre = nullptr;
+  uint64_t* d_delta_counts = nullptr;  // fr::DeltaCount
+  uint32_t* d_delta_bits = nullptr;    // bitmap of a host list
+  uint32_t* d_delta_ids = nullptr;     // a host list, uploaded
+  uint32_t* h_delta_ids = nullptr;     // pinned staging of a host list
+  hipEvent_t delta_ids_copied = nullptr;  // the last upload from the staging has completed
   fr::Scratch scratch{};
   fr::LaunchCfg cfg{};
 };

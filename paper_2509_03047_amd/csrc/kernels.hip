@@ -184,7 +184,17 @@ struct Walk {
   uint32_t spc_shift; // log2(SPC), slices per chunk
   uint32_t g_shift;   // log2(G), accumulators per chunk
   uint32_t line;      // line-aligned walk: 1 at arena lines, 2 at payload lines (SlotTable::shift)
+  const u64* count;   // implicit walk of a list built on the device: its number of units
 };
+
+// Workgroup ids a launch covers: every slot of the walk, or for a list
+// built on the device (whose length the host does not know) the slots of
+// its first *count units.
+__device__ __forceinline__ u64 walk_slices(const Walk& wk) {
+  if (!wk.count) return wk.n_slices;
+  const u64 n = *wk.count << wk.imp_shift;
+  return n < wk.n_slices ? n : wk.n_slices;
+}
 
 // Vectors a line-aligned walk starts a unit's slices early (0 for a plain walk).
 __device__ __forceinline__ uint32_t lead_vectors(const Walk& wk, const SrcUnit& r) {
@@ -218,7 +228,8 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
                                             fr_chunk_sum* __restrict__ acc_out) {
   __shared__ u64 lds[2][B / 64][2];
   int parity = 0;
-  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x) {
+  const u64 n_slices = walk_slices(wk);
+  for (u64 g = blockIdx.x; g < n_slices; g += gridDim.x) {
     const u64 e = slot_of(wk, g);
     const SrcUnit r = units[e >> 32];
     const uint32_t c = r.c, j = uint32_t(e);
@@ -381,7 +392,8 @@ __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ de
   __shared__ u64 lds[2][B / 64][4];
   __shared__ u64 lds2[2][B / 64][2];
   int parity = 0;
-  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x) {
+  const u64 n_slices = walk_slices(wk);
+  for (u64 g = blockIdx.x; g < n_slices; g += gridDim.x) {
     const u64 e = slot_of(wk, g);
     if (uint32_t(e) & kSlotDerived) {
       const DerivedUnit r = derived[e >> 32];
@@ -422,7 +434,8 @@ __global__ __launch_bounds__(B) void k_rederive(const DerivedUnit* __restrict__ 
                                                 fr_chunk_sum* __restrict__ acc_out) {
   __shared__ u64 lds[2][B / 64][4];
   int parity = 0;
-  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x) {
+  const u64 n_slices = walk_slices(wk);
+  for (u64 g = blockIdx.x; g < n_slices; g += gridDim.x) {
     const u64 e = slot_of(wk, g);
     const DerivedUnit r = derived[e >> 32];
     const uint32_t j = uint32_t(e) & ~kSlotDerived;
@@ -449,7 +462,8 @@ __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units,
                                               fr_chunk_sum* __restrict__ acc_b) {
   __shared__ u64 lds[2][B / 64][4];
   int parity = 0;
-  for (u64 g = blockIdx.x; g < wk.n_slices; g += gridDim.x) {
+  const u64 n_slices = walk_slices(wk);
+  for (u64 g = blockIdx.x; g < n_slices; g += gridDim.x) {
     const u64 e = slot_of(wk, g);
     const SrcUnit r = units[e >> 32];
     const uint32_t c = r.c, j = uint32_t(e);
@@ -525,13 +539,14 @@ struct FinalArgs {
   const fr_chunk_sum* acc;  // accumulators (A for kFlags)
   const fr_chunk_sum* acc_b;
   const fr_chunk_sum* sent;
-  const uint32_t* flags;
+  const uint32_t* flags;    // kFlags: the compare's flags; kCompare: NULL, or chunks to flag anyway
   fr_chunk_sum* out;  // sums (A for kFlags)
   fr_chunk_sum* out_b;
   uint32_t* bitmap;
   u64* count;
-  uint32_t n_chunks;
+  uint32_t n_chunks;  // bitmap bits written (ceil(n_chunks / 32) words)
   uint32_t g_shift;
+  const u64* live;    // NULL, or a device count: positions from *live on are not chunks (bit 0, no sums)
 };
 
 __device__ __forceinline__ fr_chunk_sum fold(const fr_chunk_sum* acc, u64 c, uint32_t g_shift) {
@@ -552,10 +567,12 @@ __global__ __launch_bounds__(kFinalThreads) void k_finalize(FinalArgs f) {
   const uint32_t lane = threadIdx.x & 63;
   const u64 stride = u64(gridDim.x) * blockDim.x;
   u64 count = 0;  // set bits seen by this wave (uniform)
+  u64 n_live = f.n_chunks;
+  if (f.live && *f.live < n_live) n_live = *f.live;
   for (u64 base = u64(blockIdx.x) * blockDim.x + (threadIdx.x & ~63u); base < f.n_chunks;
        base += stride) {
     const u64 c = base + lane;
-    const bool live = c < f.n_chunks;
+    const bool live = c < n_live;
     bool bit = false;
     if (kMode == kFold) {
       if (live) f.out[c] = fold(f.acc, c, f.g_shift);
@@ -563,7 +580,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_finalize(FinalArgs f) {
     }
     if (kMode == kCompare && live) {
       const fr_chunk_sum got = fold(f.acc, c, f.g_shift);
-      bit = got.sum != f.sent[c].sum || got.wsum != f.sent[c].wsum;
+      bit = got.sum != f.sent[c].sum || got.wsum != f.sent[c].wsum || (f.flags && f.flags[c]);
     }
     if (kMode == kFlags && live) {
       bit = f.flags[c] != 0;
@@ -587,6 +604,231 @@ __global__ __launch_bounds__(kFinalThreads) void k_finalize(FinalArgs f) {
     for (int i = 0; i < kFinalThreads / 64; i++) t += wave_count[i];
     if (t) atomicAdd(f.count, t);
   }
+}
+
+// ----------------------------------------------------------- delta lists
+//
+// A delta call's list of chunks, given as a bitmap over the plan's chunk
+// ids (bit c set: chunk c is listed; list positions follow chunk order),
+// becomes the call's unit records on the device, so a repair from the
+// compare's bitmap needs no host round trip.  In the delta payload a sent
+// chunk that continues the previous sent chunk of its entry follows it, any
+// other starts at the next multiple of the segment alignment A.  Where a
+// chunk lands depends on every chunk before it, but each one acts on the
+// running payload end x as x -> x + len (continuing) or x -> align_A(x) +
+// len, and such maps compose within the family {x -> x + q} u
+// {x -> align_A(x + p) + q}, because align_A(align_A(z) + w) = align_A(z) +
+// align_A(w) for w >= 0.  So:
+//   k_delta_agg   one thread per bitmap word: the composed map of the word's
+//                 sent chunks and its counts of sent and derived chunks;
+//   k_delta_scan  one workgroup: composes the words' maps in order, giving
+//                 each word the payload end and the counts before it, and
+//                 the totals;
+//   k_delta_build one thread per word: places its chunks and writes their
+//                 unit records (pack: one per listed chunk in list order;
+//                 unpack: sent and derived chunks in two lists).
+
+__device__ __forceinline__ u64 align_a(u64 x, u64 a) { return (x + a - 1) & ~(a - 1); }
+
+// g after f.
+__device__ __forceinline__ DeltaAgg delta_then(const DeltaAgg& f, const DeltaAgg& g, u64 A) {
+  DeltaAgg h;
+  h.ns = f.ns + g.ns;
+  h.nd = f.nd + g.nd;
+  h.pad_ = 0;
+  if (!g.has) {
+    h.has = f.has;
+    h.p = f.p;
+    h.q = f.q + g.q;
+  } else if (!f.has) {
+    h.has = 1;
+    h.p = f.q + g.p;
+    h.q = g.q;
+  } else {
+    h.has = 1;
+    h.p = f.p;
+    h.q = align_a(f.q + g.p, A) + g.q;
+  }
+  return h;
+}
+
+__device__ __forceinline__ u64 delta_apply(const DeltaAgg& f, u64 x, u64 A) {
+  return f.has ? align_a(x + f.p, A) + f.q : x + f.q;
+}
+
+// Listed chunks of bitmap word w (bits past the last chunk cleared).
+__device__ __forceinline__ uint32_t listed_bits(const uint32_t* bits, u64 w, u64 n_chunks) {
+  const u64 c0 = w * 32;
+  const uint32_t b = bits[w];
+  return n_chunks - c0 >= 32 ? b : b & ((1u << uint32_t(n_chunks - c0)) - 1u);
+}
+
+__device__ __forceinline__ bool listed(const uint32_t* bits, u64 c, u64 n_chunks) {
+  return c < n_chunks && ((bits[c >> 5] >> (c & 31)) & 1u);
+}
+
+// The entry holding chunk c: the last k with chunk_base[k] <= c (empty
+// entries share their chunk_base with the next one).
+__device__ __forceinline__ uint32_t entry_of_chunk(const DeltaTables& t, u64 c) {
+  uint32_t lo = 0, hi = t.n_entries;  // chunk_base[lo] <= c < chunk_base[hi]
+  while (hi - lo > 1) {
+    const uint32_t mid = lo + (hi - lo) / 2;
+    if (t.chunk_base[mid] <= c) lo = mid;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Chunk c of entry e, as the walk of a word meets it.
+struct ListedChunk {
+  u64 j;         // index within the entry
+  uint32_t len;  // bytes
+  bool derived;  // a bf16 parameter re-derived from its master: sends nothing
+  bool cont;     // sent, and continues the previous listed chunk of its entry
+  bool next_cont;// sent, and the next chunk of its entry is listed (it continues this one)
+};
+
+__device__ __forceinline__ ListedChunk listed_chunk(const DeltaTables& t, const uint32_t* bits,
+                                                    u64 n_chunks, uint32_t e, u64 c) {
+  const fr_tensor_desc& d = t.desc[e];
+  const u64 nb = d.numel * (d.dtype == FR_F32 ? 4u : 2u);
+  ListedChunk k;
+  k.j = c - t.chunk_base[e];
+  const u64 rest = nb - k.j * t.C;
+  k.len = uint32_t(rest < t.C ? rest : t.C);
+  k.derived = d.derive_from >= 0;
+  const u64 nch = t.chunk_base[e + 1] - t.chunk_base[e];
+  k.cont = !k.derived && k.j > 0 && listed(bits, c - 1, n_chunks);
+  k.next_cont = !k.derived && k.j + 1 < nch && listed(bits, c + 1, n_chunks);
+  return k;
+}
+
+// Calls fn(c, e) for the listed chunks of word w in increasing order.
+template <typename Fn>
+__device__ __forceinline__ void for_listed(const DeltaBuild& b, u64 w, Fn fn) {
+  uint32_t m = listed_bits(b.bits, w, b.n_chunks);
+  if (!m) return;
+  uint32_t e = entry_of_chunk(b.t, w * 32 + __builtin_ctz(m));
+  while (m) {
+    const u64 c = w * 32 + __builtin_ctz(m);
+    m &= m - 1;
+    while (b.t.chunk_base[e + 1] <= c) e++;
+    fn(c, e);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_delta_agg(DeltaBuild b, u64 n_words) {
+  const u64 w = u64(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (w >= n_words) return;
+  DeltaAgg a{0, 0, 0, 0, 0, 0};
+  for_listed(b, w, [&](u64 c, uint32_t e) {
+    const ListedChunk k = listed_chunk(b.t, b.bits, b.n_chunks, e, c);
+    if (k.derived) {
+      a.nd++;
+      return;
+    }
+    const DeltaAgg one{1, 0, k.cont ? 0u : 1u, 0, 0, k.len};
+    a = delta_then(a, one, b.t.seg);
+  });
+  b.agg[w] = a;
+}
+
+constexpr int kScanThreads = 1024;
+
+// Thread i composes words [i k, (i + 1) k); an inclusive scan of the
+// threads' maps through LDS gives each thread the map of everything before
+// its words; it then walks its words again with the running payload end.
+__global__ __launch_bounds__(kScanThreads) void k_delta_scan(DeltaBuild b, u64 n_words) {
+  __shared__ DeltaAgg lds[kScanThreads];
+  const uint32_t i = threadIdx.x;
+  const u64 k = (n_words + kScanThreads - 1) / kScanThreads;
+  const u64 w0 = u64(i) * k < n_words ? u64(i) * k : n_words;
+  const u64 w1 = w0 + k < n_words ? w0 + k : n_words;
+  const u64 A = b.t.seg;
+  DeltaAgg a{0, 0, 0, 0, 0, 0};
+  for (u64 w = w0; w < w1; w++) a = delta_then(a, b.agg[w], A);
+  lds[i] = a;
+  __syncthreads();
+  for (uint32_t d = 1; d < kScanThreads; d <<= 1) {
+    const DeltaAgg x = i >= d ? delta_then(lds[i - d], lds[i], A) : lds[i];
+    __syncthreads();
+    lds[i] = x;
+    __syncthreads();
+  }
+  const DeltaAgg before = i ? lds[i - 1] : DeltaAgg{0, 0, 0, 0, 0, 0};
+  u64 x = delta_apply(before, 0, A);
+  uint32_t ns = before.ns, nd = before.nd;
+  for (u64 w = w0; w < w1; w++) {
+    b.pre[w] = DeltaPre{x, ns, nd};
+    const DeltaAgg& g = b.agg[w];
+    x = delta_apply(g, x, A);
+    ns += g.ns;
+    nd += g.nd;
+  }
+  if (i == kScanThreads - 1) {
+    const DeltaAgg& all = lds[kScanThreads - 1];
+    const u64 end = delta_apply(all, 0, A);
+    b.counts[kDeltaIds] = u64(all.ns) + all.nd;
+    b.counts[kDeltaSent] = all.ns;
+    b.counts[kDeltaDerived] = all.nd;
+    b.counts[kDeltaEnd] = end;
+    if (b.user_counts) {
+      b.user_counts[0] = u64(all.ns) + all.nd;
+      b.user_counts[1] = align_a(end, 16);
+    }
+  }
+}
+
+template <bool kForPack>
+__global__ __launch_bounds__(256) void k_delta_build(DeltaBuild b, u64 n_words) {
+  const u64 w = u64(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (w >= n_words) return;
+  const DeltaPre pre = b.pre[w];
+  const u64 A = b.t.seg, total_end = b.counts[kDeltaEnd];
+  u64 x = pre.end;
+  uint32_t ns = pre.ns, nd = pre.nd;
+  for_listed(b, w, [&](u64 c, uint32_t e) {
+    const ListedChunk k = listed_chunk(b.t, b.bits, b.n_chunks, e, c);
+    const fr_tensor_desc& d = b.t.desc[e];
+    const uint32_t pos = ns + nd;  // list position
+    const u64 src_off = d.src_offset + k.j * b.t.C, dst_off = d.dst_offset + k.j * b.t.C;
+    if (k.derived) {
+      if (kForPack) {
+        b.src_units[pos] = SrcUnit{src_off, kNoPayload, k.len, pos, 0, uint16_t(src_off % kLine), 0};
+      } else {
+        // re-derived from the receiver's own master bytes of this chunk
+        const u64 m_dst = b.t.desc[d.derive_from].dst_offset + 2 * k.j * b.t.C;
+        b.derived[nd] = DerivedUnit{m_dst, m_dst, dst_off, k.len, 0, pos, 0};
+        b.bad[pos] = 0;
+      }
+      nd++;
+      return;
+    }
+    const u64 pay = k.cont ? x : align_a(x, A);
+    const u64 end = pay + k.len;
+    x = end;
+    if (kForPack) {
+      // zero gap up to the next sent chunk: none after the last one or before
+      // a continuing one, else up to the next segment boundary
+      const u64 gap = (end == total_end || k.next_cont) ? 0 : align_a(end, A) - align_a(end, 16);
+      const bool fits = align_a(end, 16) + gap <= b.payload_limit;  // never false for a checked cap
+      b.src_units[pos] = SrcUnit{src_off, fits ? pay : kNoPayload, k.len, pos,
+                                 fits ? uint32_t(gap >> 4) : 0u, uint16_t(src_off % kLine),
+                                 uint16_t(pay % kLine)};
+    } else {
+      // a chunk past the readable payload is neither read nor written, and flagged
+      const bool readable = align_a(end, 16) <= b.payload_limit;
+      b.plain[ns] = PlainUnit{readable ? pay : 0, dst_off, readable ? k.len : 0u, pos, 0};
+      b.bad[pos] = readable ? 0u : 1u;
+    }
+    ns++;
+  });
+}
+
+__global__ __launch_bounds__(256) void k_ids_to_bits(const uint32_t* __restrict__ ids, u64 n,
+                                                     uint32_t* __restrict__ bits) {
+  const u64 i = u64(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) atomicOr(bits + (ids[i] >> 5), 1u << (ids[i] & 31u));
 }
 
 // ------------------------------------------------------------- utilities
@@ -661,6 +903,16 @@ inline uint32_t grid_for(u64 units, const LaunchCfg& cfg) {
   return uint32_t(units < cap ? units : cap);
 }
 
+// A walk over a list built on the device covers the list's largest possible
+// length; its grid is capped (workgroups then loop), so that a short list
+// does not pay for the dispatch of a grid sized for the longest.
+template <int B>
+inline uint32_t grid_of(const Walk& wk, const LaunchCfg& cfg) {
+  uint32_t g = grid_for<B>(wk.n_slices, cfg);
+  if (wk.count && cfg.delta_grid && g > cfg.delta_grid) g = cfg.delta_grid;
+  return g;
+}
+
 // Slice geometry for chunks of C bytes and a tile of `tile_bytes`, walked by
 // the slot table `t` (built for that slice size).
 inline Walk walk_for(uint64_t C, uint32_t tile_bytes, const SlotTable& t) {
@@ -674,6 +926,7 @@ inline Walk walk_for(uint64_t C, uint32_t tile_bytes, const SlotTable& t) {
   w.imp_shift = t.implicit_shift;
   w.sl_vec = uint32_t(sl >> 4);
   w.line = t.shift;
+  w.count = reinterpret_cast<const u64*>(t.count);
   w.spc_shift = sh;
   w.g_shift = sh > kAccSlicesShift ? sh - kAccSlicesShift : 0;
   return w;
@@ -710,11 +963,11 @@ int pack_impl(bool store, const SrcUnit* units, const SlotTable& slots, uint32_t
   const auto* s = static_cast<const uint8_t*>(src);
   auto* p = static_cast<uint8_t*>(payload);
   if (store)
-    hipLaunchKernelGGL((k_pack<B, U, true>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0, st,
-                       units, wk, s, p, scr.acc);
+    hipLaunchKernelGGL((k_pack<B, U, true>), dim3(grid_of<B>(wk, cfg)), dim3(B), 0, st, units, wk,
+                       s, p, scr.acc);
   else
-    hipLaunchKernelGGL((k_pack<B, U, false>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0,
-                       st, units, wk, s, p, scr.acc);
+    hipLaunchKernelGGL((k_pack<B, U, false>), dim3(grid_of<B>(wk, cfg)), dim3(B), 0, st, units, wk,
+                       s, p, scr.acc);
   e = int(hipGetLastError());
   if (e) return e;
   FinalArgs f{};
@@ -722,6 +975,7 @@ int pack_impl(bool store, const SrcUnit* units, const SlotTable& slots, uint32_t
   f.out = sums;
   f.n_chunks = n_chunks;
   f.g_shift = wk.g_shift;
+  f.live = wk.count;  // a list built on the device: its length
   return launch_finalize(kFold, f, st);
 }
 
@@ -764,7 +1018,7 @@ int unpack_delta_impl(const UnpackDeltaArgs& u, const LaunchCfg& cfg, hipStream_
   if (e || u.n_ids == 0) return e;
   const uint32_t cvec = uint32_t(u.C >> 4);
   if (wp.n_slices) {  // sent chunks first: the masters the second phase reads
-    hipLaunchKernelGGL((k_unpack<B, U>), dim3(grid_for<B>(wp.n_slices, cfg)), dim3(B), 0, st,
+    hipLaunchKernelGGL((k_unpack<B, U>), dim3(grid_of<B>(wp, cfg)), dim3(B), 0, st,
                        static_cast<const DerivedUnit*>(nullptr), u.plain, wp, cvec,
                        static_cast<const uint8_t*>(u.payload), static_cast<uint8_t*>(u.dst),
                        u.scratch.acc);
@@ -772,7 +1026,7 @@ int unpack_delta_impl(const UnpackDeltaArgs& u, const LaunchCfg& cfg, hipStream_
     if (e) return e;
   }
   if (wd.n_slices) {
-    hipLaunchKernelGGL((k_rederive<B, U>), dim3(grid_for<B>(wd.n_slices, cfg)), dim3(B), 0, st,
+    hipLaunchKernelGGL((k_rederive<B, U>), dim3(grid_of<B>(wd, cfg)), dim3(B), 0, st,
                        u.derived, wd, cvec, static_cast<uint8_t*>(u.dst), u.scratch.acc);
     e = int(hipGetLastError());
     if (e) return e;
@@ -784,6 +1038,8 @@ int unpack_delta_impl(const UnpackDeltaArgs& u, const LaunchCfg& cfg, hipStream_
   f.count = reinterpret_cast<u64*>(u.n_bad);
   f.n_chunks = u.n_ids;
   f.g_shift = wp.g_shift;
+  f.live = reinterpret_cast<const u64*>(u.live);
+  f.flags = u.bad;
   return launch_finalize(kCompare, f, st);
 }
 
@@ -853,6 +1109,35 @@ int launch_expand_slots(const uint64_t* first, const uint64_t* base, uint64_t n_
   hipLaunchKernelGGL(k_expand_slots, dim3(blocks), dim3(256), 0, hipStream_t(stream),
                      reinterpret_cast<const u64*>(first), reinterpret_cast<const u64*>(base),
                      u64(n_runs), u64(n), u64(stride), reinterpret_cast<u64*>(out));
+  return int(hipGetLastError());
+}
+
+int launch_delta_build(const DeltaBuild& b, bool for_pack, void* stream) {
+  const hipStream_t st = hipStream_t(stream);
+  const u64 n_words = (b.n_chunks + 31) / 32;
+  const dim3 grid(uint32_t((n_words + 255) / 256)), block(256);
+  if (n_words) {
+    hipLaunchKernelGGL(k_delta_agg, grid, block, 0, st, b, n_words);
+    if (const hipError_t e = hipGetLastError()) return int(e);
+  }
+  hipLaunchKernelGGL(k_delta_scan, dim3(1), dim3(kScanThreads), 0, st, b, n_words);
+  if (const hipError_t e = hipGetLastError()) return int(e);
+  if (n_words) {
+    if (for_pack) hipLaunchKernelGGL(k_delta_build<true>, grid, block, 0, st, b, n_words);
+    else hipLaunchKernelGGL(k_delta_build<false>, grid, block, 0, st, b, n_words);
+  }
+  return int(hipGetLastError());
+}
+
+int launch_ids_to_bits(const uint32_t* ids, uint64_t n, uint32_t* bits, uint64_t words,
+                       void* stream) {
+  const hipStream_t st = hipStream_t(stream);
+  Zeroes z;
+  z.add(bits, words * 4);
+  const int e = z.launch(st);
+  if (e || n == 0) return e;
+  hipLaunchKernelGGL(k_ids_to_bits, dim3(uint32_t((n + 255) / 256)), dim3(256), 0, st, ids, u64(n),
+                     bits);
   return int(hipGetLastError());
 }
 

@@ -26,6 +26,9 @@ constexpr uint32_t kDefaultTilePack = 4, kDefaultTileUnpack = 5, kDefaultTileVer
 // Line-aligned walks (0 off, 1 at lines of the arena read, 2 at lines of the
 // payload written): pack cuts at payload lines, the compare at arena lines.
 constexpr int kDefaultLinePack = 2, kDefaultLineVerify = 1, kDefaultLineChecksum = 0;
+// Workgroups of a launch that walks a delta list built on the device (the
+// host knows only its largest possible length): 256 per CU.
+constexpr uint32_t kDefaultDeltaGrid = 65536;
 
 static uint64_t esize(uint32_t dtype) { return dtype == FR_F32 ? 4 : 2; }
 static uint64_t align16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
@@ -79,10 +82,16 @@ int validate_and_layout(const fr_tensor_desc* t, uint32_t n, uint64_t C, uint64_
   L->pay_off.assign(n, 0);
   L->chunk_base.assign(size_t(n) + 1, 0);
   uint64_t base = 0, end = 0;  // end of the last payload segment so far
+  uint64_t sent_bytes = 0;
+  L->n_sent_chunks = 0;
   for (uint32_t k = 0; k < n; k++) {
     uint64_t nb = t[k].numel * esize(t[k].dtype);
     L->chunk_base[k] = base;
     base += (nb + C - 1) / C;
+    if (t[k].derive_from < 0) {
+      L->n_sent_chunks += (nb + C - 1) / C;
+      sent_bytes += nb;
+    }
     if (t[k].derive_from >= 0) {
       L->pay_off[k] = kNoPayload;
     } else if (nb == 0) {
@@ -97,6 +106,11 @@ int validate_and_layout(const fr_tensor_desc* t, uint32_t n, uint64_t C, uint64_
   L->n_chunks = base;
   L->payload_bytes = align16(end);
   L->state_bytes = state;
+  // A delta payload never outgrows the full one when C >= A: chunk by chunk
+  // its offsets stay at or below the full payload's, whose chunks all start
+  // on multiples of A.  With C < A each sent chunk adds at most its bytes and
+  // a gap below A.
+  L->delta_payload_max = C >= seg ? L->payload_bytes : align16(sent_bytes + L->n_sent_chunks * seg);
   return FR_OK;
 }
 
@@ -112,6 +126,7 @@ static void fill_info(const Layout& L, uint32_t n, uint64_t src, uint64_t dst, i
   info->state_bytes = L.state_bytes;
   info->device = dev;
   info->segment_align = L.seg;
+  info->delta_payload_max = L.delta_payload_max;
 }
 
 static uint32_t env_u32(const char* name, uint32_t dflt) {
@@ -222,7 +237,10 @@ extern "C" int fr_plan_destroy(fr_plan* p) {
   if (p->d_derived) (void)hipFree(p->d_derived);
   if (p->d_plain) (void)hipFree(p->d_plain);
   if (p->d_scratch) (void)hipFree(p->d_scratch);
+  if (p->delta_ids_copied) (void)hipEventSynchronize(p->delta_ids_copied);
   if (p->d_delta) (void)hipFree(p->d_delta);
+  if (p->h_delta_ids) (void)hipHostFree(p->h_delta_ids);
+  if (p->delta_ids_copied) (void)hipEventDestroy(p->delta_ids_copied);
   if (switched) (void)hipSetDevice(prev);
   delete p;
   return FR_OK;
@@ -236,6 +254,7 @@ namespace {
 LaunchCfg launch_config() {
   LaunchCfg cfg;
   cfg.max_grid = env_u32("FLASHRESTORE_MAX_GRID", 0);
+  cfg.delta_grid = env_u32("FLASHRESTORE_DELTA_GRID", kDefaultDeltaGrid);
   const uint32_t all = env_u32("FLASHRESTORE_TILE", ~0u);  // one tile for every operation
   auto pick = [&](const char* name, uint32_t dflt) {
     return int(env_u32(name, all != ~0u ? all : dflt));
@@ -407,6 +426,56 @@ int build_scratch(fr_plan* p) {
   return rc;
 }
 
+// Delta lists built on the device: the tensor table and chunk bases they are
+// read from, room for the records of the longest list (pack's one per chunk,
+// or unpack's plain and derived ones), the scan state, and the staging of a
+// list given on the host (pinned, so that its upload is asynchronous; an
+// event marks when the staging may be refilled).  Allocated once here, so
+// that no delta call allocates.
+int build_delta(fr_plan* p) {
+  const Layout& L = p->layout;
+  const uint64_t n = p->table.size(), nc = L.n_chunks, nw = (nc + 31) / 32;
+  auto up = [](uint64_t b) { return (b + 255) & ~uint64_t(255); };
+  const uint64_t b_desc = up(n * sizeof(fr_tensor_desc)), b_base = up((n + 1) * 8);
+  const uint64_t b_units = up(std::max(nc * sizeof(SrcUnit), L.n_sent_chunks * sizeof(PlainUnit) +
+                                                              (nc - L.n_sent_chunks) * sizeof(DerivedUnit)));
+  const uint64_t b_agg = up(nw * sizeof(DeltaAgg)), b_pre = up(nw * sizeof(DeltaPre));
+  const uint64_t b_counts = 256, b_bits = up(nw * 4), b_ids = up(nc * 4);
+  const uint64_t total = b_desc + b_base + b_units + b_agg + b_pre + b_counts + b_bits + b_ids;
+  int rc = upload(nullptr, total, &p->d_delta);
+  if (rc != FR_OK) return rc;
+  uint8_t* q = static_cast<uint8_t*>(p->d_delta);
+  auto take = [&](uint64_t b) {
+    uint8_t* r = q;
+    q += b;
+    return r;
+  };
+  fr_tensor_desc* desc = reinterpret_cast<fr_tensor_desc*>(take(b_desc));
+  uint64_t* base = reinterpret_cast<uint64_t*>(take(b_base));
+  uint8_t* units = take(b_units);
+  p->d_delta_src = reinterpret_cast<SrcUnit*>(units);
+  p->d_delta_plain = reinterpret_cast<PlainUnit*>(units);
+  p->d_delta_derived = reinterpret_cast<DerivedUnit*>(units + L.n_sent_chunks * sizeof(PlainUnit));
+  p->d_delta_agg = reinterpret_cast<DeltaAgg*>(take(b_agg));
+  p->d_delta_pre = reinterpret_cast<DeltaPre*>(take(b_pre));
+  p->d_delta_counts = reinterpret_cast<uint64_t*>(take(b_counts));
+  p->d_delta_bits = reinterpret_cast<uint32_t*>(take(b_bits));
+  p->d_delta_ids = reinterpret_cast<uint32_t*>(take(b_ids));
+  hipError_t e = hipSuccess;
+  if (n) e = hipMemcpy(desc, p->table.data(), n * sizeof(fr_tensor_desc), hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy(base, L.chunk_base.data(), (n + 1) * 8, hipMemcpyHostToDevice);
+  if (e == hipSuccess && nc)
+    e = hipHostMalloc(reinterpret_cast<void**>(&p->h_delta_ids), nc * 4, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&p->delta_ids_copied, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e == hipErrorOutOfMemory ? FR_E_NOMEM : hip_fail(e);
+  }
+  p->delta_tables = DeltaTables{desc, base, uint32_t(n), L.C, L.seg};
+  return FR_OK;
+}
+
 }  // namespace
 
 extern "C" int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n, uint64_t C,
@@ -453,6 +522,7 @@ extern "C" int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n, uint64
     if (rc == FR_OK)
       rc = upload(plain.data(), plain.size() * sizeof(PlainUnit), (void**)&p->d_plain);
     if (rc == FR_OK) rc = build_scratch(p);
+    if (rc == FR_OK) rc = build_delta(p);
     if (rc != FR_OK) {
       fr_plan_destroy(p);
       return rc;

@@ -50,6 +50,7 @@ class fr_plan_info(C.Structure):
         ("state_bytes", C.c_uint64),
         ("device", C.c_int64),
         ("segment_align", C.c_uint64),
+        ("delta_payload_max", C.c_uint64),
     ]
 
     def as_dict(self):
@@ -108,6 +109,8 @@ def _load():
         "fr_delta_layout": [P, P, u64, C.POINTER(u64)],
         "fr_pack_chunks": [P, P, P, u64, P, u64, P, P],
         "fr_unpack_chunks": [P, P, u64, P, P, u64, P, P, P, P],
+        "fr_pack_flagged": [P, P, P, P, u64, P, P, P],
+        "fr_unpack_flagged": [P, P, u64, P, P, P, P, P, P],
         "fr_tracker_create": [u32, P, C.c_double, C.c_double, C.POINTER(P)],
         "fr_tracker_destroy": [P],
         "fr_tracker_heartbeat": [P, u32, C.c_int64, C.c_double],
@@ -137,8 +140,9 @@ _lib = _load()
 EXPORTED = (
     "fr_plan_create", "fr_plan_create_ex", "fr_plan_get_info", "fr_plan_chunk_of", "fr_plan_entry_layout",
     "fr_plan_destroy", "fr_layout_query", "fr_pack_state", "fr_unpack_state",
-    "fr_verify_replicas", "fr_verify_replicas_noalloc", "fr_checksum_state", "fr_delta_layout", "fr_pack_chunks",
-    "fr_unpack_chunks", "fr_tracker_create", "fr_tracker_destroy", "fr_tracker_heartbeat",
+    "fr_verify_replicas", "fr_verify_replicas_noalloc", "fr_checksum_state", "fr_delta_layout",
+    "fr_pack_chunks", "fr_unpack_chunks", "fr_pack_flagged", "fr_unpack_flagged",
+    "fr_tracker_create", "fr_tracker_destroy", "fr_tracker_heartbeat",
     "fr_tracker_report_failure", "fr_tracker_decide", "fr_tracker_failed_ranks", "fr_tracker_donors",
     "fr_layout_rank_coords", "fr_layout_donors", "fr_layout_state_table",
     "fr_strerror", "fr_last_hip_error", "fr_abi_version",
@@ -328,6 +332,22 @@ class Plan:
     def unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream=None, payload_bytes=None,
                       sync=False):
         return fr_unpack_chunks(self, payload, sums, chunk_ids, dst, bitmap, n_bad, stream, payload_bytes, sync)
+
+    @property
+    def delta_payload_max(self) -> int:
+        return self.info["delta_payload_max"]
+
+    def empty_delta_payload(self, device="cuda"):
+        import torch
+
+        return torch.empty(max(self.delta_payload_max, 16), dtype=torch.uint8, device=device)
+
+    def pack_flagged(self, src, flagged, payload, sums, counts=None, stream=None, payload_cap=None):
+        return fr_pack_flagged(self, src, flagged, payload, payload_cap, sums, counts, stream)
+
+    def unpack_flagged(self, payload, sums, flagged, dst, bitmap, n_bad, stream=None, payload_bytes=None,
+                       sync=False):
+        return fr_unpack_flagged(self, payload, payload_bytes, sums, flagged, dst, bitmap, n_bad, stream, sync)
 
 
 def _synced_bits(bitmap, n: int, stream) -> np.ndarray:
@@ -581,3 +601,37 @@ def bitmap_indices(bitmap, n_chunks: int) -> np.ndarray:
     b = bitmap.detach().cpu().numpy() if hasattr(bitmap, "detach") else np.asarray(bitmap)
     bits = np.unpackbits(np.ascontiguousarray(b).view(np.uint8), bitorder="little")
     return np.nonzero(bits[:n_chunks])[0]
+
+
+def fr_pack_flagged(plan: Plan, src, flagged, payload, payload_cap, sums, counts=None, stream=None) -> None:
+    """Delta pack of the chunks whose bits are set in the device bitmap
+    `flagged`; `counts` (None or a device tensor of two int64) receives the
+    list's length and its delta payload bytes."""
+    i = plan.info
+    if payload_cap is None:
+        payload_cap = _nbytes(payload)
+        if payload_cap is None:
+            payload_cap = i["delta_payload_max"]
+    _check(_lib.fr_pack_flagged(plan.handle, _dev(src, i["src_arena_bytes"], "src"),
+                                _dev(flagged, 4 * i["bitmap_words"], "flagged"),
+                                _dev(payload, min(payload_cap, i["delta_payload_max"]), "payload"), payload_cap,
+                                _dev(sums, SUM_BYTES * i["n_chunks"], "sums"), _dev(counts, 16, "counts"),
+                                _stream(stream)), "fr_pack_flagged")
+
+
+def fr_unpack_flagged(plan: Plan, payload, payload_bytes, sums, flagged, dst, bad_bitmap, n_bad, stream=None,
+                      sync=False):
+    """Delta unpack of the chunks whose bits are set in `flagged`; with
+    sync=True wait and return the sorted list positions that failed."""
+    i = plan.info
+    if payload_bytes is None:
+        payload_bytes = _nbytes(payload)
+        if payload_bytes is None:
+            raise ValueError("payload_bytes is needed with a raw payload address")
+    _check(_lib.fr_unpack_flagged(plan.handle, _dev(payload, payload_bytes, "payload"), payload_bytes,
+                                  _dev(sums, SUM_BYTES * i["n_chunks"], "sums"),
+                                  _dev(flagged, 4 * i["bitmap_words"], "flagged"),
+                                  _dev(dst, i["dst_arena_bytes"], "dst"),
+                                  _dev(bad_bitmap, 4 * i["bitmap_words"], "bad_bitmap"),
+                                  _dev(n_bad, 8, "n_bad"), _stream(stream)), "fr_unpack_flagged")
+    return _synced_bits(bad_bitmap, i["n_chunks"], stream) if sync else None

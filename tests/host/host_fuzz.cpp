@@ -24,6 +24,8 @@ namespace fr {
 uint32_t tile_bytes(int) { return 4096; }
 uint64_t accumulators_per_chunk(uint64_t, int) { return 1; }
 int static_scratch_address(int, void**) { return 1; }
+int launch_delta_build(const DeltaBuild&, bool, void*) { return 1; }
+int launch_ids_to_bits(const uint32_t*, uint64_t, uint32_t*, uint64_t, void*) { return 1; }
 int launch_pack(const SrcUnit*, const SlotTable&, uint32_t, uint64_t, const void*, void*,
                 fr_chunk_sum*, const Scratch&, const LaunchCfg&, void*) { return 1; }
 int launch_checksum(const SrcUnit*, const SlotTable&, uint32_t, uint64_t, const void*,

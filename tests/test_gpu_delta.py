@@ -23,35 +23,65 @@ def _gpu():
         pytest.skip("no GPU")
 
 
+def flagged_bitmap(plan, ids):
+    """The device bitmap over the plan's chunk ids with the bits of `ids` set."""
+    bits = np.zeros(max(plan.bitmap_words, 1), np.uint32)
+    np.bitwise_or.at(bits, ids.astype(np.int64) >> 5, (np.uint32(1) << (ids & 31).astype(np.uint32)))
+    return to_dev(bits.view(np.int32))
+
+
 def _one(t, C, src_np, recv_np, ids, rng, tag, seg=None):
+    """The host-list calls and the bitmap-driven calls on one list, each
+    against the oracle: delta payload (gaps included), sums, receiver arena
+    and result set, with the wire corrupted at random."""
     plan = F.Plan(t, C, max(src_np.size, 16), max(recv_np.size, 16), seg)
     oseg = cpu.SEGMENT if seg is None else seg
     src = to_dev(src_np) if src_np.size else torch.zeros(16, dtype=torch.uint8, device="cuda")
     dst = to_dev(recv_np) if recv_np.size else torch.zeros(16, dtype=torch.uint8, device="cuda")
+    dst2 = dst.clone()
     pb = plan.delta_layout(ids)
     off, opb = cpu.delta_layout(t, C, ids, oseg)
     assert pb == opb, tag
+    assert pb <= plan.delta_payload_max, tag
     payload = torch.full((max(pb, 16),), 0xEE, dtype=torch.uint8, device="cuda")  # gaps must be written
     sums = torch.empty(max(ids.size, 1), 2, dtype=torch.int64, device="cuda")
     plan.pack_chunks(src, ids, payload, sums)
     opay, osums = cpu.pack_chunks(t, C, src_np, ids, oseg)
+    flagged = flagged_bitmap(plan, ids)
+    fpay = plan.empty_delta_payload().fill_(0xEE)
+    fsums = plan.empty_sums().fill_(-1)
+    counts = torch.full((2,), -1, dtype=torch.int64, device="cuda")
+    plan.pack_flagged(src, flagged, fpay, fsums, counts)
     torch.cuda.synchronize()
     assert np.array_equal(to_host(payload)[:pb], opay), f"payload {tag}"
     assert np.array_equal(sums_host(sums, ids.size), osums), f"sums {tag}"
+    assert counts.tolist() == [ids.size, pb], f"flagged counts {tag}"
+    assert np.array_equal(to_host(fpay)[:pb], opay), f"flagged payload {tag}"
+    assert np.array_equal(sums_host(fsums, ids.size), osums), f"flagged sums {tag}"
+    assert bool((fsums[ids.size:] == -1).all()), f"flagged sums past the list {tag}"
     if pb and rng.random() < 0.4:  # corrupt the wire
         b = int(rng.integers(0, pb * 8))
         opay[b // 8] ^= np.uint8(1 << (b % 8))
         payload[b // 8] ^= 1 << (b % 8)
+        fpay[b // 8] ^= 1 << (b % 8)
     bad = torch.empty(max((ids.size + 31) // 32, 1), dtype=torch.int32, device="cuda")
     nbad = torch.empty(1, dtype=torch.int64, device="cuda")
     plan.unpack_chunks(payload, sums, ids, dst, bad, nbad)
+    fbad = plan.empty_bitmap().fill_(-1)
+    fnbad = plan.empty_counter().fill_(-1)
+    plan.unpack_flagged(fpay, fsums, flagged, dst2, fbad, fnbad, payload_bytes=pb)
     orecv = recv_np.copy()
     obm, onbad = cpu.unpack_chunks(t, C, opay, osums, ids, orecv, oseg)
     torch.cuda.synchronize()
     if recv_np.size:
         assert np.array_equal(to_host(dst)[: recv_np.size], orecv), f"dst {tag}"
-    assert set(F.bitmap_indices(bad, ids.size).tolist()) == set(cpu.bitmap_to_set(obm, ids.size)), tag
+        assert np.array_equal(to_host(dst2)[: recv_np.size], orecv), f"flagged dst {tag}"
+    want = set(cpu.bitmap_to_set(obm, ids.size))
+    assert set(F.bitmap_indices(bad, ids.size).tolist()) == want, tag
     assert int(nbad.item()) == onbad
+    # every word of the flagged call's bitmap is written: bits past the list are 0
+    assert set(F.bitmap_indices(fbad, plan.n_chunks).tolist()) == want, f"flagged bits {tag}"
+    assert int(fnbad.item()) == onbad, tag
 
 
 def test_delta_bruteforce_tiny_tables():
@@ -136,6 +166,52 @@ def test_delta_capped_grid_multiwave_tiles(tile):
                 os.environ[k] = v
 
 
+def test_flagged_unpack_flags_chunks_past_the_readable_payload():
+    """fr_unpack_flagged given fewer payload bytes than the list needs: the
+    chunks that lie past them are neither read nor written and are flagged;
+    the others are restored and pass."""
+    rng = np.random.default_rng(404)
+    done = 0
+    for it in range(200):
+        t, sb, db = W.random_tiny_table(rng, max_entries=8, max_numel=2000, allow_derive=False)
+        C = int(rng.choice([16, 64, 256]))
+        _, base, _, _ = cpu.plan(t, C)
+        nc = int(base[-1])
+        if nc == 0:
+            continue
+        ids = np.sort(rng.choice(nc, size=int(rng.integers(1, nc + 1)), replace=False)).astype(np.uint32)
+        src_np = W.random_tiny_state(t, sb, rng)
+        recv_np = rng.integers(0, 256, size=db, dtype=np.uint8)
+        off, pb = cpu.delta_layout(t, C, ids)
+        opay, osums = cpu.pack_chunks(t, C, src_np, ids)
+        limit = int(rng.integers(0, pb + 1))
+        plan = F.Plan(t, C, sb, db)
+        pay = to_dev(opay[:limit]) if limit else torch.zeros(16, dtype=torch.uint8, device="cuda")
+        sums = plan.empty_sums()
+        sums[: ids.size] = torch.from_numpy(osums.view(np.int64).reshape(-1, 2)).to("cuda")
+        dst = to_dev(recv_np)
+        bad, nbad = plan.empty_bitmap(), plan.empty_counter()
+        got = plan.unpack_flagged(pay, sums, flagged_bitmap(plan, ids), dst, bad, nbad,
+                                  payload_bytes=limit, sync=True)
+        exp_dst, exp_bad = recv_np.copy(), set()
+        for i, c in enumerate(ids):
+            k = int(np.searchsorted(base, c, side="right")) - 1
+            e = t[k]
+            nb = int(e["numel"]) * (4 if int(e["dtype"]) == W.F32 else 2)
+            j = int(c) - int(base[k])
+            ln = min(C, nb - j * C)
+            if -(-(int(off[i]) + ln) // 16) * 16 <= limit:
+                s0, d0 = int(e["src_offset"]) + j * C, int(e["dst_offset"]) + j * C
+                exp_dst[d0:d0 + ln] = src_np[s0:s0 + ln]
+            else:
+                exp_bad.add(i)
+        assert set(got.tolist()) == exp_bad and int(nbad.item()) == len(exp_bad), it
+        assert np.array_equal(to_host(dst), exp_dst), it
+        done += 1
+    assert done > 100
+    log(f"truncated payloads: {done} lists")
+
+
 def test_listing_every_chunk_equals_the_full_pack():
     w = W.make_workload(0)
     src = to_dev(W.fill_state(w))
@@ -194,6 +270,21 @@ def test_repair_llama8b_share_from_the_flagged_chunks():
     torch.cuda.synchronize()
     assert int(nbad.item()) == 0 and int(ndiff.item()) == 0 and torch.equal(recv, donor)
     log(f"repaired {ids.size} chunks with {pb} payload bytes")
+    # the same repair driven by the compare's device bitmap, no host list
+    recv[idx] = recv[idx] ^ torch.from_numpy(np.bitwise_or.reduceat(masks, start)).to("cuda")
+    del payload
+    fpay = plan.empty_delta_payload()
+    fsums = plan.empty_sums()
+    counts = torch.empty(2, dtype=torch.int64, device="cuda")
+    fbad = plan.empty_bitmap()
+    plan.verify_replicas(donor, recv, diff, ndiff)
+    plan.pack_flagged(donor, diff, fpay, fsums, counts)
+    plan.unpack_flagged(fpay, fsums, diff, recv, fbad, nbad, payload_bytes=fpay.numel())
+    torch.cuda.synchronize()
+    assert counts.tolist() == [ids.size, pb]
+    assert np.array_equal(to_host(fpay[:pb]), opay) and np.array_equal(sums_host(fsums, ids.size), osums)
+    assert int(nbad.item()) == 0 and torch.equal(recv, donor)
+    log("repaired again from the device bitmap")
 
 
 @pytest.mark.parametrize("seg", [None, 4096])

@@ -1,8 +1,9 @@
 """Streams and graphs.  A whole restore step captured in a HIP graph (the
 operations are kernel launches only: no memsets, no host work on the stream)
 and replayed several times, with eager work and synchronisation between
-replays, every replay checked against the eager result; and two plans run
-concurrently on two streams."""
+replays, every replay checked against the eager result; a replica compare and
+the repair it drives (the flagged delta calls) captured and replayed on
+different divergences; and two plans run concurrently on two streams."""
 import numpy as np
 import pytest
 import torch
@@ -71,6 +72,62 @@ def test_captured_restore_step_replays_correctly():
     torch.cuda.synchronize()
     assert torch.equal(payload, ref[0]) and torch.equal(sums, ref[1])
     assert torch.equal(dst, ref[2]) and torch.equal(csum, ref[3])
+
+
+def test_captured_compare_and_repair_replays_correctly():
+    """Replica compare -> delta pack of the flagged chunks -> delta unpack
+    into the replica, captured once and replayed on a different divergence
+    each time: the replica equals the donor again, and the delta payload and
+    sums equal the oracle's for the flagged list."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from oracle import cpu
+
+    w = W.make_workload(0)
+    t, C = w.table, w.chunk_bytes
+    donor_np = W.fill_state(w)
+    plan = F.Plan(t, C, w.src_arena_bytes, w.src_arena_bytes)
+    donor = torch.from_numpy(donor_np).to("cuda")
+    replica = donor.clone()
+    diff, ndiff = plan.empty_bitmap(), plan.empty_counter()
+    pay, sums = plan.empty_delta_payload(), plan.empty_sums()
+    counts = torch.empty(2, dtype=torch.int64, device="cuda")
+    bad, nbad = plan.empty_bitmap(), plan.empty_counter()
+
+    def repair():
+        plan.verify_replicas(donor, replica, diff, ndiff)
+        plan.pack_flagged(donor, diff, pay, sums, counts)
+        plan.unpack_flagged(pay, sums, diff, replica, bad, nbad, payload_bytes=pay.numel())
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        repair()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        repair()
+    torch.cuda.synchronize()
+
+    rng = np.random.default_rng(17)
+    for rep, k in enumerate((1, 7, 0, 300, 64)):
+        pos = rng.choice(donor_np.size * 8, size=k, replace=False)
+        rep_np = donor_np.copy()
+        for p in pos:
+            rep_np[p // 8] ^= np.uint8(1 << (p % 8))
+        replica.copy_(torch.from_numpy(rep_np).to("cuda"))
+        nbad.fill_(99)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        bm, nd = cpu.verify(t, C, donor_np, rep_np)
+        ids = np.array(cpu.bitmap_to_set(bm, plan.n_chunks), np.uint32)
+        opay, osums = cpu.pack_chunks(t, C, donor_np, ids)
+        assert int(ndiff.item()) == nd and counts.tolist() == [ids.size, opay.size], rep
+        assert np.array_equal(pay[: opay.size].cpu().numpy(), opay), rep
+        assert np.array_equal(sums[: ids.size].cpu().numpy().view(np.uint64).reshape(-1), osums), rep
+        assert int(nbad.item()) == 0 and torch.equal(replica, donor), rep
 
 
 def test_two_plans_on_two_streams_run_concurrently():
