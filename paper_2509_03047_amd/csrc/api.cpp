@@ -98,11 +98,12 @@ int launch_result(int hip_rc) {
 // The plan's pack / checksum / compare walk at the slice size of `tile`,
 // line-aligned or not (the plan builds one for each configuration its
 // operations use, so this finds one for the plan's own).
-const SlotTable* src_walk(const fr_plan* plan, int tile, int line) {
+const SlotTable* src_walk(const fr_plan* plan, int tile, int line, int absorb = 0) {
   const uint32_t sl = slice_bytes(plan->layout.C, tile);
   const uint32_t shift = line_walk(plan, tile, line);
+  const uint32_t ab = shift && absorb ? 1u : 0u;
   for (const auto& w : plan->src_walks)
-    if (w.sl == sl && w.t.shift == shift) return &w.t;
+    if (w.sl == sl && w.t.shift == shift && w.t.absorb == ab) return &w.t;
   return nullptr;
 }
 
@@ -126,7 +127,7 @@ extern "C" int fr_pack_state(const fr_plan* plan, const void* src_base, void* pa
   const Region outs[] = {{payload, L.payload_bytes}, {sums, L.n_chunks * sizeof(fr_chunk_sum)}};
   const Region ins[] = {{src_base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 2, ins, 1));
-  const SlotTable* walk = src_walk(plan, plan->cfg.tile_pack, plan->cfg.line_pack);
+  const SlotTable* walk = src_walk(plan, plan->cfg.tile_pack, plan->cfg.line_pack, plan->cfg.absorb_pack);
   if (!walk) return FR_E_INVAL;
   return launch_result(launch_pack(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, src_base,
                                    payload, sums, plan->scratch, plan->cfg, stream));
@@ -188,7 +189,7 @@ int verify_checks(const fr_plan* plan, const void* base_a, const void* base_b,
   const Region outs[] = {{diff_bitmap, words * 4}, {n_diff, 8}, {sums_a, sb}, {sums_b, sb}};
   const Region ins[] = {{base_a, plan->src_arena_bytes}, {base_b, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 4, ins, 2));
-  *walk = src_walk(plan, plan->cfg.tile_verify, plan->cfg.line_verify);
+  *walk = src_walk(plan, plan->cfg.tile_verify, plan->cfg.line_verify, plan->cfg.absorb_verify);
   return *walk ? FR_OK : FR_E_INVAL;
 }
 
@@ -242,7 +243,8 @@ extern "C" int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk
   const Region outs[] = {{sums, L.n_chunks * sizeof(fr_chunk_sum)}};
   const Region ins[] = {{base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 1, ins, 1));
-  const SlotTable* walk = src_walk(plan, plan->cfg.tile_checksum, plan->cfg.line_checksum);
+  const SlotTable* walk =
+      src_walk(plan, plan->cfg.tile_checksum, plan->cfg.line_checksum, plan->cfg.absorb_checksum);
   if (!walk) return FR_E_INVAL;
   return launch_result(launch_checksum(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, base,
                                        sums, plan->scratch, plan->cfg, stream));
@@ -316,12 +318,15 @@ int upload_list(const fr_plan* plan, const uint32_t* ids, uint64_t n_ids, hipStr
   return launch_result(launch_ids_to_bits(plan->d_delta_ids, n_ids, plan->d_delta_bits, words, stream));
 }
 
+// Arguments of the list builder for a call of operation `tile` (whose
+// accumulators per list position it clears, with *zero_word if given).
 DeltaBuild delta_build(const fr_plan* plan, const uint32_t* bits, uint64_t* user_counts,
-                       uint64_t payload_limit) {
+                       uint64_t payload_limit, int tile, uint64_t* zero_word) {
   DeltaBuild b{};
-  b.t = plan->delta_tables;
+  b.loc = plan->d_delta_loc;
   b.bits = bits;
   b.n_chunks = plan->layout.n_chunks;
+  b.seg = plan->layout.seg;
   b.agg = plan->d_delta_agg;
   b.pre = plan->d_delta_pre;
   b.counts = plan->d_delta_counts;
@@ -331,6 +336,11 @@ DeltaBuild delta_build(const fr_plan* plan, const uint32_t* bits, uint64_t* user
   b.derived = plan->d_delta_derived;
   b.bad = plan->scratch.flags;
   b.payload_limit = payload_limit;
+  b.acc = plan->scratch.acc;
+  uint32_t g = 0;
+  while ((uint64_t(1) << g) < accumulators_per_chunk(plan->layout.C, tile)) g++;
+  b.acc_shift = g;
+  b.zero_word = zero_word;
   return b;
 }
 
@@ -339,7 +349,8 @@ DeltaBuild delta_build(const fr_plan* plan, const uint32_t* bits, uint64_t* user
 int pack_list(const fr_plan* plan, const void* src_base, const uint32_t* bits, uint64_t bound,
               void* payload, uint64_t payload_cap, fr_chunk_sum* sums, uint64_t* user_counts,
               hipStream_t stream) {
-  FR_TRY(launch_result(launch_delta_build(delta_build(plan, bits, user_counts, payload_cap), true, stream)));
+  FR_TRY(launch_result(launch_delta_build(
+      delta_build(plan, bits, user_counts, payload_cap, plan->cfg.tile_pack, nullptr), true, stream)));
   const uint64_t C = plan->layout.C;
   return launch_result(launch_pack(plan->d_delta_src,
                                    list_walk(bound, plan->d_delta_counts + kDeltaIds, C,
@@ -355,8 +366,8 @@ int unpack_list(const fr_plan* plan, const void* payload, uint64_t payload_bytes
                 const fr_chunk_sum* sums, const uint32_t* bits, uint64_t bound, void* dst_base,
                 uint32_t* bad_bitmap, uint64_t* n_bad, hipStream_t stream) {
   if (bound) {
-    FR_TRY(launch_result(
-        launch_delta_build(delta_build(plan, bits, nullptr, payload_bytes), false, stream)));
+    FR_TRY(launch_result(launch_delta_build(
+        delta_build(plan, bits, nullptr, payload_bytes, plan->cfg.tile_unpack, n_bad), false, stream)));
   }
   const uint64_t C = plan->layout.C;
   UnpackDeltaArgs a{};
@@ -374,8 +385,10 @@ int unpack_list(const fr_plan* plan, const void* payload, uint64_t payload_bytes
   a.bitmap = bad_bitmap;
   a.n_bad = n_bad;
   a.scratch = plan->scratch;
-  a.live = plan->d_delta_counts + kDeltaIds;
-  a.bad = plan->scratch.flags;
+  if (bound) {  // the builder cleared the accumulators and n_bad
+    a.live = plan->d_delta_counts + kDeltaIds;
+    a.bad = plan->scratch.flags;
+  }
   return launch_result(launch_unpack_delta(a, plan->cfg, stream));
 }
 

@@ -19,6 +19,9 @@ constexpr uint64_t kDefaultSegmentAlign = 16;
 constexpr uint64_t kMaxSegmentAlign = uint64_t(1) << 20;
 constexpr uint32_t kNoMaster = 0xFFFFFFFFu;
 constexpr uint32_t kLine = 128;  // L2 cache line (bytes)
+// Unit records keep offsets modulo this, enough for any slice size (at most
+// 16 KiB), so that a walk can cut slices at lines or at slice boundaries.
+constexpr uint32_t kLeadMod = 32768;
 // Bytes of the static device array the no-allocation calls use as scratch
 // (kernels.hip); the public limit FR_STATIC_SCRATCH_BYTES.
 constexpr uint64_t kStaticScratchBytes = FR_STATIC_SCRATCH_BYTES;
@@ -47,8 +50,8 @@ struct alignas(16) SrcUnit {
   uint32_t c;        // its sums slot: global chunk id, or list position for a delta
   uint32_t gap_v;    // zero vectors pack writes after the chunk's 16-byte-padded end
                      //   (the gap up to the next segment; < segment alignment / 16)
-  uint16_t lead;     // src_off mod kLine: how far into a cache line the chunk starts
-  uint16_t plead;    // pay_off mod kLine (0 without payload): the same in the payload
+  uint16_t lead;     // src_off mod kLeadMod: where the chunk starts within lines / slices
+  uint16_t plead;    // pay_off mod kLeadMod (0 without payload): the same in the payload
 };
 static_assert(sizeof(SrcUnit) == 32, "SrcUnit is 32 bytes");
 
@@ -72,7 +75,8 @@ struct alignas(16) PlainUnit {
   uint64_t dst_off;
   uint32_t len;
   uint32_t c;
-  uint64_t pad_;
+  uint32_t plead;  // pay_off mod kLeadMod
+  uint32_t dlead;  // dst_off mod kLeadMod
 };
 static_assert(sizeof(PlainUnit) == 32, "PlainUnit is 32 bytes");
 
@@ -103,9 +107,15 @@ struct SlotTable {
   // on a cache-line boundary and no line is fetched or written by two
   // workgroups; a chunk has ceil((lead + len) / SL) slices (one more than a
   // plain walk's when it starts inside a line and ends near a slice end).
-  // shift 1 takes lead from the arena read (SrcUnit::lead), 2 from the
-  // payload written (SrcUnit::plead).
+  // shift 1 takes lead as the offset into a line of the arena read
+  // (SrcUnit::lead), 2 into a line of the payload (SrcUnit::plead); 3 cuts
+  // at multiples of SL in the payload instead of lines (lead = the payload
+  // offset mod SL; for pack's SrcUnit walks and unpack's plain chunks).
   uint32_t shift = 0;
+  // With absorb, a unit keeps the plain walk's ceil(len / SL) slices and its
+  // last slice also takes the leftover lead bytes (at most a line less 16
+  // bytes for modes 1 and 2) instead of a further, nearly empty, slice.
+  uint32_t absorb = 0;
   // Implicit walk over a list built on the device: n covers the longest
   // list, and only the slots of the first *count units work.
   const uint64_t* count = nullptr;
@@ -147,10 +157,12 @@ struct LaunchCfg {
   uint32_t max_grid = 0;  // cap on workgroups per launch (0: hardware limit); grid-stride beyond
   uint32_t delta_grid = 0;  // cap on workgroups walking a list built on the device (0: none)
   int tile_pack = 0, tile_unpack = 0, tile_verify = 0, tile_checksum = 0;
-  // line-aligned walks (SlotTable::shift) per operation
-  // line-aligned walks: 0 off, 1 cut at lines of the arena read, 2 (pack
-  // only) cut at lines of the payload written
-  int line_pack = 0, line_verify = 0, line_checksum = 0;
+  // line-aligned walks (SlotTable::shift) per operation: 0 off, 1 cut at
+  // lines of the arena read, 2 (pack) at lines of the payload, 3 (pack,
+  // unpack) at slice boundaries of the payload
+  int line_pack = 0, line_unpack = 0, line_verify = 0, line_checksum = 0;
+  // line-aligned walks whose units' last slice absorbs the lead
+  int absorb_pack = 0, absorb_unpack = 0, absorb_verify = 0, absorb_checksum = 0;
 };
 
 // Device scratch owned by a plan: per-chunk accumulators (G per chunk, see
@@ -199,14 +211,19 @@ struct UnpackDeltaArgs {
   const uint32_t* bad = nullptr;   // per list position: 1 = flag it whatever its sums
 };
 
-// Device tables of a plan for lists of chunks built on the device.
-struct DeltaTables {
-  const fr_tensor_desc* desc;   // the tensor table
-  const uint64_t* chunk_base;   // n_entries + 1: prefix of the entries' chunk counts
-  uint32_t n_entries;
-  uint64_t C;
-  uint64_t seg;                 // payload segment alignment A
+// Where a chunk lives, for lists of chunks built on the device: one record
+// per chunk id, so that a lane finds everything about its chunk with one load.
+constexpr uint32_t kLocDerived = 1;  // a bf16 parameter re-derived from its master
+constexpr uint32_t kLocFirst = 2;    // the first chunk of its entry
+constexpr uint32_t kLocLast = 4;     // the last chunk of its entry
+struct alignas(16) ChunkLoc {
+  uint64_t src_off;    // in the sender / replica arena
+  uint64_t dst_off;    // in the receiver arena
+  uint64_t m_dst_off;  // derived: receiver offset of the master bytes it is rounded from
+  uint32_t len;        // bytes
+  uint32_t flags;      // kLoc*
 };
+static_assert(sizeof(ChunkLoc) == 32, "ChunkLoc is 32 bytes");
 
 // Scan element of a delta list: the map x -> x + q (has = 0) or
 // x -> align_A(x + p) + q (has = 1) of the payload end over some chunks,
@@ -215,20 +232,23 @@ struct DeltaAgg {
   uint32_t ns, nd, has, pad_;
   uint64_t p, q;
 };
-// Before a bitmap word: the payload end and the counts.
+// Before a block of chunks: the payload end and the counts.
 struct DeltaPre {
   uint64_t end;
   uint32_t ns, nd;
 };
 // Totals of a list built on the device (plan-owned device words).
 enum DeltaCount { kDeltaIds = 0, kDeltaSent = 1, kDeltaDerived = 2, kDeltaEnd = 3 };
+// Chunks per block of the list builder (one lane each).
+constexpr uint32_t kListBlock = 256;
 
 struct DeltaBuild {
-  DeltaTables t;
+  const ChunkLoc* loc;       // per chunk id
   const uint32_t* bits;      // the list: bit c set = chunk c listed
   uint64_t n_chunks;         // the plan's chunks (bits past them are ignored)
-  DeltaAgg* agg;             // per bitmap word
-  DeltaPre* pre;             // per bitmap word
+  uint64_t seg;              // payload segment alignment A
+  DeltaAgg* agg;             // per block of kListBlock chunks
+  DeltaPre* pre;             // per block
   uint64_t* counts;          // [kDeltaIds, kDeltaSent, kDeltaDerived, kDeltaEnd]
   uint64_t* user_counts;     // NULL or the caller's [list length, payload bytes]
   SrcUnit* src_units;        // pack: one per listed chunk, list order
@@ -236,6 +256,9 @@ struct DeltaBuild {
   DerivedUnit* derived;      // unpack: derived chunks (re-derived from the receiver's masters)
   uint32_t* bad;             // unpack: per list position, 1 = beyond the readable payload
   uint64_t payload_limit;    // pack: payload capacity; unpack: readable payload bytes
+  fr_chunk_sum* acc;         // accumulators of the operation, cleared per listed position
+  uint32_t acc_shift;        // log2 of the accumulators per list position
+  uint64_t* zero_word;       // NULL, or a counter the operation starts from 0 (n_bad)
 };
 
 // Bytes of one slice for a tile, and the accumulators a chunk of C bytes
@@ -249,9 +272,11 @@ uint64_t accumulators_per_chunk(uint64_t C, int tile);
 
 // The line-aligned mode an operation with this tile and line setting walks
 // in: the setting when some chunk starts inside a line of the side it keys
-// on and a slice spans at least two lines, else 0 (the plain walk is then
-// the same thing).
-inline uint32_t line_walk(const fr_plan* p, int tile, int line);
+// on (mode 1: the arena the operation reads, or with `receiver` unpack's
+// receiver arena) and a slice spans at least two lines, else 0 (the plain
+// walk is then the same thing).
+inline uint32_t line_walk(const fr_plan* p, int tile, int line, bool receiver = false);
+inline uint32_t lead_bytes(uint32_t lead, uint32_t plead, uint32_t line, uint32_t sl);
 
 // Kernel launchers (kernels.hip).  They assume validated arguments, enqueue
 // on `stream` and return the hipError_t of the launches as an int.
@@ -270,7 +295,9 @@ int launch_verify(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunk
                   fr_chunk_sum* sums_a, fr_chunk_sum* sums_b, const Scratch& scr,
                   const LaunchCfg& cfg, void* stream);
 // The unit records of a delta list given as a bitmap, built on the device:
-// pack's SrcUnit list, or unpack's plain and derived lists, and the counts.
+// pack's SrcUnit list, or unpack's plain and derived lists, and the counts;
+// it also clears the accumulators of the listed positions and *zero_word,
+// so the operation's own launches need not.
 int launch_delta_build(const DeltaBuild& b, bool for_pack, void* stream);
 // bits[0 .. words) <- the bitmap of ids[0 .. n) (ids < 32 * words).
 int launch_ids_to_bits(const uint32_t* ids, uint64_t n, uint32_t* bits, uint64_t words,
@@ -300,8 +327,9 @@ struct fr_plan {
     fr::SlotTable t{};  // t.shift: the line-aligned mode (0 off, 1 arena lines, 2 payload lines)
     uint64_t* mem = nullptr;
   };
-  bool any_lead = false;             // some chunk starts inside a cache line
-  bool any_plead = false;            // some chunk starts inside a payload line
+  uint32_t dst_align = fr::kLeadMod;     // the same for every plain unpack chunk's receiver offset
+  uint32_t src_align = fr::kLeadMod;   // largest power of two (<= kLeadMod) dividing every chunk's src_off
+  uint32_t pay_align = fr::kLeadMod;   // the same for every sent chunk's payload offset
   std::vector<Walk> src_walks;
   Walk unpack_walk;
   fr::DerivedUnit* d_derived = nullptr;  // unpack units: derived groups
@@ -311,7 +339,7 @@ struct fr_plan {
   void* d_scratch = nullptr;         // one allocation holding `scratch`
   // Delta lists, built on the device (one allocation, carved at creation):
   void* d_delta = nullptr;
-  fr::DeltaTables delta_tables{};     // the table and chunk bases
+  fr::ChunkLoc* d_delta_loc = nullptr;  // per chunk id
   fr::SrcUnit* d_delta_src = nullptr; // pack records; shares its bytes with the two below
   fr::PlainUnit* d_delta_plain = nullptr;
   fr::DerivedUnit* d_delta_derived = nullptr;
@@ -326,7 +354,15 @@ struct fr_plan {
   fr::LaunchCfg cfg{};
 };
 
-inline uint32_t fr::line_walk(const fr_plan* p, int tile, int line) {
-  const bool some = line == 1 ? p->any_lead : line == 2 ? p->any_plead : false;
-  return some && slice_bytes(p->layout.C, tile) >= 2 * kLine ? uint32_t(line) : 0u;
+inline uint32_t fr::line_walk(const fr_plan* p, int tile, int line, bool receiver) {
+  const uint32_t sl = slice_bytes(p->layout.C, tile);
+  const uint32_t grain = line == 1 || line == 2 ? kLine : line == 3 ? sl : 0;
+  const uint32_t align = line == 1 ? (receiver ? p->dst_align : p->src_align) : p->pay_align;
+  return grain && align < grain && sl >= 2 * kLine ? uint32_t(line) : 0u;
+}
+
+// Bytes a walk of mode `line` starts a unit early: its offset into a line,
+// or into a slice of `sl` bytes (mode 3); 0 for a plain walk.
+inline uint32_t fr::lead_bytes(uint32_t lead, uint32_t plead, uint32_t line, uint32_t sl) {
+  return line == 1 ? lead % kLine : line == 2 ? plead % kLine : line == 3 ? plead % sl : 0u;
 }

@@ -184,6 +184,7 @@ struct Walk {
   uint32_t spc_shift; // log2(SPC), slices per chunk
   uint32_t g_shift;   // log2(G), accumulators per chunk
   uint32_t line;      // line-aligned walk: 1 at arena lines, 2 at payload lines (SlotTable::shift)
+  uint32_t absorb;    // line-aligned walk: the last slice of a unit takes its leftover lead
   const u64* count;   // implicit walk of a list built on the device: its number of units
 };
 
@@ -196,9 +197,15 @@ __device__ __forceinline__ u64 walk_slices(const Walk& wk) {
   return n < wk.n_slices ? n : wk.n_slices;
 }
 
-// Vectors a line-aligned walk starts a unit's slices early (0 for a plain walk).
-__device__ __forceinline__ uint32_t lead_vectors(const Walk& wk, const SrcUnit& r) {
-  return wk.line == 1 ? uint32_t(r.lead) >> 4 : wk.line == 2 ? uint32_t(r.plead) >> 4 : 0u;
+// Vectors a line-aligned walk starts a unit's slices early (0 for a plain
+// walk): the unit's offset into a line of the arena (mode 1) or of the
+// payload (2), or into a slice of the payload (3).
+__device__ __forceinline__ uint32_t lead_vectors(const Walk& wk, uint32_t lead, uint32_t plead) {
+  const uint32_t b = wk.line == 1   ? lead % kLine
+                     : wk.line == 2 ? plead % kLine
+                     : wk.line == 3 ? plead & ((wk.sl_vec << 4) - 1)
+                                    : 0u;
+  return b >> 4;
 }
 
 // Slot of workgroup id g: (unit << 32) | j.
@@ -238,9 +245,15 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
     // First vector of the slice; a line-aligned walk starts it lead_v
     // vectors early (the first slice's leading lanes then come before the
     // chunk: their unsigned index wraps past nvec and they do nothing).
-    const uint32_t lead_v = lead_vectors(wk, r);
+    const uint32_t lead_v = lead_vectors(wk, r.lead, r.plead);
     const uint32_t v0 = j * wk.sl_vec - lead_v;
     if (j * wk.sl_vec >= endv + lead_v) continue;  // guard: no listed slot is empty
+    // Vectors of the slice: a whole slice, except that a walk that absorbs
+    // the lead gives the chunk's last slice everything up to its end (up to
+    // lead_v vectors more than a slice) instead of one more, nearly empty,
+    // slice.
+    const bool last = (j + 1) * wk.sl_vec >= endv + (wk.absorb ? 0u : lead_v);
+    const uint32_t n = last && wk.absorb ? endv - v0 : wk.sl_vec;
     const u32x4* s = reinterpret_cast<const u32x4*>(src + r.src_off);
     const bool store = kStore && r.pay_off != kNoPayload;
     u32x4* d = reinterpret_cast<u32x4*>(payload + (store ? r.pay_off : 0));
@@ -259,14 +272,22 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
         if (store) st_nt(x[q], d + v);
       }
     }
-    if (tail && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
+    for (uint32_t l = wk.sl_vec + threadIdx.x; l < n; l += B) {  // an absorbing last slice
+      const uint32_t v = v0 + l;
+      if (v < nvec) {
+        const u32x4 y = ld_nt(s + v);
+        acc4(y, 4 * v, acc[0], acc[1]);
+        if (store) st_nt(y, d + v);
+      }
+    }
+    if (tail && nvec - v0 < n && threadIdx.x == (nvec - v0) % B) {
       const u32x4 t = load_tail(reinterpret_cast<const uint8_t*>(s + nvec), tail);
       acc4(t, 4 * nvec, acc[0], acc[1]);
       if (store) d[nvec] = t;  // the segment's zero padding is written with it
     }
     // The chunk's last slice zero-fills the gap up to the next payload
     // segment (fewer than segment alignment / 16 vectors).
-    if (store && r.gap_v && (j + 1) * wk.sl_vec >= endv + lead_v) {
+    if (store && r.gap_v && last) {
       for (uint32_t v = endv + threadIdx.x; v < endv + r.gap_v; v += B)
         st_nt(u32x4{0, 0, 0, 0}, d + v);
     }
@@ -349,14 +370,21 @@ __device__ __forceinline__ bool derived_slice(const DerivedUnit& r, uint32_t j, 
   return true;
 }
 
-// One slice of a plain chunk: copy, and sum the bytes as written.
+// One slice of a plain chunk: copy, and sum the bytes as written.  A walk
+// cut at slice boundaries of the payload (mode 3) starts the chunk's slices
+// lead_v vectors early (the first slice's leading lanes then come before the
+// chunk: their unsigned index wraps past nvec and they do nothing).
 template <int B, int U>
 __device__ __forceinline__ bool plain_slice(const PlainUnit& r, uint32_t j, const Walk& wk,
                                             const uint8_t* payload, uint8_t* dst,
                                             u64 (&acc)[2]) {
-  const uint32_t nvec = r.len >> 4, tail = r.len & 15;
-  const uint32_t v0 = j * wk.sl_vec;
-  if (v0 > nvec || (v0 == nvec && tail == 0)) return false;
+  const uint32_t nvec = r.len >> 4, tail = r.len & 15, endv = nvec + (tail ? 1u : 0u);
+  const uint32_t lead_v = lead_vectors(wk, r.dlead, r.plead);
+  if (j * wk.sl_vec >= endv + lead_v) return false;
+  const uint32_t v0 = j * wk.sl_vec - lead_v;
+  // as in k_pack: an absorbing walk's last slice runs to the chunk's end
+  const bool last = (j + 1) * wk.sl_vec >= endv + (wk.absorb ? 0u : lead_v);
+  const uint32_t n = last && wk.absorb ? endv - v0 : wk.sl_vec;
   const u32x4* s = reinterpret_cast<const u32x4*>(payload + r.pay_off);
   u32x4* d = reinterpret_cast<u32x4*>(dst + r.dst_off);
   u32x4 x[U];
@@ -373,7 +401,15 @@ __device__ __forceinline__ bool plain_slice(const PlainUnit& r, uint32_t j, cons
       acc4(x[q], 4 * v, acc[0], acc[1]);
     }
   }
-  if (tail && nvec >= v0 && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
+  for (uint32_t l = wk.sl_vec + threadIdx.x; l < n; l += B) {  // an absorbing last slice
+    const uint32_t v = v0 + l;
+    if (v < nvec) {
+      const u32x4 y = ld_nt(s + v);
+      st_nt(y, d + v);
+      acc4(y, 4 * v, acc[0], acc[1]);
+    }
+  }
+  if (tail && nvec - v0 < n && threadIdx.x == (nvec - v0) % B) {
     // The payload segment is padded to 16 bytes, so the whole vector is
     // readable; only the entry's bytes are written and summed.
     const u32x4 t = mask_tail(s[nvec], tail);
@@ -419,8 +455,7 @@ __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ de
       if (!plain_slice<B, U>(r, j, wk, payload, dst, acc)) continue;
       block_sum<B, 2>(acc, lds2, parity);
       parity ^= 1;
-      if (threadIdx.x == 0)
-        add_sum(acc_out + ((u64(r.c) << wk.g_shift) + (j >> kAccSlicesShift)), acc[0], acc[1]);
+      if (threadIdx.x == 0) add_sum(acc_out + acc_index(wk, r.c, j), acc[0], acc[1]);
     }
   }
 }
@@ -468,9 +503,12 @@ __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units,
     const SrcUnit r = units[e >> 32];
     const uint32_t c = r.c, j = uint32_t(e);
     const uint32_t nvec = r.len >> 4, tail = r.len & 15;
-    const uint32_t lead_v = lead_vectors(wk, r);  // as in k_pack
+    const uint32_t endv = nvec + (tail ? 1u : 0u);
+    const uint32_t lead_v = lead_vectors(wk, r.lead, r.plead);  // as in k_pack
     const uint32_t v0 = j * wk.sl_vec - lead_v;
-    if (j * wk.sl_vec >= nvec + (tail ? 1u : 0u) + lead_v) continue;
+    if (j * wk.sl_vec >= endv + lead_v) continue;
+    const bool last = (j + 1) * wk.sl_vec >= endv + (wk.absorb ? 0u : lead_v);
+    const uint32_t n = last && wk.absorb ? endv - v0 : wk.sl_vec;
     const u32x4* pa = reinterpret_cast<const u32x4*>(a + r.src_off);
     const u32x4* pb = reinterpret_cast<const u32x4*>(b + r.src_off);
     u64 acc[4] = {0, 0, 0, 0};
@@ -496,7 +534,19 @@ __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units,
         }
       }
     }
-    if (tail && nvec - v0 < wk.sl_vec && threadIdx.x == (nvec - v0) % B) {
+    for (uint32_t l = wk.sl_vec + threadIdx.x; l < n; l += B) {  // an absorbing last slice
+      const uint32_t v = v0 + l;
+      if (v < nvec) {
+        const u32x4 ya = ld_nt(pa + v), yb = ld_nt(pb + v);
+        const u32x4 x = ya ^ yb;
+        diff |= x.x | x.y | x.z | x.w;
+        if (kSums) {
+          acc4(ya, 4 * v, acc[0], acc[1]);
+          acc4(yb, 4 * v, acc[2], acc[3]);
+        }
+      }
+    }
+    if (tail && nvec - v0 < n && threadIdx.x == (nvec - v0) % B) {
       const u32x4 ta = load_tail(reinterpret_cast<const uint8_t*>(pa + nvec), tail);
       const u32x4 tb = load_tail(reinterpret_cast<const uint8_t*>(pb + nvec), tail);
       const u32x4 x = ta ^ tb;
@@ -618,17 +668,18 @@ __global__ __launch_bounds__(kFinalThreads) void k_finalize(FinalArgs f) {
 // running payload end x as x -> x + len (continuing) or x -> align_A(x) +
 // len, and such maps compose within the family {x -> x + q} u
 // {x -> align_A(x + p) + q}, because align_A(align_A(z) + w) = align_A(z) +
-// align_A(w) for w >= 0.  So:
-//   k_delta_agg   one thread per bitmap word: the composed map of the word's
-//                 sent chunks and its counts of sent and derived chunks;
-//   k_delta_scan  one workgroup: composes the words' maps in order, giving
-//                 each word the payload end and the counts before it, and
-//                 the totals;
-//   k_delta_build one thread per word: places its chunks and writes their
-//                 unit records (pack: one per listed chunk in list order;
-//                 unpack: sent and derived chunks in two lists).
+// align_A(w) for w >= 0: a prefix scan over the chunks places them all.
+// One lane per chunk id, blocks of kListBlock ids:
+//   k_list_blocks  each block's composed map and counts (a scan over its
+//                  lanes with cross-lane shuffles, then LDS over its waves);
+//   k_list_scan    one workgroup: every block's payload end and counts
+//                  before it, and the totals;
+//   k_list_build   each lane places its chunk from its block's start and the
+//                  scan within the block, and writes its unit records.
 
 __device__ __forceinline__ u64 align_a(u64 x, u64 a) { return (x + a - 1) & ~(a - 1); }
+
+__device__ __forceinline__ DeltaAgg delta_identity() { return DeltaAgg{0, 0, 0, 0, 0, 0}; }
 
 // g after f.
 __device__ __forceinline__ DeltaAgg delta_then(const DeltaAgg& f, const DeltaAgg& g, u64 A) {
@@ -656,117 +707,109 @@ __device__ __forceinline__ u64 delta_apply(const DeltaAgg& f, u64 x, u64 A) {
   return f.has ? align_a(x + f.p, A) + f.q : x + f.q;
 }
 
-// Listed chunks of bitmap word w (bits past the last chunk cleared).
-__device__ __forceinline__ uint32_t listed_bits(const uint32_t* bits, u64 w, u64 n_chunks) {
-  const u64 c0 = w * 32;
-  const uint32_t b = bits[w];
-  return n_chunks - c0 >= 32 ? b : b & ((1u << uint32_t(n_chunks - c0)) - 1u);
+__device__ __forceinline__ DeltaAgg shfl_up_agg(const DeltaAgg& a, uint32_t d) {
+  DeltaAgg o;
+  o.ns = uint32_t(__shfl_up(int(a.ns), d, 64));
+  o.nd = uint32_t(__shfl_up(int(a.nd), d, 64));
+  o.has = uint32_t(__shfl_up(int(a.has), d, 64));
+  o.pad_ = 0;
+  o.p = u64(__shfl_up((long long)a.p, d, 64));
+  o.q = u64(__shfl_up((long long)a.q, d, 64));
+  return o;
 }
 
 __device__ __forceinline__ bool listed(const uint32_t* bits, u64 c, u64 n_chunks) {
   return c < n_chunks && ((bits[c >> 5] >> (c & 31)) & 1u);
 }
 
-// The entry holding chunk c: the last k with chunk_base[k] <= c (empty
-// entries share their chunk_base with the next one).
-__device__ __forceinline__ uint32_t entry_of_chunk(const DeltaTables& t, u64 c) {
-  uint32_t lo = 0, hi = t.n_entries;  // chunk_base[lo] <= c < chunk_base[hi]
-  while (hi - lo > 1) {
-    const uint32_t mid = lo + (hi - lo) / 2;
-    if (t.chunk_base[mid] <= c) lo = mid;
-    else hi = mid;
-  }
-  return lo;
-}
-
-// Chunk c of entry e, as the walk of a word meets it.
-struct ListedChunk {
-  u64 j;         // index within the entry
-  uint32_t len;  // bytes
-  bool derived;  // a bf16 parameter re-derived from its master: sends nothing
-  bool cont;     // sent, and continues the previous listed chunk of its entry
-  bool next_cont;// sent, and the next chunk of its entry is listed (it continues this one)
+// Lane c's chunk: its element of the scan and its location (valid if listed).
+struct ListLane {
+  bool on;        // listed
+  bool cont;      // sent, continuing the previous listed chunk of its entry
+  bool next_cont; // sent, and the next chunk of its entry is listed
+  ChunkLoc loc;
+  DeltaAgg e;
 };
 
-__device__ __forceinline__ ListedChunk listed_chunk(const DeltaTables& t, const uint32_t* bits,
-                                                    u64 n_chunks, uint32_t e, u64 c) {
-  const fr_tensor_desc& d = t.desc[e];
-  const u64 nb = d.numel * (d.dtype == FR_F32 ? 4u : 2u);
-  ListedChunk k;
-  k.j = c - t.chunk_base[e];
-  const u64 rest = nb - k.j * t.C;
-  k.len = uint32_t(rest < t.C ? rest : t.C);
-  k.derived = d.derive_from >= 0;
-  const u64 nch = t.chunk_base[e + 1] - t.chunk_base[e];
-  k.cont = !k.derived && k.j > 0 && listed(bits, c - 1, n_chunks);
-  k.next_cont = !k.derived && k.j + 1 < nch && listed(bits, c + 1, n_chunks);
-  return k;
-}
-
-// Calls fn(c, e) for the listed chunks of word w in increasing order.
-template <typename Fn>
-__device__ __forceinline__ void for_listed(const DeltaBuild& b, u64 w, Fn fn) {
-  uint32_t m = listed_bits(b.bits, w, b.n_chunks);
-  if (!m) return;
-  uint32_t e = entry_of_chunk(b.t, w * 32 + __builtin_ctz(m));
-  while (m) {
-    const u64 c = w * 32 + __builtin_ctz(m);
-    m &= m - 1;
-    while (b.t.chunk_base[e + 1] <= c) e++;
-    fn(c, e);
+__device__ __forceinline__ ListLane list_lane(const DeltaBuild& b, u64 c) {
+  ListLane l;
+  l.on = listed(b.bits, c, b.n_chunks);
+  l.cont = l.next_cont = false;
+  l.e = delta_identity();
+  if (!l.on) return l;
+  l.loc = b.loc[c];
+  if (l.loc.flags & kLocDerived) {
+    l.e.nd = 1;
+    return l;
   }
+  l.cont = !(l.loc.flags & kLocFirst) && listed(b.bits, c - 1, b.n_chunks);
+  l.next_cont = !(l.loc.flags & kLocLast) && listed(b.bits, c + 1, b.n_chunks);
+  l.e.ns = 1;
+  l.e.has = l.cont ? 0u : 1u;
+  l.e.q = l.loc.len;
+  return l;
 }
 
-__global__ __launch_bounds__(256) void k_delta_agg(DeltaBuild b, u64 n_words) {
-  const u64 w = u64(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (w >= n_words) return;
-  DeltaAgg a{0, 0, 0, 0, 0, 0};
-  for_listed(b, w, [&](u64 c, uint32_t e) {
-    const ListedChunk k = listed_chunk(b.t, b.bits, b.n_chunks, e, c);
-    if (k.derived) {
-      a.nd++;
-      return;
-    }
-    const DeltaAgg one{1, 0, k.cont ? 0u : 1u, 0, 0, k.len};
-    a = delta_then(a, one, b.t.seg);
-  });
-  b.agg[w] = a;
+// Scan of `e` over the kThreads lanes of a workgroup (cross-lane shuffles
+// within each wave, then the wave totals through LDS): `excl` receives the
+// lane's exclusive prefix, and the return value is the workgroup's total.
+// Every lane must call it.
+template <int kThreads>
+__device__ __forceinline__ DeltaAgg block_scan(DeltaAgg e, u64 A, DeltaAgg& excl) {
+  __shared__ DeltaAgg wave_total[kThreads / 64];
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  DeltaAgg inc = e;
+  for (uint32_t d = 1; d < 64; d <<= 1) {
+    const DeltaAgg o = shfl_up_agg(inc, d);
+    if (lane >= d) inc = delta_then(o, inc, A);
+  }
+  if (lane == 63) wave_total[wave] = inc;
+  // every lane takes part in the shuffle (a lane reading an inactive lane
+  // gets nothing), lane 0 then drops what it read
+  const DeltaAgg prev = shfl_up_agg(inc, 1);
+  const DeltaAgg wexcl = lane ? prev : delta_identity();
+  __syncthreads();
+  DeltaAgg before = delta_identity();  // the waves before this one
+  for (uint32_t w = 0; w < wave; w++) before = delta_then(before, wave_total[w], A);
+  excl = delta_then(before, wexcl, A);
+  DeltaAgg total = before;
+  for (uint32_t w = wave; w < kThreads / 64; w++) total = delta_then(total, wave_total[w], A);
+  return total;
+}
+
+__global__ __launch_bounds__(kListBlock) void k_list_blocks(DeltaBuild b) {
+  const u64 c = u64(blockIdx.x) * kListBlock + threadIdx.x;
+  const ListLane l = list_lane(b, c);
+  DeltaAgg excl;
+  const DeltaAgg total = block_scan<kListBlock>(l.e, b.seg, excl);
+  if (threadIdx.x == 0) b.agg[blockIdx.x] = total;
 }
 
 constexpr int kScanThreads = 1024;
 
-// Thread i composes words [i k, (i + 1) k); an inclusive scan of the
-// threads' maps through LDS gives each thread the map of everything before
-// its words; it then walks its words again with the running payload end.
-__global__ __launch_bounds__(kScanThreads) void k_delta_scan(DeltaBuild b, u64 n_words) {
-  __shared__ DeltaAgg lds[kScanThreads];
+// Thread i composes blocks [i k, (i + 1) k); a scan over the threads gives
+// each thread the map of everything before its blocks; it then walks its
+// blocks again with the running payload end.
+__global__ __launch_bounds__(kScanThreads) void k_list_scan(DeltaBuild b, u64 n_blocks) {
   const uint32_t i = threadIdx.x;
-  const u64 k = (n_words + kScanThreads - 1) / kScanThreads;
-  const u64 w0 = u64(i) * k < n_words ? u64(i) * k : n_words;
-  const u64 w1 = w0 + k < n_words ? w0 + k : n_words;
-  const u64 A = b.t.seg;
-  DeltaAgg a{0, 0, 0, 0, 0, 0};
+  const u64 k = (n_blocks + kScanThreads - 1) / kScanThreads;
+  const u64 w0 = u64(i) * k < n_blocks ? u64(i) * k : n_blocks;
+  const u64 w1 = w0 + k < n_blocks ? w0 + k : n_blocks;
+  const u64 A = b.seg;
+  DeltaAgg a = delta_identity();
   for (u64 w = w0; w < w1; w++) a = delta_then(a, b.agg[w], A);
-  lds[i] = a;
-  __syncthreads();
-  for (uint32_t d = 1; d < kScanThreads; d <<= 1) {
-    const DeltaAgg x = i >= d ? delta_then(lds[i - d], lds[i], A) : lds[i];
-    __syncthreads();
-    lds[i] = x;
-    __syncthreads();
-  }
-  const DeltaAgg before = i ? lds[i - 1] : DeltaAgg{0, 0, 0, 0, 0, 0};
+  DeltaAgg before;
+  const DeltaAgg all = block_scan<kScanThreads>(a, A, before);
   u64 x = delta_apply(before, 0, A);
   uint32_t ns = before.ns, nd = before.nd;
   for (u64 w = w0; w < w1; w++) {
     b.pre[w] = DeltaPre{x, ns, nd};
-    const DeltaAgg& g = b.agg[w];
+    const DeltaAgg g = b.agg[w];
     x = delta_apply(g, x, A);
     ns += g.ns;
     nd += g.nd;
   }
-  if (i == kScanThreads - 1) {
-    const DeltaAgg& all = lds[kScanThreads - 1];
+  if (i == 0) {
     const u64 end = delta_apply(all, 0, A);
     b.counts[kDeltaIds] = u64(all.ns) + all.nd;
     b.counts[kDeltaSent] = all.ns;
@@ -776,53 +819,53 @@ __global__ __launch_bounds__(kScanThreads) void k_delta_scan(DeltaBuild b, u64 n
       b.user_counts[0] = u64(all.ns) + all.nd;
       b.user_counts[1] = align_a(end, 16);
     }
+    if (b.zero_word) *b.zero_word = 0;
   }
 }
 
 template <bool kForPack>
-__global__ __launch_bounds__(256) void k_delta_build(DeltaBuild b, u64 n_words) {
-  const u64 w = u64(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (w >= n_words) return;
-  const DeltaPre pre = b.pre[w];
-  const u64 A = b.t.seg, total_end = b.counts[kDeltaEnd];
-  u64 x = pre.end;
-  uint32_t ns = pre.ns, nd = pre.nd;
-  for_listed(b, w, [&](u64 c, uint32_t e) {
-    const ListedChunk k = listed_chunk(b.t, b.bits, b.n_chunks, e, c);
-    const fr_tensor_desc& d = b.t.desc[e];
-    const uint32_t pos = ns + nd;  // list position
-    const u64 src_off = d.src_offset + k.j * b.t.C, dst_off = d.dst_offset + k.j * b.t.C;
-    if (k.derived) {
-      if (kForPack) {
-        b.src_units[pos] = SrcUnit{src_off, kNoPayload, k.len, pos, 0, uint16_t(src_off % kLine), 0};
-      } else {
-        // re-derived from the receiver's own master bytes of this chunk
-        const u64 m_dst = b.t.desc[d.derive_from].dst_offset + 2 * k.j * b.t.C;
-        b.derived[nd] = DerivedUnit{m_dst, m_dst, dst_off, k.len, 0, pos, 0};
-        b.bad[pos] = 0;
-      }
-      nd++;
-      return;
-    }
-    const u64 pay = k.cont ? x : align_a(x, A);
-    const u64 end = pay + k.len;
-    x = end;
+__global__ __launch_bounds__(kListBlock) void k_list_build(DeltaBuild b) {
+  const u64 c = u64(blockIdx.x) * kListBlock + threadIdx.x;
+  const ListLane l = list_lane(b, c);
+  DeltaAgg excl;
+  (void)block_scan<kListBlock>(l.e, b.seg, excl);
+  if (!l.on) return;
+  const DeltaPre pre = b.pre[blockIdx.x];
+  const u64 A = b.seg;
+  const uint32_t pos = pre.ns + pre.nd + excl.ns + excl.nd;  // list position
+  for (uint32_t a = 0; a < (1u << b.acc_shift); a++)
+    b.acc[(u64(pos) << b.acc_shift) + a] = fr_chunk_sum{0, 0};
+  const ChunkLoc& r = l.loc;
+  if (r.flags & kLocDerived) {
     if (kForPack) {
-      // zero gap up to the next sent chunk: none after the last one or before
-      // a continuing one, else up to the next segment boundary
-      const u64 gap = (end == total_end || k.next_cont) ? 0 : align_a(end, A) - align_a(end, 16);
-      const bool fits = align_a(end, 16) + gap <= b.payload_limit;  // never false for a checked cap
-      b.src_units[pos] = SrcUnit{src_off, fits ? pay : kNoPayload, k.len, pos,
-                                 fits ? uint32_t(gap >> 4) : 0u, uint16_t(src_off % kLine),
-                                 uint16_t(pay % kLine)};
+      b.src_units[pos] = SrcUnit{r.src_off, kNoPayload, r.len, pos, 0, uint16_t(r.src_off % kLeadMod), 0};
     } else {
-      // a chunk past the readable payload is neither read nor written, and flagged
-      const bool readable = align_a(end, 16) <= b.payload_limit;
-      b.plain[ns] = PlainUnit{readable ? pay : 0, dst_off, readable ? k.len : 0u, pos, 0};
-      b.bad[pos] = readable ? 0u : 1u;
+      // re-derived from the receiver's own master bytes of this chunk
+      b.derived[pre.nd + excl.nd] = DerivedUnit{r.m_dst_off, r.m_dst_off, r.dst_off, r.len, 0, pos, 0};
+      b.bad[pos] = 0;
     }
-    ns++;
-  });
+    return;
+  }
+  const u64 x = delta_apply(excl, pre.end, A);  // the payload end before this chunk
+  const u64 pay = l.cont ? x : align_a(x, A);
+  const u64 end = pay + r.len;
+  if (kForPack) {
+    // zero gap up to the next sent chunk: none after the last one or before
+    // a continuing one, else up to the next segment boundary
+    const u64 gap =
+        (end == b.counts[kDeltaEnd] || l.next_cont) ? 0 : align_a(end, A) - align_a(end, 16);
+    const bool fits = align_a(end, 16) + gap <= b.payload_limit;  // never false for a checked cap
+    b.src_units[pos] = SrcUnit{r.src_off, fits ? pay : kNoPayload, r.len, pos,
+                               fits ? uint32_t(gap >> 4) : 0u, uint16_t(r.src_off % kLeadMod),
+                               uint16_t(pay % kLeadMod)};
+  } else {
+    // a chunk past the readable payload is neither read nor written, and flagged
+    const bool readable = align_a(end, 16) <= b.payload_limit;
+    b.plain[pre.ns + excl.ns] =
+        PlainUnit{readable ? pay : 0, r.dst_off, readable ? r.len : 0u, pos, uint32_t(pay % kLeadMod),
+                  uint32_t(r.dst_off % kLeadMod)};
+    b.bad[pos] = readable ? 0u : 1u;
+  }
 }
 
 __global__ __launch_bounds__(256) void k_ids_to_bits(const uint32_t* __restrict__ ids, u64 n,
@@ -926,6 +969,7 @@ inline Walk walk_for(uint64_t C, uint32_t tile_bytes, const SlotTable& t) {
   w.imp_shift = t.implicit_shift;
   w.sl_vec = uint32_t(sl >> 4);
   w.line = t.shift;
+  w.absorb = t.absorb;
   w.count = reinterpret_cast<const u64*>(t.count);
   w.spc_shift = sh;
   w.g_shift = sh > kAccSlicesShift ? sh - kAccSlicesShift : 0;
@@ -957,7 +1001,8 @@ int pack_impl(bool store, const SrcUnit* units, const SlotTable& slots, uint32_t
   const Walk wk = walk_for(C, B * U * 16, slots);
   const u64 n_acc = u64(n_chunks) << wk.g_shift;
   Zeroes z;
-  z.add(scr.acc, n_acc * sizeof(fr_chunk_sum));
+  if (!wk.count)  // a list built on the device: its builder cleared the accumulators
+    z.add(scr.acc, n_acc * sizeof(fr_chunk_sum));
   int e = z.launch(st);
   if (e) return e;
   const auto* s = static_cast<const uint8_t*>(src);
@@ -1012,8 +1057,10 @@ int unpack_delta_impl(const UnpackDeltaArgs& u, const LaunchCfg& cfg, hipStream_
   const Walk wp = walk_for(u.C, B * U * 16, u.plain_slots);
   const u64 n_acc = u64(u.n_ids) << wp.g_shift;
   Zeroes z;
-  z.add(u.scratch.acc, n_acc * sizeof(fr_chunk_sum));
-  z.add(u.n_bad, 8);
+  if (!u.live) {  // else the list's builder cleared the accumulators and n_bad
+    z.add(u.scratch.acc, n_acc * sizeof(fr_chunk_sum));
+    z.add(u.n_bad, 8);
+  }
   int e = z.launch(st);
   if (e || u.n_ids == 0) return e;
   const uint32_t cvec = uint32_t(u.C >> 4);
@@ -1114,17 +1161,17 @@ int launch_expand_slots(const uint64_t* first, const uint64_t* base, uint64_t n_
 
 int launch_delta_build(const DeltaBuild& b, bool for_pack, void* stream) {
   const hipStream_t st = hipStream_t(stream);
-  const u64 n_words = (b.n_chunks + 31) / 32;
-  const dim3 grid(uint32_t((n_words + 255) / 256)), block(256);
-  if (n_words) {
-    hipLaunchKernelGGL(k_delta_agg, grid, block, 0, st, b, n_words);
+  const u64 n_blocks = (b.n_chunks + kListBlock - 1) / kListBlock;
+  const dim3 grid = dim3(uint32_t(n_blocks)), block = dim3(kListBlock);
+  if (n_blocks) {
+    hipLaunchKernelGGL(k_list_blocks, grid, block, 0, st, b);
     if (const hipError_t e = hipGetLastError()) return int(e);
   }
-  hipLaunchKernelGGL(k_delta_scan, dim3(1), dim3(kScanThreads), 0, st, b, n_words);
+  hipLaunchKernelGGL(k_list_scan, dim3(1), dim3(kScanThreads), 0, st, b, n_blocks);
   if (const hipError_t e = hipGetLastError()) return int(e);
-  if (n_words) {
-    if (for_pack) hipLaunchKernelGGL(k_delta_build<true>, grid, block, 0, st, b, n_words);
-    else hipLaunchKernelGGL(k_delta_build<false>, grid, block, 0, st, b, n_words);
+  if (n_blocks) {
+    if (for_pack) hipLaunchKernelGGL(k_list_build<true>, grid, block, 0, st, b);
+    else hipLaunchKernelGGL(k_list_build<false>, grid, block, 0, st, b);
   }
   return int(hipGetLastError());
 }

@@ -25,7 +25,12 @@ constexpr uint32_t kDefaultTilePack = 4, kDefaultTileUnpack = 5, kDefaultTileVer
                    kDefaultTileChecksum = 3;
 // Line-aligned walks (0 off, 1 at lines of the arena read, 2 at lines of the
 // payload written): pack cuts at payload lines, the compare at arena lines.
-constexpr int kDefaultLinePack = 2, kDefaultLineVerify = 1, kDefaultLineChecksum = 0;
+constexpr int kDefaultLinePack = 2, kDefaultLineUnpack = 1, kDefaultLineVerify = 1,
+              kDefaultLineChecksum = 0;
+// Whether a line-aligned pack / unpack walk lets a unit's last slice absorb
+// the lead instead of adding a slice.
+constexpr uint32_t kDefaultAbsorbPack = 1, kDefaultAbsorbUnpack = 1, kDefaultAbsorbVerify = 0,
+                   kDefaultAbsorbChecksum = 0;
 // Workgroups of a launch that walks a delta list built on the device (the
 // host knows only its largest possible length): 256 per CU.
 constexpr uint32_t kDefaultDeltaGrid = 65536;
@@ -263,16 +268,25 @@ LaunchCfg launch_config() {
   cfg.tile_unpack = pick("FLASHRESTORE_TILE_UNPACK", kDefaultTileUnpack);
   cfg.tile_verify = pick("FLASHRESTORE_TILE_VERIFY", kDefaultTileVerify);
   cfg.tile_checksum = pick("FLASHRESTORE_TILE_CHECKSUM", kDefaultTileChecksum);
-  // line-aligned walks: 0 off, 1 arena lines, 2 payload lines (pack only;
-  // elsewhere any nonzero value means 1); FLASHRESTORE_LINE sets all three
+  // line-aligned walks: 0 off, 1 lines of the arena read (for unpack: of the
+  // receiver arena written), 2 payload lines, 3 payload slices (pack takes
+  // 1-3, unpack 1-3; compare and checksum 0 or 1, any nonzero value
+  // meaning 1); FLASHRESTORE_LINE sets all four
   const uint32_t lall = env_u32("FLASHRESTORE_LINE", ~0u);
-  auto lpick = [&](const char* name, int dflt, bool payload_side) {
+  auto lpick = [&](const char* name, int dflt, uint32_t modes) {
     const uint32_t v = env_u32(name, lall != ~0u ? lall : uint32_t(dflt));
-    return v == 0 ? 0 : (v == 2 && payload_side) ? 2 : 1;
+    if (v == 0) return 0;
+    if (v < 4 && (modes >> v) & 1u) return int(v);
+    return (modes >> 1) & 1u ? 1 : 0;  // the operation's nearest mode
   };
-  cfg.line_pack = lpick("FLASHRESTORE_LINE_PACK", kDefaultLinePack, true);
-  cfg.line_verify = lpick("FLASHRESTORE_LINE_VERIFY", kDefaultLineVerify, false);
-  cfg.line_checksum = lpick("FLASHRESTORE_LINE_CHECKSUM", kDefaultLineChecksum, false);
+  cfg.line_pack = lpick("FLASHRESTORE_LINE_PACK", kDefaultLinePack, 0xE);
+  cfg.line_unpack = lpick("FLASHRESTORE_LINE_UNPACK", kDefaultLineUnpack, 0xE);
+  cfg.absorb_pack = int(env_u32("FLASHRESTORE_ABSORB_PACK", kDefaultAbsorbPack) != 0);
+  cfg.absorb_unpack = int(env_u32("FLASHRESTORE_ABSORB_UNPACK", kDefaultAbsorbUnpack) != 0);
+  cfg.absorb_verify = int(env_u32("FLASHRESTORE_ABSORB_VERIFY", kDefaultAbsorbVerify) != 0);
+  cfg.absorb_checksum = int(env_u32("FLASHRESTORE_ABSORB_CHECKSUM", kDefaultAbsorbChecksum) != 0);
+  cfg.line_verify = lpick("FLASHRESTORE_LINE_VERIFY", kDefaultLineVerify, 0x2);
+  cfg.line_checksum = lpick("FLASHRESTORE_LINE_CHECKSUM", kDefaultLineChecksum, 0x2);
   return cfg;
 }
 
@@ -297,21 +311,30 @@ std::vector<ChunkRec> chunk_records(const fr_tensor_desc* table, uint32_t n, con
   return recs;
 }
 
+// Largest power of two, at most kLeadMod, dividing x.
+uint32_t pow2_align(uint64_t x) {
+  uint32_t a = 1;
+  while (a < kLeadMod && x % (2 * a) == 0) a *= 2;
+  return a;
+}
+
 // Pack / checksum / compare units: every chunk, in chunk order.  The last
 // chunk of each sent entry zero-fills the payload gap up to the next one.
+// *src_align / *pay_align: the alignment every chunk's sender (payload)
+// offset has, up to kLeadMod.
 std::vector<SrcUnit> src_units(const std::vector<ChunkRec>& recs, uint32_t n, const Layout& L,
-                               bool* any_lead, bool* any_plead) {
+                               uint32_t* src_align, uint32_t* pay_align) {
   std::vector<SrcUnit> units(recs.size());
-  *any_lead = *any_plead = false;
+  *src_align = *pay_align = kLeadMod;
   for (uint64_t c = 0; c < recs.size(); c++) {
     units[c].src_off = recs[c].src_off;
     units[c].pay_off = recs[c].pay_off;
     units[c].len = recs[c].len;
     units[c].c = uint32_t(c);
-    units[c].lead = uint16_t(recs[c].src_off % kLine);
-    units[c].plead = recs[c].pay_off == kNoPayload ? 0 : uint16_t(recs[c].pay_off % kLine);
-    *any_lead = *any_lead || units[c].lead != 0;
-    *any_plead = *any_plead || units[c].plead != 0;
+    units[c].lead = uint16_t(recs[c].src_off % kLeadMod);
+    units[c].plead = recs[c].pay_off == kNoPayload ? 0 : uint16_t(recs[c].pay_off % kLeadMod);
+    *src_align = std::min(*src_align, pow2_align(recs[c].src_off));
+    if (recs[c].pay_off != kNoPayload) *pay_align = std::min(*pay_align, pow2_align(recs[c].pay_off));
   }
   for (uint32_t k = 0, prev = UINT32_MAX; k < n; k++) {
     if (L.pay_off[k] == kNoPayload || L.chunk_base[k + 1] == L.chunk_base[k]) continue;
@@ -352,6 +375,8 @@ void unpack_units(const fr_tensor_desc* table, uint32_t n, const Layout& L,
         u.dst_off = recs[c].dst_off;
         u.len = recs[c].len;
         u.c = uint32_t(c);
+        u.plead = uint32_t(recs[c].pay_off % kLeadMod);
+        u.dlead = uint32_t(recs[c].dst_off % kLeadMod);
         plain->push_back(u);
       }
     }
@@ -359,28 +384,34 @@ void unpack_units(const fr_tensor_desc* table, uint32_t n, const Layout& L,
 }
 
 // Walks of pack / checksum / compare: every chunk in order, one table per
-// slice size and alignment their configurations use (a line-aligned walk is
-// the plain one when every chunk starts on a line).
+// slice size, alignment and lead handling their configurations use (a
+// line-aligned walk is the plain one when every chunk starts on a line).
 int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units) {
   const Layout& L = p->layout;
-  const std::pair<int, int> walks[] = {{p->cfg.tile_pack, p->cfg.line_pack},
-                                        {p->cfg.tile_checksum, p->cfg.line_checksum},
-                                        {p->cfg.tile_verify, p->cfg.line_verify}};
-  for (const auto& tw : walks) {
-    const uint32_t sl = slice_bytes(L.C, tw.first);
-    const uint32_t shift = line_walk(p, tw.first, tw.second);
+  struct Want {
+    int tile, line, absorb;
+  };
+  const Want walks[] = {{p->cfg.tile_pack, p->cfg.line_pack, p->cfg.absorb_pack},
+                        {p->cfg.tile_checksum, p->cfg.line_checksum, p->cfg.absorb_checksum},
+                        {p->cfg.tile_verify, p->cfg.line_verify, p->cfg.absorb_verify}};
+  for (const Want& tw : walks) {
+    const uint32_t sl = slice_bytes(L.C, tw.tile);
+    const uint32_t shift = line_walk(p, tw.tile, tw.line);
+    const uint32_t absorb = shift && tw.absorb ? 1u : 0u;
     bool have = false;
-    for (const auto& w : p->src_walks) have = have || (w.sl == sl && w.t.shift == shift);
+    for (const auto& w : p->src_walks)
+      have = have || (w.sl == sl && w.t.shift == shift && w.t.absorb == absorb);
     if (have) continue;
     SlotRuns b;
     b.sl = sl;
     b.first.reserve(units.size() + 1);
     b.base.reserve(units.size());
     for (uint64_t c = 0; c < units.size(); c++)
-      b.add(uint32_t(c), units[c].len + (shift == 1 ? units[c].lead : shift == 2 ? units[c].plead : 0), 0);
+      b.add(uint32_t(c), units[c].len + (absorb ? 0 : lead_bytes(units[c].lead, units[c].plead, shift, sl)), 0);
     p->src_walks.emplace_back();
     const int rc = upload_walk(b, p->src_walks.back());
     p->src_walks.back().t.shift = shift;
+    p->src_walks.back().t.absorb = absorb;
     if (rc != FR_OK) return rc;
   }
   return FR_OK;
@@ -395,16 +426,29 @@ int build_unpack_walk(fr_plan* p, const std::vector<ChunkRec>& recs,
   b.sl = slice_bytes(L.C, p->cfg.tile_unpack);
   b.first.reserve(L.n_chunks + 1);
   b.base.reserve(L.n_chunks);
+  // plain chunks may be cut at lines of the receiver (mode 1) or of the
+  // payload (mode 2), or at slice boundaries of the payload (mode 3), with
+  // or without their last slice absorbing the lead
+  const uint32_t line = line_walk(p, p->cfg.tile_unpack, p->cfg.line_unpack, true);
+  const uint32_t absorb = line && p->cfg.absorb_unpack ? 1u : 0u;
   uint32_t id = 0, ip = 0;
   for (uint32_t k = 0; k < p->table.size(); k++) {
     const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];
     if (p->table[k].derive_from >= 0) {
       for (uint64_t c = c0; c < c1; c++) b.add(id++, 2 * uint64_t(recs[c].len), kSlotDerived);
     } else if (!is_master[k]) {
-      for (uint64_t c = c0; c < c1; c++) b.add(ip++, recs[c].len, 0);
+      for (uint64_t c = c0; c < c1; c++) {
+        const uint32_t lead = absorb ? 0
+                                     : lead_bytes(uint32_t(recs[c].dst_off % kLeadMod),
+                                                  uint32_t(recs[c].pay_off % kLeadMod), line, b.sl);
+        b.add(ip++, recs[c].len + lead, 0);
+      }
     }
   }
-  return upload_walk(b, p->unpack_walk);
+  const int rc = upload_walk(b, p->unpack_walk);
+  p->unpack_walk.t.shift = line;
+  p->unpack_walk.t.absorb = absorb;
+  return rc;
 }
 
 // Scratch: accumulators for the largest G any configured tile needs, for two
@@ -426,22 +470,22 @@ int build_scratch(fr_plan* p) {
   return rc;
 }
 
-// Delta lists built on the device: the tensor table and chunk bases they are
-// read from, room for the records of the longest list (pack's one per chunk,
-// or unpack's plain and derived ones), the scan state, and the staging of a
-// list given on the host (pinned, so that its upload is asynchronous; an
-// event marks when the staging may be refilled).  Allocated once here, so
-// that no delta call allocates.
-int build_delta(fr_plan* p) {
+// Delta lists built on the device: a location record per chunk (what a
+// lane needs about its chunk), room for the records of the longest list
+// (pack's one per chunk, or unpack's plain and derived ones), the scan state,
+// and the staging of a list given on the host (pinned, so that its upload
+// is asynchronous; an event marks when the staging may be refilled).
+// Allocated once here, so that no delta call allocates.
+int build_delta(fr_plan* p, const std::vector<ChunkRec>& recs) {
   const Layout& L = p->layout;
-  const uint64_t n = p->table.size(), nc = L.n_chunks, nw = (nc + 31) / 32;
+  const uint64_t nc = L.n_chunks, nb = (nc + kListBlock - 1) / kListBlock, nw = (nc + 31) / 32;
   auto up = [](uint64_t b) { return (b + 255) & ~uint64_t(255); };
-  const uint64_t b_desc = up(n * sizeof(fr_tensor_desc)), b_base = up((n + 1) * 8);
+  const uint64_t b_loc = up(nc * sizeof(ChunkLoc));
   const uint64_t b_units = up(std::max(nc * sizeof(SrcUnit), L.n_sent_chunks * sizeof(PlainUnit) +
                                                               (nc - L.n_sent_chunks) * sizeof(DerivedUnit)));
-  const uint64_t b_agg = up(nw * sizeof(DeltaAgg)), b_pre = up(nw * sizeof(DeltaPre));
+  const uint64_t b_agg = up(nb * sizeof(DeltaAgg)), b_pre = up(nb * sizeof(DeltaPre));
   const uint64_t b_counts = 256, b_bits = up(nw * 4), b_ids = up(nc * 4);
-  const uint64_t total = b_desc + b_base + b_units + b_agg + b_pre + b_counts + b_bits + b_ids;
+  const uint64_t total = b_loc + b_units + b_agg + b_pre + b_counts + b_bits + b_ids;
   int rc = upload(nullptr, total, &p->d_delta);
   if (rc != FR_OK) return rc;
   uint8_t* q = static_cast<uint8_t*>(p->d_delta);
@@ -450,8 +494,7 @@ int build_delta(fr_plan* p) {
     q += b;
     return r;
   };
-  fr_tensor_desc* desc = reinterpret_cast<fr_tensor_desc*>(take(b_desc));
-  uint64_t* base = reinterpret_cast<uint64_t*>(take(b_base));
+  p->d_delta_loc = reinterpret_cast<ChunkLoc*>(take(b_loc));
   uint8_t* units = take(b_units);
   p->d_delta_src = reinterpret_cast<SrcUnit*>(units);
   p->d_delta_plain = reinterpret_cast<PlainUnit*>(units);
@@ -461,10 +504,23 @@ int build_delta(fr_plan* p) {
   p->d_delta_counts = reinterpret_cast<uint64_t*>(take(b_counts));
   p->d_delta_bits = reinterpret_cast<uint32_t*>(take(b_bits));
   p->d_delta_ids = reinterpret_cast<uint32_t*>(take(b_ids));
+  std::vector<ChunkLoc> loc(nc);
+  for (uint32_t k = 0; k < p->table.size(); k++) {
+    const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];
+    for (uint64_t c = c0; c < c1; c++) {
+      const ChunkRec& r = recs[c];
+      ChunkLoc& l = loc[c];
+      l.src_off = r.src_off;
+      l.dst_off = r.dst_off;
+      // a derived chunk's master bytes: master chunks 2j and 2j + 1 from chunk 2j on
+      l.m_dst_off = r.master == kNoMaster ? 0 : recs[r.master].dst_off;
+      l.len = r.len;
+      l.flags = (r.master == kNoMaster ? 0u : kLocDerived) | (c == c0 ? kLocFirst : 0u) |
+                (c + 1 == c1 ? kLocLast : 0u);
+    }
+  }
   hipError_t e = hipSuccess;
-  if (n) e = hipMemcpy(desc, p->table.data(), n * sizeof(fr_tensor_desc), hipMemcpyHostToDevice);
-  if (e == hipSuccess)
-    e = hipMemcpy(base, L.chunk_base.data(), (n + 1) * 8, hipMemcpyHostToDevice);
+  if (nc) e = hipMemcpy(p->d_delta_loc, loc.data(), nc * sizeof(ChunkLoc), hipMemcpyHostToDevice);
   if (e == hipSuccess && nc)
     e = hipHostMalloc(reinterpret_cast<void**>(&p->h_delta_ids), nc * 4, hipHostMallocDefault);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&p->delta_ids_copied, hipEventDisableTiming);
@@ -472,7 +528,6 @@ int build_delta(fr_plan* p) {
     (void)hipGetLastError();
     return e == hipErrorOutOfMemory ? FR_E_NOMEM : hip_fail(e);
   }
-  p->delta_tables = DeltaTables{desc, base, uint32_t(n), L.C, L.seg};
   return FR_OK;
 }
 
@@ -512,7 +567,8 @@ extern "C" int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n, uint64
     unpack_units(table, n, L, recs, is_master, &derived, &plain);
     p->n_derived = uint32_t(derived.size());
     p->n_plain = uint32_t(plain.size());
-    const std::vector<SrcUnit> units = src_units(recs, n, L, &p->any_lead, &p->any_plead);
+    for (const PlainUnit& u : plain) p->dst_align = std::min(p->dst_align, pow2_align(u.dst_off));
+    const std::vector<SrcUnit> units = src_units(recs, n, L, &p->src_align, &p->pay_align);
 
     rc = upload(units.data(), units.size() * sizeof(SrcUnit), (void**)&p->d_units);
     if (rc == FR_OK) rc = build_src_walks(p, units);
@@ -522,7 +578,7 @@ extern "C" int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n, uint64
     if (rc == FR_OK)
       rc = upload(plain.data(), plain.size() * sizeof(PlainUnit), (void**)&p->d_plain);
     if (rc == FR_OK) rc = build_scratch(p);
-    if (rc == FR_OK) rc = build_delta(p);
+    if (rc == FR_OK) rc = build_delta(p, recs);
     if (rc != FR_OK) {
       fr_plan_destroy(p);
       return rc;

@@ -337,20 +337,30 @@ def test_every_slice_count_per_tile(tile):
 
 
 @pytest.mark.parametrize("tile", [0, 3, 4, 5, 7, 10])
-@pytest.mark.parametrize("line", ["1", "2"])
-def test_line_aligned_walks_match_oracle(tile, line):
+@pytest.mark.parametrize("absorb", ["0", "1"])
+@pytest.mark.parametrize("line", ["1", "2", "3"])
+def test_line_aligned_walks_match_oracle(tile, line, absorb):
     """Line-aligned walks (every slice cut at a 128-byte line, one more
     slice for a chunk that starts inside a line) give the oracle's bytes:
-    line 1 cuts pack, compare and checksum at lines of the arena read, line 2
-    cuts pack at lines of the payload it writes (the compare and checksum at
-    arena lines).  Random tables at random 16-byte offsets (16-byte payload
+    line 1 cuts pack, compare and checksum at lines of the arena read and
+    unpack's plain chunks at lines of the receiver, line 2 cuts pack and
+    unpack at lines of the payload (the compare and checksum at arena
+    lines), line 3 cuts pack and unpack's plain chunks at slice boundaries
+    of the payload (one more slice for a chunk that starts inside a slice;
+    the compare and checksum at arena lines); with absorb, every operation's
+    chunks keep their plain slice count and the last slice takes the
+    leftover lead.  Random tables at random 16-byte offsets
+    (16-byte payload
     segments, so payload chunks start inside lines too), chunks from 16 B
     (several chunks per line) to 1 MiB, and short chunks of every slice
     count."""
-    names = ("FLASHRESTORE_TILE", "FLASHRESTORE_LINE", "FLASHRESTORE_MAX_GRID")
+    absorbs = tuple(f"FLASHRESTORE_ABSORB_{op}" for op in ("PACK", "UNPACK", "VERIFY", "CHECKSUM"))
+    names = ("FLASHRESTORE_TILE", "FLASHRESTORE_LINE", "FLASHRESTORE_MAX_GRID") + absorbs
     old = {k: os.environ.get(k) for k in names}
     os.environ["FLASHRESTORE_TILE"], os.environ["FLASHRESTORE_LINE"] = str(tile), line
-    rng = np.random.default_rng(700 + tile + 50 * int(line))
+    for k in absorbs:
+        os.environ[k] = absorb
+    rng = np.random.default_rng(700 + tile + 50 * int(line) + 1000 * int(absorb))
     try:
         for it in range(40):
             # grid-stride launches too (a capped grid walks several slices per workgroup)
