@@ -10,7 +10,8 @@ times (default plan, one workgroup per unit).
   the host (payload, sums and receiver arena compared slice by slice), plus
   sampled chunks, a located wire flip and properties that hold at any size
   (exact round trip, nothing flagged, checksum == pack sums, replica compare
-  empty).
+  empty); a replica with 4,096 flips: compare set, both arenas' sums and the
+  checksum against the whole oracle.
 * Replica compare on two copies of the 8B share with k in {0, 1, 64, 4096}
   distinct random bit flips: the flagged set equals the closed form
   {chunk of each flipped byte} and the oracle's set; the 4,096-flip replica
@@ -334,6 +335,53 @@ def test_llama70b_stage0_sampled_parity(llama70b):
     r.unpack()
     assert r.bad_set() == exp
     assert int(r.n_bad.item()) == len(exp)
+
+
+def _flips_over_entries(t, k, seed):
+    """k distinct random bit flips over the table-order concatenation of the
+    entries' bytes: (arena byte offsets, bit numbers, entry of each, byte
+    within that entry)."""
+    nb = t["numel"].astype(np.int64) * np.where(t["dtype"] == W.F32, 4, 2)
+    starts = np.concatenate([[0], np.cumsum(nb)])
+    pos = W.flip_positions(int(starts[-1]) * 8, k, seed).astype(np.int64)
+    cat = pos // 8
+    e = np.searchsorted(starts, cat, side="right") - 1
+    by = t["src_offset"].astype(np.int64)[e] + (cat - starts[e])
+    return by, (pos % 8).astype(np.int64), e, cat - starts[e]
+
+
+@pytest.mark.timeout(900)
+def test_llama70b_stage0_replica_compare_and_checksum_whole_oracle(llama70b):
+    """A replica of the 70B share with 4,096 distinct random bit flips: the
+    replica compare's flagged set, count and both arenas' chunk sums, and
+    the checksum of the flipped replica, equal the whole oracle's on the full
+    31.8 GB arenas; the flagged set is also the closed form {chunk of each
+    flipped byte}."""
+    w, src_np = llama70b
+    t, C = w.table, w.chunk_bytes
+    r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes)
+    donor = _upload(src_np)
+    by, bit, e, off = _flips_over_entries(t, 4096, 7096)
+    _, base, _, _ = cpu.plan(t, C)
+    expect = {int(base[x]) + int(o) // C for x, o in zip(e, off)}
+    rep_np = src_np.copy()
+    np.bitwise_xor.at(rep_np, by, (np.uint8(1) << bit.astype(np.uint8)).astype(np.uint8))
+    replica = _upload(rep_np)
+    nc = r.n_chunks
+    sa, sb = r.plan.empty_sums(), r.plan.empty_sums()
+    r.verify(donor, replica, sa, sb)
+    r.checksum(replica)
+    torch.cuda.synchronize()
+    got = r.diff_set()
+    log(f"GPU compare: {len(got)} chunks differ")
+    bm, nd, osa, osb = cpu.verify(t, C, src_np, rep_np, with_sums=True)
+    log("oracle compare done")
+    assert got == set(cpu.bitmap_to_set(bm, nc)) == expect
+    assert int(r.n_diff.item()) == nd == len(expect)
+    assert np.array_equal(sums_host(sa, nc), osa) and np.array_equal(sums_host(sb, nc), osb)
+    ocs = cpu.checksum(t, C, rep_np)
+    assert np.array_equal(sums_host(r.csum, nc), ocs)
+    log(f"compare sums and checksum equal the oracle's; {len(expect)} flagged of {nc}")
 
 
 @pytest.mark.timeout(900)
