@@ -37,7 +37,9 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 METRIC = "state restore GB/s per GPU (pack+checksum, unpack+verify) and % of HBM peak"
 KERNEL_SOURCES = ("paper_2509_03047_amd/csrc/kernels.hip", "paper_2509_03047_amd/csrc/fr_internal.h")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama8b_tp8.json")
+# HBM traffic per launch measured with rocprofv3 counters, per workload
+TRAFFIC_FILES = {1: "hbm_traffic_llama8b_tp8.json", 2: "hbm_traffic_descriptor_stress_20k.json",
+                 3: "hbm_traffic_llama70b_tp8pp4.json"}
 KERNEL_NAMES = {"pack": "k_pack", "unpack": "k_unpack", "verify": "k_verify", "checksum": "k_pack"}
 
 
@@ -111,7 +113,15 @@ def algorithmic_bytes(info, table=None) -> dict:
 
 
 def copy_calibration():
+    """Known traffic for scaling the HBM counters: a 4 GiB device copy
+    (torch's, the runtime's copy kernel) ten times after five warm-ups, then
+    one launch each of the plain copy and read-only kernels of libfrceil on
+    the same 4 GiB (reads 4 GiB and writes 4 GiB; reads 4 GiB)."""
+    import ctypes
+
     import torch
+
+    from paper_2509_03047_amd import build as B
 
     n = 4 << 30
     a = torch.empty(n, dtype=torch.uint8, device="cuda")
@@ -129,7 +139,17 @@ def copy_calibration():
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / reps
-    return {"bytes_per_copy": 2 * n, "ms": ms, "gbs": 2 * n / ms / 1e6}
+    lib = ctypes.CDLL(B.CEIL_LIB)
+    P, u64, u32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32
+    lib.frc_copy.argtypes = [P, P, u64, P]
+    lib.frc_read.argtypes = [P, u64, u32, P, P]
+    sink = torch.zeros(64, dtype=torch.int32, device="cuda")
+    sp = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if lib.frc_copy(b.data_ptr(), a.data_ptr(), n, sp) or lib.frc_read(a.data_ptr(), n, 7, sink.data_ptr(), sp):
+        raise RuntimeError("ceiling kernel launch failed")
+    torch.cuda.synchronize()
+    return {"bytes_per_copy": 2 * n, "ms": ms, "gbs": 2 * n / ms / 1e6,
+            "plain_kernels": {"k_copy": {"read": n, "write": n}, "k_read": {"read": n, "write": 0}}}
 
 
 def ceilings(reps: int = 10, nbytes: int = 4 << 30):
@@ -620,12 +640,13 @@ def main():
     roof = {"bound": "hbm", "kernel": KERNEL_NAMES[dom], "op": dom,
             "achieved": op_report[dom]["hbm_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": op_report[dom]["frac_of_peak"], "traffic": None}
-    try:
-        with open(TRAFFIC_FILE) as f:
+    try:  # counters taken on these kernels' code for this workload, else null
+        with open(os.path.join(ROOT, "profiles", TRAFFIC_FILES[args.config])) as f:
             tr = json.load(f)
-        if tr.get("kernel_source_sha") == kernel_source_hash() and tr.get("config") == args.config:
+        if (tr.get("kernel_source_sha") == kernel_source_hash() and tr.get("config") == args.config
+                and args.segment_align in (None, 16)):
             roof["traffic"] = tr.get("ops", {}).get(dom, {}).get("bytes_per_launch")
-    except (OSError, ValueError):
+    except (KeyError, OSError, ValueError):
         pass
 
     out = {
