@@ -25,16 +25,21 @@
 //     SPC slices owns G = max(1, SPC / 16) accumulators in the plan's
 //     scratch, cleared by a fill kernel launched first;
 //   * replica compare marks a differing chunk with a plain store of 1 to a
-//     per-chunk flag (idempotent, so no atomics on shared bitmap words), and
-//     by default walks line-aligned: for tensors that start inside a cache
-//     line its cuts fall on lines of the arenas, so no line is fetched
-//     twice (pack and checksum measured slower that way; the plan's
-//     launch configuration sets it per operation, see LaunchCfg);
+//     per-chunk flag (idempotent, so no atomics on shared bitmap words);
+//   * for tensors that start inside a cache line, walks cut slices at lines
+//     of one side so that no line is touched by two workgroups: pack at
+//     lines of the payload it writes, unpack at lines of the receiver, the
+//     compare at lines of the arenas (the checksum measured slower that
+//     way); pack and unpack let a chunk's last slice take the leftover lead
+//     instead of adding a nearly empty slice (the plan's launch
+//     configuration sets all of it per operation, see LaunchCfg);
 //   * a finalize kernel, one lane per chunk, folds the G accumulators into
 //     the chunk's sums (pack, checksum, compare) or compares them with the
 //     sums sent (unpack), and writes whole bitmap words from wave ballots.
 // Plan creation uses one more kernel: the host describes each slot table as
 // one run of slots per unit and k_expand_slots writes the table itself.
+// Delta calls build their lists' unit records on the device (k_list_*,
+// below), so that a repair can follow the compare with no host work.
 #include <hip/hip_runtime.h>
 
 #include <mutex>
