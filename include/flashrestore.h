@@ -159,9 +159,11 @@ typedef struct fr_plan_info {
  * multiples of 16 (FR_E_ALIGN), receiver ranges must not overlap
  * (FR_E_OVERLAP; sender ranges may), the chunk count must be < 2^32
  * (FR_E_RANGE).  Synchronous: the plan's device tables are complete before
- * return (they are partly built by a kernel on the null stream, which this
- * call waits for; so create plans outside graph capture, as the allocations
- * also require).  The plan is immutable and bound to the device current at
+ * return.  They are copied and partly built by a kernel on a stream of the
+ * call's own that does not synchronise with the null stream, and only that
+ * stream is waited for, so work already queued elsewhere on the device is
+ * neither waited for nor blocked.  Create plans outside graph capture, as
+ * the allocations require.  The plan is immutable and bound to the device current at
  * creation.  Launch shapes are read from the environment at creation, and
  * results never depend on them: FLASHRESTORE_TILE (every operation) or
  * FLASHRESTORE_TILE_PACK / _UNPACK / _VERIFY / _CHECKSUM select a tile

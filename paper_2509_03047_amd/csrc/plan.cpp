@@ -170,8 +170,31 @@ static int hip_fail(hipError_t e) {
   return FR_E_DEVICE;
 }
 
+// Plan creation works on a stream of its own that does not synchronise with
+// the null stream, and frees nothing on success (hipFree waits for the whole
+// device), so that creating a plan does not stall other work on the device.
+// `runs` stages the run descriptions of the slot tables; it points into the
+// plan's scratch, which no call has used yet and every call clears first.
+struct Staging {
+  hipStream_t s = nullptr;
+  uint64_t* runs = nullptr;
+  uint64_t runs_cap = 0;  // in uint64_t
+  ~Staging() {
+    if (s) (void)hipStreamDestroy(s);
+  }
+};
+
+// Host-to-device copy on the creation stream, finished before returning (the
+// host arrays are temporaries of the caller).
+static int copy_in(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return FR_OK;
+  hipError_t e = hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  return e == hipSuccess ? FR_OK : hip_fail(e);
+}
+
 // Device copy of a host array (or an uninitialised buffer when src is NULL).
-static int upload(const void* src, size_t bytes, void** out) {
+static int upload(const void* src, size_t bytes, void** out, hipStream_t s) {
   *out = nullptr;
   if (bytes == 0) return FR_OK;
   hipError_t e = hipMalloc(out, bytes);
@@ -180,11 +203,7 @@ static int upload(const void* src, size_t bytes, void** out) {
     (void)hipGetLastError();
     return e == hipErrorOutOfMemory ? FR_E_NOMEM : hip_fail(e);
   }
-  if (src) {
-    e = hipMemcpy(*out, src, bytes, hipMemcpyHostToDevice);
-    if (e != hipSuccess) return hip_fail(e);
-  }
-  return FR_OK;
+  return src ? copy_in(*out, src, bytes, s) : FR_OK;
 }
 
 namespace fr {
@@ -202,27 +221,25 @@ namespace {
 
 // Allocates the slot table of `r` on the device and expands it there: the
 // host uploads one (first slot, base) pair per run instead of every slot.
-int upload_walk(const SlotRuns& r, fr_plan::Walk& w) {
+int upload_walk(const SlotRuns& r, fr_plan::Walk& w, const Staging& st) {
   w.sl = r.sl;
   w.t.n = r.n();
   w.t.stride = r.stride();
-  int rc = upload(nullptr, 8 * r.stride() * sizeof(uint64_t), (void**)&w.mem);
+  int rc = upload(nullptr, 8 * r.stride() * sizeof(uint64_t), (void**)&w.mem, st.s);
   w.t.d = w.mem;
   if (rc != FR_OK || !w.mem) return rc;
   const uint64_t n_runs = r.base.size();
-  void* runs = nullptr;
-  rc = upload(nullptr, (2 * n_runs + 1) * sizeof(uint64_t), &runs);
-  if (rc != FR_OK) return rc;
-  uint64_t* d_first = static_cast<uint64_t*>(runs);
+  if (2 * n_runs + 1 > st.runs_cap) return FR_E_RANGE;  // not reached: one run per chunk at most
+  uint64_t* d_first = st.runs;
   uint64_t* d_base = d_first + n_runs + 1;
-  hipError_t e = hipMemcpy(d_first, r.first.data(), (n_runs + 1) * sizeof(uint64_t),
-                           hipMemcpyHostToDevice);
+  hipError_t e = hipMemcpyAsync(d_first, r.first.data(), (n_runs + 1) * sizeof(uint64_t),
+                                hipMemcpyHostToDevice, st.s);
   if (e == hipSuccess)
-    e = hipMemcpy(d_base, r.base.data(), n_runs * sizeof(uint64_t), hipMemcpyHostToDevice);
+    e = hipMemcpyAsync(d_base, r.base.data(), n_runs * sizeof(uint64_t), hipMemcpyHostToDevice,
+                       st.s);
   if (e == hipSuccess)
-    e = hipError_t(launch_expand_slots(d_first, d_base, n_runs, r.n(), r.stride(), w.mem, nullptr));
-  if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
-  (void)hipFree(runs);
+    e = hipError_t(launch_expand_slots(d_first, d_base, n_runs, r.n(), r.stride(), w.mem, st.s));
+  if (e == hipSuccess) e = hipStreamSynchronize(st.s);
   return e == hipSuccess ? FR_OK : hip_fail(e);
 }
 
@@ -386,7 +403,7 @@ void unpack_units(const fr_tensor_desc* table, uint32_t n, const Layout& L,
 // Walks of pack / checksum / compare: every chunk in order, one table per
 // slice size, alignment and lead handling their configurations use (a
 // line-aligned walk is the plain one when every chunk starts on a line).
-int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units) {
+int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units, const Staging& st) {
   const Layout& L = p->layout;
   struct Want {
     int tile, line, absorb;
@@ -409,7 +426,7 @@ int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units) {
     for (uint64_t c = 0; c < units.size(); c++)
       b.add(uint32_t(c), units[c].len + (absorb ? 0 : lead_bytes(units[c].lead, units[c].plead, shift, sl)), 0);
     p->src_walks.emplace_back();
-    const int rc = upload_walk(b, p->src_walks.back());
+    const int rc = upload_walk(b, p->src_walks.back(), st);
     p->src_walks.back().t.shift = shift;
     p->src_walks.back().t.absorb = absorb;
     if (rc != FR_OK) return rc;
@@ -420,7 +437,7 @@ int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units) {
 // Walk of unpack, in payload (table) order: a derived entry's groups (their
 // master bytes) where the entry stands, plain chunks where theirs.
 int build_unpack_walk(fr_plan* p, const std::vector<ChunkRec>& recs,
-                      const std::vector<uint8_t>& is_master) {
+                      const std::vector<uint8_t>& is_master, const Staging& st) {
   const Layout& L = p->layout;
   SlotRuns b;
   b.sl = slice_bytes(L.C, p->cfg.tile_unpack);
@@ -445,27 +462,31 @@ int build_unpack_walk(fr_plan* p, const std::vector<ChunkRec>& recs,
       }
     }
   }
-  const int rc = upload_walk(b, p->unpack_walk);
+  const int rc = upload_walk(b, p->unpack_walk, st);
   p->unpack_walk.t.shift = line;
   p->unpack_walk.t.absorb = absorb;
   return rc;
 }
 
 // Scratch: accumulators for the largest G any configured tile needs, for two
-// arenas, and one flag per chunk.
-int build_scratch(fr_plan* p) {
+// arenas, and one flag per chunk.  Its accumulators (16 bytes per chunk at
+// least, twice) also hold the staged runs of each slot table (at most one
+// run per chunk: 16 bytes per run, and 8 more).
+int build_scratch(fr_plan* p, Staging* st) {
   const Layout& L = p->layout;
   uint64_t g = 1;
   for (int t : {p->cfg.tile_pack, p->cfg.tile_unpack, p->cfg.tile_verify, p->cfg.tile_checksum})
     g = std::max<uint64_t>(g, accumulators_per_chunk(L.C, t));
   const uint64_t acc_bytes = L.n_chunks * g * sizeof(fr_chunk_sum);
   const uint64_t flag_bytes = (L.n_chunks * 4 + 255) & ~uint64_t(255);
-  const int rc = upload(nullptr, 2 * acc_bytes + flag_bytes, &p->d_scratch);
+  const int rc = upload(nullptr, 2 * acc_bytes + flag_bytes, &p->d_scratch, st->s);
   if (rc == FR_OK && p->d_scratch) {
     uint8_t* base = static_cast<uint8_t*>(p->d_scratch);
     p->scratch.acc = reinterpret_cast<fr_chunk_sum*>(base);
     p->scratch.acc_b = reinterpret_cast<fr_chunk_sum*>(base + acc_bytes);
     p->scratch.flags = reinterpret_cast<uint32_t*>(base + 2 * acc_bytes);
+    st->runs = reinterpret_cast<uint64_t*>(base);
+    st->runs_cap = 2 * acc_bytes / sizeof(uint64_t);
   }
   return rc;
 }
@@ -476,7 +497,7 @@ int build_scratch(fr_plan* p) {
 // and the staging of a list given on the host (pinned, so that its upload
 // is asynchronous; an event marks when the staging may be refilled).
 // Allocated once here, so that no delta call allocates.
-int build_delta(fr_plan* p, const std::vector<ChunkRec>& recs) {
+int build_delta(fr_plan* p, const std::vector<ChunkRec>& recs, const Staging& st) {
   const Layout& L = p->layout;
   const uint64_t nc = L.n_chunks, nb = (nc + kListBlock - 1) / kListBlock, nw = (nc + 31) / 32;
   auto up = [](uint64_t b) { return (b + 255) & ~uint64_t(255); };
@@ -486,7 +507,7 @@ int build_delta(fr_plan* p, const std::vector<ChunkRec>& recs) {
   const uint64_t b_agg = up(nb * sizeof(DeltaAgg)), b_pre = up(nb * sizeof(DeltaPre));
   const uint64_t b_counts = 256, b_bits = up(nw * 4), b_ids = up(nc * 4);
   const uint64_t total = b_loc + b_units + b_agg + b_pre + b_counts + b_bits + b_ids;
-  int rc = upload(nullptr, total, &p->d_delta);
+  int rc = upload(nullptr, total, &p->d_delta, st.s);
   if (rc != FR_OK) return rc;
   uint8_t* q = static_cast<uint8_t*>(p->d_delta);
   auto take = [&](uint64_t b) {
@@ -519,9 +540,10 @@ int build_delta(fr_plan* p, const std::vector<ChunkRec>& recs) {
                 (c + 1 == c1 ? kLocLast : 0u);
     }
   }
+  rc = copy_in(p->d_delta_loc, loc.data(), nc * sizeof(ChunkLoc), st.s);
+  if (rc != FR_OK) return rc;
   hipError_t e = hipSuccess;
-  if (nc) e = hipMemcpy(p->d_delta_loc, loc.data(), nc * sizeof(ChunkLoc), hipMemcpyHostToDevice);
-  if (e == hipSuccess && nc)
+  if (nc)
     e = hipHostMalloc(reinterpret_cast<void**>(&p->h_delta_ids), nc * 4, hipHostMallocDefault);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&p->delta_ids_copied, hipEventDisableTiming);
   if (e != hipSuccess) {
@@ -570,15 +592,24 @@ extern "C" int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n, uint64
     for (const PlainUnit& u : plain) p->dst_align = std::min(p->dst_align, pow2_align(u.dst_off));
     const std::vector<SrcUnit> units = src_units(recs, n, L, &p->src_align, &p->pay_align);
 
-    rc = upload(units.data(), units.size() * sizeof(SrcUnit), (void**)&p->d_units);
-    if (rc == FR_OK) rc = build_src_walks(p, units);
-    if (rc == FR_OK) rc = build_unpack_walk(p, recs, is_master);
+    Staging st;
+    const hipError_t es = hipStreamCreateWithFlags(&st.s, hipStreamNonBlocking);
+    if (es != hipSuccess) {
+      st.s = nullptr;
+      delete p;
+      return hip_fail(es);
+    }
+    rc = build_scratch(p, &st);
     if (rc == FR_OK)
-      rc = upload(derived.data(), derived.size() * sizeof(DerivedUnit), (void**)&p->d_derived);
+      rc = upload(units.data(), units.size() * sizeof(SrcUnit), (void**)&p->d_units, st.s);
+    if (rc == FR_OK) rc = build_src_walks(p, units, st);
+    if (rc == FR_OK) rc = build_unpack_walk(p, recs, is_master, st);
     if (rc == FR_OK)
-      rc = upload(plain.data(), plain.size() * sizeof(PlainUnit), (void**)&p->d_plain);
-    if (rc == FR_OK) rc = build_scratch(p);
-    if (rc == FR_OK) rc = build_delta(p, recs);
+      rc = upload(derived.data(), derived.size() * sizeof(DerivedUnit), (void**)&p->d_derived,
+                  st.s);
+    if (rc == FR_OK)
+      rc = upload(plain.data(), plain.size() * sizeof(PlainUnit), (void**)&p->d_plain, st.s);
+    if (rc == FR_OK) rc = build_delta(p, recs, st);
     if (rc != FR_OK) {
       fr_plan_destroy(p);
       return rc;
