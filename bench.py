@@ -41,6 +41,10 @@ KERNEL_SOURCES = ("paper_2509_03047_amd/csrc/kernels.hip", "paper_2509_03047_amd
 TRAFFIC_FILES = {1: "hbm_traffic_llama8b_tp8.json", 2: "hbm_traffic_descriptor_stress_20k.json",
                  3: "hbm_traffic_llama70b_tp8pp4.json"}
 KERNEL_NAMES = {"pack": "k_pack", "unpack": "k_unpack", "verify": "k_verify", "checksum": "k_pack"}
+WALK_TILES = 4  # fr_plan_info pack_walk / unpack_walk: one aligned tile of the side written per workgroup
+TILE_KERNELS = {"pack": "k_pack_blocks", "unpack": "k_unpack_blocks"}
+WALK_NAMES = {0: "slices", 1: "slices cut at arena / receiver lines", 2: "slices cut at payload lines",
+              3: "slices cut at payload slice boundaries", WALK_TILES: "tiles of the side written"}
 
 
 def _code_only(text: str) -> str:
@@ -637,7 +641,9 @@ def main():
                          "ms_min": round(min(op_ms[op]), 4), "alg_bytes": alg[op],
                          "hbm_gbs": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
     dom = max(ops, key=lambda o: per_op[o])
-    roof = {"bound": "hbm", "kernel": KERNEL_NAMES[dom], "op": dom,
+    walks = {"pack": info["pack_walk"], "unpack": info["unpack_walk"]}
+    kernel = TILE_KERNELS[dom] if walks.get(dom) == WALK_TILES else KERNEL_NAMES[dom]
+    roof = {"bound": "hbm", "kernel": kernel, "op": dom,
             "achieved": op_report[dom]["hbm_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": op_report[dom]["frac_of_peak"], "traffic": None}
     try:  # counters taken on these kernels' code for this workload, else null
@@ -671,6 +677,7 @@ def main():
             "segment_align": info["segment_align"],
             "n_chunks": info["n_chunks"],
             "step": "pack+checksum -> unpack+derive+verify -> verify_replicas -> checksum_state",
+            "walks": {op: WALK_NAMES.get(v, str(v)) for op, v in walks.items()},
         },
         "restore_ms": round(restore_ms, 4),
         "step_gbs": round(info["state_bytes"] / (ms_step * 1e-3) / 1e9, 2),

@@ -89,7 +89,7 @@
 extern "C" {
 #endif
 
-#define FR_ABI_VERSION 4
+#define FR_ABI_VERSION 5
 
 enum fr_dtype { FR_F32 = 1, FR_BF16 = 2 };
 
@@ -141,7 +141,17 @@ typedef struct fr_plan_info {
                                  need: payload_bytes when chunk_bytes >= A, else
                                  the sent bytes plus A per sent chunk, rounded up
                                  to 16 */
+  uint32_t pack_walk;       /* how fr_pack_state and fr_unpack_state divide their */
+  uint32_t unpack_walk;     /* work (0 for a layout query): 0 slices of chunks,
+                               1-3 slices cut at cache lines of one side, 4 one
+                               aligned tile of the side written (the payload for
+                               pack, the receiver arena for unpack) per workgroup,
+                               the default where that side's chunks start inside
+                               cache lines; FR_WALK_* */
 } fr_plan_info;
+
+#define FR_WALK_SLICES 0
+#define FR_WALK_TILES 4
 
 /* ---------------------------------------------------------------- plans */
 

@@ -127,6 +127,10 @@ extern "C" int fr_pack_state(const fr_plan* plan, const void* src_base, void* pa
   const Region outs[] = {{payload, L.payload_bytes}, {sums, L.n_chunks * sizeof(fr_chunk_sum)}};
   const Region ins[] = {{src_base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 2, ins, 1));
+  if (plan->cfg.line_pack == kLineBlocks)
+    return launch_result(launch_pack_blocks(plan->d_units, plan->pack_blocks, uint32_t(L.n_chunks),
+                                            L.C, src_base, payload, sums, plan->scratch, plan->cfg,
+                                            stream));
   const SlotTable* walk = src_walk(plan, plan->cfg.tile_pack, plan->cfg.line_pack, plan->cfg.absorb_pack);
   if (!walk) return FR_E_INVAL;
   return launch_result(launch_pack(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, src_base,
@@ -162,6 +166,8 @@ extern "C" int fr_unpack_state(const fr_plan* plan, const void* payload, const f
   u.bitmap = bad_bitmap;
   u.n_bad = n_bad;
   u.scratch = plan->scratch;
+  if (plan->cfg.line_unpack == kLineBlocks)
+    return launch_result(launch_unpack_blocks(u, plan->unpack_blocks, plan->cfg, stream));
   return launch_result(launch_unpack(u, plan->cfg, stream));
 }
 

@@ -159,10 +159,14 @@ struct LaunchCfg {
   int tile_pack = 0, tile_unpack = 0, tile_verify = 0, tile_checksum = 0;
   // line-aligned walks (SlotTable::shift) per operation: 0 off, 1 cut at
   // lines of the arena read, 2 (pack) at lines of the payload, 3 (pack,
-  // unpack) at slice boundaries of the payload
+  // unpack) at slice boundaries of the payload; pack 4: by blocks of the
+  // payload (PackBlocks) instead of slices of chunks
   int line_pack = 0, line_unpack = 0, line_verify = 0, line_checksum = 0;
   // line-aligned walks whose units' last slice absorbs the lead
   int absorb_pack = 0, absorb_unpack = 0, absorb_verify = 0, absorb_checksum = 0;
+  // slices loaded through buffer resources (every load of a thread in
+  // flight at once) rather than predicated global loads
+  int buf_pack = 0, buf_unpack = 0, buf_verify = 0, buf_checksum = 0;
 };
 
 // Device scratch owned by a plan: per-chunk accumulators (G per chunk, see
@@ -278,6 +282,32 @@ uint64_t accumulators_per_chunk(uint64_t C, int tile);
 inline uint32_t line_walk(const fr_plan* p, int tile, int line, bool receiver = false);
 inline uint32_t lead_bytes(uint32_t lead, uint32_t plead, uint32_t line, uint32_t sl);
 
+// Pack walked by blocks of the payload, one tile (T = B U vectors) per
+// workgroup across chunk boundaries, plus a slot walk over the chunks that
+// have no payload (launch_pack_blocks).
+struct PackBlocks {
+  const SrcUnit* units = nullptr;   // sent chunks in payload order (c = global chunk id)
+  const uint32_t* first = nullptr;  // per block, XCD-major: the unit holding its first vector
+  uint64_t n_units = 0, n_blocks = 0, stride = 0, pay_vecs = 0;
+  SlotTable extra{};  // the chunks without payload, ids into the plan's d_units
+};
+// Pack walked by blocks of the payload, unpack by blocks of the receiver
+// arena (tiles of the side written).
+constexpr int kLineBlocks = 4;
+// Blocks where chunks of the side written start inside lines, else the
+// operation's line walk.
+constexpr int kLineAuto = -1;
+
+// Unpack walked by blocks of the receiver arena: the plain chunks in
+// receiver order, the tiles that hold some of their bytes, and the walk of
+// the derived groups (launch_unpack_blocks).
+struct UnpackBlocks {
+  const PlainUnit* units = nullptr;
+  const uint64_t* blocks = nullptr;  // XCD-major: (tile index << 32) | first unit in it
+  uint64_t n_units = 0, n_blocks = 0, stride = 0;
+  SlotTable derived{};  // derived groups only, ids into the plan's d_derived
+};
+
 // Kernel launchers (kernels.hip).  They assume validated arguments, enqueue
 // on `stream` and return the hipError_t of the launches as an int.
 // `units` holds n_chunks records whose sums slots c cover [0, n_chunks);
@@ -285,6 +315,16 @@ inline uint32_t lead_bytes(uint32_t lead, uint32_t plead, uint32_t line, uint32_
 int launch_pack(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks, uint64_t C,
                 const void* src, void* payload, fr_chunk_sum* sums, const Scratch& scr,
                 const LaunchCfg& cfg, void* stream);
+int launch_pack_blocks(const SrcUnit* units, const PackBlocks& pb, uint32_t n_chunks, uint64_t C,
+                       const void* src, void* payload, fr_chunk_sum* sums, const Scratch& scr,
+                       const LaunchCfg& cfg, void* stream);
+// out[0 .. 8 * stride) <- the first unit of every block of block_vecs
+// vectors (PackBlocks::first), for units whose payload offsets are
+// pay_off[0], pay_off[4], ... (32-byte records).
+int launch_block_first(const uint64_t* pay_off, uint64_t n_units, uint64_t n_blocks,
+                       uint64_t stride, uint32_t block_vecs, uint32_t* out, void* stream);
+int launch_unpack_blocks(const UnpackArgs& args, const UnpackBlocks& ub, const LaunchCfg& cfg,
+                         void* stream);
 int launch_checksum(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks, uint64_t C,
                     const void* base, fr_chunk_sum* sums, const Scratch& scr,
                     const LaunchCfg& cfg, void* stream);
@@ -332,6 +372,16 @@ struct fr_plan {
   uint32_t pay_align = fr::kLeadMod;   // the same for every sent chunk's payload offset
   std::vector<Walk> src_walks;
   Walk unpack_walk;
+  // pack / unpack by payload blocks (cfg.line_* == kLineBlocks): the sent
+  // chunks' units in payload order and each block's first unit (one
+  // allocation each), and the walk of the rest (pack: the chunks without
+  // payload; unpack: the derived groups)
+  void* d_blocks = nullptr;
+  fr::PackBlocks pack_blocks{};
+  Walk pack_extra;
+  void* d_ublocks = nullptr;
+  fr::UnpackBlocks unpack_blocks{};
+  Walk unpack_derived;
   fr::DerivedUnit* d_derived = nullptr;  // unpack units: derived groups
   uint32_t n_derived = 0;
   fr::PlainUnit* d_plain = nullptr;      // unpack units: plain chunks

@@ -57,6 +57,48 @@ __device__ __forceinline__ u32x4 ld_nt(const u32x4* p) { return __builtin_nontem
 __device__ __forceinline__ void st_nt(u32x4 v, u32x4* p) { __builtin_nontemporal_store(v, p); }
 __device__ __forceinline__ void st_nt2(u32x2 v, u32x2* p) { __builtin_nontemporal_store(v, p); }
 
+// Raw buffer accesses: a resource describes `bytes` bytes from `base`
+// (stride 0, the gfx9 family's default format word); a 16-byte load at a
+// byte offset at or past `bytes` returns zeros and a store there is dropped,
+// with no memory access.  Every lane then issues its loads unconditionally,
+// so nothing waits on a load before all of a thread's loads are in flight.
+// Cache policy 2 is the non-temporal hint.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOob = 0xFFFFFFF0u;  // an offset past every range used here
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), int(bytes), 0x00020000);
+}
+__device__ __forceinline__ u32x4 ld_buf(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, int(off), 0, 2);
+}
+__device__ __forceinline__ void st_buf(const u32x4& v, rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, int(off), 0, 2);
+}
+
+// Thread's vectors q (slice vector l = q B + threadIdx.x, unit vector
+// v0 + l) of a slice of sl_vec vectors of a unit whose nvec whole vectors
+// start at s.  Vectors outside [0, nvec) (a lead wraps v0 + l past it) or
+// past the slice are zeros (kBuf) or left unset (callers use only the
+// others).
+template <int B, int U, bool kBuf>
+__device__ __forceinline__ void load_slice(u32x4 (&x)[U], const u32x4* s, uint32_t nvec, uint32_t v0,
+                                           uint32_t sl_vec) {
+  if constexpr (kBuf) {
+    const rsrc_t in = make_rsrc(s, 16 * nvec);
+#pragma unroll
+    for (int q = 0; q < U; q++) {
+      const uint32_t l = q * B + threadIdx.x;
+      x[q] = ld_buf(in, l < sl_vec ? 16 * (v0 + l) : kOob);
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < U; q++) {
+      const uint32_t l = q * B + threadIdx.x, v = v0 + l;
+      if (l < sl_vec && v < nvec) x[q] = ld_nt(s + v);
+    }
+  }
+}
+
 // FRSUM-128 contribution of four consecutive words whose 0-based word index
 // within the chunk starts at i0: sum += w, wsum += (index + 1) * w.
 __device__ __forceinline__ void acc4(const u32x4& x, uint32_t i0, u64& s, u64& ws) {
@@ -233,7 +275,9 @@ __device__ __forceinline__ u64 acc_index(const Walk& wk, uint32_t c, uint32_t j)
 // kStore: pack (copy non-derived chunks into the payload); otherwise
 // checksum only.  Sums of the bytes read at src go to acc (zeroed), every
 // chunk's own accumulators; derived entries are read and summed only.
-template <int B, int U, bool kStore>
+// kBuf: the slices' loads through a buffer resource (all in flight at
+// once), else predicated global loads.
+template <int B, int U, bool kStore, bool kBuf>
 __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, Walk wk,
                                             const uint8_t* __restrict__ src,
                                             uint8_t* __restrict__ payload,
@@ -264,12 +308,8 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
     u32x4* d = reinterpret_cast<u32x4*>(payload + (store ? r.pay_off : 0));
     u64 acc[2] = {0, 0};
     u32x4 x[U];
-#pragma unroll
-    for (int q = 0; q < U; q++) {
-      const uint32_t l = q * B + threadIdx.x, v = v0 + l;
-      if (l < wk.sl_vec && v < nvec) x[q] = ld_nt(s + v);
-    }
-#pragma unroll
+    load_slice<B, U, kBuf>(x, s, nvec, v0, wk.sl_vec);
+  #pragma unroll
     for (int q = 0; q < U; q++) {
       const uint32_t l = q * B + threadIdx.x, v = v0 + l;
       if (l < wk.sl_vec && v < nvec) {
@@ -302,6 +342,116 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
   }
 }
 
+// Pack walked by blocks of the payload: workgroup b writes the payload's
+// vectors [b T, (b + 1) T) (T = B U, the tile), whatever chunks they belong
+// to, so that every workgroup stores one whole aligned tile of the payload
+// even where segments start inside lines.  Vector o of the payload belongs to
+// the last sent chunk u with u.pay_off / 16 <= o: its data, its ragged tail
+// (zero-padded) or the zero gap after it.  A block's chunks are found from
+// the first one (`first`, XCD-major like a slot table) on; its sums are
+// reduced once per chunk it touches.  The chunks without payload (derived
+// entries: read and summed only) are walked by k_pack in a launch of their
+// own.
+struct PackBlocksArgs {
+  const SrcUnit* pay_units;  // sent chunks in payload order
+  const uint32_t* first;     // per block, XCD-major: index of the unit holding its first vector
+  u64 n_units, n_blocks, stride, pay_vecs;
+};
+
+template <int B, int U>
+__device__ __forceinline__ void pack_block(const PackBlocksArgs& a, const Walk& wk, u64 b,
+                                           const uint8_t* __restrict__ src,
+                                           uint8_t* __restrict__ payload,
+                                           fr_chunk_sum* __restrict__ acc_out,
+                                           u64 (&lds)[2][B / 64][2], int& parity) {
+  constexpr uint32_t T = B * U;
+  const u64 v_blk = b * T;
+  // vectors of this block (T except in the last one); a thread's vector q is
+  // the block's vector l = q B + threadIdx.x, payload vector v_blk + l
+  const uint32_t n_here = uint32_t(v_blk + T < a.pay_vecs ? T : a.pay_vecs - v_blk);
+  const u64 v_end = v_blk + n_here;
+  const rsrc_t out = make_rsrc(payload + 16 * v_blk, 16 * n_here);
+  const u64 u0 = a.first[(b & 7) * a.stride + (b >> 3)];
+  // The block's units from u0 on, one pass each: block vectors [lb, le) of
+  // unit u are its vectors from du on.  Its data vectors are read through a
+  // resource that ends before its ragged tail (so the tail and the gap after
+  // the unit load as zeros), and the tail's thread reads the tail's bytes.
+  // (Loading two units' vectors together measured slower on the descriptor
+  // stress table: 5.70 against 5.77 TB/s.)
+  u64 u = u0;
+  uint32_t lb = 0;
+  while (true) {
+    const SrcUnit r = a.pay_units[u];
+    const u64 pn = u + 1 < a.n_units ? (a.pay_units[u + 1].pay_off >> 4) : a.pay_vecs;
+    const uint32_t le = pn < v_end ? uint32_t(pn - v_blk) : n_here;
+    const uint32_t du = u == u0 ? uint32_t(v_blk - (r.pay_off >> 4)) : 0u;
+    const uint32_t nvec = r.len >> 4;
+    const rsrc_t in = make_rsrc(src + r.src_off, 16 * nvec);
+    u32x4 x[U];
+#pragma unroll
+    for (int q = 0; q < U; q++) {
+      const uint32_t l = q * B + threadIdx.x;
+      x[q] = ld_buf(in, l >= lb && l < le ? 16 * (l - lb + du) : kOob);
+    }
+    const uint32_t lt = nvec - du + lb;  // block vector of the ragged tail
+    const bool tail = (r.len & 15) && nvec >= du && lt < le;
+    u32x4 tv = u32x4{0, 0, 0, 0};
+    if (tail && threadIdx.x == lt % B) tv = load_tail(src + r.src_off + 16 * u64(nvec), r.len & 15);
+    u64 t[2] = {0, 0};
+#pragma unroll
+    for (int q = 0; q < U; q++) {
+      const uint32_t l = q * B + threadIdx.x;
+      if (tail && l == lt) x[q] = tv;
+      if (l >= lb && l < le) {
+        st_buf(x[q], out, 16 * l);
+        acc4(x[q], 4 * (l - lb + du), t[0], t[1]);  // zeros (gap) add nothing
+      }
+    }
+    block_sum<B, 2>(t, lds, parity);
+    parity ^= 1;
+    if (threadIdx.x == 0) add_sum(acc_out + acc_index(wk, r.c, du / wk.sl_vec), t[0], t[1]);
+    if (le >= n_here) break;
+    u++;
+    lb = le;
+  }
+}
+
+template <int B, int U>
+__global__ __launch_bounds__(B) void k_pack_blocks(PackBlocksArgs a, Walk wk,
+                                                   const uint8_t* __restrict__ src,
+                                                   uint8_t* __restrict__ payload,
+                                                   fr_chunk_sum* __restrict__ acc_out) {
+  __shared__ u64 lds[2][B / 64][2];
+  int parity = 0;
+  for (u64 g = blockIdx.x; g < a.n_blocks; g += gridDim.x)
+    pack_block<B, U>(a, wk, g, src, payload, acc_out, lds, parity);
+}
+
+// First unit of every payload block (see k_pack_blocks): the last unit
+// starting at or before the block's first vector, by binary search over the
+// units' payload offsets (pay_off[4 u]: 32-byte unit records); written
+// XCD-major, zero past the blocks.
+__global__ __launch_bounds__(256) void k_block_first(const u64* __restrict__ pay_off, u64 n_units,
+                                                     u64 n_blocks, u64 stride, uint32_t block_vecs,
+                                                     uint32_t* __restrict__ out) {
+  const u64 total = 8 * stride;
+  for (u64 b = u64(blockIdx.x) * blockDim.x + threadIdx.x; b < total;
+       b += u64(gridDim.x) * blockDim.x) {
+    uint32_t v = 0;
+    if (b < n_blocks) {
+      const u64 o = b * block_vecs;
+      u64 lo = 0, hi = n_units;  // the first unit starts the payload: pay_off 0 <= o
+      while (hi - lo > 1) {
+        const u64 mid = (lo + hi) / 2;
+        if ((pay_off[4 * mid] >> 4) <= o) lo = mid;
+        else hi = mid;
+      }
+      v = uint32_t(lo);
+    }
+    out[(b & 7) * stride + (b >> 3)] = v;
+  }
+}
+
 // ---------------------------------------------------------------- unpack
 
 // Two kinds of units, listed by the walk in payload order (a derived group
@@ -319,7 +469,7 @@ __global__ __launch_bounds__(B) void k_pack(const SrcUnit* __restrict__ units, W
 // bytes to the receiver.  acc[0..1] get the master words' sums (relative to
 // master chunk m0 + part), acc[2..3] the parameter words'.  Returns false
 // for a slice past the group's end.
-template <int B, int U, bool kFromPayload>
+template <int B, int U, bool kFromPayload, bool kBuf>
 __device__ __forceinline__ bool derived_slice(const DerivedUnit& r, uint32_t j, const Walk& wk,
                                               uint32_t cvec, const uint8_t* msrc, uint8_t* dst,
                                               u64 (&acc)[4], uint32_t& part) {
@@ -333,11 +483,7 @@ __device__ __forceinline__ bool derived_slice(const DerivedUnit& r, uint32_t j, 
   u32x4* md = reinterpret_cast<u32x4*>(dst + r.m_dst_off);
   u32x2* pd = reinterpret_cast<u32x2*>(dst + r.p_dst_off);
   u32x4 x[U];
-#pragma unroll
-  for (int q = 0; q < U; q++) {
-    const uint32_t l = q * B + threadIdx.x, v = v0 + l;
-    if (l < wk.sl_vec && v < mvec) x[q] = ld_nt(s + v);
-  }
+  load_slice<B, U, kBuf>(x, s, mvec, v0, wk.sl_vec);
 #pragma unroll
   for (int q = 0; q < U; q++) {
     const uint32_t l = q * B + threadIdx.x, v = v0 + l;
@@ -379,7 +525,7 @@ __device__ __forceinline__ bool derived_slice(const DerivedUnit& r, uint32_t j, 
 // cut at slice boundaries of the payload (mode 3) starts the chunk's slices
 // lead_v vectors early (the first slice's leading lanes then come before the
 // chunk: their unsigned index wraps past nvec and they do nothing).
-template <int B, int U>
+template <int B, int U, bool kBuf>
 __device__ __forceinline__ bool plain_slice(const PlainUnit& r, uint32_t j, const Walk& wk,
                                             const uint8_t* payload, uint8_t* dst,
                                             u64 (&acc)[2]) {
@@ -393,11 +539,7 @@ __device__ __forceinline__ bool plain_slice(const PlainUnit& r, uint32_t j, cons
   const u32x4* s = reinterpret_cast<const u32x4*>(payload + r.pay_off);
   u32x4* d = reinterpret_cast<u32x4*>(dst + r.dst_off);
   u32x4 x[U];
-#pragma unroll
-  for (int q = 0; q < U; q++) {
-    const uint32_t l = q * B + threadIdx.x, v = v0 + l;
-    if (l < wk.sl_vec && v < nvec) x[q] = ld_nt(s + v);
-  }
+  load_slice<B, U, kBuf>(x, s, nvec, v0, wk.sl_vec);
 #pragma unroll
   for (int q = 0; q < U; q++) {
     const uint32_t l = q * B + threadIdx.x, v = v0 + l;
@@ -424,7 +566,7 @@ __device__ __forceinline__ bool plain_slice(const PlainUnit& r, uint32_t j, cons
   return true;
 }
 
-template <int B, int U>
+template <int B, int U, bool kBuf>
 __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ derived,
                                               const PlainUnit* __restrict__ plain, Walk wk,
                                               uint32_t cvec, const uint8_t* __restrict__ payload,
@@ -441,7 +583,7 @@ __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ de
       const uint32_t j = uint32_t(e) & ~kSlotDerived;
       u64 acc[4] = {0, 0, 0, 0};
       uint32_t part = 0;
-      if (!derived_slice<B, U, true>(r, j, wk, cvec, payload, dst, acc, part)) continue;
+      if (!derived_slice<B, U, true, kBuf>(r, j, wk, cvec, payload, dst, acc, part)) continue;
       block_sum<B, 4>(acc, lds, parity);
       parity ^= 1;
       if (threadIdx.x == 0) {
@@ -457,10 +599,139 @@ __global__ __launch_bounds__(B) void k_unpack(const DerivedUnit* __restrict__ de
       const PlainUnit r = plain[e >> 32];
       const uint32_t j = uint32_t(e);
       u64 acc[2] = {0, 0};
-      if (!plain_slice<B, U>(r, j, wk, payload, dst, acc)) continue;
+      if (!plain_slice<B, U, kBuf>(r, j, wk, payload, dst, acc)) continue;
       block_sum<B, 2>(acc, lds2, parity);
       parity ^= 1;
       if (threadIdx.x == 0) add_sum(acc_out + acc_index(wk, r.c, j), acc[0], acc[1]);
+    }
+  }
+}
+
+// Unpack walked by blocks of the receiver (for tables whose receiver chunks
+// start inside lines): workgroup g writes the plain chunks' bytes inside one
+// aligned tile of the receiver arena (T = B U vectors), so that no line is
+// written by two workgroups and every workgroup's writes fall in one
+// aligned tile; the gaps between entries are not touched.  Only tiles that
+// hold some chunk bytes are listed.  A chunk's data is read from its payload
+// segment and summed with its chunk-relative word indices; its ragged tail
+// is masked to its bytes (the payload's padding is not trusted).  The
+// derived groups (which write their masters too) are walked by k_unpack in
+// a launch of their own.
+struct UnpackBlocksArgs {
+  const PlainUnit* units;  // plain chunks in receiver order
+  const u64* blocks;       // listed tiles, XCD-major: (tile index << 32) | first unit touching it
+  u64 n_units, n_blocks, stride;
+};
+
+// One unit's part of a receiver tile: the unit's vectors from du on are the
+// tile's vectors from lb on.  Its ragged tail (if in the tile) is masked to
+// its bytes, written and added to t by the thread holding it.
+__device__ __forceinline__ void unpack_tile_tail(const PlainUnit& r, uint32_t lb, uint32_t du,
+                                                 uint32_t T, uint32_t B, const uint8_t* payload,
+                                                 uint8_t* dst, u64 (&t)[2]) {
+  const uint32_t nvec = r.len >> 4, tail = r.len & 15;
+  const uint32_t lt = nvec - du + lb;  // tile vector of the ragged tail
+  if (tail && nvec >= du && lt < T && threadIdx.x == lt % B) {
+    const u32x4 tv = mask_tail(ld_nt(reinterpret_cast<const u32x4*>(payload + r.pay_off) + nvec), tail);
+    store_tail(dst + r.dst_off + 16 * u64(nvec), tv, tail);
+    acc4(tv, 4 * nvec, t[0], t[1]);
+  }
+}
+
+template <int B, int U>
+__global__ __launch_bounds__(B) void k_unpack_blocks(UnpackBlocksArgs a, Walk wk,
+                                                     const uint8_t* __restrict__ payload,
+                                                     uint8_t* __restrict__ dst,
+                                                     fr_chunk_sum* __restrict__ acc_out) {
+  constexpr uint32_t T = B * U;
+  __shared__ u64 lds[2][B / 64][2];
+  int parity = 0;
+  for (u64 g = blockIdx.x; g < a.n_blocks; g += gridDim.x) {
+    const u64 e = a.blocks[(g & 7) * a.stride + (g >> 3)];
+    const u64 v_blk = (e >> 32) * T, v_end = v_blk + T;  // receiver vectors of the tile
+    const u64 u0 = uint32_t(e);
+    const PlainUnit r0 = a.units[u0];
+    const u64 dv0 = r0.dst_off >> 4;
+    const uint32_t lb0 = dv0 > v_blk ? uint32_t(dv0 - v_blk) : 0u;
+    const uint32_t du0 = v_blk > dv0 ? uint32_t(v_blk - dv0) : 0u;
+    const bool two = u0 + 1 < a.n_units && (a.units[u0 + 1].dst_off >> 4) < v_end;
+    const bool many = two && u0 + 2 < a.n_units && (a.units[u0 + 2].dst_off >> 4) < v_end;
+    if (!many) {
+      // One or two units, the common case: both units' loads in flight
+      // together.  A thread's vector belongs to unit 1 from lb1 on; every
+      // other vector outside a unit's data loads as zero and is not stored.
+      const PlainUnit r1 = two ? a.units[u0 + 1] : r0;
+      const uint32_t lb1 = two ? uint32_t((r1.dst_off >> 4) - v_blk) : T;
+      const rsrc_t in0 = make_rsrc(payload + r0.pay_off, 16 * (r0.len >> 4));
+      const rsrc_t out0 = make_rsrc(dst + r0.dst_off, 16 * (r0.len >> 4));
+      u32x4 x[U];
+#pragma unroll
+      for (int q = 0; q < U; q++) {
+        const uint32_t l = q * B + threadIdx.x;
+        x[q] = ld_buf(in0, l >= lb0 && l < lb1 ? 16 * (l - lb0 + du0) : kOob);
+      }
+      if (two) {
+        const rsrc_t in1 = make_rsrc(payload + r1.pay_off, 16 * (r1.len >> 4));
+        const rsrc_t out1 = make_rsrc(dst + r1.dst_off, 16 * (r1.len >> 4));
+        u32x4 y[U];
+#pragma unroll
+        for (int q = 0; q < U; q++) {
+          const uint32_t l = q * B + threadIdx.x;
+          y[q] = ld_buf(in1, l >= lb1 ? 16 * (l - lb1) : kOob);
+        }
+#pragma unroll
+        for (int q = 0; q < U; q++) {
+          const uint32_t l = q * B + threadIdx.x;
+          st_buf(y[q], out1, l >= lb1 ? 16 * (l - lb1) : kOob);
+          x[q] |= y[q];
+        }
+      }
+      u64 t0[2] = {0, 0}, t1[2] = {0, 0};
+#pragma unroll
+      for (int q = 0; q < U; q++) {
+        const uint32_t l = q * B + threadIdx.x;
+        st_buf(x[q], out0, l >= lb0 && l < lb1 ? 16 * (l - lb0 + du0) : kOob);
+        if (l >= lb1) acc4(x[q], 4 * (l - lb1), t1[0], t1[1]);  // zeros add nothing
+        else if (l >= lb0) acc4(x[q], 4 * (l - lb0 + du0), t0[0], t0[1]);
+      }
+      unpack_tile_tail(r0, lb0, du0, T, B, payload, dst, t0);
+      if (two) unpack_tile_tail(r1, lb1, 0, T, B, payload, dst, t1);
+      block_sum<B, 2>(t0, lds, parity);
+      parity ^= 1;
+      if (threadIdx.x == 0) add_sum(acc_out + acc_index(wk, r0.c, du0 / wk.sl_vec), t0[0], t0[1]);
+      if (two) {  // the second unit starts inside the tile: its slice 0
+        block_sum<B, 2>(t1, lds, parity);
+        parity ^= 1;
+        if (threadIdx.x == 0) add_sum(acc_out + acc_index(wk, r1.c, 0), t1[0], t1[1]);
+      }
+      continue;
+    }
+    // Three or more units (short entries): one pass per unit.
+    for (u64 u = u0; u < a.n_units; u++) {
+      const PlainUnit r = a.units[u];
+      const u64 dv = r.dst_off >> 4;
+      if (dv >= v_end) break;
+      const uint32_t lb = dv > v_blk ? uint32_t(dv - v_blk) : 0u;
+      const uint32_t du = v_blk > dv ? uint32_t(v_blk - dv) : 0u;
+      const rsrc_t in = make_rsrc(payload + r.pay_off, 16 * (r.len >> 4));
+      const rsrc_t out = make_rsrc(dst + r.dst_off, 16 * (r.len >> 4));
+      u32x4 x[U];
+#pragma unroll
+      for (int q = 0; q < U; q++) {
+        const uint32_t l = q * B + threadIdx.x;
+        x[q] = ld_buf(in, l >= lb ? 16 * (l - lb + du) : kOob);  // zeros past the data
+      }
+      u64 t[2] = {0, 0};
+#pragma unroll
+      for (int q = 0; q < U; q++) {
+        const uint32_t l = q * B + threadIdx.x;
+        st_buf(x[q], out, l >= lb ? 16 * (l - lb + du) : kOob);
+        if (l >= lb) acc4(x[q], 4 * (l - lb + du), t[0], t[1]);  // zeros add nothing
+      }
+      unpack_tile_tail(r, lb, du, T, B, payload, dst, t);
+      block_sum<B, 2>(t, lds, parity);
+      parity ^= 1;
+      if (threadIdx.x == 0) add_sum(acc_out + acc_index(wk, r.c, du / wk.sl_vec), t[0], t[1]);
     }
   }
 }
@@ -481,7 +752,7 @@ __global__ __launch_bounds__(B) void k_rederive(const DerivedUnit* __restrict__ 
     const uint32_t j = uint32_t(e) & ~kSlotDerived;
     u64 acc[4] = {0, 0, 0, 0};
     uint32_t part = 0;
-    if (!derived_slice<B, U, false>(r, j, wk, cvec, dst, dst, acc, part)) continue;
+    if (!derived_slice<B, U, false, false>(r, j, wk, cvec, dst, dst, acc, part)) continue;
     block_sum<B, 4>(acc, lds, parity);
     parity ^= 1;
     if (threadIdx.x == 0)
@@ -493,7 +764,7 @@ __global__ __launch_bounds__(B) void k_rederive(const DerivedUnit* __restrict__ 
 
 // flags[c] <- 1 when any slice of chunk c differs (flags zeroed); with kSums
 // the sums of both arenas go to acc_a / acc_b (zeroed).
-template <int B, int U, bool kSums>
+template <int B, int U, bool kSums, bool kBuf>
 __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units, Walk wk,
                                               const uint8_t* __restrict__ a,
                                               const uint8_t* __restrict__ b,
@@ -519,14 +790,8 @@ __global__ __launch_bounds__(B) void k_verify(const SrcUnit* __restrict__ units,
     u64 acc[4] = {0, 0, 0, 0};
     uint32_t diff = 0;
     u32x4 xa[U], xb[U];
-#pragma unroll
-    for (int q = 0; q < U; q++) {
-      const uint32_t l = q * B + threadIdx.x, v = v0 + l;
-      if (l < wk.sl_vec && v < nvec) {
-        xa[q] = ld_nt(pa + v);
-        xb[q] = ld_nt(pb + v);
-      }
-    }
+    load_slice<B, U, kBuf>(xa, pa, nvec, v0, wk.sl_vec);
+    load_slice<B, U, kBuf>(xb, pb, nvec, v0, wk.sl_vec);
 #pragma unroll
     for (int q = 0; q < U; q++) {
       const uint32_t l = q * B + threadIdx.x, v = v0 + l;
@@ -1012,12 +1277,15 @@ int pack_impl(bool store, const SrcUnit* units, const SlotTable& slots, uint32_t
   if (e) return e;
   const auto* s = static_cast<const uint8_t*>(src);
   auto* p = static_cast<uint8_t*>(payload);
-  if (store)
-    hipLaunchKernelGGL((k_pack<B, U, true>), dim3(grid_of<B>(wk, cfg)), dim3(B), 0, st, units, wk,
-                       s, p, scr.acc);
+  const dim3 grid(grid_of<B>(wk, cfg));
+  if (store && cfg.buf_pack)
+    hipLaunchKernelGGL((k_pack<B, U, true, true>), grid, dim3(B), 0, st, units, wk, s, p, scr.acc);
+  else if (store)
+    hipLaunchKernelGGL((k_pack<B, U, true, false>), grid, dim3(B), 0, st, units, wk, s, p, scr.acc);
+  else if (cfg.buf_checksum)
+    hipLaunchKernelGGL((k_pack<B, U, false, true>), grid, dim3(B), 0, st, units, wk, s, p, scr.acc);
   else
-    hipLaunchKernelGGL((k_pack<B, U, false>), dim3(grid_of<B>(wk, cfg)), dim3(B), 0, st, units, wk,
-                       s, p, scr.acc);
+    hipLaunchKernelGGL((k_pack<B, U, false, false>), grid, dim3(B), 0, st, units, wk, s, p, scr.acc);
   e = int(hipGetLastError());
   if (e) return e;
   FinalArgs f{};
@@ -1026,6 +1294,45 @@ int pack_impl(bool store, const SrcUnit* units, const SlotTable& slots, uint32_t
   f.n_chunks = n_chunks;
   f.g_shift = wk.g_shift;
   f.live = wk.count;  // a list built on the device: its length
+  return launch_finalize(kFold, f, st);
+}
+
+template <int B, int U>
+int pack_blocks_impl(const SrcUnit* units, const PackBlocks& pb, uint32_t n_chunks, uint64_t C,
+                     const void* src, void* payload, fr_chunk_sum* sums, const Scratch& scr,
+                     const LaunchCfg& cfg, hipStream_t st) {
+  if (n_chunks == 0) return 0;
+  const Walk wk = walk_for(C, B * U * 16, pb.extra);
+  Zeroes z;
+  z.add(scr.acc, (u64(n_chunks) << wk.g_shift) * sizeof(fr_chunk_sum));
+  int e = z.launch(st);
+  if (e) return e;
+  PackBlocksArgs a;
+  a.pay_units = pb.units;
+  a.first = pb.first;
+  a.n_units = pb.n_units;
+  a.n_blocks = pb.n_blocks;
+  a.stride = pb.stride;
+  a.pay_vecs = pb.pay_vecs;
+  const auto* s = static_cast<const uint8_t*>(src);
+  auto* p = static_cast<uint8_t*>(payload);
+  if (a.n_blocks) {
+    hipLaunchKernelGGL((k_pack_blocks<B, U>), dim3(grid_for<B>(a.n_blocks, cfg)), dim3(B), 0, st, a,
+                       wk, s, p, scr.acc);
+    e = int(hipGetLastError());
+    if (e) return e;
+  }
+  if (wk.n_slices) {
+    hipLaunchKernelGGL((k_pack<B, U, true, true>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0,
+                       st, units, wk, s, p, scr.acc);
+    e = int(hipGetLastError());
+    if (e) return e;
+  }
+  FinalArgs f{};
+  f.acc = scr.acc;
+  f.out = sums;
+  f.n_chunks = n_chunks;
+  f.g_shift = wk.g_shift;
   return launch_finalize(kFold, f, st);
 }
 
@@ -1039,10 +1346,56 @@ int unpack_impl(const UnpackArgs& u, const LaunchCfg& cfg, hipStream_t st) {
   int e = z.launch(st);
   if (e || u.n_chunks == 0) return e;
   if (wk.n_slices) {
-    hipLaunchKernelGGL((k_unpack<B, U>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0, st,
-                       u.derived, u.plain, wk, uint32_t(u.C >> 4),
-                       static_cast<const uint8_t*>(u.payload), static_cast<uint8_t*>(u.dst),
-                       u.scratch.acc);
+    if (cfg.buf_unpack)
+      hipLaunchKernelGGL((k_unpack<B, U, true>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0, st,
+                         u.derived, u.plain, wk, uint32_t(u.C >> 4),
+                         static_cast<const uint8_t*>(u.payload), static_cast<uint8_t*>(u.dst),
+                         u.scratch.acc);
+    else
+      hipLaunchKernelGGL((k_unpack<B, U, false>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0, st,
+                         u.derived, u.plain, wk, uint32_t(u.C >> 4),
+                         static_cast<const uint8_t*>(u.payload), static_cast<uint8_t*>(u.dst),
+                         u.scratch.acc);
+    e = int(hipGetLastError());
+    if (e) return e;
+  }
+  FinalArgs f{};
+  f.acc = u.scratch.acc;
+  f.sent = u.sums;
+  f.bitmap = u.bitmap;
+  f.count = reinterpret_cast<u64*>(u.n_bad);
+  f.n_chunks = u.n_chunks;
+  f.g_shift = wk.g_shift;
+  return launch_finalize(kCompare, f, st);
+}
+
+template <int B, int U>
+int unpack_blocks_impl(const UnpackArgs& u, const UnpackBlocks& ub, const LaunchCfg& cfg,
+                       hipStream_t st) {
+  const Walk wk = walk_for(u.C, B * U * 16, ub.derived);
+  const u64 n_acc = u64(u.n_chunks) << wk.g_shift;
+  Zeroes z;
+  z.add(u.scratch.acc, n_acc * sizeof(fr_chunk_sum));
+  z.add(u.n_bad, 8);
+  int e = z.launch(st);
+  if (e || u.n_chunks == 0) return e;
+  const auto* pay = static_cast<const uint8_t*>(u.payload);
+  auto* dst = static_cast<uint8_t*>(u.dst);
+  if (ub.n_blocks) {
+    UnpackBlocksArgs a;
+    a.units = ub.units;
+    a.blocks = reinterpret_cast<const u64*>(ub.blocks);
+    a.n_units = ub.n_units;
+    a.n_blocks = ub.n_blocks;
+    a.stride = ub.stride;
+    hipLaunchKernelGGL((k_unpack_blocks<B, U>), dim3(grid_for<B>(ub.n_blocks, cfg)), dim3(B), 0, st,
+                       a, wk, pay, dst, u.scratch.acc);
+    e = int(hipGetLastError());
+    if (e) return e;
+  }
+  if (wk.n_slices) {  // the derived groups
+    hipLaunchKernelGGL((k_unpack<B, U, false>), dim3(grid_for<B>(wk.n_slices, cfg)), dim3(B), 0, st,
+                       u.derived, u.plain, wk, uint32_t(u.C >> 4), pay, dst, u.scratch.acc);
     e = int(hipGetLastError());
     if (e) return e;
   }
@@ -1070,7 +1423,7 @@ int unpack_delta_impl(const UnpackDeltaArgs& u, const LaunchCfg& cfg, hipStream_
   if (e || u.n_ids == 0) return e;
   const uint32_t cvec = uint32_t(u.C >> 4);
   if (wp.n_slices) {  // sent chunks first: the masters the second phase reads
-    hipLaunchKernelGGL((k_unpack<B, U>), dim3(grid_of<B>(wp, cfg)), dim3(B), 0, st,
+    hipLaunchKernelGGL((k_unpack<B, U, false>), dim3(grid_of<B>(wp, cfg)), dim3(B), 0, st,
                        static_cast<const DerivedUnit*>(nullptr), u.plain, wp, cvec,
                        static_cast<const uint8_t*>(u.payload), static_cast<uint8_t*>(u.dst),
                        u.scratch.acc);
@@ -1114,11 +1467,17 @@ int verify_impl(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks,
   const auto* pa = static_cast<const uint8_t*>(a);
   const auto* pb = static_cast<const uint8_t*>(b);
   const dim3 grid(grid_for<B>(wk.n_slices, cfg));
-  if (sums_a)
-    hipLaunchKernelGGL((k_verify<B, U, true>), grid, dim3(B), 0, st, units, wk, pa, pb,
+  if (sums_a && cfg.buf_verify)
+    hipLaunchKernelGGL((k_verify<B, U, true, true>), grid, dim3(B), 0, st, units, wk, pa, pb,
+                       scr.flags, scr.acc, scr.acc_b);
+  else if (sums_a)
+    hipLaunchKernelGGL((k_verify<B, U, true, false>), grid, dim3(B), 0, st, units, wk, pa, pb,
+                       scr.flags, scr.acc, scr.acc_b);
+  else if (cfg.buf_verify)
+    hipLaunchKernelGGL((k_verify<B, U, false, true>), grid, dim3(B), 0, st, units, wk, pa, pb,
                        scr.flags, scr.acc, scr.acc_b);
   else
-    hipLaunchKernelGGL((k_verify<B, U, false>), grid, dim3(B), 0, st, units, wk, pa, pb,
+    hipLaunchKernelGGL((k_verify<B, U, false, false>), grid, dim3(B), 0, st, units, wk, pa, pb,
                        scr.flags, scr.acc, scr.acc_b);
   e = int(hipGetLastError());
   if (e) return e;
@@ -1221,6 +1580,24 @@ int launch_pack(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks,
               cfg, hipStream_t(stream));
 }
 
+int launch_pack_blocks(const SrcUnit* units, const PackBlocks& pb, uint32_t n_chunks, uint64_t C,
+                       const void* src, void* payload, fr_chunk_sum* sums, const Scratch& scr,
+                       const LaunchCfg& cfg, void* stream) {
+  FR_DISPATCH(cfg.tile_pack, pack_blocks_impl, units, pb, n_chunks, C, src, payload, sums, scr, cfg,
+              hipStream_t(stream));
+}
+
+int launch_block_first(const uint64_t* pay_off, uint64_t n_units, uint64_t n_blocks,
+                       uint64_t stride, uint32_t block_vecs, uint32_t* out, void* stream) {
+  const u64 total = 8 * stride;
+  if (total == 0) return 0;
+  const u64 want = (total + 255) / 256;
+  const uint32_t blocks = uint32_t(want < 65536 ? want : 65536);
+  hipLaunchKernelGGL(k_block_first, dim3(blocks), dim3(256), 0, hipStream_t(stream),
+                     reinterpret_cast<const u64*>(pay_off), u64(n_units), u64(n_blocks), u64(stride), block_vecs, out);
+  return int(hipGetLastError());
+}
+
 int launch_checksum(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks, uint64_t C,
                     const void* base, fr_chunk_sum* sums, const Scratch& scr,
                     const LaunchCfg& cfg, void* stream) {
@@ -1230,6 +1607,11 @@ int launch_checksum(const SrcUnit* units, const SlotTable& slots, uint32_t n_chu
 
 int launch_unpack(const UnpackArgs& u, const LaunchCfg& cfg, void* stream) {
   FR_DISPATCH(cfg.tile_unpack, unpack_impl, u, cfg, hipStream_t(stream));
+}
+
+int launch_unpack_blocks(const UnpackArgs& u, const UnpackBlocks& ub, const LaunchCfg& cfg,
+                         void* stream) {
+  FR_DISPATCH(cfg.tile_unpack, unpack_blocks_impl, u, ub, cfg, hipStream_t(stream));
 }
 
 int launch_unpack_delta(const UnpackDeltaArgs& u, const LaunchCfg& cfg, void* stream) {

@@ -23,10 +23,23 @@ thread_local int g_last_hip_error = 0;
 // 8B and 70B rank shares and the descriptor stress table.
 constexpr uint32_t kDefaultTilePack = 4, kDefaultTileUnpack = 5, kDefaultTileVerify = 5,
                    kDefaultTileChecksum = 3;
-// Line-aligned walks (0 off, 1 at lines of the arena read, 2 at lines of the
-// payload written): pack cuts at payload lines, the compare at arena lines.
-constexpr int kDefaultLinePack = 2, kDefaultLineUnpack = 1, kDefaultLineVerify = 1,
+// Walks (0 plain; 1 cut at lines of the arena read, for unpack of the
+// receiver; 2 at lines of the payload; 4 by blocks of the payload): pack and
+// unpack by payload blocks when payload chunks start inside lines (16-byte
+// segments of tensors whose sizes are not multiples of 128 bytes), else pack
+// at payload lines and unpack at receiver lines (both plain walks when every
+// chunk starts on a line); the compare at arena lines.
+constexpr int kDefaultLinePack = kLineAuto, kDefaultLineUnpack = kLineAuto, kDefaultLineVerify = 1,
               kDefaultLineChecksum = 0;
+constexpr int kAlignedLinePack = 2, kAlignedLineUnpack = 1;
+// Slice walks loading through buffer resources (every load of a thread in
+// flight at once) instead of predicated global loads: off by default.  On
+// MI355X they made pack 2.5 % slower and the stress table's pack 2-3 %
+// faster (the block walk that table takes is faster still), unpack 1.5-2.5 %
+// slower, the checksum no faster, and the compare between 0.5 % slower and
+// 1.3 % faster from one box to the next.
+constexpr uint32_t kDefaultBufPack = 0, kDefaultBufUnpack = 0, kDefaultBufVerify = 0,
+                   kDefaultBufChecksum = 0;
 // Whether a line-aligned pack / unpack walk lets a unit's last slice absorb
 // the lead instead of adding a slice.
 constexpr uint32_t kDefaultAbsorbPack = 1, kDefaultAbsorbUnpack = 1, kDefaultAbsorbVerify = 0,
@@ -120,7 +133,7 @@ int validate_and_layout(const fr_tensor_desc* t, uint32_t n, uint64_t C, uint64_
 }
 
 static void fill_info(const Layout& L, uint32_t n, uint64_t src, uint64_t dst, int64_t dev,
-                      fr_plan_info* info) {
+                      fr_plan_info* info, uint32_t pack_walk = 0, uint32_t unpack_walk = 0) {
   info->n_entries = n;
   info->chunk_bytes = L.C;
   info->n_chunks = L.n_chunks;
@@ -132,6 +145,8 @@ static void fill_info(const Layout& L, uint32_t n, uint64_t src, uint64_t dst, i
   info->device = dev;
   info->segment_align = L.seg;
   info->delta_payload_max = L.delta_payload_max;
+  info->pack_walk = pack_walk;
+  info->unpack_walk = unpack_walk;
 }
 
 static uint32_t env_u32(const char* name, uint32_t dflt) {
@@ -256,6 +271,10 @@ extern "C" int fr_plan_destroy(fr_plan* p) {
   for (auto& w : p->src_walks)
     if (w.mem) (void)hipFree(w.mem);
   if (p->unpack_walk.mem) (void)hipFree(p->unpack_walk.mem);
+  if (p->pack_extra.mem) (void)hipFree(p->pack_extra.mem);
+  if (p->d_blocks) (void)hipFree(p->d_blocks);
+  if (p->unpack_derived.mem) (void)hipFree(p->unpack_derived.mem);
+  if (p->d_ublocks) (void)hipFree(p->d_ublocks);
   if (p->d_derived) (void)hipFree(p->d_derived);
   if (p->d_plain) (void)hipFree(p->d_plain);
   if (p->d_scratch) (void)hipFree(p->d_scratch);
@@ -285,24 +304,30 @@ LaunchCfg launch_config() {
   cfg.tile_unpack = pick("FLASHRESTORE_TILE_UNPACK", kDefaultTileUnpack);
   cfg.tile_verify = pick("FLASHRESTORE_TILE_VERIFY", kDefaultTileVerify);
   cfg.tile_checksum = pick("FLASHRESTORE_TILE_CHECKSUM", kDefaultTileChecksum);
-  // line-aligned walks: 0 off, 1 lines of the arena read (for unpack: of the
-  // receiver arena written), 2 payload lines, 3 payload slices (pack takes
-  // 1-3, unpack 1-3; compare and checksum 0 or 1, any nonzero value
-  // meaning 1); FLASHRESTORE_LINE sets all four
+  // walks: 0 plain, 1 lines of the arena read (for unpack: of the receiver
+  // arena written), 2 payload lines, 3 payload slices, 4 payload blocks
+  // (pack and unpack take 1-4; compare and checksum 0 or 1, any nonzero
+  // value meaning 1); FLASHRESTORE_LINE sets all four; unset, pack and
+  // unpack choose by the table (kLineAuto)
   const uint32_t lall = env_u32("FLASHRESTORE_LINE", ~0u);
   auto lpick = [&](const char* name, int dflt, uint32_t modes) {
-    const uint32_t v = env_u32(name, lall != ~0u ? lall : uint32_t(dflt));
+    const uint32_t v = env_u32(name, lall);
+    if (v == ~0u) return dflt;
     if (v == 0) return 0;
-    if (v < 4 && (modes >> v) & 1u) return int(v);
+    if (v < 5 && (modes >> v) & 1u) return int(v);
     return (modes >> 1) & 1u ? 1 : 0;  // the operation's nearest mode
   };
-  cfg.line_pack = lpick("FLASHRESTORE_LINE_PACK", kDefaultLinePack, 0xE);
-  cfg.line_unpack = lpick("FLASHRESTORE_LINE_UNPACK", kDefaultLineUnpack, 0xE);
+  cfg.line_pack = lpick("FLASHRESTORE_LINE_PACK", kDefaultLinePack, 0x1E);
+  cfg.line_unpack = lpick("FLASHRESTORE_LINE_UNPACK", kDefaultLineUnpack, 0x1E);
   cfg.absorb_pack = int(env_u32("FLASHRESTORE_ABSORB_PACK", kDefaultAbsorbPack) != 0);
   cfg.absorb_unpack = int(env_u32("FLASHRESTORE_ABSORB_UNPACK", kDefaultAbsorbUnpack) != 0);
   cfg.absorb_verify = int(env_u32("FLASHRESTORE_ABSORB_VERIFY", kDefaultAbsorbVerify) != 0);
   cfg.absorb_checksum = int(env_u32("FLASHRESTORE_ABSORB_CHECKSUM", kDefaultAbsorbChecksum) != 0);
   cfg.line_verify = lpick("FLASHRESTORE_LINE_VERIFY", kDefaultLineVerify, 0x2);
+  cfg.buf_pack = int(env_u32("FLASHRESTORE_BUF_PACK", kDefaultBufPack) != 0);
+  cfg.buf_unpack = int(env_u32("FLASHRESTORE_BUF_UNPACK", kDefaultBufUnpack) != 0);
+  cfg.buf_verify = int(env_u32("FLASHRESTORE_BUF_VERIFY", kDefaultBufVerify) != 0);
+  cfg.buf_checksum = int(env_u32("FLASHRESTORE_BUF_CHECKSUM", kDefaultBufChecksum) != 0);
   cfg.line_checksum = lpick("FLASHRESTORE_LINE_CHECKSUM", kDefaultLineChecksum, 0x2);
   return cfg;
 }
@@ -412,6 +437,7 @@ int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units, const Staging
                         {p->cfg.tile_checksum, p->cfg.line_checksum, p->cfg.absorb_checksum},
                         {p->cfg.tile_verify, p->cfg.line_verify, p->cfg.absorb_verify}};
   for (const Want& tw : walks) {
+    if (&tw == &walks[0] && p->cfg.line_pack == kLineBlocks) continue;  // build_pack_blocks
     const uint32_t sl = slice_bytes(L.C, tw.tile);
     const uint32_t shift = line_walk(p, tw.tile, tw.line);
     const uint32_t absorb = shift && tw.absorb ? 1u : 0u;
@@ -432,6 +458,101 @@ int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units, const Staging
     if (rc != FR_OK) return rc;
   }
   return FR_OK;
+}
+
+// Pack by blocks of the payload (PackBlocks): the sent chunks' units in
+// payload order, each block's first unit (found on the device), and a plain
+// walk of the chunks without payload.
+int build_pack_blocks(fr_plan* p, const std::vector<SrcUnit>& units, const Staging& st) {
+  const Layout& L = p->layout;
+  const uint32_t block_vecs = tile_bytes(p->cfg.tile_pack) / 16;
+  std::vector<SrcUnit> pay;
+  pay.reserve(L.n_sent_chunks);
+  SlotRuns b;
+  b.sl = slice_bytes(L.C, p->cfg.tile_pack);
+  for (uint64_t c = 0; c < units.size(); c++) {
+    if (units[c].pay_off != kNoPayload) pay.push_back(units[c]);
+    else b.add(uint32_t(c), units[c].len, 0);
+  }
+  PackBlocks& pb = p->pack_blocks;
+  pb.n_units = pay.size();
+  pb.pay_vecs = pay.empty() ? 0 : L.payload_bytes / 16;
+  pb.n_blocks = (pb.pay_vecs + block_vecs - 1) / block_vecs;
+  pb.stride = (pb.n_blocks + 7) / 8;
+  const uint64_t b_units = (pay.size() * sizeof(SrcUnit) + 255) & ~uint64_t(255);
+  int rc = upload(nullptr, b_units + 8 * pb.stride * sizeof(uint32_t), &p->d_blocks, st.s);
+  if (rc == FR_OK && p->d_blocks) {
+    auto* q = static_cast<uint8_t*>(p->d_blocks);
+    pb.units = reinterpret_cast<const SrcUnit*>(q);
+    pb.first = reinterpret_cast<const uint32_t*>(q + b_units);
+    rc = copy_in(q, pay.data(), pay.size() * sizeof(SrcUnit), st.s);
+    if (rc == FR_OK) {
+      hipError_t e = hipError_t(launch_block_first(&pb.units->pay_off, pb.n_units, pb.n_blocks,
+                                                   pb.stride, block_vecs,
+                                                   reinterpret_cast<uint32_t*>(q + b_units), st.s));
+      if (e == hipSuccess) e = hipStreamSynchronize(st.s);
+      if (e != hipSuccess) rc = hip_fail(e);
+    }
+  }
+  if (rc == FR_OK) rc = upload_walk(b, p->pack_extra, st);
+  pb.extra = p->pack_extra.t;
+  return rc;
+}
+
+// Unpack by blocks of the receiver (UnpackBlocks): the plain chunks sorted
+// by receiver offset, the receiver tiles that hold some of their bytes with
+// the first chunk touching each (XCD-major), and the walk of the derived
+// groups in table order (ids into d_derived, as unpack_units lists them).
+int build_unpack_blocks(fr_plan* p, const std::vector<ChunkRec>& recs,
+                        const std::vector<uint8_t>& is_master, const Staging& st) {
+  const Layout& L = p->layout;
+  const uint64_t tile_vecs = tile_bytes(p->cfg.tile_unpack) / 16;
+  std::vector<PlainUnit> units;
+  units.reserve(L.n_sent_chunks);
+  SlotRuns b;
+  b.sl = slice_bytes(L.C, p->cfg.tile_unpack);
+  uint32_t id = 0;
+  for (uint32_t k = 0; k < p->table.size(); k++) {
+    const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];
+    for (uint64_t c = c0; c < c1; c++) {
+      if (p->table[k].derive_from >= 0) {
+        b.add(id++, 2 * uint64_t(recs[c].len), kSlotDerived);
+      } else if (!is_master[k]) {
+        PlainUnit u{};
+        u.pay_off = recs[c].pay_off;
+        u.dst_off = recs[c].dst_off;
+        u.len = recs[c].len;
+        u.c = uint32_t(c);
+        units.push_back(u);
+      }
+    }
+  }
+  std::sort(units.begin(), units.end(),
+            [](const PlainUnit& x, const PlainUnit& y) { return x.dst_off < y.dst_off; });
+  std::vector<uint64_t> tiles;  // (tile << 32) | first unit, in receiver order
+  for (uint64_t u = 0; u < units.size(); u++) {
+    const uint64_t v0 = units[u].dst_off / 16, v1 = v0 + (units[u].len + 15) / 16;
+    for (uint64_t t = v0 / tile_vecs; t * tile_vecs < v1; t++)
+      if (tiles.empty() || (tiles.back() >> 32) < t) tiles.push_back((t << 32) | u);
+  }
+  UnpackBlocks& ub = p->unpack_blocks;
+  ub.n_units = units.size();
+  ub.n_blocks = tiles.size();
+  ub.stride = (ub.n_blocks + 7) / 8;
+  std::vector<uint64_t> xcd(8 * ub.stride, 0);
+  for (uint64_t g = 0; g < tiles.size(); g++) xcd[(g & 7) * ub.stride + (g >> 3)] = tiles[g];
+  const uint64_t b_units = (units.size() * sizeof(PlainUnit) + 255) & ~uint64_t(255);
+  int rc = upload(nullptr, b_units + xcd.size() * sizeof(uint64_t), &p->d_ublocks, st.s);
+  if (rc == FR_OK && p->d_ublocks) {
+    auto* q = static_cast<uint8_t*>(p->d_ublocks);
+    ub.units = reinterpret_cast<const PlainUnit*>(q);
+    ub.blocks = reinterpret_cast<const uint64_t*>(q + b_units);
+    rc = copy_in(q, units.data(), units.size() * sizeof(PlainUnit), st.s);
+    if (rc == FR_OK) rc = copy_in(q + b_units, xcd.data(), xcd.size() * sizeof(uint64_t), st.s);
+  }
+  if (rc == FR_OK) rc = upload_walk(b, p->unpack_derived, st);
+  ub.derived = p->unpack_derived.t;
+  return rc;
 }
 
 // Walk of unpack, in payload (table) order: a derived entry's groups (their
@@ -591,6 +712,12 @@ extern "C" int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n, uint64
     p->n_plain = uint32_t(plain.size());
     for (const PlainUnit& u : plain) p->dst_align = std::min(p->dst_align, pow2_align(u.dst_off));
     const std::vector<SrcUnit> units = src_units(recs, n, L, &p->src_align, &p->pay_align);
+    // automatic walks: blocks where chunks of the side written start inside lines
+    auto resolve = [](int mode, uint32_t align, int aligned) {
+      return mode != kLineAuto ? mode : align < kLine ? kLineBlocks : aligned;
+    };
+    p->cfg.line_pack = resolve(p->cfg.line_pack, p->pay_align, kAlignedLinePack);
+    p->cfg.line_unpack = resolve(p->cfg.line_unpack, p->dst_align, kAlignedLineUnpack);
 
     Staging st;
     const hipError_t es = hipStreamCreateWithFlags(&st.s, hipStreamNonBlocking);
@@ -603,7 +730,9 @@ extern "C" int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n, uint64
     if (rc == FR_OK)
       rc = upload(units.data(), units.size() * sizeof(SrcUnit), (void**)&p->d_units, st.s);
     if (rc == FR_OK) rc = build_src_walks(p, units, st);
-    if (rc == FR_OK) rc = build_unpack_walk(p, recs, is_master, st);
+    if (rc == FR_OK && p->cfg.line_pack == kLineBlocks) rc = build_pack_blocks(p, units, st);
+    if (rc == FR_OK && p->cfg.line_unpack != kLineBlocks) rc = build_unpack_walk(p, recs, is_master, st);
+    if (rc == FR_OK && p->cfg.line_unpack == kLineBlocks) rc = build_unpack_blocks(p, recs, is_master, st);
     if (rc == FR_OK)
       rc = upload(derived.data(), derived.size() * sizeof(DerivedUnit), (void**)&p->d_derived,
                   st.s);
@@ -629,8 +758,15 @@ extern "C" int fr_plan_create(const fr_tensor_desc* table, uint32_t n, uint64_t 
 
 extern "C" int fr_plan_get_info(const fr_plan* p, fr_plan_info* info) {
   if (!p || !info) return FR_E_INVAL;
+  // the walks the operations take (a line-aligned mode is the plain walk
+  // where every chunk of its side starts on a line)
+  const LaunchCfg& c = p->cfg;
+  const uint32_t pw = c.line_pack == kLineBlocks ? uint32_t(kLineBlocks)
+                                                 : line_walk(p, c.tile_pack, c.line_pack);
+  const uint32_t uw = c.line_unpack == kLineBlocks ? uint32_t(kLineBlocks)
+                                                   : line_walk(p, c.tile_unpack, c.line_unpack, true);
   fill_info(p->layout, uint32_t(p->table.size()), p->src_arena_bytes, p->dst_arena_bytes,
-            p->device, info);
+            p->device, info, pw, uw);
   return FR_OK;
 }
 

@@ -51,6 +51,8 @@ class fr_plan_info(C.Structure):
         ("device", C.c_int64),
         ("segment_align", C.c_uint64),
         ("delta_payload_max", C.c_uint64),
+        ("pack_walk", C.c_uint32),
+        ("unpack_walk", C.c_uint32),
     ]
 
     def as_dict(self):
@@ -130,7 +132,7 @@ def _load():
         f.argtypes = args
         f.restype = C.c_int
     lib.fr_strerror.restype = C.c_char_p
-    if lib.fr_abi_version() != 4:
+    if lib.fr_abi_version() != 5:
         raise ImportError("libflashrestore ABI version mismatch")
     return lib
 

@@ -28,6 +28,12 @@ int launch_delta_build(const DeltaBuild&, bool, void*) { return 1; }
 int launch_ids_to_bits(const uint32_t*, uint64_t, uint32_t*, uint64_t, void*) { return 1; }
 int launch_pack(const SrcUnit*, const SlotTable&, uint32_t, uint64_t, const void*, void*,
                 fr_chunk_sum*, const Scratch&, const LaunchCfg&, void*) { return 1; }
+int launch_pack_blocks(const SrcUnit*, const PackBlocks&, uint32_t, uint64_t, const void*, void*,
+                       fr_chunk_sum*, const Scratch&, const LaunchCfg&, void*) { return 1; }
+int launch_block_first(const uint64_t*, uint64_t, uint64_t, uint64_t, uint32_t, uint32_t*, void*) {
+  return 1;
+}
+int launch_unpack_blocks(const UnpackArgs&, const UnpackBlocks&, const LaunchCfg&, void*) { return 1; }
 int launch_checksum(const SrcUnit*, const SlotTable&, uint32_t, uint64_t, const void*,
                     fr_chunk_sum*, const Scratch&, const LaunchCfg&, void*) { return 1; }
 int launch_unpack(const UnpackArgs&, const LaunchCfg&, void*) { return 1; }

@@ -49,7 +49,7 @@ def test_library_is_gfx950_only():
 
 
 def test_version_and_strerror():
-    assert F.fr_abi_version() == 4
+    assert F.fr_abi_version() == 5
     msgs = {c: F.fr_strerror(c) for c in range(-7, 1)}
     assert msgs[0] == "ok" and len(set(msgs.values())) == 8
     assert F.fr_strerror(-99) == "unknown status"

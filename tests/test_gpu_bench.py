@@ -44,6 +44,11 @@ def test_bench_json_line(config, extra):
         assert abs(o["frac_of_ceiling"] - o["hbm_gbs"] / ce[o["ceiling"] + "_gbs"]) < 1e-3
     r = d["roofline"]
     assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    # the stress table's chunks start inside lines on both sides written: tile walks
+    walks = d["config"]["walks"]
+    if config == 2:
+        assert walks == {"pack": "tiles of the side written", "unpack": "tiles of the side written"}
+        assert r["kernel"] in ("k_pack_blocks", "k_unpack_blocks", "k_verify", "k_pack")
     assert abs(r["frac"] - r["achieved"] / r["peak"]) < 1e-3
     assert d["parity_ok"] is True
     assert d["delta_repair"]["ok"] is True and d["control_plane"]["ok"] is True

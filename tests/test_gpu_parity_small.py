@@ -388,6 +388,93 @@ def test_line_aligned_walks_match_oracle(tile, line, absorb):
                 os.environ[k] = v
 
 
+@pytest.mark.parametrize("tile", [0, 3, 4, 5, 7, 10])
+def test_payload_block_walks_match_oracle(tile):
+    """Pack and unpack walked by blocks of the payload (each workgroup moves
+    one whole tile of the payload, across chunk and entry boundaries), forced
+    whatever the table's alignment, give the oracle's payload, sums, receiver
+    arena and bad sets: random tables at random 16-byte offsets with derived
+    entries (pack sums them, and unpack restores them with their masters, in
+    slice walks of their own), chunks from 16 B (many chunks per block) to
+    1 MiB, segment alignments 16, 64 and 4096 (zero gaps inside blocks),
+    capped grids, short chunks of every slice count, corrupted wires, and
+    tables with nothing to send."""
+    names = ("FLASHRESTORE_TILE", "FLASHRESTORE_LINE_PACK", "FLASHRESTORE_LINE_UNPACK",
+             "FLASHRESTORE_MAX_GRID")
+    old = {k: os.environ.get(k) for k in names}
+    os.environ["FLASHRESTORE_TILE"] = str(tile)
+    os.environ["FLASHRESTORE_LINE_PACK"] = os.environ["FLASHRESTORE_LINE_UNPACK"] = "4"
+    rng = np.random.default_rng(900 + tile)
+    try:
+        for it in range(40):
+            os.environ["FLASHRESTORE_MAX_GRID"] = str(int(rng.choice([0, 1, 7, 300])))
+            t, sb, db = W.random_tiny_table(rng)
+            C = int(rng.choice([16, 32, 64, 256, 1024]))
+            seg = int(rng.choice([16, 16, 64, 4096]))
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, seg=seg,
+                                  tag=f"blocks tile {tile} table {it} C={C} seg={seg}")
+        for it in range(6):
+            os.environ["FLASHRESTORE_MAX_GRID"] = str(int(rng.choice([0, 7, 300])))
+            t, sb, db = W.random_tiny_table(rng, max_entries=8, max_numel=200_000)
+            C = int(rng.choice([4096, 16384, 65536, 1 << 20]))
+            seg = int(rng.choice([16, 4096]))
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, seg=seg,
+                                  tag=f"blocks tile {tile} multi {it} C={C} seg={seg}")
+        if tile in SLICE_BYTES:
+            os.environ["FLASHRESTORE_MAX_GRID"] = "0"
+            t, src, so, do = _slice_count_table(rng, 1 << 16, SLICE_BYTES[tile])
+            _check_against_oracle(t, 1 << 16, src, so, do, corrupt_rng=rng, tag=f"blocks tile {tile} slice counts")
+        # no derived entries (no slice walk in the launch), and only empty entries
+        for max_numel in (300, 0):
+            t, sb, db = W.random_tiny_table(rng, max_numel=max_numel, allow_derive=False)
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, 64, src, sb, db, corrupt_rng=rng, tag=f"blocks tile {tile} plain {max_numel}")
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+def test_walks_follow_the_alignment_of_the_side_written():
+    """By default pack walks tiles of the payload where payload chunks start
+    inside cache lines and unpack tiles of the receiver where receiver chunks
+    do; otherwise both walk slices (plan info reports the walk taken), and
+    either way the restore equals the oracle's."""
+    from paper_2509_03047_amd import flashrestore as F
+
+    names = ("FLASHRESTORE_LINE", "FLASHRESTORE_LINE_PACK", "FLASHRESTORE_LINE_UNPACK")
+    old = {k: os.environ.pop(k, None) for k in names}
+    rng = np.random.default_rng(77)
+    try:
+        table = np.zeros(3, dtype=W.TABLE_DTYPE)
+        table["numel"] = [1000, 4096, 333]  # 4000, 16384, 1332 bytes
+        table["dtype"] = [F.FR_F32, F.FR_F32, F.FR_F32]
+        table["derive_from"] = -1
+        cases = [  # src offsets, dst offsets, segment alignment, expected (pack walk, unpack walk)
+            ([0, 4096, 24576], [0, 8192, 32768], 16, (4, 0)),     # payload segments inside lines
+            ([0, 4096, 24576], [0, 8192, 32784], 4096, (0, 4)),   # the receiver's last entry inside a line
+            ([0, 4096, 24576], [0, 8192, 32768], 4096, (0, 0)),   # every side on lines
+            ([16, 4112, 24592], [16, 8208, 32784], 16, (4, 4)),
+        ]
+        for so, do, seg, want in cases:
+            t = table.copy()
+            t["src_offset"], t["dst_offset"] = so, do
+            sb, db = so[-1] + 1344, do[-1] + 1344
+            plan = F.Plan(t, 1024, sb, db, segment_align=seg)
+            assert (plan.info["pack_walk"], plan.info["unpack_walk"]) == want, (so, do, seg)
+            del plan
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, 1024, src, sb, db, corrupt_rng=rng, seg=seg, tag=f"walks {want}")
+    finally:
+        for k, v in old.items():
+            if v is not None:
+                os.environ[k] = v
+
+
 def test_mixed_tiles_per_operation():
     """Each operation with its own tile (so one plan holds several walks of
     different slice sizes) still gives the oracle's bytes."""
