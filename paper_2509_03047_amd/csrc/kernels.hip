@@ -26,12 +26,14 @@
 //     scratch, cleared by a fill kernel launched first;
 //   * replica compare marks a differing chunk with a plain store of 1 to a
 //     per-chunk flag (idempotent, so no atomics on shared bitmap words);
-//   * for tensors that start inside a cache line, walks cut slices at lines
-//     of one side so that no line is touched by two workgroups: pack at
-//     lines of the payload it writes, unpack at lines of the receiver, the
-//     compare at lines of the arenas (the checksum measured slower that
-//     way); pack and unpack let a chunk's last slice take the leftover lead
-//     instead of adding a nearly empty slice (the plan's launch
+//   * for tensors that start inside a cache line, pack and unpack walk
+//     tiles of the side they write instead of slices of chunks: workgroup g
+//     writes one aligned tile of the payload (pack) or of the receiver arena
+//     (unpack), across chunk and entry boundaries, summing each chunk's part
+//     with the chunk's own word indices (k_pack_blocks, k_unpack_blocks);
+//     the compare cuts its slices at lines of the arenas so that no line is
+//     read by two workgroups (the checksum measured slower that way); other
+//     line-aligned slice walks remain options (the plan's launch
 //     configuration sets all of it per operation, see LaunchCfg);
 //   * a finalize kernel, one lane per chunk, folds the G accumulators into
 //     the chunk's sums (pack, checksum, compare) or compares them with the
