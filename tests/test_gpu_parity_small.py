@@ -439,6 +439,42 @@ def test_payload_block_walks_match_oracle(tile):
                 os.environ[k] = v
 
 
+@pytest.mark.parametrize("tile", [3, 4, 5, 7])
+@pytest.mark.parametrize("line", ["0", "1", "2"])
+def test_buffer_load_slices_match_oracle(tile, line):
+    """The slice kernels loading through buffer resources (the option that
+    keeps every load of a thread in flight: lanes outside a chunk's data load
+    zeros) give the oracle's bytes for all four operations and the delta
+    calls, on slice walks plain and cut at lines (tile walks off)."""
+    ops = ("PACK", "UNPACK", "VERIFY", "CHECKSUM")
+    names = ("FLASHRESTORE_TILE", "FLASHRESTORE_LINE", "FLASHRESTORE_ABSORB_PACK",
+             "FLASHRESTORE_ABSORB_UNPACK") + tuple(f"FLASHRESTORE_BUF_{op}" for op in ops)
+    old = {k: os.environ.get(k) for k in names}
+    os.environ["FLASHRESTORE_TILE"], os.environ["FLASHRESTORE_LINE"] = str(tile), line
+    for op in ops:
+        os.environ[f"FLASHRESTORE_BUF_{op}"] = "1"
+    rng = np.random.default_rng(1300 + tile + 10 * int(line))
+    try:
+        for it in range(16):
+            os.environ["FLASHRESTORE_ABSORB_PACK"] = os.environ["FLASHRESTORE_ABSORB_UNPACK"] = str(it % 2)
+            t, sb, db = W.random_tiny_table(rng)
+            C = int(rng.choice([16, 64, 256, 1024]))
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"buf tile {tile} line {line} {it}")
+        for it in range(3):
+            t, sb, db = W.random_tiny_table(rng, max_entries=8, max_numel=200_000)
+            C = int(rng.choice([4096, 65536, 1 << 20]))
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"buf tile {tile} multi {it}")
+            _delta_against_oracle(t, C, src, sb, db, rng, f"buf tile {tile} multi {it}")
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
 def test_walks_follow_the_alignment_of_the_side_written():
     """By default pack walks tiles of the payload where payload chunks start
     inside cache lines and unpack tiles of the receiver where receiver chunks
