@@ -180,12 +180,22 @@ typedef struct fr_plan_info {
  * 0-10 (threads x 16-byte vectors per workgroup: 256x1, 512x1, 256x2,
  * 256x4, 64x4, 128x2, 64x2, 64x1, 128x1, 128x4, 64x8; defaults pack 64x4,
  * unpack and compare 128x2, checksum 256x4), FLASHRESTORE_LINE (every
- * operation) or FLASHRESTORE_LINE_PACK / _VERIFY / _CHECKSUM choose
- * line-aligned slices (each workgroup's share of a chunk cut at 128-byte
- * lines, for data placed inside lines): 0 off, 1 at lines of the arena
- * read, 2 (pack only; 1 elsewhere) at lines of the payload written;
- * defaults pack 2, compare 1, checksum 0.  FLASHRESTORE_MAX_GRID caps the
- * workgroups per launch (0 or unset: one per slice). */
+ * operation) or FLASHRESTORE_LINE_PACK / _UNPACK / _VERIFY / _CHECKSUM
+ * choose how work is divided for data placed inside 128-byte lines: 0
+ * plain slices of chunks, 1 slices cut at lines of the arena read (unpack:
+ * of the receiver written), 2 (pack, unpack) at lines of the payload, 3
+ * (pack, unpack) at slice boundaries of the payload, 4 (pack, unpack) one
+ * aligned tile of the side written per workgroup (the payload for pack,
+ * the receiver arena for unpack); unset, pack and unpack take 4 where the
+ * side they write has chunks starting inside lines and 2 (pack) or 1
+ * (unpack) otherwise, the compare 1 and the checksum 0 (fr_plan_info
+ * reports what pack and unpack take).  FLASHRESTORE_ABSORB_PACK / _UNPACK
+ * / _VERIFY / _CHECKSUM (defaults 1, 1, 0, 0): a cut slice walk gives a
+ * chunk's last slice its leftover lead instead of one more slice.
+ * FLASHRESTORE_BUF_PACK / _UNPACK / _VERIFY / _CHECKSUM (default 0): slice
+ * walks load through buffer resources, all of a thread's loads in flight
+ * at once.  FLASHRESTORE_MAX_GRID caps the workgroups per launch (0 or
+ * unset: one per slice or tile). */
 int fr_plan_create(const fr_tensor_desc* table, uint32_t n_entries, uint64_t chunk_bytes,
                    uint64_t src_arena_bytes, uint64_t dst_arena_bytes, fr_plan** out);
 
