@@ -194,7 +194,10 @@ typedef struct fr_plan_info {
  * chunk's last slice its leftover lead instead of one more slice.
  * FLASHRESTORE_BUF_PACK / _UNPACK / _VERIFY / _CHECKSUM (default 0): slice
  * walks load through buffer resources, all of a thread's loads in flight
- * at once.  FLASHRESTORE_MAX_GRID caps the workgroups per launch (0 or
+ * at once.  FLASHRESTORE_ORDER_VERIFY / _CHECKSUM (defaults 1, 0): the
+ * compare's or the checksum's slices in arena address order rather than
+ * chunk order (they differ for tables that list tensors out of arena
+ * order).  FLASHRESTORE_MAX_GRID caps the workgroups per launch (0 or
  * unset: one per slice or tile). */
 int fr_plan_create(const fr_tensor_desc* table, uint32_t n_entries, uint64_t chunk_bytes,
                    uint64_t src_arena_bytes, uint64_t dst_arena_bytes, fr_plan** out);

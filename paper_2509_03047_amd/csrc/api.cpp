@@ -96,14 +96,16 @@ int launch_result(int hip_rc) {
 }
 
 // The plan's pack / checksum / compare walk at the slice size of `tile`,
-// line-aligned or not (the plan builds one for each configuration its
-// operations use, so this finds one for the plan's own).
-const SlotTable* src_walk(const fr_plan* plan, int tile, int line, int absorb = 0) {
+// line-aligned or not, in chunk order or (arena) in arena address order
+// (the plan builds one for each configuration its operations use, so this
+// finds one for the plan's own).
+const SlotTable* src_walk(const fr_plan* plan, int tile, int line, int absorb, bool arena) {
   const uint32_t sl = slice_bytes(plan->layout.C, tile);
   const uint32_t shift = line_walk(plan, tile, line);
   const uint32_t ab = shift && absorb ? 1u : 0u;
+  const bool order = arena && !plan->chunks_in_arena_order;
   for (const auto& w : plan->src_walks)
-    if (w.sl == sl && w.t.shift == shift && w.t.absorb == ab) return &w.t;
+    if (w.sl == sl && w.t.shift == shift && w.t.absorb == ab && w.arena_order == order) return &w.t;
   return nullptr;
 }
 
@@ -131,7 +133,8 @@ extern "C" int fr_pack_state(const fr_plan* plan, const void* src_base, void* pa
     return launch_result(launch_pack_blocks(plan->d_units, plan->pack_blocks, uint32_t(L.n_chunks),
                                             L.C, src_base, payload, sums, plan->scratch, plan->cfg,
                                             stream));
-  const SlotTable* walk = src_walk(plan, plan->cfg.tile_pack, plan->cfg.line_pack, plan->cfg.absorb_pack);
+  const SlotTable* walk =
+      src_walk(plan, plan->cfg.tile_pack, plan->cfg.line_pack, plan->cfg.absorb_pack, false);
   if (!walk) return FR_E_INVAL;
   return launch_result(launch_pack(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, src_base,
                                    payload, sums, plan->scratch, plan->cfg, stream));
@@ -195,7 +198,8 @@ int verify_checks(const fr_plan* plan, const void* base_a, const void* base_b,
   const Region outs[] = {{diff_bitmap, words * 4}, {n_diff, 8}, {sums_a, sb}, {sums_b, sb}};
   const Region ins[] = {{base_a, plan->src_arena_bytes}, {base_b, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 4, ins, 2));
-  *walk = src_walk(plan, plan->cfg.tile_verify, plan->cfg.line_verify, plan->cfg.absorb_verify);
+  *walk = src_walk(plan, plan->cfg.tile_verify, plan->cfg.line_verify, plan->cfg.absorb_verify,
+                   plan->cfg.order_verify != 0);
   return *walk ? FR_OK : FR_E_INVAL;
 }
 
@@ -250,7 +254,8 @@ extern "C" int fr_checksum_state(const fr_plan* plan, const void* base, fr_chunk
   const Region ins[] = {{base, plan->src_arena_bytes}};
   FR_TRY(check_disjoint(outs, 1, ins, 1));
   const SlotTable* walk =
-      src_walk(plan, plan->cfg.tile_checksum, plan->cfg.line_checksum, plan->cfg.absorb_checksum);
+      src_walk(plan, plan->cfg.tile_checksum, plan->cfg.line_checksum, plan->cfg.absorb_checksum,
+               plan->cfg.order_checksum != 0);
   if (!walk) return FR_E_INVAL;
   return launch_result(launch_checksum(plan->d_units, *walk, uint32_t(L.n_chunks), L.C, base,
                                        sums, plan->scratch, plan->cfg, stream));

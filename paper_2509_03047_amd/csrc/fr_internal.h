@@ -167,6 +167,9 @@ struct LaunchCfg {
   // slices loaded through buffer resources (every load of a thread in
   // flight at once) rather than predicated global loads
   int buf_pack = 0, buf_unpack = 0, buf_verify = 0, buf_checksum = 0;
+  // the compare's and the checksum's walks in arena address order rather
+  // than chunk order (they differ when a table lists tensors out of arena order)
+  int order_verify = 0, order_checksum = 0;
 };
 
 // Device scratch owned by a plan: per-chunk accumulators (G per chunk, see
@@ -366,7 +369,9 @@ struct fr_plan {
     uint32_t sl = 0;
     fr::SlotTable t{};  // t.shift: the line-aligned mode (0 off, 1 arena lines, 2 payload lines)
     uint64_t* mem = nullptr;
+    bool arena_order = false;  // units in arena address order rather than chunk (payload) order
   };
+  bool chunks_in_arena_order = true;  // chunk order is already arena address order
   uint32_t dst_align = fr::kLeadMod;     // the same for every plain unpack chunk's receiver offset
   uint32_t src_align = fr::kLeadMod;   // largest power of two (<= kLeadMod) dividing every chunk's src_off
   uint32_t pay_align = fr::kLeadMod;   // the same for every sent chunk's payload offset

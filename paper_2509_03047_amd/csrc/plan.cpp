@@ -40,6 +40,11 @@ constexpr int kAlignedLinePack = 2, kAlignedLineUnpack = 1;
 // 1.3 % faster from one box to the next.
 constexpr uint32_t kDefaultBufPack = 0, kDefaultBufUnpack = 0, kDefaultBufVerify = 0,
                    kDefaultBufChecksum = 0;
+// The compare's and the checksum's walks in arena address order instead of
+// chunk order, for tables that list tensors out of arena order: on the
+// descriptor stress table the compare gains 2.8 % (7.19 against 6.99 TB/s)
+// and the checksum loses 1.1 % (6.50 against 6.57).
+constexpr uint32_t kDefaultOrderVerify = 1, kDefaultOrderChecksum = 0;
 // Whether a line-aligned pack / unpack walk lets a unit's last slice absorb
 // the lead instead of adding a slice.
 constexpr uint32_t kDefaultAbsorbPack = 1, kDefaultAbsorbUnpack = 1, kDefaultAbsorbVerify = 0,
@@ -328,6 +333,8 @@ LaunchCfg launch_config() {
   cfg.buf_unpack = int(env_u32("FLASHRESTORE_BUF_UNPACK", kDefaultBufUnpack) != 0);
   cfg.buf_verify = int(env_u32("FLASHRESTORE_BUF_VERIFY", kDefaultBufVerify) != 0);
   cfg.buf_checksum = int(env_u32("FLASHRESTORE_BUF_CHECKSUM", kDefaultBufChecksum) != 0);
+  cfg.order_verify = int(env_u32("FLASHRESTORE_ORDER_VERIFY", kDefaultOrderVerify) != 0);
+  cfg.order_checksum = int(env_u32("FLASHRESTORE_ORDER_CHECKSUM", kDefaultOrderChecksum) != 0);
   cfg.line_checksum = lpick("FLASHRESTORE_LINE_CHECKSUM", kDefaultLineChecksum, 0x2);
   return cfg;
 }
@@ -425,36 +432,55 @@ void unpack_units(const fr_tensor_desc* table, uint32_t n, const Layout& L,
   }
 }
 
-// Walks of pack / checksum / compare: every chunk in order, one table per
-// slice size, alignment and lead handling their configurations use (a
+// Walks of pack / checksum / compare: every chunk once, one table per slice
+// size, alignment, lead handling and order their configurations use (a
 // line-aligned walk is the plain one when every chunk starts on a line).
+// Pack walks in chunk order, which is payload order; the compare, which
+// only reads the arenas, walks them in address order by default (the same
+// unless the table lists its tensors out of arena order; the checksum
+// measured slower that way, see kDefaultOrderVerify).
 int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units, const Staging& st) {
   const Layout& L = p->layout;
   struct Want {
     int tile, line, absorb;
+    bool arena;
   };
-  const Want walks[] = {{p->cfg.tile_pack, p->cfg.line_pack, p->cfg.absorb_pack},
-                        {p->cfg.tile_checksum, p->cfg.line_checksum, p->cfg.absorb_checksum},
-                        {p->cfg.tile_verify, p->cfg.line_verify, p->cfg.absorb_verify}};
+  for (uint64_t c = 1; c < units.size(); c++)
+    p->chunks_in_arena_order = p->chunks_in_arena_order && units[c - 1].src_off <= units[c].src_off;
+  const Want walks[] = {
+      {p->cfg.tile_pack, p->cfg.line_pack, p->cfg.absorb_pack, false},
+      {p->cfg.tile_checksum, p->cfg.line_checksum, p->cfg.absorb_checksum, p->cfg.order_checksum != 0},
+      {p->cfg.tile_verify, p->cfg.line_verify, p->cfg.absorb_verify, p->cfg.order_verify != 0}};
+  std::vector<uint32_t> by_addr;
   for (const Want& tw : walks) {
     if (&tw == &walks[0] && p->cfg.line_pack == kLineBlocks) continue;  // build_pack_blocks
     const uint32_t sl = slice_bytes(L.C, tw.tile);
     const uint32_t shift = line_walk(p, tw.tile, tw.line);
     const uint32_t absorb = shift && tw.absorb ? 1u : 0u;
+    const bool arena = tw.arena && !p->chunks_in_arena_order;
     bool have = false;
     for (const auto& w : p->src_walks)
-      have = have || (w.sl == sl && w.t.shift == shift && w.t.absorb == absorb);
+      have = have || (w.sl == sl && w.t.shift == shift && w.t.absorb == absorb && w.arena_order == arena);
     if (have) continue;
+    if (arena && by_addr.empty()) {
+      by_addr.resize(units.size());
+      for (uint32_t c = 0; c < by_addr.size(); c++) by_addr[c] = c;
+      std::stable_sort(by_addr.begin(), by_addr.end(),
+                       [&](uint32_t x, uint32_t y) { return units[x].src_off < units[y].src_off; });
+    }
     SlotRuns b;
     b.sl = sl;
     b.first.reserve(units.size() + 1);
     b.base.reserve(units.size());
-    for (uint64_t c = 0; c < units.size(); c++)
-      b.add(uint32_t(c), units[c].len + (absorb ? 0 : lead_bytes(units[c].lead, units[c].plead, shift, sl)), 0);
+    for (uint64_t i = 0; i < units.size(); i++) {
+      const uint32_t c = arena ? by_addr[i] : uint32_t(i);
+      b.add(c, units[c].len + (absorb ? 0 : lead_bytes(units[c].lead, units[c].plead, shift, sl)), 0);
+    }
     p->src_walks.emplace_back();
     const int rc = upload_walk(b, p->src_walks.back(), st);
     p->src_walks.back().t.shift = shift;
     p->src_walks.back().t.absorb = absorb;
+    p->src_walks.back().arena_order = arena;
     if (rc != FR_OK) return rc;
   }
   return FR_OK;

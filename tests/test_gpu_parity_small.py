@@ -475,6 +475,30 @@ def test_buffer_load_slices_match_oracle(tile, line):
                 os.environ[k] = v
 
 
+@pytest.mark.parametrize("order", ["0", "1"])
+def test_walk_orders_match_oracle(order):
+    """The compare and the checksum walking the arena in chunk order or in
+    arena address order (tables list their tensors in shuffled arena order)
+    give the oracle's sets and sums, also under capped grids."""
+    names = ("FLASHRESTORE_ORDER_VERIFY", "FLASHRESTORE_ORDER_CHECKSUM", "FLASHRESTORE_MAX_GRID")
+    old = {k: os.environ.get(k) for k in names}
+    os.environ["FLASHRESTORE_ORDER_VERIFY"] = os.environ["FLASHRESTORE_ORDER_CHECKSUM"] = order
+    rng = np.random.default_rng(1400 + int(order))
+    try:
+        for it in range(20):
+            os.environ["FLASHRESTORE_MAX_GRID"] = str(int(rng.choice([0, 0, 7, 300])))
+            t, sb, db = W.random_tiny_table(rng, max_entries=10, max_numel=3000)
+            C = int(rng.choice([16, 256, 4096]))
+            src = W.random_tiny_state(t, sb, rng)
+            _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng, tag=f"order {order} {it}")
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
 def test_walks_follow_the_alignment_of_the_side_written():
     """By default pack walks tiles of the payload where payload chunks start
     inside cache lines and unpack tiles of the receiver where receiver chunks
