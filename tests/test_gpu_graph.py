@@ -14,15 +14,42 @@ from paper_2509_03047_amd import flashrestore as F  # noqa: E402
 from paper_2509_03047_amd import workloads as W  # noqa: E402
 
 
-def test_captured_restore_step_replays_correctly():
+def _scattered_case():
+    """40 tensors at shuffled 16-byte offsets (the same layout on both
+    sides, so the receiver equals the sender): pack and unpack walk tiles."""
+    rng = np.random.default_rng(8)
+    t, sb, _ = W.random_tiny_table(rng, max_entries=40, max_numel=60_000)
+    t["dst_offset"] = t["src_offset"]
+    return t, 4096, sb, sb, W.random_tiny_state(t, sb, rng)
+
+
+@pytest.mark.parametrize("case", ["toy", "scattered"])
+def test_captured_restore_step_replays_correctly(case):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
-    w = W.make_workload(0)
-    src_np = W.fill_state(w)
-    plan = F.Plan(w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes)
+    if case == "toy":
+        w = W.make_workload(0)
+        table, C, sb, db, src_np = w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes, W.fill_state(w)
+    else:
+        table, C, sb, db, src_np = _scattered_case()
+    plan = F.Plan(table, C, sb, db)
+    if case == "scattered":
+        assert plan.info["pack_walk"] == 4 and plan.info["unpack_walk"] == 4
     src = torch.from_numpy(src_np).to("cuda")
     payload, sums = plan.empty_payload(), plan.empty_sums()
-    dst = torch.zeros(w.dst_arena_bytes, dtype=torch.uint8, device="cuda")
+    dst = torch.zeros(db, dtype=torch.uint8, device="cuda")
+    covered = torch.zeros(sb, dtype=torch.bool)  # the entries' bytes (the rest are gaps)
+    plain = torch.zeros(sb, dtype=torch.bool)    # those of entries neither derived nor masters
+    masters = {int(e["derive_from"]) for e in table if int(e["derive_from"]) >= 0}
+    for k, e in enumerate(table):
+        n = int(e["numel"]) * (4 if int(e["dtype"]) == F.FR_F32 else 2)
+        covered[int(e["src_offset"]):int(e["src_offset"]) + n] = True
+        if int(e["derive_from"]) < 0 and k not in masters:
+            plain[int(e["src_offset"]):int(e["src_offset"]) + n] = True
+    covered = covered.to("cuda")
+    # flips go to plain entries: the receiver re-derives a derived entry from
+    # its master, so a flip in either would (rightly) be flagged
+    entries = torch.nonzero(plain).flatten().numpy()
     bad, nbad = plan.empty_bitmap(), plan.empty_counter()
     diff, ndiff = plan.empty_bitmap(), plan.empty_counter()
     csum = plan.empty_sums()
@@ -36,6 +63,7 @@ def test_captured_restore_step_replays_correctly():
     # eager reference of the unmodified state
     step()
     torch.cuda.synchronize()
+    assert torch.equal(dst[covered], src[covered]) and int(nbad.item()) == 0 and int(ndiff.item()) == 0
     ref = (payload.clone(), sums.clone(), dst.clone(), csum.clone())
 
     s = torch.cuda.Stream()
@@ -52,7 +80,7 @@ def test_captured_restore_step_replays_correctly():
     rng = np.random.default_rng(3)
     for rep in range(4):
         # eager work between replays: perturb the donor, then restore it later
-        flip = int(rng.integers(0, src.numel()))
+        flip = int(entries[int(rng.integers(0, entries.size))])
         src[flip] ^= 0x10
         dst.fill_(0x77)
         nbad.fill_(99)
@@ -64,14 +92,14 @@ def test_captured_restore_step_replays_correctly():
         plan.pack(src, exp_payload, exp_sums)
         torch.cuda.synchronize()
         assert torch.equal(payload, exp_payload) and torch.equal(sums, exp_sums), rep
-        assert torch.equal(dst, src) and int(nbad.item()) == 0 and int(ndiff.item()) == 0
+        assert torch.equal(dst[covered], src[covered]) and int(nbad.item()) == 0 and int(ndiff.item()) == 0
         assert torch.equal(csum, sums)
         src[flip] ^= 0x10  # undo
     torch.cuda.synchronize()
     g.replay()
     torch.cuda.synchronize()
     assert torch.equal(payload, ref[0]) and torch.equal(sums, ref[1])
-    assert torch.equal(dst, ref[2]) and torch.equal(csum, ref[3])
+    assert torch.equal(dst[covered], ref[2][covered]) and torch.equal(csum, ref[3])
 
 
 def test_captured_compare_and_repair_replays_correctly():
