@@ -462,11 +462,15 @@ int build_src_walks(fr_plan* p, const std::vector<SrcUnit>& units, const Staging
     for (const auto& w : p->src_walks)
       have = have || (w.sl == sl && w.t.shift == shift && w.t.absorb == absorb && w.arena_order == arena);
     if (have) continue;
-    if (arena && by_addr.empty()) {
-      by_addr.resize(units.size());
-      for (uint32_t c = 0; c < by_addr.size(); c++) by_addr[c] = c;
-      std::stable_sort(by_addr.begin(), by_addr.end(),
-                       [&](uint32_t x, uint32_t y) { return units[x].src_off < units[y].src_off; });
+    if (arena && by_addr.empty()) {  // entries by sender offset, each entry's chunks in order
+      std::vector<uint32_t> ent(p->table.size());
+      for (uint32_t k = 0; k < ent.size(); k++) ent[k] = k;
+      std::stable_sort(ent.begin(), ent.end(), [&](uint32_t x, uint32_t y) {
+        return p->table[x].src_offset < p->table[y].src_offset;
+      });
+      by_addr.reserve(units.size());
+      for (uint32_t k : ent)
+        for (uint64_t c = L.chunk_base[k]; c < L.chunk_base[k + 1]; c++) by_addr.push_back(uint32_t(c));
     }
     SlotRuns b;
     b.sl = sl;
@@ -533,40 +537,58 @@ int build_unpack_blocks(fr_plan* p, const std::vector<ChunkRec>& recs,
                         const std::vector<uint8_t>& is_master, const Staging& st) {
   const Layout& L = p->layout;
   const uint64_t tile_vecs = tile_bytes(p->cfg.tile_unpack) / 16;
-  std::vector<PlainUnit> units;
-  units.reserve(L.n_sent_chunks);
   SlotRuns b;
   b.sl = slice_bytes(L.C, p->cfg.tile_unpack);
   uint32_t id = 0;
+  std::vector<uint32_t> ent;  // plain entries, by receiver offset (ranges never overlap)
   for (uint32_t k = 0; k < p->table.size(); k++) {
-    const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];
-    for (uint64_t c = c0; c < c1; c++) {
-      if (p->table[k].derive_from >= 0) {
+    if (p->table[k].derive_from >= 0) {
+      for (uint64_t c = L.chunk_base[k]; c < L.chunk_base[k + 1]; c++)
         b.add(id++, 2 * uint64_t(recs[c].len), kSlotDerived);
-      } else if (!is_master[k]) {
-        PlainUnit u{};
-        u.pay_off = recs[c].pay_off;
-        u.dst_off = recs[c].dst_off;
-        u.len = recs[c].len;
-        u.c = uint32_t(c);
-        units.push_back(u);
-      }
+    } else if (!is_master[k]) {
+      ent.push_back(k);
     }
   }
-  std::sort(units.begin(), units.end(),
-            [](const PlainUnit& x, const PlainUnit& y) { return x.dst_off < y.dst_off; });
-  std::vector<uint64_t> tiles;  // (tile << 32) | first unit, in receiver order
-  for (uint64_t u = 0; u < units.size(); u++) {
-    const uint64_t v0 = units[u].dst_off / 16, v1 = v0 + (units[u].len + 15) / 16;
-    for (uint64_t t = v0 / tile_vecs; t * tile_vecs < v1; t++)
-      if (tiles.empty() || (tiles.back() >> 32) < t) tiles.push_back((t << 32) | u);
+  std::sort(ent.begin(), ent.end(), [&](uint32_t x, uint32_t y) {
+    return p->table[x].dst_offset < p->table[y].dst_offset;
+  });
+  std::vector<PlainUnit> units;
+  units.reserve(L.n_sent_chunks);
+  for (uint32_t k : ent) {
+    for (uint64_t c = L.chunk_base[k]; c < L.chunk_base[k + 1]; c++) {
+      PlainUnit u{};
+      u.pay_off = recs[c].pay_off;
+      u.dst_off = recs[c].dst_off;
+      u.len = recs[c].len;
+      u.c = uint32_t(c);
+      units.push_back(u);
+    }
   }
+  // (tile << 32) | first unit touching it, for every tile some unit touches,
+  // in receiver order, stored XCD-major: counted, then written
+  auto each_tile = [&](auto&& emit) {
+    uint64_t last = ~uint64_t(0);
+    for (uint64_t u = 0; u < units.size(); u++) {
+      const uint64_t v0 = units[u].dst_off / 16, v1 = v0 + (units[u].len + 15) / 16;
+      for (uint64_t t = v0 / tile_vecs; t * tile_vecs < v1; t++)
+        if (last == ~uint64_t(0) || last < t) {
+          emit((t << 32) | u);
+          last = t;
+        }
+    }
+  };
+  uint64_t n_tiles = 0;
+  each_tile([&](uint64_t) { n_tiles++; });
   UnpackBlocks& ub = p->unpack_blocks;
   ub.n_units = units.size();
-  ub.n_blocks = tiles.size();
+  ub.n_blocks = n_tiles;
   ub.stride = (ub.n_blocks + 7) / 8;
   std::vector<uint64_t> xcd(8 * ub.stride, 0);
-  for (uint64_t g = 0; g < tiles.size(); g++) xcd[(g & 7) * ub.stride + (g >> 3)] = tiles[g];
+  uint64_t g = 0;
+  each_tile([&](uint64_t e) {
+    xcd[(g & 7) * ub.stride + (g >> 3)] = e;
+    g++;
+  });
   const uint64_t b_units = (units.size() * sizeof(PlainUnit) + 255) & ~uint64_t(255);
   int rc = upload(nullptr, b_units + xcd.size() * sizeof(uint64_t), &p->d_ublocks, st.s);
   if (rc == FR_OK && p->d_ublocks) {
