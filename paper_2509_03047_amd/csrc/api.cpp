@@ -346,6 +346,8 @@ DeltaBuild delta_build(const fr_plan* plan, const uint32_t* bits, uint64_t* user
   b.plain = plan->d_delta_plain;
   b.derived = plan->d_delta_derived;
   b.bad = plan->scratch.flags;
+  b.pay_of = plan->d_delta_payof;
+  b.m0 = plan->d_delta_m0;
   b.payload_limit = payload_limit;
   b.acc = plan->scratch.acc;
   uint32_t g = 0;
@@ -371,8 +373,9 @@ int pack_list(const fr_plan* plan, const void* src_base, const uint32_t* bits, u
 }
 
 // The device half of a delta unpack: build the list's records from `bits`,
-// write the sent chunks, re-derive the listed parameters from the
-// receiver's masters, check every listed chunk (at most `bound`).
+// write the sent chunks and re-derive the listed parameters (from re-sent
+// masters in the payload, else from the receiver's own) in one launch,
+// check every listed chunk (at most `bound`).
 int unpack_list(const fr_plan* plan, const void* payload, uint64_t payload_bytes,
                 const fr_chunk_sum* sums, const uint32_t* bits, uint64_t bound, void* dst_base,
                 uint32_t* bad_bitmap, uint64_t* n_bad, hipStream_t stream) {
@@ -400,6 +403,8 @@ int unpack_list(const fr_plan* plan, const void* payload, uint64_t payload_bytes
     a.live = plan->d_delta_counts + kDeltaIds;
     a.bad = plan->scratch.flags;
   }
+  a.bits = bits;
+  a.pay_of = plan->d_delta_payof;
   return launch_result(launch_unpack_delta(a, plan->cfg, stream));
 }
 

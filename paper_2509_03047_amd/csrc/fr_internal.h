@@ -216,6 +216,11 @@ struct UnpackDeltaArgs {
   Scratch scratch;
   const uint64_t* live = nullptr;  // list built on the device: its length (n_ids is the bound)
   const uint32_t* bad = nullptr;   // per list position: 1 = flag it whatever its sums
+  // the list (bit c set = chunk c listed) and each listed sent chunk's
+  // payload offset (DeltaBuild::pay_of): a derived chunk reads a master
+  // chunk from the payload when it was re-sent, else from the receiver
+  const uint32_t* bits = nullptr;
+  const uint64_t* pay_of = nullptr;
 };
 
 // Where a chunk lives, for lists of chunks built on the device: one record
@@ -262,6 +267,9 @@ struct DeltaBuild {
   PlainUnit* plain;          // unpack: sent chunks
   DerivedUnit* derived;      // unpack: derived chunks (re-derived from the receiver's masters)
   uint32_t* bad;             // unpack: per list position, 1 = beyond the readable payload
+  uint64_t* pay_of;          // unpack: per chunk id, a listed sent chunk's payload offset
+                             //   (kNoPayload if beyond the readable payload)
+  const uint32_t* m0;        // per chunk id: a derived chunk's first master chunk
   uint64_t payload_limit;    // pack: payload capacity; unpack: readable payload bytes
   fr_chunk_sum* acc;         // accumulators of the operation, cleared per listed position
   uint32_t acc_shift;        // log2 of the accumulators per list position
@@ -403,6 +411,8 @@ struct fr_plan {
   uint64_t* d_delta_counts = nullptr;  // fr::DeltaCount
   uint32_t* d_delta_bits = nullptr;    // bitmap of a host list
   uint32_t* d_delta_ids = nullptr;     // a host list, uploaded
+  uint64_t* d_delta_payof = nullptr;   // per chunk: payload offset in the last delta unpack
+  uint32_t* d_delta_m0 = nullptr;      // per chunk: a derived chunk's first master chunk
   uint32_t* h_delta_ids = nullptr;     // pinned staging of a host list
   hipEvent_t delta_ids_copied = nullptr;  // the last upload from the staging has completed
   fr::Scratch scratch{};

@@ -738,27 +738,60 @@ __global__ __launch_bounds__(B) void k_unpack_blocks(UnpackBlocksArgs a, Walk wk
   }
 }
 
-// Delta restore, second phase: recompute listed bf16 parameter chunks from
-// the receiver's own master bytes (m_pay_off holds the master's receiver
-// offset); parameter sums go to the list position r.c.
+// Delta restore in one launch over a list built on the device: workgroup ids
+// first walk the listed sent chunks (wp), then the listed bf16 parameter
+// chunks (wd), which are re-derived from their master chunks: a master
+// chunk re-sent in this list is read from the payload (pay_of: its offset
+// there; kNoPayload if it lies past the readable payload), any other from
+// the receiver, which this launch does not write there.  So no slice reads
+// what another writes, and the whole delta runs as one kernel.  Parameter
+// sums go to list position r.c.
 template <int B, int U>
-__global__ __launch_bounds__(B) void k_rederive(const DerivedUnit* __restrict__ derived, Walk wk,
-                                                uint32_t cvec, uint8_t* dst,
-                                                fr_chunk_sum* __restrict__ acc_out) {
+__global__ __launch_bounds__(B) void k_unpack_list(const PlainUnit* __restrict__ plain, Walk wp,
+                                                   const DerivedUnit* __restrict__ derived, Walk wd,
+                                                   uint32_t cvec, const uint8_t* __restrict__ payload,
+                                                   uint8_t* __restrict__ dst,
+                                                   const uint32_t* __restrict__ bits,
+                                                   const u64* __restrict__ pay_of,
+                                                   fr_chunk_sum* __restrict__ acc_out) {
   __shared__ u64 lds[2][B / 64][4];
+  __shared__ u64 lds2[2][B / 64][2];
   int parity = 0;
-  const u64 n_slices = walk_slices(wk);
-  for (u64 g = blockIdx.x; g < n_slices; g += gridDim.x) {
-    const u64 e = slot_of(wk, g);
-    const DerivedUnit r = derived[e >> 32];
-    const uint32_t j = uint32_t(e) & ~kSlotDerived;
-    u64 acc[4] = {0, 0, 0, 0};
-    uint32_t part = 0;
-    if (!derived_slice<B, U, false, false>(r, j, wk, cvec, dst, dst, acc, part)) continue;
-    block_sum<B, 4>(acc, lds, parity);
-    parity ^= 1;
-    if (threadIdx.x == 0)
-      add_sum(acc_out + ((u64(r.c) << wk.g_shift) + (j >> (kAccSlicesShift + 1))), acc[2], acc[3]);
+  const u64 np = walk_slices(wp), n = np + walk_slices(wd);
+  for (u64 g = blockIdx.x; g < n; g += gridDim.x) {
+    if (g < np) {
+      const u64 e = slot_of(wp, g);
+      const PlainUnit r = plain[e >> 32];
+      const uint32_t j = uint32_t(e);
+      u64 acc[2] = {0, 0};
+      if (!plain_slice<B, U, false>(r, j, wp, payload, dst, acc)) continue;
+      block_sum<B, 2>(acc, lds2, parity);
+      parity ^= 1;
+      if (threadIdx.x == 0) add_sum(acc_out + acc_index(wp, r.c, j), acc[0], acc[1]);
+    } else {
+      const u64 e = slot_of(wd, g - np);
+      DerivedUnit r = derived[e >> 32];
+      const uint32_t j = uint32_t(e) & ~kSlotDerived;
+      // this slice's master chunk m0 + part, and where its bytes are: the
+      // slice indexes the group's master bytes from the group's start, so a
+      // part read from the payload is addressed from cvec * part vectors
+      // before its offset there
+      const uint32_t part = j >> wd.spc_shift;
+      const u64 m = u64(r.m0) + part;
+      const u64 po = ((bits[m >> 5] >> (m & 31)) & 1u) ? pay_of[m] : kNoPayload;
+      const uint8_t* msrc = dst;
+      if (po != kNoPayload) {
+        msrc = payload;
+        r.m_pay_off = po - u64(part) * cvec * 16;
+      }
+      u64 acc[4] = {0, 0, 0, 0};
+      uint32_t got = 0;
+      if (!derived_slice<B, U, false, false>(r, j, wd, cvec, msrc, dst, acc, got)) continue;
+      block_sum<B, 4>(acc, lds, parity);
+      parity ^= 1;
+      if (threadIdx.x == 0)
+        add_sum(acc_out + ((u64(r.c) << wd.g_shift) + (j >> (kAccSlicesShift + 1))), acc[2], acc[3]);
+    }
   }
 }
 
@@ -1112,8 +1145,11 @@ __global__ __launch_bounds__(kListBlock) void k_list_build(DeltaBuild b) {
     if (kForPack) {
       b.src_units[pos] = SrcUnit{r.src_off, kNoPayload, r.len, pos, 0, uint16_t(r.src_off % kLeadMod), 0};
     } else {
-      // re-derived from the receiver's own master bytes of this chunk
-      b.derived[pre.nd + excl.nd] = DerivedUnit{r.m_dst_off, r.m_dst_off, r.dst_off, r.len, 0, pos, 0};
+      // re-derived from its master chunks: m_pay_off is their receiver offset,
+      // and a master chunk re-sent in this list is read from the payload
+      // instead (the unpack finds its offset in pay_of)
+      b.derived[pre.nd + excl.nd] =
+          DerivedUnit{r.m_dst_off, r.m_dst_off, r.dst_off, r.len, b.m0[c], pos, 0};
       b.bad[pos] = 0;
     }
     return;
@@ -1137,6 +1173,7 @@ __global__ __launch_bounds__(kListBlock) void k_list_build(DeltaBuild b) {
         PlainUnit{readable ? pay : 0, r.dst_off, readable ? r.len : 0u, pos, uint32_t(pay % kLeadMod),
                   uint32_t(r.dst_off % kLeadMod)};
     b.bad[pos] = readable ? 0u : 1u;
+    b.pay_of[c] = readable ? pay : kNoPayload;
   }
 }
 
@@ -1424,17 +1461,13 @@ int unpack_delta_impl(const UnpackDeltaArgs& u, const LaunchCfg& cfg, hipStream_
   int e = z.launch(st);
   if (e || u.n_ids == 0) return e;
   const uint32_t cvec = uint32_t(u.C >> 4);
-  if (wp.n_slices) {  // sent chunks first: the masters the second phase reads
-    hipLaunchKernelGGL((k_unpack<B, U, false>), dim3(grid_of<B>(wp, cfg)), dim3(B), 0, st,
-                       static_cast<const DerivedUnit*>(nullptr), u.plain, wp, cvec,
-                       static_cast<const uint8_t*>(u.payload), static_cast<uint8_t*>(u.dst),
+  if (wp.n_slices + wd.n_slices) {  // sent and derived chunks in one launch
+    Walk both = wp;
+    both.n_slices = wp.n_slices + wd.n_slices;
+    hipLaunchKernelGGL((k_unpack_list<B, U>), dim3(grid_of<B>(both, cfg)), dim3(B), 0, st, u.plain,
+                       wp, u.derived, wd, cvec, static_cast<const uint8_t*>(u.payload),
+                       static_cast<uint8_t*>(u.dst), u.bits, reinterpret_cast<const u64*>(u.pay_of),
                        u.scratch.acc);
-    e = int(hipGetLastError());
-    if (e) return e;
-  }
-  if (wd.n_slices) {
-    hipLaunchKernelGGL((k_rederive<B, U>), dim3(grid_of<B>(wd, cfg)), dim3(B), 0, st,
-                       u.derived, wd, cvec, static_cast<uint8_t*>(u.dst), u.scratch.acc);
     e = int(hipGetLastError());
     if (e) return e;
   }

@@ -674,8 +674,8 @@ int build_delta(fr_plan* p, const std::vector<ChunkRec>& recs, const Staging& st
   const uint64_t b_units = up(std::max(nc * sizeof(SrcUnit), L.n_sent_chunks * sizeof(PlainUnit) +
                                                               (nc - L.n_sent_chunks) * sizeof(DerivedUnit)));
   const uint64_t b_agg = up(nb * sizeof(DeltaAgg)), b_pre = up(nb * sizeof(DeltaPre));
-  const uint64_t b_counts = 256, b_bits = up(nw * 4), b_ids = up(nc * 4);
-  const uint64_t total = b_loc + b_units + b_agg + b_pre + b_counts + b_bits + b_ids;
+  const uint64_t b_counts = 256, b_bits = up(nw * 4), b_ids = up(nc * 4), b_payof = up(nc * 8);
+  const uint64_t total = b_loc + b_units + b_agg + b_pre + b_counts + b_bits + b_ids + b_payof + b_ids;
   int rc = upload(nullptr, total, &p->d_delta, st.s);
   if (rc != FR_OK) return rc;
   uint8_t* q = static_cast<uint8_t*>(p->d_delta);
@@ -694,7 +694,10 @@ int build_delta(fr_plan* p, const std::vector<ChunkRec>& recs, const Staging& st
   p->d_delta_counts = reinterpret_cast<uint64_t*>(take(b_counts));
   p->d_delta_bits = reinterpret_cast<uint32_t*>(take(b_bits));
   p->d_delta_ids = reinterpret_cast<uint32_t*>(take(b_ids));
+  p->d_delta_payof = reinterpret_cast<uint64_t*>(take(b_payof));
+  p->d_delta_m0 = reinterpret_cast<uint32_t*>(take(b_ids));
   std::vector<ChunkLoc> loc(nc);
+  std::vector<uint32_t> m0(nc, 0);
   for (uint32_t k = 0; k < p->table.size(); k++) {
     const uint64_t c0 = L.chunk_base[k], c1 = L.chunk_base[k + 1];
     for (uint64_t c = c0; c < c1; c++) {
@@ -707,9 +710,11 @@ int build_delta(fr_plan* p, const std::vector<ChunkRec>& recs, const Staging& st
       l.len = r.len;
       l.flags = (r.master == kNoMaster ? 0u : kLocDerived) | (c == c0 ? kLocFirst : 0u) |
                 (c + 1 == c1 ? kLocLast : 0u);
+      m0[c] = r.master == kNoMaster ? 0u : r.master;
     }
   }
   rc = copy_in(p->d_delta_loc, loc.data(), nc * sizeof(ChunkLoc), st.s);
+  if (rc == FR_OK) rc = copy_in(p->d_delta_m0, m0.data(), nc * sizeof(uint32_t), st.s);
   if (rc != FR_OK) return rc;
   hipError_t e = hipSuccess;
   if (nc)
