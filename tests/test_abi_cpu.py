@@ -62,6 +62,7 @@ def _check_layout(t, C, sb, db, seg=16):
     assert info["payload_bytes"] == opb
     assert info["n_chunks"] == int(obase[-1])
     assert info["bitmap_words"] == (int(obase[-1]) + 31) // 32
+    assert info["device"] == -1 and info["pack_walk"] == info["unpack_walk"] == 0  # no plan
     assert np.array_equal(base, obase)
     for k in range(len(t)):
         if int(t[k]["derive_from"]) >= 0:
