@@ -159,13 +159,18 @@ __device__ __forceinline__ u32x4 mask_tail(const u32x4& x, uint32_t t) {
   return u32x4{o[0], o[1], o[2], o[3]};
 }
 
-// 64-bit value of lane (i op CTRL) for a DPP lane pattern, moved as two
-// 32-bit halves.
+// v plus the v of lane (i op CTRL) for a DPP lane pattern that reads a
+// lane for every lane: the halves moved across lanes (no old value kept),
+// then added as 32-bit halves with a carry (fewer instructions than a
+// 64-bit move and add).
 template <int CTRL>
-__device__ __forceinline__ u64 dpp64(u64 v) {
-  const uint32_t lo = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(v)), CTRL, 0xF, 0xF, false));
-  const uint32_t hi = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(v >> 32)), CTRL, 0xF, 0xF, false));
-  return (u64(hi) << 32) | lo;
+__device__ __forceinline__ u64 add_dpp(u64 v) {
+  const uint32_t lo = uint32_t(v), hi = uint32_t(v >> 32);
+  const uint32_t plo = uint32_t(__builtin_amdgcn_mov_dpp(int(lo), CTRL, 0xF, 0xF, false));
+  const uint32_t phi = uint32_t(__builtin_amdgcn_mov_dpp(int(hi), CTRL, 0xF, 0xF, false));
+  const uint32_t rlo = lo + plo;
+  const uint32_t rhi = hi + phi + (rlo < lo ? 1u : 0u);
+  return (u64(rhi) << 32) | rlo;
 }
 
 __device__ __forceinline__ u64 readlane64(u64 v, int lane) {
@@ -180,10 +185,10 @@ __device__ __forceinline__ u64 readlane64(u64 v, int lane) {
 // every lane of a row holds the row's total; the four row totals are then
 // read into scalar registers and added.
 __device__ __forceinline__ u64 wave_sum(u64 v) {
-  v += dpp64<0xB1>(v);   // quad_perm [1,0,3,2]
-  v += dpp64<0x4E>(v);   // quad_perm [2,3,0,1]
-  v += dpp64<0x124>(v);  // row_ror:4
-  v += dpp64<0x128>(v);  // row_ror:8
+  v = add_dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+  v = add_dpp<0x4E>(v);   // quad_perm [2,3,0,1]
+  v = add_dpp<0x124>(v);  // row_ror:4
+  v = add_dpp<0x128>(v);  // row_ror:8
   return readlane64(v, 0) + readlane64(v, 16) + readlane64(v, 32) + readlane64(v, 48);
 }
 

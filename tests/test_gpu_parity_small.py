@@ -439,6 +439,68 @@ def test_payload_block_walks_match_oracle(tile):
                 os.environ[k] = v
 
 
+def _overlapping_sender_table(rng, n_max=10, max_numel=3000):
+    """Entries whose sender ranges overlap (the sender arena is about half
+    the bytes the entries read; any 16-byte offset), receiver ranges apart.
+    No derived entries."""
+    n = int(rng.integers(2, n_max + 1))
+    numel = rng.integers(0, max_numel + 1, size=n).astype(np.uint64)
+    dts = np.where(rng.random(n) < 0.5, W.F32, W.BF16).astype(np.uint32)
+    nbytes = numel * np.where(dts == W.F32, 4, 2).astype(np.uint64)
+    span = max(16, int(nbytes.sum()) // 32 * 16)
+    src_off = np.array([int(rng.integers(0, span // 16 + 1)) * 16 for _ in range(n)], dtype=np.uint64)
+    sb = int(max(int(src_off[k] + nbytes[k]) for k in range(n)))
+    sb = -(-sb // 16) * 16
+    dst_off, db = W._scatter_layout(nbytes, rng)
+    t = np.zeros(n, dtype=W.TABLE_DTYPE)
+    t["src_offset"], t["dst_offset"], t["numel"], t["dtype"] = src_off, dst_off, numel, dts
+    t["derive_from"] = -1
+    return t, sb, int(db)
+
+
+WALK_SETS = {
+    "default": {},
+    "lines": {"FLASHRESTORE_LINE": "1"},
+    "payload tiles": {"FLASHRESTORE_LINE_PACK": "4", "FLASHRESTORE_LINE_UNPACK": "4"},
+    "slices": {"FLASHRESTORE_LINE": "0"},
+    "buffer loads": {"FLASHRESTORE_BUF_PACK": "1", "FLASHRESTORE_BUF_UNPACK": "1",
+                     "FLASHRESTORE_BUF_VERIFY": "1", "FLASHRESTORE_BUF_CHECKSUM": "1"},
+}
+
+
+@pytest.mark.parametrize("walks", sorted(WALK_SETS))
+@pytest.mark.parametrize("tile", [None, 3, 7])
+def test_overlapping_sender_ranges_match_oracle(walks, tile):
+    """Entries may read the same sender bytes (their receiver ranges stay
+    apart): pack, unpack, compare and checksum give the oracle's payload,
+    sums, receiver arena and bad sets when sender ranges overlap, at any
+    16-byte offset, from tiny chunks (many per slice) to large ones, with
+    capped grids, under every walk."""
+    names = ("FLASHRESTORE_TILE", "FLASHRESTORE_MAX_GRID") + tuple(
+        {k for env in WALK_SETS.values() for k in env})
+    old = {k: os.environ.get(k) for k in names}
+    for k in names:
+        os.environ.pop(k, None)
+    os.environ.update(WALK_SETS[walks])
+    if tile is not None:
+        os.environ["FLASHRESTORE_TILE"] = str(tile)
+    rng = np.random.default_rng(1700 + (tile or 0) + 31 * sorted(WALK_SETS).index(walks))
+    try:
+        for it in range(10):
+            os.environ["FLASHRESTORE_MAX_GRID"] = str(int(rng.choice([0, 0, 7])))
+            t, sb, db = _overlapping_sender_table(rng, max_numel=int(rng.choice([300, 30_000])))
+            C = int(rng.choice([16, 64, 1024, 16384]))
+            src = rng.integers(0, 256, size=sb, dtype=np.uint8)
+            _check_against_oracle(t, C, src, sb, db, corrupt_rng=rng,
+                                  tag=f"overlap {walks} tile {tile} table {it} C={C}")
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
 @pytest.mark.parametrize("tile", [3, 4, 5, 7])
 @pytest.mark.parametrize("line", ["0", "1", "2"])
 def test_buffer_load_slices_match_oracle(tile, line):
