@@ -178,8 +178,10 @@ typedef struct fr_plan_info {
  * results never depend on them: FLASHRESTORE_TILE (every operation) or
  * FLASHRESTORE_TILE_PACK / _UNPACK / _VERIFY / _CHECKSUM select a tile
  * 0-10 (threads x 16-byte vectors per workgroup: 256x1, 512x1, 256x2,
- * 256x4, 64x4, 128x2, 64x2, 64x1, 128x1, 128x4, 64x8; defaults pack 64x4,
- * unpack and compare 128x2, checksum 256x4), FLASHRESTORE_LINE (every
+ * 256x4, 64x4, 128x2, 64x2, 64x1, 128x1, 128x4, 64x8; unset, by chunk
+ * size: pack 64x4; unpack 64x1 up to 1 KiB chunks, 64x2 at 2 KiB, else
+ * 128x2; compare 64x1 up to 2 KiB, else 128x2; checksum 64x4 up to 4 KiB,
+ * 128x4 at 8 KiB, else 256x4), FLASHRESTORE_LINE (every
  * operation) or FLASHRESTORE_LINE_PACK / _UNPACK / _VERIFY / _CHECKSUM
  * choose how work is divided for data placed inside 128-byte lines: 0
  * plain slices of chunks, 1 slices cut at lines of the arena read (unpack:

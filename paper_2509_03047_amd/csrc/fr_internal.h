@@ -308,6 +308,8 @@ constexpr int kLineBlocks = 4;
 // Blocks where chunks of the side written start inside lines, else the
 // operation's line walk.
 constexpr int kLineAuto = -1;
+// A tile chosen by the chunk size at plan creation (no tile variable set).
+constexpr int kTileAuto = -1;
 
 // Unpack walked by blocks of the receiver arena: the plain chunks in
 // receiver order, the tiles that hold some of their bytes, and the walk of

@@ -23,6 +23,23 @@ thread_local int g_last_hip_error = 0;
 // 8B and 70B rank shares and the descriptor stress table.
 constexpr uint32_t kDefaultTilePack = 4, kDefaultTileUnpack = 5, kDefaultTileVerify = 5,
                    kDefaultTileChecksum = 3;
+
+// The tile an operation takes for chunks of C bytes when no tile variable is
+// set: the default above, except that chunks smaller than its slice would
+// leave most lanes idle, so smaller chunks take smaller tiles (sweeps of
+// seven tiles at 1-8 KiB chunks on the 8B share and the stress table:
+// unpack 2.7 -> 4.1 TB/s at 1 KiB with 64 x 1, compare 3.8 -> 7.2, the
+// checksum 1.0 -> 3.2 at 1 KiB and 3.8 -> 6.6 at 4 KiB with 64 x 4; pack is
+// as fast with its default at every size).
+enum TileOp { kOpPack, kOpUnpack, kOpVerify, kOpChecksum };
+int auto_tile(TileOp op, uint64_t C) {
+  switch (op) {
+    case kOpUnpack: return C <= 1024 ? 7 : C <= 2048 ? 6 : int(kDefaultTileUnpack);
+    case kOpVerify: return C <= 2048 ? 7 : int(kDefaultTileVerify);
+    case kOpChecksum: return C <= 4096 ? 4 : C <= 8192 ? 9 : int(kDefaultTileChecksum);
+    default: return int(kDefaultTilePack);
+  }
+}
 // Walks (0 plain; 1 cut at lines of the arena read, for unpack of the
 // receiver; 2 at lines of the payload; 4 by blocks of the payload): pack and
 // unpack by payload blocks when payload chunks start inside lines (16-byte
@@ -305,10 +322,10 @@ LaunchCfg launch_config() {
   auto pick = [&](const char* name, uint32_t dflt) {
     return int(env_u32(name, all != ~0u ? all : dflt));
   };
-  cfg.tile_pack = pick("FLASHRESTORE_TILE_PACK", kDefaultTilePack);
-  cfg.tile_unpack = pick("FLASHRESTORE_TILE_UNPACK", kDefaultTileUnpack);
-  cfg.tile_verify = pick("FLASHRESTORE_TILE_VERIFY", kDefaultTileVerify);
-  cfg.tile_checksum = pick("FLASHRESTORE_TILE_CHECKSUM", kDefaultTileChecksum);
+  cfg.tile_pack = pick("FLASHRESTORE_TILE_PACK", uint32_t(kTileAuto));
+  cfg.tile_unpack = pick("FLASHRESTORE_TILE_UNPACK", uint32_t(kTileAuto));
+  cfg.tile_verify = pick("FLASHRESTORE_TILE_VERIFY", uint32_t(kTileAuto));
+  cfg.tile_checksum = pick("FLASHRESTORE_TILE_CHECKSUM", uint32_t(kTileAuto));
   // walks: 0 plain, 1 lines of the arena read (for unpack: of the receiver
   // arena written), 2 payload lines, 3 payload slices, 4 payload blocks
   // (pack and unpack take 1-4; compare and checksum 0 or 1, any nonzero
@@ -752,6 +769,11 @@ extern "C" int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n, uint64
     }
     p->device = dev;
     p->cfg = launch_config();
+    auto tile = [&](int t, TileOp op) { return t == kTileAuto ? auto_tile(op, C) : t; };
+    p->cfg.tile_pack = tile(p->cfg.tile_pack, kOpPack);
+    p->cfg.tile_unpack = tile(p->cfg.tile_unpack, kOpUnpack);
+    p->cfg.tile_verify = tile(p->cfg.tile_verify, kOpVerify);
+    p->cfg.tile_checksum = tile(p->cfg.tile_checksum, kOpChecksum);
 
     const Layout& L = p->layout;
     const std::vector<ChunkRec> recs = chunk_records(table, n, L);
