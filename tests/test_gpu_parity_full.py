@@ -12,6 +12,8 @@ times (default plan, one workgroup per unit).
   (exact round trip, nothing flagged, checksum == pack sums, replica compare
   empty); a replica with 4,096 flips: compare set, both arenas' sums and the
   checksum against the whole oracle.
+* One tensor of 1.2 G parameters (16.8 GB state): offsets past 2^32 bytes
+  inside one entry, whole oracle and a wire flip 4.5 GB into the master.
 * Replica compare on two copies of the 8B share with k in {0, 1, 64, 4096}
   distinct random bit flips: the flagged set equals the closed form
   {chunk of each flipped byte} and the oracle's set; the 4,096-flip replica
@@ -26,6 +28,7 @@ pytestmark = pytest.mark.gpu
 from oracle import cpu  # noqa: E402
 from paper_2509_03047_amd import workloads as W  # noqa: E402
 
+from paper_2509_03047_amd import flashrestore as F  # noqa: E402
 from tests.gpu_util import Restore, log, sums_host, to_host  # noqa: E402
 
 
@@ -98,6 +101,68 @@ def test_llama8b_tp8_full_parity(llama8b):
     assert np.array_equal(to_host(r.dst), dst)
     assert int(r.n_diff.item()) == 0 and r.diff_set() == set()
     assert np.array_equal(sums_host(r.csum, nc), sums)
+
+
+@pytest.fixture(scope="module")
+def over_4gib():
+    """A table whose middle tensor has 1.2 G parameters: its fp32 master, m
+    and v are 4.8 GB entries each, past 2^32 bytes inside one entry."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    tensors = [("head", 3_001), ("huge", 1_200_000_000), ("tail", 70_001)]
+    table, nb = W.state_table(tensors)
+    w = W.Workload("one-tensor-over-4GiB", table, 1 << 20, nb, nb, tensors, 7)
+    log(f"generating {w.name} ({w.state_bytes} B)")
+    return w, W.fill_state(w)
+
+
+@pytest.mark.timeout(900)
+def test_tensor_over_4gib_full_parity(over_4gib):
+    """Offsets past 2^32 bytes inside one entry: the master, m and v of one
+    tensor are 4.8 GB each, its bf16 image (2.4 GB) is re-derived from master
+    bytes read up to 4.8 GB into the entry, and the last tensor starts past
+    16 GB.  Whole oracle: payload, sums, receiver arena (canaries in the
+    padding), flags, compare and checksum; then a wire flip 4.5 GB into the
+    master's payload is flagged as the oracle flags it."""
+    w, src_np = over_4gib
+    t, C = w.table, w.chunk_bytes
+    assert int(t["numel"][5]) * 4 > (1 << 32) and int(t["src_offset"][8]) > 16 * 10**9
+    r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes, canary=0xA5)
+    src = _upload(src_np)
+    r.pack(src)
+    r.unpack()
+    r.verify(src, r.dst)
+    r.checksum(r.dst)
+    torch.cuda.synchronize()
+    log("gpu ops done")
+    pay, sums = cpu.pack(t, C, src_np)
+    log("oracle pack done")
+    nc = r.n_chunks
+    assert np.array_equal(sums_host(r.sums, nc), sums)
+    g_pay = to_host(r.payload)
+    assert np.array_equal(g_pay[: pay.size], pay)
+    del g_pay
+    dst = np.full(w.dst_arena_bytes, 0xA5, np.uint8)
+    bm, nbad = cpu.unpack(t, C, pay, sums, dst)
+    log("oracle unpack done")
+    assert nbad == 0 and int(r.n_bad.item()) == 0 and r.bad_set() == set()
+    assert np.array_equal(to_host(r.dst), dst)
+    assert int(r.n_diff.item()) == 0 and r.diff_set() == set()
+    assert np.array_equal(sums_host(r.csum, nc), sums)
+    # a wire flip 4.5 GB into the huge master's payload segment
+    info, pay_of_entry, base = F.fr_layout_query(t, C, w.src_arena_bytes, w.dst_arena_bytes)
+    byte = int(pay_of_entry[5]) + 4_500_000_003
+    pay[byte] ^= np.uint8(0x10)
+    r.payload[byte] ^= 0x10
+    r.dst.fill_(0xA5)
+    r.unpack()
+    dst.fill(0xA5)
+    bm, nbad = cpu.unpack(t, C, pay, sums, dst)
+    log("flipped unpack done")
+    want = set(cpu.bitmap_to_set(bm, nc))
+    assert int(base[5]) + 4_500_000_003 // C in want
+    assert r.bad_set() == want and int(r.n_bad.item()) == nbad
+    assert np.array_equal(to_host(r.dst), dst)
 
 
 @pytest.mark.timeout(900)
