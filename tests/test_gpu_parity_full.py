@@ -103,7 +103,7 @@ def test_llama8b_tp8_full_parity(llama8b):
     assert np.array_equal(sums_host(r.csum, nc), sums)
 
 
-@pytest.fixture(scope="module")
+@pytest.fixture
 def over_4gib():
     """A table whose middle tensor has 1.2 G parameters: its fp32 master, m
     and v are 4.8 GB entries each, past 2^32 bytes inside one entry."""
