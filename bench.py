@@ -45,6 +45,8 @@ WALK_TILES = 4  # fr_plan_info pack_walk / unpack_walk: one aligned tile of the 
 TILE_KERNELS = {"pack": "k_pack_blocks", "unpack": "k_unpack_blocks"}
 WALK_NAMES = {0: "slices", 1: "slices cut at arena / receiver lines", 2: "slices cut at payload lines",
               3: "slices cut at payload slice boundaries", WALK_TILES: "tiles of the side written"}
+# fr_plan_info tile_*: threads x 16-byte vectors per workgroup
+TILE_SHAPES = ("256x1", "512x1", "256x2", "256x4", "64x4", "128x2", "64x2", "64x1", "128x1", "128x4", "64x8")
 
 
 def _code_only(text: str) -> str:
@@ -678,6 +680,8 @@ def main():
             "n_chunks": info["n_chunks"],
             "step": "pack+checksum -> unpack+derive+verify -> verify_replicas -> checksum_state",
             "walks": {op: WALK_NAMES.get(v, str(v)) for op, v in walks.items()},
+            "tiles": {op: TILE_SHAPES[info[f"tile_{op}"]] if info[f"tile_{op}"] < len(TILE_SHAPES)
+                      else str(info[f"tile_{op}"]) for op in ("pack", "unpack", "verify", "checksum")},
         },
         "restore_ms": round(restore_ms, 4),
         "step_gbs": round(info["state_bytes"] / (ms_step * 1e-3) / 1e9, 2),

@@ -89,7 +89,7 @@
 extern "C" {
 #endif
 
-#define FR_ABI_VERSION 5
+#define FR_ABI_VERSION 6
 
 enum fr_dtype { FR_F32 = 1, FR_BF16 = 2 };
 
@@ -148,6 +148,12 @@ typedef struct fr_plan_info {
                                pack, the receiver arena for unpack) per workgroup,
                                the default where that side's chunks start inside
                                cache lines; FR_WALK_* */
+  uint32_t tile_pack;       /* the tile each operation launches with, 0-10 (threads x */
+  uint32_t tile_unpack;     /* 16-byte vectors per workgroup: 256x1, 512x1, 256x2, */
+  uint32_t tile_verify;     /* 256x4, 64x4, 128x2, 64x2, 64x1, 128x1, 128x4, 64x8): */
+  uint32_t tile_checksum;   /* set by FLASHRESTORE_TILE*, else chosen by chunk size;
+                               a layout query reports what a plan created now, in
+                               the same environment, would take */
 } fr_plan_info;
 
 #define FR_WALK_SLICES 0

@@ -155,7 +155,8 @@ int validate_and_layout(const fr_tensor_desc* t, uint32_t n, uint64_t C, uint64_
 }
 
 static void fill_info(const Layout& L, uint32_t n, uint64_t src, uint64_t dst, int64_t dev,
-                      fr_plan_info* info, uint32_t pack_walk = 0, uint32_t unpack_walk = 0) {
+                      const LaunchCfg& cfg, fr_plan_info* info, uint32_t pack_walk = 0,
+                      uint32_t unpack_walk = 0) {
   info->n_entries = n;
   info->chunk_bytes = L.C;
   info->n_chunks = L.n_chunks;
@@ -169,6 +170,10 @@ static void fill_info(const Layout& L, uint32_t n, uint64_t src, uint64_t dst, i
   info->delta_payload_max = L.delta_payload_max;
   info->pack_walk = pack_walk;
   info->unpack_walk = unpack_walk;
+  info->tile_pack = uint32_t(cfg.tile_pack);
+  info->tile_unpack = uint32_t(cfg.tile_unpack);
+  info->tile_verify = uint32_t(cfg.tile_verify);
+  info->tile_checksum = uint32_t(cfg.tile_checksum);
 }
 
 static uint32_t env_u32(const char* name, uint32_t dflt) {
@@ -183,6 +188,8 @@ static uint32_t env_u32(const char* name, uint32_t dflt) {
 
 using namespace fr;
 
+LaunchCfg plan_launch_config(uint64_t C);
+
 extern "C" int fr_layout_query(const fr_tensor_desc* table, uint32_t n, uint64_t C,
                                uint64_t src_bytes, uint64_t dst_bytes, uint64_t seg,
                                fr_plan_info* info, uint64_t* payload_offset,
@@ -196,7 +203,7 @@ extern "C" int fr_layout_query(const fr_tensor_desc* table, uint32_t n, uint64_t
     return FR_E_NOMEM;
   }
   if (rc != FR_OK) return rc;
-  fill_info(L, n, src_bytes, dst_bytes, -1, info);
+  fill_info(L, n, src_bytes, dst_bytes, -1, plan_launch_config(C), info);
   if (payload_offset && n) std::memcpy(payload_offset, L.pay_off.data(), sizeof(uint64_t) * n);
   if (chunk_base) std::memcpy(chunk_base, L.chunk_base.data(), sizeof(uint64_t) * (size_t(n) + 1));
   return FR_OK;
@@ -355,6 +362,22 @@ LaunchCfg launch_config() {
   cfg.line_checksum = lpick("FLASHRESTORE_LINE_CHECKSUM", kDefaultLineChecksum, 0x2);
   return cfg;
 }
+
+}  // namespace
+
+// The launch configuration of a plan for chunks of C bytes: the
+// environment's, with the tiles left unset chosen by chunk size.
+LaunchCfg plan_launch_config(uint64_t C) {
+  LaunchCfg cfg = launch_config();
+  auto tile = [&](int t, TileOp op) { return t == kTileAuto ? auto_tile(op, C) : t; };
+  cfg.tile_pack = tile(cfg.tile_pack, kOpPack);
+  cfg.tile_unpack = tile(cfg.tile_unpack, kOpUnpack);
+  cfg.tile_verify = tile(cfg.tile_verify, kOpVerify);
+  cfg.tile_checksum = tile(cfg.tile_checksum, kOpChecksum);
+  return cfg;
+}
+
+namespace {
 
 // One record per global chunk.
 std::vector<ChunkRec> chunk_records(const fr_tensor_desc* table, uint32_t n, const Layout& L) {
@@ -768,12 +791,7 @@ extern "C" int fr_plan_create_ex(const fr_tensor_desc* table, uint32_t n, uint64
       return hip_fail(e);
     }
     p->device = dev;
-    p->cfg = launch_config();
-    auto tile = [&](int t, TileOp op) { return t == kTileAuto ? auto_tile(op, C) : t; };
-    p->cfg.tile_pack = tile(p->cfg.tile_pack, kOpPack);
-    p->cfg.tile_unpack = tile(p->cfg.tile_unpack, kOpUnpack);
-    p->cfg.tile_verify = tile(p->cfg.tile_verify, kOpVerify);
-    p->cfg.tile_checksum = tile(p->cfg.tile_checksum, kOpChecksum);
+    p->cfg = plan_launch_config(C);
 
     const Layout& L = p->layout;
     const std::vector<ChunkRec> recs = chunk_records(table, n, L);
@@ -841,7 +859,7 @@ extern "C" int fr_plan_get_info(const fr_plan* p, fr_plan_info* info) {
   const uint32_t uw = c.line_unpack == kLineBlocks ? uint32_t(kLineBlocks)
                                                    : line_walk(p, c.tile_unpack, c.line_unpack, true);
   fill_info(p->layout, uint32_t(p->table.size()), p->src_arena_bytes, p->dst_arena_bytes,
-            p->device, info, pw, uw);
+            p->device, c, info, pw, uw);
   return FR_OK;
 }
 

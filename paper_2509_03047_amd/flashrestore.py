@@ -53,6 +53,10 @@ class fr_plan_info(C.Structure):
         ("delta_payload_max", C.c_uint64),
         ("pack_walk", C.c_uint32),
         ("unpack_walk", C.c_uint32),
+        ("tile_pack", C.c_uint32),
+        ("tile_unpack", C.c_uint32),
+        ("tile_verify", C.c_uint32),
+        ("tile_checksum", C.c_uint32),
     ]
 
     def as_dict(self):
@@ -132,7 +136,7 @@ def _load():
         f.argtypes = args
         f.restype = C.c_int
     lib.fr_strerror.restype = C.c_char_p
-    if lib.fr_abi_version() != 5:
+    if lib.fr_abi_version() != 6:
         raise ImportError("libflashrestore ABI version mismatch")
     return lib
 

@@ -49,7 +49,7 @@ def test_library_is_gfx950_only():
 
 
 def test_version_and_strerror():
-    assert F.fr_abi_version() == 5
+    assert F.fr_abi_version() == 6
     msgs = {c: F.fr_strerror(c) for c in range(-7, 1)}
     assert msgs[0] == "ok" and len(set(msgs.values())) == 8
     assert F.fr_strerror(-99) == "unknown status"
@@ -172,6 +172,44 @@ def test_segment_alignment_rule(seg, code):
     except F.FlashRestoreError as e:
         rc = e.status
     assert rc == code
+
+
+TILE_KEYS = ("tile_pack", "tile_unpack", "tile_verify", "tile_checksum")
+
+
+def _tiles(C):
+    info, _, _ = F.fr_layout_query(_rows(), C, 1 << 20, 1 << 20)
+    return tuple(info[k] for k in TILE_KEYS)
+
+
+def _clear_tile_env(monkeypatch):
+    for k in list(os.environ):
+        if k.startswith("FLASHRESTORE_TILE"):
+            monkeypatch.delenv(k)
+
+
+@pytest.mark.parametrize("C, want", [(16, (4, 7, 7, 4)), (1024, (4, 7, 7, 4)), (2048, (4, 6, 7, 4)),
+                                     (4096, (4, 5, 5, 4)), (8192, (4, 5, 5, 9)), (16384, (4, 5, 5, 3)),
+                                     (1 << 30, (4, 5, 5, 3))])
+def test_tiles_follow_the_chunk_size(C, want, monkeypatch):
+    """Unset, each operation's tile follows the chunk size (pack 64x4 = 4;
+    unpack 64x1 = 7 up to 1 KiB, 64x2 = 6 at 2 KiB, else 128x2 = 5; compare
+    64x1 up to 2 KiB, else 128x2; checksum 64x4 up to 4 KiB, 128x4 = 9 at
+    8 KiB, else 256x4 = 3)."""
+    _clear_tile_env(monkeypatch)
+    assert _tiles(C) == want
+
+
+def test_tile_variables_override_the_chunk_size_rule(monkeypatch):
+    _clear_tile_env(monkeypatch)
+    monkeypatch.setenv("FLASHRESTORE_TILE", "9")
+    assert _tiles(1024) == (9, 9, 9, 9)
+    monkeypatch.setenv("FLASHRESTORE_TILE_CHECKSUM", "2")
+    assert _tiles(1024) == (9, 9, 9, 2)
+    monkeypatch.delenv("FLASHRESTORE_TILE")
+    monkeypatch.setenv("FLASHRESTORE_TILE_UNPACK", "0")
+    assert _tiles(1024) == (4, 0, 7, 2)
+    assert _tiles(1 << 20) == (4, 0, 5, 2)
 
 
 def test_chunk_id_limit():

@@ -49,6 +49,8 @@ def test_bench_json_line(config, extra):
     if config == 2:
         assert walks == {"pack": "tiles of the side written", "unpack": "tiles of the side written"}
         assert r["kernel"] in ("k_pack_blocks", "k_unpack_blocks", "k_verify", "k_pack")
+    # 64 KiB and 16 KiB chunks keep every operation's default tile
+    assert d["config"]["tiles"] == {"pack": "64x4", "unpack": "128x2", "verify": "128x2", "checksum": "256x4"}
     assert abs(r["frac"] - r["achieved"] / r["peak"]) < 1e-3
     assert d["parity_ok"] is True
     assert d["delta_repair"]["ok"] is True and d["control_plane"]["ok"] is True

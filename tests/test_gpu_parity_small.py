@@ -588,6 +588,10 @@ def test_walks_follow_the_alignment_of_the_side_written():
             sb, db = so[-1] + 1344, do[-1] + 1344
             plan = F.Plan(t, 1024, sb, db, segment_align=seg)
             assert (plan.info["pack_walk"], plan.info["unpack_walk"]) == want, (so, do, seg)
+            # the tiles the plan took are the ones a layout query predicts
+            q, _, _ = F.fr_layout_query(t, 1024, sb, db, seg)
+            for k in ("tile_pack", "tile_unpack", "tile_verify", "tile_checksum"):
+                assert plan.info[k] == q[k], k
             del plan
             src = W.random_tiny_state(t, sb, rng)
             _check_against_oracle(t, 1024, src, sb, db, corrupt_rng=rng, seg=seg, tag=f"walks {want}")
