@@ -1,6 +1,7 @@
 """Randomised GPU parity campaign: random tables (1-200 entries, scattered
 layouts, derived parameters), each under a random launch configuration
-(tile, the pack / unpack / compare / checksum walks, absorbing last slices,
+(one tile for all, or tiles chosen by chunk size, sometimes one operation
+with its own, the pack / unpack / compare / checksum walks, absorbing last slices,
 buffer loads, walk orders, grid and delta grid caps) and a random payload
 segment alignment, chunks of 16 B to 1 MiB, random wire corruption; whole
 restore, replica compare, checksum and (at 16-byte segments) a delta repair
@@ -34,7 +35,11 @@ KNOBS = ("FLASHRESTORE_TILE", "FLASHRESTORE_LINE_PACK", "FLASHRESTORE_LINE_UNPAC
 def _random_knobs(rng) -> str:
     for k in KNOBS:
         os.environ.pop(k, None)
-    os.environ["FLASHRESTORE_TILE"] = str(int(rng.integers(0, 11)))
+    tile = int(rng.integers(-4, 11))  # negative: unset, each tile chosen by the chunk size
+    if tile >= 0:
+        os.environ["FLASHRESTORE_TILE"] = str(tile)
+    if rng.random() < 0.25:  # one operation with a tile of its own
+        os.environ[str(rng.choice(KNOBS[16:]))] = str(int(rng.integers(0, 11)))
     for k in ("FLASHRESTORE_LINE_PACK", "FLASHRESTORE_LINE_UNPACK"):
         v = int(rng.integers(-1, 5))  # -1: unset, the walk chosen by the table
         if v >= 0:
