@@ -4,6 +4,8 @@ and replayed several times, with eager work and synchronisation between
 replays, every replay checked against the eager result; a replica compare and
 the repair it drives (the flagged delta calls) captured and replayed on
 different divergences; and two plans run concurrently on two streams."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -14,27 +16,31 @@ from paper_2509_03047_amd import flashrestore as F  # noqa: E402
 from paper_2509_03047_amd import workloads as W  # noqa: E402
 
 
-def _scattered_case():
+def _scattered_case(C=4096):
     """40 tensors at shuffled 16-byte offsets (the same layout on both
     sides, so the receiver equals the sender): pack and unpack walk tiles."""
     rng = np.random.default_rng(8)
     t, sb, _ = W.random_tiny_table(rng, max_entries=40, max_numel=60_000)
     t["dst_offset"] = t["src_offset"]
-    return t, 4096, sb, sb, W.random_tiny_state(t, sb, rng)
+    return t, C, sb, sb, W.random_tiny_state(t, sb, rng)
 
 
-@pytest.mark.parametrize("case", ["toy", "scattered"])
-def test_captured_restore_step_replays_correctly(case):
+@pytest.mark.parametrize("case", ["toy", "scattered", "scattered 1 KiB chunks"])
+def test_captured_restore_step_replays_correctly(case, monkeypatch):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     if case == "toy":
         w = W.make_workload(0)
         table, C, sb, db, src_np = w.table, w.chunk_bytes, w.src_arena_bytes, w.dst_arena_bytes, W.fill_state(w)
-    else:
-        table, C, sb, db, src_np = _scattered_case()
+    else:  # 1 KiB chunks: unpack and the compare take 64 x 1 tiles, the checksum 64 x 4
+        table, C, sb, db, src_np = _scattered_case(1024 if "1 KiB" in case else 4096)
+    for k in [k for k in os.environ if k.startswith("FLASHRESTORE_TILE")]:
+        monkeypatch.delenv(k)
     plan = F.Plan(table, C, sb, db)
-    if case == "scattered":
+    if case != "toy":
         assert plan.info["pack_walk"] == 4 and plan.info["unpack_walk"] == 4
+    if "1 KiB" in case:
+        assert (plan.info["tile_unpack"], plan.info["tile_verify"], plan.info["tile_checksum"]) == (7, 7, 4)
     src = torch.from_numpy(src_np).to("cuda")
     payload, sums = plan.empty_payload(), plan.empty_sums()
     dst = torch.zeros(db, dtype=torch.uint8, device="cuda")
