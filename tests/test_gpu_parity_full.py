@@ -4,8 +4,9 @@ times (default plan, one workgroup per unit).
 * Llama-3-8B TP=8 rank share (14.06 GB state): the whole oracle runs on the
   host; payload, sums, receiver arena and result sets are compared bit for bit.
 * 20,000-entry descriptor stress (7.6 GB): whole oracle, scattered layouts,
-  canaries in every receiver gap; its replica compare (line-aligned, since
-  its tensors start inside cache lines) with flips at chunk and line edges.
+  canaries in every receiver gap, at 16-byte and 4 KiB payload segments;
+  its replica compare (line-aligned, since its tensors start inside cache
+  lines) with flips at chunk and line edges.
 * Llama-3-70B TP=8 x PP=4 first-stage share (31.8 GB): the whole oracle on
   the host (payload, sums and receiver arena compared slice by slice), plus
   sampled chunks, a located wire flip and properties that hold at any size
@@ -246,6 +247,43 @@ def test_descriptor_stress_full_parity():
     dst = np.full(w.dst_arena_bytes, 0xA5, np.uint8)
     bm, nbad = cpu.unpack(t, C, pay, sums, dst)
     assert r.bad_set() == set(cpu.bitmap_to_set(bm, nc)) and int(r.n_bad.item()) == nbad
+
+
+@pytest.mark.timeout(900)
+def test_descriptor_stress_4kib_segments_full_parity():
+    """The stress table with the 4 KiB payload-segment wire format (every
+    segment starts on a 4 KiB boundary, gaps zero): pack walks plain slices,
+    unpack walks receiver tiles; whole oracle at that alignment, and a
+    corrupted wire."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    w = W.make_workload(2)
+    t, C = w.table, w.chunk_bytes
+    src_np = W.fill_state(w)
+    r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes, canary=0xA5, seg=4096)
+    assert (r.plan.info["pack_walk"], r.plan.info["unpack_walk"]) == (0, 4)
+    src = _upload(src_np)
+    r.pack(src)
+    r.unpack()
+    torch.cuda.synchronize()
+    pay, sums = cpu.pack(t, C, src_np, 4096)
+    nc = r.n_chunks
+    assert np.array_equal(sums_host(r.sums, nc), sums)
+    assert np.array_equal(to_host(r.payload)[: pay.size], pay)
+    dst = np.full(w.dst_arena_bytes, 0xA5, np.uint8)
+    bm, nbad = cpu.unpack(t, C, pay, sums, dst, 4096)
+    assert nbad == 0 and r.bad_set() == set() and int(r.n_bad.item()) == 0
+    assert np.array_equal(to_host(r.dst), dst)
+    rng = np.random.default_rng(6)
+    for _ in range(3):
+        bit = int(rng.integers(0, pay.size * 8))
+        pay[bit // 8] ^= np.uint8(1 << (bit % 8))
+        r.payload[bit // 8] ^= 1 << (bit % 8)
+    r.unpack()
+    dst = np.full(w.dst_arena_bytes, 0xA5, np.uint8)
+    bm, nbad = cpu.unpack(t, C, pay, sums, dst, 4096)
+    assert r.bad_set() == set(cpu.bitmap_to_set(bm, nc)) and int(r.n_bad.item()) == nbad
+    assert np.array_equal(to_host(r.dst), dst)
 
 
 @pytest.mark.timeout(900)
