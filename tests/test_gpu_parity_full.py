@@ -2,7 +2,8 @@
 times (default plan, one workgroup per unit).
 
 * Llama-3-8B TP=8 rank share (14.06 GB state): the whole oracle runs on the
-  host; payload, sums, receiver arena and result sets are compared bit for bit.
+  host; payload, sums, receiver arena and result sets are compared bit for bit,
+  at 64 KiB chunks and at 1 KiB chunks (the tiles chosen by chunk size).
 * 20,000-entry descriptor stress (7.6 GB): whole oracle, scattered layouts,
   canaries in every receiver gap, at 16-byte and 4 KiB payload segments;
   its replica compare (line-aligned, since its tensors start inside cache
@@ -20,6 +21,8 @@ times (default plan, one workgroup per unit).
   {chunk of each flipped byte} and the oracle's set; the 4,096-flip replica
   repaired by a delta (payload and sums against the oracle).
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -98,6 +101,39 @@ def test_llama8b_tp8_full_parity(llama8b):
     dst = np.full(w.dst_arena_bytes, 0xA5, np.uint8)
     bm, nbad = cpu.unpack(t, C, pay, sums, dst)
     log("oracle unpack done")
+    assert nbad == 0 and int(r.n_bad.item()) == 0 and r.bad_set() == set()
+    assert np.array_equal(to_host(r.dst), dst)
+    assert int(r.n_diff.item()) == 0 and r.diff_set() == set()
+    assert np.array_equal(sums_host(r.csum, nc), sums)
+
+
+@pytest.mark.timeout(900)
+def test_llama8b_1kib_chunks_full_parity(llama8b, monkeypatch):
+    """The 8B share in 1 KiB chunks (13.7 million chunks) with the tiles chosen
+    by chunk size (unpack and compare 64 x 1, checksum 64 x 4): whole
+    oracle for pack, unpack, compare and checksum."""
+    for k in [k for k in os.environ if k.startswith("FLASHRESTORE_TILE")]:
+        monkeypatch.delenv(k)
+    w, src_np = llama8b
+    t, C = w.table, 1024
+    r = Restore(t, C, w.src_arena_bytes, w.dst_arena_bytes, canary=0xA5)
+    info = r.plan.info
+    assert (info["tile_pack"], info["tile_unpack"], info["tile_verify"], info["tile_checksum"]) == (4, 7, 7, 4)
+    src = _upload(src_np)
+    r.pack(src)
+    r.unpack()
+    r.verify(src, r.dst)
+    r.checksum(r.dst)
+    torch.cuda.synchronize()
+    log("gpu ops done")
+    pay, sums = cpu.pack(t, C, src_np)
+    nc = r.n_chunks
+    assert nc > 13_000_000
+    assert np.array_equal(sums_host(r.sums, nc), sums)
+    assert np.array_equal(to_host(r.payload)[: pay.size], pay)
+    dst = np.full(w.dst_arena_bytes, 0xA5, np.uint8)
+    bm, nbad = cpu.unpack(t, C, pay, sums, dst)
+    log("oracle done")
     assert nbad == 0 and int(r.n_bad.item()) == 0 and r.bad_set() == set()
     assert np.array_equal(to_host(r.dst), dst)
     assert int(r.n_diff.item()) == 0 and r.diff_set() == set()
