@@ -89,6 +89,10 @@
 extern "C" {
 #endif
 
+#if defined(__GNUC__)
+#pragma GCC visibility push(default) /* the exported interface */
+#endif
+
 #define FR_ABI_VERSION 6
 
 enum fr_dtype { FR_F32 = 1, FR_BF16 = 2 };
@@ -517,6 +521,10 @@ int fr_layout_state_table(const fr_layout3d* layout, uint32_t rank, const uint64
 const char* fr_strerror(int status);
 int fr_last_hip_error(void); /* HIP error code behind the last FR_E_DEVICE on this thread */
 int fr_abi_version(void);    /* FR_ABI_VERSION */
+
+#if defined(__GNUC__)
+#pragma GCC visibility pop
+#endif
 
 #ifdef __cplusplus
 }

@@ -38,10 +38,16 @@ def hipcc_command(out: str = LIB, extra=(), sources=SOURCES):
     ]
 
 
+# The library's host code exports only what include/flashrestore.h declares
+# (its declarations sit in a default-visibility region); device code is
+# compiled as before.
+LIB_EXTRA = ("-Xarch_host", "-fvisibility=hidden")
+
+
 def build(verbose: bool = False) -> str:
-    for lib, sources in ((LIB, SOURCES), (CEIL_LIB, CEIL_SOURCES)):
+    for lib, sources, extra in ((LIB, SOURCES, LIB_EXTRA), (CEIL_LIB, CEIL_SOURCES, ())):
         tmp = lib + ".tmp"
-        cmd = hipcc_command(tmp, sources=sources)
+        cmd = hipcc_command(tmp, extra=extra, sources=sources)
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.run(cmd, check=True)

@@ -188,7 +188,7 @@ static uint32_t env_u32(const char* name, uint32_t dflt) {
 
 using namespace fr;
 
-LaunchCfg plan_launch_config(uint64_t C);
+static LaunchCfg plan_launch_config(uint64_t C);
 
 extern "C" int fr_layout_query(const fr_tensor_desc* table, uint32_t n, uint64_t C,
                                uint64_t src_bytes, uint64_t dst_bytes, uint64_t seg,
@@ -367,7 +367,7 @@ LaunchCfg launch_config() {
 
 // The launch configuration of a plan for chunks of C bytes: the
 // environment's, with the tiles left unset chosen by chunk size.
-LaunchCfg plan_launch_config(uint64_t C) {
+static LaunchCfg plan_launch_config(uint64_t C) {
   LaunchCfg cfg = launch_config();
   auto tile = [&](int t, TileOp op) { return t == kTileAuto ? auto_tile(op, C) : t; };
   cfg.tile_pack = tile(cfg.tile_pack, kOpPack);

@@ -37,6 +37,9 @@ def test_library_exports_every_declared_symbol():
     exported = set(re.findall(r"\sT\s+(fr_\w+)$", out, flags=re.M))
     missing = set(declared_functions()) - exported
     assert not missing, missing
+    # and nothing else: the host internals are hidden
+    functions = set(re.findall(r"\sT\s+(\S+)$", out, flags=re.M))
+    assert functions == set(declared_functions()), functions - set(declared_functions())
     for n in declared_functions():
         assert getattr(F._lib, n) is not None
 
