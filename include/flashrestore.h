@@ -201,7 +201,7 @@ typedef struct fr_plan_info {
  * the receiver arena for unpack); unset, pack and unpack take 4 where the
  * side they write has chunks starting inside lines and 2 (pack) or 1
  * (unpack) otherwise, the compare 1 and the checksum 0 (fr_plan_info
- * reports what pack and unpack take).  FLASHRESTORE_ABSORB_PACK / _UNPACK
+ * reports the walks pack and unpack take and every operation's tile).  FLASHRESTORE_ABSORB_PACK / _UNPACK
  * / _VERIFY / _CHECKSUM (defaults 1, 1, 0, 0): a cut slice walk gives a
  * chunk's last slice its leftover lead instead of one more slice.
  * FLASHRESTORE_BUF_PACK / _UNPACK / _VERIFY / _CHECKSUM (default 0): slice
