@@ -289,6 +289,21 @@ int fr_verify_replicas(const fr_plan* plan, const void* base_a, const void* base
                        uint32_t* diff_bitmap, uint64_t* n_diff, fr_chunk_sum* sums_a,
                        fr_chunk_sum* sums_b, hipStream_t stream);
 
+/* Replica-consistency check from chunk sums alone (Section III-A): for
+ * replicas on different GPUs, each runs fr_checksum_state on its own arena
+ * and the 16-byte sums travel instead of the state; bit c of diff_bitmap is
+ * set iff sums_a[c] and sums_b[c] differ (either field); *n_diff = number of
+ * set bits.  The bitmap drives fr_pack_flagged / fr_unpack_flagged like the
+ * one fr_verify_replicas writes.  (Unlike that exact compare it sees only
+ * what the sums see: every change of one or two bits of a chunk, see
+ * FRSUM-128 above.)
+ *   sums_a, sums_b  device, 16-byte aligned, n_chunks entries each
+ *   diff_bitmap     device, 4-byte aligned, bitmap_words words; written
+ *   n_diff          device, 8-byte aligned, one uint64; zeroed by the call
+ * Outputs must not overlap the inputs or each other (FR_E_OVERLAP). */
+int fr_compare_sums(const fr_plan* plan, const fr_chunk_sum* sums_a, const fr_chunk_sum* sums_b,
+                    uint32_t* diff_bitmap, uint64_t* n_diff, hipStream_t stream);
+
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): the replica
  * compare of fr_verify_replicas, with the same arguments, checks and outputs,

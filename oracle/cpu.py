@@ -36,6 +36,7 @@ def lib():
         l.oro_rne_bf16.argtypes = [u32]
         l.oro_rne_bf16.restype = C.c_uint16
         l.oro_rne_bf16_array.argtypes = [P, P, u64]
+        l.oro_compare_sums.argtypes = [P, P, u64, P, P]
         l.oro_pack.argtypes = [P, u32, u64, u64, P, P, P]
         l.oro_unpack.argtypes = [P, u32, u64, u64, P, P, P, P, P]
         l.oro_verify.argtypes = [P, u32, u64, P, P, P, P, P, P]
@@ -174,6 +175,21 @@ def checksum_chunks(t, C_, base: np.ndarray, ids: np.ndarray):
     if lib().oro_checksum_chunks(_p(t), len(t), C_, _p(base), _p(ids), ids.size, _p(sums)) != 0:
         raise RuntimeError("oro_checksum_chunks")
     return sums[: 2 * ids.size]
+
+
+def compare_sums(sums_a: np.ndarray, sums_b: np.ndarray):
+    """(bitmap, count) of the chunks whose (sum, wsum) differ; sums as two
+    uint64 words per chunk, as the other calls return them."""
+    a = np.ascontiguousarray(sums_a, np.uint64)
+    b = np.ascontiguousarray(sums_b, np.uint64)
+    if a.size != b.size or a.size % 2:
+        raise ValueError("sums of equal chunk counts")
+    nc = a.size // 2
+    bitmap = np.zeros(max((nc + 31) // 32, 1), np.uint32)
+    nd = np.zeros(1, np.uint64)
+    if lib().oro_compare_sums(_p(a), _p(b), nc, _p(bitmap), _p(nd)) != 0:
+        raise RuntimeError("oro_compare_sums")
+    return bitmap[: (nc + 31) // 32], int(nd[0])
 
 
 def bitmap_to_set(bitmap: np.ndarray, n: int) -> list:

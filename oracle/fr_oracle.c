@@ -307,6 +307,22 @@ int oro_checksum_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_
   return 0;
 }
 
+/* Replica-consistency check from sums alone (Section III-A): a chunk is
+ * flagged when either of its two sums differs between the replicas. */
+int oro_compare_sums(const uint64_t* a, const uint64_t* b, uint64_t n_chunks, uint32_t* bitmap,
+                     uint64_t* n_diff) {
+  uint64_t nd = 0;
+  for (uint64_t w = 0; w < (n_chunks + 31) / 32; w++) bitmap[w] = 0;
+  for (uint64_t c = 0; c < n_chunks; c++) {
+    if (a[2 * c] != b[2 * c] || a[2 * c + 1] != b[2 * c + 1]) {
+      bitmap[c / 32] |= 1u << (c % 32);
+      nd++;
+    }
+  }
+  *n_diff = nd;
+  return 0;
+}
+
 /* ------------------------------------------------------------ delta repair
  *
  * Re-sending only the chunks in which a replica diverged.  The caller lists

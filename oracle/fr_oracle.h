@@ -52,6 +52,11 @@ int oro_verify(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* a, con
 int oro_checksum(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* base, uint64_t* sums);
 int oro_checksum_chunks(const oro_entry* t, uint32_t n, uint64_t C, const uint8_t* base,
                         const uint64_t* ids, uint64_t n_ids, uint64_t* sums);
+/* Replica-consistency check from sums alone (Section III-A): bit c of
+ * bitmap set iff chunk c's (sum, wsum) differ between a and b (2 words per
+ * chunk each); *n_diff = set bits.  bitmap: ceil(n_chunks / 32) words. */
+int oro_compare_sums(const uint64_t* a, const uint64_t* b, uint64_t n_chunks, uint32_t* bitmap,
+                     uint64_t* n_diff);
 
 /* Delta repair over a strictly increasing list of global chunk ids (see
  * fr_oracle.c).  pay_off[i] is ORO_NO_PAYLOAD for derived chunks; bitmap and

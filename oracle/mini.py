@@ -129,6 +129,13 @@ def checksum(table, C, arena: bytes):
     return [frsum(b) for _, b in _chunks(table, C, arena, "src_offset")]
 
 
+def compare_sums(sums_a, sums_b):
+    """Chunks whose sums differ between two replicas' checksums (each a
+    list of (sum, wsum) per chunk): the consistency check that needs only
+    the sums to travel."""
+    return {c for c, (x, y) in enumerate(zip(sums_a, sums_b)) if tuple(x) != tuple(y)}
+
+
 def verify_with_sums(table, C, a: bytes, b: bytes):
     """The replica compare together with both arenas' chunk sums."""
     return verify(table, C, a, b), checksum(table, C, a), checksum(table, C, b)

@@ -216,6 +216,25 @@ extern "C" int fr_verify_replicas(const fr_plan* plan, const void* base_a, const
                                      plan->cfg, stream));
 }
 
+extern "C" int fr_compare_sums(const fr_plan* plan, const fr_chunk_sum* sums_a,
+                               const fr_chunk_sum* sums_b, uint32_t* diff_bitmap,
+                               uint64_t* n_diff, hipStream_t stream) {
+  if (!plan || !n_diff) return FR_E_INVAL;
+  const Layout& L = plan->layout;
+  const uint64_t words = (L.n_chunks + 31) / 32;
+  const uint64_t sb = L.n_chunks * sizeof(fr_chunk_sum);
+  FR_TRY(check_device_and_stream(plan, stream));
+  FR_TRY(check_buffer(plan, sums_a, sb, 16));
+  FR_TRY(check_buffer(plan, sums_b, sb, 16));
+  FR_TRY(check_buffer(plan, diff_bitmap, words * 4, 4));
+  FR_TRY(check_buffer(plan, n_diff, 8, 8));
+  const Region outs[] = {{diff_bitmap, words * 4}, {n_diff, 8}};
+  const Region ins[] = {{sums_a, sb}, {sums_b, sb}};
+  FR_TRY(check_disjoint(outs, 2, ins, 2));
+  return launch_result(
+      launch_compare_sums(sums_a, sums_b, uint32_t(L.n_chunks), diff_bitmap, n_diff, stream));
+}
+
 extern "C" int fr_verify_replicas_noalloc(const fr_plan* plan, const void* base_a,
                                           const void* base_b, uint32_t* diff_bitmap,
                                           uint64_t* n_diff, fr_chunk_sum* sums_a,

@@ -347,6 +347,9 @@ int launch_verify(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunk
                   const void* a, const void* b, uint32_t* bitmap, uint64_t* n_diff,
                   fr_chunk_sum* sums_a, fr_chunk_sum* sums_b, const Scratch& scr,
                   const LaunchCfg& cfg, void* stream);
+// Bit c of `bitmap` set iff the two sums of chunk c differ; `count` the bits set.
+int launch_compare_sums(const fr_chunk_sum* a, const fr_chunk_sum* b, uint32_t n_chunks,
+                        uint32_t* bitmap, uint64_t* count, void* stream);
 // The unit records of a delta list given as a bitmap, built on the device:
 // pack's SrcUnit list, or unpack's plain and derived lists, and the counts;
 // it also clears the accumulators of the listed positions and *zero_word,

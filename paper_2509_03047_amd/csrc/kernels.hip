@@ -1658,6 +1658,25 @@ int launch_unpack_delta(const UnpackDeltaArgs& u, const LaunchCfg& cfg, void* st
   FR_DISPATCH(cfg.tile_unpack, unpack_delta_impl, u, cfg, hipStream_t(stream));
 }
 
+int launch_compare_sums(const fr_chunk_sum* a, const fr_chunk_sum* b, uint32_t n_chunks,
+                        uint32_t* bitmap, uint64_t* count, void* stream) {
+  // the compare finalize with one accumulator per chunk: the first sums
+  // folded (as they are) against the second as the sums sent
+  const hipStream_t st = hipStream_t(stream);
+  Zeroes z;
+  z.add(count, sizeof(u64));
+  const int e = z.launch(st);
+  if (e) return e;
+  FinalArgs f{};
+  f.acc = a;
+  f.sent = b;
+  f.bitmap = bitmap;
+  f.count = reinterpret_cast<u64*>(count);
+  f.n_chunks = n_chunks;
+  f.g_shift = 0;
+  return launch_finalize(kCompare, f, st);
+}
+
 int launch_verify(const SrcUnit* units, const SlotTable& slots, uint32_t n_chunks, uint64_t C,
                   const void* a, const void* b, uint32_t* bitmap, uint64_t* n_diff,
                   fr_chunk_sum* sums_a, fr_chunk_sum* sums_b, const Scratch& scr,

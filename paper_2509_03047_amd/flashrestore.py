@@ -111,6 +111,7 @@ def _load():
         "fr_unpack_state": [P, P, P, P, P, P, P],
         "fr_verify_replicas": [P, P, P, P, P, P, P, P],
         "fr_verify_replicas_noalloc": [P, P, P, P, P, P, P, P],
+        "fr_compare_sums": [P, P, P, P, P, P],
         "fr_checksum_state": [P, P, P, P],
         "fr_delta_layout": [P, P, u64, C.POINTER(u64)],
         "fr_pack_chunks": [P, P, P, u64, P, u64, P, P],
@@ -146,7 +147,8 @@ _lib = _load()
 EXPORTED = (
     "fr_plan_create", "fr_plan_create_ex", "fr_plan_get_info", "fr_plan_chunk_of", "fr_plan_entry_layout",
     "fr_plan_destroy", "fr_layout_query", "fr_pack_state", "fr_unpack_state",
-    "fr_verify_replicas", "fr_verify_replicas_noalloc", "fr_checksum_state", "fr_delta_layout",
+    "fr_verify_replicas", "fr_verify_replicas_noalloc", "fr_compare_sums", "fr_checksum_state",
+    "fr_delta_layout",
     "fr_pack_chunks", "fr_unpack_chunks", "fr_pack_flagged", "fr_unpack_flagged",
     "fr_tracker_create", "fr_tracker_destroy", "fr_tracker_heartbeat",
     "fr_tracker_report_failure", "fr_tracker_decide", "fr_tracker_failed_ranks", "fr_tracker_donors",
@@ -326,6 +328,9 @@ class Plan:
                                 sync=False):
         return fr_verify_replicas_noalloc(self, a, b, bitmap, n_diff, sums_a, sums_b, stream, sync)
 
+    def compare_sums(self, sums_a, sums_b, bitmap, n_diff, stream=None, sync=False):
+        return fr_compare_sums(self, sums_a, sums_b, bitmap, n_diff, stream, sync)
+
     def checksum_state(self, base, sums, stream=None):
         return fr_checksum_state(self, base, sums, stream)
 
@@ -444,6 +449,18 @@ def fr_verify_replicas_noalloc(plan: Plan, base_a, base_b, diff_bitmap, n_diff, 
                                            _dev(n_diff, 8, "n_diff"), _dev(sums_a, sb, "sums_a"),
                                            _dev(sums_b, sb, "sums_b"), _stream(stream)),
            "fr_verify_replicas_noalloc")
+    return _synced_bits(diff_bitmap, i["n_chunks"], stream) if sync else None
+
+
+def fr_compare_sums(plan: Plan, sums_a, sums_b, diff_bitmap, n_diff, stream=None, sync=False):
+    """Enqueue the compare of two sums arrays (each from fr_checksum_state of
+    one replica); with sync=True wait and return the sorted ids of the chunks
+    whose sums differ (else None)."""
+    i = plan.info
+    sb = SUM_BYTES * i["n_chunks"]
+    _check(_lib.fr_compare_sums(plan.handle, _dev(sums_a, sb, "sums_a"), _dev(sums_b, sb, "sums_b"),
+                                _dev(diff_bitmap, 4 * i["bitmap_words"], "diff_bitmap"),
+                                _dev(n_diff, 8, "n_diff"), _stream(stream)), "fr_compare_sums")
     return _synced_bits(diff_bitmap, i["n_chunks"], stream) if sync else None
 
 

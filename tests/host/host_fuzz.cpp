@@ -37,6 +37,8 @@ int launch_unpack_blocks(const UnpackArgs&, const UnpackBlocks&, const LaunchCfg
 int launch_checksum(const SrcUnit*, const SlotTable&, uint32_t, uint64_t, const void*,
                     fr_chunk_sum*, const Scratch&, const LaunchCfg&, void*) { return 1; }
 int launch_unpack(const UnpackArgs&, const LaunchCfg&, void*) { return 1; }
+int launch_compare_sums(const fr_chunk_sum*, const fr_chunk_sum*, uint32_t, uint32_t*, uint64_t*,
+                        void*) { return 1; }
 int launch_unpack_delta(const UnpackDeltaArgs&, const LaunchCfg&, void*) { return 1; }
 int launch_verify(const SrcUnit*, const SlotTable&, uint32_t, uint64_t, const void*, const void*,
                   uint32_t*, uint64_t*, fr_chunk_sum*, fr_chunk_sum*, const Scratch&,

@@ -360,3 +360,72 @@ def test_delta_every_subset_of_a_small_table():
         assert set(F.bitmap_indices(bad, ids.size).tolist()) == set(cpu.bitmap_to_set(obm, ids.size)), mask
         assert int(nbad.item()) == onbad, mask
     log(f"delta subsets {1 << n}")
+
+
+def test_compare_sums_flags_the_oracle_chunks_and_drives_the_repair():
+    """Replicas on different GPUs compare chunk sums, not state:
+    fr_compare_sums on the sums of two replicas (each from fr_checksum_state)
+    flags the oracle's chunks (replicas that differ in sum alone, in wsum
+    alone, in one bit of the last chunk, identical ones, random tables with
+    flips), and its bitmap drives fr_pack_flagged / fr_unpack_flagged, which
+    restore the replica to the donor.  Raw sums arrays of chunk counts 0 to
+    129 (ragged bitmap words) against the oracle's compare."""
+    from tests.test_oracle_checksum import _crafted_sums_cases
+
+    t, C, a, cases = _crafted_sums_cases()
+    plan = F.Plan(t, C, a.size, a.size)
+    sa, sb = plan.empty_sums(), plan.empty_sums()
+    bm, nd = plan.empty_bitmap(), plan.empty_counter()
+    plan.checksum_state(to_dev(a), sa)
+    for name, b, want in cases:
+        plan.checksum_state(to_dev(b), sb)
+        got = plan.compare_sums(sa, sb, bm, nd, sync=True)
+        assert set(got) == want and int(nd.item()) == len(want), name
+    rng = np.random.default_rng(1234)
+    repaired = 0
+    for it in range(30):
+        t, nbytes, _ = W.random_tiny_table(rng, max_entries=8, max_numel=3000)
+        t["dst_offset"] = t["src_offset"]  # a replica: the donor's layout
+        C = int(rng.choice([16, 64, 256, 1024, 4096]))
+        x = W.random_tiny_state(t, nbytes, rng)
+        inside = np.concatenate([np.arange(int(e["src_offset"]), int(e["src_offset"]) + int(e["numel"]) *
+                                           (4 if int(e["dtype"]) == F.FR_F32 else 2)) for e in t] + [np.zeros(0, int)])
+        if inside.size == 0:
+            continue
+        y = x.copy()
+        for p in rng.choice(inside, size=int(rng.integers(1, 6))):
+            y[p] ^= np.uint8(1 << int(rng.integers(0, 8)))
+        plan = F.Plan(t, C, nbytes, nbytes)
+        A, B = to_dev(x), to_dev(y)
+        sa, sb = plan.empty_sums(), plan.empty_sums()
+        bm, nd = plan.empty_bitmap(), plan.empty_counter()
+        plan.checksum_state(A, sa)
+        plan.checksum_state(B, sb)
+        got = plan.compare_sums(sa, sb, bm, nd, sync=True)
+        nc = plan.n_chunks
+        obm, ond = cpu.compare_sums(cpu.checksum(t, C, x), cpu.checksum(t, C, y))
+        assert set(got) == set(cpu.bitmap_to_set(obm, nc)) and int(nd.item()) == ond, (it, C)
+        fpay, fsums = plan.empty_delta_payload(), plan.empty_sums()
+        counts = torch.empty(2, dtype=torch.int64, device="cuda")
+        fbad, fnb = plan.empty_bitmap(), plan.empty_counter()
+        plan.pack_flagged(A, bm, fpay, fsums, counts)
+        plan.unpack_flagged(fpay, fsums, bm, B, fbad, fnb, payload_bytes=fpay.numel())
+        torch.cuda.synchronize()
+        assert int(counts[0].item()) == ond and int(fnb.item()) == 0 and torch.equal(B, A), (it, C)
+        repaired += 1
+    assert repaired > 20
+    for n in list(range(0, 70)) + [100, 127, 128, 129]:
+        t = np.zeros(1, dtype=W.TABLE_DTYPE)
+        t["numel"], t["dtype"], t["derive_from"] = 4 * n, W.F32, -1  # n chunks of 16 bytes
+        plan = F.Plan(t, 16, max(16 * n, 16), max(16 * n, 16))
+        xs = rng.integers(0, 4, size=2 * n, dtype=np.uint64)
+        ys = xs.copy()
+        ys[rng.random(2 * n) < 0.15] ^= np.uint64(2)
+        X = to_dev(xs.view(np.int64).reshape(-1, 2)) if n else plan.empty_sums()
+        Y = to_dev(ys.view(np.int64).reshape(-1, 2)) if n else plan.empty_sums()
+        bm, nd = plan.empty_bitmap().fill_(-1), plan.empty_counter().fill_(7)
+        got = plan.compare_sums(X, Y, bm, nd, sync=True)
+        obm, ond = cpu.compare_sums(xs, ys)
+        assert set(got) == set(cpu.bitmap_to_set(obm, n)) and int(nd.item()) == ond, n
+        words = to_host(bm).view(np.uint32)[: (n + 31) // 32]
+        assert np.array_equal(words, obm), n  # every word written, bits past the last chunk clear

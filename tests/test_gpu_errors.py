@@ -226,3 +226,33 @@ def test_compare_of_an_arena_with_itself_is_empty(setup):
     assert int(nd.item()) == 0
     n = plan.n_chunks
     assert torch.equal(sa[:n], sums[:n]) and torch.equal(sb[:n], sums[:n])
+
+
+def test_compare_sums_errors_touch_nothing(setup):
+    """fr_compare_sums: null, misaligned, host and overlapping arguments
+    return their codes, and the bitmap and count keep their pattern."""
+    w, plan, src = setup
+    sa, sb = plan.empty_sums(), plan.empty_sums()
+    plan.checksum_state(src, sa)
+    plan.checksum_state(src, sb)
+    bm = torch.full((plan.bitmap_words,), -1, dtype=torch.int32, device="cuda")
+    nd = torch.full((1,), 77, dtype=torch.int64, device="cuda")
+    base_b, base_n = bm.clone(), nd.clone()
+    host = np.zeros(16 * plan.n_chunks + 64, np.uint8)
+    hp = (host.ctypes.data + 15) & ~15
+    cases = [
+        ((plan, None, sb, bm, nd), -1),                        # null sums
+        ((plan, sa, sb, bm, None), -1),                        # null count
+        ((plan, sa.data_ptr() + 8, sb, bm, nd), -2),           # misaligned sums
+        ((plan, sa, sb, bm.data_ptr() + 2, nd), -2),           # misaligned bitmap
+        ((plan, sa, sb, bm, nd.data_ptr() + 4), -2),           # misaligned count
+        ((plan, hp, sb, bm, nd), -1),                          # host memory
+        ((plan, sa, sb, sa.data_ptr() + 16, nd), -4),          # bitmap inside sums_a
+        ((plan, sa, sb, bm, bm), -4),                          # count inside the bitmap
+    ]
+    for args, code in cases:
+        assert _status(F.fr_compare_sums, *args) == code, code
+    torch.cuda.synchronize()
+    assert torch.equal(bm, base_b) and torch.equal(nd, base_n)
+    # identical sums: nothing flagged
+    assert len(plan.compare_sums(sa, sb, bm, nd, sync=True)) == 0 and int(nd.item()) == 0

@@ -15,7 +15,12 @@ produces, read at the sender offsets.  Pinned here by:
   the pure-Python oracle's pack, at every chunk id next to an empty entry,
   the first and the last chunk included;
 * location: a single flipped bit of the arena changes the sums of exactly
-  the chunk that holds it, found by walking the table in the test.
+  the chunk that holds it, found by walking the table in the test;
+* the consistency check from sums alone (both oracles): replicas built from
+  FRSUM's definition to differ in sum alone, in wsum alone, or in one bit of
+  the last chunk are flagged exactly there, identical ones not at all,
+  single flips at the chunks that hold them, and the C oracle's bitmap has
+  its words and ragged last word right for every count from 0 to 100.
 """
 import os
 
@@ -214,3 +219,104 @@ def test_a_flipped_bit_changes_only_its_chunk():
             changed = {c for c, (x, y) in enumerate(zip(ref, got)) if x != y}
             c = _chunk_of_byte(t, C, p)
             assert changed == (set() if c is None else {c}), (it, p)
+
+
+# ------------------------------------------------ consistency from sums alone
+
+def _crafted_sums_cases():
+    """One fp32 entry of 64 words in 64-byte chunks (4 chunks of 16 words),
+    and replicas that differ in one chunk only in (a) sum alone, (b) wsum
+    alone, (c) a single bit of the last chunk, built from FRSUM's
+    definition: words w_i, w_j of chunk 2 with bit q set in w_j and clear in
+    w_i.  (a) w_0 gains bit q + 1 and w_1 loses bit q: sum +2^q, wsum
+    1 * 2^(q+1) - 2 * 2^q = 0.  (b) w_0 gains bit q and w_1 loses it: sum
+    unchanged, wsum 2^q (1 - 2) != 0."""
+    t = np.zeros(1, dtype=W.TABLE_DTYPE)
+    t["numel"], t["dtype"], t["derive_from"] = 64, W.F32, -1
+    a = np.zeros(256, np.uint8)
+    words = a.view("<u4")
+    words[:] = np.arange(64, dtype=np.uint32) * np.uint32(2654435761)
+    q = 5
+    w0, w1 = 32, 33  # words 0 and 1 of chunk 2
+    words[w0] &= ~np.uint32((1 << q) | (1 << (q + 1)))
+    words[w1] |= np.uint32(1 << q)
+    cases = []
+    b = a.copy()
+    bw = b.view("<u4")
+    bw[w0] |= np.uint32(1 << (q + 1))
+    bw[w1] &= ~np.uint32(1 << q)
+    cases.append(("sum only", b, {2}))
+    b = a.copy()
+    bw = b.view("<u4")
+    bw[w0] |= np.uint32(1 << q)
+    bw[w1] &= ~np.uint32(1 << q)
+    cases.append(("wsum only", b, {2}))
+    b = a.copy()
+    b[255] ^= np.uint8(0x80)
+    cases.append(("last chunk", b, {3}))
+    cases.append(("identical", a.copy(), set()))
+    return t, 64, a, cases
+
+
+def compare_pins(compare, checksum):
+    """Names of the pins that `compare(sums_a, sums_b) -> set` fails, with
+    `checksum(table, C, arena bytes) -> [(sum, wsum), ...]` giving each
+    replica's sums."""
+    failed = []
+    t, C, a, cases = _crafted_sums_cases()
+    sa = checksum(t, C, a.tobytes())
+    for name, b, want in cases:
+        sb = checksum(t, C, b.tobytes())
+        if name == "sum only" and not (sa[2][0] != sb[2][0] and sa[2][1] == sb[2][1]):
+            failed.append("construction (sum only)")
+        if name == "wsum only" and not (sa[2][0] == sb[2][0] and sa[2][1] != sb[2][1]):
+            failed.append("construction (wsum only)")
+        if compare(sa, sb) != want:
+            failed.append(name)
+    rng = np.random.default_rng(77)
+    for _ in range(60):  # single flips land in the chunks that hold them
+        t0, sb_, db = W.random_tiny_table(rng, max_entries=6, max_numel=200)
+        if sb_ == 0:
+            continue
+        C = int(rng.choice([16, 32, 64, 256]))
+        x = W.random_tiny_state(t0, sb_, rng)
+        y = x.copy()
+        want = set()
+        for p in rng.integers(0, sb_, size=int(rng.integers(1, 4))):
+            y[p] ^= np.uint8(1 << int(rng.integers(0, 8)))
+            c = _chunk_of_byte(t0, C, int(p))
+            if c is not None:
+                want.add(c)
+        if compare(checksum(t0, C, x.tobytes()), checksum(t0, C, y.tobytes())) != want:
+            failed.append("flip locations")
+            break
+    return failed
+
+
+def _c_compare(sa, sb):
+    bm, nd = cpu.compare_sums(np.asarray(sa, np.uint64).reshape(-1), np.asarray(sb, np.uint64).reshape(-1))
+    got = set(cpu.bitmap_to_set(bm, len(sa)))
+    assert nd == len(got)
+    return got
+
+
+def test_compare_sums_pins_accept_both_oracles():
+    assert compare_pins(_c_compare, lambda t, C, x: _pairs(cpu.checksum(t, C, np.frombuffer(x, np.uint8)))) == []
+    assert compare_pins(mini.compare_sums, mini.checksum) == []
+
+
+def test_c_compare_sums_bitmap_words_and_ragged_counts():
+    """Bits past the last chunk stay clear; every count from 0 to 100 chunks
+    (ragged last words) against the pure-Python oracle."""
+    rng = np.random.default_rng(5)
+    for n in range(0, 101):
+        a = rng.integers(0, 4, size=2 * n, dtype=np.uint64)
+        b = a.copy()
+        sel = rng.random(2 * n) < 0.2
+        b[sel] ^= np.uint64(1)
+        bm, nd = cpu.compare_sums(a, b)
+        assert bm.size == (n + 31) // 32
+        want = mini.compare_sums(_pairs(a), _pairs(b))
+        assert set(cpu.bitmap_to_set(bm, n)) == want and nd == len(want)
+        if n % 32:
+            assert int(bm[-1]) >> (n % 32) == 0

@@ -705,3 +705,26 @@ def test_planner_mutant_is_caught(name):
     P = _fresh_planner(name.replace(" ", "_"))
     PLANNER_MUTANTS[name](P)
     assert planner_pins(P), name
+
+
+# ------------------------------------------ consistency from sums alone
+
+COMPARE_MUTANTS = {
+    "sum field only": lambda sa, sb: {c for c, (x, y) in enumerate(zip(sa, sb)) if x[0] != y[0]},
+    "wsum field only": lambda sa, sb: {c for c, (x, y) in enumerate(zip(sa, sb)) if x[1] != y[1]},
+    "chunk ids off by one": lambda sa, sb: {c + 1 for c, (x, y) in enumerate(zip(sa, sb)) if x != y},
+    "last chunk dropped": lambda sa, sb: {c for c, (x, y) in enumerate(zip(sa[:-1], sb[:-1])) if x != y},
+}
+
+
+def test_compare_pins_accept_the_oracle():
+    from tests.test_oracle_checksum import compare_pins
+
+    assert compare_pins(_fresh_mini("compare_clean").compare_sums, mini.checksum) == []
+
+
+@pytest.mark.parametrize("name", sorted(COMPARE_MUTANTS))
+def test_compare_mutant_is_caught(name):
+    from tests.test_oracle_checksum import compare_pins
+
+    assert compare_pins(COMPARE_MUTANTS[name], mini.checksum), name
