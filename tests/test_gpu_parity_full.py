@@ -243,6 +243,12 @@ def test_llama8b_replica_verify_flips(llama8b):
             ii = ids.astype(np.int64)
             moved = (g_sb.reshape(-1, 2)[ii] != g_sa.reshape(-1, 2)[ii]).any(axis=1)
             assert moved.all(), f"checksum collisions at k={k}: {ids[~moved].tolist()}"
+        # ... and fr_compare_sums on the two sums arrays finds it, as the
+        # oracle's compare of the same sums does
+        cbm, cnd = r.plan.empty_bitmap(), r.plan.empty_counter()
+        got_s = set(int(c) for c in r.plan.compare_sums(sa, sb, cbm, cnd, sync=True))
+        obm, ond = cpu.compare_sums(ref_sums, cpu.checksum(t, C, b_np))
+        assert got_s == exp == set(cpu.bitmap_to_set(obm, nc)) and int(cnd.item()) == ond == len(exp)
         del b_np
         _flip_on_device(b, pos)  # restore B
         log(f"replica verify k={k}: {len(exp)} chunks")
