@@ -408,12 +408,17 @@ def flips(table, C, k):
 def replica_compare(plan, table, donor, replica, stream, ks=(0, 1, 64, 4096), reps=5):
     """The replica compare on two copies of the state with k distinct random
     bit flips in the second: median time (HIP events) and whether the flagged
-    set is exactly {chunk of each flipped byte}.  The copy is restored after
-    each k by flipping the same bits back."""
+    set is exactly {chunk of each flipped byte}; and the same from the two
+    copies' chunk sums alone (fr_compare_sums, the check replicas on
+    different GPUs run after exchanging their sums): its median time and
+    whether its set is the same.  The copy is restored after each k by
+    flipping the same bits back."""
     import numpy as np
     import torch
 
     diff, ndiff = plan.empty_bitmap(), plan.empty_counter()
+    sums_a, sums_b = plan.empty_sums(), plan.empty_sums()
+    plan.checksum_state(donor, sums_a, stream=stream)
     out = {}
     for k in ks:
         idx, xor, expect = flips(table, plan.info["chunk_bytes"], k)
@@ -427,9 +432,22 @@ def replica_compare(plan, table, donor, replica, stream, ks=(0, 1, 64, 4096), re
             torch.cuda.synchronize()
             ts.append(e0.elapsed_time(e1))
         got = plan.verify_replicas(donor, replica, diff, ndiff, stream=stream, sync=True)
+        n_diff = int(ndiff.item())
+        plan.checksum_state(replica, sums_b, stream=stream)
+        ss = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            plan.compare_sums(sums_a, sums_b, diff, ndiff, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ss.append(e0.elapsed_time(e1))
+        got_s = plan.compare_sums(sums_a, sums_b, diff, ndiff, stream=stream, sync=True)
         replica[idx] ^= xor
-        out[str(k)] = {"ms": round(float(np.median(ts)), 4), "n_diff": int(ndiff.item()),
-                       "exact": set(int(x) for x in got) == expect}
+        out[str(k)] = {"ms": round(float(np.median(ts)), 4), "n_diff": n_diff,
+                       "exact": set(int(x) for x in got) == expect,
+                       "sums_ms": round(float(np.median(ss)), 4),
+                       "sums_exact": set(int(x) for x in got_s) == expect}
     torch.cuda.synchronize()
     return out
 

@@ -56,6 +56,7 @@ def test_bench_json_line(config, extra):
     assert d["delta_repair"]["ok"] is True and d["control_plane"]["ok"] is True
     rc = d["replica_compare"]
     assert set(rc) == {"0", "1", "64", "4096"} and all(v["exact"] for v in rc.values())
+    assert all(v["sums_exact"] and v["sums_ms"] > 0 for v in rc.values())
     assert rc["0"]["n_diff"] == 0 and rc["1"]["n_diff"] == 1
     if "--no-cpu-baseline" not in extra:
         cb = d["cpu_baseline"]
