@@ -69,10 +69,10 @@
  *   concurrently (issue them on one stream, or order the streams), and one
  *   plan must not be used from several host threads at once; use one plan per
  *   concurrent stream.
- *   Graph capture.  The four whole-state operations and the flagged delta
- *   calls enqueue kernel launches only (no memset, no host copy, no
- *   allocation), so a capture of them into a HIP graph replays the same
- *   work.  The host-list delta calls copy the list from host memory: they
+ *   Graph capture.  The four whole-state operations, fr_compare_sums and
+ *   the flagged delta calls enqueue kernel launches only (no memset, no
+ *   host copy, no allocation), so a capture of them into a HIP graph
+ *   replays the same work.  The host-list delta calls copy the list from host memory: they
  *   are not for capture.
  */
 #ifndef FLASHRESTORE_H

@@ -164,6 +164,64 @@ def test_captured_compare_and_repair_replays_correctly():
         assert int(nbad.item()) == 0 and torch.equal(replica, donor), rep
 
 
+def test_captured_sums_check_and_repair_replays_correctly():
+    """The cross-GPU form of the same repair, on one GPU: checksum of each
+    replica -> fr_compare_sums of the two sums arrays -> delta pack of the
+    flagged chunks -> delta unpack, captured once and replayed on a
+    different divergence each time: the flagged set is the oracle's compare
+    of the two replicas' sums, and the replica equals the donor again."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from oracle import cpu
+
+    w = W.make_workload(0)
+    t, C = w.table, w.chunk_bytes
+    donor_np = W.fill_state(w)
+    plan = F.Plan(t, C, w.src_arena_bytes, w.src_arena_bytes)
+    donor = torch.from_numpy(donor_np).to("cuda")
+    replica = donor.clone()
+    sa, sb = plan.empty_sums(), plan.empty_sums()
+    diff, ndiff = plan.empty_bitmap(), plan.empty_counter()
+    pay, sums = plan.empty_delta_payload(), plan.empty_sums()
+    counts = torch.empty(2, dtype=torch.int64, device="cuda")
+    bad, nbad = plan.empty_bitmap(), plan.empty_counter()
+
+    def repair():
+        plan.checksum_state(donor, sa)
+        plan.checksum_state(replica, sb)
+        plan.compare_sums(sa, sb, diff, ndiff)
+        plan.pack_flagged(donor, diff, pay, sums, counts)
+        plan.unpack_flagged(pay, sums, diff, replica, bad, nbad, payload_bytes=pay.numel())
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        repair()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        repair()
+    torch.cuda.synchronize()
+
+    rng = np.random.default_rng(23)
+    ref = cpu.checksum(t, C, donor_np)
+    for rep, k in enumerate((3, 0, 120, 1)):
+        pos = rng.choice(donor_np.size * 8, size=k, replace=False)
+        rep_np = donor_np.copy()
+        for p in pos:
+            rep_np[p // 8] ^= np.uint8(1 << (p % 8))
+        replica.copy_(torch.from_numpy(rep_np).to("cuda"))
+        nbad.fill_(99)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        bm, nd = cpu.compare_sums(ref, cpu.checksum(t, C, rep_np))
+        ids = np.array(cpu.bitmap_to_set(bm, plan.n_chunks), np.uint32)
+        assert int(ndiff.item()) == nd and int(counts[0].item()) == ids.size, rep
+        assert int(nbad.item()) == 0 and torch.equal(replica, donor), rep
+
+
 def test_two_plans_on_two_streams_run_concurrently():
     """One plan per concurrent stream: two plans' whole restore steps, queued
     on two streams without ordering between them, give the same results as
