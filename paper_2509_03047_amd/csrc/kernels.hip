@@ -37,7 +37,9 @@
 //     configuration sets all of it per operation, see LaunchCfg);
 //   * a finalize kernel, one lane per chunk, folds the G accumulators into
 //     the chunk's sums (pack, checksum, compare) or compares them with the
-//     sums sent (unpack), and writes whole bitmap words from wave ballots.
+//     sums sent (unpack; and, given two replicas' sums as accumulators and
+//     as the sums sent, the consistency check from sums alone), and writes
+//     whole bitmap words from wave ballots.
 // Plan creation uses one more kernel: the host describes each slot table as
 // one run of slots per unit and k_expand_slots writes the table itself.
 // Delta calls build their lists' unit records on the device (k_list_*,
